@@ -1,0 +1,284 @@
+#!/usr/bin/env python3
+"""Benchmark of the CyFA core operator on one MI355X.
+
+Default: the chunk-wise forward at the 1.4B-scale layer shape (B=4, T=4096,
+H=16, d_k=d_v=128, chunk 64, bf16 inputs, fp32 accumulation) on synthetic
+seeded inputs already resident in HBM.  One step = one cyfa_forward over the
+whole batch.  Prints one JSON line.
+
+Extra fields: ``roofline`` of the dominant kernel (the fused chunk kernel, timed
+alone with HIP events the library records on its launch stream), ``mfma``
+(algorithmic TFLOP/s against the bf16 dense MFMA peak), ``cpu_baseline`` (the
+fp64 CPU oracle timed on a bounded sample of the same workload on this host)
+and ``decode`` (the single-token decode step at 256 streams x 16 heads).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "CyFA fwd tokens/s + TFLOP/s (% MFMA peak) at 1.4B shape, 1 MI355X"
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2516.6       # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
+M_ACTIVE = 127
+
+# Published HBM-traffic calibration and counter readings (see profiles/); None until taken
+TRAFFIC_BYTES_PER_LAUNCH = None
+
+
+def alg_flops_per_token_head(dk: int, dv: int, m: int = M_ACTIVE, C: int = 64) -> float:
+    """Algorithmic FLOPs of the chunk-wise method per token and head: the inter-chunk
+    products and state updates of both passes 2m(dk+dv), the two readout products 2m^2,
+    and the causal half of the intra-chunk tiles ((C+1)/2)(dk+dv+2m); times 2 for FMA."""
+    return 2.0 * (2 * m * (dk + dv) + 2 * m * m + (C + 1) / 2.0 * (dk + dv + 2 * m))
+
+
+def alg_bytes(B, T, H, dk, dv, in_bytes, m=M_ACTIVE) -> float:
+    """Compulsory HBM bytes: read q, k, v and the three per-token scalars, write o, read R."""
+    th = B * T * H
+    return th * ((2 * dk + dv) * in_bytes + dv * in_bytes + 12) + 4.0 * H * m * m
+
+
+class HipEvents:
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        if self.lib.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        st = self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if st != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({st})")
+        return ms.value
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
+
+
+def upload_inputs(torch, x, dev):
+    t = {}
+    for key in ("q", "k", "v", "delta", "log_alpha", "beta", "R"):
+        a = torch.from_numpy(x[key]).to(dev)
+        if key in ("q", "k", "v") and x["dtype"] == "bf16":
+            a = a.to(torch.bfloat16)
+        t[key] = a
+    return t
+
+
+def forward_bench(args, torch, cyfa, w):
+    from paper_2609_36259_amd.inputs import workload_inputs
+    dev = torch.device("cuda:0")
+    x = workload_inputs(w)
+    t = upload_inputs(torch, x, dev)
+    kernel = {"auto": cyfa.KERNEL_AUTO, "valu": cyfa.KERNEL_VALU, "mfma": cyfa.KERNEL_MFMA}[args.kernel]
+    desc = cyfa.forward_desc(w.B, w.T, w.H, w.dk, w.dv, m=w.m, chunk=args.chunk,
+                             segments=args.segments, scale=x["scale"],
+                             dtype=cyfa.BF16 if w.dtype == "bf16" else cyfa.F32, kernel=kernel)
+    nbytes = cyfa.forward_workspace_size(desc)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    o = torch.empty((w.B, w.T, w.H, w.dv), dtype=t["q"].dtype, device=dev)
+    del x
+
+    def step():
+        cyfa.forward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                     scale=desc.scale, m=w.m, chunk=args.chunk, segments=args.segments,
+                     kernel=kernel, out=o, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    hip = HipEvents()
+    evs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        cyfa.set_timing_events(evs[i][0], evs[i][1])
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cyfa.set_timing_events(None, None)
+    kms = [hip.elapsed_ms(a, b) for a, b in evs]
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    kernel_ms = sum(kms) / len(kms)
+    in_bytes = 2 if w.dtype == "bf16" else 4
+    flops = alg_flops_per_token_head(w.dk, w.dv, w.m) * w.B * w.T * w.H
+    nbytes_alg = alg_bytes(w.B, w.T, w.H, w.dk, w.dv, in_bytes, w.m)
+    plan_kernel = cyfa.selected_kernel(desc)
+    del t, ws, o
+    torch.cuda.empty_cache()
+    return dict(ms_per_step=ms_per_step, kernel_ms=kernel_ms, kernel_ms_min=min(kms),
+                flops=flops, bytes=nbytes_alg, kernel=plan_kernel)
+
+
+def decode_bench(args, torch, cyfa):
+    """Decode step at 256 streams x 16 heads, d = 128, fp32 state (the state is
+    filled with random values of the right scale; the step's cost does not
+    depend on them)."""
+    dev = torch.device("cuda:0")
+    N, H, d, m = 256, 16, 128, M_ACTIVE
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    K = torch.randn((N, H, 128, d), device=dev, generator=g) * 0.1
+    V = torch.randn((N, H, 128, d), device=dev, generator=g) * 0.1
+    K[:, :, m:] = 0
+    V[:, :, m:] = 0
+    clk = torch.zeros((N, H), dtype=torch.float64, device=dev)
+    q = torch.nn.functional.normalize(torch.randn((N, H, d), device=dev, generator=g), dim=-1)
+    k = torch.nn.functional.normalize(torch.randn((N, H, d), device=dev, generator=g), dim=-1)
+    v = torch.randn((N, H, d), device=dev, generator=g)
+    delta = torch.nn.functional.softplus(torch.randn((N, H), device=dev, generator=g))
+    la = torch.nn.functional.logsigmoid(torch.randn((N, H), device=dev, generator=g) + 3)
+    beta = torch.sigmoid(torch.randn((N, H), device=dev, generator=g))
+    R = torch.eye(m, device=dev).expand(H, m, m).contiguous() + \
+        0.1 * torch.randn((H, m, m), device=dev, generator=g)
+    desc = cyfa.decode_desc(N, H, d, d, m=m)
+    ws = torch.empty(cyfa.decode_workspace_size(desc), dtype=torch.uint8, device=dev)
+    out = torch.empty((N, H, d), device=dev)
+
+    def step():
+        cyfa.decode_step(q, k, v, delta, K, V, clk, la, beta, R, out=out, workspace=ws)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    hip = HipEvents()
+    steps = 64
+    evs = [(hip.create(), hip.create()) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        cyfa.set_timing_events(evs[i][0], evs[i][1])
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cyfa.set_timing_events(None, None)
+    kms = sum(hip.elapsed_ms(a, b) for a, b in evs) / steps
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    # compulsory bytes: both states read and written (active rows), q, k, v, o, scalars, clock
+    state = 2 * 2 * m * d * 4
+    per = state + 4 * d * 4 + 3 * 4 + 2 * 8
+    nb = N * H * per
+    res = dict(workload="decode N256 H16 d128 fp32 state", steps=steps,
+               ms_per_step=(t1 - t0) * 1000 / steps, kernel_ms=kms,
+               tokens_per_s=N / ((t1 - t0) / steps),
+               achieved_gbs=nb / (kms * 1e-3) / 1e9, peak_gbs=PEAK_HBM_GBS)
+    res["frac"] = res["achieved_gbs"] / PEAK_HBM_GBS
+    del K, V
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(w, budget_s: float):
+    """Time the CPU oracle on a bounded sample of the workload (leading (b, h)
+    sequences, leading tokens), sized to about `budget_s` seconds."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_36259_amd.inputs import workload_inputs
+    x = workload_inputs(w)
+    npairs = min(w.B * w.H, max(1, len(os.sched_getaffinity(0))))
+    pairs = np.arange(npairs, dtype=np.int32)
+    args = (x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"])
+    probe = 32
+    t0 = time.perf_counter()
+    r = oracle.forward(*args, m=w.m, scale=x["scale"], pairs=pairs, T_run=probe, want_z=False)
+    dt = time.perf_counter() - t0
+    T_run = int(min(w.T, max(probe, probe * budget_s / max(dt, 1e-6))))
+    t0 = time.perf_counter()
+    r = oracle.forward(*args, m=w.m, scale=x["scale"], pairs=pairs, T_run=T_run, want_z=False)
+    dt = time.perf_counter() - t0
+    token_heads = npairs * T_run
+    return dict(value=token_heads / dt / w.H, unit="tokens/s", cores=int(r["threads"]),
+                kind="oracle",
+                sample=f"{npairs} (b,h) sequences x first {T_run} tokens of {w.name}; "
+                       f"token-heads/s divided by H={w.H}",
+                seconds=dt)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="1.4B", choices=["tiny", "400M", "1.4B", "long"])
+    ap.add_argument("--kernel", default="auto", choices=["auto", "valu", "mfma"])
+    ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--segments", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}); the operator's multi-GPU sharding is a design, not "
+              "built here", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_36259_amd import cyfa
+    from paper_2609_36259_amd.inputs import FWD_1P4B, FWD_400M, FWD_LONG, FWD_TINY
+    w = {"tiny": FWD_TINY, "400M": FWD_400M, "1.4B": FWD_1P4B, "long": FWD_LONG}[args.workload]
+    cyfa.load()
+
+    fb = forward_bench(args, torch, cyfa, w)
+    tokens = w.B * w.T
+    value = tokens / (fb["ms_per_step"] * 1e-3)
+    ks = fb["kernel_ms"] * 1e-3
+    hbm = fb["bytes"] / ks / 1e9
+    tfl = fb["flops"] / ks / 1e12
+    bound = "hbm" if fb["bytes"] / (PEAK_HBM_GBS * 1e9) >= fb["flops"] / (PEAK_BF16_TFLOPS * 1e12) \
+        else "mfma"
+    roof = {"bound": bound, "kernel": f"cyfa fused chunk kernel ({fb['kernel']})",
+            "launch_ms": fb["kernel_ms"], "traffic": TRAFFIC_BYTES_PER_LAUNCH}
+    if bound == "hbm":
+        roof.update(achieved=hbm, peak=PEAK_HBM_GBS, unit="GB/s", frac=hbm / PEAK_HBM_GBS,
+                    alg_bytes_per_launch=fb["bytes"])
+    else:
+        roof.update(achieved=tfl, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=tfl / PEAK_BF16_TFLOPS, alg_flops_per_launch=fb["flops"])
+    line = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": fb["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if fb["kernel"] == "mfma" else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "d_k": w.dk, "d_v": w.dv,
+                   "chunk": 64 if fb["kernel"] == "mfma" else (args.chunk or 16), "m": w.m,
+                   "io_dtype": w.dtype, "kernel": fb["kernel"], "segments": args.segments},
+        "tflops": fb["flops"] / (fb["ms_per_step"] * 1e-3) / 1e12,
+        "roofline": roof,
+        "mfma": {"achieved": tfl, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                 "frac": tfl / PEAK_BF16_TFLOPS, "alg_flops_per_launch": fb["flops"]},
+        "hbm": {"achieved": hbm, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": hbm / PEAK_HBM_GBS},
+    }
+    if not args.no_decode:
+        line["decode"] = decode_bench(args, torch, cyfa)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,209 @@
+/*
+ * cyfa.h -- C ABI of the MI355X (gfx950) CyFA core operator.
+ *
+ * CyFA (Cyclic Flow Attention) keeps key and value states whose rows are
+ * relative-time slots.  Every token moves both states by the same fractional
+ * cyclic shift P(delta_t), scales them by the forget gate alpha_t, writes
+ * beta_t k_t and beta_t v_t into slot 0 (Sec. 3.1, Eq. cyfa-physical-recurrence)
+ * and reads out o_t = (R V_t)^T softmax(scale R K_t q_t) (Eq. cyfa-physical-readout).
+ * The library computes the same map in absolute-clock coordinates (Sec. 3.2,
+ * Eqs. cyfa-absolute-recurrence and cyfa-absolute-readout), where each state is
+ * carried by a scalar decay and the clock lambda_t = lambda_{t-1} + delta_t
+ * (Eq. cyfa-cumulative-clock) enters through the temporal write vector
+ * beta_t U(-lambda_t) b; the forward pass is evaluated chunk by chunk as two
+ * scalar-gated linear-attention passes joined by a token-wise softmax readout
+ * (Sec. 3.3, Eq. cyfa-two-pass; App. B).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers (HIP device memory of the current
+ *     device), dense row-major with the shapes given below.  q, k, v, o and the
+ *     state pointers must be 16-byte aligned; scalar arrays 4-byte aligned;
+ *     clock arrays 8-byte aligned.
+ *   - The caller owns every buffer.  The library never allocates device memory;
+ *     scratch comes from the caller's workspace, sized by the matching
+ *     *_workspace_size query.
+ *   - Every call validates all of its arguments on the host before it launches
+ *     anything: on any error nothing is launched and nothing is written.
+ *     Errors are returned as cyfa_status; no exception crosses the ABI, and
+ *     cyfa_last_error() gives a human-readable detail for the calling thread.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means the
+ *     default stream) with no host synchronisation.  The library holds no
+ *     global mutable state (only the per-thread error text and timing hook)
+ *     and may be called from several threads.
+ *   - m is the number of active relative-time slots (odd, 3..127).  States are
+ *     stored with 128 rows (m* = 128): rows 0..m-1 hold the absolute-clock
+ *     coordinates in the basis order of App. A.1 (row 0 = DC component, row
+ *     2j-1 = cosine of frequency j, row 2j = its sine) and rows m..127 are
+ *     padding (App. A.7): ignored on input, written as zero on output.
+ *   - Clocks are double precision and are reported reduced modulo m, which is
+ *     exact because U(tau + m) = U(tau) (App. A.1, Prop. 1) and the output
+ *     depends only on clock differences (App. A.4, Prop. 6).
+ *   - NaN or Inf in the inputs propagate to the outputs; they never fault.
+ */
+#ifndef CYFA_H_
+#define CYFA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CYFA_OK = 0,
+    CYFA_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, bad size, bad enum   */
+    CYFA_ERR_UNSUPPORTED = 2,      /* valid request this build does not implement   */
+    CYFA_ERR_WORKSPACE = 3,        /* workspace missing or smaller than required     */
+    CYFA_ERR_LAUNCH = 4            /* the HIP runtime refused a launch               */
+} cyfa_status;
+
+typedef enum {
+    CYFA_F32 = 0,   /* q, k, v, o stored as float                              */
+    CYFA_BF16 = 1   /* q, k, v, o stored as bfloat16; accumulation is float   */
+} cyfa_dtype;
+
+typedef enum {
+    CYFA_KERNEL_AUTO = 0,  /* BF16 with d_k = d_v = 128: matrix-core kernel;
+                              anything else: the vector-ALU kernel            */
+    CYFA_KERNEL_VALU = 1,  /* vector-ALU chunk kernel, fp32 arithmetic, any
+                              supported shape and dtype                        */
+    CYFA_KERNEL_MFMA = 2   /* matrix-core (bf16 MFMA) chunk kernel: BF16,
+                              d_k = d_v = 128, chunk 64                         */
+} cyfa_kernel;
+
+/*
+ * Forward problem descriptor.
+ *   B, T, H      batch, tokens, heads (B, H >= 1; T >= 0; T = 0 is a no-op that
+ *                still writes the final state and clock when requested)
+ *   d_k, d_v     head dims: 64 or 128 each (the matrix-core kernel: 128 only)
+ *   m            active slots, odd, 3..127
+ *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
+ *                8 or 16 (default 16); MFMA kernel: 64.  Results do not depend
+ *                on it beyond rounding (App. B: the chunk form is exact).
+ *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
+ *                else 1..1024 (MFMA kernel only; the VALU kernel uses 1).  The
+ *                state entering a segment is obtained from a pre-pass over the
+ *                earlier segments.  Results do not depend on it beyond rounding.
+ *   scale        logit scale (the paper leaves the dot-product scaling out of
+ *                its notation, Sec. 3.1 footnote); multiplies R K_t q_t
+ *   dtype        storage type of q, k, v and o
+ *   kernel       cyfa_kernel selector
+ */
+typedef struct {
+    int32_t B, T, H, d_k, d_v;
+    int32_t m;
+    int32_t chunk;
+    int32_t segments;
+    float scale;
+    int32_t dtype;   /* cyfa_dtype  */
+    int32_t kernel;  /* cyfa_kernel */
+} cyfa_fwd_desc;
+
+/* Bytes of device workspace cyfa_forward needs for `desc` (host-only query). */
+cyfa_status cyfa_forward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes);
+
+/*
+ * Chunk-wise CyFA forward (Sec. 3.3 Eq. cyfa-two-pass; App. B Eqs.
+ * app-cyfa-key-chunk, app-cyfa-value-chunk).
+ *
+ *   q, k        [B, T, H, d_k]  dtype
+ *   v           [B, T, H, d_v]  dtype
+ *   delta       [B, T, H] float clock increments delta_t (Eq. cyfa-cumulative-
+ *               clock); any finite value is accepted (the paper draws them from
+ *               (0, 1); negative values run the clock backwards)
+ *   log_alpha   [B, T, H] float g_t = log alpha_t (forget gate, normally <= 0);
+ *               NULL means alpha = 1
+ *   beta        [B, T, H] float write strength beta_t; NULL means beta = 1
+ *   R           [H, m, m] float readout matrices R_h (Sec. 3.1); NULL = identity
+ *   K0, V0      [B, H, 128, d_k] / [B, H, 128, d_v] float initial absolute-clock
+ *               states; NULL means zero
+ *   clock0      [B, H] double initial clock lambda_0; NULL means 0
+ *   o           [B, T, H, d_v] dtype output (required)
+ *   K_out,V_out [B, H, 128, d] float final states, or NULL to skip; may alias
+ *               K0 / V0 (resume in place); must not alias any other argument
+ *   clock_out   [B, H] double final clock reduced mod m, or NULL; may alias clock0
+ *   logits_out  [B, T, H, m] float slot logits z_t = scale R K_t q_t
+ *               (Eq. cyfa-physical-readout, before the softmax), or NULL
+ *   workspace   device scratch of at least cyfa_forward_workspace_size bytes
+ *               (256-byte aligned); contents on entry are ignored
+ *   stream      hipStream_t
+ */
+cyfa_status cyfa_forward(const cyfa_fwd_desc *desc,
+                         const void *q, const void *k, const void *v,
+                         const float *delta, const float *log_alpha, const float *beta,
+                         const float *R,
+                         const float *K0, const float *V0, const double *clock0,
+                         void *o,
+                         float *K_out, float *V_out, double *clock_out,
+                         float *logits_out,
+                         void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
+ * Single-token decode descriptor: N independent streams, H heads each.
+ *   d_k, d_v 64 or 128; m odd 3..127; dtype of q, k, v, o.
+ */
+typedef struct {
+    int32_t N, H, d_k, d_v;
+    int32_t m;
+    float scale;
+    int32_t dtype;   /* cyfa_dtype */
+} cyfa_dec_desc;
+
+/* Bytes of device workspace cyfa_decode_step needs for `desc` (host-only). */
+cyfa_status cyfa_decode_workspace_size(const cyfa_dec_desc *desc, size_t *bytes);
+
+/*
+ * One recurrent step in absolute-clock coordinates, in place
+ * (Sec. 3.2, Eqs. cyfa-absolute-recurrence and cyfa-absolute-readout):
+ *   lambda <- lambda + delta;  a = beta U(-lambda) b
+ *   Kbar <- alpha Kbar + a k^T;  Vbar <- alpha Vbar + a v^T
+ *   o = Vbar^T U(-lambda) Phi^T R^T softmax(scale R Phi U(lambda) Kbar q)
+ *
+ *   q, k        [N, H, d_k] dtype;  v [N, H, d_v] dtype
+ *   delta, log_alpha, beta   [N, H] float (log_alpha/beta may be NULL as above)
+ *   R           [H, m, m] float or NULL (identity)
+ *   K, V        [N, H, 128, d_k] / [N, H, 128, d_v] float states, read and
+ *               updated in place (required)
+ *   clock       [N, H] double, read and updated in place (reduced mod m)
+ *   o           [N, H, d_v] dtype output (required)
+ *   logits_out  [N, H, m] float slot logits, or NULL
+ *   workspace   at least cyfa_decode_workspace_size bytes, 256-byte aligned
+ * A step must not run concurrently with another call that touches the same
+ * states.
+ */
+cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc,
+                             const void *q, const void *k, const void *v,
+                             const float *delta, const float *log_alpha, const float *beta,
+                             const float *R,
+                             float *K, float *V, double *clock,
+                             void *o, float *logits_out,
+                             void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/*
+ * Optional timing hook for profilers and benchmarks.  When both events are
+ * non-NULL (hipEvent_t handles), every later cyfa_forward / cyfa_decode_step
+ * call made from the calling thread records `start` on its stream immediately
+ * before its main kernel (the fused chunk kernel, or the decode kernel) and
+ * `stop` immediately after it, so hipEventElapsedTime gives that kernel's
+ * duration alone.  Passing NULL for both clears the hook.  Setting only one of
+ * them is CYFA_ERR_INVALID_ARGUMENT.  The events stay owned by the caller.
+ */
+cyfa_status cyfa_set_timing_events(void *start_event, void *stop_event);
+
+/* Static description of a status code. */
+const char *cyfa_status_string(cyfa_status status);
+
+/* Detail of the last failed call on the calling thread ("" if none). */
+const char *cyfa_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t cyfa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CYFA_H_ */

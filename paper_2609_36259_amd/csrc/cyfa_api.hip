@@ -1,0 +1,277 @@
+// Host side of the C ABI declared in include/cyfa.h: argument validation,
+// workspace layout and kernel dispatch.  Every check runs before the first
+// launch, so a rejected call enqueues nothing and writes nothing.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/cyfa.h"
+#include "cyfa_internal.h"
+
+namespace cyfa {
+int valu_chunk_max();
+bool mfma_supported(const FwdParams &p);
+size_t mfma_workspace_bytes(const FwdParams &p, int segments);
+int mfma_auto_segments(const FwdParams &p);
+hipError_t launch_fwd_mfma(const FwdParams &p, int segments, void *ws, hipStream_t s,
+                           hipEvent_t ev_start, hipEvent_t ev_stop);
+}  // namespace cyfa
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+thread_local hipEvent_t g_ev_start = nullptr;
+thread_local hipEvent_t g_ev_stop = nullptr;
+
+hipError_t mark(hipEvent_t ev, hipStream_t s) {
+    return ev ? hipEventRecord(ev, s) : hipSuccess;
+}
+
+cyfa_status fail(cyfa_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+cyfa_status ok() {
+    g_last_error[0] = '\0';
+    return CYFA_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+constexpr size_t kWsAlign = 256;
+size_t round_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+bool head_dim_ok(int d) { return d == 64 || d == 128; }
+
+struct FwdPlan {
+    bool mfma;
+    int chunk;
+    int segments;
+    size_t ws_bytes;
+};
+
+cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
+    if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
+    if (d->B < 1 || d->H < 1 || d->T < 0)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "need B >= 1, H >= 1, T >= 0 (got B=%d T=%d H=%d)",
+                    d->B, d->T, d->H);
+    if ((double)d->B * d->T * d->H * (d->d_k > d->d_v ? d->d_k : d->d_v) > 4.0e12)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "problem too large");
+    if (d->d_k <= 0 || d->d_v <= 0)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
+    if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
+        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64 or 128 (got d_k=%d d_v=%d)",
+                    d->d_k, d->d_v);
+    if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
+        return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
+                                                               : CYFA_ERR_INVALID_ARGUMENT,
+                    "m must be odd and in [3, 127] (got %d)", d->m);
+    if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
+    if (d->kernel < CYFA_KERNEL_AUTO || d->kernel > CYFA_KERNEL_MFMA)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad kernel selector %d", d->kernel);
+    if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
+    if (d->segments < 0 || d->segments > 1024)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "segments must be in [0, 1024]");
+    if (d->chunk < 0) return fail(CYFA_ERR_INVALID_ARGUMENT, "chunk must be >= 0");
+
+    cyfa::FwdParams probe{};
+    probe.B = d->B; probe.T = d->T; probe.H = d->H; probe.dk = d->d_k; probe.dv = d->d_v;
+    probe.m = d->m; probe.dtype = d->dtype; probe.chunk = d->chunk ? d->chunk : 64;
+    const bool mfma_ok = cyfa::mfma_supported(probe);
+    bool use_mfma;
+    if (d->kernel == CYFA_KERNEL_MFMA) {
+        if (!mfma_ok)
+            return fail(CYFA_ERR_UNSUPPORTED,
+                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 and chunk 64");
+        use_mfma = true;
+    } else if (d->kernel == CYFA_KERNEL_VALU) {
+        use_mfma = false;
+    } else {
+        use_mfma = mfma_ok && d->chunk == 0;
+        if (d->chunk == 64 && mfma_ok) use_mfma = true;
+    }
+    plan->mfma = use_mfma;
+    size_t ws = round_up(cyfa::readout_f32_bytes(d->H));
+    if (use_mfma) {
+        plan->chunk = 64;
+        plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
+        const int nchunks = (d->T + 63) / 64;
+        if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
+        if (plan->segments < 1) plan->segments = 1;
+        ws += round_up(cyfa::mfma_workspace_bytes(probe, plan->segments));
+    } else {
+        const int c = d->chunk ? d->chunk : cyfa::valu_chunk_max();
+        if (c != 8 && c != 16)
+            return fail(CYFA_ERR_UNSUPPORTED, "vector-ALU kernel supports chunk 8 or 16 (got %d)", c);
+        if (d->segments > 1)
+            return fail(CYFA_ERR_UNSUPPORTED, "vector-ALU kernel runs one segment per sequence");
+        plan->chunk = c;
+        plan->segments = 1;
+    }
+    plan->ws_bytes = ws;
+    return CYFA_OK;
+}
+
+cyfa_status check_dec(const cyfa_dec_desc *d) {
+    if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
+    if (d->N < 1 || d->H < 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "need N >= 1 and H >= 1");
+    if ((double)d->N * d->H > 2.0e9) return fail(CYFA_ERR_INVALID_ARGUMENT, "too many streams");
+    if (d->d_k <= 0 || d->d_v <= 0) return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
+    if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
+        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64 or 128");
+    if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
+        return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
+                                                               : CYFA_ERR_INVALID_ARGUMENT,
+                    "m must be odd and in [3, 127] (got %d)", d->m);
+    if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
+    if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
+    return CYFA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cyfa_status cyfa_forward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes) {
+    if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    FwdPlan plan;
+    cyfa_status st = plan_forward(desc, &plan);
+    if (st != CYFA_OK) return st;
+    *bytes = plan.ws_bytes;
+    return ok();
+}
+
+cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                         const float *delta, const float *log_alpha, const float *beta,
+                         const float *R, const float *K0, const float *V0, const double *clock0,
+                         void *o, float *K_out, float *V_out, double *clock_out,
+                         float *logits_out, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+    FwdPlan plan;
+    cyfa_status st = plan_forward(desc, &plan);
+    if (st != CYFA_OK) return st;
+    const bool has_tokens = desc->T > 0;
+    if (has_tokens && (!q || !k || !v || !delta || !o))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "q, k, v, delta and o are required");
+    const void *vec[] = {q, k, v, o, K0, V0, K_out, V_out};
+    const char *vec_names[] = {"q", "k", "v", "o", "K0", "V0", "K_out", "V_out"};
+    for (int i = 0; i < 8; ++i)
+        if (vec[i] && !aligned(vec[i], 16))
+            return fail(CYFA_ERR_INVALID_ARGUMENT, "%s must be 16-byte aligned", vec_names[i]);
+    const void *sc[] = {delta, log_alpha, beta, R, logits_out};
+    for (const void *p : sc)
+        if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    if ((clock0 && !aligned(clock0, 8)) || (clock_out && !aligned(clock_out, 8)))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "clock arrays must be 8-byte aligned");
+    if ((K_out && (K_out == (const float *)V0 || (const void *)K_out == q || (const void *)K_out == k)) ||
+        (V_out && (V_out == (const float *)K0 || (const void *)V_out == v)) ||
+        (K_out && K_out == V_out) || (o && (o == (void *)K_out || o == (void *)V_out)))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias other arguments");
+    if (!workspace || workspace_bytes < plan.ws_bytes)
+        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required (got %zu)", plan.ws_bytes,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, kWsAlign))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+
+    cyfa::FwdParams p{};
+    p.B = desc->B; p.T = desc->T; p.H = desc->H; p.dk = desc->d_k; p.dv = desc->d_v;
+    p.m = desc->m; p.chunk = plan.chunk; p.segments = plan.segments; p.scale = desc->scale;
+    p.dtype = desc->dtype;
+    p.q = q; p.k = k; p.v = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R;
+    p.K0 = K0; p.V0 = V0; p.clock0 = clock0; p.o = o; p.K_out = K_out; p.V_out = V_out;
+    p.clock_out = clock_out; p.logits = logits_out;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *ws = static_cast<char *>(workspace);
+    float *M = reinterpret_cast<float *>(ws);
+    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, s);
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
+    if (plan.mfma) {
+        e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
+    } else {
+        e = mark(g_ev_start, s);
+        if (e == hipSuccess) e = cyfa::launch_fwd_valu(p, M, s);
+        if (e == hipSuccess) e = mark(g_ev_stop, s);
+    }
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "forward launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+cyfa_status cyfa_decode_workspace_size(const cyfa_dec_desc *desc, size_t *bytes) {
+    if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    cyfa_status st = check_dec(desc);
+    if (st != CYFA_OK) return st;
+    *bytes = round_up(cyfa::readout_f32_bytes(desc->H));
+    return ok();
+}
+
+cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
+                             const float *delta, const float *log_alpha, const float *beta,
+                             const float *R, float *K, float *V, double *clock, void *o,
+                             float *logits_out, void *workspace, size_t workspace_bytes,
+                             void *stream) {
+    cyfa_status st = check_dec(desc);
+    if (st != CYFA_OK) return st;
+    if (!q || !k || !v || !delta || !K || !V || !clock || !o)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "q, k, v, delta, K, V, clock and o are required");
+    const void *vec[] = {q, k, v, o, K, V};
+    for (const void *p : vec)
+        if (!aligned(p, 16)) return fail(CYFA_ERR_INVALID_ARGUMENT, "tensors must be 16-byte aligned");
+    const void *sc[] = {delta, log_alpha, beta, R, logits_out};
+    for (const void *p : sc)
+        if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    if (!aligned(clock, 8)) return fail(CYFA_ERR_INVALID_ARGUMENT, "clock must be 8-byte aligned");
+    if (K == V || o == (void *)K || o == (void *)V)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias each other");
+    const size_t need = round_up(cyfa::readout_f32_bytes(desc->H));
+    if (!workspace || workspace_bytes < need)
+        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (!aligned(workspace, kWsAlign))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+
+    cyfa::DecParams p{};
+    p.N = desc->N; p.H = desc->H; p.dk = desc->d_k; p.dv = desc->d_v; p.m = desc->m;
+    p.scale = desc->scale; p.dtype = desc->dtype;
+    p.q = q; p.k = k; p.v = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R;
+    p.K = K; p.V = V; p.clock = clock; p.o = o; p.logits = logits_out;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    float *M = static_cast<float *>(workspace);
+    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, s);
+    if (e == hipSuccess) e = mark(g_ev_start, s);
+    if (e == hipSuccess) e = cyfa::launch_decode(p, M, s);
+    if (e == hipSuccess) e = mark(g_ev_stop, s);
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "decode launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+const char *cyfa_status_string(cyfa_status status) {
+    switch (status) {
+        case CYFA_OK: return "ok";
+        case CYFA_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case CYFA_ERR_UNSUPPORTED: return "unsupported configuration";
+        case CYFA_ERR_WORKSPACE: return "workspace missing or too small";
+        case CYFA_ERR_LAUNCH: return "kernel launch failed";
+    }
+    return "unknown status";
+}
+
+const char *cyfa_last_error(void) { return g_last_error; }
+
+cyfa_status cyfa_set_timing_events(void *start_event, void *stop_event) {
+    if ((start_event == nullptr) != (stop_event == nullptr))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "set both timing events or neither");
+    g_ev_start = static_cast<hipEvent_t>(start_event);
+    g_ev_stop = static_cast<hipEvent_t>(stop_event);
+    return ok();
+}
+
+int32_t cyfa_version(void) { return 100; }
+
+}  // extern "C"

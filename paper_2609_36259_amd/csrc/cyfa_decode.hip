@@ -1,0 +1,258 @@
+// Single-token CyFA decode step in absolute-clock coordinates, in place.
+//
+// Per (stream, head) (Sec. 3.2, Eqs. cyfa-absolute-recurrence and
+// cyfa-absolute-readout):
+//   lambda <- lambda + delta                     (Eq. cyfa-cumulative-clock)
+//   a = beta U(-lambda) b                        temporal write vector
+//   Kbar <- alpha Kbar + a k^T,  o' = Kbar q     (streamed through registers)
+//   Vbar <- alpha Vbar + a v^T                   (kept in registers)
+//   z = scale M U(lambda) o',  w = softmax(z),  o'' = U(-lambda) M^T w,  M = R Phi
+//   o = Vbar^T o''
+// The step reads and writes each state once; it is bound by HBM bandwidth.
+// Each workgroup streams its two 128 x d float states with 16-byte loads laid
+// out so that consecutive lanes touch consecutive addresses.
+#include "cyfa_internal.h"
+
+namespace cyfa {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const float *__restrict__ Mg) {
+    constexpr int KQ = DK / 4;                       // float4 per key-state row
+    constexpr int VQ = DV / 4;                       // float4 per value-state row
+    constexpr int KIT = kStoreRows * KQ / kThreads;  // float4 per thread (key state)
+    constexpr int VIT = kStoreRows * VQ / kThreads;  // float4 per thread (value state)
+    constexpr int KROWS_PER_IT = kThreads / KQ;
+    constexpr int VROWS_PER_IT = kThreads / VQ;
+
+    __shared__ float qs[DK], ks[DK], vs[DV];
+    __shared__ float a_s[kStoreRows], op[kStoreRows], xs[kStoreRows], ws[kStoreRows];
+    __shared__ float yp[2][kStoreRows];
+    __shared__ float2 cs[64];
+    __shared__ float4 opart[kThreads / 64][VQ];
+
+    const int nh = blockIdx.x;
+    const int h = nh % p.H;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int m = p.m;
+    const int J = (m - 1) / 2;
+    const Tin *q = static_cast<const Tin *>(p.q);
+    const Tin *k = static_cast<const Tin *>(p.k);
+    const Tin *v = static_cast<const Tin *>(p.v);
+
+    const float alpha = p.log_alpha ? __expf(p.log_alpha[nh]) : 1.f;
+    const float beta = p.beta ? p.beta[nh] : 1.f;
+    const double lam = reduce_clock(p.clock[nh] + (double)p.delta[nh], m);
+
+    for (int c = tid; c < DK; c += kThreads) {
+        qs[c] = load_as_float(q, (size_t)nh * DK + c);
+        ks[c] = load_as_float(k, (size_t)nh * DK + c);
+    }
+    for (int c = tid; c < DV; c += kThreads) vs[c] = load_as_float(v, (size_t)nh * DV + c);
+    if (tid < J) {
+        float c, s;
+        clock_phase(lam, tid + 1, m, &c, &s);
+        cs[tid] = make_float2(c, s);
+    }
+    __syncthreads();
+    if (tid < kStoreRows) {
+        const int i = tid;
+        float val = 0.f;
+        if (i == 0) {
+            val = beta / sqrtf((float)m);
+        } else if (i < m) {
+            const float2 t = cs[(i - 1) >> 1];
+            const float amp = beta * sqrtf(2.0f / (float)m);
+            val = (i & 1) ? amp * t.x : -amp * t.y;
+        }
+        a_s[i] = val;
+    }
+    __syncthreads();
+
+    // ---- key state: update in place and form o' = Kbar q
+    {
+        float4 *K4 = reinterpret_cast<float4 *>(p.K + (size_t)nh * kStoreRows * DK);
+        const int c4 = tid % KQ;
+        const float4 q4 = make_float4(qs[4 * c4], qs[4 * c4 + 1], qs[4 * c4 + 2], qs[4 * c4 + 3]);
+        const float4 k4 = make_float4(ks[4 * c4], ks[4 * c4 + 1], ks[4 * c4 + 2], ks[4 * c4 + 3]);
+#pragma unroll
+        for (int it = 0; it < KIT; ++it) {
+            const int row = it * KROWS_PER_IT + tid / KQ;
+            float part = 0.f;
+            if (row < m) {
+                float4 x = K4[(size_t)row * KQ + c4];
+                const float ar = a_s[row];
+                x.x = fmaf(alpha, x.x, ar * k4.x);
+                x.y = fmaf(alpha, x.y, ar * k4.y);
+                x.z = fmaf(alpha, x.z, ar * k4.z);
+                x.w = fmaf(alpha, x.w, ar * k4.w);
+                K4[(size_t)row * KQ + c4] = x;
+                part = x.x * q4.x + x.y * q4.y + x.z * q4.z + x.w * q4.w;
+            }
+#pragma unroll
+            for (int off = 1; off < KQ; off <<= 1) part += __shfl_xor(part, off);
+            if (c4 == 0) op[row] = row < m ? part : 0.f;
+        }
+    }
+    // ---- value state: update in place, keep the new values for the readout
+    float4 vreg[VIT];
+    {
+        float4 *V4 = reinterpret_cast<float4 *>(p.V + (size_t)nh * kStoreRows * DV);
+        const int c4 = tid % VQ;
+        const float4 v4 = make_float4(vs[4 * c4], vs[4 * c4 + 1], vs[4 * c4 + 2], vs[4 * c4 + 3]);
+#pragma unroll
+        for (int it = 0; it < VIT; ++it) {
+            const int row = it * VROWS_PER_IT + tid / VQ;
+            float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (row < m) {
+                x = V4[(size_t)row * VQ + c4];
+                const float ar = a_s[row];
+                x.x = fmaf(alpha, x.x, ar * v4.x);
+                x.y = fmaf(alpha, x.y, ar * v4.y);
+                x.z = fmaf(alpha, x.z, ar * v4.z);
+                x.w = fmaf(alpha, x.w, ar * v4.w);
+                V4[(size_t)row * VQ + c4] = x;
+            }
+            vreg[it] = x;
+        }
+    }
+    __syncthreads();
+    // ---- middle step
+    if (tid < kStoreRows) {
+        const int i = tid;
+        float x = 0.f;
+        if (i == 0) {
+            x = p.scale * op[0];
+        } else if (i < m) {
+            const int jj = (i - 1) >> 1;
+            const float2 t = cs[jj];
+            const float a0 = op[2 * jj + 1], a1 = op[2 * jj + 2];
+            x = p.scale * ((i & 1) ? (t.x * a0 - t.y * a1) : (t.y * a0 + t.x * a1));
+        }
+        xs[i] = x;
+    }
+    __syncthreads();
+    const float *Mh = Mg + (size_t)h * kStoreRows * kStoreRows;
+    {
+        // z_i = sum_j M_ij x_j: two threads per slot row, 64 columns each
+        const int i = tid >> 1, half = tid & 1;
+        float acc = 0.f;
+        if (i < m) {
+            const float4 *row4 = reinterpret_cast<const float4 *>(Mh + (size_t)i * kStoreRows) + half * 16;
+#pragma unroll
+            for (int c = 0; c < 16; ++c) {
+                const float4 mm = row4[c];
+                const int j = half * 64 + 4 * c;
+                acc = fmaf(mm.x, xs[j], acc);
+                acc = fmaf(mm.y, xs[j + 1], acc);
+                acc = fmaf(mm.z, xs[j + 2], acc);
+                acc = fmaf(mm.w, xs[j + 3], acc);
+            }
+        }
+        acc += __shfl_xor(acc, 1);
+        if (half == 0) ws[i] = i < m ? acc : -INFINITY;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const float z0 = ws[lane], z1 = ws[lane + 64];
+        if (p.logits) {
+            if (lane < m) p.logits[(size_t)nh * m + lane] = z0;
+            if (lane + 64 < m) p.logits[(size_t)nh * m + lane + 64] = z1;
+        }
+        float mx = fmaxf(z0, z1);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        const float e0 = lane < m ? __expf(z0 - mx) : 0.f;
+        const float e1 = lane + 64 < m ? __expf(z1 - mx) : 0.f;
+        float sum = e0 + e1;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+        const float inv = 1.f / sum;
+        ws[lane] = e0 * inv;
+        ws[lane + 64] = e1 * inv;
+    }
+    __syncthreads();
+    {
+        // y_j = sum_i M_ij w_i: thread (j, half) sums 64 slot rows
+        const int j = tid & (kStoreRows - 1), half = tid >> 7;
+        float acc = 0.f;
+        for (int i = half * 64; i < half * 64 + 64 && i < m; ++i) acc = fmaf(Mh[(size_t)i * kStoreRows + j], ws[i], acc);
+        yp[half][j] = acc;
+    }
+    __syncthreads();
+    if (tid < kStoreRows) {
+        const int i = tid;
+        float x = 0.f;
+        if (i == 0) {
+            x = yp[0][0] + yp[1][0];
+        } else if (i < m) {
+            const int jj = (i - 1) >> 1;
+            const float2 t = cs[jj];
+            const float a0 = yp[0][2 * jj + 1] + yp[1][2 * jj + 1];
+            const float a1 = yp[0][2 * jj + 2] + yp[1][2 * jj + 2];
+            x = (i & 1) ? (t.x * a0 + t.y * a1) : (-t.y * a0 + t.x * a1);
+        }
+        xs[i] = x;   // o''
+    }
+    __syncthreads();
+    // ---- o = Vbar^T o''
+    {
+        const int c4 = tid % VQ;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int it = 0; it < VIT; ++it) {
+            const int row = it * VROWS_PER_IT + tid / VQ;
+            const float w = xs[row];
+            acc.x = fmaf(vreg[it].x, w, acc.x);
+            acc.y = fmaf(vreg[it].y, w, acc.y);
+            acc.z = fmaf(vreg[it].z, w, acc.z);
+            acc.w = fmaf(vreg[it].w, w, acc.w);
+        }
+        // threads sharing c4 within a wave: lanes differing in the bits above log2(VQ)
+#pragma unroll
+        for (int off = VQ; off < 64; off <<= 1) {
+            acc.x += __shfl_xor(acc.x, off);
+            acc.y += __shfl_xor(acc.y, off);
+            acc.z += __shfl_xor(acc.z, off);
+            acc.w += __shfl_xor(acc.w, off);
+        }
+        if (lane < VQ) opart[wave][c4] = acc;
+    }
+    __syncthreads();
+    if (tid < DV) {
+        const int c4 = tid >> 2, comp = tid & 3;
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) {
+            const float4 t = opart[w][c4];
+            s += comp == 0 ? t.x : comp == 1 ? t.y : comp == 2 ? t.z : t.w;
+        }
+        store_from_float(static_cast<Tin *>(p.o), (size_t)nh * DV + tid, s);
+    }
+    if (tid == 0) p.clock[nh] = lam;
+}
+
+template <int DK, int DV>
+hipError_t launch_typed(const DecParams &p, const float *M, hipStream_t s) {
+    const dim3 grid(p.N * p.H), block(kThreads);
+    if (p.dtype == 0)
+        hipLaunchKernelGGL((decode_kernel<DK, DV, float>), grid, block, 0, s, p, M);
+    else
+        hipLaunchKernelGGL((decode_kernel<DK, DV, __hip_bfloat16>), grid, block, 0, s, p, M);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecParams &p, const float *M, hipStream_t s) {
+    if (p.dk == 128 && p.dv == 128) return launch_typed<128, 128>(p, M, s);
+    if (p.dk == 64 && p.dv == 64) return launch_typed<64, 64>(p, M, s);
+    if (p.dk == 128 && p.dv == 64) return launch_typed<128, 64>(p, M, s);
+    return launch_typed<64, 128>(p, M, s);
+}
+
+}  // namespace cyfa

@@ -1,0 +1,321 @@
+// Vector-ALU chunk-wise CyFA forward (fp32 arithmetic, any supported shape).
+//
+// One workgroup per (b, h) sequence walks its chunks in order and keeps both
+// absolute-clock states in registers.  Per chunk of C tokens (App. B):
+//   clock and log-decay prefix sums      lambda_r (double), G_r = sum log alpha
+//   temporal write matrix                A_r = beta_r U(-lambda_r) b  (Eq. app-temporal-writes)
+//   key pass     O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A        (Eq. app-cyfa-key-chunk)
+//                Kbar <- gamma^C Kbar + (right-rescaled A)^T K
+//   middle step  O''_r = U(-lambda_r) M^T softmax(M U(lambda_r) scale O'_r),  M = R Phi
+//                                                                   (Eq. cyfa-two-pass, middle line)
+//   value pass   O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V      (Eq. app-cyfa-value-chunk)
+//                Vbar <- gamma^C Vbar + A^T (right-rescaled V)
+// gamma^r = exp(G_r), Gamma_rs = exp(G_r - G_s) for r >= s (Eq. app-chunk-decay).
+// The basis order inside the kernel is the one of App. A.1 (0 = DC, 2j-1 =
+// cos_j, 2j = sin_j); rows m..127 are padding and stay zero.
+#include "cyfa_internal.h"
+
+namespace cyfa {
+
+namespace {
+
+constexpr int kValuChunkMax = 16;
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+    return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kThreads) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
+    constexpr int CM = kValuChunkMax;
+    constexpr int KH = DK / 2;             // key-state columns per thread
+    constexpr int VP = kThreads / DV;      // threads sharing a value-state column
+    constexpr int VR = kStoreRows / VP;    // value-state rows per thread
+
+    __shared__ float Qs[CM][DK + 1];
+    __shared__ float Ks[CM][DK + 1];
+    __shared__ float Vs[CM][DV];
+    __shared__ float As[CM][kStoreRows + 1];
+    __shared__ float Ob[CM][kStoreRows];
+    __shared__ float Xb[CM][kStoreRows];
+    __shared__ float Ss[CM][CM];
+    __shared__ float Ms[kStoreRows][kStoreRows + 1];
+    __shared__ float2 CSs[CM][64];
+    __shared__ double lam_s[CM];
+    __shared__ float G_s[CM];
+    __shared__ float beta_s[CM];
+    __shared__ double lam_carry;
+
+    const int bh = blockIdx.x;
+    const int b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int m = p.m, C = p.chunk, T = p.T, H = p.H;
+    const int J = (m - 1) / 2;
+    const float dc = 1.0f / sqrtf((float)m);
+    const float ac = sqrtf(2.0f / (float)m);
+    const Tin *q = static_cast<const Tin *>(p.q);
+    const Tin *k = static_cast<const Tin *>(p.k);
+    const Tin *v = static_cast<const Tin *>(p.v);
+    Tin *o = static_cast<Tin *>(p.o);
+
+    // state ownership
+    const int ki = tid >> 1, kh = tid & 1;            // Kbar row ki, columns [kh*KH, kh*KH+KH)
+    const int vc = tid / VP, vpart = tid % VP;        // Vbar column vc, rows [vpart*VR, +VR)
+    float kst[KH];
+    float vst[VR];
+    {
+        const size_t kbase = ((size_t)bh * kStoreRows + ki) * DK + kh * KH;
+#pragma unroll
+        for (int c = 0; c < KH; ++c) kst[c] = (p.K0 && ki < m) ? p.K0[kbase + c] : 0.f;
+#pragma unroll
+        for (int ii = 0; ii < VR; ++ii) {
+            const int row = vpart * VR + ii;
+            vst[ii] = (p.V0 && row < m) ? p.V0[((size_t)bh * kStoreRows + row) * DV + vc] : 0.f;
+        }
+    }
+    for (int e = tid; e < kStoreRows * kStoreRows; e += kThreads)
+        Ms[e / kStoreRows][e % kStoreRows] = Mg[(size_t)h * kStoreRows * kStoreRows + e];
+    if (tid == 0) lam_carry = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
+    __syncthreads();
+
+    for (int t0 = 0; t0 < T; t0 += C) {
+        const int n = min(C, T - t0);
+        // ---- load the chunk (rows past the end are zero: no write, no decay, no shift)
+        for (int e = tid; e < C * DK; e += kThreads) {
+            const int r = e / DK, c = e % DK;
+            const size_t gi = (((size_t)b * T + t0 + r) * H + h) * DK + c;
+            Qs[r][c] = r < n ? load_as_float(q, gi) : 0.f;
+            Ks[r][c] = r < n ? load_as_float(k, gi) : 0.f;
+        }
+        for (int e = tid; e < C * DV; e += kThreads) {
+            const int r = e / DV, c = e % DV;
+            Vs[r][c] = r < n ? load_as_float(v, (((size_t)b * T + t0 + r) * H + h) * DV + c) : 0.f;
+        }
+        if (tid < C) {
+            const int r = tid;
+            const size_t si = ((size_t)b * T + t0 + r) * H + h;
+            lam_s[r] = r < n ? (double)p.delta[si] : 0.0;
+            G_s[r] = (r < n && p.log_alpha) ? p.log_alpha[si] : 0.f;
+            beta_s[r] = r < n ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+        }
+        __syncthreads();
+        // ---- clock and log-decay prefix sums (double clock, reduced mod m)
+        if (tid == 0) {
+            double lam = lam_carry;
+            float G = 0.f;
+            for (int r = 0; r < C; ++r) {
+                lam += lam_s[r];
+                lam_s[r] = reduce_clock(lam, m);
+                G += G_s[r];
+                G_s[r] = G;
+            }
+            lam_carry = reduce_clock(lam, m);
+        }
+        __syncthreads();
+        for (int e = tid; e < C * J; e += kThreads) {
+            const int r = e / J, jj = e % J;
+            float c, s;
+            clock_phase(lam_s[r], jj + 1, m, &c, &s);
+            CSs[r][jj] = make_float2(c, s);
+        }
+        // S = (Q K^T) (.) Gamma
+        for (int e = tid; e < C * C; e += kThreads) {
+            const int r = e / C, s = e % C;
+            float acc = 0.f;
+            if (s <= r) {
+                for (int c = 0; c < DK; ++c) acc = fmaf(Qs[r][c], Ks[s][c], acc);
+                acc *= __expf(G_s[r] - G_s[s]);
+            }
+            Ss[r][s] = acc;
+        }
+        __syncthreads();
+        // temporal write matrix A_r = beta_r U(-lambda_r) b
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, i = e % kStoreRows;
+            const float be = beta_s[r];
+            float val = 0.f;
+            if (i == 0) {
+                val = be * dc;
+            } else if (i < m) {
+                const float2 cs = CSs[r][(i - 1) >> 1];
+                val = (i & 1) ? be * ac * cs.x : -be * ac * cs.y;
+            }
+            As[r][i] = val;
+        }
+        // key pass, inter-chunk part: O'_r = gamma^r Kbar q_r (old state)
+        for (int r = 0; r < C; ++r) {
+            float part = 0.f;
+#pragma unroll
+            for (int c = 0; c < KH; ++c) part = fmaf(Qs[r][kh * KH + c], kst[c], part);
+            part += __shfl_xor(part, 1);
+            if (kh == 0) Ob[r][ki] = __expf(G_s[r]) * part;
+        }
+        __syncthreads();
+        // key pass, intra-chunk part: O' += S A
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, i = e % kStoreRows;
+            float acc = Ob[r][i];
+            for (int s = 0; s <= r; ++s) acc = fmaf(Ss[r][s], As[s][i], acc);
+            Ob[r][i] = acc;
+        }
+        // key state carry: Kbar <- gamma^C Kbar + (right-rescaled A)^T K
+        {
+            const float Glast = G_s[C - 1];
+            const float gC = __expf(Glast);
+#pragma unroll
+            for (int c = 0; c < KH; ++c) kst[c] *= gC;
+            for (int r = 0; r < C; ++r) {
+                const float w = As[r][ki] * __expf(Glast - G_s[r]);
+#pragma unroll
+                for (int c = 0; c < KH; ++c) kst[c] = fmaf(w, Ks[r][kh * KH + c], kst[c]);
+            }
+        }
+        __syncthreads();
+        // middle step: X_r = U(lambda_r) (scale O'_r)
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, i = e % kStoreRows;
+            float x = 0.f;
+            if (i == 0) {
+                x = p.scale * Ob[r][0];
+            } else if (i < m) {
+                const int jj = (i - 1) >> 1;
+                const float2 cs = CSs[r][jj];
+                const float a0 = Ob[r][2 * jj + 1], a1 = Ob[r][2 * jj + 2];
+                x = p.scale * ((i & 1) ? (cs.x * a0 - cs.y * a1) : (cs.y * a0 + cs.x * a1));
+            }
+            Xb[r][i] = x;
+        }
+        __syncthreads();
+        // slot logits Z_r = M X_r
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, i = e % kStoreRows;
+            float acc = 0.f;
+            if (i < m) {
+                for (int j = 0; j < m; ++j) acc = fmaf(Ms[i][j], Xb[r][j], acc);
+                if (p.logits && r < n)
+                    p.logits[(((size_t)b * T + t0 + r) * H + h) * m + i] = acc;
+            }
+            Ob[r][i] = acc;
+        }
+        __syncthreads();
+        // softmax over the m active slots (padding slots excluded)
+        for (int r = wave; r < C; r += kThreads / 64) {
+            const float z0 = lane < m ? Ob[r][lane] : -INFINITY;
+            const float z1 = lane + 64 < m ? Ob[r][lane + 64] : -INFINITY;
+            const float mx = wave_max(fmaxf(z0, z1));
+            const float e0 = lane < m ? __expf(z0 - mx) : 0.f;
+            const float e1 = lane + 64 < m ? __expf(z1 - mx) : 0.f;
+            const float inv = 1.f / wave_sum(e0 + e1);
+            Ob[r][lane] = e0 * inv;
+            Ob[r][lane + 64] = e1 * inv;
+        }
+        __syncthreads();
+        // Y_r = M^T W_r
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, j = e % kStoreRows;
+            float acc = 0.f;
+            if (j < m)
+                for (int i = 0; i < m; ++i) acc = fmaf(Ob[r][i], Ms[i][j], acc);
+            Xb[r][j] = acc;
+        }
+        __syncthreads();
+        // O''_r = U(-lambda_r) Y_r
+        for (int e = tid; e < C * kStoreRows; e += kThreads) {
+            const int r = e / kStoreRows, i = e % kStoreRows;
+            float x = 0.f;
+            if (i == 0) {
+                x = Xb[r][0];
+            } else if (i < m) {
+                const int jj = (i - 1) >> 1;
+                const float2 cs = CSs[r][jj];
+                const float a0 = Xb[r][2 * jj + 1], a1 = Xb[r][2 * jj + 2];
+                x = (i & 1) ? (cs.x * a0 + cs.y * a1) : (-cs.y * a0 + cs.x * a1);
+            }
+            Ob[r][i] = x;
+        }
+        __syncthreads();
+        // value pass: S2 = (O'' A^T) (.) Gamma
+        for (int e = tid; e < C * C; e += kThreads) {
+            const int r = e / C, s = e % C;
+            float acc = 0.f;
+            if (s <= r) {
+                for (int i = 0; i < m; ++i) acc = fmaf(Ob[r][i], As[s][i], acc);
+                acc *= __expf(G_s[r] - G_s[s]);
+            }
+            Ss[r][s] = acc;
+        }
+        __syncthreads();
+        // O_r = gamma^r Vbar^T O''_r + sum_s S2_rs V_s
+        for (int r = 0; r < C; ++r) {
+            float part = 0.f;
+#pragma unroll
+            for (int ii = 0; ii < VR; ++ii) part = fmaf(Ob[r][vpart * VR + ii], vst[ii], part);
+#pragma unroll
+            for (int off = 1; off < VP; off <<= 1) part += __shfl_xor(part, off);
+            if (vpart == 0 && r < n) {
+                float acc = __expf(G_s[r]) * part;
+                for (int s = 0; s <= r; ++s) acc = fmaf(Ss[r][s], Vs[s][vc], acc);
+                store_from_float(o, (((size_t)b * T + t0 + r) * H + h) * DV + vc, acc);
+            }
+        }
+        // value state carry: Vbar <- gamma^C Vbar + A^T (right-rescaled V)
+        {
+            const float Glast = G_s[C - 1];
+            const float gC = __expf(Glast);
+#pragma unroll
+            for (int ii = 0; ii < VR; ++ii) vst[ii] *= gC;
+            for (int r = 0; r < C; ++r) {
+                const float w = Vs[r][vc] * __expf(Glast - G_s[r]);
+#pragma unroll
+                for (int ii = 0; ii < VR; ++ii) vst[ii] = fmaf(As[r][vpart * VR + ii], w, vst[ii]);
+            }
+        }
+        __syncthreads();
+    }
+
+    if (p.K_out) {
+        const size_t kbase = ((size_t)bh * kStoreRows + ki) * DK + kh * KH;
+#pragma unroll
+        for (int c = 0; c < KH; ++c) p.K_out[kbase + c] = ki < m ? kst[c] : 0.f;
+    }
+    if (p.V_out) {
+#pragma unroll
+        for (int ii = 0; ii < VR; ++ii) {
+            const int row = vpart * VR + ii;
+            p.V_out[((size_t)bh * kStoreRows + row) * DV + vc] = row < m ? vst[ii] : 0.f;
+        }
+    }
+    if (p.clock_out && tid == 0) p.clock_out[bh] = lam_carry;
+}
+
+template <int DK, int DV>
+hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
+    const dim3 grid(p.B * p.H), block(kThreads);
+    if (p.dtype == 0)
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, float>), grid, block, 0, s, p, M);
+    else
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, __hip_bfloat16>), grid, block, 0, s, p, M);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int valu_chunk_max() { return kValuChunkMax; }
+
+hipError_t launch_fwd_valu(const FwdParams &p, const float *M, hipStream_t s) {
+    if (p.dk == 128 && p.dv == 128) return launch_typed<128, 128>(p, M, s);
+    if (p.dk == 64 && p.dv == 64) return launch_typed<64, 64>(p, M, s);
+    if (p.dk == 128 && p.dv == 64) return launch_typed<128, 64>(p, M, s);
+    return launch_typed<64, 128>(p, M, s);
+}
+
+}  // namespace cyfa

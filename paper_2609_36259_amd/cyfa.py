@@ -1,0 +1,235 @@
+"""Thin Python binding of libcyfa.so (the C ABI in include/cyfa.h).
+
+Argument marshalling only: tensors are torch CUDA (HIP) tensors, the work is
+enqueued on torch's current stream, and every step of the operator runs in the
+library's HIP kernels.  There is no fallback: if the library is missing the
+calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcyfa.so")
+
+F32, BF16 = 0, 1
+KERNEL_AUTO, KERNEL_VALU, KERNEL_MFMA = 0, 1, 2
+STATUS = {0: "CYFA_OK", 1: "CYFA_ERR_INVALID_ARGUMENT", 2: "CYFA_ERR_UNSUPPORTED",
+          3: "CYFA_ERR_WORKSPACE", 4: "CYFA_ERR_LAUNCH"}
+STORE_ROWS = 128
+
+# Every symbol include/cyfa.h declares.
+EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_decode_workspace_size",
+            "cyfa_decode_step", "cyfa_set_timing_events", "cyfa_status_string",
+            "cyfa_last_error", "cyfa_version")
+
+
+class CyfaError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class FwdDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("m", ctypes.c_int32),
+                ("chunk", ctypes.c_int32), ("segments", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32), ("kernel", ctypes.c_int32)]
+
+
+class DecDesc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("d_k", ctypes.c_int32),
+                ("d_v", ctypes.c_int32), ("m", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+_vp = ctypes.c_void_p
+
+
+def load() -> ctypes.CDLL:
+    """Load libcyfa.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "or python -m paper_2609_36259_amd.build")
+        lib = ctypes.CDLL(LIB_PATH)
+        lib.cyfa_forward_workspace_size.argtypes = [ctypes.POINTER(FwdDesc),
+                                                    ctypes.POINTER(ctypes.c_size_t)]
+        lib.cyfa_forward_workspace_size.restype = ctypes.c_int
+        lib.cyfa_forward.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 16 + [ctypes.c_size_t, _vp]
+        lib.cyfa_forward.restype = ctypes.c_int
+        lib.cyfa_decode_workspace_size.argtypes = [ctypes.POINTER(DecDesc),
+                                                   ctypes.POINTER(ctypes.c_size_t)]
+        lib.cyfa_decode_workspace_size.restype = ctypes.c_int
+        lib.cyfa_decode_step.argtypes = [ctypes.POINTER(DecDesc)] + [_vp] * 13 + [ctypes.c_size_t, _vp]
+        lib.cyfa_decode_step.restype = ctypes.c_int
+        lib.cyfa_status_string.argtypes = [ctypes.c_int]
+        lib.cyfa_status_string.restype = ctypes.c_char_p
+        lib.cyfa_last_error.argtypes = []
+        lib.cyfa_last_error.restype = ctypes.c_char_p
+        lib.cyfa_set_timing_events.argtypes = [_vp, _vp]
+        lib.cyfa_set_timing_events.restype = ctypes.c_int
+        lib.cyfa_version.argtypes = []
+        lib.cyfa_version.restype = ctypes.c_int32
+        _lib = lib
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise CyfaError(status, load().cyfa_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"q/k/v must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need(t, shape, dtype, name):
+    if t is None:
+        return None
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    return t
+
+
+def _stream_handle(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def set_timing_events(start_event, stop_event):
+    """Install (or clear with None, None) hipEvent_t handles recorded around the main kernel."""
+    _check(load().cyfa_set_timing_events(start_event, stop_event))
+
+
+def forward_desc(B, T, H, dk, dv, *, m=127, chunk=0, segments=0, scale=None, dtype=BF16,
+                 kernel=KERNEL_AUTO) -> FwdDesc:
+    return FwdDesc(B, T, H, dk, dv, m, chunk, segments,
+                   float(dk ** -0.5 if scale is None else scale), dtype, kernel)
+
+
+def forward_workspace_size(desc: FwdDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().cyfa_forward_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def selected_kernel(desc: FwdDesc) -> str:
+    """Which kernel a forward with this descriptor runs: "mfma" or "valu"."""
+    if desc.kernel == KERNEL_VALU:
+        return "valu"
+    if desc.kernel == KERNEL_MFMA:
+        return "mfma"
+    trial = FwdDesc.from_buffer_copy(desc)
+    trial.kernel = KERNEL_MFMA
+    n = ctypes.c_size_t(0)
+    ok = load().cyfa_forward_workspace_size(ctypes.byref(trial), ctypes.byref(n)) == 0
+    return "mfma" if ok and desc.chunk in (0, 64) else "valu"
+
+
+def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=127,
+            chunk=0, segments=0, kernel=KERNEL_AUTO, K0=None, V0=None, clock0=None,
+            return_state=False, return_logits=False, out=None, workspace=None, stream=None):
+    """CyFA forward: q,k [B,T,H,dk], v [B,T,H,dv] (float32 or bfloat16), scalars [B,T,H] float32.
+
+    Returns ``o`` [B,T,H,dv] (dtype of q) or a dict with ``o`` and, when requested,
+    the final absolute-clock states ``K``/``V`` [B,H,128,d], ``clock`` [B,H] (float64)
+    and the slot ``logits`` [B,T,H,m].
+    """
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = _dtype_code(q)
+    _need(q, (B, T, H, dk), q.dtype, "q")
+    _need(k, (B, T, H, dk), q.dtype, "k")
+    _need(v, (B, T, H, dv), q.dtype, "v")
+    for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
+        _need(t, (B, T, H), torch.float32, name)
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(K0, (B, H, STORE_ROWS, dk), torch.float32, "K0")
+    _need(V0, (B, H, STORE_ROWS, dv), torch.float32, "V0")
+    _need(clock0, (B, H), torch.float64, "clock0")
+    desc = forward_desc(B, T, H, dk, dv, m=m, chunk=chunk, segments=segments, scale=scale,
+                        dtype=dt, kernel=kernel)
+    nbytes = forward_workspace_size(desc)
+    dev = q.device
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    o = out if out is not None else torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    _need(o, (B, T, H, dv), q.dtype, "out")
+    K_out = torch.empty((B, H, STORE_ROWS, dk), dtype=torch.float32, device=dev) if return_state else None
+    V_out = torch.empty((B, H, STORE_ROWS, dv), dtype=torch.float32, device=dev) if return_state else None
+    clk = torch.empty((B, H), dtype=torch.float64, device=dev) if return_state else None
+    logits = torch.empty((B, T, H, m), dtype=torch.float32, device=dev) if return_logits else None
+    st = load().cyfa_forward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
+                             _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(K0), _ptr(V0),
+                             _ptr(clock0), _ptr(o), _ptr(K_out), _ptr(V_out), _ptr(clk),
+                             _ptr(logits), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+                             _stream_handle(stream))
+    _check(st)
+    if not (return_state or return_logits):
+        return o
+    res = {"o": o}
+    if return_state:
+        res.update(K=K_out, V=V_out, clock=clk)
+    if return_logits:
+        res["logits"] = logits
+    return res
+
+
+def decode_desc(N, H, dk, dv, *, m=127, scale=None, dtype=F32) -> DecDesc:
+    return DecDesc(N, H, dk, dv, m, float(dk ** -0.5 if scale is None else scale), dtype)
+
+
+def decode_workspace_size(desc: DecDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().cyfa_decode_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def decode_step(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, *, scale=None,
+                m=127, return_logits=False, out=None, workspace=None, stream=None):
+    """One in-place decode step: q,k [N,H,dk], v [N,H,dv]; scalars [N,H] float32;
+    states K [N,H,128,dk], V [N,H,128,dv] float32 and clock [N,H] float64 (updated)."""
+    N, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = _dtype_code(q)
+    _need(k, (N, H, dk), q.dtype, "k")
+    _need(v, (N, H, dv), q.dtype, "v")
+    for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
+        _need(t, (N, H), torch.float32, name)
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(K, (N, H, STORE_ROWS, dk), torch.float32, "K")
+    _need(V, (N, H, STORE_ROWS, dv), torch.float32, "V")
+    _need(clock, (N, H), torch.float64, "clock")
+    desc = decode_desc(N, H, dk, dv, m=m, scale=scale, dtype=dt)
+    nbytes = decode_workspace_size(desc)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    o = out if out is not None else torch.empty((N, H, dv), dtype=q.dtype, device=q.device)
+    logits = torch.empty((N, H, m), dtype=torch.float32, device=q.device) if return_logits else None
+    st = load().cyfa_decode_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
+                                 _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(K), _ptr(V),
+                                 _ptr(clock), _ptr(o), _ptr(logits), _ptr(workspace),
+                                 ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
+    _check(st)
+    return (o, logits) if return_logits else o

@@ -1,0 +1,112 @@
+"""The C ABI library loads, exports every declared symbol, and validates on the
+host (no GPU needed: every rejected call returns before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36259_amd import cyfa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    txt = open(os.path.join(ROOT, "include", "cyfa.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(cyfa_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = cyfa.load()
+    names = _declared_functions()
+    assert set(names) == set(cyfa.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.cyfa_version() >= 100
+    for code in range(5):
+        assert lib.cyfa_status_string(code)
+
+
+def _ws(desc):
+    return cyfa.forward_workspace_size(desc)
+
+
+def test_workspace_sizes_and_kernel_selection():
+    d = cyfa.forward_desc(4, 4096, 16, 128, 128, dtype=cyfa.BF16)
+    assert _ws(d) >= 16 * 128 * 128 * 4
+    d = cyfa.forward_desc(1, 256, 2, 64, 64, dtype=cyfa.F32)
+    assert _ws(d) == 2 * 128 * 128 * 4
+    dd = cyfa.decode_desc(256, 16, 128, 128)
+    assert cyfa.decode_workspace_size(dd) == 16 * 128 * 128 * 4
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("m", 128, cyfa.CyfaError), ("m", 1, cyfa.CyfaError), ("m", 129, cyfa.CyfaError),
+    ("d_k", 96, cyfa.CyfaError), ("d_v", 0, cyfa.CyfaError), ("B", 0, cyfa.CyfaError),
+    ("H", 0, cyfa.CyfaError), ("T", -1, cyfa.CyfaError), ("dtype", 5, cyfa.CyfaError),
+    ("kernel", 7, cyfa.CyfaError), ("segments", -1, cyfa.CyfaError), ("chunk", 48, cyfa.CyfaError),
+])
+def test_descriptor_validation(field, value, status):
+    d = cyfa.forward_desc(2, 64, 2, 64, 64, dtype=cyfa.F32)
+    setattr(d, field, value)
+    with pytest.raises(status):
+        _ws(d)
+
+
+def test_status_codes():
+    lib = cyfa.load()
+    n = ctypes.c_size_t(0)
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, m=128)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 1
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, m=255)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    assert b"127" in lib.cyfa_last_error()
+    d = cyfa.forward_desc(1, 16, 1, 96, 64)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    assert lib.cyfa_forward_workspace_size(None, ctypes.byref(n)) == 1
+
+
+def _call_forward(desc, ptrs, ws=0, ws_bytes=0):
+    lib = cyfa.load()
+    args = [ptrs.get(k) for k in ("q", "k", "v", "delta", "log_alpha", "beta", "R", "K0", "V0",
+                                  "clock0", "o", "K_out", "V_out", "clock_out", "logits")]
+    return lib.cyfa_forward(ctypes.byref(desc), *[ctypes.c_void_p(a) if a else None for a in args],
+                            ctypes.c_void_p(ws) if ws else None, ctypes.c_size_t(ws_bytes), None)
+
+
+def test_forward_rejects_before_launch():
+    # fake, never dereferenced, suitably aligned addresses: every call below must
+    # fail validation before touching the device
+    base = 1 << 40
+    good = dict(q=base, k=base + (1 << 20), v=base + (2 << 20), delta=base + (3 << 20),
+                o=base + (4 << 20))
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, dtype=cyfa.F32)
+    need = _ws(d)
+    assert _call_forward(d, {k: v for k, v in good.items() if k != "q"}, base, need) == 1
+    assert _call_forward(d, dict(good, q=base + 8), base, need) == 1          # misaligned
+    assert _call_forward(d, good, 0, 0) == 3                                   # no workspace
+    assert _call_forward(d, good, base, need - 1) == 3                         # too small
+    assert _call_forward(d, good, base + 128, need) == 1                       # ws misaligned
+    assert _call_forward(d, dict(good, K_out=base + (5 << 20), V_out=base + (5 << 20)), base, need) == 1
+    d.kernel = cyfa.KERNEL_MFMA
+    d.dtype = cyfa.F32
+    assert _call_forward(d, good, base, need) == 2                             # unsupported
+
+
+def test_decode_rejects_before_launch():
+    lib = cyfa.load()
+    d = cyfa.decode_desc(2, 2, 64, 64)
+    args = [None] * 13
+    st = lib.cyfa_decode_step(ctypes.byref(d), *args, ctypes.c_size_t(0), None)
+    assert st == 1
+    d = cyfa.decode_desc(2, 2, 64, 64, m=4)
+    st = lib.cyfa_decode_step(ctypes.byref(d), *args, ctypes.c_size_t(0), None)
+    assert st == 1
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(cyfa, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(cyfa, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        cyfa.load()

@@ -1,0 +1,194 @@
+"""GPU parity of the vector-ALU forward kernel and of the decode step against the oracle."""
+import numpy as np
+import pytest
+
+from paper_2609_36259_amd.inputs import FWD_TINY, make_forward_inputs, workload_inputs
+from tests.harness import (TOL_BF16, TOL_F32, clock_err, oracle_states_abs, pairs_view, rel_err,
+                           run_oracle, state_view, upload)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _cyfa():
+    from paper_2609_36259_amd import cyfa
+    return cyfa
+
+
+def _fwd(x, t, **kw):
+    return _cyfa().forward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                           scale=x["scale"], m=x["m"], **kw)
+
+
+def _check_full(x, res, tol, *, check_state=True):
+    B, T, H = x["delta"].shape
+    ref = run_oracle(x)
+    pairs = list(range(B * H))
+    e_o = rel_err(pairs_view(res["o"], pairs, H), ref["o"])
+    out = {"o": e_o}
+    if "logits" in res:
+        out["z"] = rel_err(pairs_view(res["logits"], pairs, H), ref["z"])
+    if check_state and "K" in res:
+        Kref, Vref = oracle_states_abs(ref, x["m"])
+        out["K"] = rel_err(state_view(res["K"], pairs, H), Kref)
+        out["V"] = rel_err(state_view(res["V"], pairs, H), Vref)
+        out["clock"] = clock_err(res["clock"].cpu().numpy().reshape(-1), ref["lam"], x["m"])
+    print("errors", {k: f"{v:.2e}" for k, v in out.items()}, flush=True)
+    for k, v in out.items():
+        assert v <= (1e-9 if k == "clock" else tol), (k, v)
+    return out
+
+
+def test_tiny_f32_workload_full_parity():
+    x = workload_inputs(FWD_TINY)
+    t = upload(x)
+    res = _fwd(x, t, return_state=True, return_logits=True)
+    _check_full(x, res, TOL_F32)
+
+
+@pytest.mark.parametrize("variant", ["no_beta_no_R", "peaky", "small_m", "ragged_chunk8",
+                                     "d128_f32", "mixed_dims"])
+def test_f32_variants(variant):
+    kw = {}
+    dk = dv = 64
+    B, T, H, m = 1, 130, 2, 127
+    if variant == "small_m":
+        m = 7
+    if variant == "ragged_chunk8":
+        T, kw = 77, {"chunk": 8}
+    if variant == "d128_f32":
+        dk = dv = 128
+    x = make_forward_inputs(B, T, H, dk, dv, seed=21, dtype="f32", m=m,
+                            with_beta=variant != "no_beta_no_R", with_R=variant != "no_beta_no_R")
+    if variant == "mixed_dims":
+        y = make_forward_inputs(B, T, H, 128, 64, seed=22, dtype="f32")
+        x = y
+    if variant == "peaky":
+        x["scale"] = 30.0
+    t = upload(x)
+    res = _fwd(x, t, return_state=True, return_logits=True, **kw)
+    _check_full(x, res, TOL_F32)
+
+
+def test_bf16_valu_kernel():
+    x = make_forward_inputs(2, 150, 3, 128, 128, seed=23, dtype="bf16")
+    t = upload(x)
+    res = _fwd(x, t, return_state=True, return_logits=True, kernel=_cyfa().KERNEL_VALU)
+    _check_full(x, res, TOL_BF16)
+
+
+def test_split_and_resume_equals_one_pass():
+    cyfa = _cyfa()
+    x = make_forward_inputs(2, 100, 2, 64, 64, seed=24, dtype="f32")
+    t = upload(x)
+    full = _fwd(x, t, return_state=True)
+    t1 = 37
+    a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    first = _fwd(x, a, return_state=True)
+    second = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
+                          scale=x["scale"], K0=first["K"], V0=first["V"], clock0=first["clock"],
+                          return_state=True)
+    torch.cuda.synchronize()
+    o_split = torch.cat([first["o"], second["o"]], dim=1)
+    assert rel_err(o_split.cpu().numpy(), full["o"].cpu().numpy()) <= 1e-5
+    assert rel_err(second["K"].cpu().numpy(), full["K"].cpu().numpy()) <= 1e-5
+    assert clock_err(second["clock"].cpu().numpy(), full["clock"].cpu().numpy(), 127) <= 1e-9
+
+
+def test_empty_sequence_returns_initial_state():
+    cyfa = _cyfa()
+    x = make_forward_inputs(1, 0, 2, 64, 64, seed=25, dtype="f32")
+    t = upload(x)
+    K0 = torch.randn(1, 2, 128, 64, device="cuda")
+    K0[:, :, 127:] = 0
+    V0 = torch.randn(1, 2, 128, 64, device="cuda")
+    V0[:, :, 127:] = 0
+    c0 = torch.tensor([[3.5, 200.25]], dtype=torch.float64, device="cuda")
+    res = cyfa.forward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                       K0=K0, V0=V0, clock0=c0, return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(res["K"], K0) and torch.equal(res["V"], V0)
+    np.testing.assert_allclose(res["clock"].cpu().numpy(), [[3.5, 200.25 - 127]], atol=1e-12)
+
+
+def test_deterministic():
+    x = make_forward_inputs(1, 64, 2, 64, 64, seed=26, dtype="f32")
+    t = upload(x)
+    a = _fwd(x, t)
+    b = _fwd(x, t)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_nan_input_propagates_without_fault():
+    x = make_forward_inputs(1, 40, 1, 64, 64, seed=27, dtype="f32")
+    x["q"][0, 10, 0, 3] = np.nan
+    t = upload(x)
+    o = _fwd(x, t)
+    torch.cuda.synchronize()
+    o = o.cpu().numpy()
+    assert np.isnan(o[0, 10]).all()
+    assert np.isfinite(o[0, :10]).all()
+
+
+def _decode_case(N, H, d, prefix, steps, seed, dtype="f32", with_logits=True):
+    cyfa = _cyfa()
+    x = make_forward_inputs(N, prefix + steps, H, d, d, seed=seed, dtype=dtype)
+    ref = run_oracle(x)
+    t = upload(x)
+    pre = {k: (v[:, :prefix].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    st = cyfa.forward(pre["q"], pre["k"], pre["v"], pre["delta"], pre["log_alpha"], pre["beta"],
+                      pre["R"], scale=x["scale"], return_state=True)
+    K, V, clk = st["K"], st["V"], st["clock"]
+    outs, logits = [], []
+    for s in range(steps):
+        tok = {k: (v[:, prefix + s].contiguous() if v is not None and k != "R" else v)
+               for k, v in t.items()}
+        o, z = cyfa.decode_step(tok["q"], tok["k"], tok["v"], tok["delta"], K, V, clk,
+                                tok["log_alpha"], tok["beta"], t["R"], scale=x["scale"],
+                                return_logits=True)
+        outs.append(o.float().cpu().numpy())
+        logits.append(z.cpu().numpy())
+    torch.cuda.synchronize()
+    pairs = list(range(N * H))
+    got = np.stack(outs, axis=1)                       # [N, steps, H, d]
+    got = np.stack([got[p // H, :, p % H] for p in pairs])
+    zg = np.stack(logits, axis=1)
+    zg = np.stack([zg[p // H, :, p % H] for p in pairs])
+    e_o = rel_err(got, ref["o"][:, prefix:])
+    e_z = rel_err(zg, ref["z"][:, prefix:])
+    Kref, Vref = oracle_states_abs(ref, x["m"])
+    e_K = rel_err(state_view(K, pairs, H), Kref)
+    e_c = clock_err(clk.cpu().numpy().reshape(-1), ref["lam"], x["m"])
+    print(f"decode errors o {e_o:.2e} z {e_z:.2e} K {e_K:.2e} clock {e_c:.1e}", flush=True)
+    return e_o, e_z, e_K, e_c
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_steps_match_oracle_f32(d):
+    e_o, e_z, e_K, e_c = _decode_case(3, 2, d, prefix=33, steps=6, seed=30 + d)
+    assert e_o <= TOL_F32 and e_z <= TOL_F32 and e_K <= TOL_F32 and e_c <= 1e-9
+
+
+def test_decode_steps_match_oracle_bf16():
+    e_o, e_z, e_K, e_c = _decode_case(2, 3, 128, prefix=20, steps=4, seed=33, dtype="bf16")
+    assert e_o <= TOL_BF16 and e_z <= TOL_BF16 and e_K <= TOL_BF16 and e_c <= 1e-9
+
+
+def test_decode_consistent_with_forward():
+    """forward over T+1 tokens == forward over T tokens, then one decode step."""
+    cyfa = _cyfa()
+    x = make_forward_inputs(2, 41, 2, 128, 128, seed=34, dtype="f32")
+    t = upload(x)
+    full = _fwd(x, t, return_state=True)
+    pre = {k: (v[:, :40].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    st = cyfa.forward(pre["q"], pre["k"], pre["v"], pre["delta"], pre["log_alpha"], pre["beta"],
+                      pre["R"], scale=x["scale"], return_state=True)
+    tok = {k: (v[:, 40].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    o = cyfa.decode_step(tok["q"], tok["k"], tok["v"], tok["delta"], st["K"], st["V"], st["clock"],
+                         tok["log_alpha"], tok["beta"], t["R"], scale=x["scale"])
+    torch.cuda.synchronize()
+    assert rel_err(o.cpu().numpy(), full["o"][:, 40].cpu().numpy()) <= 1e-5
+    assert rel_err(st["K"].cpu().numpy(), full["K"].cpu().numpy()) <= 1e-5

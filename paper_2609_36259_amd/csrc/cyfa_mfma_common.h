@@ -1,0 +1,134 @@
+// Shared pieces of the matrix-core (bf16 MFMA) forward kernels.
+//
+// Slot/basis index order used inside these kernels (the "internal" order):
+// the 63 cosine/sine pairs of the real Fourier basis (App. A.1) come first,
+// pair j = 1..63 at internal indices (2j-2, 2j-1) = (cos_j, sin_j); the DC
+// component sits at internal index 126 and index 127 is the storage padding
+// (App. A.7).  In paper order the same coordinates are 2j-1, 2j and 0.  With
+// pairs on adjacent indices, a rotation U(tau) acts on neighbouring lanes of
+// an MFMA accumulator.  For m < 127 the unused pairs are zero padding too.
+//
+// MFMA v_mfma_f32_32x32x16_bf16 lane layouts (l = lane, h = l / 32):
+//   A (32 x 16): lane l holds A[l % 32][8h + p], p = 0..7
+//   B (16 x 32): lane l holds B[8h + p][l % 32]
+//   D (32 x 32): lane l, register v holds D[8(v/4) + 4h + v%4][l % 32]
+// A state accumulator fed back as a B operand supplies, at k-step ks, the
+// k indices 16ks + {4h..4h+3, 8+4h..8+4h+3}; the other operand is read in
+// that same permuted order ("perm" reads below).
+#pragma once
+
+#include "cyfa_internal.h"
+
+namespace cyfa {
+namespace mfma {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+constexpr int C = 64;             // chunk length
+constexpr int D = 128;            // head dim
+constexpr int NT = 256;           // threads per workgroup (4 waves)
+constexpr int QS = 136;           // row stride (bf16) of [64][128] tiles
+constexpr int TS = 72;            // row stride (bf16) of [128][64] tiles
+constexpr int SS = 72;            // row stride (bf16) of the [64][64] score tile
+constexpr int ZS = 132;           // row stride (float) of the [64][128] logit tile
+constexpr int kDC = 126;          // internal index of the DC coordinate
+constexpr int kStateFloats = 2 * 128 * 128;   // one (b, h) segment: K then V
+
+__device__ __forceinline__ f32x16 mma(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// A zero accumulator materialised where it is used: keeps the compiler from
+// hoisting one zero vector per accumulator out of the chunk loop and holding
+// them all live across it.
+__device__ __forceinline__ f32x16 zero_acc() {
+    f32x16 z = {};
+    asm volatile("" : "+v"(z));
+    return z;
+}
+
+__device__ __forceinline__ bf16x8 lds8(const __bf16 *p) {      // 16-byte LDS read
+    return *reinterpret_cast<const bf16x8 *>(p);
+}
+__device__ __forceinline__ bf16x8 lds8_perm(const __bf16 *row, int k0, int h) {
+    // k indices k0 + {4h..4h+3} and k0 + 8 + {4h..4h+3}
+    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(row + k0 + 4 * h);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(row + k0 + 8 + 4 * h);
+    bf16x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+}
+// registers 8*half .. 8*half+7 of an accumulator as a bf16 B operand
+__device__ __forceinline__ bf16x8 acc_to_operand(const f32x16 &acc, int half) {
+    bf16x8 r;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) r[p] = (__bf16)acc[8 * half + p];
+    return r;
+}
+
+// internal index -> paper-order basis index (or -1 for padding)
+__host__ __device__ __forceinline__ int internal_to_paper(int i, int m) {
+    if (i == kDC) return 0;
+    if (i < m - 1) return i + 1;
+    return -1;
+}
+
+// Offsets of element (i, c) of a segment state in the accumulator-dump layout.
+// Key state: wave w = i / 32 owns columns i of Kbar^T (rows d = c), blocks db = c / 32.
+__host__ __device__ __forceinline__ int dump_index_K(int i, int c) {
+    const int w = i >> 5, lane_lo = i & 31;
+    const int db = c >> 5, cr = c & 31;
+    const int h = (cr >> 2) & 1;
+    const int v = ((cr >> 3) << 2) | (cr & 3);
+    const int lane = lane_lo + 32 * h;
+    return ((w * 4 + db) * 16 + v) * 64 + lane;
+}
+// Value state: wave w = c / 32 owns columns c of Vbar (rows i), blocks ib = i / 32.
+__host__ __device__ __forceinline__ int dump_index_V(int i, int c) {
+    const int w = c >> 5, lane_lo = c & 31;
+    const int ib = i >> 5, ir = i & 31;
+    const int h = (ir >> 2) & 1;
+    const int v = ((ir >> 3) << 2) | (ir & 3);
+    const int lane = lane_lo + 32 * h;
+    return 128 * 128 + ((w * 4 + ib) * 16 + v) * 64 + lane;
+}
+
+// Value of lane l ^ 1 (DPP quad permutation [1,0,3,2]).
+__device__ __forceinline__ float swap_pair(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+}
+// Value of lane l ^ 2 (DPP quad permutation [2,3,0,1]).
+__device__ __forceinline__ float swap_halves4(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+}
+
+// ---- chunk-local prefix sums on one wave (lane = token row) --------------
+__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+__device__ __forceinline__ double wave_incl_scan(double x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
+// cos / sin of 2 pi * rev (rev in revolutions, |rev| < 256) on the hardware units
+__device__ __forceinline__ void sincos_rev(float rev, float *s, float *c) {
+    *s = __builtin_amdgcn_sinf(rev);
+    *c = __builtin_amdgcn_cosf(rev);
+}
+
+}  // namespace mfma
+}  // namespace cyfa

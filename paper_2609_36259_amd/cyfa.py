@@ -226,6 +226,7 @@ def decode_step(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, 
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     o = out if out is not None else torch.empty((N, H, dv), dtype=q.dtype, device=q.device)
+    _need(o, (N, H, dv), q.dtype, "out")
     logits = torch.empty((N, H, m), dtype=torch.float32, device=q.device) if return_logits else None
     st = load().cyfa_decode_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
                                  _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(K), _ptr(V),

@@ -2,7 +2,8 @@
 import numpy as np
 import pytest
 
-from paper_2609_36259_amd.inputs import FWD_TINY, make_forward_inputs, workload_inputs
+from paper_2609_36259_amd.inputs import (DECODE, FWD_TINY, make_decode_inputs, make_forward_inputs,
+                                         workload_inputs)
 from tests.harness import (TOL_BF16, TOL_F32, clock_err, oracle_states_abs, pairs_view, rel_err,
                            run_oracle, state_view, upload)
 
@@ -177,6 +178,19 @@ def test_decode_steps_match_oracle_bf16():
     assert e_o <= TOL_BF16 and e_z <= TOL_BF16 and e_K <= TOL_BF16 and e_c <= 1e-9
 
 
+def test_decode_rejects_strided_output():
+    cyfa = _cyfa()
+    x = make_forward_inputs(2, 1, 2, 64, 64, seed=35, dtype="f32")
+    t = upload(x)
+    K = torch.zeros(2, 2, 128, 64, device="cuda")
+    V = torch.zeros(2, 2, 128, 64, device="cuda")
+    clk = torch.zeros(2, 2, dtype=torch.float64, device="cuda")
+    big = torch.empty(2, 3, 2, 64, device="cuda")
+    with pytest.raises(ValueError):
+        cyfa.decode_step(t["q"][:, 0], t["k"][:, 0], t["v"][:, 0], t["delta"][:, 0], K, V, clk,
+                         out=big[:, 1])
+
+
 def test_decode_consistent_with_forward():
     """forward over T+1 tokens == forward over T tokens, then one decode step."""
     cyfa = _cyfa()
@@ -192,3 +206,47 @@ def test_decode_consistent_with_forward():
     torch.cuda.synchronize()
     assert rel_err(o.cpu().numpy(), full["o"][:, 40].cpu().numpy()) <= 1e-5
     assert rel_err(st["K"].cpu().numpy(), full["K"].cpu().numpy()) <= 1e-5
+
+
+def test_decode_full_size_sampled():
+    """256 streams x 16 heads, d = 128: 512-token prefix (GPU forward), then 64
+    decode steps; sampled stream-heads compared with the oracle stepped token by
+    token over all 576 tokens."""
+    cyfa = _cyfa()
+    N, H, d = DECODE.B, DECODE.H, DECODE.dk
+    prefix, steps = DECODE.extra["prefix"], DECODE.extra["steps"]
+    x = make_decode_inputs(N, H, d, prefix, steps, seed=DECODE.seed)
+    x["dtype"] = "f32"
+    t = upload(x)
+    pre = {k: (v[:, :prefix].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    st = cyfa.forward(pre["q"], pre["k"], pre["v"], pre["delta"], pre["log_alpha"], pre["beta"],
+                      pre["R"], scale=x["scale"], return_state=True)
+    del pre
+    K, V, clk = st["K"], st["V"], st["clock"]
+    outs = torch.empty((N, steps, H, d), device="cuda")
+    ws = torch.empty(cyfa.decode_workspace_size(cyfa.decode_desc(N, H, d, d)), dtype=torch.uint8,
+                     device="cuda")
+    for s_ in range(steps):
+        tok = {k: (v[:, prefix + s_].contiguous() if v is not None and k != "R" else v)
+               for k, v in t.items()}
+        o_step = cyfa.decode_step(tok["q"], tok["k"], tok["v"], tok["delta"], K, V, clk,
+                                  tok["log_alpha"], tok["beta"], t["R"], scale=x["scale"],
+                                  workspace=ws)
+        outs[:, s_] = o_step
+    torch.cuda.synchronize()
+    pairs = [0, N * H - 1, 1000, 2050, 3333]
+    ref = oracle_forward_decode(x, pairs)
+    got = outs.cpu().numpy()
+    got = np.stack([got[p // H, :, p % H] for p in pairs])
+    e_o = rel_err(got, ref["o"][:, prefix:])
+    Kref, _ = oracle_states_abs(ref, x["m"])
+    e_K = rel_err(state_view(K, pairs, H), Kref)
+    e_c = clock_err(clk.cpu().numpy().reshape(-1)[pairs], ref["lam"], x["m"])
+    print(f"decode full-size errors o {e_o:.2e} K {e_K:.2e} clock {e_c:.1e}", flush=True)
+    assert e_o <= TOL_F32 and e_K <= TOL_F32 and e_c <= 1e-9
+
+
+def oracle_forward_decode(x, pairs):
+    import oracle
+    return oracle.forward(x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"],
+                          m=x["m"], scale=x["scale"], pairs=np.array(pairs, np.int32), want_z=False)

@@ -228,6 +228,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (for scaling "
+                         "the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -237,6 +240,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 3}), flush=True)
+        return
 
     from paper_2609_36259_amd import cyfa
     from paper_2609_36259_amd.inputs import FWD_1P4B, FWD_400M, FWD_LONG, FWD_TINY
@@ -265,7 +278,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if fb["kernel"] == "mfma" else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "d_k": w.dk, "d_v": w.dv,
-                   "chunk": 64 if fb["kernel"] == "mfma" else (args.chunk or 16), "m": w.m,
+                   "chunk": args.chunk or cyfa.DEFAULT_CHUNK[fb["kernel"]], "m": w.m,
                    "io_dtype": w.dtype, "kernel": fb["kernel"], "segments": args.segments},
         "tflops": fb["flops"] / (fb["ms_per_step"] * 1e-3) / 1e12,
         "roofline": roof,

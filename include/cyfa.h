@@ -69,7 +69,7 @@ typedef enum {
     CYFA_KERNEL_VALU = 1,  /* vector-ALU chunk kernel, fp32 arithmetic, any
                               supported shape and dtype                        */
     CYFA_KERNEL_MFMA = 2   /* matrix-core (bf16 MFMA) chunk kernel: BF16,
-                              d_k = d_v = 128, chunk 64                         */
+                              d_k = d_v = 128, chunk 32 or 64                   */
 } cyfa_kernel;
 
 /*
@@ -79,8 +79,9 @@ typedef enum {
  *   d_k, d_v     head dims: 64 or 128 each (the matrix-core kernel: 128 only)
  *   m            active slots, odd, 3..127
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
- *                8 or 16 (default 16); MFMA kernel: 64.  Results do not depend
- *                on it beyond rounding (App. B: the chunk form is exact).
+ *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 32).
+ *                Results do not depend on it beyond rounding (App. B: the
+ *                chunk form is exact).
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
  *                else 1..1024 (MFMA kernel only; the VALU kernel uses 1).  The
  *                state entering a segment is obtained from a pre-pass over the

@@ -14,6 +14,7 @@ int valu_chunk_max();
 bool mfma_supported(const FwdParams &p);
 size_t mfma_workspace_bytes(const FwdParams &p, int segments);
 int mfma_auto_segments(const FwdParams &p);
+int mfma_default_chunk();
 hipError_t launch_fwd_mfma(const FwdParams &p, int segments, void *ws, hipStream_t s,
                            hipEvent_t ev_start, hipEvent_t ev_stop);
 }  // namespace cyfa
@@ -82,26 +83,26 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
 
     cyfa::FwdParams probe{};
     probe.B = d->B; probe.T = d->T; probe.H = d->H; probe.dk = d->d_k; probe.dv = d->d_v;
-    probe.m = d->m; probe.dtype = d->dtype; probe.chunk = d->chunk ? d->chunk : 64;
+    probe.m = d->m; probe.dtype = d->dtype;
+    probe.chunk = d->chunk ? d->chunk : cyfa::mfma_default_chunk();
     const bool mfma_ok = cyfa::mfma_supported(probe);
     bool use_mfma;
     if (d->kernel == CYFA_KERNEL_MFMA) {
         if (!mfma_ok)
             return fail(CYFA_ERR_UNSUPPORTED,
-                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 and chunk 64");
+                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 and chunk 32 or 64");
         use_mfma = true;
     } else if (d->kernel == CYFA_KERNEL_VALU) {
         use_mfma = false;
     } else {
-        use_mfma = mfma_ok && d->chunk == 0;
-        if (d->chunk == 64 && mfma_ok) use_mfma = true;
+        use_mfma = mfma_ok;          // chunk 0, 32 or 64 with bf16 and d = 128
     }
     plan->mfma = use_mfma;
     size_t ws = round_up(cyfa::readout_f32_bytes(d->H));
     if (use_mfma) {
-        plan->chunk = 64;
+        plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
-        const int nchunks = (d->T + 63) / 64;
+        const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
         if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
         if (plan->segments < 1) plan->segments = 1;
         ws += round_up(cyfa::mfma_workspace_bytes(probe, plan->segments));

@@ -1,4 +1,4 @@
-// Matrix-core (bf16 MFMA) chunk-wise CyFA forward for d_k = d_v = 128, C = 64.
+// Matrix-core (bf16 MFMA) chunk-wise CyFA forward for d_k = d_v = 128, chunks of 32 or 64.
 //
 // Work decomposition.  Each (b, h) sequence is cut into P segments of whole
 // chunks.  Four kernels run in order on the caller's stream:
@@ -30,6 +30,7 @@ struct MfmaArgs {
     int P;               // segments per (b, h)
     int cps;             // chunks per segment
     int nchunks;         // chunks per sequence
+    int chunk;           // chunk length (32 or 64)
     const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j
     const __bf16 *My;    // [H][128][128]  row = internal basis j, column = slot i'
     float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
@@ -43,82 +44,104 @@ struct MfmaArgs {
 
 namespace {
 
-// ---- LDS map of the fused kernel (bytes) ----------------------------------
-constexpr int R_Q = 0;                          // Q  [64][QS] bf16 -> X -> W
-constexpr int R_K = R_Q + C * QS * 2;           // K  [64][QS] bf16 }  logits Z
-constexpr int R_KT = R_K + C * QS * 2;          // K^T [128][TS] bf16 } [64][ZS] f32
-constexpr int R_VT = R_KT + D * TS * 2;         // V^T [128][TS] bf16
-constexpr int R_A = R_VT + D * TS * 2;          // A  [64][QS] bf16
-constexpr int R_AT = R_A + C * QS * 2;          // A^T [128][TS] bf16 -> O'' [64][QS]
-constexpr int R_ATD = R_AT + D * TS * 2;        // right-decayed A^T [128][TS] bf16
-constexpr int R_S = R_ATD + D * TS * 2;         // scores [64][SS] bf16
-constexpr int R_CS = R_S + C * SS * 2;          // (cos, sin) [64][64] half pairs
-constexpr int R_SC = R_CS + C * 64 * 4;         // per-token scalars
-constexpr int SMEM_BYTES = R_SC + 64 * (4 + 4 + 4 + 8) + 64;
-static_assert(C * ZS * 4 <= R_VT - R_K, "logit tile must fit in the K / K^T region");
-static_assert(C * QS * 2 <= D * TS * 2, "O'' must fit in the A^T region");
-static_assert(SMEM_BYTES <= 160 * 1024, "LDS budget");
-
-typedef _Float16 half2v __attribute__((ext_vector_type(2)));
-
-union Piece {
-    uint4 u;
-    __bf16 b[8];
+// ---- LDS maps (bytes) ---------------------------------------------------------
+// Fused kernel: every bf16 tile is row-major [CC][QS]; operands whose k index
+// runs down the rows are read with the transpose read.
+template <int CC>
+struct Lay {
+    static constexpr int RB = CC / 32;                 // 32-row blocks per tile
+    static constexpr int SSC = CC + 8;                 // row stride of the score tile
+    static constexpr int TILE = CC * QS * 2;
+    static constexpr int Q = 0;                        // Q   -> X -> W
+    static constexpr int K = Q + TILE;                 // K   -> O''
+    static constexpr int V = K + TILE;                 // V
+    static constexpr int A = V + TILE;                 // A   (temporal writes)
+    static constexpr int AD = A + TILE;                // A, rows right-decayed to the chunk end
+    static constexpr int S = AD + TILE;                // scores [CC][SSC] bf16
+    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs
+    static constexpr int Z = CS + CC * 64 * 4;         // logits [CC][ZS] f32 -> output staging
+    static constexpr int SC = Z + CC * ZS * 4;         // per-token scalars (64 entries each)
+    static constexpr int BYTES = SC + 64 * (4 + 4 + 4 + 8);
+    // state pre-pass: K, V, A_dec and the scalars
+    static constexpr int PK = 0, PV = TILE, PAD = 2 * TILE, PSC = 3 * TILE;
+    static constexpr int PBYTES = PSC + 64 * (4 + 4 + 4 + 8);
+    static_assert(BYTES <= 160 * 1024, "LDS budget");
+    static_assert(TILE <= CC * ZS * 4, "output staging fits in the logit tile");
 };
 
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+
 struct Tiles {
-    __bf16 *Qs, *Ks, *KTs, *VTs, *As, *ATs, *ATds, *Ss, *Xs, *Ws, *Os;
+    __bf16 *Qs, *Ks, *Vs, *As, *Ads, *Ss, *Xs, *Ws, *Os, *Stage;
     float *Zf;
     half2v *CS;
     float *Gs, *gam, *betas;
     double *lams;
-    double *carry;
 };
 
-__device__ __forceinline__ Tiles tiles(char *smem) {
-    Tiles t;
-    t.Qs = reinterpret_cast<__bf16 *>(smem + R_Q);
-    t.Xs = t.Qs;
-    t.Ws = t.Qs;
-    t.Ks = reinterpret_cast<__bf16 *>(smem + R_K);
-    t.Zf = reinterpret_cast<float *>(smem + R_K);
-    t.KTs = reinterpret_cast<__bf16 *>(smem + R_KT);
-    t.VTs = reinterpret_cast<__bf16 *>(smem + R_VT);
-    t.As = reinterpret_cast<__bf16 *>(smem + R_A);
-    t.ATs = reinterpret_cast<__bf16 *>(smem + R_AT);
-    t.Os = t.ATs;
-    t.ATds = reinterpret_cast<__bf16 *>(smem + R_ATD);
-    t.Ss = reinterpret_cast<__bf16 *>(smem + R_S);
-    t.CS = reinterpret_cast<half2v *>(smem + R_CS);
-    t.Gs = reinterpret_cast<float *>(smem + R_SC);
+__device__ __forceinline__ void scalars_at(Tiles &t, char *base) {
+    t.Gs = reinterpret_cast<float *>(base);
     t.gam = t.Gs + 64;
     t.betas = t.gam + 64;
     t.lams = reinterpret_cast<double *>(t.betas + 64);
-    t.carry = t.lams + 64;
+}
+
+template <int CC>
+__device__ __forceinline__ Tiles fused_tiles(char *smem) {
+    using L = Lay<CC>;
+    Tiles t{};
+    t.Qs = reinterpret_cast<__bf16 *>(smem + L::Q);
+    t.Xs = t.Qs;
+    t.Ws = t.Qs;
+    t.Ks = reinterpret_cast<__bf16 *>(smem + L::K);
+    t.Os = t.Ks;
+    t.Vs = reinterpret_cast<__bf16 *>(smem + L::V);
+    t.As = reinterpret_cast<__bf16 *>(smem + L::A);
+    t.Ads = reinterpret_cast<__bf16 *>(smem + L::AD);
+    t.Ss = reinterpret_cast<__bf16 *>(smem + L::S);
+    t.CS = reinterpret_cast<half2v *>(smem + L::CS);
+    t.Zf = reinterpret_cast<float *>(smem + L::Z);
+    t.Stage = reinterpret_cast<__bf16 *>(smem + L::Z);
+    scalars_at(t, smem + L::SC);
     return t;
 }
 
-// Global -> register prefetch of one chunk: 4 x 16-byte pieces per thread per
-// tensor (rows r = e / 16, columns 8 (e % 16)), plus one token's scalars on wave 0.
+template <int CC>
+__device__ __forceinline__ Tiles prepass_tiles(char *smem) {
+    using L = Lay<CC>;
+    Tiles t{};
+    t.Ks = reinterpret_cast<__bf16 *>(smem + L::PK);
+    t.Vs = reinterpret_cast<__bf16 *>(smem + L::PV);
+    t.Ads = reinterpret_cast<__bf16 *>(smem + L::PAD);
+    scalars_at(t, smem + L::PSC);
+    return t;
+}
+
+// Global -> register prefetch of one chunk: CC/16 x 16-byte pieces per thread per
+// tensor (rows 16 it + tid / 16, columns 8 (tid % 16)), plus one token's scalars
+// on the first CC lanes.
+template <int CC>
 struct Prefetch {
-    uint4 q[4], k[4], v[4];
+    uint4 q[CC / 16], k[CC / 16], v[CC / 16];
     float g, dl, be;
 };
 
-template <bool kWithQ>
+template <int CC, bool kWithQ>
 __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int tid,
-                                           Prefetch &pf) {
+                                           Prefetch<CC> &pf) {
     const uint4 zero = make_uint4(0, 0, 0, 0);
     const __bf16 *q = static_cast<const __bf16 *>(p.q);
     const __bf16 *k = static_cast<const __bf16 *>(p.k);
     const __bf16 *v = static_cast<const __bf16 *>(p.v);
+    const int r0 = tid >> 4, d0 = (tid & 15) * 8;
+    const size_t row_stride = (size_t)p.H * D;
+    const size_t base = (((size_t)b * p.T + t0 + r0) * p.H + h) * D + d0;
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        const int e = it * NT + tid;
-        const int r = e >> 4, d0 = (e & 15) * 8;
-        const int t = t0 + r;
+    for (int it = 0; it < CC / 16; ++it) {
+        const int t = t0 + r0 + 16 * it;
+        const size_t off = base + (size_t)(16 * it) * row_stride;
         if (t < p.T) {
-            const size_t off = (((size_t)b * p.T + t) * p.H + h) * D + d0;
             if (kWithQ) pf.q[it] = *reinterpret_cast<const uint4 *>(q + off);
             pf.k[it] = *reinterpret_cast<const uint4 *>(k + off);
             pf.v[it] = *reinterpret_cast<const uint4 *>(v + off);
@@ -130,47 +153,36 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     }
     if (tid < 64) {
         const int t = t0 + tid;
-        if (t < p.T) {
+        if (tid < CC && t < p.T) {
             const size_t si = ((size_t)b * p.T + t) * p.H + h;
             pf.dl = p.delta[si];
             pf.g = p.log_alpha ? p.log_alpha[si] : 0.f;
             pf.be = p.beta ? p.beta[si] : 1.f;
         } else {
-            pf.dl = 0.f;   // tokens past the end: no shift, no decay, no write
+            pf.dl = 0.f;   // rows past the chunk or the sequence: no shift, no decay, no write
             pf.g = 0.f;
             pf.be = 0.f;
         }
     }
 }
 
-// Registers -> LDS: Q and K row-major, K and V transposed.
-template <bool kWithQ>
-__device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefetch &pf) {
-    const int r0 = tid >> 4, d0 = (tid & 15) * 8;
-    __bf16 *qrow = s.Qs + r0 * QS + d0;
-    __bf16 *krow = s.Ks + r0 * QS + d0;
-    __bf16 *ktcol = s.KTs + d0 * TS + r0;
-    __bf16 *vtcol = s.VTs + d0 * TS + r0;
+// Registers -> LDS, row-major tiles.
+template <int CC, bool kWithQ>
+__device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefetch<CC> &pf) {
+    const int off = (tid >> 4) * QS + (tid & 15) * 8;
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {            // piece it: row r0 + 16 it
-        if (kWithQ) {
-            *reinterpret_cast<uint4 *>(qrow + 16 * it * QS) = pf.q[it];
-            *reinterpret_cast<uint4 *>(krow + 16 * it * QS) = pf.k[it];
-        }
-        Piece pk, pv;
-        pk.u = pf.k[it];
-        pv.u = pf.v[it];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            ktcol[j * TS + 16 * it] = pk.b[j];
-            vtcol[j * TS + 16 * it] = pv.b[j];
-        }
+    for (int it = 0; it < CC / 16; ++it) {
+        if (kWithQ) *reinterpret_cast<uint4 *>(s.Qs + off + 16 * it * QS) = pf.q[it];
+        *reinterpret_cast<uint4 *>(s.Ks + off + 16 * it * QS) = pf.k[it];
+        *reinterpret_cast<uint4 *>(s.Vs + off + 16 * it * QS) = pf.v[it];
     }
 }
 
 // Wave 0: chunk-local inclusive prefix sums of log alpha (float) and of the
 // clock increments (double, continuing the carried clock), reduced mod m.
-__device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch &pf,
+// Lanes past the chunk hold zeros, so entry 63 equals the chunk total.
+template <int CC>
+__device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC> &pf,
                                             double &carry, double &gsum) {
     const float G = wave_incl_scan(pf.g, lane);
     const double lam = carry + wave_incl_scan((double)pf.dl, lane);
@@ -185,12 +197,17 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
 
 // Temporal write matrix for the chunk (Eq. app-temporal-writes):
 // A_r = beta_r U(-lambda_r) b, i.e. beta_r [sqrt(2/m) cos th_j, -sqrt(2/m) sin th_j]
-// on pair j and beta_r / sqrt(m) on DC, th_j = 2 pi j lambda_r / m.
-// Thread (r = tid / 4, quarter q = tid % 4) handles frequencies 16q+1 .. 16q+16;
-// the phases advance by angle addition from an accurately reduced start.
-template <bool kFull>
+// on pair j and beta_r / sqrt(m) on DC, th_j = 2 pi j lambda_r / m.  The copy
+// A_dec has row r scaled by gamma^C / gamma^r (right rescaling, Eq. app-chunk-rescale).
+// Thread (r = tid / TPR, q = tid % TPR) fills internal columns NCOL q .. NCOL q + NCOL-1
+// of row r; the last quarter also holds DC (column 126) and padding (127).  The
+// phases advance by angle addition from an accurately reduced start.
+template <int CC, bool kFull>
 __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
-    const int r = tid >> 2, q = tid & 3;
+    constexpr int TPR = NT / CC;          // threads per row
+    constexpr int NCOL = 128 / TPR;       // columns per thread
+    constexpr int NP = NCOL / 2;          // pairs per thread
+    const int r = tid / TPR, q = tid % TPR;
     const int J = (m - 1) >> 1;
     const float dc = 1.0f / sqrtf((float)m);
     const float ac = sqrtf(2.0f / (float)m);
@@ -200,58 +217,56 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
     float s1, c1, sn, cs;
     sincos_rev((float)u, &s1, &c1);
     {
-        const int j0 = 16 * q + 1;
-        double rev = (double)j0 * u;
+        double rev = (double)(NP * q + 1) * u;
         rev -= floor(rev);
         sincos_rev((float)rev, &sn, &cs);
     }
-    __bf16 *As_t = s.As + r * QS + 32 * q;
-    __bf16 *ATs_t = s.ATs + 32 * q * TS + r;
-    __bf16 *ATds_t = s.ATds + 32 * q * TS + r;
-    half2v *CS_t = s.CS + r * 64 + 16 * q;
+    float av[NCOL];
+    half8v csv[NP / 4];
 #pragma unroll
-    for (int jj = 0; jj < 16; ++jj) {
-        const int j = 16 * q + 1 + jj;
-        if (j <= 63) {
-            const float cv = j <= J ? cs : 0.f;
-            const float sv = j <= J ? sn : 0.f;
-            const float a_c = be * ac * cv, a_s = -be * ac * sv;
-            // internal columns 32 q + 2 jj (cos) and 32 q + 2 jj + 1 (sin)
-            if (kFull) {
-                CS_t[jj] = half2v{(_Float16)cv, (_Float16)sv};
-                bf16x2 pr;
-                pr[0] = (__bf16)a_c;
-                pr[1] = (__bf16)a_s;
-                *reinterpret_cast<bf16x2 *>(As_t + 2 * jj) = pr;
-                ATs_t[(2 * jj) * TS] = (__bf16)a_c;
-                ATs_t[(2 * jj + 1) * TS] = (__bf16)a_s;
-            }
-            ATds_t[(2 * jj) * TS] = (__bf16)(a_c * wdec);
-            ATds_t[(2 * jj + 1) * TS] = (__bf16)(a_s * wdec);
-        }
+    for (int jj = 0; jj < NP; ++jj) {
+        const int j = NP * q + 1 + jj;
+        const bool live = j <= J && j <= 63;
+        const float cv = live ? cs : 0.f;
+        const float sv = live ? sn : 0.f;
+        av[2 * jj] = be * ac * cv;
+        av[2 * jj + 1] = -be * ac * sv;
+        csv[jj >> 2][2 * (jj & 3)] = (_Float16)cv;
+        csv[jj >> 2][2 * (jj & 3) + 1] = (_Float16)sv;
         const float nc = cs * c1 - sn * s1;
         const float ns = sn * c1 + cs * s1;
         cs = nc;
         sn = ns;
     }
-    if (q == 3) {
-        const float a0 = be * dc;
-        if (kFull) {
-            bf16x2 pr;
-            pr[0] = (__bf16)a0;
-            pr[1] = (__bf16)0.f;
-            *reinterpret_cast<bf16x2 *>(s.As + r * QS + kDC) = pr;
-            s.ATs[kDC * TS + r] = (__bf16)a0;
-            s.ATs[(kDC + 1) * TS + r] = (__bf16)0.f;
+    if (q == TPR - 1) {    // internal columns 126 (DC) and 127 (padding)
+        av[NCOL - 2] = be * dc;
+        av[NCOL - 1] = 0.f;
+    }
+    __bf16 *arow = s.As + r * QS + NCOL * q;
+    __bf16 *adrow = s.Ads + r * QS + NCOL * q;
+#pragma unroll
+    for (int k8 = 0; k8 < NCOL / 8; ++k8) {
+        bf16x8 a8, ad8;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            a8[k] = (__bf16)av[8 * k8 + k];
+            ad8[k] = (__bf16)(av[8 * k8 + k] * wdec);
         }
-        s.ATds[kDC * TS + r] = (__bf16)(a0 * wdec);
-        s.ATds[(kDC + 1) * TS + r] = (__bf16)0.f;
+        if (kFull) *reinterpret_cast<bf16x8 *>(arow + 8 * k8) = a8;
+        *reinterpret_cast<bf16x8 *>(adrow + 8 * k8) = ad8;
+    }
+    if (kFull) {
+        half8v *csrow = reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q);
+#pragma unroll
+        for (int k4 = 0; k4 < NP / 4; ++k4) csrow[k4] = csv[k4];
     }
 }
 
 // Carried-state updates of one chunk (App. B):
-//   Kbar^T <- gamma^C Kbar^T + K^T (right-decayed A),  Vbar <- gamma^C Vbar + (right-decayed A)^T V
-__device__ __forceinline__ void update_states(const Tiles &s, int w, int l32, int hl,
+//   Kbar^T <- gamma^C Kbar^T + K^T A_dec,   Vbar <- gamma^C Vbar + A_dec^T V
+// Operands: K^T, A_dec and V come from row-major tiles through transpose reads.
+template <int CC>
+__device__ __forceinline__ void update_states(const Tiles &s, int w, int lane,
                                               f32x16 (&kacc)[4], f32x16 (&vacc)[4]) {
     const float gC = s.gam[63];
 #pragma unroll
@@ -261,28 +276,32 @@ __device__ __forceinline__ void update_states(const Tiles &s, int w, int l32, in
             kacc[x][v] *= gC;
             vacc[x][v] *= gC;
         }
+    const __bf16 *Kt = tr_base(s.Ks, QS, lane);
+    const __bf16 *Vt = tr_base(s.Vs, QS, lane) + 32 * w;
+    const __bf16 *Adt = tr_base(s.Ads, QS, lane);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 at_w = lds8(s.ATds + (32 * w + l32) * TS + 16 * ks + 8 * hl);
-        const bf16x8 vt_w = lds8(s.VTs + (32 * w + l32) * TS + 16 * ks + 8 * hl);
+    for (int ks = 0; ks < CC / 16; ++ks) {
+        const bf16x8 ad_w = lds8_tr(Adt + 16 * ks * QS + 32 * w, QS);
+        const bf16x8 v_w = lds8_tr(Vt + 16 * ks * QS, QS);
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
-            const bf16x8 kt = lds8(s.KTs + (32 * x + l32) * TS + 16 * ks + 8 * hl);
-            kacc[x] = mma(kt, at_w, kacc[x]);
-            const bf16x8 atd = lds8(s.ATds + (32 * x + l32) * TS + 16 * ks + 8 * hl);
-            vacc[x] = mma(atd, vt_w, vacc[x]);
+            kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
+            vacc[x] = mma(lds8_tr(Adt + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
         }
     }
 }
 
-// row offset (within a 64-row tile, excluding the lane's 4h) of accumulator register v of block blk
+// row offset (within a tile, excluding the lane's 4h) of accumulator register v of block blk
 __device__ __forceinline__ constexpr int acc_off(int blk, int v) {
     return 32 * blk + 8 * (v >> 2) + (v & 3);
 }
 
-// Causal score tile (S (.) Gamma) for block (rb, sb) -> Ss (bf16).
+// Causal score tile (S (.) Gamma) for 32 x 32 block (rb, sb) -> Ss (bf16).
+// A rows come from Arow (row-major, k along the row), B columns from Brow's rows.
+template <int CC>
 __device__ __forceinline__ void score_tile(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
                                            int rb, int sb, int l32, int hl) {
+    constexpr int SSC = Lay<CC>::SSC;
     f32x16 acc = zero_acc();
     const __bf16 *ap = Arow + (32 * rb + l32) * QS + 8 * hl;
     const __bf16 *bp = Brow + (32 * sb + l32) * QS + 8 * hl;
@@ -291,13 +310,24 @@ __device__ __forceinline__ void score_tile(const Tiles &s, const __bf16 *Arow, c
     const int scol = 32 * sb + l32;
     const float Gs_col = s.Gs[scol];
     const float *Gr = s.Gs + 32 * rb + 4 * hl;
-    __bf16 *Sr = s.Ss + (32 * rb + 4 * hl) * SS + scol;
+    __bf16 *Sr = s.Ss + (32 * rb + 4 * hl) * SSC + scol;
     const int rbase = 32 * rb + 4 * hl;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const int ro = acc_off(0, v);
         const float val = scol <= rbase + ro ? acc[v] * __expf(Gr[ro] - Gs_col) : 0.f;
-        Sr[ro * SS] = (__bf16)val;
+        Sr[ro * SSC] = (__bf16)val;
+    }
+}
+
+// the 32 x 32 score blocks of a causal CC x CC tile: (0,0) [, (1,0), (1,1)]
+template <int CC>
+__device__ __forceinline__ void score_tiles(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
+                                            int w, int l32, int hl) {
+    if (CC == 64) {
+        if (w < 3) score_tile<CC>(s, Arow, Brow, w == 0 ? 0 : 1, w == 2 ? 1 : 0, l32, hl);
+    } else {
+        if (w == 0) score_tile<CC>(s, Arow, Brow, 0, 0, l32, hl);
     }
 }
 
@@ -324,13 +354,14 @@ __device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32
 }
 
 // ---- 1. per-segment state contributions -------------------------------------
-__global__ __launch_bounds__(NT, 1) void segment_state_kernel(MfmaArgs a) {
-    __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
-    const Tiles s = tiles(smem);
+template <int CC>
+__global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
+    __shared__ __attribute__((aligned(16))) char smem[Lay<CC>::PBYTES];
+    const Tiles s = prepass_tiles<CC>(smem);
     const int Pm1 = a.P - 1;
     const int bh = blockIdx.x / Pm1, p = blockIdx.x % Pm1;
     const int b = bh / a.p.H, h = bh % a.p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int c_begin = p * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
     f32x16 kacc[4], vacc[4];
 #pragma unroll
@@ -339,16 +370,16 @@ __global__ __launch_bounds__(NT, 1) void segment_state_kernel(MfmaArgs a) {
         vacc[x] = f32x16{};
     }
     double carry = 0.0, gsum = 0.0;
-    Prefetch pf;
-    load_chunk<false>(a.p, b, h, c_begin * C, tid, pf);
+    Prefetch<CC> pf;
+    load_chunk<CC, false>(a.p, b, h, c_begin * CC, tid, pf);
     for (int c = c_begin; c < c_end; ++c) {
-        store_chunk<false>(s, tid, pf);
-        if (w == 0) chunk_scans(s, lane, a.p.m, pf, carry, gsum);
+        store_chunk<CC, false>(s, tid, pf);
+        if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum);
         __syncthreads();
-        if (c + 1 < c_end) load_chunk<false>(a.p, b, h, (c + 1) * C, tid, pf);
-        build_writes<false>(s, tid, a.p.m);
+        if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
+        build_writes<CC, false>(s, tid, a.p.m);
         __syncthreads();
-        update_states(s, w, l32, hl, kacc, vacc);
+        update_states<CC>(s, w, lane, kacc, vacc);
         __syncthreads();
     }
     const size_t slot = (size_t)bh * a.P + p;
@@ -360,40 +391,72 @@ __global__ __launch_bounds__(NT, 1) void segment_state_kernel(MfmaArgs a) {
 }
 
 // ---- 2. states entering each segment ----------------------------------------
-// grid (B*H, 32): each thread owns one rotation pair (internal i = 2 ip, 2 ip + 1)
-// of one column c of the key or the value state, and walks the segments.
+// Element pairs that a rotation U(tau) mixes sit next to each other in the
+// accumulator-dump layout: key-state partners are adjacent lanes (offsets e,
+// e + 1), value-state partners are adjacent registers (offsets e, e + 64).
+// grid (B*H, 32): thread = one pair; consecutive threads touch consecutive words.
+struct PairRef {
+    int o0, o1;        // dump offsets of the (cos, sin) pair
+    int i0;            // internal index of the first element (even)
+    int col;           // state column (d for the key state, d for the value state)
+    bool value;
+};
+
+__device__ __forceinline__ PairRef pair_ref(int gidx) {
+    PairRef r;
+    if (gidx < 8192) {                                   // key state: lanes (2k, 2k+1)
+        const int e = 2 * gidx;
+        const int lane = e & 63, v = (e >> 6) & 15, blk = (e >> 10) & 3, w = e >> 12;
+        r.o0 = e;
+        r.o1 = e + 1;
+        r.i0 = 32 * w + (lane & 31);
+        const int h = lane >> 5;
+        r.col = 32 * blk + 8 * (v >> 2) + 4 * h + (v & 3);
+        r.value = false;
+    } else {                                             // value state: registers (2k, 2k+1)
+        const int g = gidx - 8192;
+        const int lane = g & 63, vp = (g >> 6) & 7, blk = (g >> 9) & 3, w = g >> 11;
+        const int v = 2 * vp;
+        const int e = ((w * 4 + blk) * 16 + v) * 64 + lane;
+        r.o0 = 128 * 128 + e;
+        r.o1 = 128 * 128 + e + 64;
+        const int h = lane >> 5;
+        r.i0 = 32 * blk + 8 * (v >> 2) + 4 * h + (v & 3);
+        r.col = 32 * w + (lane & 31);
+        r.value = true;
+    }
+    return r;
+}
+
+// (x0, x1) <- U(tau) (x0, x1) for the pair at internal indices (2j-2, 2j-1)
+__device__ __forceinline__ void rotate_pair(double tau, int j, int m, float &x0, float &x1) {
+    double rev = (double)j * reduce_clock(tau, m) / (double)m;
+    rev -= floor(rev);
+    float sn, cs;
+    sincos_rev((float)rev, &sn, &cs);
+    const float y0 = cs * x0 - sn * x1;
+    const float y1 = sn * x0 + cs * x1;
+    x0 = y0;
+    x1 = y1;
+}
+
 __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
     const int bh = blockIdx.x;
-    const int gidx = blockIdx.y * NT + threadIdx.x;          // 0 .. 2*64*128-1
-    const int kind = gidx >> 13;                             // 0: key, 1: value
-    const int ip = (gidx >> 7) & 63, col = gidx & 127;
-    const int i0 = 2 * ip, i1 = 2 * ip + 1;
+    const int gidx = blockIdx.y * NT + threadIdx.x;      // 0 .. 16383
     const int m = a.p.m;
-    const int j = ip + 1;                                    // frequency of the pair
-    const bool rotates = ip < 63 && j <= (m - 1) / 2;
-    const int o0 = kind ? dump_index_V(i0, col) : dump_index_K(i0, col);
-    const int o1 = kind ? dump_index_V(i1, col) : dump_index_K(i1, col);
-    const float *init = kind ? a.p.V0 : a.p.K0;
+    const PairRef pr = pair_ref(gidx);
+    const int j = (pr.i0 >> 1) + 1;                      // frequency of the pair
+    const bool rotates = pr.i0 < kDC && j <= (m - 1) / 2;
+    const float *init = pr.value ? a.p.V0 : a.p.K0;
     const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
-    double x0 = 0.0, x1 = 0.0;
+    float x0 = 0.f, x1 = 0.f;
     if (init) {
-        const int p0 = internal_to_paper(i0, m), p1 = internal_to_paper(i1, m);
-        const size_t base = (size_t)bh * 128 * 128;
-        x0 = p0 >= 0 ? (double)init[base + (size_t)p0 * 128 + col] : 0.0;
-        x1 = p1 >= 0 ? (double)init[base + (size_t)p1 * 128 + col] : 0.0;
+        const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
+        const size_t base = (size_t)bh * 128 * 128 + pr.col;
+        x0 = p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
+        x1 = p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
     }
-    auto rot = [&](double tau) {                             // (x0, x1) <- U(tau) (x0, x1)
-        if (!rotates) return;
-        double rev = (double)j * reduce_clock(tau, m) / (double)m;
-        rev -= floor(rev);
-        double sn, cs;
-        sincospi(2.0 * rev, &sn, &cs);
-        const double y0 = cs * x0 - sn * x1;
-        const double y1 = sn * x0 + cs * x1;
-        x0 = y0;
-        x1 = y1;
-    };
-    rot(c0);                      // initial state in the frame whose origin is clock0
+    if (rotates) rotate_pair(c0, j, m, x0, x1);   // initial state in the frame with origin clock0
     double origin = reduce_clock(c0, m);
     for (int q = 0; q < a.P; ++q) {
         const size_t slot = (size_t)bh * a.P + q;
@@ -401,25 +464,29 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
         if (gidx == 0) a.seg_origin[slot] = origin;
         float d0 = 0.f, d1 = 0.f;
         if (q < a.P - 1) {
-            d0 = st[o0];
-            d1 = st[o1];
+            d0 = st[pr.o0];
+            d1 = st[pr.o1];
         }
-        st[o0] = (float)x0;
-        st[o1] = (float)x1;
+        st[pr.o0] = x0;
+        st[pr.o1] = x1;
         if (q < a.P - 1) {
-            const double gdec = exp(a.seg_gsum[slot]);
-            x0 = gdec * x0 + (double)d0;
-            x1 = gdec * x1 + (double)d1;
-            rot(a.seg_span[slot]);
+            const float gdec = (float)exp(a.seg_gsum[slot]);
+            x0 = fmaf(gdec, x0, d0);
+            x1 = fmaf(gdec, x1, d1);
+            if (rotates) rotate_pair(a.seg_span[slot], j, m, x0, x1);
             origin = reduce_clock(origin + a.seg_span[slot], m);
         }
     }
 }
 
 // ---- 3. fused chunk forward ----------------------------------------------------
-__global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
-    __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
-    const Tiles s = tiles(smem);
+template <int CC>
+__global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(MfmaArgs a) {
+    using L = Lay<CC>;
+    constexpr int RB = L::RB;
+    constexpr int SSC = L::SSC;
+    __shared__ __attribute__((aligned(16))) char smem[L::BYTES];
+    const Tiles s = fused_tiles<CC>(smem);
     const FwdParams &p = a.p;
     const int bh = blockIdx.x / a.P, seg = blockIdx.x % a.P;
     const int b = bh / p.H, h = bh % p.H;
@@ -434,18 +501,18 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
     const __bf16 *Myr = a.My + ((size_t)h * 128 + icol) * 128 + 8 * hl;
     const float *gam_l = s.gam + h4;                                      // accumulator rows
     const half2v *CS_l = s.CS + h4 * 64 + (icol >> 1);
-    __bf16 *X_l = s.Xs + h4 * QS + icol;                                  // also W's tile
-    __bf16 *O2_l = s.Os + h4 * QS + icol;                                 // O'' and output staging
+    __bf16 *X_l = s.Xs + h4 * QS + icol;                                  // X (then W) tile
+    __bf16 *O2_l = s.Os + h4 * QS + icol;                                 // O'' tile
+    __bf16 *St_l = s.Stage + h4 * QS + icol;                              // output staging
     float *Z_l = s.Zf + h4 * ZS + icol;
     const __bf16 *Qperm = s.Qs + l32 * QS + h4;                           // permuted-k A operands
     const __bf16 *Operm = s.Os + l32 * QS + h4;
     const __bf16 *Xa = s.Xs + l32 * QS + 8 * hl;                          // natural-k A operands
-    const __bf16 *Sa = s.Ss + l32 * SS + 8 * hl;
-    const __bf16 *ATb = s.ATs + icol * TS + 8 * hl;                       // natural-k B operands
-    const __bf16 *ATdb = s.ATds + icol * TS + 8 * hl;
-    const __bf16 *VTb = s.VTs + icol * TS + 8 * hl;
-    const __bf16 *KTa = s.KTs + l32 * TS + 8 * hl;
-    const __bf16 *ATda = s.ATds + l32 * TS + 8 * hl;
+    const __bf16 *Sa = s.Ss + l32 * SSC + 8 * hl;
+    const __bf16 *At = tr_base(s.As, QS, lane) + 32 * w;                  // transposed B operands
+    const __bf16 *Vt = tr_base(s.Vs, QS, lane) + 32 * w;
+    const __bf16 *Adt = tr_base(s.Ads, QS, lane);
+    const __bf16 *Kt = tr_base(s.Ks, QS, lane);
 
     f32x16 kacc[4], vacc[4];
     float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
@@ -459,59 +526,67 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
         }
     }
     double carry = 0.0, gsum = 0.0;
-    Prefetch pf;
-    load_chunk<true>(p, b, h, c_begin * C, tid, pf);
+    // With one workgroup per compute unit (64-token chunks) the next chunk is
+    // prefetched into registers during the current one; with two workgroups
+    // per unit (32-token chunks) the other workgroup covers the load latency
+    // and the registers are needed elsewhere.
+    constexpr bool kPrefetch = CC == 64;
+    Prefetch<CC> pf;
+    if (kPrefetch) load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
 
     for (int c = c_begin; c < c_end; ++c) {
-        const int t0 = c * C;
-        const int n = min(C, p.T - t0);
+        const int t0 = c * CC;
+        const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes
-        store_chunk<true>(s, tid, pf);
-        if (w == 0) chunk_scans(s, lane, m, pf, carry, gsum);
+        if (!kPrefetch) load_chunk<CC, true>(p, b, h, t0, tid, pf);
+        store_chunk<CC, true>(s, tid, pf);
+        if (w == 0) chunk_scans<CC>(s, lane, m, pf, carry, gsum);
         __syncthreads();
-        if (c + 1 < c_end) load_chunk<true>(p, b, h, (c + 1) * C, tid, pf);
-        build_writes<true>(s, tid, m);
+        if (kPrefetch && c + 1 < c_end) load_chunk<CC, true>(p, b, h, (c + 1) * CC, tid, pf);
+        build_writes<CC, true>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
-        if (w < 3) score_tile(s, s.Qs, s.Ks, w == 0 ? 0 : 1, w == 2 ? 1 : 0, l32, hl);
-        f32x16 oacc[2] = {zero_acc(), zero_acc()};
+        score_tiles<CC>(s, s.Qs, s.Ks, w, l32, hl);
+        f32x16 oacc[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) oacc[rb] = zero_acc();
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
             const bf16x8 kb = acc_to_operand(kacc[ks >> 1], ks & 1);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
                 oacc[rb] = mma(lds8_perm(Qperm + 32 * rb * QS, 16 * ks, 0), kb, oacc[rb]);
         }
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) oacc[rb][v] *= gam_l[acc_off(rb, v)];
         __syncthreads();
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                if (rb == 0 && ks >= 2) continue;    // rows 0..31 see only columns 0..31
-                oacc[rb] = mma(lds8(Sa + 32 * rb * SS + 16 * ks), lds8(ATb + 16 * ks), oacc[rb]);
-            }
+            for (int ks = 0; ks < 2 * (rb + 1); ++ks)   // causal: row block rb sees columns < 32 (rb + 1)
+                oacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(At + 16 * ks * QS, QS),
+                               oacc[rb]);
         {
-            // key state: Kbar^T <- gamma^C Kbar^T + K^T (right-decayed A)
+            // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec
             const float gC = s.gam[63];
 #pragma unroll
             for (int x = 0; x < 4; ++x)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) kacc[x][v] *= gC;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 at_w = lds8(ATdb + 16 * ks);
+            for (int ks = 0; ks < CC / 16; ++ks) {
+                const bf16x8 ad_w = lds8_tr(Adt + 16 * ks * QS + 32 * w, QS);
 #pragma unroll
-                for (int x = 0; x < 4; ++x) kacc[x] = mma(lds8(KTa + 32 * x * TS + 16 * ks), at_w, kacc[x]);
+                for (int x = 0; x < 4; ++x)
+                    kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
             }
         }
         // -- middle step 1: X_r = scale U(lambda_r) O'_r -> X tile (reuses Q's)
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int ro = acc_off(rb, v);
@@ -528,30 +603,34 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
                 X_l[ro * QS] = (__bf16)(p.scale * x);
             }
         __syncthreads();
-        // -- middle step 2: slot logits Z = X M^T -> Z tile (reuses K / K^T)
+        // -- middle step 2: slot logits Z = X M^T -> logit tile
         {
             bf16x8 mz[8];
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
-            f32x16 zacc[2] = {zero_acc(), zero_acc()};
+            f32x16 zacc[RB];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) zacc[rb] = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-                for (int rb = 0; rb < 2; ++rb)
+                for (int rb = 0; rb < RB; ++rb)
                     zacc[rb] = mma(lds8(Xa + 32 * rb * QS + 16 * ks), mz[ks], zacc[rb]);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) Z_l[acc_off(rb, v) * ZS] = zacc[rb][v];
         }
         __syncthreads();
         // -- middle step 3: softmax over the m active slots -> W tile (reuses X's)
         {
-            const int r = tid >> 2, q = tid & 3;
-            const float *zr = s.Zf + r * ZS + 32 * q;
-            float zv[32];
+            constexpr int TPR = NT / CC;            // threads per row
+            constexpr int NS = 128 / TPR;           // slots per thread
+            const int r = tid / TPR, q = tid % TPR;
+            const float *zr = s.Zf + r * ZS + NS * q;
+            float zv[NS];
 #pragma unroll
-            for (int k4 = 0; k4 < 8; ++k4) {
+            for (int k4 = 0; k4 < NS / 4; ++k4) {
                 const float4 z4 = *reinterpret_cast<const float4 *>(zr + 4 * k4);
                 zv[4 * k4] = z4.x;
                 zv[4 * k4 + 1] = z4.y;
@@ -559,31 +638,33 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
                 zv[4 * k4 + 3] = z4.w;
             }
             if (p.logits && r < n) {
-                float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m + 32 * q;
+                float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m + NS * q;
 #pragma unroll
-                for (int k = 0; k < 32; ++k)
-                    if (32 * q + k < m) lg[k] = zv[k];
+                for (int k = 0; k < NS; ++k)
+                    if (NS * q + k < m) lg[k] = zv[k];
             }
             float mx = -INFINITY;
 #pragma unroll
-            for (int k = 0; k < 32; ++k) {
-                if (32 * q + k >= m) zv[k] = -INFINITY;
+            for (int k = 0; k < NS; ++k) {
+                if (NS * q + k >= m) zv[k] = -INFINITY;
                 mx = fmaxf(mx, zv[k]);
             }
             mx = fmaxf(mx, swap_pair(mx));
             mx = fmaxf(mx, swap_halves4(mx));
+            if (TPR == 8) mx = fmaxf(mx, swap_quads8(mx));
             float sum = 0.f;
 #pragma unroll
-            for (int k = 0; k < 32; ++k) {
+            for (int k = 0; k < NS; ++k) {
                 zv[k] = __expf(zv[k] - mx);
                 sum += zv[k];
             }
             sum += swap_pair(sum);
             sum += swap_halves4(sum);
+            if (TPR == 8) sum += swap_quads8(sum);
             const float inv = 1.f / sum;
-            __bf16 *wr = s.Ws + r * QS + 32 * q;
+            __bf16 *wr = s.Ws + r * QS + NS * q;
 #pragma unroll
-            for (int k8 = 0; k8 < 4; ++k8) {
+            for (int k8 = 0; k8 < NS / 8; ++k8) {
                 bf16x8 wv;
 #pragma unroll
                 for (int k = 0; k < 8; ++k) wv[k] = (__bf16)(zv[8 * k8 + k] * inv);
@@ -591,19 +672,21 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
             }
         }
         __syncthreads();
-        // -- middle step 4: O''_r = U(-lambda_r) M^T W_r -> O'' tile (reuses A^T's)
+        // -- middle step 4: O''_r = U(-lambda_r) M^T W_r -> O'' tile (reuses K's)
         {
             bf16x8 my[8];
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
-            f32x16 yacc[2] = {zero_acc(), zero_acc()};
+            f32x16 yacc[RB];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) yacc[rb] = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-                for (int rb = 0; rb < 2; ++rb)
+                for (int rb = 0; rb < RB; ++rb)
                     yacc[rb] = mma(lds8(Xa + 32 * rb * QS + 16 * ks), my[ks], yacc[rb]);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int ro = acc_off(rb, v);
@@ -622,55 +705,57 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
         }
         __syncthreads();
         // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V
-        if (w < 3) score_tile(s, s.Os, s.As, w == 0 ? 0 : 1, w == 2 ? 1 : 0, l32, hl);
-        f32x16 pacc[2] = {zero_acc(), zero_acc()};
+        score_tiles<CC>(s, s.Os, s.As, w, l32, hl);
+        f32x16 pacc[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) pacc[rb] = zero_acc();
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
             const bf16x8 vb = acc_to_operand(vacc[ks >> 1], ks & 1);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
                 pacc[rb] = mma(lds8_perm(Operm + 32 * rb * QS, 16 * ks, 0), vb, pacc[rb]);
         }
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) pacc[rb][v] *= gam_l[acc_off(rb, v)];
         __syncthreads();
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                if (rb == 0 && ks >= 2) continue;
-                pacc[rb] = mma(lds8(Sa + 32 * rb * SS + 16 * ks), lds8(VTb + 16 * ks), pacc[rb]);
-            }
-        // output tile -> staging (O'' is dead) for 16-byte global stores
+            for (int ks = 0; ks < 2 * (rb + 1); ++ks)
+                pacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(Vt + 16 * ks * QS, QS),
+                               pacc[rb]);
+        // output tile -> staging (the logit tile is dead) for 16-byte global stores
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) O2_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
+            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
         {
-            // value state: Vbar <- gamma^C Vbar + (right-decayed A)^T V
+            // value state: Vbar <- gamma^C Vbar + A_dec^T V
             const float gC = s.gam[63];
 #pragma unroll
             for (int x = 0; x < 4; ++x)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) vacc[x][v] *= gC;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 vt_w = lds8(VTb + 16 * ks);
+            for (int ks = 0; ks < CC / 16; ++ks) {
+                const bf16x8 v_w = lds8_tr(Vt + 16 * ks * QS, QS);
 #pragma unroll
-                for (int x = 0; x < 4; ++x) vacc[x] = mma(lds8(ATda + 32 * x * TS + 16 * ks), vt_w, vacc[x]);
+                for (int x = 0; x < 4; ++x)
+                    vacc[x] = mma(lds8_tr(Adt + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
             }
         }
         __syncthreads();
         {
             const int r0 = tid >> 4, d0 = (tid & 15) * 8;
 #pragma unroll
-            for (int it = 0; it < 4; ++it) {
+            for (int it = 0; it < CC / 16; ++it) {
                 const int r = r0 + 16 * it;
                 if (r < n)
                     *reinterpret_cast<uint4 *>(o + (((size_t)b * p.T + t0 + r) * p.H + h) * D + d0) =
-                        *reinterpret_cast<const uint4 *>(s.Os + r * QS + d0);
+                        *reinterpret_cast<const uint4 *>(s.Stage + r * QS + d0);
             }
         }
     }
@@ -681,39 +766,28 @@ __global__ __launch_bounds__(NT, 1) void chunk_forward_kernel(MfmaArgs a) {
 }
 
 // ---- 4. final state in the ABI layout ------------------------------------------
-// grid (B*H, 32): thread = one rotation pair of one column of K or V.
+// grid (B*H, 32): thread = one rotation pair of the key or value state.
 __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     const int bh = blockIdx.x;
     const int gidx = blockIdx.y * NT + threadIdx.x;
-    const int kind = gidx >> 13;
-    const int ip = (gidx >> 7) & 63, col = gidx & 127;
-    const int i0 = 2 * ip, i1 = 2 * ip + 1;
     const int m = a.p.m;
-    const int j = ip + 1;
+    const PairRef pr = pair_ref(gidx);
+    const int j = (pr.i0 >> 1) + 1;
     const size_t slot = (size_t)bh * a.P + (a.P - 1);
     const float *st = a.seg_state + slot * kStateFloats;
     const double origin = a.seg_origin[slot];
-    double x0 = st[kind ? dump_index_V(i0, col) : dump_index_K(i0, col)];
-    double x1 = st[kind ? dump_index_V(i1, col) : dump_index_K(i1, col)];
-    if (ip < 63 && j <= (m - 1) / 2) {
-        // local frame (origin at the last segment's start) -> absolute clock: U(-origin)
-        double rev = (double)j * origin / (double)m;
-        rev -= floor(rev);
-        double sn, cs;
-        sincospi(2.0 * rev, &sn, &cs);
-        const double y0 = cs * x0 + sn * x1;
-        const double y1 = -sn * x0 + cs * x1;
-        x0 = y0;
-        x1 = y1;
-    }
-    float *out = kind ? a.p.V_out : a.p.K_out;
+    float x0 = st[pr.o0], x1 = st[pr.o1];
+    // local frame (origin at the last segment's start) -> absolute clock: U(-origin)
+    if (pr.i0 < kDC && j <= (m - 1) / 2) rotate_pair(-origin, j, m, x0, x1);
+    float *out = pr.value ? a.p.V_out : a.p.K_out;
     if (out) {
-        const size_t base = (size_t)bh * 128 * 128;
-        const int p0 = internal_to_paper(i0, m), p1 = internal_to_paper(i1, m);
-        if (p0 >= 0) out[base + (size_t)p0 * 128 + col] = (float)x0;
-        if (p1 >= 0) out[base + (size_t)p1 * 128 + col] = (float)x1;
-        // padding rows m..127 of the ABI layout are written as zero
-        for (int row = m + ip; row < 128; row += 64) out[base + (size_t)row * 128 + col] = 0.f;
+        const size_t base = (size_t)bh * 128 * 128 + pr.col;
+        const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
+        if (p0 >= 0) out[base + (size_t)p0 * 128] = x0;
+        if (p1 >= 0) out[base + (size_t)p1 * 128] = x1;
+        // padding rows m..127 of the ABI layout are written as zero (one writer per row)
+        const int ip = pr.i0 >> 1;
+        for (int row = m + ip; row < 128; row += 64) out[base + (size_t)row * 128] = 0.f;
     }
     if (gidx == 0 && a.p.clock_out) {
         // with no tokens the final state is the initial one and the local clock is 0
@@ -743,9 +817,13 @@ __global__ __launch_bounds__(NT) void readout_pack_kernel(int m, const float *__
 }  // namespace
 
 // ---- host side --------------------------------------------------------------
+constexpr int kMfmaDefaultChunk = 32;
+
 bool mfma_supported(const FwdParams &p) {
-    return p.dtype == 1 && p.dk == 128 && p.dv == 128 && p.chunk == 64;
+    return p.dtype == 1 && p.dk == 128 && p.dv == 128 && (p.chunk == 32 || p.chunk == 64);
 }
+
+int mfma_default_chunk() { return kMfmaDefaultChunk; }
 
 namespace {
 struct WsLayout {
@@ -773,6 +851,27 @@ WsLayout ws_layout(const FwdParams &p, int P) {
     L.total = off;
     return L;
 }
+
+template <int CC>
+hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_start,
+                     hipEvent_t ev_stop) {
+    hipError_t e;
+    if (a.P > 1 && a.nchunks > 0) {
+        hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (a.has_init) {
+        hipLaunchKernelGGL(segment_scan_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
+    if (a.nchunks > 0) {
+        hipLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
+    return hipSuccess;
+}
 }  // namespace
 
 size_t mfma_workspace_bytes(const FwdParams &p, int segments) {
@@ -781,9 +880,12 @@ size_t mfma_workspace_bytes(const FwdParams &p, int segments) {
 }
 
 int mfma_auto_segments(const FwdParams &p) {
-    // one workgroup per compute unit: split sequences until B*H*P covers 256 CUs
+    // workgroups resident per compute unit: 2 with 32-token chunks, 1 with 64;
+    // split sequences until B*H*P fills 256 compute units
+    const int C = p.chunk;
+    const int slots = 256 * (C == 32 ? 2 : 1);
     const int seqs = p.B * p.H;
-    int P = (256 + seqs - 1) / seqs;
+    int P = (slots + seqs - 1) / seqs;
     const int nchunks = (p.T + C - 1) / C;
     if (P > nchunks) P = nchunks;
     return P < 1 ? 1 : P;
@@ -793,8 +895,10 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop) {
     char *base = static_cast<char *>(ws);
     const WsLayout L = ws_layout(p, P);
+    const int C = p.chunk;
     MfmaArgs a{};
     a.p = p;
+    a.chunk = C;
     a.nchunks = (p.T + C - 1) / C;
     a.P = P;
     a.cps = (a.nchunks + P - 1) / P;
@@ -808,8 +912,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.seg_origin = reinterpret_cast<double *>(base + L.origin);
     a.final_lam = reinterpret_cast<double *>(base + L.flam);
     a.want_final = (p.K_out || p.V_out || p.clock_out) ? 1 : 0;
-    const bool scan = a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final;
-    a.has_init = scan ? 1 : 0;
+    a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     const int BH = p.B * p.H;
 
     hipLaunchKernelGGL(readout_pack_kernel, dim3(p.H, 8), dim3(NT), 0, st, p.m,
@@ -817,20 +920,8 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                        const_cast<__bf16 *>(a.My));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (a.P > 1 && a.nchunks > 0) {
-        hipLaunchKernelGGL(segment_state_kernel, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (scan) {
-        hipLaunchKernelGGL(segment_scan_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
-    if (a.nchunks > 0) {
-        hipLaunchKernelGGL(chunk_forward_kernel, dim3(BH * a.P), dim3(NT), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
+    e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
+    if (e != hipSuccess) return e;
     if (a.want_final) {
         hipLaunchKernelGGL(state_out_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -15,6 +15,13 @@
 // A state accumulator fed back as a B operand supplies, at k-step ks, the
 // k indices 16ks + {4h..4h+3, 8+4h..8+4h+3}; the other operand is read in
 // that same permuted order ("perm" reads below).
+//
+// Operands whose k index runs down the rows of a row-major LDS tile (the
+// "transposed" operands K^T, V^T, A^T) are read with ds_read_b64_tr_b16: within
+// each group of 16 lanes, output lane i, element j is element (i mod 4) of the
+// 8 bytes addressed by lane 4j + i/4.  When lane s of the group addresses row
+// r0 + s/4, columns c0 + 4 (s mod 4) .. +3, output lane i receives column c0 + i
+// of rows r0 .. r0 + 3.
 #pragma once
 
 #include "cyfa_internal.h"
@@ -62,6 +69,28 @@ __device__ __forceinline__ bf16x8 lds8_perm(const __bf16 *row, int k0, int h) {
     r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
     return r;
 }
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// Four rows of one column through the transpose read (see the layout note above).
+__device__ __forceinline__ bf16x4 lds4_tr(const __bf16 *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(p));
+}
+// Lane's base address for a transposed operand from a row-major tile with row
+// stride `stride`: the operand of column n = l % 32 and k = 8h + p is then
+// lds8_tr(base + k0 * stride + n0) for a tile block starting at (k0, n0).
+__device__ __forceinline__ const __bf16 *tr_base(const __bf16 *tile, int stride, int lane) {
+    const int s = lane & 15, g = lane >> 4;
+    return tile + (8 * (g >> 1) + (s >> 2)) * stride + 16 * (g & 1) + 4 * (s & 3);
+}
+__device__ __forceinline__ bf16x8 lds8_tr(const __bf16 *p, int stride) {
+    const bf16x4 lo = lds4_tr(p);
+    const bf16x4 hi = lds4_tr(p + 4 * stride);
+    bf16x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+}
+
 // registers 8*half .. 8*half+7 of an accumulator as a bf16 B operand
 __device__ __forceinline__ bf16x8 acc_to_operand(const f32x16 &acc, int half) {
     bf16x8 r;
@@ -104,6 +133,12 @@ __device__ __forceinline__ float swap_pair(float x) {
 // Value of lane l ^ 2 (DPP quad permutation [2,3,0,1]).
 __device__ __forceinline__ float swap_halves4(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+}
+
+// Value of lane l ^ 7 within each group of 8 (DPP row_half_mirror); after the
+// two swaps above have made each quad uniform, this fetches the other quad.
+__device__ __forceinline__ float swap_quads8(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
 }
 
 // ---- chunk-local prefix sums on one wave (lane = token row) --------------

@@ -16,8 +16,8 @@ constexpr int kPrepRowsPerBlock = 8;
 // grid (H, 128 / 8): block (h, rb) writes rows [8 rb, 8 rb + 8) of M_h.
 __global__ __launch_bounds__(256) void readout_prep_kernel(int m, const float *__restrict__ R,
                                                            float *__restrict__ M) {
-    // cos / sin of 2 pi r / m for r = 0..m-1; Phi[s][2l-1] = ac * cos(2 pi (l s mod m) / m)
-    __shared__ float tab_c[kMaxActive], tab_s[kMaxActive];
+    __shared__ float tab_c[kMaxActive], tab_s[kMaxActive];   // cos, sin of 2 pi r / m
+    __shared__ float phi[kMaxActive][kStoreRows];            // Phi[s][j], j < 128 (zero padded)
     __shared__ float Rrows[kPrepRowsPerBlock][kMaxActive];
     const int h = blockIdx.x;
     const int row0 = blockIdx.y * kPrepRowsPerBlock;
@@ -37,28 +37,39 @@ __global__ __launch_bounds__(256) void readout_prep_kernel(int m, const float *_
     __syncthreads();
     const float dc = (float)(1.0 / sqrt((double)m));
     const float ac = (float)sqrt(2.0 / (double)m);
-    float *Mh = M + (size_t)h * kStoreRows * kStoreRows;
-    for (int e = tid; e < kPrepRowsPerBlock * kStoreRows; e += blockDim.x) {
-        const int r = e / kStoreRows, j = e % kStoreRows;
-        const int i = row0 + r;
-        float acc = 0.f;
-        if (i < m && j < m) {
+    {
+        // thread (column j, half) fills rows s = half, half + 2, ...: the angle
+        // index (l s) mod m advances by 2 l mod m without any division
+        const int j = tid & 127, half = tid >> 7;
+        const int l = (j + 1) >> 1;
+        const int step = (2 * l) % m;
+        int idx = (l * half) % m;
+        for (int s = half; s < m; s += 2) {
+            float val = 0.f;
             if (j == 0) {
-                for (int s = 0; s < m; ++s) acc += Rrows[r][s];
-                acc *= dc;
-            } else {
-                const int l = (j + 1) >> 1;
-                const float *tab = (j & 1) ? tab_c : tab_s;
-                int idx = 0;                           // (l * s) mod m, advanced exactly
-                for (int s = 0; s < m; ++s) {
-                    acc = fmaf(Rrows[r][s], tab[idx], acc);
-                    idx += l;
-                    if (idx >= m) idx -= m;
-                }
-                acc *= ac;
+                val = dc;
+            } else if (j < m) {
+                val = ac * ((j & 1) ? tab_c[idx] : tab_s[idx]);
             }
+            phi[s][j] = val;
+            idx += step;
+            if (idx >= m) idx -= m;
         }
-        Mh[(size_t)i * kStoreRows + j] = acc;
+    }
+    __syncthreads();
+    // thread (j = tid % 128, half = tid / 128) computes rows 4 half .. 4 half + 3 of column j
+    const int j = tid & 127, r0 = 4 * (tid >> 7);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < m; ++s) {
+        const float ph = phi[s][j];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[k] = fmaf(Rrows[r0 + k][s], ph, acc[k]);
+    }
+    float *Mh = M + (size_t)h * kStoreRows * kStoreRows;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int i = row0 + r0 + k;
+        Mh[(size_t)i * kStoreRows + j] = (i < m && j < m) ? acc[k] : 0.f;
     }
 }
 

@@ -144,7 +144,10 @@ def selected_kernel(desc: FwdDesc) -> str:
     trial.kernel = KERNEL_MFMA
     n = ctypes.c_size_t(0)
     ok = load().cyfa_forward_workspace_size(ctypes.byref(trial), ctypes.byref(n)) == 0
-    return "mfma" if ok and desc.chunk in (0, 64) else "valu"
+    return "mfma" if ok and desc.chunk in (0, 32, 64) else "valu"
+
+
+DEFAULT_CHUNK = {"mfma": 32, "valu": 16}
 
 
 def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=127,

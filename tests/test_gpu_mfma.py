@@ -53,18 +53,29 @@ def _assert_ok(err, tol=TOL_BF16):
         assert v <= (1e-9 if k == "clock" else tol), (k, v)
 
 
-@pytest.mark.parametrize("segments", [1, 2, 3])
-def test_small_full_parity_and_segment_invariance(segments):
+@pytest.mark.parametrize("chunk,segments", [(32, 1), (32, 3), (32, 7), (64, 1), (64, 2), (64, 3)])
+def test_small_full_parity_and_segment_invariance(chunk, segments):
     x = make_forward_inputs(2, 200, 3, 128, 128, seed=41, dtype="bf16")
     t = upload(x)
-    res = _fwd(x, t, segments=segments, return_state=True, return_logits=True)
+    res = _fwd(x, t, chunk=chunk, segments=segments, return_state=True, return_logits=True)
     _assert_ok(_errors(x, res))
+
+
+def test_chunk_length_changes_only_rounding():
+    x = make_forward_inputs(2, 64 * 5 + 17, 2, 128, 128, seed=49, dtype="bf16")
+    t = upload(x)
+    a = _fwd(x, t, chunk=32, return_state=True)
+    b = _fwd(x, t, chunk=64, return_state=True)
+    torch.cuda.synchronize()
+    assert rel_err(a["o"].float().cpu().numpy(), b["o"].float().cpu().numpy()) <= 1e-2
+    assert rel_err(a["K"].cpu().numpy(), b["K"].cpu().numpy()) <= 1e-2
+    assert clock_err(a["clock"].cpu().numpy(), b["clock"].cpu().numpy(), 127) <= 1e-9
 
 
 def test_segment_count_changes_only_rounding():
     x = make_forward_inputs(1, 64 * 9 + 5, 2, 128, 128, seed=42, dtype="bf16")
     t = upload(x)
-    outs = [_fwd(x, t, segments=sgm, return_state=True) for sgm in (1, 4, 10)]
+    outs = [_fwd(x, t, segments=sgm, return_state=True) for sgm in (1, 4, 10, 19)]
     torch.cuda.synchronize()
     base = outs[0]["o"].float().cpu().numpy()
     for r in outs[1:]:
@@ -136,11 +147,12 @@ def test_empty_sequence_mfma():
     np.testing.assert_allclose(res["clock"].cpu().numpy(), [[5.25, 3.5]], atol=1e-9)
 
 
-def test_deterministic_mfma():
+@pytest.mark.parametrize("chunk", [32, 64])
+def test_deterministic_mfma(chunk):
     x = make_forward_inputs(2, 257, 2, 128, 128, seed=47, dtype="bf16")
     t = upload(x)
-    a = _fwd(x, t, segments=3)
-    b = _fwd(x, t, segments=3)
+    a = _fwd(x, t, segments=3, chunk=chunk)
+    b = _fwd(x, t, segments=3, chunk=chunk)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
 

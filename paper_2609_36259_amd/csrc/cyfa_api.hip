@@ -6,7 +6,7 @@
 #include <cstdio>
 #include <cstring>
 
-#include "../../include/cyfa.h"
+#include "cyfa.h"
 #include "cyfa_internal.h"
 
 namespace cyfa {

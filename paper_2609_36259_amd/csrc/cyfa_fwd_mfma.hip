@@ -51,40 +51,48 @@ template <int CC>
 struct Lay {
     static constexpr int RB = CC / 32;                 // 32-row blocks per tile
     static constexpr int SSC = CC + 8;                 // row stride of the score tile
+    static constexpr bool kMInLds = CC == 64;          // readout matrix resident in LDS
     static constexpr int TILE = CC * QS * 2;
     static constexpr int Q = 0;                        // Q   -> X -> W
     static constexpr int K = Q + TILE;                 // K   -> O''
     static constexpr int V = K + TILE;                 // V
-    static constexpr int A = V + TILE;                 // A   (temporal writes)
+    static constexpr int A = V + TILE;                 // A   (temporal writes) -> output staging
     static constexpr int AD = A + TILE;                // A, rows right-decayed to the chunk end
     static constexpr int S = AD + TILE;                // scores [CC][SSC] bf16
     static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs
-    static constexpr int Z = CS + CC * 64 * 4;         // logits [CC][ZS] f32 -> output staging
-    static constexpr int SC = Z + CC * ZS * 4;         // per-token scalars (64 entries each)
-    static constexpr int BYTES = SC + 64 * (4 + 4 + 4 + 8);
+    static constexpr int MT = CS + CC * 64 * 4;        // readout matrix [128][QS] bf16 (64-token chunks)
+    static constexpr int RED = MT + (kMInLds ? 128 * QS * 2 : 0);   // softmax (max, sum) per wave x row
+    static constexpr int SC = RED + 4 * CC * 8;        // per-token scalars (64 entries each)
+    static constexpr int SCB = 64 * (4 + 4 + 4 + 4 + 8) + 16;   // scalar block bytes
+    static constexpr int BYTES = SC + SCB;
     // state pre-pass: K, V, A_dec and the scalars
     static constexpr int PK = 0, PV = TILE, PAD = 2 * TILE, PSC = 3 * TILE;
-    static constexpr int PBYTES = PSC + 64 * (4 + 4 + 4 + 8);
+    static constexpr int PBYTES = PSC + SCB;
     static_assert(BYTES <= 160 * 1024, "LDS budget");
-    static_assert(TILE <= CC * ZS * 4, "output staging fits in the logit tile");
 };
 
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef _Float16 half8v __attribute__((ext_vector_type(8)));
 
 struct Tiles {
-    __bf16 *Qs, *Ks, *Vs, *As, *Ads, *Ss, *Xs, *Ws, *Os, *Stage;
-    float *Zf;
+    __bf16 *Qs, *Ks, *Vs, *As, *Ads, *Ss, *Xs, *Ws, *Os, *Stage, *Mt;
+    float2 *red;
     half2v *CS;
-    float *Gs, *gam, *betas;
-    double *lams;
+    float *Gs;      // chunk-local prefix sums of log alpha
+    float *gam;     // row scale of the inter-chunk terms: exp(G_r + L)
+    float *betas;
+    float *decw;    // multiplier of A_dec rows
+    double *urev;   // clock at each row reduced mod m, divided by m (revolutions)
+    float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
 };
 
 __device__ __forceinline__ void scalars_at(Tiles &t, char *base) {
     t.Gs = reinterpret_cast<float *>(base);
     t.gam = t.Gs + 64;
     t.betas = t.gam + 64;
-    t.lams = reinterpret_cast<double *>(t.betas + 64);
+    t.decw = t.betas + 64;
+    t.urev = reinterpret_cast<double *>(t.decw + 64);
+    t.ctl = reinterpret_cast<float *>(t.urev + 64);
 }
 
 template <int CC>
@@ -101,8 +109,9 @@ __device__ __forceinline__ Tiles fused_tiles(char *smem) {
     t.Ads = reinterpret_cast<__bf16 *>(smem + L::AD);
     t.Ss = reinterpret_cast<__bf16 *>(smem + L::S);
     t.CS = reinterpret_cast<half2v *>(smem + L::CS);
-    t.Zf = reinterpret_cast<float *>(smem + L::Z);
-    t.Stage = reinterpret_cast<__bf16 *>(smem + L::Z);
+    t.Mt = reinterpret_cast<__bf16 *>(smem + L::MT);
+    t.red = reinterpret_cast<float2 *>(smem + L::RED);
+    t.Stage = t.As;
     scalars_at(t, smem + L::SC);
     return t;
 }
@@ -181,18 +190,37 @@ __device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefe
 // Wave 0: chunk-local inclusive prefix sums of log alpha (float) and of the
 // clock increments (double, continuing the carried clock), reduced mod m.
 // Lanes past the chunk hold zeros, so entry 63 equals the chunk total.
+//
+// Carried states are kept as Kbar = exp(L) Kt (same L for Vbar).  Normally a
+// chunk only adds to Kt: Kt += K^T (A exp(-G_r - L)) and L += G_C, which is
+// Kbar <- gamma^C Kbar + K^T (A gamma^C / gamma^r) (App. B, Eq. app-scalar-chunk)
+// without touching the state registers.  When exp(+-(G_r + L)) could leave
+// [e^-60, e^60] the chunk instead rescales Kt by exp(L + G_C), uses
+// A gamma^C / gamma^r and restarts L at 0.
 template <int CC>
 __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC> &pf,
-                                            double &carry, double &gsum) {
+                                            double &carry, double &gsum, float &L) {
     const float G = wave_incl_scan(pf.g, lane);
     const double lam = carry + wave_incl_scan((double)pf.dl, lane);
+    const float GC = __shfl(G, 63);
+    float gabs = fabsf(G);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) gabs = fmaxf(gabs, __shfl_xor(gabs, o));
+    const bool lazy = fabsf(L) + gabs <= 60.f;
     s.Gs[lane] = G;
-    s.gam[lane] = __expf(G);
+    s.gam[lane] = __expf(G + L);
+    s.decw[lane] = lazy ? __expf(-G - L) : __expf(GC - G);
     s.betas[lane] = pf.be;
-    s.lams[lane] = reduce_clock(lam, m);
+    s.urev[lane] = reduce_clock(lam, m) / (double)m;
+    const float state_factor = lazy ? 1.f : __expf(L + GC);
+    L = lazy ? L + GC : 0.f;
+    if (lane == 0) {
+        s.ctl[0] = state_factor;
+        s.ctl[1] = L;
+    }
     const double last = __shfl(lam, 63);
     carry = reduce_clock(last, m);
-    gsum += (double)__shfl(G, 63);
+    gsum += (double)GC;
 }
 
 // Temporal write matrix for the chunk (Eq. app-temporal-writes):
@@ -212,8 +240,8 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
     const float dc = 1.0f / sqrtf((float)m);
     const float ac = sqrtf(2.0f / (float)m);
     const float be = s.betas[r];
-    const float wdec = __expf(s.Gs[63] - s.Gs[r]);
-    const double u = s.lams[r] / (double)m;          // revolutions per unit frequency
+    const float wdec = s.decw[r];
+    const double u = s.urev[r];                      // revolutions per unit frequency
     float s1, c1, sn, cs;
     sincos_rev((float)u, &s1, &c1);
     {
@@ -231,7 +259,9 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
         const float sv = live ? sn : 0.f;
         av[2 * jj] = be * ac * cv;
         av[2 * jj + 1] = -be * ac * sv;
-        csv[jj >> 2][2 * (jj & 3)] = (_Float16)cv;
+        // table entry 63 (internal columns 126, 127: DC and padding) is (1, 0),
+        // so the token-wise rotations pass those columns through unchanged
+        csv[jj >> 2][2 * (jj & 3)] = (_Float16)(j == 64 ? 1.f : cv);
         csv[jj >> 2][2 * (jj & 3) + 1] = (_Float16)sv;
         const float nc = cs * c1 - sn * s1;
         const float ns = sn * c1 + cs * s1;
@@ -268,14 +298,16 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
 template <int CC>
 __device__ __forceinline__ void update_states(const Tiles &s, int w, int lane,
                                               f32x16 (&kacc)[4], f32x16 (&vacc)[4]) {
-    const float gC = s.gam[63];
+    const float sf = s.ctl[0];
+    if (sf != 1.f) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            kacc[x][v] *= gC;
-            vacc[x][v] *= gC;
-        }
+            for (int v = 0; v < 16; ++v) {
+                kacc[x][v] *= sf;
+                vacc[x][v] *= sf;
+            }
+    }
     const __bf16 *Kt = tr_base(s.Ks, QS, lane);
     const __bf16 *Vt = tr_base(s.Vs, QS, lane) + 32 * w;
     const __bf16 *Adt = tr_base(s.Ads, QS, lane);
@@ -296,39 +328,53 @@ __device__ __forceinline__ constexpr int acc_off(int blk, int v) {
     return 32 * blk + 8 * (v >> 2) + (v & 3);
 }
 
-// Causal score tile (S (.) Gamma) for 32 x 32 block (rb, sb) -> Ss (bf16).
-// A rows come from Arow (row-major, k along the row), B columns from Brow's rows.
+// One 16 x 16 block (rb, sb) of the causal score tile (S (.) Gamma) -> Ss (bf16),
+// k = 128 along the rows of both operand tiles.
 template <int CC>
-__device__ __forceinline__ void score_tile(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
-                                           int rb, int sb, int l32, int hl) {
+__device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
+                                            int rb, int sb, int lane) {
     constexpr int SSC = Lay<CC>::SSC;
-    f32x16 acc = zero_acc();
-    const __bf16 *ap = Arow + (32 * rb + l32) * QS + 8 * hl;
-    const __bf16 *bp = Brow + (32 * sb + l32) * QS + 8 * hl;
+    const int l16 = lane & 15, g = lane >> 4;
+    f32x4 acc = zero_acc4();
+    const __bf16 *ap = Arow + (16 * rb + l16) * QS + 8 * g;
+    const __bf16 *bp = Brow + (16 * sb + l16) * QS + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) acc = mma(lds8(ap + 16 * ks), lds8(bp + 16 * ks), acc);
-    const int scol = 32 * sb + l32;
+    for (int ks = 0; ks < 4; ++ks) acc = mma16(lds8(ap + 32 * ks), lds8(bp + 32 * ks), acc);
+    const int scol = 16 * sb + l16;
+    const int row0 = 16 * rb + 4 * g;
     const float Gs_col = s.Gs[scol];
-    const float *Gr = s.Gs + 32 * rb + 4 * hl;
-    __bf16 *Sr = s.Ss + (32 * rb + 4 * hl) * SSC + scol;
-    const int rbase = 32 * rb + 4 * hl;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        const int ro = acc_off(0, v);
-        const float val = scol <= rbase + ro ? acc[v] * __expf(Gr[ro] - Gs_col) : 0.f;
-        Sr[ro * SSC] = (__bf16)val;
+    for (int r = 0; r < 4; ++r) {
+        const float val = scol <= row0 + r ? acc[r] * __expf(s.Gs[row0 + r] - Gs_col) : 0.f;
+        s.Ss[(row0 + r) * SSC + scol] = (__bf16)val;
     }
 }
 
-// the 32 x 32 score blocks of a causal CC x CC tile: (0,0) [, (1,0), (1,1)]
+// The 16 x 16 blocks of the causal CC x CC score tile that the intra-chunk
+// products read (the lower triangle plus the upper halves of the 32 x 32
+// diagonal blocks, which come out as zeros), spread evenly over the 4 waves.
 template <int CC>
 __device__ __forceinline__ void score_tiles(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
-                                            int w, int l32, int hl) {
-    if (CC == 64) {
-        if (w < 3) score_tile<CC>(s, Arow, Brow, w == 0 ? 0 : 1, w == 2 ? 1 : 0, l32, hl);
+                                            int w, int lane) {
+    if (CC == 32) {
+        score_block<CC>(s, Arow, Brow, w >> 1, w & 1, lane);
     } else {
-        if (w == 0) score_tile<CC>(s, Arow, Brow, 0, 0, l32, hl);
+        // (rb, sb) lists per wave: 12 blocks, 3 each
+        constexpr int kRb[12] = {0, 1, 1, 0, 2, 2, 2, 2, 3, 3, 3, 3};
+        constexpr int kSb[12] = {0, 0, 1, 1, 0, 1, 2, 3, 0, 1, 2, 3};
+#pragma unroll
+        for (int k = 0; k < 3; ++k) score_block<CC>(s, Arow, Brow, kRb[3 * w + k], kSb[3 * w + k], lane);
     }
+}
+
+__device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4], float f) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            kacc[x][v] *= f;
+            vacc[x][v] *= f;
+        }
 }
 
 __device__ __forceinline__ void load_state(const float *st, int w, int lane, f32x16 (&kacc)[4],
@@ -370,11 +416,12 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
         vacc[x] = f32x16{};
     }
     double carry = 0.0, gsum = 0.0;
+    float L = 0.f;
     Prefetch<CC> pf;
     load_chunk<CC, false>(a.p, b, h, c_begin * CC, tid, pf);
     for (int c = c_begin; c < c_end; ++c) {
         store_chunk<CC, false>(s, tid, pf);
-        if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum);
+        if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
         build_writes<CC, false>(s, tid, a.p.m);
@@ -383,6 +430,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
         __syncthreads();
     }
     const size_t slot = (size_t)bh * a.P + p;
+    scale_states(kacc, vacc, __expf(s.ctl[1]));
     dump_state(a.seg_state + slot * kStateFloats, w, lane, kacc, vacc);
     if (tid == 0) {
         a.seg_span[slot] = carry;
@@ -482,10 +530,10 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
 // ---- 3. fused chunk forward ----------------------------------------------------
 template <int CC>
 __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(MfmaArgs a) {
-    using L = Lay<CC>;
-    constexpr int RB = L::RB;
-    constexpr int SSC = L::SSC;
-    __shared__ __attribute__((aligned(16))) char smem[L::BYTES];
+    using Ly = Lay<CC>;
+    constexpr int RB = Ly::RB;
+    constexpr int SSC = Ly::SSC;
+    __shared__ __attribute__((aligned(16))) char smem[Ly::BYTES];
     const Tiles s = fused_tiles<CC>(smem);
     const FwdParams &p = a.p;
     const int bh = blockIdx.x / a.P, seg = blockIdx.x % a.P;
@@ -495,16 +543,21 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
     const int icol = 32 * w + l32;                   // this lane's internal column
     const int h4 = 4 * hl;
+    // U(theta) on a (cos, sin) pair held by lanes (2k, 2k+1): c x - s x' on the cos
+    // lane, c x + s x' on the sin lane
+    const float sgn = (icol & 1) ? 1.f : -1.f;
 
     // Per-lane bases: every unrolled LDS access below is base + compile-time offset.
-    const __bf16 *Mzr = a.Mz + ((size_t)h * 128 + icol) * 128 + 8 * hl;   // B operand rows (L2)
+    // Readout operand rows when the readout matrix is read from L2 (32-token chunks).
+    const __bf16 *Mzr = a.Mz + ((size_t)h * 128 + icol) * 128 + 8 * hl;
     const __bf16 *Myr = a.My + ((size_t)h * 128 + icol) * 128 + 8 * hl;
+    const __bf16 *Mza = s.Mt + icol * QS + 8 * hl;                        // M rows (LDS)
+    const __bf16 *Myt = tr_base(s.Mt, QS, lane) + 32 * w;                 // M columns (LDS)
+    const float zs = p.scale * 1.4426950408889634f;                       // logits in log2 units
     const float *gam_l = s.gam + h4;                                      // accumulator rows
     const half2v *CS_l = s.CS + h4 * 64 + (icol >> 1);
     __bf16 *X_l = s.Xs + h4 * QS + icol;                                  // X (then W) tile
-    __bf16 *O2_l = s.Os + h4 * QS + icol;                                 // O'' tile
     __bf16 *St_l = s.Stage + h4 * QS + icol;                              // output staging
-    float *Z_l = s.Zf + h4 * ZS + icol;
     const __bf16 *Qperm = s.Qs + l32 * QS + h4;                           // permuted-k A operands
     const __bf16 *Operm = s.Os + l32 * QS + h4;
     const __bf16 *Xa = s.Xs + l32 * QS + 8 * hl;                          // natural-k A operands
@@ -514,6 +567,17 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
     const __bf16 *Adt = tr_base(s.Ads, QS, lane);
     const __bf16 *Kt = tr_base(s.Ks, QS, lane);
 
+    if (Ly::kMInLds) {
+        // readout matrix M_h (slot rows, internal basis columns), resident for the whole segment
+        const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int e = it * NT + tid;
+            const int row = e >> 4, c0 = (e & 15) * 8;
+            *reinterpret_cast<uint4 *>(s.Mt + row * QS + c0) =
+                *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
+        }
+    }
     f32x16 kacc[4], vacc[4];
     float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
     if (a.has_init) {
@@ -526,6 +590,7 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
         }
     }
     double carry = 0.0, gsum = 0.0;
+    float logf = 0.f;                                // carried states are exp(logf) x registers
     // With one workgroup per compute unit (64-token chunks) the next chunk is
     // prefetched into registers during the current one; with two workgroups
     // per unit (32-token chunks) the other workgroup covers the load latency
@@ -541,13 +606,13 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
         // -- A: stage the chunk, prefix sums, temporal writes
         if (!kPrefetch) load_chunk<CC, true>(p, b, h, t0, tid, pf);
         store_chunk<CC, true>(s, tid, pf);
-        if (w == 0) chunk_scans<CC>(s, lane, m, pf, carry, gsum);
+        if (w == 0) chunk_scans<CC>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (kPrefetch && c + 1 < c_end) load_chunk<CC, true>(p, b, h, (c + 1) * CC, tid, pf);
         build_writes<CC, true>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
-        score_tiles<CC>(s, s.Qs, s.Ks, w, l32, hl);
+        score_tiles<CC>(s, s.Qs, s.Ks, w, lane);
         f32x16 oacc[RB];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) oacc[rb] = zero_acc();
@@ -570,12 +635,14 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
                 oacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(At + 16 * ks * QS, QS),
                                oacc[rb]);
         {
-            // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec
-            const float gC = s.gam[63];
+            // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec (decay kept in L)
+            const float sf = s.ctl[0];
+            if (sf != 1.f) {
 #pragma unroll
-            for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 4; ++x)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) kacc[x][v] *= gC;
+                    for (int v = 0; v < 16; ++v) kacc[x][v] *= sf;
+            }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
                 const bf16x8 ad_w = lds8_tr(Adt + 16 * ks * QS + 32 * w, QS);
@@ -584,7 +651,7 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
                     kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
             }
         }
-        // -- middle step 1: X_r = scale U(lambda_r) O'_r -> X tile (reuses Q's)
+        // -- middle step 1: X_r = U(lambda_r) O'_r, times scale log2(e) -> X tile (reuses Q's)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -592,120 +659,125 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
                 const int ro = acc_off(rb, v);
                 const float self = oacc[rb][v];
                 const float part = swap_pair(self);
-                float x = 0.f;
-                if (icol < kDC) {
-                    const half2v cs = CS_l[ro * 64];
-                    const float cc = (float)cs[0], sn = (float)cs[1];
-                    x = (icol & 1) ? (sn * part + cc * self) : (cc * self - sn * part);
-                } else if (icol == kDC) {
-                    x = self;
-                }
-                X_l[ro * QS] = (__bf16)(p.scale * x);
+                const half2v cs = CS_l[ro * 64];
+                X_l[ro * QS] = (__bf16)(zs * fmaf(sgn * (float)cs[1], part, (float)cs[0] * self));
             }
         __syncthreads();
-        // -- middle step 2: slot logits Z = X M^T -> logit tile
+        // -- middle step 2: slot logits, transposed: Z^T = M X^T.  Wave w owns slots
+        //    32w .. 32w+31; lane (token 32 nb + l32, half hl) holds 16 of them.
+        f32x16 zacc[RB];
         {
+#pragma unroll
+            for (int nb = 0; nb < RB; ++nb) zacc[nb] = zero_acc();
             bf16x8 mz[8];
+            if (!Ly::kMInLds) {
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
-            f32x16 zacc[RB];
+                for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
+            }
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) zacc[rb] = zero_acc();
+            for (int ks = 0; ks < 8; ++ks) {
+                const bf16x8 ma = Ly::kMInLds ? lds8(Mza + 16 * ks) : mz[ks];
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks)
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-                    zacc[rb] = mma(lds8(Xa + 32 * rb * QS + 16 * ks), mz[ks], zacc[rb]);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) Z_l[acc_off(rb, v) * ZS] = zacc[rb][v];
+                for (int nb = 0; nb < RB; ++nb)
+                    zacc[nb] = mma(ma, lds8(Xa + 32 * nb * QS + 16 * ks), zacc[nb]);
+            }
         }
-        __syncthreads();
-        // -- middle step 3: softmax over the m active slots -> W tile (reuses X's)
-        {
-            constexpr int TPR = NT / CC;            // threads per row
-            constexpr int NS = 128 / TPR;           // slots per thread
-            const int r = tid / TPR, q = tid % TPR;
-            const float *zr = s.Zf + r * ZS + NS * q;
-            float zv[NS];
+        // -- middle step 3: softmax over the m active slots.  Per token: in-lane over
+        //    16 slots, across the two lane halves, then one (max, sum) exchange
+        //    between the 4 waves.
 #pragma unroll
-            for (int k4 = 0; k4 < NS / 4; ++k4) {
-                const float4 z4 = *reinterpret_cast<const float4 *>(zr + 4 * k4);
-                zv[4 * k4] = z4.x;
-                zv[4 * k4 + 1] = z4.y;
-                zv[4 * k4 + 2] = z4.z;
-                zv[4 * k4 + 3] = z4.w;
-            }
-            if (p.logits && r < n) {
-                float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m + NS * q;
-#pragma unroll
-                for (int k = 0; k < NS; ++k)
-                    if (NS * q + k < m) lg[k] = zv[k];
-            }
+        for (int nb = 0; nb < RB; ++nb) {
             float mx = -INFINITY;
 #pragma unroll
-            for (int k = 0; k < NS; ++k) {
-                if (NS * q + k >= m) zv[k] = -INFINITY;
-                mx = fmaxf(mx, zv[k]);
+            for (int v = 0; v < 16; ++v) {
+                const int slot = icol - l32 + 8 * (v >> 2) + h4 + (v & 3);
+                if (slot >= m) zacc[nb][v] = -INFINITY;
+                mx = fmaxf(mx, zacc[nb][v]);
             }
-            mx = fmaxf(mx, swap_pair(mx));
-            mx = fmaxf(mx, swap_halves4(mx));
-            if (TPR == 8) mx = fmaxf(mx, swap_quads8(mx));
-            float sum = 0.f;
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            // a wave whose slots are all inactive (m <= 32 w) contributes (-inf, 0)
+            const float mref = mx == -INFINITY ? 0.f : mx;
+            float sm = 0.f;
 #pragma unroll
-            for (int k = 0; k < NS; ++k) {
-                zv[k] = __expf(zv[k] - mx);
-                sum += zv[k];
-            }
-            sum += swap_pair(sum);
-            sum += swap_halves4(sum);
-            if (TPR == 8) sum += swap_quads8(sum);
-            const float inv = 1.f / sum;
-            __bf16 *wr = s.Ws + r * QS + NS * q;
+            for (int v = 0; v < 16; ++v) sm += __builtin_amdgcn_exp2f(zacc[nb][v] - mref);
+            sm += __shfl_xor(sm, 32);
+            const int r = 32 * nb + l32;
+            if (hl == 0) s.red[w * CC + r] = make_float2(mx, sm);
+            if (p.logits && r < n) {
+                // the logit accumulators hold log2(e) z; report z
+                float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m;
 #pragma unroll
-            for (int k8 = 0; k8 < NS / 8; ++k8) {
-                bf16x8 wv;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) wv[k] = (__bf16)(zv[8 * k8 + k] * inv);
-                *reinterpret_cast<bf16x8 *>(wr + 8 * k8) = wv;
+                for (int v = 0; v < 16; ++v) {
+                    const int slot = icol - l32 + 8 * (v >> 2) + h4 + (v & 3);
+                    if (slot < m) lg[slot] = zacc[nb][v] * 0.69314718055994531f;
+                }
             }
         }
         __syncthreads();
-        // -- middle step 4: O''_r = U(-lambda_r) M^T W_r -> O'' tile (reuses K's)
-        {
-            bf16x8 my[8];
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
+        for (int nb = 0; nb < RB; ++nb) {
+            const int r = 32 * nb + l32;
+            float2 pr[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) pr[x] = s.red[x * CC + r];
+            const float M = fmaxf(fmaxf(pr[0].x, pr[1].x), fmaxf(pr[2].x, pr[3].x));
+            float Lsum = 0.f;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) Lsum += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
+            const float inv = 1.f / Lsum;
+            __bf16 *wrow = s.Ws + r * QS + 32 * w + h4;
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+                bf16x4 wv;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    wv[k] = (__bf16)(__builtin_amdgcn_exp2f(zacc[nb][4 * v4 + k] - M) * inv);
+                *reinterpret_cast<bf16x4 *>(wrow + 8 * v4) = wv;
+            }
+        }
+        __syncthreads();
+        // -- middle step 4: O''_r = U(-lambda_r) M^T W_r, transposed: Y^T = M^T W^T.
+        //    Wave w owns basis rows 32w .. 32w+31; each (cos, sin) pair sits in two
+        //    consecutive registers of one lane, so the rotation is in-lane.
+        {
             f32x16 yacc[RB];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) yacc[rb] = zero_acc();
+            for (int nb = 0; nb < RB; ++nb) yacc[nb] = zero_acc();
+            bf16x8 my[8];
+            if (!Ly::kMInLds) {
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks)
+                for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
+            }
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-                    yacc[rb] = mma(lds8(Xa + 32 * rb * QS + 16 * ks), my[ks], yacc[rb]);
+            for (int ks = 0; ks < 8; ++ks) {
+                const bf16x8 mt = Ly::kMInLds ? lds8_tr(Myt + 16 * ks * QS, QS) : my[ks];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
+                for (int nb = 0; nb < RB; ++nb)
+                    yacc[nb] = mma(mt, lds8(Xa + 32 * nb * QS + 16 * ks), yacc[nb]);
+            }
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int ro = acc_off(rb, v);
-                    const float self = yacc[rb][v];
-                    const float part = swap_pair(self);
-                    float x = 0.f;
-                    if (icol < kDC) {
-                        const half2v cs = CS_l[ro * 64];
-                        const float cc = (float)cs[0], sn = (float)cs[1];
-                        x = (icol & 1) ? (cc * self - sn * part) : (cc * self + sn * part);
-                    } else if (icol == kDC) {
-                        x = self;
+            for (int nb = 0; nb < RB; ++nb) {
+                const int r = 32 * nb + l32;
+                const half2v *csr = s.CS + r * 64 + 16 * w + 2 * hl;
+                __bf16 *orow = s.Os + r * QS + 32 * w + h4;
+#pragma unroll
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    bf16x4 ov;
+#pragma unroll
+                    for (int k2 = 0; k2 < 2; ++k2) {
+                        const half2v cs = csr[4 * v4 + k2];
+                        const float c = (float)cs[0], sn = (float)cs[1];
+                        const float yc = yacc[nb][4 * v4 + 2 * k2], ysn = yacc[nb][4 * v4 + 2 * k2 + 1];
+                        ov[2 * k2] = (__bf16)fmaf(sn, ysn, c * yc);
+                        ov[2 * k2 + 1] = (__bf16)fmaf(-sn, yc, c * ysn);
                     }
-                    O2_l[ro * QS] = (__bf16)x;
+                    *reinterpret_cast<bf16x4 *>(orow + 8 * v4) = ov;
                 }
+            }
         }
         __syncthreads();
         // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V
-        score_tiles<CC>(s, s.Os, s.As, w, l32, hl);
+        score_tiles<CC>(s, s.Os, s.As, w, lane);
         f32x16 pacc[RB];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) pacc[rb] = zero_acc();
@@ -733,12 +805,14 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
 #pragma unroll
             for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
         {
-            // value state: Vbar <- gamma^C Vbar + A_dec^T V
-            const float gC = s.gam[63];
+            // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
+            const float sf = s.ctl[0];
+            if (sf != 1.f) {
 #pragma unroll
-            for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 4; ++x)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) vacc[x][v] *= gC;
+                    for (int v = 0; v < 16; ++v) vacc[x][v] *= sf;
+            }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
                 const bf16x8 v_w = lds8_tr(Vt + 16 * ks * QS, QS);
@@ -760,6 +834,7 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
         }
     }
     if (a.want_final && seg == a.P - 1) {
+        scale_states(kacc, vacc, __expf(s.ctl[1]));
         dump_state(slot_state, w, lane, kacc, vacc);
         if (tid == 0) a.final_lam[bh] = carry;
     }

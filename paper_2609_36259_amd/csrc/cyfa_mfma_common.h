@@ -33,6 +33,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int C = 64;             // chunk length
 constexpr int D = 128;            // head dim
@@ -47,12 +48,24 @@ constexpr int kStateFloats = 2 * 128 * 128;   // one (b, h) segment: K then V
 __device__ __forceinline__ f32x16 mma(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+// v_mfma_f32_16x16x32_bf16 (l = lane, g = l / 16):
+//   A (16 x 32): lane l holds A[l % 16][8g + p];  B (32 x 16): B[8g + p][l % 16]
+//   D (16 x 16): lane l, register r holds D[4g + r][l % 16]
+__device__ __forceinline__ f32x4 mma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
 
 // A zero accumulator materialised where it is used: keeps the compiler from
 // hoisting one zero vector per accumulator out of the chunk loop and holding
 // them all live across it.
 __device__ __forceinline__ f32x16 zero_acc() {
     f32x16 z = {};
+    asm volatile("" : "+v"(z));
+    return z;
+}
+
+__device__ __forceinline__ f32x4 zero_acc4() {
+    f32x4 z = {};
     asm volatile("" : "+v"(z));
     return z;
 }

@@ -100,6 +100,26 @@ def test_variants(variant):
     _assert_ok(_errors(x, res))
 
 
+@pytest.mark.parametrize("chunk", [32, 64])
+def test_extreme_and_mixed_gates(chunk):
+    """Stretches of heavy forgetting (the carried-state rescaling path), of no
+    forgetting and of ordinary gates, plus a case with no gates at all."""
+    x = make_forward_inputs(1, 517, 2, 128, 128, seed=50, dtype="bf16")
+    g = x["log_alpha"]
+    g[:, 40:140] = -6.0          # exp(-6 * 32) per chunk: forces the rescaling branch
+    g[:, 200:330] = 0.0          # alpha = 1
+    g[:, 400:410] = -40.0        # near-total erasure
+    t = upload(x)
+    res = _fwd(x, t, chunk=chunk, segments=3, return_state=True, return_logits=True)
+    _assert_ok(_errors(x, res))
+    y = make_forward_inputs(1, 300, 2, 128, 128, seed=51, dtype="bf16")
+    y["log_alpha"] = None
+    y["beta"] = None
+    ty = upload(y)
+    res = _fwd(y, ty, chunk=chunk, segments=2, return_state=True)
+    _assert_ok(_errors(y, res))
+
+
 def test_initial_state_and_resume():
     cyfa = _cyfa()
     x = make_forward_inputs(2, 300, 2, 128, 128, seed=44, dtype="bf16")

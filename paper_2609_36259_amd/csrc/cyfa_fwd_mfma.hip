@@ -19,28 +19,11 @@
 //      accumulators for the whole segment.
 //   4. state_out_kernel  (b, h): rotates the last segment's final state back to
 //      the absolute clock and writes it in the ABI layout (only when asked).
-#include "cyfa_mfma_common.h"
+#include "cyfa_mfma_chunk.h"
 
 namespace cyfa {
 
 using namespace mfma;
-
-struct MfmaArgs {
-    FwdParams p;
-    int P;               // segments per (b, h)
-    int cps;             // chunks per segment
-    int nchunks;         // chunks per sequence
-    int chunk;           // chunk length (32 or 64)
-    const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j
-    const __bf16 *My;    // [H][128][128]  row = internal basis j, column = slot i'
-    float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
-    double *seg_span;    // [B*H*P] clock span of each segment (reduced mod m)
-    double *seg_gsum;    // [B*H*P] sum of log alpha over each segment
-    double *seg_origin;  // [B*H*P] absolute clock at each segment start (reduced)
-    double *final_lam;   // [B*H] local clock after the last segment (reduced)
-    int has_init;        // segment-entry states are read from seg_state
-    int want_final;      // last segment dumps its final state into seg_state
-};
 
 namespace {
 
@@ -51,7 +34,6 @@ template <int CC>
 struct Lay {
     static constexpr int RB = CC / 32;                 // 32-row blocks per tile
     static constexpr int SSC = CC + 8;                 // row stride of the score tile
-    static constexpr bool kMInLds = CC == 64;          // readout matrix resident in LDS
     static constexpr int TILE = CC * QS * 2;
     static constexpr int Q = 0;                        // Q   -> X -> W
     static constexpr int K = Q + TILE;                 // K   -> O''
@@ -60,8 +42,7 @@ struct Lay {
     static constexpr int AD = A + TILE;                // A, rows right-decayed to the chunk end
     static constexpr int S = AD + TILE;                // scores [CC][SSC] bf16
     static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs
-    static constexpr int MT = CS + CC * 64 * 4;        // readout matrix [128][QS] bf16 (64-token chunks)
-    static constexpr int RED = MT + (kMInLds ? 128 * QS * 2 : 0);   // softmax (max, sum) per wave x row
+    static constexpr int RED = CS + CC * 64 * 4;       // softmax (max, sum) per wave x row
     static constexpr int SC = RED + 4 * CC * 8;        // per-token scalars (64 entries each)
     static constexpr int SCB = 64 * (4 + 4 + 4 + 4 + 8) + 16;   // scalar block bytes
     static constexpr int BYTES = SC + SCB;
@@ -70,30 +51,6 @@ struct Lay {
     static constexpr int PBYTES = PSC + SCB;
     static_assert(BYTES <= 160 * 1024, "LDS budget");
 };
-
-typedef _Float16 half2v __attribute__((ext_vector_type(2)));
-typedef _Float16 half8v __attribute__((ext_vector_type(8)));
-
-struct Tiles {
-    __bf16 *Qs, *Ks, *Vs, *As, *Ads, *Ss, *Xs, *Ws, *Os, *Stage, *Mt;
-    float2 *red;
-    half2v *CS;
-    float *Gs;      // chunk-local prefix sums of log alpha
-    float *gam;     // row scale of the inter-chunk terms: exp(G_r + L)
-    float *betas;
-    float *decw;    // multiplier of A_dec rows
-    double *urev;   // clock at each row reduced mod m, divided by m (revolutions)
-    float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
-};
-
-__device__ __forceinline__ void scalars_at(Tiles &t, char *base) {
-    t.Gs = reinterpret_cast<float *>(base);
-    t.gam = t.Gs + 64;
-    t.betas = t.gam + 64;
-    t.decw = t.betas + 64;
-    t.urev = reinterpret_cast<double *>(t.decw + 64);
-    t.ctl = reinterpret_cast<float *>(t.urev + 64);
-}
 
 template <int CC>
 __device__ __forceinline__ Tiles fused_tiles(char *smem) {
@@ -109,7 +66,6 @@ __device__ __forceinline__ Tiles fused_tiles(char *smem) {
     t.Ads = reinterpret_cast<__bf16 *>(smem + L::AD);
     t.Ss = reinterpret_cast<__bf16 *>(smem + L::S);
     t.CS = reinterpret_cast<half2v *>(smem + L::CS);
-    t.Mt = reinterpret_cast<__bf16 *>(smem + L::MT);
     t.red = reinterpret_cast<float2 *>(smem + L::RED);
     t.Stage = t.As;
     scalars_at(t, smem + L::SC);
@@ -125,171 +81,6 @@ __device__ __forceinline__ Tiles prepass_tiles(char *smem) {
     t.Ads = reinterpret_cast<__bf16 *>(smem + L::PAD);
     scalars_at(t, smem + L::PSC);
     return t;
-}
-
-// Global -> register prefetch of one chunk: CC/16 x 16-byte pieces per thread per
-// tensor (rows 16 it + tid / 16, columns 8 (tid % 16)), plus one token's scalars
-// on the first CC lanes.
-template <int CC>
-struct Prefetch {
-    uint4 q[CC / 16], k[CC / 16], v[CC / 16];
-    float g, dl, be;
-};
-
-template <int CC, bool kWithQ>
-__device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int tid,
-                                           Prefetch<CC> &pf) {
-    const uint4 zero = make_uint4(0, 0, 0, 0);
-    const __bf16 *q = static_cast<const __bf16 *>(p.q);
-    const __bf16 *k = static_cast<const __bf16 *>(p.k);
-    const __bf16 *v = static_cast<const __bf16 *>(p.v);
-    const int r0 = tid >> 4, d0 = (tid & 15) * 8;
-    const size_t row_stride = (size_t)p.H * D;
-    const size_t base = (((size_t)b * p.T + t0 + r0) * p.H + h) * D + d0;
-#pragma unroll
-    for (int it = 0; it < CC / 16; ++it) {
-        const int t = t0 + r0 + 16 * it;
-        const size_t off = base + (size_t)(16 * it) * row_stride;
-        if (t < p.T) {
-            if (kWithQ) pf.q[it] = *reinterpret_cast<const uint4 *>(q + off);
-            pf.k[it] = *reinterpret_cast<const uint4 *>(k + off);
-            pf.v[it] = *reinterpret_cast<const uint4 *>(v + off);
-        } else {
-            if (kWithQ) pf.q[it] = zero;
-            pf.k[it] = zero;
-            pf.v[it] = zero;
-        }
-    }
-    if (tid < 64) {
-        const int t = t0 + tid;
-        if (tid < CC && t < p.T) {
-            const size_t si = ((size_t)b * p.T + t) * p.H + h;
-            pf.dl = p.delta[si];
-            pf.g = p.log_alpha ? p.log_alpha[si] : 0.f;
-            pf.be = p.beta ? p.beta[si] : 1.f;
-        } else {
-            pf.dl = 0.f;   // rows past the chunk or the sequence: no shift, no decay, no write
-            pf.g = 0.f;
-            pf.be = 0.f;
-        }
-    }
-}
-
-// Registers -> LDS, row-major tiles.
-template <int CC, bool kWithQ>
-__device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefetch<CC> &pf) {
-    const int off = (tid >> 4) * QS + (tid & 15) * 8;
-#pragma unroll
-    for (int it = 0; it < CC / 16; ++it) {
-        if (kWithQ) *reinterpret_cast<uint4 *>(s.Qs + off + 16 * it * QS) = pf.q[it];
-        *reinterpret_cast<uint4 *>(s.Ks + off + 16 * it * QS) = pf.k[it];
-        *reinterpret_cast<uint4 *>(s.Vs + off + 16 * it * QS) = pf.v[it];
-    }
-}
-
-// Wave 0: chunk-local inclusive prefix sums of log alpha (float) and of the
-// clock increments (double, continuing the carried clock), reduced mod m.
-// Lanes past the chunk hold zeros, so entry 63 equals the chunk total.
-//
-// Carried states are kept as Kbar = exp(L) Kt (same L for Vbar).  Normally a
-// chunk only adds to Kt: Kt += K^T (A exp(-G_r - L)) and L += G_C, which is
-// Kbar <- gamma^C Kbar + K^T (A gamma^C / gamma^r) (App. B, Eq. app-scalar-chunk)
-// without touching the state registers.  When exp(+-(G_r + L)) could leave
-// [e^-60, e^60] the chunk instead rescales Kt by exp(L + G_C), uses
-// A gamma^C / gamma^r and restarts L at 0.
-template <int CC>
-__device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC> &pf,
-                                            double &carry, double &gsum, float &L) {
-    const float G = wave_incl_scan(pf.g, lane);
-    const double lam = carry + wave_incl_scan((double)pf.dl, lane);
-    const float GC = __shfl(G, 63);
-    float gabs = fabsf(G);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) gabs = fmaxf(gabs, __shfl_xor(gabs, o));
-    const bool lazy = fabsf(L) + gabs <= 60.f;
-    s.Gs[lane] = G;
-    s.gam[lane] = __expf(G + L);
-    s.decw[lane] = lazy ? __expf(-G - L) : __expf(GC - G);
-    s.betas[lane] = pf.be;
-    s.urev[lane] = reduce_clock(lam, m) / (double)m;
-    const float state_factor = lazy ? 1.f : __expf(L + GC);
-    L = lazy ? L + GC : 0.f;
-    if (lane == 0) {
-        s.ctl[0] = state_factor;
-        s.ctl[1] = L;
-    }
-    const double last = __shfl(lam, 63);
-    carry = reduce_clock(last, m);
-    gsum += (double)GC;
-}
-
-// Temporal write matrix for the chunk (Eq. app-temporal-writes):
-// A_r = beta_r U(-lambda_r) b, i.e. beta_r [sqrt(2/m) cos th_j, -sqrt(2/m) sin th_j]
-// on pair j and beta_r / sqrt(m) on DC, th_j = 2 pi j lambda_r / m.  The copy
-// A_dec has row r scaled by gamma^C / gamma^r (right rescaling, Eq. app-chunk-rescale).
-// Thread (r = tid / TPR, q = tid % TPR) fills internal columns NCOL q .. NCOL q + NCOL-1
-// of row r; the last quarter also holds DC (column 126) and padding (127).  The
-// phases advance by angle addition from an accurately reduced start.
-template <int CC, bool kFull>
-__device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
-    constexpr int TPR = NT / CC;          // threads per row
-    constexpr int NCOL = 128 / TPR;       // columns per thread
-    constexpr int NP = NCOL / 2;          // pairs per thread
-    const int r = tid / TPR, q = tid % TPR;
-    const int J = (m - 1) >> 1;
-    const float dc = 1.0f / sqrtf((float)m);
-    const float ac = sqrtf(2.0f / (float)m);
-    const float be = s.betas[r];
-    const float wdec = s.decw[r];
-    const double u = s.urev[r];                      // revolutions per unit frequency
-    float s1, c1, sn, cs;
-    sincos_rev((float)u, &s1, &c1);
-    {
-        double rev = (double)(NP * q + 1) * u;
-        rev -= floor(rev);
-        sincos_rev((float)rev, &sn, &cs);
-    }
-    float av[NCOL];
-    half8v csv[NP / 4];
-#pragma unroll
-    for (int jj = 0; jj < NP; ++jj) {
-        const int j = NP * q + 1 + jj;
-        const bool live = j <= J && j <= 63;
-        const float cv = live ? cs : 0.f;
-        const float sv = live ? sn : 0.f;
-        av[2 * jj] = be * ac * cv;
-        av[2 * jj + 1] = -be * ac * sv;
-        // table entry 63 (internal columns 126, 127: DC and padding) is (1, 0),
-        // so the token-wise rotations pass those columns through unchanged
-        csv[jj >> 2][2 * (jj & 3)] = (_Float16)(j == 64 ? 1.f : cv);
-        csv[jj >> 2][2 * (jj & 3) + 1] = (_Float16)sv;
-        const float nc = cs * c1 - sn * s1;
-        const float ns = sn * c1 + cs * s1;
-        cs = nc;
-        sn = ns;
-    }
-    if (q == TPR - 1) {    // internal columns 126 (DC) and 127 (padding)
-        av[NCOL - 2] = be * dc;
-        av[NCOL - 1] = 0.f;
-    }
-    __bf16 *arow = s.As + r * QS + NCOL * q;
-    __bf16 *adrow = s.Ads + r * QS + NCOL * q;
-#pragma unroll
-    for (int k8 = 0; k8 < NCOL / 8; ++k8) {
-        bf16x8 a8, ad8;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            a8[k] = (__bf16)av[8 * k8 + k];
-            ad8[k] = (__bf16)(av[8 * k8 + k] * wdec);
-        }
-        if (kFull) *reinterpret_cast<bf16x8 *>(arow + 8 * k8) = a8;
-        *reinterpret_cast<bf16x8 *>(adrow + 8 * k8) = ad8;
-    }
-    if (kFull) {
-        half8v *csrow = reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q);
-#pragma unroll
-        for (int k4 = 0; k4 < NP / 4; ++k4) csrow[k4] = csv[k4];
-    }
 }
 
 // Carried-state updates of one chunk (App. B):
@@ -506,30 +297,49 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
     }
     if (rotates) rotate_pair(c0, j, m, x0, x1);   // initial state in the frame with origin clock0
     double origin = reduce_clock(c0, m);
-    for (int q = 0; q < a.P; ++q) {
-        const size_t slot = (size_t)bh * a.P + q;
-        float *st = a.seg_state + slot * kStateFloats;
-        if (gidx == 0) a.seg_origin[slot] = origin;
-        float d0 = 0.f, d1 = 0.f;
-        if (q < a.P - 1) {
-            d0 = st[pr.o0];
-            d1 = st[pr.o1];
+    // Segment contributions are fetched kBatch segments at a time, ahead of the
+    // dependent chain through them.  Every thread owns the same two offsets in
+    // every segment, so the loads of a batch never see this batch's stores.
+    constexpr int kBatch = 8;
+    for (int q0 = 0; q0 < a.P; q0 += kBatch) {
+        float d0[kBatch], d1[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = q0 + u;
+            d0[u] = 0.f;
+            d1[u] = 0.f;
+            if (q < a.P - 1) {
+                const float *st = a.seg_state + ((size_t)bh * a.P + q) * kStateFloats;
+                d0[u] = st[pr.o0];
+                d1[u] = st[pr.o1];
+            }
         }
-        st[pr.o0] = x0;
-        st[pr.o1] = x1;
-        if (q < a.P - 1) {
-            const float gdec = (float)exp(a.seg_gsum[slot]);
-            x0 = fmaf(gdec, x0, d0);
-            x1 = fmaf(gdec, x1, d1);
-            if (rotates) rotate_pair(a.seg_span[slot], j, m, x0, x1);
-            origin = reduce_clock(origin + a.seg_span[slot], m);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = q0 + u;
+            if (q >= a.P) break;
+            const size_t slot = (size_t)bh * a.P + q;
+            float *st = a.seg_state + slot * kStateFloats;
+            if (gidx == 0) a.seg_origin[slot] = origin;
+            st[pr.o0] = x0;
+            st[pr.o1] = x1;
+            if (q < a.P - 1) {
+                const float gdec = (float)exp(a.seg_gsum[slot]);
+                x0 = fmaf(gdec, x0, d0[u]);
+                x1 = fmaf(gdec, x1, d1[u]);
+                if (rotates) rotate_pair(a.seg_span[slot], j, m, x0, x1);
+                origin = reduce_clock(origin + a.seg_span[slot], m);
+            }
         }
     }
 }
 
-// ---- 3. fused chunk forward ----------------------------------------------------
+// ---- 3. fused chunk forward, 32-token chunks ------------------------------------
+// (64-token chunks run the eight-wave kernel of cyfa_fwd_w8.hip.)  Two
+// workgroups share a compute unit; the readout matrix operands come from L2.
 template <int CC>
-__global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
+    static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
     using Ly = Lay<CC>;
     constexpr int RB = Ly::RB;
     constexpr int SSC = Ly::SSC;
@@ -548,11 +358,9 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
     const float sgn = (icol & 1) ? 1.f : -1.f;
 
     // Per-lane bases: every unrolled LDS access below is base + compile-time offset.
-    // Readout operand rows when the readout matrix is read from L2 (32-token chunks).
+    // Readout operand rows (read from L2).
     const __bf16 *Mzr = a.Mz + ((size_t)h * 128 + icol) * 128 + 8 * hl;
     const __bf16 *Myr = a.My + ((size_t)h * 128 + icol) * 128 + 8 * hl;
-    const __bf16 *Mza = s.Mt + icol * QS + 8 * hl;                        // M rows (LDS)
-    const __bf16 *Myt = tr_base(s.Mt, QS, lane) + 32 * w;                 // M columns (LDS)
     const float zs = p.scale * 1.4426950408889634f;                       // logits in log2 units
     const float *gam_l = s.gam + h4;                                      // accumulator rows
     const half2v *CS_l = s.CS + h4 * 64 + (icol >> 1);
@@ -567,17 +375,6 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
     const __bf16 *Adt = tr_base(s.Ads, QS, lane);
     const __bf16 *Kt = tr_base(s.Ks, QS, lane);
 
-    if (Ly::kMInLds) {
-        // readout matrix M_h (slot rows, internal basis columns), resident for the whole segment
-        const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
-#pragma unroll
-        for (int it = 0; it < 8; ++it) {
-            const int e = it * NT + tid;
-            const int row = e >> 4, c0 = (e & 15) * 8;
-            *reinterpret_cast<uint4 *>(s.Mt + row * QS + c0) =
-                *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
-        }
-    }
     f32x16 kacc[4], vacc[4];
     float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
     if (a.has_init) {
@@ -591,24 +388,18 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
     }
     double carry = 0.0, gsum = 0.0;
     float logf = 0.f;                                // carried states are exp(logf) x registers
-    // With one workgroup per compute unit (64-token chunks) the next chunk is
-    // prefetched into registers during the current one; with two workgroups
-    // per unit (32-token chunks) the other workgroup covers the load latency
-    // and the registers are needed elsewhere.
-    constexpr bool kPrefetch = CC == 64;
+    // The other workgroup on the compute unit covers the load latency.
     Prefetch<CC> pf;
-    if (kPrefetch) load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
         const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes
-        if (!kPrefetch) load_chunk<CC, true>(p, b, h, t0, tid, pf);
+        load_chunk<CC, true>(p, b, h, t0, tid, pf);
         store_chunk<CC, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
-        if (kPrefetch && c + 1 < c_end) load_chunk<CC, true>(p, b, h, (c + 1) * CC, tid, pf);
         build_writes<CC, true>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
@@ -670,13 +461,11 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) zacc[nb] = zero_acc();
             bf16x8 mz[8];
-            if (!Ly::kMInLds) {
 #pragma unroll
-                for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
-            }
+            for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 ma = Ly::kMInLds ? lds8(Mza + 16 * ks) : mz[ks];
+                const bf16x8 ma = mz[ks];
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     zacc[nb] = mma(ma, lds8(Xa + 32 * nb * QS + 16 * ks), zacc[nb]);
@@ -744,13 +533,11 @@ __global__ __launch_bounds__(NT, (CC == 32 ? 2 : 1)) void chunk_forward_kernel(M
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) yacc[nb] = zero_acc();
             bf16x8 my[8];
-            if (!Ly::kMInLds) {
 #pragma unroll
-                for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
-            }
+            for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 mt = Ly::kMInLds ? lds8_tr(Myt + 16 * ks * QS, QS) : my[ks];
+                const bf16x8 mt = my[ks];
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     yacc[nb] = mma(mt, lds8(Xa + 32 * nb * QS + 16 * ks), yacc[nb]);
@@ -892,7 +679,7 @@ __global__ __launch_bounds__(NT) void readout_pack_kernel(int m, const float *__
 }  // namespace
 
 // ---- host side --------------------------------------------------------------
-constexpr int kMfmaDefaultChunk = 32;
+constexpr int kMfmaDefaultChunk = 64;
 
 bool mfma_supported(const FwdParams &p) {
     return p.dtype == 1 && p.dk == 128 && p.dv == 128 && (p.chunk == 32 || p.chunk == 64);
@@ -941,8 +728,12 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
     }
     if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
     if (a.nchunks > 0) {
-        hipLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if constexpr (CC == 64) {
+            if ((e = launch_chunk64_w8(a, BH * a.P, st)) != hipSuccess) return e;
+        } else {
+            hipLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
     if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
     return hipSuccess;

@@ -1,0 +1,223 @@
+// Pieces shared by the matrix-core forward kernels: kernel arguments, the LDS
+// tile set, staging of one chunk (global -> registers -> LDS), the chunk-local
+// prefix sums and the temporal write matrix.  NTH is the workgroup size.
+#pragma once
+
+#include "cyfa_mfma_common.h"
+
+namespace cyfa {
+
+struct MfmaArgs {
+    FwdParams p;
+    int P;               // segments per (b, h)
+    int cps;             // chunks per segment
+    int nchunks;         // chunks per sequence
+    int chunk;           // chunk length (32 or 64)
+    const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j
+    const __bf16 *My;    // [H][128][128]  row = internal basis j, column = slot i'
+    float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
+    double *seg_span;    // [B*H*P] clock span of each segment (reduced mod m)
+    double *seg_gsum;    // [B*H*P] sum of log alpha over each segment
+    double *seg_origin;  // [B*H*P] absolute clock at each segment start (reduced)
+    double *final_lam;   // [B*H] local clock after the last segment (reduced)
+    int has_init;        // segment-entry states are read from seg_state
+    int want_final;      // last segment dumps its final state into seg_state
+};
+
+// fused forward for 64-token chunks on eight waves (one workgroup per (b, h, p))
+hipError_t launch_chunk64_w8(const MfmaArgs &a, int groups, hipStream_t st);
+
+namespace mfma {
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+
+struct Tiles {
+    __bf16 *Qs, *Ks, *Vs, *As, *Ads, *Ss, *Xs, *Ws, *Os, *Stage, *Mt;
+    float2 *red;
+    half2v *CS;
+    float *Gs;      // chunk-local prefix sums of log alpha
+    float *gam;     // row scale of the inter-chunk terms: exp(G_r + L)
+    float *betas;
+    float *decw;    // multiplier of A_dec rows
+    double *urev;   // clock at each row reduced mod m, divided by m (revolutions)
+    float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
+};
+
+__device__ __forceinline__ void scalars_at(Tiles &t, char *base) {
+    t.Gs = reinterpret_cast<float *>(base);
+    t.gam = t.Gs + 64;
+    t.betas = t.gam + 64;
+    t.decw = t.betas + 64;
+    t.urev = reinterpret_cast<double *>(t.decw + 64);
+    t.ctl = reinterpret_cast<float *>(t.urev + 64);
+}
+
+// Global -> register prefetch of one chunk: CC NTH/16 x 16-byte pieces per thread
+// per tensor (rows (NTH/16) it + tid / 16, columns 8 (tid % 16)), plus one
+// token's scalars on the first CC lanes.
+template <int CC, int NTH = NT>
+struct Prefetch {
+    static constexpr int kIt = CC * 16 / NTH;
+    uint4 q[kIt], k[kIt], v[kIt];
+    float g, dl, be;
+};
+
+template <int CC, bool kWithQ, int NTH = NT>
+__device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int tid,
+                                           Prefetch<CC, NTH> &pf) {
+    constexpr int kRows = NTH / 16;                  // rows per pass
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    const __bf16 *q = static_cast<const __bf16 *>(p.q);
+    const __bf16 *k = static_cast<const __bf16 *>(p.k);
+    const __bf16 *v = static_cast<const __bf16 *>(p.v);
+    const int r0 = tid >> 4, d0 = (tid & 15) * 8;
+    const size_t row_stride = (size_t)p.H * D;
+    const size_t base = (((size_t)b * p.T + t0 + r0) * p.H + h) * D + d0;
+#pragma unroll
+    for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
+        const int t = t0 + r0 + kRows * it;
+        const size_t off = base + (size_t)(kRows * it) * row_stride;
+        if (t < p.T) {
+            if (kWithQ) pf.q[it] = *reinterpret_cast<const uint4 *>(q + off);
+            pf.k[it] = *reinterpret_cast<const uint4 *>(k + off);
+            pf.v[it] = *reinterpret_cast<const uint4 *>(v + off);
+        } else {
+            if (kWithQ) pf.q[it] = zero;
+            pf.k[it] = zero;
+            pf.v[it] = zero;
+        }
+    }
+    if (tid < 64) {
+        const int t = t0 + tid;
+        if (tid < CC && t < p.T) {
+            const size_t si = ((size_t)b * p.T + t) * p.H + h;
+            pf.dl = p.delta[si];
+            pf.g = p.log_alpha ? p.log_alpha[si] : 0.f;
+            pf.be = p.beta ? p.beta[si] : 1.f;
+        } else {
+            pf.dl = 0.f;   // rows past the chunk or the sequence: no shift, no decay, no write
+            pf.g = 0.f;
+            pf.be = 0.f;
+        }
+    }
+}
+
+// Registers -> LDS, row-major tiles.
+template <int CC, bool kWithQ, int NTH = NT>
+__device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefetch<CC, NTH> &pf) {
+    constexpr int kRows = NTH / 16;
+    const int off = (tid >> 4) * QS + (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
+        if (kWithQ) *reinterpret_cast<uint4 *>(s.Qs + off + kRows * it * QS) = pf.q[it];
+        *reinterpret_cast<uint4 *>(s.Ks + off + kRows * it * QS) = pf.k[it];
+        *reinterpret_cast<uint4 *>(s.Vs + off + kRows * it * QS) = pf.v[it];
+    }
+}
+
+// Wave 0: chunk-local inclusive prefix sums of log alpha (float) and of the
+// clock increments (double, continuing the carried clock), reduced mod m.
+// Lanes past the chunk hold zeros, so entry 63 equals the chunk total.
+//
+// Carried states are kept as Kbar = exp(L) Kt (same L for Vbar).  Normally a
+// chunk only adds to Kt: Kt += K^T (A exp(-G_r - L)) and L += G_C, which is
+// Kbar <- gamma^C Kbar + K^T (A gamma^C / gamma^r) (App. B, Eq. app-scalar-chunk)
+// without touching the state registers.  When exp(+-(G_r + L)) could leave
+// [e^-60, e^60] the chunk instead rescales Kt by exp(L + G_C), uses
+// A gamma^C / gamma^r and restarts L at 0.
+template <int CC, int NTH = NT>
+__device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC, NTH> &pf,
+                                            double &carry, double &gsum, float &L) {
+    const float G = wave_incl_scan(pf.g);
+    const double lam = carry + wave_incl_scan((double)pf.dl);
+    const float GC = lane63(G);
+    const float gabs = wave_max_nonneg(fabsf(G));
+    const bool lazy = fabsf(L) + gabs <= 60.f;
+    s.Gs[lane] = G;
+    s.gam[lane] = __expf(G + L);
+    s.decw[lane] = lazy ? __expf(-G - L) : __expf(GC - G);
+    s.betas[lane] = pf.be;
+    s.urev[lane] = reduce_clock(lam, m) / (double)m;
+    const float state_factor = lazy ? 1.f : __expf(L + GC);
+    L = lazy ? L + GC : 0.f;
+    if (lane == 0) {
+        s.ctl[0] = state_factor;
+        s.ctl[1] = L;
+    }
+    const double last = lane63(lam);
+    carry = reduce_clock(last, m);
+    gsum += (double)GC;
+}
+
+// Temporal write matrix for the chunk (Eq. app-temporal-writes):
+// A_r = beta_r U(-lambda_r) b, i.e. beta_r [sqrt(2/m) cos th_j, -sqrt(2/m) sin th_j]
+// on pair j and beta_r / sqrt(m) on DC, th_j = 2 pi j lambda_r / m.  The copy
+// A_dec has row r scaled by gamma^C / gamma^r (right rescaling, Eq. app-chunk-rescale).
+// Thread (r = tid / TPR, q = tid % TPR) fills internal columns NCOL q .. NCOL q + NCOL-1
+// of row r; the last quarter also holds DC (column 126) and padding (127).  The
+// phases advance by angle addition from an accurately reduced start.
+template <int CC, bool kFull, int NTH = NT>
+__device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
+    constexpr int TPR = NTH / CC;         // threads per row
+    constexpr int NCOL = 128 / TPR;       // columns per thread
+    constexpr int NP = NCOL / 2;          // pairs per thread
+    const int r = tid / TPR, q = tid % TPR;
+    const int J = (m - 1) >> 1;
+    const float dc = 1.0f / sqrtf((float)m);
+    const float ac = sqrtf(2.0f / (float)m);
+    const float be = s.betas[r];
+    const float wdec = s.decw[r];
+    const double u = s.urev[r];                      // revolutions per unit frequency
+    float s1, c1, sn, cs;
+    sincos_rev((float)u, &s1, &c1);
+    {
+        double rev = (double)(NP * q + 1) * u;
+        rev -= floor(rev);
+        sincos_rev((float)rev, &sn, &cs);
+    }
+    float av[NCOL];
+    half8v csv[NP / 4];
+#pragma unroll
+    for (int jj = 0; jj < NP; ++jj) {
+        const int j = NP * q + 1 + jj;
+        const bool live = j <= J && j <= 63;
+        const float cv = live ? cs : 0.f;
+        const float sv = live ? sn : 0.f;
+        av[2 * jj] = be * ac * cv;
+        av[2 * jj + 1] = -be * ac * sv;
+        // table entry 63 (internal columns 126, 127: DC and padding) is (1, 0),
+        // so the token-wise rotations pass those columns through unchanged
+        csv[jj >> 2][2 * (jj & 3)] = (_Float16)(j == 64 ? 1.f : cv);
+        csv[jj >> 2][2 * (jj & 3) + 1] = (_Float16)sv;
+        const float nc = cs * c1 - sn * s1;
+        const float ns = sn * c1 + cs * s1;
+        cs = nc;
+        sn = ns;
+    }
+    if (q == TPR - 1) {    // internal columns 126 (DC) and 127 (padding)
+        av[NCOL - 2] = be * dc;
+        av[NCOL - 1] = 0.f;
+    }
+    __bf16 *arow = s.As + r * QS + NCOL * q;
+    __bf16 *adrow = s.Ads + r * QS + NCOL * q;
+#pragma unroll
+    for (int k8 = 0; k8 < NCOL / 8; ++k8) {
+        bf16x8 a8, ad8;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            a8[k] = (__bf16)av[8 * k8 + k];
+            ad8[k] = (__bf16)(av[8 * k8 + k] * wdec);
+        }
+        if (kFull) *reinterpret_cast<bf16x8 *>(arow + 8 * k8) = a8;
+        *reinterpret_cast<bf16x8 *>(adrow + 8 * k8) = ad8;
+    }
+    if (kFull) {
+        half8v *csrow = reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q);
+#pragma unroll
+        for (int k4 = 0; k4 < NP / 4; ++k4) csrow[k4] = csv[k4];
+    }
+}
+
+}  // namespace mfma
+}  // namespace cyfa

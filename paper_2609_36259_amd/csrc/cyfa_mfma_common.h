@@ -155,21 +155,64 @@ __device__ __forceinline__ float swap_quads8(float x) {
 }
 
 // ---- chunk-local prefix sums on one wave (lane = token row) --------------
-__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const float y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
+// DPP lane moves (no lane-address registers): row_shr:n within rows of 16 lanes
+// (sources outside the row read 0), then row_bcast:15 / row_bcast:31 carry the
+// row totals into the following rows.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ int dpp0(int x) {
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, true);
+}
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ float dppf(float x) {
+    return __int_as_float(dpp0<CTRL, ROWS>(__float_as_int(x)));
+}
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ double dppd(double x) {
+    const unsigned long long v = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)dpp0<CTRL, ROWS>((int)(unsigned)v);
+    const unsigned hi = (unsigned)dpp0<CTRL, ROWS>((int)(unsigned)(v >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+__device__ __forceinline__ float wave_incl_scan(float x) {
+    x += dppf<0x111>(x);
+    x += dppf<0x112>(x);
+    x += dppf<0x114>(x);
+    x += dppf<0x118>(x);
+    x += dppf<0x142, 0xA>(x);
+    x += dppf<0x143, 0xC>(x);
     return x;
 }
-__device__ __forceinline__ double wave_incl_scan(double x, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const double y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
+__device__ __forceinline__ double wave_incl_scan(double x) {
+    x += dppd<0x111>(x);
+    x += dppd<0x112>(x);
+    x += dppd<0x114>(x);
+    x += dppd<0x118>(x);
+    x += dppd<0x142, 0xA>(x);
+    x += dppd<0x143, 0xC>(x);
     return x;
+}
+// maximum over the wave of values >= 0 (0 is the identity of the moves above)
+__device__ __forceinline__ float wave_max_nonneg(float x) {
+    x = fmaxf(x, dppf<0x111>(x));
+    x = fmaxf(x, dppf<0x112>(x));
+    x = fmaxf(x, dppf<0x114>(x));
+    x = fmaxf(x, dppf<0x118>(x));
+    x = fmaxf(x, dppf<0x142, 0xA>(x));
+    x = fmaxf(x, dppf<0x143, 0xC>(x));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+__device__ __forceinline__ float lane63(float x) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+__device__ __forceinline__ double lane63(double x) {
+    const unsigned long long v = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)v, 63);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), 63);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+// value of lane l ^ 16 (ds_swizzle, bitmask mode: and 0x1F, xor 0x10, within 32 lanes)
+__device__ __forceinline__ float swap16(float x) {
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));
 }
 
 // cos / sin of 2 pi * rev (rev in revolutions, |rev| < 256) on the hardware units

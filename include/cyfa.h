@@ -79,7 +79,7 @@ typedef enum {
  *   d_k, d_v     head dims: 64 or 128 each (the matrix-core kernel: 128 only)
  *   m            active slots, odd, 3..127
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
- *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 64).
+ *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 32).
  *                Results do not depend on it beyond rounding (App. B: the
  *                chunk form is exact).
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,

@@ -28,8 +28,11 @@ using namespace mfma;
 namespace {
 
 // ---- LDS maps (bytes) ---------------------------------------------------------
-// Fused kernel: every bf16 tile is row-major [CC][QS]; operands whose k index
-// runs down the rows are read with the transpose read.
+// Fused kernel (32-token chunks): every bf16 tile is row-major [CC][QS];
+// operands whose k index runs down the rows are read with the transpose read.
+// Two workgroups share a compute unit, so the map stays within half of its
+// 160 KiB: there is no A_dec tile (its row scale is applied to the other
+// operand of each state update) and the softmax partials share the score tile.
 template <int CC>
 struct Lay {
     static constexpr int RB = CC / 32;                 // 32-row blocks per tile
@@ -38,18 +41,18 @@ struct Lay {
     static constexpr int Q = 0;                        // Q   -> X -> W
     static constexpr int K = Q + TILE;                 // K   -> O''
     static constexpr int V = K + TILE;                 // V
-    static constexpr int A = V + TILE;                 // A   (temporal writes) -> output staging
-    static constexpr int AD = A + TILE;                // A, rows right-decayed to the chunk end
-    static constexpr int S = AD + TILE;                // scores [CC][SSC] bf16
-    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs
-    static constexpr int RED = CS + CC * 64 * 4;       // softmax (max, sum) per wave x row
-    static constexpr int SC = RED + 4 * CC * 8;        // per-token scalars (64 entries each)
-    static constexpr int SCB = 64 * (4 + 4 + 4 + 4 + 8) + 16;   // scalar block bytes
-    static constexpr int BYTES = SC + SCB;
-    // state pre-pass: K, V, A_dec and the scalars
+    static constexpr int A = V + TILE;                 // A   (temporal writes)
+    static constexpr int S = A + TILE;                 // scores [CC][SSC] bf16 / softmax partials
+    static constexpr int RED = S;                      // (max, sum) per wave x row, middle step only
+    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs -> output staging
+    static constexpr int MT = CS + CC * 64 * 4;        // readout matrix [128][QS] bf16
+    static constexpr int SC = MT + 128 * QS * 2;       // per-token scalars (CC entries each)
+    static constexpr int BYTES = SC + scalar_bytes(CC);
+    static_assert(4 * CC * 8 <= CC * SSC * 2, "softmax partials fit the score tile");
+    static_assert(CC != 32 || BYTES <= 80 * 1024, "two workgroups per compute unit");
+    // state pre-pass: K, V, A_dec and the scalars (64 entries)
     static constexpr int PK = 0, PV = TILE, PAD = 2 * TILE, PSC = 3 * TILE;
-    static constexpr int PBYTES = PSC + SCB;
-    static_assert(BYTES <= 160 * 1024, "LDS budget");
+    static constexpr int PBYTES = PSC + scalar_bytes(64);
 };
 
 template <int CC>
@@ -63,12 +66,13 @@ __device__ __forceinline__ Tiles fused_tiles(char *smem) {
     t.Os = t.Ks;
     t.Vs = reinterpret_cast<__bf16 *>(smem + L::V);
     t.As = reinterpret_cast<__bf16 *>(smem + L::A);
-    t.Ads = reinterpret_cast<__bf16 *>(smem + L::AD);
+    t.Ads = nullptr;
     t.Ss = reinterpret_cast<__bf16 *>(smem + L::S);
     t.CS = reinterpret_cast<half2v *>(smem + L::CS);
+    t.Mt = reinterpret_cast<__bf16 *>(smem + L::MT);
     t.red = reinterpret_cast<float2 *>(smem + L::RED);
-    t.Stage = t.As;
-    scalars_at(t, smem + L::SC);
+    t.Stage = reinterpret_cast<__bf16 *>(smem + L::CS);
+    scalars_at(t, smem + L::SC, CC);
     return t;
 }
 
@@ -215,7 +219,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
         if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
-        build_writes<CC, false>(s, tid, a.p.m);
+        build_writes<CC, false, true>(s, tid, a.p.m);
         __syncthreads();
         update_states<CC>(s, w, lane, kacc, vacc);
         __syncthreads();
@@ -268,8 +272,14 @@ __device__ __forceinline__ PairRef pair_ref(int gidx) {
 }
 
 // (x0, x1) <- U(tau) (x0, x1) for the pair at internal indices (2j-2, 2j-1)
-__device__ __forceinline__ void rotate_pair(double tau, int j, int m, float &x0, float &x1) {
-    double rev = (double)j * reduce_clock(tau, m) / (double)m;
+// u: the rotation angle tau in revolutions of the m-slot ring, tau / m mod 1
+// (same for every pair, so computed once by the caller)
+__device__ __forceinline__ double ring_rev(double tau, int m) {
+    const double inv_m = 1.0 / (double)m;
+    return reduce_clock(tau, (double)m, inv_m) * inv_m;
+}
+__device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x1) {
+    double rev = (double)j * u;
     rev -= floor(rev);
     float sn, cs;
     sincos_rev((float)rev, &sn, &cs);
@@ -295,8 +305,9 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
         x0 = p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
         x1 = p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
     }
-    if (rotates) rotate_pair(c0, j, m, x0, x1);   // initial state in the frame with origin clock0
-    double origin = reduce_clock(c0, m);
+    if (rotates) rotate_pair(ring_rev(c0, m), j, x0, x1);   // initial state in the frame with origin clock0
+    const double inv_m = 1.0 / (double)m;
+    double origin = reduce_clock(c0, (double)m, inv_m);
     // Segment contributions are fetched kBatch segments at a time, ahead of the
     // dependent chain through them.  Every thread owns the same two offsets in
     // every segment, so the loads of a batch never see this batch's stores.
@@ -324,19 +335,34 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
             st[pr.o0] = x0;
             st[pr.o1] = x1;
             if (q < a.P - 1) {
-                const float gdec = (float)exp(a.seg_gsum[slot]);
+                const float gdec = __expf((float)a.seg_gsum[slot]);
                 x0 = fmaf(gdec, x0, d0[u]);
                 x1 = fmaf(gdec, x1, d1[u]);
-                if (rotates) rotate_pair(a.seg_span[slot], j, m, x0, x1);
-                origin = reduce_clock(origin + a.seg_span[slot], m);
+                const double span = a.seg_span[slot];
+                if (rotates) rotate_pair(span * inv_m, j, x0, x1);   // span is already reduced to [0, m)
+                origin = reduce_clock(origin + span, (double)m, inv_m);
             }
         }
     }
 }
 
+// Transposed operand whose k index is the token s = 16 ks + 8 hl + p, times the
+// right-decay factor of that token (the A_dec row scale, Eq. app-chunk-rescale);
+// dw points at decw[16 ks + 8 hl].
+__device__ __forceinline__ bf16x8 decay_rows(bf16x8 v, const float *dw) {
+    const float4 d0 = *reinterpret_cast<const float4 *>(dw);
+    const float4 d1 = *reinterpret_cast<const float4 *>(dw + 4);
+    const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    bf16x8 r;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = (__bf16)((float)v[q] * d[q]);
+    return r;
+}
+
 // ---- 3. fused chunk forward, 32-token chunks ------------------------------------
 // (64-token chunks run the eight-wave kernel of cyfa_fwd_w8.hip.)  Two
-// workgroups share a compute unit; the readout matrix operands come from L2.
+// workgroups share a compute unit; the readout matrix sits in LDS and the next
+// chunk is prefetched into registers.
 template <int CC>
 __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
@@ -357,24 +383,47 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     // lane, c x + s x' on the sin lane
     const float sgn = (icol & 1) ? 1.f : -1.f;
 
-    // Per-lane bases: every unrolled LDS access below is base + compile-time offset.
-    // Readout operand rows (read from L2).
-    const __bf16 *Mzr = a.Mz + ((size_t)h * 128 + icol) * 128 + 8 * hl;
-    const __bf16 *Myr = a.My + ((size_t)h * 128 + icol) * 128 + 8 * hl;
     const float zs = p.scale * 1.4426950408889634f;                       // logits in log2 units
-    const float *gam_l = s.gam + h4;                                      // accumulator rows
-    const half2v *CS_l = s.CS + h4 * 64 + (icol >> 1);
-    __bf16 *X_l = s.Xs + h4 * QS + icol;                                  // X (then W) tile
-    __bf16 *St_l = s.Stage + h4 * QS + icol;                              // output staging
-    const __bf16 *Qperm = s.Qs + l32 * QS + h4;                           // permuted-k A operands
-    const __bf16 *Operm = s.Os + l32 * QS + h4;
-    const __bf16 *Xa = s.Xs + l32 * QS + 8 * hl;                          // natural-k A operands
-    const __bf16 *Sa = s.Ss + l32 * SSC + 8 * hl;
-    const __bf16 *At = tr_base(s.As, QS, lane) + 32 * w;                  // transposed B operands
-    const __bf16 *Vt = tr_base(s.Vs, QS, lane) + 32 * w;
-    const __bf16 *Adt = tr_base(s.Ads, QS, lane);
-    const __bf16 *Kt = tr_base(s.Ks, QS, lane);
+    // Per-lane bases (opaque byte offsets): every unrolled LDS access below is one
+    // of these plus a compile-time offset.
+    constexpr int TE = Ly::TILE / 2;                                      // tile size in elements
+    const int trl = tr_off(QS, lane);
+    const float *gam_l = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + h4)));           // gam, accumulator rows
+    const float *dw_l = lds_at<float>(smem, opq(Ly::SC + 4 * (3 * CC + 8 * hl)));    // decw, operand tokens
+    const __bf16 *Mza = lds_at<__bf16>(smem, opq(Ly::MT + 2 * (icol * QS + 8 * hl)));  // M rows
+    const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + 2 * (trl + 32 * w)));         // M columns
+    const half2v *CS_l = lds_at<half2v>(smem, opq(Ly::CS + 4 * (h4 * 64 + (icol >> 1))));
+    __bf16 *X_l = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (h4 * QS + icol)));           // X (then W) tile
+    // output staging: [CC][128] bf16 in the (cos, sin) table, which is free from the
+    // O'' rotation until the next chunk's temporal writes
+    __bf16 *St_l = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (h4 * 128 + icol)));
+    const __bf16 *Qperm = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + h4)));   // permuted-k A operands
+    const __bf16 *Operm = Qperm + TE;
+    const __bf16 *Xa = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 8 * hl)));  // natural-k operands
+    const __bf16 *Sa = lds_at<__bf16>(smem, opq(Ly::S + 2 * (l32 * SSC + 8 * hl)));
+    const __bf16 *At = lds_at<__bf16>(smem, opq(Ly::A + 2 * (trl + 32 * w)));       // transposed operands
+    const __bf16 *Vt = lds_at<__bf16>(smem, opq(Ly::V + 2 * (trl + 32 * w)));
+    const __bf16 *Atx = lds_at<__bf16>(smem, opq(Ly::A + 2 * trl));
+    const __bf16 *Kt = lds_at<__bf16>(smem, opq(Ly::K + 2 * trl));
+    // token-row bases of the readout step: row l32 (+ 32 nb), columns 32w + 4hl ..
+    __bf16 *Wrow = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 32 * w + h4)));
+    __bf16 *O2row = Wrow + TE;
+    const half2v *CSrow = lds_at<half2v>(smem, opq(Ly::CS + 4 * (l32 * 64 + 16 * w + 2 * hl)));
+    float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
+    const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
+    const __bf16 *Stg = lds_at<__bf16>(smem, opq(Ly::CS + 2 * ((tid >> 4) * 128 + (tid & 15) * 8)));
 
+    {
+        // readout matrix M_h (slot rows, internal basis columns), resident for the segment
+        const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int e = it * NT + tid;
+            const int row = e >> 4, c0 = (e & 15) * 8;
+            *reinterpret_cast<uint4 *>(s.Mt + row * QS + c0) =
+                *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
+        }
+    }
     f32x16 kacc[4], vacc[4];
     float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
     if (a.has_init) {
@@ -388,19 +437,19 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     }
     double carry = 0.0, gsum = 0.0;
     float logf = 0.f;                                // carried states are exp(logf) x registers
-    // The other workgroup on the compute unit covers the load latency.
     Prefetch<CC> pf;
+    load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
         const int n = min(CC, p.T - t0);
-        // -- A: stage the chunk, prefix sums, temporal writes
-        load_chunk<CC, true>(p, b, h, t0, tid, pf);
+        // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true>(s, tid, pf);
-        if (w == 0) chunk_scans<CC>(s, lane, m, pf, carry, gsum, logf);
+        if (w == 0) chunk_scans<CC, NT, CC>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
-        build_writes<CC, true>(s, tid, m);
+        if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
+        build_writes<CC, true, false>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
         score_tiles<CC>(s, s.Qs, s.Ks, w, lane);
@@ -436,7 +485,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 ad_w = lds8_tr(Adt + 16 * ks * QS + 32 * w, QS);
+                const bf16x8 ad_w = decay_rows(lds8_tr(At + 16 * ks * QS, QS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
                     kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
@@ -460,12 +509,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         {
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) zacc[nb] = zero_acc();
-            bf16x8 mz[8];
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) mz[ks] = *reinterpret_cast<const bf16x8 *>(Mzr + 16 * ks);
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 ma = mz[ks];
+                const bf16x8 ma = lds8(Mza + 16 * ks);
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     zacc[nb] = mma(ma, lds8(Xa + 32 * nb * QS + 16 * ks), zacc[nb]);
@@ -491,7 +537,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             for (int v = 0; v < 16; ++v) sm += __builtin_amdgcn_exp2f(zacc[nb][v] - mref);
             sm += __shfl_xor(sm, 32);
             const int r = 32 * nb + l32;
-            if (hl == 0) s.red[w * CC + r] = make_float2(mx, sm);
+            if (hl == 0) redw[32 * nb] = make_float2(mx, sm);
             if (p.logits && r < n) {
                 // the logit accumulators hold log2(e) z; report z
                 float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m;
@@ -508,13 +554,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             const int r = 32 * nb + l32;
             float2 pr[4];
 #pragma unroll
-            for (int x = 0; x < 4; ++x) pr[x] = s.red[x * CC + r];
+            for (int x = 0; x < 4; ++x) pr[x] = redr[x * CC + 32 * nb];
             const float M = fmaxf(fmaxf(pr[0].x, pr[1].x), fmaxf(pr[2].x, pr[3].x));
             float Lsum = 0.f;
 #pragma unroll
             for (int x = 0; x < 4; ++x) Lsum += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
             const float inv = 1.f / Lsum;
-            __bf16 *wrow = s.Ws + r * QS + 32 * w + h4;
+            __bf16 *wrow = Wrow + 32 * nb * QS;
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4) {
                 bf16x4 wv;
@@ -532,12 +578,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             f32x16 yacc[RB];
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) yacc[nb] = zero_acc();
-            bf16x8 my[8];
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) my[ks] = *reinterpret_cast<const bf16x8 *>(Myr + 16 * ks);
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 mt = my[ks];
+                const bf16x8 mt = lds8_tr(Myt + 16 * ks * QS, QS);
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     yacc[nb] = mma(mt, lds8(Xa + 32 * nb * QS + 16 * ks), yacc[nb]);
@@ -545,8 +588,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) {
                 const int r = 32 * nb + l32;
-                const half2v *csr = s.CS + r * 64 + 16 * w + 2 * hl;
-                __bf16 *orow = s.Os + r * QS + 32 * w + h4;
+                const half2v *csr = CSrow + 32 * nb * 64;
+                __bf16 *orow = O2row + 32 * nb * QS;
 #pragma unroll
                 for (int v4 = 0; v4 < 4; ++v4) {
                     bf16x4 ov;
@@ -586,11 +629,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             for (int ks = 0; ks < 2 * (rb + 1); ++ks)
                 pacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(Vt + 16 * ks * QS, QS),
                                pacc[rb]);
-        // output tile -> staging (the logit tile is dead) for 16-byte global stores
+        // output tile -> staging for 16-byte global stores
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
+            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * 128] = (__bf16)pacc[rb][v];
         {
             // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
             const float sf = s.ctl[0];
@@ -602,10 +645,10 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 v_w = lds8_tr(Vt + 16 * ks * QS, QS);
+                const bf16x8 v_w = decay_rows(lds8_tr(Vt + 16 * ks * QS, QS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
-                    vacc[x] = mma(lds8_tr(Adt + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
+                    vacc[x] = mma(lds8_tr(Atx + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
             }
         }
         __syncthreads();
@@ -616,7 +659,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 const int r = r0 + 16 * it;
                 if (r < n)
                     *reinterpret_cast<uint4 *>(o + (((size_t)b * p.T + t0 + r) * p.H + h) * D + d0) =
-                        *reinterpret_cast<const uint4 *>(s.Stage + r * QS + d0);
+                        *reinterpret_cast<const uint4 *>(Stg + 16 * it * 128);
             }
         }
     }
@@ -640,7 +683,7 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     const double origin = a.seg_origin[slot];
     float x0 = st[pr.o0], x1 = st[pr.o1];
     // local frame (origin at the last segment's start) -> absolute clock: U(-origin)
-    if (pr.i0 < kDC && j <= (m - 1) / 2) rotate_pair(-origin, j, m, x0, x1);
+    if (pr.i0 < kDC && j <= (m - 1) / 2) rotate_pair(ring_rev(-origin, m), j, x0, x1);
     float *out = pr.value ? a.p.V_out : a.p.K_out;
     if (out) {
         const size_t base = (size_t)bh * 128 * 128 + pr.col;
@@ -679,7 +722,7 @@ __global__ __launch_bounds__(NT) void readout_pack_kernel(int m, const float *__
 }  // namespace
 
 // ---- host side --------------------------------------------------------------
-constexpr int kMfmaDefaultChunk = 64;
+constexpr int kMfmaDefaultChunk = 32;
 
 bool mfma_supported(const FwdParams &p) {
     return p.dtype == 1 && p.dk == 128 && p.dv == 128 && (p.chunk == 32 || p.chunk == 64);

@@ -41,19 +41,6 @@ struct LayW8 {
     static_assert(BYTES <= 160 * 1024, "LDS budget");
 };
 
-// A lane's LDS byte offset, opaque to the compiler: accesses written as
-// smem + offset + constant then keep one base register per access pattern
-// (the constant folds into the instruction) instead of one register per
-// (tile, row) combination held across the chunk loop.
-__device__ __forceinline__ int opq(int x) {
-    asm volatile("" : "+v"(x));
-    return x;
-}
-template <typename T>
-__device__ __forceinline__ T *lds_at(char *smem, int byte_off) {
-    return reinterpret_cast<T *>(smem + byte_off);
-}
-
 // Lane offset (elements) for transposed 16x16x32 operands from a row-major tile:
 // with base = tile + tr16_off, the operand element (n = l16, k = 8g + p) of the
 // tile block at (k0, n0) is lds8_tr(base + k0 * stride + n0, stride), i.e.
@@ -245,7 +232,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
         if (w == 0) chunk_scans<CK, W8>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CK, true, W8>(p, b, h, t0 + CK, tid, pf);
-        build_writes<CK, true, W8>(s, tid, m);
+        build_writes<CK, true, true, W8>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
         score_tiles16(s, Qn, Kn, Sw, w, lane);

@@ -64,6 +64,13 @@ __device__ __forceinline__ double reduce_clock(double lam, int m) {
     double r = lam - (double)m * floor(lam / (double)m);
     return (r >= (double)m) ? r - (double)m : r;
 }
+// Same with a multiply by inv_m = 1/m in place of the division: the quotient
+// may round across an integer, which the two-sided correction undoes.
+__device__ __forceinline__ double reduce_clock(double lam, double m, double inv_m) {
+    double r = lam - m * floor(lam * inv_m);
+    r = (r >= m) ? r - m : r;
+    return (r < 0.0) ? r + m : r;
+}
 
 // cos and sin of theta_j = 2 pi j lam / m for a clock already reduced to
 // [0, m).  The angle is reduced in revolutions in double precision first, so

@@ -44,14 +44,16 @@ struct Tiles {
     float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
 };
 
-__device__ __forceinline__ void scalars_at(Tiles &t, char *base) {
+// n entries per array (the chunk length or 64); block size scalar_bytes(n)
+__device__ __forceinline__ void scalars_at(Tiles &t, char *base, int n = 64) {
     t.Gs = reinterpret_cast<float *>(base);
-    t.gam = t.Gs + 64;
-    t.betas = t.gam + 64;
-    t.decw = t.betas + 64;
-    t.urev = reinterpret_cast<double *>(t.decw + 64);
-    t.ctl = reinterpret_cast<float *>(t.urev + 64);
+    t.gam = t.Gs + n;
+    t.betas = t.gam + n;
+    t.decw = t.betas + n;
+    t.urev = reinterpret_cast<double *>(t.decw + n);
+    t.ctl = reinterpret_cast<float *>(t.urev + n);
 }
+__host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 8) + 16; }
 
 // Global -> register prefetch of one chunk: CC NTH/16 x 16-byte pieces per thread
 // per tensor (rows (NTH/16) it + tid / 16, columns 8 (tid % 16)), plus one
@@ -126,19 +128,25 @@ __device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefe
 // without touching the state registers.  When exp(+-(G_r + L)) could leave
 // [e^-60, e^60] the chunk instead rescales Kt by exp(L + G_C), uses
 // A gamma^C / gamma^r and restarts L at 0.
-template <int CC, int NTH = NT>
+// NSC: entries of the scalar arrays (lanes >= NSC hold no token and write nothing)
+template <int CC, int NTH = NT, int NSC = 64>
 __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC, NTH> &pf,
                                             double &carry, double &gsum, float &L) {
+    const double inv_m = 1.0 / (double)m;
     const float G = wave_incl_scan(pf.g);
     const double lam = carry + wave_incl_scan((double)pf.dl);
     const float GC = lane63(G);
     const float gabs = wave_max_nonneg(fabsf(G));
     const bool lazy = fabsf(L) + gabs <= 60.f;
-    s.Gs[lane] = G;
-    s.gam[lane] = __expf(G + L);
-    s.decw[lane] = lazy ? __expf(-G - L) : __expf(GC - G);
-    s.betas[lane] = pf.be;
-    s.urev[lane] = reduce_clock(lam, m) / (double)m;
+    if (lane < NSC) {
+        const int ol = opq(lane);                   // one address register for the five writes
+        s.Gs[ol] = G;
+        s.gam[ol] = __expf(G + L);
+        s.decw[ol] = lazy ? __expf(-G - L) : __expf(GC - G);
+        s.betas[ol] = pf.be;
+        const double q = lam * inv_m;               // clock in revolutions of the m-slot ring
+        s.urev[ol] = q - floor(q);
+    }
     const float state_factor = lazy ? 1.f : __expf(L + GC);
     L = lazy ? L + GC : 0.f;
     if (lane == 0) {
@@ -146,7 +154,7 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
         s.ctl[1] = L;
     }
     const double last = lane63(lam);
-    carry = reduce_clock(last, m);
+    carry = reduce_clock(last, (double)m, inv_m);
     gsum += (double)GC;
 }
 
@@ -154,19 +162,20 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
 // A_r = beta_r U(-lambda_r) b, i.e. beta_r [sqrt(2/m) cos th_j, -sqrt(2/m) sin th_j]
 // on pair j and beta_r / sqrt(m) on DC, th_j = 2 pi j lambda_r / m.  The copy
 // A_dec has row r scaled by gamma^C / gamma^r (right rescaling, Eq. app-chunk-rescale).
+// kA: write A and the (cos, sin) table; kAd: write A_dec.
 // Thread (r = tid / TPR, q = tid % TPR) fills internal columns NCOL q .. NCOL q + NCOL-1
 // of row r; the last quarter also holds DC (column 126) and padding (127).  The
 // phases advance by angle addition from an accurately reduced start.
-template <int CC, bool kFull, int NTH = NT>
+template <int CC, bool kA, bool kAd, int NTH = NT>
 __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
     constexpr int TPR = NTH / CC;         // threads per row
     constexpr int NCOL = 128 / TPR;       // columns per thread
     constexpr int NP = NCOL / 2;          // pairs per thread
+    static_assert(NP % 4 == 0, "whole 8-column groups per thread");
     const int r = tid / TPR, q = tid % TPR;
     const int J = (m - 1) >> 1;
     const float dc = 1.0f / sqrtf((float)m);
-    const float ac = sqrtf(2.0f / (float)m);
-    const float be = s.betas[r];
+    const float bac = s.betas[r] * sqrtf(2.0f / (float)m);
     const float wdec = s.decw[r];
     const double u = s.urev[r];                      // revolutions per unit frequency
     float s1, c1, sn, cs;
@@ -176,46 +185,40 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
         rev -= floor(rev);
         sincos_rev((float)rev, &sn, &cs);
     }
-    float av[NCOL];
-    half8v csv[NP / 4];
+    // Emitted 4 pairs (8 columns) at a time: few values live at once.
 #pragma unroll
-    for (int jj = 0; jj < NP; ++jj) {
-        const int j = NP * q + 1 + jj;
-        const bool live = j <= J && j <= 63;
-        const float cv = live ? cs : 0.f;
-        const float sv = live ? sn : 0.f;
-        av[2 * jj] = be * ac * cv;
-        av[2 * jj + 1] = -be * ac * sv;
-        // table entry 63 (internal columns 126, 127: DC and padding) is (1, 0),
-        // so the token-wise rotations pass those columns through unchanged
-        csv[jj >> 2][2 * (jj & 3)] = (_Float16)(j == 64 ? 1.f : cv);
-        csv[jj >> 2][2 * (jj & 3) + 1] = (_Float16)sv;
-        const float nc = cs * c1 - sn * s1;
-        const float ns = sn * c1 + cs * s1;
-        cs = nc;
-        sn = ns;
-    }
-    if (q == TPR - 1) {    // internal columns 126 (DC) and 127 (padding)
-        av[NCOL - 2] = be * dc;
-        av[NCOL - 1] = 0.f;
-    }
-    __bf16 *arow = s.As + r * QS + NCOL * q;
-    __bf16 *adrow = s.Ads + r * QS + NCOL * q;
-#pragma unroll
-    for (int k8 = 0; k8 < NCOL / 8; ++k8) {
+    for (int k8 = 0; k8 < NP / 4; ++k8) {
         bf16x8 a8, ad8;
+        half8v cs8;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            a8[k] = (__bf16)av[8 * k8 + k];
-            ad8[k] = (__bf16)(av[8 * k8 + k] * wdec);
+        for (int jj = 0; jj < 4; ++jj) {
+            const int j = NP * q + 1 + 4 * k8 + jj;
+            const bool live = j <= J && j <= 63;
+            const float cv = live ? cs : 0.f;
+            const float sv = live ? sn : 0.f;
+            float a0 = bac * cv, a1 = -bac * sv;
+            if (q == TPR - 1 && k8 == NP / 4 - 1 && jj == 3) {
+                a0 = s.betas[r] * dc;            // internal column 126: DC
+                a1 = 0.f;                        // 127: padding
+            }
+            a8[2 * jj] = (__bf16)a0;
+            a8[2 * jj + 1] = (__bf16)a1;
+            ad8[2 * jj] = (__bf16)(a0 * wdec);
+            ad8[2 * jj + 1] = (__bf16)(a1 * wdec);
+            // table entry 63 (internal columns 126, 127: DC and padding) is (1, 0),
+            // so the token-wise rotations pass those columns through unchanged
+            cs8[2 * jj] = (_Float16)(j == 64 ? 1.f : cv);
+            cs8[2 * jj + 1] = (_Float16)sv;
+            const float nc = cs * c1 - sn * s1;
+            const float ns = sn * c1 + cs * s1;
+            cs = nc;
+            sn = ns;
         }
-        if (kFull) *reinterpret_cast<bf16x8 *>(arow + 8 * k8) = a8;
-        *reinterpret_cast<bf16x8 *>(adrow + 8 * k8) = ad8;
-    }
-    if (kFull) {
-        half8v *csrow = reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q);
-#pragma unroll
-        for (int k4 = 0; k4 < NP / 4; ++k4) csrow[k4] = csv[k4];
+        if (kA) {
+            *reinterpret_cast<bf16x8 *>(s.As + r * QS + NCOL * q + 8 * k8) = a8;
+            *reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q + 4 * k8) = cs8;
+        }
+        if (kAd) *reinterpret_cast<bf16x8 *>(s.Ads + r * QS + NCOL * q + 8 * k8) = ad8;
     }
 }
 

@@ -55,19 +55,22 @@ __device__ __forceinline__ f32x4 mma16(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// A zero accumulator materialised where it is used: keeps the compiler from
-// hoisting one zero vector per accumulator out of the chunk loop and holding
-// them all live across it.
-__device__ __forceinline__ f32x16 zero_acc() {
-    f32x16 z = {};
-    asm volatile("" : "+v"(z));
-    return z;
-}
+// Zero accumulators: the first product of each chain then takes the inline
+// constant 0 as its accumulator input, so no zero registers are held.
+__device__ __forceinline__ f32x16 zero_acc() { return f32x16{}; }
+__device__ __forceinline__ f32x4 zero_acc4() { return f32x4{}; }
 
-__device__ __forceinline__ f32x4 zero_acc4() {
-    f32x4 z = {};
-    asm volatile("" : "+v"(z));
-    return z;
+// A lane's LDS byte offset, opaque to the compiler: accesses written as
+// smem + offset + constant then keep one base register per access pattern (the
+// constant folds into the instruction's offset field) instead of one register
+// per (tile, row) combination held across a loop.
+__device__ __forceinline__ int opq(int x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+template <typename T>
+__device__ __forceinline__ T *lds_at(char *smem, int byte_off) {
+    return reinterpret_cast<T *>(smem + byte_off);
 }
 
 __device__ __forceinline__ bf16x8 lds8(const __bf16 *p) {      // 16-byte LDS read
@@ -91,9 +94,12 @@ __device__ __forceinline__ bf16x4 lds4_tr(const __bf16 *p) {
 // Lane's base address for a transposed operand from a row-major tile with row
 // stride `stride`: the operand of column n = l % 32 and k = 8h + p is then
 // lds8_tr(base + k0 * stride + n0) for a tile block starting at (k0, n0).
-__device__ __forceinline__ const __bf16 *tr_base(const __bf16 *tile, int stride, int lane) {
+__device__ __forceinline__ int tr_off(int stride, int lane) {
     const int s = lane & 15, g = lane >> 4;
-    return tile + (8 * (g >> 1) + (s >> 2)) * stride + 16 * (g & 1) + 4 * (s & 3);
+    return (8 * (g >> 1) + (s >> 2)) * stride + 16 * (g & 1) + 4 * (s & 3);
+}
+__device__ __forceinline__ const __bf16 *tr_base(const __bf16 *tile, int stride, int lane) {
+    return tile + tr_off(stride, lane);
 }
 __device__ __forceinline__ bf16x8 lds8_tr(const __bf16 *p, int stride) {
     const bf16x4 lo = lds4_tr(p);

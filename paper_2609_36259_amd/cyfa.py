@@ -147,7 +147,7 @@ def selected_kernel(desc: FwdDesc) -> str:
     return "mfma" if ok and desc.chunk in (0, 32, 64) else "valu"
 
 
-DEFAULT_CHUNK = {"mfma": 64, "valu": 16}
+DEFAULT_CHUNK = {"mfma": 32, "valu": 16}
 
 
 def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=127,

@@ -2,7 +2,7 @@
 """Benchmark of the CyFA core operator on one MI355X.
 
 Default: the chunk-wise forward at the 1.4B-scale layer shape (B=4, T=4096,
-H=16, d_k=d_v=128, chunk 64, bf16 inputs, fp32 accumulation) on synthetic
+H=16, d_k=d_v=128, chunk 32, bf16 inputs, fp32 accumulation) on synthetic
 seeded inputs already resident in HBM.  One step = one cyfa_forward over the
 whole batch.  Prints one JSON line.
 
@@ -30,8 +30,34 @@ PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2516.6       # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
 M_ACTIVE = 127
 
-# Published HBM-traffic calibration and counter readings (see profiles/); None until taken
-TRAFFIC_BYTES_PER_LAUNCH = None
+# Measured HBM bytes per launch of the fused 32-token kernel on the 1.4B-layer
+# workload: rocprofv3 FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 (KiB per dispatch; the
+# factors come from the same counters on a 1 GiB device copy), taken on the kernel
+# sources whose digest is recorded here.  Reported only while those sources are
+# unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
+TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 343165464,
+           "fetch_kib": 134800, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
+           "sources_sha256": "17d2f142122ce61a59190565afafdf59132233d7c4a395ec60093c96b2a09422"}
+TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h")
+
+
+def kernel_sources_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        h.update(name.encode())
+        with open(os.path.join(ROOT, "paper_2609_36259_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, chunk: int):
+    """Counter-measured HBM bytes per launch, or None when they do not apply."""
+    if workload != TRAFFIC["workload"] or chunk != TRAFFIC["chunk"]:
+        return None
+    if kernel_sources_digest() != TRAFFIC["sources_sha256"]:
+        return None
+    return TRAFFIC["bytes"]
 
 
 def alg_flops_per_token_head(dk: int, dv: int, m: int = M_ACTIVE, C: int = 64) -> float:
@@ -121,13 +147,14 @@ def forward_bench(args, torch, cyfa, w):
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     kernel_ms = sum(kms) / len(kms)
     in_bytes = 2 if w.dtype == "bf16" else 4
-    flops = alg_flops_per_token_head(w.dk, w.dv, w.m) * w.B * w.T * w.H
+    chunk = args.chunk or cyfa.DEFAULT_CHUNK[cyfa.selected_kernel(desc)]
+    flops = alg_flops_per_token_head(w.dk, w.dv, w.m, chunk) * w.B * w.T * w.H
     nbytes_alg = alg_bytes(w.B, w.T, w.H, w.dk, w.dv, in_bytes, w.m)
     plan_kernel = cyfa.selected_kernel(desc)
     del t, ws, o
     torch.cuda.empty_cache()
     return dict(ms_per_step=ms_per_step, kernel_ms=kernel_ms, kernel_ms_min=min(kms),
-                flops=flops, bytes=nbytes_alg, kernel=plan_kernel)
+                flops=flops, bytes=nbytes_alg, kernel=plan_kernel, chunk=chunk)
 
 
 def decode_bench(args, torch, cyfa):
@@ -197,7 +224,7 @@ def cpu_baseline(w, budget_s: float):
     import oracle
     from paper_2609_36259_amd.inputs import workload_inputs
     x = workload_inputs(w)
-    npairs = min(w.B * w.H, max(1, len(os.sched_getaffinity(0))))
+    npairs = w.B * w.H
     pairs = np.arange(npairs, dtype=np.int32)
     args = (x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"])
     probe = 32
@@ -265,7 +292,8 @@ def main():
     bound = "hbm" if fb["bytes"] / (PEAK_HBM_GBS * 1e9) >= fb["flops"] / (PEAK_BF16_TFLOPS * 1e12) \
         else "mfma"
     roof = {"bound": bound, "kernel": f"cyfa fused chunk kernel ({fb['kernel']})",
-            "launch_ms": fb["kernel_ms"], "traffic": TRAFFIC_BYTES_PER_LAUNCH}
+            "launch_ms": fb["kernel_ms"],
+            "traffic": measured_traffic(args.workload, fb["chunk"]) if fb["kernel"] == "mfma" else None}
     if bound == "hbm":
         roof.update(achieved=hbm, peak=PEAK_HBM_GBS, unit="GB/s", frac=hbm / PEAK_HBM_GBS,
                     alg_bytes_per_launch=fb["bytes"])
@@ -278,7 +306,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if fb["kernel"] == "mfma" else "f32", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "d_k": w.dk, "d_v": w.dv,
-                   "chunk": args.chunk or cyfa.DEFAULT_CHUNK[fb["kernel"]], "m": w.m,
+                   "chunk": fb["chunk"], "m": w.m,
                    "io_dtype": w.dtype, "kernel": fb["kernel"], "segments": args.segments},
         "tflops": fb["flops"] / (fb["ms_per_step"] * 1e-3) / 1e12,
         "roofline": roof,

@@ -192,11 +192,13 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
     hipStream_t s = static_cast<hipStream_t>(stream);
     char *ws = static_cast<char *>(workspace);
     float *M = reinterpret_cast<float *>(ws);
-    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, s);
-    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
+    hipError_t e;
     if (plan.mfma) {
+        // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else {
+        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, s);
+        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
         e = mark(g_ev_start, s);
         if (e == hipSuccess) e = cyfa::launch_fwd_valu(p, M, s);
         if (e == hipSuccess) e = mark(g_ev_stop, s);
@@ -244,7 +246,7 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     p.K = K; p.V = V; p.clock = clock; p.o = o; p.logits = logits_out;
     hipStream_t s = static_cast<hipStream_t>(stream);
     float *M = static_cast<float *>(workspace);
-    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, s);
+    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, s);
     if (e == hipSuccess) e = mark(g_ev_start, s);
     if (e == hipSuccess) e = cyfa::launch_decode(p, M, s);
     if (e == hipSuccess) e = mark(g_ev_stop, s);

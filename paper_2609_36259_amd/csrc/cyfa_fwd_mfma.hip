@@ -701,24 +701,6 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     }
 }
 
-// Readout matrices in the two bf16 layouts the fused kernel reads.
-__global__ __launch_bounds__(NT) void readout_pack_kernel(int m, const float *__restrict__ M,
-                                                          __bf16 *__restrict__ Mz, __bf16 *__restrict__ My) {
-    const int h = blockIdx.x;
-    const float *Mh = M + (size_t)h * 128 * 128;
-    __bf16 *Mzh = Mz + (size_t)h * 128 * 128;
-    __bf16 *Myh = My + (size_t)h * 128 * 128;
-    for (int e = blockIdx.y * NT + threadIdx.x; e < 128 * 128; e += gridDim.y * NT) {
-        const int row = e >> 7, col = e & 127;
-        // Mz[i'][j_int] = M[i'][paper(j_int)]
-        const int pj = internal_to_paper(col, m);
-        Mzh[e] = (__bf16)(pj >= 0 ? Mh[(size_t)row * 128 + pj] : 0.f);
-        // My[j_int][i'] = M[i'][paper(j_int)]
-        const int pr = internal_to_paper(row, m);
-        Myh[e] = (__bf16)(pr >= 0 ? Mh[(size_t)col * 128 + pr] : 0.f);
-    }
-}
-
 }  // namespace
 
 // ---- host side --------------------------------------------------------------
@@ -732,15 +714,13 @@ int mfma_default_chunk() { return kMfmaDefaultChunk; }
 
 namespace {
 struct WsLayout {
-    size_t mz, my, state, span, gsum, origin, flam, total;
+    size_t mz, state, span, gsum, origin, flam, total;
 };
 WsLayout ws_layout(const FwdParams &p, int P) {
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
     WsLayout L{};
     size_t off = up(readout_f32_bytes(p.H));
     L.mz = off;
-    off += up((size_t)p.H * 128 * 128 * 2);
-    L.my = off;
     off += up((size_t)p.H * 128 * 128 * 2);
     const size_t nseg = (size_t)p.B * p.H * P;
     L.state = off;
@@ -814,7 +794,6 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     if (a.nchunks > 0) a.P = (a.nchunks + a.cps - 1) / a.cps;   // no empty trailing segment
     if (a.P < 1) a.P = 1;
     a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
-    a.My = reinterpret_cast<const __bf16 *>(base + L.my);
     a.seg_state = reinterpret_cast<float *>(base + L.state);
     a.seg_span = reinterpret_cast<double *>(base + L.span);
     a.seg_gsum = reinterpret_cast<double *>(base + L.gsum);
@@ -824,10 +803,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     const int BH = p.B * p.H;
 
-    hipLaunchKernelGGL(readout_pack_kernel, dim3(p.H, 8), dim3(NT), 0, st, p.m,
-                       reinterpret_cast<const float *>(base), const_cast<__bf16 *>(a.Mz),
-                       const_cast<__bf16 *>(a.My));
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, const_cast<__bf16 *>(a.Mz), st);
     if (e != hipSuccess) return e;
     e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
     if (e != hipSuccess) return e;

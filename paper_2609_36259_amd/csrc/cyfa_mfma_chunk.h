@@ -14,7 +14,6 @@ struct MfmaArgs {
     int nchunks;         // chunks per sequence
     int chunk;           // chunk length (32 or 64)
     const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j
-    const __bf16 *My;    // [H][128][128]  row = internal basis j, column = slot i'
     float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
     double *seg_span;    // [B*H*P] clock span of each segment (reduced mod m)
     double *seg_gsum;    // [B*H*P] sum of log alpha over each segment

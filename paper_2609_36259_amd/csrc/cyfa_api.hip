@@ -197,7 +197,7 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
         // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else {
-        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, s);
+        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
         if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
         e = mark(g_ev_start, s);
         if (e == hipSuccess) e = cyfa::launch_fwd_valu(p, M, s);
@@ -246,7 +246,7 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     p.K = K; p.V = V; p.clock = clock; p.o = o; p.logits = logits_out;
     hipStream_t s = static_cast<hipStream_t>(stream);
     float *M = static_cast<float *>(workspace);
-    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, s);
+    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
     if (e == hipSuccess) e = mark(g_ev_start, s);
     if (e == hipSuccess) e = cyfa::launch_decode(p, M, s);
     if (e == hipSuccess) e = mark(g_ev_stop, s);

@@ -383,7 +383,10 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     // lane, c x + s x' on the sin lane
     const float sgn = (icol & 1) ? 1.f : -1.f;
 
-    const float zs = p.scale * 1.4426950408889634f;                       // logits in log2 units
+    // the readout matrix in LDS is M times zs = scale log2(e): slot logits come out in
+    // log2 units, and the readout weights are divided by zs to compensate
+    const float zs = __int_as_float(__builtin_amdgcn_readfirstlane(
+        __float_as_int(p.scale * 1.4426950408889634f)));             // uniform: a scalar register
     // Per-lane bases (opaque byte offsets): every unrolled LDS access below is one
     // of these plus a compile-time offset.
     constexpr int TE = Ly::TILE / 2;                                      // tile size in elements
@@ -500,7 +503,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 const float self = oacc[rb][v];
                 const float part = swap_pair(self);
                 const half2v cs = CS_l[ro * 64];
-                X_l[ro * QS] = (__bf16)(zs * fmaf(sgn * (float)cs[1], part, (float)cs[0] * self));
+                X_l[ro * QS] = (__bf16)fmaf(sgn * (float)cs[1], part, (float)cs[0] * self);
             }
         __syncthreads();
         // -- middle step 2: slot logits, transposed: Z^T = M X^T.  Wave w owns slots
@@ -520,24 +523,19 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // -- middle step 3: softmax over the m active slots.  Per token: in-lane over
         //    16 slots, across the two lane halves, then one (max, sum) exchange
         //    between the 4 waves.
+        float mwave[RB];                        // this wave's max over its slots (-inf: none active)
 #pragma unroll
         for (int nb = 0; nb < RB; ++nb) {
-            float mx = -INFINITY;
+            if (32 * w + 31 >= m) {             // this wave holds inactive slots (uniform)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int slot = icol - l32 + 8 * (v >> 2) + h4 + (v & 3);
-                if (slot >= m) zacc[nb][v] = -INFINITY;
-                mx = fmaxf(mx, zacc[nb][v]);
+                for (int v = 0; v < 16; ++v)
+                    if (icol - l32 + 8 * (v >> 2) + h4 + (v & 3) >= m) zacc[nb][v] = -INFINITY;
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            // a wave whose slots are all inactive (m <= 32 w) contributes (-inf, 0)
-            const float mref = mx == -INFINITY ? 0.f : mx;
-            float sm = 0.f;
+            float mx = zacc[nb][0];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sm += __builtin_amdgcn_exp2f(zacc[nb][v] - mref);
-            sm += __shfl_xor(sm, 32);
+            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, zacc[nb][v]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
             const int r = 32 * nb + l32;
-            if (hl == 0) redw[32 * nb] = make_float2(mx, sm);
             if (p.logits && r < n) {
                 // the logit accumulators hold log2(e) z; report z
                 float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m;
@@ -547,11 +545,24 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                     if (slot < m) lg[slot] = zacc[nb][v] * 0.69314718055994531f;
                 }
             }
+            // a wave whose slots are all inactive (m <= 32 w) contributes (-inf, 0)
+            mwave[nb] = mx;
+            const float mref = mx == -INFINITY ? 0.f : mx;
+            // the accumulators now hold exp2(z - mref), reused for the weights below
+#pragma unroll
+            for (int v = 0; v < 16; ++v) zacc[nb][v] = __builtin_amdgcn_exp2f(zacc[nb][v] - mref);
+            float t8[8];
+#pragma unroll
+            for (int v = 0; v < 8; ++v) t8[v] = zacc[nb][v] + zacc[nb][v + 8];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) t8[v] += t8[v + 4];
+            float sm = (t8[0] + t8[2]) + (t8[1] + t8[3]);
+            sm += __shfl_xor(sm, 32);
+            if (hl == 0) redw[32 * nb] = make_float2(mx, sm);
         }
         __syncthreads();
 #pragma unroll
         for (int nb = 0; nb < RB; ++nb) {
-            const int r = 32 * nb + l32;
             float2 pr[4];
 #pragma unroll
             for (int x = 0; x < 4; ++x) pr[x] = redr[x * CC + 32 * nb];
@@ -559,14 +570,16 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             float Lsum = 0.f;
 #pragma unroll
             for (int x = 0; x < 4; ++x) Lsum += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
-            const float inv = 1.f / Lsum;
+            // W = exp2(z - M) / L / zs = e * exp2(mwave - M) / (L zs), mwave <= M
+            const float f = mwave[nb] == -INFINITY
+                                ? 0.f
+                                : __builtin_amdgcn_exp2f(mwave[nb] - M) * __builtin_amdgcn_rcpf(Lsum * zs);
             __bf16 *wrow = Wrow + 32 * nb * QS;
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4) {
                 bf16x4 wv;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    wv[k] = (__bf16)(__builtin_amdgcn_exp2f(zacc[nb][4 * v4 + k] - M) * inv);
+                for (int k = 0; k < 4; ++k) wv[k] = (__bf16)(zacc[nb][4 * v4 + k] * f);
                 *reinterpret_cast<bf16x4 *>(wrow + 8 * v4) = wv;
             }
         }
@@ -803,7 +816,9 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     const int BH = p.B * p.H;
 
-    hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, const_cast<__bf16 *>(a.Mz), st);
+    // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
+    hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, const_cast<__bf16 *>(a.Mz),
+                                       p.scale * 1.4426950408889634f, st);
     if (e != hipSuccess) return e;
     e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
     if (e != hipSuccess) return e;

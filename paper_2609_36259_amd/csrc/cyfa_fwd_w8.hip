@@ -162,7 +162,10 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
     const int col = 16 * w + l16;                     // this lane's state / output column
     // U(theta) on a (cos, sin) column pair held by lanes (2k, 2k+1)
     const float sgn = (l16 & 1) ? 1.f : -1.f;
-    const float zs = p.scale * 1.4426950408889634f;  // logits in log2 units
+    // the readout matrix is M times zs = scale log2(e) (logits in log2 units); the
+    // readout weights are divided by zs to compensate
+    const float zs = __int_as_float(__builtin_amdgcn_readfirstlane(
+        __float_as_int(p.scale * 1.4426950408889634f)));
 
     // Per-lane operand bases, one opaque byte offset per access pattern; every
     // unrolled access below adds a compile-time constant below 64 KiB.
@@ -274,7 +277,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
                     kacc[db] = mma16(lds8_tr(Ktr + 32 * ks * QS + 16 * db, QS), adw, kacc[db]);
             }
         }
-        // -- middle step 1: X_r = U(lambda_r) O'_r, times scale log2(e) -> X tile (Q's)
+        // -- middle step 1: X_r = U(lambda_r) O'_r -> X tile (Q's)
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
@@ -283,7 +286,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
                 const float self = oacc[rt][r];
                 const float part = swap_pair(self);
                 const half2v cs = CSx[ro * 64];
-                Xw[ro * QS] = (__bf16)(zs * fmaf(sgn * (float)cs[1], part, (float)cs[0] * self));
+                Xw[ro * QS] = (__bf16)fmaf(sgn * (float)cs[1], part, (float)cs[0] * self);
             }
         __syncthreads();
         // -- middle step 2: slot logits Z^T = M X^T; wave w owns slots 16w .. 16w+15
@@ -340,7 +343,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
             float Lsum = 0.f;
 #pragma unroll
             for (int x = 0; x < 8; ++x) Lsum += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
-            const float inv = 1.f / Lsum;
+            const float inv = __builtin_amdgcn_rcpf(Lsum * zs);
             bf16x4 wv;
 #pragma unroll
             for (int r = 0; r < 4; ++r) wv[r] = (__bf16)(__builtin_amdgcn_exp2f(zacc[rt][r] - M) * inv);

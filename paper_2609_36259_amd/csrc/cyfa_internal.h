@@ -44,7 +44,8 @@ struct DecParams {
 inline size_t readout_f32_bytes(int H) { return (size_t)H * kStoreRows * kStoreRows * 4; }
 
 // ---- launchers (return hipSuccess or the launch error) -------------------
-hipError_t launch_readout_prep(int H, int m, const float *R, float *M, __bf16 *Mz, hipStream_t s);
+hipError_t launch_readout_prep(int H, int m, const float *R, float *M, __bf16 *Mz, float mz_scale,
+                               hipStream_t s);
 hipError_t launch_fwd_valu(const FwdParams &p, const float *M, hipStream_t s);
 hipError_t launch_decode(const DecParams &p, const float *M, hipStream_t s);
 

@@ -13,7 +13,7 @@ struct MfmaArgs {
     int cps;             // chunks per segment
     int nchunks;         // chunks per sequence
     int chunk;           // chunk length (32 or 64)
-    const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j
+    const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j; times scale log2(e)
     float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
     double *seg_span;    // [B*H*P] clock span of each segment (reduced mod m)
     double *seg_gsum;    // [B*H*P] sum of log alpha over each segment

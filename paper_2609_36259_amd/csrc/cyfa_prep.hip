@@ -18,10 +18,10 @@ constexpr int kPrepRows = 4;          // rows of M_h per workgroup (two per thre
 // 4 rb + 2 g, 4 rb + 2 g + 1.  Phi[s][j] is read from a table of the m angles
 // 2 pi r / m: the index (l s) mod m advances by l per step, with no division.
 // M (fp32, paper basis order) and/or Mz (bf16, the matrix-core kernels' basis
-// order: Mz[i'][j_int] = M[i'][paper(j_int)]) are written when non-null.
+// order: Mz[i'][j_int] = mz_scale * M[i'][paper(j_int)]) are written when non-null.
 __global__ __launch_bounds__(256) void readout_prep_kernel(int m, const float *__restrict__ R,
                                                            float *__restrict__ M,
-                                                           __bf16 *__restrict__ Mz) {
+                                                           __bf16 *__restrict__ Mz, float mz_scale) {
     __shared__ float tab[2][kMaxActive];                     // cos, sin of 2 pi r / m
     __shared__ float Rrows[kPrepRows][kMaxActive + 1];
     const int h = blockIdx.x;
@@ -74,14 +74,15 @@ __global__ __launch_bounds__(256) void readout_prep_kernel(int m, const float *_
         if (M) M[((size_t)h * kStoreRows + i) * kStoreRows + j] = val;
         if (Mz) {
             const int jint = j == 0 ? kStoreRows - 2 : (j == kStoreRows - 1 ? kStoreRows - 1 : j - 1);
-            Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)val;
+            Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)(mz_scale * val);
         }
     }
 }
 
-hipError_t launch_readout_prep(int H, int m, const float *R, float *M, __bf16 *Mz, hipStream_t s) {
+hipError_t launch_readout_prep(int H, int m, const float *R, float *M, __bf16 *Mz, float mz_scale,
+                               hipStream_t s) {
     hipLaunchKernelGGL(readout_prep_kernel, dim3(H, kStoreRows / kPrepRows), dim3(256), 0, s,
-                       m, R, M, Mz);
+                       m, R, M, Mz, mz_scale);
     return hipGetLastError();
 }
 

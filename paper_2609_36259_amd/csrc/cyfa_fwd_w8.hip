@@ -37,7 +37,7 @@ struct LayW8 {
     static constexpr int MT = CS + CK * 64 * 4;         // readout matrix [128][QS]
     static constexpr int RED = MT + 128 * QS * 2;       // softmax (max, sum) [8 waves][CK]
     static constexpr int SC = RED + 8 * CK * 8;         // per-token scalars
-    static constexpr int BYTES = SC + 64 * (4 + 4 + 4 + 4 + 8) + 16;
+    static constexpr int BYTES = SC + scalar_bytes(64);
     static_assert(BYTES <= 160 * 1024, "LDS budget");
 };
 

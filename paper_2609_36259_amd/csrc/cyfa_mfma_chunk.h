@@ -39,7 +39,7 @@ struct Tiles {
     float *gam;     // row scale of the inter-chunk terms: exp(G_r + L)
     float *betas;
     float *decw;    // multiplier of A_dec rows
-    double *urev;   // clock at each row reduced mod m, divided by m (revolutions)
+    float *urev;    // clock at each row reduced mod m, divided by m (revolutions, in [0, 1))
     float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
 };
 
@@ -49,10 +49,10 @@ __device__ __forceinline__ void scalars_at(Tiles &t, char *base, int n = 64) {
     t.gam = t.Gs + n;
     t.betas = t.gam + n;
     t.decw = t.betas + n;
-    t.urev = reinterpret_cast<double *>(t.decw + n);
+    t.urev = t.decw + n;
     t.ctl = reinterpret_cast<float *>(t.urev + n);
 }
-__host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 8) + 16; }
+__host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 4) + 16; }
 
 // Global -> register prefetch of one chunk: CC NTH/16 x 16-byte pieces per thread
 // per tensor (rows (NTH/16) it + tid / 16, columns 8 (tid % 16)), plus one
@@ -144,7 +144,7 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
         s.decw[ol] = lazy ? __expf(-G - L) : __expf(GC - G);
         s.betas[ol] = pf.be;
         const double q = lam * inv_m;               // clock in revolutions of the m-slot ring
-        s.urev[ol] = q - floor(q);
+        s.urev[ol] = (float)(q - floor(q));
     }
     const float state_factor = lazy ? 1.f : __expf(L + GC);
     L = lazy ? L + GC : 0.f;
@@ -176,7 +176,9 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
     const float dc = 1.0f / sqrtf((float)m);
     const float bac = s.betas[r] * sqrtf(2.0f / (float)m);
     const float wdec = s.decw[r];
-    const double u = s.urev[r];                      // revolutions per unit frequency
+    const double u = s.urev[r];                      // revolutions per unit frequency (float:
+                                                     // the phases it starts are far finer
+                                                     // than A's bf16 rounding)
     float s1, c1, sn, cs;
     sincos_rev((float)u, &s1, &c1);
     {

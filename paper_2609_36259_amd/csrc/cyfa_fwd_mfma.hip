@@ -755,7 +755,19 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
                      hipEvent_t ev_stop) {
     hipError_t e;
     if (a.P > 1 && a.nchunks > 0) {
-        hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a);
+        // Only each segment's total contribution is needed, so the pre-pass may
+        // step through a segment in 64-token chunks (fewer barriers and per-chunk
+        // costs) whenever its length is a whole number of them.  Every segment but
+        // the last is full, and the last one is not pre-passed.
+        if (CC == 32 && a.cps % 2 == 0) {
+            MfmaArgs a64 = a;
+            a64.chunk = 64;
+            a64.cps = a.cps / 2;
+            a64.nchunks = (a.p.T + 63) / 64;
+            hipLaunchKernelGGL(segment_state_kernel<64>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a64);
+        } else {
+            hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.has_init) {

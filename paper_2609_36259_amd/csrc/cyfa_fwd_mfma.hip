@@ -237,7 +237,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
 // Element pairs that a rotation U(tau) mixes sit next to each other in the
 // accumulator-dump layout: key-state partners are adjacent lanes (offsets e,
 // e + 1), value-state partners are adjacent registers (offsets e, e + 64).
-// grid (B*H, 32): thread = one pair; consecutive threads touch consecutive words.
+// pair_ref(g) names pair g of a (b, h): g < 8192 key state, else value state.
 struct PairRef {
     int o0, o1;        // dump offsets of the (cos, sin) pair
     int i0;            // internal index of the first element (even)
@@ -289,40 +289,72 @@ __device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x
     x1 = y1;
 }
 
+// Thread = four rotation pairs moved with two 16-byte accesses per segment: key
+// state, 8 consecutive words (pairs are adjacent lanes); value state, 4
+// consecutive lanes of registers v and v + 1 (pairs are register pairs, and the
+// four share one frequency).  grid (B*H, 16): 2048 key and 2048 value threads.
 __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
     const int bh = blockIdx.x;
-    const int gidx = blockIdx.y * NT + threadIdx.x;      // 0 .. 16383
+    const int qi = blockIdx.y * NT + threadIdx.x;        // 0 .. 4095
     const int m = a.p.m;
-    const PairRef pr = pair_ref(gidx);
-    const int j = (pr.i0 >> 1) + 1;                      // frequency of the pair
-    const bool rotates = pr.i0 < kDC && j <= (m - 1) / 2;
-    const float *init = pr.value ? a.p.V0 : a.p.K0;
-    const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
-    float x0 = 0.f, x1 = 0.f;
-    if (init) {
-        const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
-        const size_t base = (size_t)bh * 128 * 128 + pr.col;
-        x0 = p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
-        x1 = p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
+    const bool value = qi >= 2048;
+    int off0, off1;                                      // dump offsets of the two float4
+    PairRef pr[4];
+    if (!value) {
+        off0 = 8 * qi;
+        off1 = off0 + 4;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) pr[k] = pair_ref(4 * qi + k);
+    } else {
+        const int q = qi - 2048;
+        const int lane0 = 4 * (q & 15), vp = (q >> 4) & 7, blk = (q >> 7) & 3, w = q >> 9;
+        off0 = 128 * 128 + ((w * 4 + blk) * 16 + 2 * vp) * 64 + lane0;
+        off1 = off0 + 64;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) pr[k] = pair_ref(8192 + lane0 + k + 64 * (vp + 8 * (blk + 4 * w)));
     }
-    if (rotates) rotate_pair(ring_rev(c0, m), j, x0, x1);   // initial state in the frame with origin clock0
+    int jf[4];
+    bool rot[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        jf[k] = (pr[k].i0 >> 1) + 1;                     // frequency of the pair
+        rot[k] = pr[k].i0 < kDC && jf[k] <= (m - 1) / 2;
+    }
+    const float *init = value ? a.p.V0 : a.p.K0;
+    const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
+    float x0[4] = {0.f, 0.f, 0.f, 0.f}, x1[4] = {0.f, 0.f, 0.f, 0.f};
+    if (init) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int p0 = internal_to_paper(pr[k].i0, m), p1 = internal_to_paper(pr[k].i0 + 1, m);
+            const size_t base = (size_t)bh * 128 * 128 + pr[k].col;
+            x0[k] = p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
+            x1[k] = p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
+        }
+    }
+    {
+        const double u0 = ring_rev(c0, m);               // initial state in the frame with origin clock0
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (rot[k]) rotate_pair(u0, jf[k], x0[k], x1[k]);
+    }
     const double inv_m = 1.0 / (double)m;
     double origin = reduce_clock(c0, (double)m, inv_m);
     // Segment contributions are fetched kBatch segments at a time, ahead of the
-    // dependent chain through them.  Every thread owns the same two offsets in
-    // every segment, so the loads of a batch never see this batch's stores.
+    // dependent chain through them.  Every thread owns the same offsets in every
+    // segment, so the loads of a batch never see this batch's stores.
     constexpr int kBatch = 8;
     for (int q0 = 0; q0 < a.P; q0 += kBatch) {
-        float d0[kBatch], d1[kBatch];
+        float4 da[kBatch], db[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int q = q0 + u;
-            d0[u] = 0.f;
-            d1[u] = 0.f;
+            da[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            db[u] = da[u];
             if (q < a.P - 1) {
                 const float *st = a.seg_state + ((size_t)bh * a.P + q) * kStateFloats;
-                d0[u] = st[pr.o0];
-                d1[u] = st[pr.o1];
+                da[u] = *reinterpret_cast<const float4 *>(st + off0);
+                db[u] = *reinterpret_cast<const float4 *>(st + off1);
             }
         }
 #pragma unroll
@@ -331,15 +363,29 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
             if (q >= a.P) break;
             const size_t slot = (size_t)bh * a.P + q;
             float *st = a.seg_state + slot * kStateFloats;
-            if (gidx == 0) a.seg_origin[slot] = origin;
-            st[pr.o0] = x0;
-            st[pr.o1] = x1;
+            if (qi == 0) a.seg_origin[slot] = origin;
+            float d0[4], d1[4];
+            if (!value) {
+                *reinterpret_cast<float4 *>(st + off0) = make_float4(x0[0], x1[0], x0[1], x1[1]);
+                *reinterpret_cast<float4 *>(st + off1) = make_float4(x0[2], x1[2], x0[3], x1[3]);
+                d0[0] = da[u].x; d1[0] = da[u].y; d0[1] = da[u].z; d1[1] = da[u].w;
+                d0[2] = db[u].x; d1[2] = db[u].y; d0[3] = db[u].z; d1[3] = db[u].w;
+            } else {
+                *reinterpret_cast<float4 *>(st + off0) = make_float4(x0[0], x0[1], x0[2], x0[3]);
+                *reinterpret_cast<float4 *>(st + off1) = make_float4(x1[0], x1[1], x1[2], x1[3]);
+                d0[0] = da[u].x; d0[1] = da[u].y; d0[2] = da[u].z; d0[3] = da[u].w;
+                d1[0] = db[u].x; d1[1] = db[u].y; d1[2] = db[u].z; d1[3] = db[u].w;
+            }
             if (q < a.P - 1) {
                 const float gdec = __expf((float)a.seg_gsum[slot]);
-                x0 = fmaf(gdec, x0, d0[u]);
-                x1 = fmaf(gdec, x1, d1[u]);
-                const double span = a.seg_span[slot];
-                if (rotates) rotate_pair(span * inv_m, j, x0, x1);   // span is already reduced to [0, m)
+                const double span = a.seg_span[slot];    // already reduced to [0, m)
+                const double u1 = span * inv_m;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    x0[k] = fmaf(gdec, x0[k], d0[k]);
+                    x1[k] = fmaf(gdec, x1[k], d1[k]);
+                    if (rot[k]) rotate_pair(u1, jf[k], x0[k], x1[k]);
+                }
                 origin = reduce_clock(origin + span, (double)m, inv_m);
             }
         }
@@ -771,7 +817,7 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.has_init) {
-        hipLaunchKernelGGL(segment_scan_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
+        hipLaunchKernelGGL(segment_scan_kernel, dim3(BH, 4096 / NT), dim3(NT), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;

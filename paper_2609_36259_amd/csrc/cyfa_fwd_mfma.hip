@@ -28,27 +28,34 @@ using namespace mfma;
 namespace {
 
 // ---- LDS maps (bytes) ---------------------------------------------------------
-// Fused kernel (32-token chunks): every bf16 tile is row-major [CC][QS];
-// operands whose k index runs down the rows are read with the transpose read.
-// Two workgroups share a compute unit, so the map stays within half of its
-// 160 KiB: there is no A_dec tile (its row scale is applied to the other
-// operand of each state update) and the softmax partials share the score tile.
+// Fused kernel (32-token chunks).  Tiles read through the transpose read (K, V,
+// A and the readout matrix M) are swizzled rows of 128; Q (then X, W), O'' and
+// the output staging are padded to stride QS.  K's region switches to the
+// padded layout when O'' replaces K.  Two workgroups share a compute unit, so
+// the map stays within half of its 160 KiB: there is no A_dec tile (its row
+// scale is applied to the other operand of each state update) and the softmax
+// partials share the score tile.
 template <int CC>
 struct Lay {
     static constexpr int RB = CC / 32;                 // 32-row blocks per tile
     static constexpr int SSC = CC + 8;                 // row stride of the score tile
-    static constexpr int TILE = CC * QS * 2;
-    static constexpr int Q = 0;                        // Q   -> X -> W
-    static constexpr int K = Q + TILE;                 // K   -> O''
-    static constexpr int V = K + TILE;                 // V
-    static constexpr int A = V + TILE;                 // A   (temporal writes)
-    static constexpr int S = A + TILE;                 // scores [CC][SSC] bf16 / softmax partials
+    static constexpr int CSW = 68;                     // row stride (half2 words) of the (cos, sin) table
+    static constexpr int TILE = CC * QS * 2;           // padded tile
+    static constexpr int STILE = CC * SWS * 2;         // swizzled tile
+    static constexpr int Q = 0;                        // Q   -> X -> W       (padded)
+    static constexpr int K = Q + TILE;                 // K (swizzled) -> O'' (padded)
+    static constexpr int V = K + TILE;                 // V   (swizzled)
+    static constexpr int A = V + STILE;                // A   (temporal writes, swizzled)
+    static constexpr int S = A + STILE;                // scores [CC][SSC] bf16 / softmax partials
     static constexpr int RED = S;                      // (max, sum) per wave x row, middle step only
-    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][64] half pairs -> output staging
-    static constexpr int MT = CS + CC * 64 * 4;        // readout matrix [128][QS] bf16
-    static constexpr int SC = MT + 128 * QS * 2;       // per-token scalars (CC entries each)
+    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][CSW] half pairs -> output staging [CC][QS]
+    static constexpr int MT = CS + CC * CSW * 4;       // readout matrix [128][SWS] bf16 (swizzled)
+    static constexpr int SC = MT + 128 * SWS * 2;      // per-token scalars (CC entries each)
     static constexpr int BYTES = SC + scalar_bytes(CC);
     static_assert(4 * CC * 8 <= CC * SSC * 2, "softmax partials fit the score tile");
+    static_assert(CSW * 4 == QS * 2, "output staging fits the (cos, sin) table");
+    static_assert(K % 256 == 0 && V % 256 == 0 && A % 256 == 0 && MT % 256 == 0,
+                  "swizzled tiles start on a bank-window boundary");
     static_assert(CC != 32 || BYTES <= 80 * 1024, "two workgroups per compute unit");
     // state pre-pass: K, V, A_dec and the scalars (64 entries)
     static constexpr int PK = 0, PV = TILE, PAD = 2 * TILE, PSC = 3 * TILE;
@@ -124,17 +131,20 @@ __device__ __forceinline__ constexpr int acc_off(int blk, int v) {
 }
 
 // One 16 x 16 block (rb, sb) of the causal score tile (S (.) Gamma) -> Ss (bf16),
-// k = 128 along the rows of both operand tiles.
+// k = 128 along the rows of both operand tiles: A rows from a padded tile, B rows
+// from the swizzled tile at byte offset Boff (column block ks of a row is its
+// first block's offset ^ 64 ks).
 template <int CC>
-__device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
+__device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, char *smem, int Boff,
                                             int rb, int sb, int lane) {
     constexpr int SSC = Lay<CC>::SSC;
     const int l16 = lane & 15, g = lane >> 4;
     f32x4 acc = zero_acc4();
     const __bf16 *ap = Arow + (16 * rb + l16) * QS + 8 * g;
-    const __bf16 *bp = Brow + (16 * sb + l16) * QS + 8 * g;
+    const int bo = Boff + 2 * swz_elem(16 * sb + l16, 8 * g);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) acc = mma16(lds8(ap + 32 * ks), lds8(bp + 32 * ks), acc);
+    for (int ks = 0; ks < 4; ++ks)
+        acc = mma16(lds8(ap + 32 * ks), lds8(lds_at<__bf16>(smem, opq(bo) ^ (64 * ks))), acc);
     const int scol = 16 * sb + l16;
     const int row0 = 16 * rb + 4 * g;
     const float Gs_col = s.Gs[scol];
@@ -149,17 +159,10 @@ __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, 
 // products read (the lower triangle plus the upper halves of the 32 x 32
 // diagonal blocks, which come out as zeros), spread evenly over the 4 waves.
 template <int CC>
-__device__ __forceinline__ void score_tiles(const Tiles &s, const __bf16 *Arow, const __bf16 *Brow,
+__device__ __forceinline__ void score_tiles(const Tiles &s, const __bf16 *Arow, char *smem, int Boff,
                                             int w, int lane) {
-    if (CC == 32) {
-        score_block<CC>(s, Arow, Brow, w >> 1, w & 1, lane);
-    } else {
-        // (rb, sb) lists per wave: 12 blocks, 3 each
-        constexpr int kRb[12] = {0, 1, 1, 0, 2, 2, 2, 2, 3, 3, 3, 3};
-        constexpr int kSb[12] = {0, 0, 1, 1, 0, 1, 2, 3, 0, 1, 2, 3};
-#pragma unroll
-        for (int k = 0; k < 3; ++k) score_block<CC>(s, Arow, Brow, kRb[3 * w + k], kSb[3 * w + k], lane);
-    }
+    static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
+    score_block<CC>(s, Arow, smem, Boff, w >> 1, w & 1, lane);
 }
 
 __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4], float f) {
@@ -415,7 +418,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     using Ly = Lay<CC>;
     constexpr int RB = Ly::RB;
     constexpr int SSC = Ly::SSC;
-    __shared__ __attribute__((aligned(16))) char smem[Ly::BYTES];
+    __shared__ __attribute__((aligned(256))) char smem[Ly::BYTES];
     const Tiles s = fused_tiles<CC>(smem);
     const FwdParams &p = a.p;
     const int bh = blockIdx.x / a.P, seg = blockIdx.x % a.P;
@@ -435,32 +438,35 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         __float_as_int(p.scale * 1.4426950408889634f)));             // uniform: a scalar register
     // Per-lane bases (opaque byte offsets): every unrolled LDS access below is one
     // of these plus a compile-time offset.
-    constexpr int TE = Ly::TILE / 2;                                      // tile size in elements
-    const int trl = tr_off(QS, lane);
+    constexpr int TE = Ly::TILE / 2;                                      // padded tile size in elements
+    constexpr int CSW = Ly::CSW;
+    const int trs = tr_off_swz(lane);
     const float *gam_l = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + h4)));           // gam, accumulator rows
     const float *dw_l = lds_at<float>(smem, opq(Ly::SC + 4 * (3 * CC + 8 * hl)));    // decw, operand tokens
-    const __bf16 *Mza = lds_at<__bf16>(smem, opq(Ly::MT + 2 * (icol * QS + 8 * hl)));  // M rows
-    const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + 2 * (trl + 32 * w)));         // M columns
-    const half2v *CS_l = lds_at<half2v>(smem, opq(Ly::CS + 4 * (h4 * 64 + (icol >> 1))));
+    // M rows (slot icol), columns 8 hl + 16 ks at byte offset Mza ^ 32 ks
+    const int Mza = opq(Ly::MT + 2 * swz_elem(icol, 8 * hl));
+    const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + (trs ^ (64 * w))));          // M columns
+    const half2v *CS_l = lds_at<half2v>(smem, opq(Ly::CS + 4 * (h4 * CSW + (icol >> 1))));
     __bf16 *X_l = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (h4 * QS + icol)));           // X (then W) tile
-    // output staging: [CC][128] bf16 in the (cos, sin) table, which is free from the
+    // output staging: [CC][QS] bf16 in the (cos, sin) table, which is free from the
     // O'' rotation until the next chunk's temporal writes
-    __bf16 *St_l = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (h4 * 128 + icol)));
+    __bf16 *St_l = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (h4 * QS + icol)));
     const __bf16 *Qperm = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + h4)));   // permuted-k A operands
     const __bf16 *Operm = Qperm + TE;
     const __bf16 *Xa = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 8 * hl)));  // natural-k operands
     const __bf16 *Sa = lds_at<__bf16>(smem, opq(Ly::S + 2 * (l32 * SSC + 8 * hl)));
-    const __bf16 *At = lds_at<__bf16>(smem, opq(Ly::A + 2 * (trl + 32 * w)));       // transposed operands
-    const __bf16 *Vt = lds_at<__bf16>(smem, opq(Ly::V + 2 * (trl + 32 * w)));
-    const __bf16 *Atx = lds_at<__bf16>(smem, opq(Ly::A + 2 * trl));
-    const __bf16 *Kt = lds_at<__bf16>(smem, opq(Ly::K + 2 * trl));
+    // transposed operands from swizzled tiles: column block w, or block x at base ^ 64 x
+    const __bf16 *At = lds_at<__bf16>(smem, opq(Ly::A + (trs ^ (64 * w))));
+    const __bf16 *Vt = lds_at<__bf16>(smem, opq(Ly::V + (trs ^ (64 * w))));
+    const int Atx = opq(Ly::A + trs);
+    const int Kt = opq(Ly::K + trs);
     // token-row bases of the readout step: row l32 (+ 32 nb), columns 32w + 4hl ..
     __bf16 *Wrow = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 32 * w + h4)));
     __bf16 *O2row = Wrow + TE;
-    const half2v *CSrow = lds_at<half2v>(smem, opq(Ly::CS + 4 * (l32 * 64 + 16 * w + 2 * hl)));
+    const half2v *CSrow = lds_at<half2v>(smem, opq(Ly::CS + 4 * (l32 * CSW + 16 * w + 2 * hl)));
     float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
     const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
-    const __bf16 *Stg = lds_at<__bf16>(smem, opq(Ly::CS + 2 * ((tid >> 4) * 128 + (tid & 15) * 8)));
+    const __bf16 *Stg = lds_at<__bf16>(smem, opq(Ly::CS + 2 * ((tid >> 4) * QS + (tid & 15) * 8)));
 
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
@@ -469,7 +475,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         for (int it = 0; it < 8; ++it) {
             const int e = it * NT + tid;
             const int row = e >> 4, c0 = (e & 15) * 8;
-            *reinterpret_cast<uint4 *>(s.Mt + row * QS + c0) =
+            *reinterpret_cast<uint4 *>(s.Mt + swz_elem(row, c0)) =
                 *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
         }
     }
@@ -494,14 +500,14 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         const int t0 = c * CC;
         const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
-        store_chunk<CC, true>(s, tid, pf);
+        store_chunk<CC, true, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC, NT, CC>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
-        build_writes<CC, true, false>(s, tid, m);
+        build_writes_swz<CC, true, false, NT, CSW>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
-        score_tiles<CC>(s, s.Qs, s.Ks, w, lane);
+        score_tiles<CC>(s, s.Qs, smem, Ly::K, w, lane);
         f32x16 oacc[RB];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) oacc[rb] = zero_acc();
@@ -521,7 +527,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int ks = 0; ks < 2 * (rb + 1); ++ks)   // causal: row block rb sees columns < 32 (rb + 1)
-                oacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(At + 16 * ks * QS, QS),
+                oacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(At + 16 * ks * SWS, SWS),
                                oacc[rb]);
         {
             // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec (decay kept in L)
@@ -534,10 +540,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 ad_w = decay_rows(lds8_tr(At + 16 * ks * QS, QS), dw_l + 16 * ks);
+                const bf16x8 ad_w = decay_rows(lds8_tr(At + 16 * ks * SWS, SWS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
-                    kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
+                    kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Kt) ^ (64 * x)) + 16 * ks * SWS, SWS), ad_w,
+                                  kacc[x]);
             }
         }
         // -- middle step 1: X_r = U(lambda_r) O'_r, times scale log2(e) -> X tile (reuses Q's)
@@ -548,7 +555,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 const int ro = acc_off(rb, v);
                 const float self = oacc[rb][v];
                 const float part = swap_pair(self);
-                const half2v cs = CS_l[ro * 64];
+                const half2v cs = CS_l[ro * CSW];
                 X_l[ro * QS] = (__bf16)fmaf(sgn * (float)cs[1], part, (float)cs[0] * self);
             }
         __syncthreads();
@@ -560,7 +567,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             for (int nb = 0; nb < RB; ++nb) zacc[nb] = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 ma = lds8(Mza + 16 * ks);
+                const bf16x8 ma = lds8(lds_at<__bf16>(smem, opq(Mza) ^ (32 * ks)));
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     zacc[nb] = mma(ma, lds8(Xa + 32 * nb * QS + 16 * ks), zacc[nb]);
@@ -639,7 +646,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             for (int nb = 0; nb < RB; ++nb) yacc[nb] = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 mt = lds8_tr(Myt + 16 * ks * QS, QS);
+                const bf16x8 mt = lds8_tr(Myt + 16 * ks * SWS, SWS);
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     yacc[nb] = mma(mt, lds8(Xa + 32 * nb * QS + 16 * ks), yacc[nb]);
@@ -647,7 +654,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) {
                 const int r = 32 * nb + l32;
-                const half2v *csr = CSrow + 32 * nb * 64;
+                const half2v *csr = CSrow + 32 * nb * CSW;
                 __bf16 *orow = O2row + 32 * nb * QS;
 #pragma unroll
                 for (int v4 = 0; v4 < 4; ++v4) {
@@ -666,7 +673,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
         __syncthreads();
         // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V
-        score_tiles<CC>(s, s.Os, s.As, w, lane);
+        score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane);
         f32x16 pacc[RB];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) pacc[rb] = zero_acc();
@@ -686,13 +693,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int ks = 0; ks < 2 * (rb + 1); ++ks)
-                pacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(Vt + 16 * ks * QS, QS),
+                pacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(Vt + 16 * ks * SWS, SWS),
                                pacc[rb]);
         // output tile -> staging for 16-byte global stores
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * 128] = (__bf16)pacc[rb][v];
+            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
         {
             // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
             const float sf = s.ctl[0];
@@ -704,10 +711,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 v_w = decay_rows(lds8_tr(Vt + 16 * ks * QS, QS), dw_l + 16 * ks);
+                const bf16x8 v_w = decay_rows(lds8_tr(Vt + 16 * ks * SWS, SWS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
-                    vacc[x] = mma(lds8_tr(Atx + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
+                    vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Atx) ^ (64 * x)) + 16 * ks * SWS, SWS), v_w,
+                                  vacc[x]);
             }
         }
         __syncthreads();
@@ -718,7 +726,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 const int r = r0 + 16 * it;
                 if (r < n)
                     *reinterpret_cast<uint4 *>(o + (((size_t)b * p.T + t0 + r) * p.H + h) * D + d0) =
-                        *reinterpret_cast<const uint4 *>(Stg + 16 * it * 128);
+                        *reinterpret_cast<const uint4 *>(Stg + 16 * it * QS);
             }
         }
     }

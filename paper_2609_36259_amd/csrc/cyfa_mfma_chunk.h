@@ -104,16 +104,20 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     }
 }
 
-// Registers -> LDS, row-major tiles.
-template <int CC, bool kWithQ, int NTH = NT>
+// Registers -> LDS, row-major tiles (Q padded to stride QS; K and V padded too,
+// or swizzled when kSwzKV).  Each group of 16 lanes stores one whole row.
+template <int CC, bool kWithQ, int NTH = NT, bool kSwzKV = false>
 __device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefetch<CC, NTH> &pf) {
     constexpr int kRows = NTH / 16;
+    static_assert(kRows % 4 == 0, "row passes keep the swizzle phase");
     const int off = (tid >> 4) * QS + (tid & 15) * 8;
+    const int kvs = kSwzKV ? SWS : QS;
+    const int kvo = kSwzKV ? swz_elem(tid >> 4, (tid & 15) * 8) : off;
 #pragma unroll
     for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
         if (kWithQ) *reinterpret_cast<uint4 *>(s.Qs + off + kRows * it * QS) = pf.q[it];
-        *reinterpret_cast<uint4 *>(s.Ks + off + kRows * it * QS) = pf.k[it];
-        *reinterpret_cast<uint4 *>(s.Vs + off + kRows * it * QS) = pf.v[it];
+        *reinterpret_cast<uint4 *>(s.Ks + kvo + kRows * it * kvs) = pf.k[it];
+        *reinterpret_cast<uint4 *>(s.Vs + kvo + kRows * it * kvs) = pf.v[it];
     }
 }
 
@@ -220,6 +224,74 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
             *reinterpret_cast<half8v *>(s.CS + r * 64 + NP * q + 4 * k8) = cs8;
         }
         if (kAd) *reinterpret_cast<bf16x8 *>(s.Ads + r * QS + NCOL * q + 8 * k8) = ad8;
+    }
+}
+
+// The same matrices stored into swizzled A / A_dec tiles, 16 threads per row so
+// that each group of 16 lanes stores one whole row, and a (cos, sin) table of
+// row stride CSW half2 words.  Thread (r, q) fills internal columns 8q .. 8q+7
+// (pairs 4q+1 .. 4q+4) of rows r = tid / 16 + (NTH / 16) it; q = 15 also holds
+// DC (column 126) and the padding (127).
+template <int CC, bool kA, bool kAd, int NTH, int CSW>
+__device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m) {
+    constexpr int RPP = NTH / 16;                    // rows per pass
+    static_assert(CC % RPP == 0 && RPP % 4 == 0, "whole passes with a fixed swizzle phase");
+    const int q = tid & 15, r0 = tid >> 4;
+    const int J = (m - 1) >> 1;
+    const float dc = 1.0f / sqrtf((float)m);
+    const float sq = sqrtf(2.0f / (float)m);
+    const int pc = swz_elem(r0, 8 * q) - r0 * SWS;   // stored column of this thread's chunk
+    // rows one after another: interleaving them raises the register peak of the
+    // fused kernel, which holds the carried states and the prefetched chunk here
+#pragma unroll 1
+    for (int it = 0; it < CC / RPP; ++it) {
+        const int r = r0 + RPP * it;
+        const float be = s.betas[r];
+        const float bac = be * sq;
+        const float wdec = kAd ? s.decw[r] : 0.f;
+        const float u = s.urev[r];
+        float s1, c1, sn, cs;
+        sincos_rev(u, &s1, &c1);
+        {
+            double rev = (double)(4 * q + 1) * (double)u;
+            rev -= floor(rev);
+            sincos_rev((float)rev, &sn, &cs);
+        }
+        bf16x8 a8, ad8;
+        half8v cs8;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int j = 4 * q + 1 + jj;
+            const bool live = j <= J && j <= 63;
+            const float cv = live ? cs : 0.f;
+            const float sv = live ? sn : 0.f;
+            float a0 = bac * cv, a1 = -bac * sv;
+            if (jj == 3 && q == 15) {
+                a0 = be * dc;                        // internal column 126: DC
+                a1 = 0.f;                            // 127: padding
+            }
+            a8[2 * jj] = (__bf16)a0;
+            a8[2 * jj + 1] = (__bf16)a1;
+            if (kAd) {
+                ad8[2 * jj] = (__bf16)(a0 * wdec);
+                ad8[2 * jj + 1] = (__bf16)(a1 * wdec);
+            }
+            // table entry 63 (DC and padding) is (1, 0): the token-wise rotations
+            // pass those columns through unchanged
+            cs8[2 * jj] = (_Float16)(j == 64 ? 1.f : cv);
+            cs8[2 * jj + 1] = (_Float16)sv;
+            if (jj < 3) {
+                const float nc = cs * c1 - sn * s1;
+                const float ns = sn * c1 + cs * s1;
+                cs = nc;
+                sn = ns;
+            }
+        }
+        if (kA) {
+            *reinterpret_cast<bf16x8 *>(s.As + r * SWS + pc) = a8;
+            *reinterpret_cast<half8v *>(s.CS + r * CSW + 4 * q) = cs8;
+        }
+        if (kAd) *reinterpret_cast<bf16x8 *>(s.Ads + r * SWS + pc) = ad8;
     }
 }
 

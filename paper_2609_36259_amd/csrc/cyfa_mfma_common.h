@@ -110,6 +110,27 @@ __device__ __forceinline__ bf16x8 lds8_tr(const __bf16 *p, int stride) {
     return r;
 }
 
+// ---- swizzled tiles -----------------------------------------------------------
+// Rows of 128 bf16 with no padding (256 bytes, one pass over the 64 banks); the
+// 16-byte chunk c of row r is stored at chunk c ^ 4 (r mod 4).  A transpose read
+// covers 4 consecutive rows x 32 columns per half-wave: the swizzle puts those
+// four 64-byte pieces in the four different quarters of the bank window, where
+// a padded row stride leaves them overlapping.  Row reads and stores in which
+// each group of 16 lanes covers one whole row are unaffected.  Stores of partial
+// rows into a swizzled tile are slow on this LDS and are not used.
+constexpr int SWS = 128;
+__host__ __device__ __forceinline__ constexpr int swz_elem(int r, int col) {
+    return r * SWS + ((((col >> 3) ^ ((r & 3) << 2))) << 3) + (col & 7);
+}
+// Byte offset, in a swizzled tile, of a lane's transposed-operand block at rows
+// 0.., column block 0 (row 8 (g/2) + s/4, column 16 (g mod 2) + 4 (s mod 4), as
+// tr_off).  Column block y (32 columns) is this offset ^ 64 y; the upper four
+// rows of lds8_tr are 4 rows (1 KiB) further, and each 16 rows 4 KiB further.
+__device__ __forceinline__ int tr_off_swz(int lane) {
+    const int s = lane & 15, g = lane >> 4;
+    return 2 * swz_elem(8 * (g >> 1) + (s >> 2), 16 * (g & 1) + 4 * (s & 3));
+}
+
 // registers 8*half .. 8*half+7 of an accumulator as a bf16 B operand
 __device__ __forceinline__ bf16x8 acc_to_operand(const f32x16 &acc, int half) {
     bf16x8 r;

@@ -57,8 +57,8 @@ struct Lay {
     static_assert(K % 256 == 0 && V % 256 == 0 && A % 256 == 0 && MT % 256 == 0,
                   "swizzled tiles start on a bank-window boundary");
     static_assert(CC != 32 || BYTES <= 80 * 1024, "two workgroups per compute unit");
-    // state pre-pass: K, V, A_dec and the scalars (64 entries)
-    static constexpr int PK = 0, PV = TILE, PAD = 2 * TILE, PSC = 3 * TILE;
+    // state pre-pass: K, V, A_dec (swizzled) and the scalars (64 entries)
+    static constexpr int PK = 0, PV = STILE, PAD = 2 * STILE, PSC = 3 * STILE;
     static constexpr int PBYTES = PSC + scalar_bytes(64);
 };
 
@@ -96,10 +96,12 @@ __device__ __forceinline__ Tiles prepass_tiles(char *smem) {
 
 // Carried-state updates of one chunk (App. B):
 //   Kbar^T <- gamma^C Kbar^T + K^T A_dec,   Vbar <- gamma^C Vbar + A_dec^T V
-// Operands: K^T, A_dec and V come from row-major tiles through transpose reads.
+// Operands: K^T, A_dec and V come from swizzled row-major tiles through
+// transpose reads (column block x of a tile at the lane's offset ^ 64 x).
 template <int CC>
-__device__ __forceinline__ void update_states(const Tiles &s, int w, int lane,
+__device__ __forceinline__ void update_states(const Tiles &s, char *smem, int w, int lane,
                                               f32x16 (&kacc)[4], f32x16 (&vacc)[4]) {
+    using L = Lay<CC>;
     const float sf = s.ctl[0];
     if (sf != 1.f) {
 #pragma unroll
@@ -110,17 +112,18 @@ __device__ __forceinline__ void update_states(const Tiles &s, int w, int lane,
                 vacc[x][v] *= sf;
             }
     }
-    const __bf16 *Kt = tr_base(s.Ks, QS, lane);
-    const __bf16 *Vt = tr_base(s.Vs, QS, lane) + 32 * w;
-    const __bf16 *Adt = tr_base(s.Ads, QS, lane);
+    const int trs = tr_off_swz(lane);
+    const int Kt = opq(L::PK + trs), Adt = opq(L::PAD + trs);
+    const __bf16 *Vt = lds_at<__bf16>(smem, opq(L::PV + (trs ^ (64 * w))));
+    const __bf16 *Adw = lds_at<__bf16>(smem, opq(L::PAD + (trs ^ (64 * w))));
 #pragma unroll
     for (int ks = 0; ks < CC / 16; ++ks) {
-        const bf16x8 ad_w = lds8_tr(Adt + 16 * ks * QS + 32 * w, QS);
-        const bf16x8 v_w = lds8_tr(Vt + 16 * ks * QS, QS);
+        const bf16x8 ad_w = lds8_tr(Adw + 16 * ks * SWS, SWS);
+        const bf16x8 v_w = lds8_tr(Vt + 16 * ks * SWS, SWS);
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
-            kacc[x] = mma(lds8_tr(Kt + 16 * ks * QS + 32 * x, QS), ad_w, kacc[x]);
-            vacc[x] = mma(lds8_tr(Adt + 16 * ks * QS + 32 * x, QS), v_w, vacc[x]);
+            kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Kt) ^ (64 * x)) + 16 * ks * SWS, SWS), ad_w, kacc[x]);
+            vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Adt) ^ (64 * x)) + 16 * ks * SWS, SWS), v_w, vacc[x]);
         }
     }
 }
@@ -200,7 +203,7 @@ __device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32
 // ---- 1. per-segment state contributions -------------------------------------
 template <int CC>
 __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
-    __shared__ __attribute__((aligned(16))) char smem[Lay<CC>::PBYTES];
+    __shared__ __attribute__((aligned(256))) char smem[Lay<CC>::PBYTES];
     const Tiles s = prepass_tiles<CC>(smem);
     const int Pm1 = a.P - 1;
     const int bh = blockIdx.x / Pm1, p = blockIdx.x % Pm1;
@@ -218,13 +221,13 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
     Prefetch<CC> pf;
     load_chunk<CC, false>(a.p, b, h, c_begin * CC, tid, pf);
     for (int c = c_begin; c < c_end; ++c) {
-        store_chunk<CC, false>(s, tid, pf);
+        store_chunk<CC, false, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
-        build_writes<CC, false, true>(s, tid, a.p.m);
+        build_writes_swz<CC, false, true, NT, 64>(s, tid, a.p.m);
         __syncthreads();
-        update_states<CC>(s, w, lane, kacc, vacc);
+        update_states<CC>(s, smem, w, lane, kacc, vacc);
         __syncthreads();
     }
     const size_t slot = (size_t)bh * a.P + p;

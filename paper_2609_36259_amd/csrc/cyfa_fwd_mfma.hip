@@ -128,11 +128,6 @@ __device__ __forceinline__ void update_states(const Tiles &s, char *smem, int w,
     }
 }
 
-// row offset (within a tile, excluding the lane's 4h) of accumulator register v of block blk
-__device__ __forceinline__ constexpr int acc_off(int blk, int v) {
-    return 32 * blk + 8 * (v >> 2) + (v & 3);
-}
-
 // One 16 x 16 block (rb, sb) of the causal score tile (S (.) Gamma) -> Ss (bf16),
 // k = 128 along the rows of both operand tiles: A rows from a padded tile, B rows
 // from the swizzled tile at byte offset Boff (column block ks of a row is its
@@ -429,11 +424,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
     const int m = p.m;
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
-    const int icol = 32 * w + l32;                   // this lane's internal column
+    const int icol = 32 * w + l32;                   // this lane's slot (readout step)
     const int h4 = 4 * hl;
-    // U(theta) on a (cos, sin) pair held by lanes (2k, 2k+1): c x - s x' on the cos
-    // lane, c x + s x' on the sin lane
-    const float sgn = (icol & 1) ? 1.f : -1.f;
 
     // the readout matrix in LDS is M times zs = scale log2(e): slot logits come out in
     // log2 units, and the readout weights are divided by zs to compensate
@@ -444,16 +436,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     constexpr int TE = Ly::TILE / 2;                                      // padded tile size in elements
     constexpr int CSW = Ly::CSW;
     const int trs = tr_off_swz(lane);
-    const float *gam_l = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + h4)));           // gam, accumulator rows
+    const float *gam_t = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + l32)));          // gam of token l32
     const float *dw_l = lds_at<float>(smem, opq(Ly::SC + 4 * (3 * CC + 8 * hl)));    // decw, operand tokens
     // M rows (slot icol), columns 8 hl + 16 ks at byte offset Mza ^ 32 ks
     const int Mza = opq(Ly::MT + 2 * swz_elem(icol, 8 * hl));
     const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + (trs ^ (64 * w))));          // M columns
-    const half2v *CS_l = lds_at<half2v>(smem, opq(Ly::CS + 4 * (h4 * CSW + (icol >> 1))));
-    __bf16 *X_l = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (h4 * QS + icol)));           // X (then W) tile
-    // output staging: [CC][QS] bf16 in the (cos, sin) table, which is free from the
-    // O'' rotation until the next chunk's temporal writes
-    __bf16 *St_l = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (h4 * QS + icol)));
     const __bf16 *Qperm = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + h4)));   // permuted-k A operands
     const __bf16 *Operm = Qperm + TE;
     const __bf16 *Xa = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 8 * hl)));  // natural-k operands
@@ -463,9 +450,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const __bf16 *Vt = lds_at<__bf16>(smem, opq(Ly::V + (trs ^ (64 * w))));
     const int Atx = opq(Ly::A + trs);
     const int Kt = opq(Ly::K + trs);
-    // token-row bases of the readout step: row l32 (+ 32 nb), columns 32w + 4hl ..
+    // token-row bases: row l32, columns 32w + 4hl (+ 8 v4) of the X / W, O'' and
+    // output-staging tiles and the matching (cos, sin) pairs
     __bf16 *Wrow = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 32 * w + h4)));
     __bf16 *O2row = Wrow + TE;
+    // output staging: [CC][QS] bf16 in the (cos, sin) table, which is free from the
+    // O'' rotation until the next chunk's temporal writes
+    __bf16 *Strow = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (l32 * QS + 32 * w + h4)));
     const half2v *CSrow = lds_at<half2v>(smem, opq(Ly::CS + 4 * (l32 * CSW + 16 * w + 2 * hl)));
     float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
     const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
@@ -509,29 +500,24 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
         build_writes_swz<CC, true, false, NT, CSW>(s, tid, m);
         __syncthreads();
-        // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A
+        // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A, computed
+        //    transposed: O'^T = (Kbar Q^T) gamma + A^T (S (.) Gamma)^T.  Wave w owns basis
+        //    rows 32w .. 32w+31; lane (token l32, half hl) holds 16 of them, so each
+        //    (cos, sin) pair sits in two consecutive registers of one lane.
         score_tiles<CC>(s, s.Qs, smem, Ly::K, w, lane);
-        f32x16 oacc[RB];
+        f32x16 oacc = zero_acc();
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) oacc[rb] = zero_acc();
+        for (int ks = 0; ks < 8; ++ks)
+            oacc = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(Qperm, 16 * ks, 0), oacc);
+        {
+            const float gt = *gam_t;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            const bf16x8 kb = acc_to_operand(kacc[ks >> 1], ks & 1);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-                oacc[rb] = mma(lds8_perm(Qperm + 32 * rb * QS, 16 * ks, 0), kb, oacc[rb]);
+            for (int v = 0; v < 16; ++v) oacc[v] *= gt;
         }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) oacc[rb][v] *= gam_l[acc_off(rb, v)];
         __syncthreads();
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int ks = 0; ks < 2 * (rb + 1); ++ks)   // causal: row block rb sees columns < 32 (rb + 1)
-                oacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(At + 16 * ks * SWS, SWS),
-                               oacc[rb]);
+        for (int ks = 0; ks < CC / 16; ++ks)
+            oacc = mma(lds8_tr(At + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), oacc);
         {
             // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec (decay kept in L)
             const float sf = s.ctl[0];
@@ -550,17 +536,20 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                                   kacc[x]);
             }
         }
-        // -- middle step 1: X_r = U(lambda_r) O'_r, times scale log2(e) -> X tile (reuses Q's)
+        // -- middle step 1: X_r = U(lambda_r) O'_r -> X tile [token][basis] (reuses Q's)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
+        for (int v4 = 0; v4 < 4; ++v4) {
+            bf16x4 xv;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int ro = acc_off(rb, v);
-                const float self = oacc[rb][v];
-                const float part = swap_pair(self);
-                const half2v cs = CS_l[ro * CSW];
-                X_l[ro * QS] = (__bf16)fmaf(sgn * (float)cs[1], part, (float)cs[0] * self);
+            for (int k2 = 0; k2 < 2; ++k2) {
+                const half2v cs = CSrow[4 * v4 + k2];
+                const float c = (float)cs[0], sn = (float)cs[1];
+                const float xc = oacc[4 * v4 + 2 * k2], xs = oacc[4 * v4 + 2 * k2 + 1];
+                xv[2 * k2] = (__bf16)fmaf(-sn, xs, c * xc);
+                xv[2 * k2 + 1] = (__bf16)fmaf(sn, xc, c * xs);
             }
+            *reinterpret_cast<bf16x4 *>(Wrow + 8 * v4) = xv;
+        }
         __syncthreads();
         // -- middle step 2: slot logits, transposed: Z^T = M X^T.  Wave w owns slots
         //    32w .. 32w+31; lane (token 32 nb + l32, half hl) holds 16 of them.
@@ -675,34 +664,31 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
         }
         __syncthreads();
-        // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V
+        // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V, computed
+        //    transposed like the key pass: lane (token l32, half hl) holds 16 output
+        //    columns of wave w's block 32w .. 32w+31.
         score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane);
-        f32x16 pacc[RB];
+        f32x16 pacc = zero_acc();
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) pacc[rb] = zero_acc();
+        for (int ks = 0; ks < 8; ++ks)
+            pacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(Operm, 16 * ks, 0), pacc);
+        {
+            const float gt = *gam_t;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            const bf16x8 vb = acc_to_operand(vacc[ks >> 1], ks & 1);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-                pacc[rb] = mma(lds8_perm(Operm + 32 * rb * QS, 16 * ks, 0), vb, pacc[rb]);
+            for (int v = 0; v < 16; ++v) pacc[v] *= gt;
         }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) pacc[rb][v] *= gam_l[acc_off(rb, v)];
         __syncthreads();
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
+        for (int ks = 0; ks < CC / 16; ++ks)
+            pacc = mma(lds8_tr(Vt + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), pacc);
+        // output tile -> staging [token][column] for 16-byte global stores
 #pragma unroll
-            for (int ks = 0; ks < 2 * (rb + 1); ++ks)
-                pacc[rb] = mma(lds8(Sa + 32 * rb * SSC + 16 * ks), lds8_tr(Vt + 16 * ks * SWS, SWS),
-                               pacc[rb]);
-        // output tile -> staging for 16-byte global stores
+        for (int v4 = 0; v4 < 4; ++v4) {
+            bf16x4 ov;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) St_l[acc_off(rb, v) * QS] = (__bf16)pacc[rb][v];
+            for (int k = 0; k < 4; ++k) ov[k] = (__bf16)pacc[4 * v4 + k];
+            *reinterpret_cast<bf16x4 *>(Strow + 8 * v4) = ov;
+        }
         {
             // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
             const float sf = s.ctl[0];

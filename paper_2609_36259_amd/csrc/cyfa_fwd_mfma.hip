@@ -129,9 +129,10 @@ __device__ __forceinline__ void update_states(const Tiles &s, char *smem, int w,
 }
 
 // One 16 x 16 block (rb, sb) of the causal score tile (S (.) Gamma) -> Ss (bf16),
-// k = 128 along the rows of both operand tiles: A rows from a padded tile, B rows
-// from the swizzled tile at byte offset Boff (column block ks of a row is its
-// first block's offset ^ 64 ks).
+// k = 128 along the rows of both operand tiles: token rows t from a padded tile,
+// rows s from the swizzled tile at byte offset Boff (column block ks of a row is
+// its first block's offset ^ 64 ks).  Computed transposed, D[s][t], so that each
+// lane stores four consecutive entries S[t][s .. s+3] at once.
 template <int CC>
 __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, char *smem, int Boff,
                                             int rb, int sb, int lane) {
@@ -142,15 +143,16 @@ __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, 
     const int bo = Boff + 2 * swz_elem(16 * sb + l16, 8 * g);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
-        acc = mma16(lds8(ap + 32 * ks), lds8(lds_at<__bf16>(smem, opq(bo) ^ (64 * ks))), acc);
-    const int scol = 16 * sb + l16;
-    const int row0 = 16 * rb + 4 * g;
-    const float Gs_col = s.Gs[scol];
+        acc = mma16(lds8(lds_at<__bf16>(smem, opq(bo) ^ (64 * ks))), lds8(ap + 32 * ks), acc);
+    const int t = 16 * rb + l16;
+    const int s0 = 16 * sb + 4 * g;
+    const float Gt = s.Gs[t];
+    const float4 G4 = *reinterpret_cast<const float4 *>(s.Gs + s0);
+    const float Gv[4] = {G4.x, G4.y, G4.z, G4.w};
+    bf16x4 sv;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const float val = scol <= row0 + r ? acc[r] * __expf(s.Gs[row0 + r] - Gs_col) : 0.f;
-        s.Ss[(row0 + r) * SSC + scol] = (__bf16)val;
-    }
+    for (int r = 0; r < 4; ++r) sv[r] = (__bf16)(s0 + r <= t ? acc[r] * __expf(Gt - Gv[r]) : 0.f);
+    *reinterpret_cast<bf16x4 *>(s.Ss + t * SSC + s0) = sv;
 }
 
 // The 16 x 16 blocks of the causal CC x CC score tile that the intra-chunk

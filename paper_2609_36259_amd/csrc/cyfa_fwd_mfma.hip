@@ -175,25 +175,28 @@ __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4
         }
 }
 
-__device__ __forceinline__ void load_state(const float *st, int w, int lane, f32x16 (&kacc)[4],
+// Segment-boundary states travel in bf16 (the precision in which the chunk
+// products consume them); the carried states themselves accumulate in fp32.
+__device__ __forceinline__ void load_state(const __bf16 *st, int w, int lane, f32x16 (&kacc)[4],
                                            f32x16 (&vacc)[4]) {
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            kacc[x][v] = st[((w * 4 + x) * 16 + v) * 64 + lane];
-            vacc[x][v] = st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane];
+            kacc[x][v] = (float)st[((w * 4 + x) * 16 + v) * 64 + lane];
+            vacc[x][v] = (float)st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane];
         }
 }
 
-__device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32x16 (&kacc)[4],
+template <typename T>
+__device__ __forceinline__ void dump_state(T *st, int w, int lane, const f32x16 (&kacc)[4],
                                            const f32x16 (&vacc)[4]) {
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            st[((w * 4 + x) * 16 + v) * 64 + lane] = kacc[x][v];
-            st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane] = vacc[x][v];
+            st[((w * 4 + x) * 16 + v) * 64 + lane] = (T)kacc[x][v];
+            st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane] = (T)vacc[x][v];
         }
 }
 
@@ -345,19 +348,20 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
     double origin = reduce_clock(c0, (double)m, inv_m);
     // Segment contributions are fetched kBatch segments at a time, ahead of the
     // dependent chain through them.  Every thread owns the same offsets in every
-    // segment, so the loads of a batch never see this batch's stores.
+    // segment, so the loads of a batch never see this batch's stores.  The chain
+    // itself runs in fp32; contributions and entering states are stored as bf16.
     constexpr int kBatch = 8;
     for (int q0 = 0; q0 < a.P; q0 += kBatch) {
-        float4 da[kBatch], db[kBatch];
+        bf16x4 da[kBatch], db[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int q = q0 + u;
-            da[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            da[u] = bf16x4{};
             db[u] = da[u];
             if (q < a.P - 1) {
-                const float *st = a.seg_state + ((size_t)bh * a.P + q) * kStateFloats;
-                da[u] = *reinterpret_cast<const float4 *>(st + off0);
-                db[u] = *reinterpret_cast<const float4 *>(st + off1);
+                const __bf16 *st = a.seg_state + ((size_t)bh * a.P + q) * kStateFloats;
+                da[u] = *reinterpret_cast<const bf16x4 *>(st + off0);
+                db[u] = *reinterpret_cast<const bf16x4 *>(st + off1);
             }
         }
 #pragma unroll
@@ -365,20 +369,26 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
             const int q = q0 + u;
             if (q >= a.P) break;
             const size_t slot = (size_t)bh * a.P + q;
-            float *st = a.seg_state + slot * kStateFloats;
+            __bf16 *st = a.seg_state + slot * kStateFloats;
             if (qi == 0) a.seg_origin[slot] = origin;
             float d0[4], d1[4];
+            bf16x4 s0, s1;
             if (!value) {
-                *reinterpret_cast<float4 *>(st + off0) = make_float4(x0[0], x1[0], x0[1], x1[1]);
-                *reinterpret_cast<float4 *>(st + off1) = make_float4(x0[2], x1[2], x0[3], x1[3]);
-                d0[0] = da[u].x; d1[0] = da[u].y; d0[1] = da[u].z; d1[1] = da[u].w;
-                d0[2] = db[u].x; d1[2] = db[u].y; d0[3] = db[u].z; d1[3] = db[u].w;
+                s0[0] = (__bf16)x0[0]; s0[1] = (__bf16)x1[0]; s0[2] = (__bf16)x0[1]; s0[3] = (__bf16)x1[1];
+                s1[0] = (__bf16)x0[2]; s1[1] = (__bf16)x1[2]; s1[2] = (__bf16)x0[3]; s1[3] = (__bf16)x1[3];
+                d0[0] = (float)da[u][0]; d1[0] = (float)da[u][1]; d0[1] = (float)da[u][2]; d1[1] = (float)da[u][3];
+                d0[2] = (float)db[u][0]; d1[2] = (float)db[u][1]; d0[3] = (float)db[u][2]; d1[3] = (float)db[u][3];
             } else {
-                *reinterpret_cast<float4 *>(st + off0) = make_float4(x0[0], x0[1], x0[2], x0[3]);
-                *reinterpret_cast<float4 *>(st + off1) = make_float4(x1[0], x1[1], x1[2], x1[3]);
-                d0[0] = da[u].x; d0[1] = da[u].y; d0[2] = da[u].z; d0[3] = da[u].w;
-                d1[0] = db[u].x; d1[1] = db[u].y; d1[2] = db[u].z; d1[3] = db[u].w;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    s0[k] = (__bf16)x0[k];
+                    s1[k] = (__bf16)x1[k];
+                    d0[k] = (float)da[u][k];
+                    d1[k] = (float)db[u][k];
+                }
             }
+            *reinterpret_cast<bf16x4 *>(st + off0) = s0;
+            *reinterpret_cast<bf16x4 *>(st + off1) = s1;
             if (q < a.P - 1) {
                 const float gdec = __expf((float)a.seg_gsum[slot]);
                 const double span = a.seg_span[slot];    // already reduced to [0, m)
@@ -476,7 +486,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
     }
     f32x16 kacc[4], vacc[4];
-    float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
+    const __bf16 *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
     if (a.has_init) {
         load_state(slot_state, w, lane, kacc, vacc);
     } else {
@@ -723,7 +733,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     }
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));
-        dump_state(slot_state, w, lane, kacc, vacc);
+        dump_state(a.fin_state + (size_t)bh * kStateFloats, w, lane, kacc, vacc);
         if (tid == 0) a.final_lam[bh] = carry;
     }
 }
@@ -737,15 +747,24 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     const PairRef pr = pair_ref(gidx);
     const int j = (pr.i0 >> 1) + 1;
     const size_t slot = (size_t)bh * a.P + (a.P - 1);
-    const float *st = a.seg_state + slot * kStateFloats;
+    const float *st = a.fin_state + (size_t)bh * kStateFloats;
     const double origin = a.seg_origin[slot];
-    float x0 = st[pr.o0], x1 = st[pr.o1];
-    // local frame (origin at the last segment's start) -> absolute clock: U(-origin)
-    if (pr.i0 < kDC && j <= (m - 1) / 2) rotate_pair(ring_rev(-origin, m), j, x0, x1);
+    const size_t base = (size_t)bh * 128 * 128 + pr.col;
+    const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
+    float x0, x1;
+    if (a.nchunks > 0) {
+        x0 = st[pr.o0];
+        x1 = st[pr.o1];
+        // local frame (origin at the last segment's start) -> absolute clock: U(-origin)
+        if (pr.i0 < kDC && j <= (m - 1) / 2) rotate_pair(ring_rev(-origin, m), j, x0, x1);
+    } else {
+        // no tokens: the final state is the initial state (zero when none is given)
+        const float *init = pr.value ? a.p.V0 : a.p.K0;
+        x0 = init && p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
+        x1 = init && p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
+    }
     float *out = pr.value ? a.p.V_out : a.p.K_out;
     if (out) {
-        const size_t base = (size_t)bh * 128 * 128 + pr.col;
-        const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
         if (p0 >= 0) out[base + (size_t)p0 * 128] = x0;
         if (p1 >= 0) out[base + (size_t)p1 * 128] = x1;
         // padding rows m..127 of the ABI layout are written as zero (one writer per row)
@@ -772,7 +791,7 @@ int mfma_default_chunk() { return kMfmaDefaultChunk; }
 
 namespace {
 struct WsLayout {
-    size_t mz, state, span, gsum, origin, flam, total;
+    size_t mz, state, fin, span, gsum, origin, flam, total;
 };
 WsLayout ws_layout(const FwdParams &p, int P) {
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -782,7 +801,9 @@ WsLayout ws_layout(const FwdParams &p, int P) {
     off += up((size_t)p.H * 128 * 128 * 2);
     const size_t nseg = (size_t)p.B * p.H * P;
     L.state = off;
-    off += up(nseg * kStateFloats * 4);
+    off += up(nseg * kStateFloats * 2);
+    L.fin = off;
+    off += up((size_t)p.B * p.H * kStateFloats * 4);
     L.span = off;
     off += up(nseg * 8);
     L.gsum = off;
@@ -864,7 +885,8 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     if (a.nchunks > 0) a.P = (a.nchunks + a.cps - 1) / a.cps;   // no empty trailing segment
     if (a.P < 1) a.P = 1;
     a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
-    a.seg_state = reinterpret_cast<float *>(base + L.state);
+    a.seg_state = reinterpret_cast<__bf16 *>(base + L.state);
+    a.fin_state = reinterpret_cast<float *>(base + L.fin);
     a.seg_span = reinterpret_cast<double *>(base + L.span);
     a.seg_gsum = reinterpret_cast<double *>(base + L.gsum);
     a.seg_origin = reinterpret_cast<double *>(base + L.origin);

@@ -109,14 +109,14 @@ __device__ __forceinline__ void score_tiles16(const Tiles &s, const __bf16 *An, 
     if (w < 4) score_block16(s, An, Bn, Sw, kRb[8 + w], kSb[8 + w], lane);
 }
 
-__device__ __forceinline__ void load_state16(const float *st, int col, int g4, f32x4 (&kacc)[8],
+__device__ __forceinline__ void load_state16(const __bf16 *st, int col, int g4, f32x4 (&kacc)[8],
                                              f32x4 (&vacc)[8]) {
 #pragma unroll
     for (int x = 0; x < 8; ++x)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            kacc[x][r] = st[dump_index_K(col, 16 * x + g4 + r)];
-            vacc[x][r] = st[dump_index_V(16 * x + g4 + r, col)];
+            kacc[x][r] = (float)st[dump_index_K(col, 16 * x + g4 + r)];
+            vacc[x][r] = (float)st[dump_index_V(16 * x + g4 + r, col)];
         }
 }
 
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
         }
     }
     f32x4 kacc[8], vacc[8];
-    float *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
+    const __bf16 *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
     if (a.has_init) {
         load_state16(slot_state, col, g4, kacc, vacc);
     } else {
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
         }
     }
     if (a.want_final && seg == a.P - 1) {
-        dump_state16(slot_state, col, g4, kacc, vacc, __expf(s.ctl[1]));
+        dump_state16(a.fin_state + (size_t)bh * kStateFloats, col, g4, kacc, vacc, __expf(s.ctl[1]));
         if (tid == 0) a.final_lam[bh] = carry;
     }
 }

@@ -14,13 +14,15 @@ struct MfmaArgs {
     int nchunks;         // chunks per sequence
     int chunk;           // chunk length (32 or 64)
     const __bf16 *Mz;    // [H][128][128]  row = slot i', column = internal basis j; times scale log2(e)
-    float *seg_state;    // [B*H*P][2*128*128] accumulator-dump layout
+    __bf16 *seg_state;   // [B*H*P][2*128*128] accumulator-dump layout, bf16: segment
+                         // contributions, then the states entering each segment
+    float *fin_state;    // [B*H][2*128*128] same layout, fp32: state after the last segment
     double *seg_span;    // [B*H*P] clock span of each segment (reduced mod m)
     double *seg_gsum;    // [B*H*P] sum of log alpha over each segment
     double *seg_origin;  // [B*H*P] absolute clock at each segment start (reduced)
     double *final_lam;   // [B*H] local clock after the last segment (reduced)
     int has_init;        // segment-entry states are read from seg_state
-    int want_final;      // last segment dumps its final state into seg_state
+    int want_final;      // last segment dumps its final state into fin_state
 };
 
 // fused forward for 64-token chunks on eight waves (one workgroup per (b, h, p))

@@ -6,11 +6,16 @@
 //      the carried states, DeltaS_p = sum_t (decay to segment end) a_t [k_t | v_t]^T,
 //      with the clock origin at the segment start, plus the segment's clock span
 //      and log-decay total.  App. B's state recurrence run from a zero state.
-//   2. segment_scan_kernel  (b, h): the states entering every segment,
+//   2. scan_prep_kernel  (b, h): the states entering every segment,
 //      S'_{p+1} = U(span_p) (exp(gsum_p) S'_p + DeltaS_p), each expressed with its
 //      own segment-start clock origin.  Moving the origin rotates an
 //      absolute-clock state by U(-c) and leaves the output unchanged
 //      (App. A.4, Prop. 6), which is what makes the segments independent.
+//      The recurrence runs in fp32; the contributions and entering states are
+//      stored in bf16, the precision in which the chunk products consume them.
+//      Extra blocks of the same launch form the bf16 readout matrix
+//      M_h = R_h Phi (times scale log2 e) for step 3.  (Without a scan the
+//      readout preparation is launched on its own.)
 //   3. chunk_forward_kernel  (b, h, p): the fused forward of App. B over the
 //      segment's chunks: clock/log-decay prefix sums, temporal write matrix
 //      A (Eq. app-temporal-writes), key pass (Eq. app-cyfa-key-chunk), token-wise
@@ -20,6 +25,7 @@
 //   4. state_out_kernel  (b, h): rotates the last segment's final state back to
 //      the absolute clock and writes it in the ABI layout (only when asked).
 #include "cyfa_mfma_chunk.h"
+#include "cyfa_prep.h"
 
 namespace cyfa {
 
@@ -295,13 +301,14 @@ __device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x
     x1 = y1;
 }
 
-// Thread = four rotation pairs moved with two 16-byte accesses per segment: key
-// state, 8 consecutive words (pairs are adjacent lanes); value state, 4
-// consecutive lanes of registers v and v + 1 (pairs are register pairs, and the
-// four share one frequency).  grid (B*H, 16): 2048 key and 2048 value threads.
-__global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
-    const int bh = blockIdx.x;
-    const int qi = blockIdx.y * NT + threadIdx.x;        // 0 .. 4095
+// Thread = four rotation pairs moved with two 8-byte (4 x bf16) accesses per
+// segment: key state, 8 consecutive entries (pairs are adjacent lanes); value
+// state, 4 consecutive lanes of registers v and v + 1 (pairs are register
+// pairs, and the four share one frequency).  Blocks (bh, y < 16) of 256
+// threads: 2048 key and 2048 value threads per (b, h).
+constexpr int kScanBlocks = 4096 / NT;                   // blocks per (b, h)
+__device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, int tid) {
+    const int qi = y * NT + tid;                         // 0 .. 4095
     const int m = a.p.m;
     const bool value = qi >= 2048;
     int off0, off1;                                      // dump offsets of the two float4
@@ -402,6 +409,19 @@ __global__ __launch_bounds__(NT) void segment_scan_kernel(MfmaArgs a) {
                 origin = reduce_clock(origin + span, (double)m, inv_m);
             }
         }
+    }
+}
+
+// The segment scan and the readout preparation (needed only by the fused kernel)
+// in one launch: blocks [0, nscan) scan, the rest form M_h = R_h Phi.
+__global__ __launch_bounds__(NT) void scan_prep_kernel(MfmaArgs a, int nscan, float mz_scale) {
+    const int b = blockIdx.x;
+    if (b < nscan) {
+        segment_scan(a, b / kScanBlocks, b % kScanBlocks, threadIdx.x);
+    } else {
+        const int q = b - nscan;
+        readout_prep_block(a.p.m, a.p.R, nullptr, const_cast<__bf16 *>(a.Mz), mz_scale,
+                           q / (kStoreRows / kPrepRows), q % (kStoreRows / kPrepRows), threadIdx.x);
     }
 }
 
@@ -836,9 +856,16 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
+    const float mz_scale = a.p.scale * 1.4426950408889634f;
     if (a.has_init) {
-        hipLaunchKernelGGL(segment_scan_kernel, dim3(BH, 4096 / NT), dim3(NT), 0, st, a);
+        const int nscan = BH * kScanBlocks;
+        const int nprep = a.p.H * (kStoreRows / kPrepRows);
+        hipLaunchKernelGGL(scan_prep_kernel, dim3(nscan + nprep), dim3(NT), 0, st, a, nscan, mz_scale);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else if ((e = launch_readout_prep(a.p.H, a.p.m, a.p.R, nullptr, const_cast<__bf16 *>(a.Mz),
+                                        mz_scale, st)) != hipSuccess) {
+        return e;
     }
     if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
     if (a.nchunks > 0) {
@@ -895,11 +922,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     const int BH = p.B * p.H;
 
-    // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
-    hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, const_cast<__bf16 *>(a.Mz),
-                                       p.scale * 1.4426950408889634f, st);
-    if (e != hipSuccess) return e;
-    e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
+    hipError_t e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
     if (e != hipSuccess) return e;
     if (a.want_final) {
         hipLaunchKernelGGL(state_out_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);

@@ -1,82 +1,13 @@
-// Readout preparation: M_h = R_h Phi for every head.
-//
-// The absolute-clock readout (Sec. 3.2, Eq. cyfa-absolute-readout) applies
-// R Phi U(lambda) to the key-pass output and U(-lambda) Phi^T R^T to the slot
-// weights.  Both use the same m x m matrix M = R Phi, so it is formed once per
-// call.  Phi is the real Fourier basis of App. A.1 (Eq. app-real-fourier):
-// column 0 = 1/sqrt(m), column 2l-1 = sqrt(2/m) cos(2 pi l s / m), column
-// 2l = sqrt(2/m) sin(2 pi l s / m).  Output [H][128][128], slot index on rows,
-// basis index on columns, zero outside the active m x m block.
-#include "cyfa_internal.h"
+// Readout preparation kernel (M_h = R_h Phi for every head); the per-block
+// computation is in cyfa_prep.h.
+#include "cyfa_prep.h"
 
 namespace cyfa {
 
-constexpr int kPrepRows = 4;          // rows of M_h per workgroup (two per thread)
-
-// grid (H, 128 / kPrepRows): block (h, rb) computes rows [4 rb, 4 rb + 4) of M_h.
-// Thread (j = tid % 128, g = tid / 128) owns paper basis column j and rows
-// 4 rb + 2 g, 4 rb + 2 g + 1.  Phi[s][j] is read from a table of the m angles
-// 2 pi r / m: the index (l s) mod m advances by l per step, with no division.
-// M (fp32, paper basis order) and/or Mz (bf16, the matrix-core kernels' basis
-// order: Mz[i'][j_int] = mz_scale * M[i'][paper(j_int)]) are written when non-null.
 __global__ __launch_bounds__(256) void readout_prep_kernel(int m, const float *__restrict__ R,
                                                            float *__restrict__ M,
                                                            __bf16 *__restrict__ Mz, float mz_scale) {
-    __shared__ float tab[2][kMaxActive];                     // cos, sin of 2 pi r / m
-    __shared__ float Rrows[kPrepRows][kMaxActive + 1];
-    const int h = blockIdx.x;
-    const int row0 = blockIdx.y * kPrepRows;
-    const int tid = threadIdx.x;
-    if (tid < m) {
-        double sn, cs;
-        sincospi(2.0 * (double)tid / (double)m, &sn, &cs);
-        tab[0][tid] = (float)cs;
-        tab[1][tid] = (float)sn;
-    }
-    const float *Rh = R ? R + (size_t)h * m * m : nullptr;
-    for (int e = tid; e < kPrepRows * m; e += blockDim.x) {
-        const int r = e / m, s = e % m;
-        const int i = row0 + r;
-        Rrows[r][s] = i < m ? (Rh ? Rh[(size_t)i * m + s] : (s == i ? 1.f : 0.f)) : 0.f;
-    }
-    __syncthreads();
-    const int j = tid & 127, r0 = 2 * (tid >> 7);
-    float acc0 = 0.f, acc1 = 0.f;
-    if (j == 0) {
-        for (int s = 0; s < m; ++s) {
-            acc0 += Rrows[r0][s];
-            acc1 += Rrows[r0 + 1][s];
-        }
-        const float dc = (float)(1.0 / sqrt((double)m));
-        acc0 *= dc;
-        acc1 *= dc;
-    } else if (j < m) {
-        const int l = (j + 1) >> 1;                          // frequency of the column
-        const float *t = tab[(j & 1) ? 0 : 1];               // odd columns cos, even sin
-        int idx = 0;
-#pragma unroll 4
-        for (int s = 0; s < m; ++s) {
-            const float ph = t[idx];
-            acc0 = fmaf(Rrows[r0][s], ph, acc0);
-            acc1 = fmaf(Rrows[r0 + 1][s], ph, acc1);
-            idx += l;
-            if (idx >= m) idx -= m;
-        }
-        const float ac = (float)sqrt(2.0 / (double)m);
-        acc0 *= ac;
-        acc1 *= ac;
-    }
-    const bool live = j < m;
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        const int i = row0 + r0 + k;
-        const float val = (live && i < m) ? (k ? acc1 : acc0) : 0.f;
-        if (M) M[((size_t)h * kStoreRows + i) * kStoreRows + j] = val;
-        if (Mz) {
-            const int jint = j == 0 ? kStoreRows - 2 : (j == kStoreRows - 1 ? kStoreRows - 1 : j - 1);
-            Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)(mz_scale * val);
-        }
-    }
+    readout_prep_block(m, R, M, Mz, mz_scale, blockIdx.x, blockIdx.y, threadIdx.x);
 }
 
 hipError_t launch_readout_prep(int H, int m, const float *R, float *M, __bf16 *Mz, float mz_scale,

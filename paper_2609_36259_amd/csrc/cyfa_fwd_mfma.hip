@@ -530,6 +530,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         if (w == 0) chunk_scans<CC, NT, CC>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
+        // factor applied to the carried states this chunk (uniform: a scalar register)
+        const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
         build_writes_swz<CC, true, false, NT, CSW>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A, computed
@@ -552,7 +554,6 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             oacc = mma(lds8_tr(At + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), oacc);
         {
             // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec (decay kept in L)
-            const float sf = s.ctl[0];
             if (sf != 1.f) {
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
@@ -569,12 +570,17 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
         }
         // -- middle step 1: X_r = U(lambda_r) O'_r -> X tile [token][basis] (reuses Q's)
+        half2v csx[8];
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4)
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2) csx[2 * v4 + k2] = CSrow[4 * v4 + k2];
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
             bf16x4 xv;
 #pragma unroll
             for (int k2 = 0; k2 < 2; ++k2) {
-                const half2v cs = CSrow[4 * v4 + k2];
+                const half2v cs = csx[2 * v4 + k2];
                 const float c = (float)cs[0], sn = (float)cs[1];
                 const float xc = oacc[4 * v4 + 2 * k2], xs = oacc[4 * v4 + 2 * k2 + 1];
                 xv[2 * k2] = (__bf16)fmaf(-sn, xs, c * xc);
@@ -665,34 +671,27 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         //    Wave w owns basis rows 32w .. 32w+31; each (cos, sin) pair sits in two
         //    consecutive registers of one lane, so the rotation is in-lane.
         {
-            f32x16 yacc[RB];
+            // the (cos, sin) pairs are read first: they do not depend on the products
+            half2v csy[8];
 #pragma unroll
-            for (int nb = 0; nb < RB; ++nb) yacc[nb] = zero_acc();
+            for (int v4 = 0; v4 < 4; ++v4)
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 mt = lds8_tr(Myt + 16 * ks * SWS, SWS);
+                for (int k2 = 0; k2 < 2; ++k2) csy[2 * v4 + k2] = CSrow[4 * v4 + k2];
+            f32x16 yacc = zero_acc();
 #pragma unroll
-                for (int nb = 0; nb < RB; ++nb)
-                    yacc[nb] = mma(mt, lds8(Xa + 32 * nb * QS + 16 * ks), yacc[nb]);
-            }
+            for (int ks = 0; ks < 8; ++ks) yacc = mma(lds8_tr(Myt + 16 * ks * SWS, SWS), lds8(Xa + 16 * ks), yacc);
 #pragma unroll
-            for (int nb = 0; nb < RB; ++nb) {
-                const int r = 32 * nb + l32;
-                const half2v *csr = CSrow + 32 * nb * CSW;
-                __bf16 *orow = O2row + 32 * nb * QS;
+            for (int v4 = 0; v4 < 4; ++v4) {
+                bf16x4 ov;
 #pragma unroll
-                for (int v4 = 0; v4 < 4; ++v4) {
-                    bf16x4 ov;
-#pragma unroll
-                    for (int k2 = 0; k2 < 2; ++k2) {
-                        const half2v cs = csr[4 * v4 + k2];
-                        const float c = (float)cs[0], sn = (float)cs[1];
-                        const float yc = yacc[nb][4 * v4 + 2 * k2], ysn = yacc[nb][4 * v4 + 2 * k2 + 1];
-                        ov[2 * k2] = (__bf16)fmaf(sn, ysn, c * yc);
-                        ov[2 * k2 + 1] = (__bf16)fmaf(-sn, yc, c * ysn);
-                    }
-                    *reinterpret_cast<bf16x4 *>(orow + 8 * v4) = ov;
+                for (int k2 = 0; k2 < 2; ++k2) {
+                    const half2v cs = csy[2 * v4 + k2];
+                    const float c = (float)cs[0], sn = (float)cs[1];
+                    const float yc = yacc[4 * v4 + 2 * k2], ysn = yacc[4 * v4 + 2 * k2 + 1];
+                    ov[2 * k2] = (__bf16)fmaf(sn, ysn, c * yc);
+                    ov[2 * k2 + 1] = (__bf16)fmaf(-sn, yc, c * ysn);
                 }
+                *reinterpret_cast<bf16x4 *>(O2row + 8 * v4) = ov;
             }
         }
         __syncthreads();
@@ -723,7 +722,6 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
         {
             // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
-            const float sf = s.ctl[0];
             if (sf != 1.f) {
 #pragma unroll
                 for (int x = 0; x < 4; ++x)

@@ -146,10 +146,12 @@ __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, 
     const int l16 = lane & 15, g = lane >> 4;
     f32x4 acc = zero_acc4();
     const __bf16 *ap = Arow + (16 * rb + l16) * QS + 8 * g;
-    const int bo = Boff + 2 * swz_elem(16 * sb + l16, 8 * g);
+    // one opaque copy of the base per call (an asm statement also fences the
+    // scheduler, so none sits between the reads and products below)
+    const int bo = opq(Boff + 2 * swz_elem(16 * sb + l16, 8 * g));
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
-        acc = mma16(lds8(lds_at<__bf16>(smem, opq(bo) ^ (64 * ks))), lds8(ap + 32 * ks), acc);
+        acc = mma16(lds8(lds_at<__bf16>(smem, bo ^ (64 * ks))), lds8(ap + 32 * ks), acc);
     const int t = 16 * rb + l16;
     const int s0 = 16 * sb + 4 * g;
     const float Gt = s.Gs[t];
@@ -472,24 +474,30 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const float *dw_l = lds_at<float>(smem, opq(Ly::SC + 4 * (3 * CC + 8 * hl)));    // decw, operand tokens
     // M rows (slot icol), columns 8 hl + 16 ks at byte offset Mza ^ 32 ks
     const int Mza = opq(Ly::MT + 2 * swz_elem(icol, 8 * hl));
-    const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + (trs ^ (64 * w))));          // M columns
+    // transposed operands from swizzled tiles: column block w at Ly::T + trw, or block
+    // x at Ly::T + (tr0 ^ 64 x) (the tile offsets are multiples of 256 bytes)
+    const int trw = opq(trs ^ (64 * w));
+    const int tr0 = opq(trs);
+    // M columns: own base (the tile sits at 44 KiB; with the k-step offsets the sum
+    // would overflow the 16-bit instruction offset)
+    const __bf16 *Myt = lds_at<__bf16>(smem, opq(Ly::MT + (trs ^ (64 * w))));
     const __bf16 *Qperm = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + h4)));   // permuted-k A operands
     const __bf16 *Operm = Qperm + TE;
     const __bf16 *Xa = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 8 * hl)));  // natural-k operands
     const __bf16 *Sa = lds_at<__bf16>(smem, opq(Ly::S + 2 * (l32 * SSC + 8 * hl)));
-    // transposed operands from swizzled tiles: column block w, or block x at base ^ 64 x
-    const __bf16 *At = lds_at<__bf16>(smem, opq(Ly::A + (trs ^ (64 * w))));
-    const __bf16 *Vt = lds_at<__bf16>(smem, opq(Ly::V + (trs ^ (64 * w))));
-    const int Atx = opq(Ly::A + trs);
-    const int Kt = opq(Ly::K + trs);
-    // token-row bases: row l32, columns 32w + 4hl (+ 8 v4) of the X / W, O'' and
-    // output-staging tiles and the matching (cos, sin) pairs
-    __bf16 *Wrow = lds_at<__bf16>(smem, opq(Ly::Q + 2 * (l32 * QS + 32 * w + h4)));
+    const __bf16 *At = lds_at<__bf16>(smem, Ly::A + trw);
+    const __bf16 *Vt = lds_at<__bf16>(smem, Ly::V + trw);
+    // token-row base: row l32, columns 32w + 4hl (+ 8 v4) of the X / W, O'' and
+    // output-staging tiles, and the matching (cos, sin) pairs (the padded tile rows
+    // and the table rows are both 272 bytes)
+    static_assert(QS * 2 == CSW * 4, "one token-row base for the padded tiles and the table");
+    const int rowb = opq(2 * (l32 * QS + 32 * w + h4));
+    __bf16 *Wrow = lds_at<__bf16>(smem, Ly::Q + rowb);
     __bf16 *O2row = Wrow + TE;
     // output staging: [CC][QS] bf16 in the (cos, sin) table, which is free from the
     // O'' rotation until the next chunk's temporal writes
-    __bf16 *Strow = lds_at<__bf16>(smem, opq(Ly::CS + 2 * (l32 * QS + 32 * w + h4)));
-    const half2v *CSrow = lds_at<half2v>(smem, opq(Ly::CS + 4 * (l32 * CSW + 16 * w + 2 * hl)));
+    __bf16 *Strow = lds_at<__bf16>(smem, Ly::CS + rowb);
+    const half2v *CSrow = lds_at<half2v>(smem, Ly::CS + rowb);
     float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
     const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
     const __bf16 *Stg = lds_at<__bf16>(smem, opq(Ly::CS + 2 * ((tid >> 4) * QS + (tid & 15) * 8)));
@@ -560,12 +568,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) kacc[x][v] *= sf;
             }
+            const int kt = opq(tr0);
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
                 const bf16x8 ad_w = decay_rows(lds8_tr(At + 16 * ks * SWS, SWS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
-                    kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Kt) ^ (64 * x)) + 16 * ks * SWS, SWS), ad_w,
+                    kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, Ly::K + (kt ^ (64 * x))) + 16 * ks * SWS, SWS), ad_w,
                                   kacc[x]);
             }
         }
@@ -595,9 +604,10 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         {
 #pragma unroll
             for (int nb = 0; nb < RB; ++nb) zacc[nb] = zero_acc();
+            const int mz = opq(Mza);            // per chunk: the xor'ed addresses are not hoisted
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 ma = lds8(lds_at<__bf16>(smem, opq(Mza) ^ (32 * ks)));
+                const bf16x8 ma = lds8(lds_at<__bf16>(smem, mz ^ (32 * ks)));
 #pragma unroll
                 for (int nb = 0; nb < RB; ++nb)
                     zacc[nb] = mma(ma, lds8(Xa + 32 * nb * QS + 16 * ks), zacc[nb]);
@@ -728,12 +738,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) vacc[x][v] *= sf;
             }
+            const int at = opq(tr0);
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
                 const bf16x8 v_w = decay_rows(lds8_tr(Vt + 16 * ks * SWS, SWS), dw_l + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
-                    vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Atx) ^ (64 * x)) + 16 * ks * SWS, SWS), v_w,
+                    vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, Ly::A + (at ^ (64 * x))) + 16 * ks * SWS, SWS), v_w,
                                   vacc[x]);
             }
         }

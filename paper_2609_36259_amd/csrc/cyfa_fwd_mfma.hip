@@ -595,6 +595,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 xv[2 * k2] = (__bf16)fmaf(-sn, xs, c * xc);
                 xv[2 * k2 + 1] = (__bf16)fmaf(sn, xc, c * xs);
             }
+            // padding column 127 (wave 3, upper lane half, last register) is set to 1:
+            // the readout matrix holds kMaskLogit there on the rows of inactive slots
+            if (v4 == 3 && w == 3 && hl) xv[3] = (__bf16)1.f;
             *reinterpret_cast<bf16x4 *>(Wrow + 8 * v4) = xv;
         }
         __syncthreads();
@@ -619,11 +622,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         float mwave[RB];                        // this wave's max over its slots (-inf: none active)
 #pragma unroll
         for (int nb = 0; nb < RB; ++nb) {
-            if (32 * w + 31 >= m) {             // this wave holds inactive slots (uniform)
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    if (icol - l32 + 8 * (v >> 2) + h4 + (v & 3) >= m) zacc[nb][v] = -INFINITY;
-            }
+            // inactive slots (>= m) come out of the product at about -1e30 (padding
+            // column of X times the readout matrix entry): no masking here
             float mx = zacc[nb][0];
 #pragma unroll
             for (int v = 1; v < 16; ++v) mx = fmaxf(mx, zacc[nb][v]);
@@ -638,7 +638,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                     if (slot < m) lg[slot] = zacc[nb][v] * 0.69314718055994531f;
                 }
             }
-            // a wave whose slots are all inactive (m <= 32 w) contributes (-inf, 0)
+            // a wave whose slots are all inactive (m <= 32 w) has mx about -1e30: its
+            // weights and its share of the sum get the factor exp2(mx - M) = 0 below
             mwave[nb] = mx;
             const float mref = mx == -INFINITY ? 0.f : mx;
             // the accumulators now hold exp2(z - mref), reused for the weights below

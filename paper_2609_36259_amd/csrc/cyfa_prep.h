@@ -14,6 +14,7 @@
 namespace cyfa {
 
 constexpr int kPrepRows = 4;          // rows of M_h per workgroup (two per thread)
+constexpr float kMaskLogit = -1e30f;  // padding-column entry of inactive slots in Mz
 
 // Block (h, rb) of the grid (H, 128 / kPrepRows) computes rows [4 rb, 4 rb + 4) of M_h.
 // Thread (j = tid % 128, g = tid / 128) owns paper basis column j and rows
@@ -75,7 +76,11 @@ __device__ __forceinline__ void readout_prep_block(int m, const float *__restric
         if (M) M[((size_t)h * kStoreRows + i) * kStoreRows + j] = val;
         if (Mz) {
             const int jint = j == 0 ? kStoreRows - 2 : (j == kStoreRows - 1 ? kStoreRows - 1 : j - 1);
-            Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)(mz_scale * val);
+            // inactive slots (rows >= m) carry kMaskLogit in the padding column: a kernel
+            // that sets that column of its operand to 1 gets their logits at about
+            // kMaskLogit, i.e. softmax weights of exactly 0, without masking code
+            const float z = (j == kStoreRows - 1 && i >= m) ? kMaskLogit : mz_scale * val;
+            Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)z;
         }
     }
 }

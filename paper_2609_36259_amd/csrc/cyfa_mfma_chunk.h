@@ -70,34 +70,44 @@ template <int CC, bool kWithQ, int NTH = NT>
 __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int tid,
                                            Prefetch<CC, NTH> &pf) {
     constexpr int kRows = NTH / 16;                  // rows per pass
+    // Uniform chunk base (scalar registers) plus a fixed 32-bit per-lane byte offset:
+    // no per-lane 64-bit address arithmetic.  Rows past the sequence read as zero.
+    const size_t row_el = (size_t)p.H * D;           // elements between consecutive tokens
+    const size_t base = ((size_t)b * p.T + t0) * row_el + (size_t)h * D;
+    const char *q = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.q) + base);
+    const char *k = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.k) + base);
+    const char *v = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.v) + base);
+    const int r0 = tid >> 4;
+    const unsigned loff = (unsigned)(r0 * (int)row_el + (tid & 15) * 8) * 2u;
+    const unsigned pass = (unsigned)(kRows * row_el * 2);
     const uint4 zero = make_uint4(0, 0, 0, 0);
-    const __bf16 *q = static_cast<const __bf16 *>(p.q);
-    const __bf16 *k = static_cast<const __bf16 *>(p.k);
-    const __bf16 *v = static_cast<const __bf16 *>(p.v);
-    const int r0 = tid >> 4, d0 = (tid & 15) * 8;
-    const size_t row_stride = (size_t)p.H * D;
-    const size_t base = (((size_t)b * p.T + t0 + r0) * p.H + h) * D + d0;
+    // (uniform part added first, so that the loads take a scalar base and a 32-bit
+    // vector offset)
+    auto ld = [&](const char *base_it) { return *reinterpret_cast<const uint4 *>(base_it + loff); };
+    if (t0 + CC <= p.T) {                            // whole chunk in range (uniform)
 #pragma unroll
-    for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
-        const int t = t0 + r0 + kRows * it;
-        const size_t off = base + (size_t)(kRows * it) * row_stride;
-        if (t < p.T) {
-            if (kWithQ) pf.q[it] = *reinterpret_cast<const uint4 *>(q + off);
-            pf.k[it] = *reinterpret_cast<const uint4 *>(k + off);
-            pf.v[it] = *reinterpret_cast<const uint4 *>(v + off);
-        } else {
-            if (kWithQ) pf.q[it] = zero;
-            pf.k[it] = zero;
-            pf.v[it] = zero;
+        for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
+            if (kWithQ) pf.q[it] = ld(q + it * pass);
+            pf.k[it] = ld(k + it * pass);
+            pf.v[it] = ld(v + it * pass);
+        }
+    } else {
+#pragma unroll
+        for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
+            const bool in = t0 + r0 + kRows * it < p.T;
+            if (kWithQ) pf.q[it] = in ? ld(q + it * pass) : zero;
+            pf.k[it] = in ? ld(k + it * pass) : zero;
+            pf.v[it] = in ? ld(v + it * pass) : zero;
         }
     }
     if (tid < 64) {
         const int t = t0 + tid;
+        const size_t sbase = ((size_t)b * p.T + t0) * p.H + h;
+        const unsigned soff = (unsigned)(tid * p.H);
         if (tid < CC && t < p.T) {
-            const size_t si = ((size_t)b * p.T + t) * p.H + h;
-            pf.dl = p.delta[si];
-            pf.g = p.log_alpha ? p.log_alpha[si] : 0.f;
-            pf.be = p.beta ? p.beta[si] : 1.f;
+            pf.dl = (p.delta + sbase)[soff];
+            pf.g = p.log_alpha ? (p.log_alpha + sbase)[soff] : 0.f;
+            pf.be = p.beta ? (p.beta + sbase)[soff] : 1.f;
         } else {
             pf.dl = 0.f;   // rows past the chunk or the sequence: no shift, no decay, no write
             pf.g = 0.f;

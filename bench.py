@@ -35,10 +35,11 @@ M_ACTIVE = 127
 # factors come from the same counters on a 1 GiB device copy), taken on the kernel
 # sources whose digest is recorded here.  Reported only while those sources are
 # unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
-TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 343165464,
-           "fetch_kib": 134800, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
-           "sources_sha256": "17d2f142122ce61a59190565afafdf59132233d7c4a395ec60093c96b2a09422"}
-TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h")
+TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 118403 * 2 * 1024 + 65536 * 1024,
+           "fetch_kib": 118403, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
+           "sources_sha256": "2b9a4345849edb5fa20e8927836fc543be82270965ff22d15f29d72cd904ddc4"}
+TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h",
+                   "cyfa_prep.h")
 
 
 def kernel_sources_digest() -> str:
@@ -260,8 +261,10 @@ def cpu_baseline(w, budget_s: float):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
+    # the GPU's clocks take a few tens of milliseconds of sustained load to settle:
+    # 300 warm-up steps (~50 ms) reach the steady state the 500 timed steps measure
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default="1.4B", choices=["tiny", "400M", "1.4B", "long"])
     ap.add_argument("--kernel", default="auto", choices=["auto", "valu", "mfma"])
     ap.add_argument("--chunk", type=int, default=0)

@@ -186,11 +186,12 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc,
 /*
  * Optional timing hook for profilers and benchmarks.  When both events are
  * non-NULL (hipEvent_t handles), every later cyfa_forward / cyfa_decode_step
- * call made from the calling thread records `start` on its stream immediately
- * before its main kernel (the fused chunk kernel, or the decode kernel) and
- * `stop` immediately after it, so hipEventElapsedTime gives that kernel's
- * duration alone.  Passing NULL for both clears the hook.  Setting only one of
- * them is CYFA_ERR_INVALID_ARGUMENT.  The events stay owned by the caller.
+ * call made from the calling thread records `start` and `stop` around its main
+ * kernel (the fused chunk kernel, or the decode kernel) on its stream -- for the
+ * matrix-core forward as part of that kernel's own dispatch -- so
+ * hipEventElapsedTime gives that kernel's duration alone.  Passing NULL for
+ * both clears the hook.  Setting only one of them is
+ * CYFA_ERR_INVALID_ARGUMENT.  The events stay owned by the caller.
  */
 cyfa_status cyfa_set_timing_events(void *start_event, void *stop_event);
 

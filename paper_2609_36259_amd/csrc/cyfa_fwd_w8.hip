@@ -15,6 +15,8 @@
 // products is read in the same permuted order.
 #include "cyfa_mfma_chunk.h"
 
+#include <hip/hip_ext.h>
+
 namespace cyfa {
 
 using namespace mfma;
@@ -443,8 +445,9 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
 
 }  // namespace
 
-hipError_t launch_chunk64_w8(const MfmaArgs &a, int groups, hipStream_t st) {
-    hipLaunchKernelGGL(chunk64_w8_kernel, dim3(groups), dim3(W8), 0, st, a);
+hipError_t launch_chunk64_w8(const MfmaArgs &a, int groups, hipStream_t st, hipEvent_t ev_start,
+                             hipEvent_t ev_stop) {
+    hipExtLaunchKernelGGL(chunk64_w8_kernel, dim3(groups), dim3(W8), 0, st, ev_start, ev_stop, 0, a);
     return hipGetLastError();
 }
 

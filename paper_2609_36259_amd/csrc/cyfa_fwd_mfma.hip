@@ -136,14 +136,16 @@ __device__ __forceinline__ void update_states(const Tiles &s, char *smem, int w,
     }
 }
 
-// One 16 x 16 block (rb, sb) of the causal score tile (S (.) Gamma) -> Ss (bf16),
-// k = 128 along the rows of both operand tiles: token rows t from a padded tile,
-// rows s from the swizzled tile at byte offset Boff (column block ks of a row is
-// its first block's offset ^ 64 ks).  Computed transposed, D[s][t], so that each
-// lane stores four consecutive entries S[t][s .. s+3] at once.
+// One 16 x 16 block (rb, sb) of the causal score tile -> Ss (bf16), k = 128 along
+// the rows of both operand tiles: token rows t from a padded tile, rows s from
+// the swizzled tile at byte offset Boff (column block ks of a row is its first
+// block's offset ^ 64 ks).  The decay Gamma_ts is applied only when the chunk is
+// not factored (fac = false); otherwise the A tile holds A_dec and Gamma becomes
+// a per-token scale of the whole pass.  Computed transposed, D[s][t], so that
+// each lane stores four consecutive entries S[t][s .. s+3] at once.
 template <int CC>
 __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, char *smem, int Boff,
-                                            int rb, int sb, int lane) {
+                                            int rb, int sb, int lane, bool fac) {
     constexpr int SSC = Lay<CC>::SSC;
     const int l16 = lane & 15, g = lane >> 4;
     f32x4 acc = zero_acc4();
@@ -156,12 +158,14 @@ __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, 
         acc = mma16(lds8(lds_at<__bf16>(smem, bo ^ (64 * ks))), lds8(ap + 32 * ks), acc);
     const int t = 16 * rb + l16;
     const int s0 = 16 * sb + 4 * g;
-    const float Gt = s.Gs[t];
-    const float4 G4 = *reinterpret_cast<const float4 *>(s.Gs + s0);
-    const float Gv[4] = {G4.x, G4.y, G4.z, G4.w};
+    if (!fac) {                                        // uniform
+        const float Gt = s.Gs[t];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] *= __expf(Gt - s.Gs[s0 + r]);
+    }
     bf16x4 sv;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sv[r] = (__bf16)(s0 + r <= t ? acc[r] * __expf(Gt - Gv[r]) : 0.f);
+    for (int r = 0; r < 4; ++r) sv[r] = (__bf16)(s0 + r <= t ? acc[r] : 0.f);
     *reinterpret_cast<bf16x4 *>(s.Ss + t * SSC + s0) = sv;
 }
 
@@ -170,9 +174,9 @@ __device__ __forceinline__ void score_block(const Tiles &s, const __bf16 *Arow, 
 // diagonal blocks, which come out as zeros), spread evenly over the 4 waves.
 template <int CC>
 __device__ __forceinline__ void score_tiles(const Tiles &s, const __bf16 *Arow, char *smem, int Boff,
-                                            int w, int lane) {
+                                            int w, int lane, bool fac) {
     static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
-    score_block<CC>(s, Arow, smem, Boff, w >> 1, w & 1, lane);
+    score_block<CC>(s, Arow, smem, Boff, w >> 1, w & 1, lane, fac);
 }
 
 __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4], float f) {
@@ -235,7 +239,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
         if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
-        build_writes_swz<CC, false, true, NT, 64>(s, tid, a.p.m);
+        build_writes_swz<CC, false, false, true, NT, 64>(s, tid, a.p.m);
         __syncthreads();
         update_states<CC>(s, smem, w, lane, kacc, vacc);
         __syncthreads();
@@ -472,8 +476,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     constexpr int TE = Ly::TILE / 2;                                      // padded tile size in elements
     constexpr int CSW = Ly::CSW;
     const int trs = tr_off_swz(lane);
-    const float *gam_t = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + l32)));          // gam of token l32
-    const float *dw_l = lds_at<float>(smem, opq(Ly::SC + 4 * (3 * CC + 8 * hl)));    // decw, operand tokens
+    const float *eps_t = lds_at<float>(smem, opq(Ly::SC + 4 * (CC + l32)));          // row scale of token l32
+    const int dw_off = Ly::SC + 4 * (3 * CC + 8 * hl);                                // decw, operand tokens
     // M rows (slot icol), columns 8 hl + 16 ks at byte offset Mza ^ 32 ks
     const int Mza = opq(Ly::MT + 2 * swz_elem(icol, 8 * hl));
     // transposed operands from swizzled tiles: column block w at Ly::T + trw, or block
@@ -537,24 +541,37 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
-        if (w == 0) chunk_scans<CC, NT, CC>(s, lane, m, pf, carry, gsum, logf);
+        if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
-        // factor applied to the carried states this chunk (uniform: a scalar register)
+        // factor applied to the carried states this chunk, and whether the chunk's
+        // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
-        build_writes_swz<CC, true, false, NT, CSW>(s, tid, m);
+        const bool fac = __builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[2])) != 0;
+        build_writes_swz<CC, true, true, false, NT, CSW, true>(s, tid, m);
         __syncthreads();
-        // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A, computed
-        //    transposed: O'^T = (Kbar Q^T) gamma + A^T (S (.) Gamma)^T.  Wave w owns basis
-        //    rows 32w .. 32w+31; lane (token l32, half hl) holds 16 of them, so each
+        // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A.  With the
+        //    tile holding A_dec (rows times the right decay), Gamma_rs = gam_r decw_s
+        //    and O' = eps (.) (Q Kbar'^T + S A_dec), S the causal Q K^T and Kbar' the
+        //    state after this chunk's rescale factor (eps: row scale of the chunk
+        //    scans).  A chunk that is not factored keeps A, applies Gamma in the score
+        //    tile, gam to the inter-chunk term and the rescale after it.  Computed
+        //    transposed: O'^T = Kbar' Q^T + A_dec^T S^T.  Wave w owns basis rows
+        //    32w .. 32w+31; lane (token l32, half hl) holds 16 of them, so each
         //    (cos, sin) pair sits in two consecutive registers of one lane.
-        score_tiles<CC>(s, s.Qs, smem, Ly::K, w, lane);
+        if (fac && sf != 1.f) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) kacc[x][v] *= sf;
+        }
+        score_tiles<CC>(s, s.Qs, smem, Ly::K, w, lane, fac);
         f32x16 oacc = zero_acc();
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks)
             oacc = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(Qperm, 16 * ks, 0), oacc);
-        {
-            const float gt = *gam_t;
+        if (!fac) {
+            const float gt = *eps_t;
 #pragma unroll
             for (int v = 0; v < 16; ++v) oacc[v] *= gt;
         }
@@ -562,9 +579,14 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks)
             oacc = mma(lds8_tr(At + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), oacc);
+        if (fac) {
+            const float et = *eps_t;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[v] *= et;
+        }
         {
-            // key state: Kbar^T <- gamma^C Kbar^T + K^T A_dec (decay kept in L)
-            if (sf != 1.f) {
+            // key state: Kbar'^T += K^T A_dec (decay kept in L)
+            if (!fac && sf != 1.f) {
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -573,7 +595,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             const int kt = opq(tr0);
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 ad_w = decay_rows(lds8_tr(At + 16 * ks * SWS, SWS), dw_l + 16 * ks);
+                bf16x8 ad_w = lds8_tr(At + 16 * ks * SWS, SWS);
+                if (!fac) ad_w = decay_rows(ad_w, lds_at<float>(smem, opq(dw_off)) + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
                     kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, Ly::K + (kt ^ (64 * x))) + 16 * ks * SWS, SWS), ad_w,
@@ -708,16 +731,23 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
         }
         __syncthreads();
-        // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V, computed
-        //    transposed like the key pass: lane (token l32, half hl) holds 16 output
-        //    columns of wave w's block 32w .. 32w+31.
-        score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane);
+        // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V, as the key
+        //    pass: O = eps (.) (O'' Vbar' + S2 V) with S2 the causal O'' A_dec^T (a
+        //    chunk that is not factored as before); computed transposed, lane (token
+        //    l32, half hl) holding 16 output columns of wave w's block 32w .. 32w+31.
+        if (fac && sf != 1.f) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) vacc[x][v] *= sf;
+        }
+        score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane, fac);
         f32x16 pacc = zero_acc();
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks)
             pacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(Operm, 16 * ks, 0), pacc);
-        {
-            const float gt = *gam_t;
+        if (!fac) {
+            const float gt = *eps_t;
 #pragma unroll
             for (int v = 0; v < 16; ++v) pacc[v] *= gt;
         }
@@ -725,6 +755,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks)
             pacc = mma(lds8_tr(Vt + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), pacc);
+        if (fac) {
+            const float et = *eps_t;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) pacc[v] *= et;
+        }
         // output tile -> staging [token][column] for 16-byte global stores
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
@@ -734,8 +769,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             *reinterpret_cast<bf16x4 *>(Strow + 8 * v4) = ov;
         }
         {
-            // value state: Vbar <- gamma^C Vbar + A_dec^T V (decay kept in L)
-            if (sf != 1.f) {
+            // value state: Vbar' += A_dec^T V (decay kept in L)
+            if (!fac && sf != 1.f) {
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -744,7 +779,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             const int at = opq(tr0);
 #pragma unroll
             for (int ks = 0; ks < CC / 16; ++ks) {
-                const bf16x8 v_w = decay_rows(lds8_tr(Vt + 16 * ks * SWS, SWS), dw_l + 16 * ks);
+                bf16x8 v_w = lds8_tr(Vt + 16 * ks * SWS, SWS);
+                if (!fac) v_w = decay_rows(v_w, lds_at<float>(smem, opq(dw_off)) + 16 * ks);
 #pragma unroll
                 for (int x = 0; x < 4; ++x)
                     vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, Ly::A + (at ^ (64 * x))) + 16 * ks * SWS, SWS), v_w,

@@ -44,7 +44,8 @@ struct Tiles {
     float *betas;
     float *decw;    // multiplier of A_dec rows
     float *urev;    // clock at each row reduced mod m, divided by m (revolutions, in [0, 1))
-    float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it
+    float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it,
+                    // [2]: 1 when the chunk's decay factors into a row scale (A_dec tile), else 0
 };
 
 // n entries per array (the chunk length or 64); block size scalar_bytes(n)
@@ -105,7 +106,9 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     if (tid < 64) {
         const int t = t0 + tid;
         const size_t sbase = ((size_t)b * p.T + t0) * p.H + h;
-        const unsigned soff = (unsigned)(tid * p.H);
+        // opaque per chunk: otherwise base + lane offset is kept per lane (64-bit)
+        // across the whole chunk loop
+        const unsigned soff = (unsigned)opq(tid * p.H);
         if (tid < CC && t < p.T) {
             pf.dl = (p.delta + sbase)[soff];
             pf.g = p.log_alpha ? (p.log_alpha + sbase)[soff] : 0.f;
@@ -146,7 +149,9 @@ __device__ __forceinline__ void store_chunk(const Tiles &s, int tid, const Prefe
 // [e^-60, e^60] the chunk instead rescales Kt by exp(L + G_C), uses
 // A gamma^C / gamma^r and restarts L at 0.
 // NSC: entries of the scalar arrays (lanes >= NSC hold no token and write nothing)
-template <int CC, int NTH = NT, int NSC = 64>
+// kEps: for the kernels whose A tile holds A_dec: gam holds the row scale eps_r
+// of a "factored" chunk (below) and ctl[2] says whether the chunk is one.
+template <int CC, int NTH = NT, int NSC = 64, bool kEps = false>
 __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, const Prefetch<CC, NTH> &pf,
                                             double &carry, double &gsum, float &L) {
     const double inv_m = 1.0 / (double)m;
@@ -155,10 +160,19 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
     const float GC = lane63(G);
     const float gabs = wave_max_nonneg(fabsf(G));
     const bool lazy = fabsf(L) + gabs <= 60.f;
+    // Factored chunk: Gamma_rs = eps_r decw_s with both factors within e^+-60, so
+    // with A_dec in place of A every intra-chunk term is eps_r (S A_dec).  Lazy:
+    // eps_r = exp(G_r + L) = gam_r.  Eager with a chunk range |G_C| <= 60: the
+    // states are rescaled by exp(L + G_C) before the inter-chunk products and
+    // eps_r = exp(G_r - G_C); that factor must stay a normal fp32 number (the
+    // first tokens' inter-chunk terms depend on the rescaled states), hence
+    // |L| + |G_C| <= 80.  Otherwise the kernel applies Gamma per score entry and
+    // gam_r before the intra products, and rescales the states after them.
+    const bool factored = lazy || (gabs <= 60.f && fabsf(L) + gabs <= 80.f);
     if (lane < NSC) {
         const int ol = opq(lane);                   // one address register for the five writes
         s.Gs[ol] = G;
-        s.gam[ol] = __expf(G + L);
+        s.gam[ol] = (kEps && !lazy && factored) ? __expf(G - GC) : __expf(G + L);
         s.decw[ol] = lazy ? __expf(-G - L) : __expf(GC - G);
         s.betas[ol] = pf.be;
         const double q = lam * inv_m;               // clock in revolutions of the m-slot ring
@@ -169,6 +183,7 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
     if (lane == 0) {
         s.ctl[0] = state_factor;
         s.ctl[1] = L;
+        s.ctl[2] = factored ? 1.f : 0.f;
     }
     const double last = lane63(lam);
     carry = reduce_clock(last, (double)m, inv_m);
@@ -245,8 +260,10 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
 // that each group of 16 lanes stores one whole row, and a (cos, sin) table of
 // row stride CSW half2 words.  Thread (r, q) fills internal columns 8q .. 8q+7
 // (pairs 4q+1 .. 4q+4) of rows r = tid / 16 + (NTH / 16) it; q = 15 also holds
-// DC (column 126) and the padding (127).
-template <int CC, bool kA, bool kAd, int NTH, int CSW>
+// DC (column 126) and the padding (127).  kTab: write the (cos, sin) table;
+// kA / kAd: write A into As / A_dec into Ads; kSel: write A_dec into As when the
+// chunk is factored (ctl[2]), else A.
+template <int CC, bool kTab, bool kA, bool kAd, int NTH, int CSW, bool kSel = false>
 __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m) {
     constexpr int RPP = NTH / 16;                    // rows per pass
     static_assert(CC % RPP == 0 && RPP % 4 == 0, "whole passes with a fixed swizzle phase");
@@ -255,6 +272,7 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
     const float dc = 1.0f / sqrtf((float)m);
     const float sq = sqrtf(2.0f / (float)m);
     const int pc = swz_elem(r0, 8 * q) - r0 * SWS;   // stored column of this thread's chunk
+    const bool sel_dec = kSel && s.ctl[2] != 0.f;     // uniform
     // rows one after another: interleaving them raises the register peak of the
     // fused kernel, which holds the carried states and the prefetched chunk here
 #pragma unroll 1
@@ -262,7 +280,7 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
         const int r = r0 + RPP * it;
         const float be = s.betas[r];
         const float bac = be * sq;
-        const float wdec = kAd ? s.decw[r] : 0.f;
+        const float wdec = kAd ? s.decw[r] : (kSel ? (sel_dec ? s.decw[r] : 1.f) : 0.f);
         const float u = s.urev[r];
         float s1, c1, sn, cs;
         sincos_rev(u, &s1, &c1);
@@ -284,8 +302,8 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
                 a0 = be * dc;                        // internal column 126: DC
                 a1 = 0.f;                            // 127: padding
             }
-            a8[2 * jj] = (__bf16)a0;
-            a8[2 * jj + 1] = (__bf16)a1;
+            a8[2 * jj] = (__bf16)(kSel ? a0 * wdec : a0);
+            a8[2 * jj + 1] = (__bf16)(kSel ? a1 * wdec : a1);
             if (kAd) {
                 ad8[2 * jj] = (__bf16)(a0 * wdec);
                 ad8[2 * jj + 1] = (__bf16)(a1 * wdec);
@@ -301,10 +319,8 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
                 sn = ns;
             }
         }
-        if (kA) {
-            *reinterpret_cast<bf16x8 *>(s.As + r * SWS + pc) = a8;
-            *reinterpret_cast<half8v *>(s.CS + r * CSW + 4 * q) = cs8;
-        }
+        if (kA) *reinterpret_cast<bf16x8 *>(s.As + r * SWS + pc) = a8;
+        if (kTab) *reinterpret_cast<half8v *>(s.CS + r * CSW + 4 * q) = cs8;
         if (kAd) *reinterpret_cast<bf16x8 *>(s.Ads + r * SWS + pc) = ad8;
     }
 }

@@ -120,6 +120,23 @@ def test_extreme_and_mixed_gates(chunk):
     _assert_ok(_errors(y, res))
 
 
+@pytest.mark.parametrize("chunk", [32, 64])
+@pytest.mark.parametrize("gate", [-0.8, -1.5])
+def test_eager_rescale_paths(chunk, gate):
+    """A long stretch of log alpha = gate between ordinary gates.  gate = -0.8:
+    each 32-token chunk decays by about e^-26, so every third chunk leaves the
+    e^+-60 running scale while |L| + |G_C| stays within 80 -- the 32-token kernel
+    rescales those chunks' states first and factors their decay into a per-token
+    scale.  gate = -1.5 (e^-48 per chunk): the rescaled states would fall below
+    fp32's normal range, so those chunks keep Gamma in the score tile.  64-token
+    chunks decay twice as much per chunk."""
+    x = make_forward_inputs(1, 431, 2, 128, 128, seed=52, dtype="bf16")
+    x["log_alpha"][:, 40:360] = gate
+    t = upload(x)
+    res = _fwd(x, t, chunk=chunk, segments=2, return_state=True, return_logits=True)
+    _assert_ok(_errors(x, res))
+
+
 def test_initial_state_and_resume():
     cyfa = _cyfa()
     x = make_forward_inputs(2, 300, 2, 128, 128, seed=44, dtype="bf16")

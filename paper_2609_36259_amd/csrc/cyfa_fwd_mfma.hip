@@ -535,12 +535,32 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     Prefetch<CC> pf;
     load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
+    // staged output tile of chunk tc -> o, 16-byte stores: uniform chunk base plus a
+    // 32-bit lane offset (opaque per call, so no 64-bit lane address lives across
+    // the loop)
+    auto flush_out = [&](int tc) {
+        const int tb = tc * CC, nn = min(CC, p.T - tb);
+        const int r0 = tid >> 4;
+        char *ob = reinterpret_cast<char *>(o + (((size_t)b * p.T + tb) * p.H + h) * D);
+        const unsigned loff = (unsigned)opq((r0 * p.H * D + (tid & 15) * 8) * 2);
+        const unsigned pass = (unsigned)(16 * p.H * D * 2);
+#pragma unroll
+        for (int it = 0; it < CC / 16; ++it)
+            if (r0 + 16 * it < nn)
+                *reinterpret_cast<uint4 *>(ob + it * pass + loff) = *reinterpret_cast<const uint4 *>(Stg + 16 * it * QS);
+    };
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
         const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
+        // The previous chunk's output (staged at its end, intact until this chunk's
+        // temporal writes) goes out only now, after the wait for this chunk's
+        // prefetched data: one counter tracks vector loads and stores, so stores
+        // issued at the end of the previous chunk would have been waited for too.
+        __builtin_amdgcn_sched_barrier(0);
+        if (c > c_begin) flush_out(c - 1);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
@@ -788,17 +808,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             }
         }
         __syncthreads();
-        {
-            const int r0 = tid >> 4, d0 = (tid & 15) * 8;
-#pragma unroll
-            for (int it = 0; it < CC / 16; ++it) {
-                const int r = r0 + 16 * it;
-                if (r < n)
-                    *reinterpret_cast<uint4 *>(o + (((size_t)b * p.T + t0 + r) * p.H + h) * D + d0) =
-                        *reinterpret_cast<const uint4 *>(Stg + 16 * it * QS);
-            }
-        }
     }
+    if (c_end > c_begin) flush_out(c_end - 1);
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));
         dump_state(a.fin_state + (size_t)bh * kStateFloats, w, lane, kacc, vacc);

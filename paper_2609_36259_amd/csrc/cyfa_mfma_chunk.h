@@ -284,11 +284,9 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
         const float u = s.urev[r];
         float s1, c1, sn, cs;
         sincos_rev(u, &s1, &c1);
-        {
-            double rev = (double)(4 * q + 1) * (double)u;
-            rev -= floor(rev);
-            sincos_rev((float)rev, &sn, &cs);
-        }
+        // start phase (4q+1) u mod 1 in fp32: u < 1 and 4q+1 <= 61, so its error is
+        // below 4e-6 revolutions, far under the bf16 / f16 rounding of A and the table
+        sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
         bf16x8 a8, ad8;
         half8v cs8;
 #pragma unroll

@@ -239,7 +239,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
         if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
-        build_writes_swz<CC, false, false, true, NT, 64>(s, tid, a.p.m);
+        build_writes_swz<CC, false, NT, 64>(s, s.Ads, tid, a.p.m);
         __syncthreads();
         update_states<CC>(s, smem, w, lane, kacc, vacc);
         __syncthreads();
@@ -568,7 +568,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
         const bool fac = __builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[2])) != 0;
-        build_writes_swz<CC, true, true, false, NT, CSW, true>(s, tid, m);
+        build_writes_swz<CC, true, NT, CSW>(s, s.As, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A.  With the
         //    tile holding A_dec (rows times the right decay), Gamma_rs = gam_r decw_s

@@ -46,6 +46,8 @@ struct Tiles {
     float *urev;    // clock at each row reduced mod m, divided by m (revolutions, in [0, 1))
     float *ctl;     // [0]: factor applied to the carried states this chunk, [1]: log scale L after it,
                     // [2]: 1 when the chunk's decay factors into a row scale (A_dec tile), else 0
+    float4 *bw;     // per row, for the temporal-write builder: amplitude beta sqrt(2/m) times the
+                    // row's decay factor (when its tile holds A_dec), urev, cos and sin of 2 pi urev
 };
 
 // n entries per array (the chunk length or 64); block size scalar_bytes(n)
@@ -56,8 +58,9 @@ __device__ __forceinline__ void scalars_at(Tiles &t, char *base, int n = 64) {
     t.decw = t.betas + n;
     t.urev = t.decw + n;
     t.ctl = reinterpret_cast<float *>(t.urev + n);
+    t.bw = reinterpret_cast<float4 *>(t.ctl + 4);      // 16-byte aligned for n a multiple of 4
 }
-__host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 4) + 16; }
+__host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 4 + 16) + 16; }
 
 // Global -> register prefetch of one chunk: CC NTH/16 x 16-byte pieces per thread
 // per tensor (rows (NTH/16) it + tid / 16, columns 8 (tid % 16)), plus one
@@ -173,10 +176,18 @@ __device__ __forceinline__ void chunk_scans(const Tiles &s, int lane, int m, con
         const int ol = opq(lane);                   // one address register for the five writes
         s.Gs[ol] = G;
         s.gam[ol] = (kEps && !lazy && factored) ? __expf(G - GC) : __expf(G + L);
-        s.decw[ol] = lazy ? __expf(-G - L) : __expf(GC - G);
+        const float dw = lazy ? __expf(-G - L) : __expf(GC - G);
+        s.decw[ol] = dw;
         s.betas[ol] = pf.be;
         const double q = lam * inv_m;               // clock in revolutions of the m-slot ring
-        s.urev[ol] = (float)(q - floor(q));
+        const float u = (float)(q - floor(q));
+        s.urev[ol] = u;
+        // builder record: its tile holds A_dec (pre-pass; fused kernel when factored)
+        // or A (fused kernel otherwise)
+        float s1, c1;
+        sincos_rev(u, &s1, &c1);
+        const float amp = pf.be * sqrtf(2.f / (float)m) * ((!kEps || factored) ? dw : 1.f);
+        s.bw[ol] = make_float4(amp, u, c1, s1);
     }
     const float state_factor = lazy ? 1.f : __expf(L + GC);
     L = lazy ? L + GC : 0.f;
@@ -256,38 +267,34 @@ __device__ __forceinline__ void build_writes(const Tiles &s, int tid, int m) {
     }
 }
 
-// The same matrices stored into swizzled A / A_dec tiles, 16 threads per row so
-// that each group of 16 lanes stores one whole row, and a (cos, sin) table of
-// row stride CSW half2 words.  Thread (r, q) fills internal columns 8q .. 8q+7
-// (pairs 4q+1 .. 4q+4) of rows r = tid / 16 + (NTH / 16) it; q = 15 also holds
-// DC (column 126) and the padding (127).  kTab: write the (cos, sin) table;
-// kA / kAd: write A into As / A_dec into Ads; kSel: write A_dec into As when the
-// chunk is factored (ctl[2]), else A.
-template <int CC, bool kTab, bool kA, bool kAd, int NTH, int CSW, bool kSel = false>
-__device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m) {
+// The temporal write matrix stored into a swizzled tile (A or A_dec, as the
+// chunk scans decided: row r is amp_r [cos th_j, -sin th_j] on pair j and
+// amp_r / sqrt(2) on DC, amp_r = beta_r sqrt(2/m) times the row's decay factor
+// when the tile holds A_dec), 16 threads per row so that each group of 16 lanes
+// stores one whole row, and (kTab) a (cos, sin) table of row stride CSW half2
+// words.  Thread (r, q) fills internal columns 8q .. 8q+7 (pairs 4q+1 .. 4q+4)
+// of rows r = tid / 16 + (NTH / 16) it; q = 15 also holds DC (column 126) and the
+// padding (127).  One 16-byte read gives a row's amplitude, clock phase u and
+// unit step (cos, sin)(2 pi u); the start phase (4q+1) u mod 1 is taken in fp32:
+// u < 1 and 4q+1 <= 61 keep its error below 4e-6 revolutions, far under the bf16
+// and f16 rounding of the tile and the table.
+template <int CC, bool kTab, int NTH, int CSW>
+__device__ __forceinline__ void build_writes_swz(const Tiles &s, __bf16 *tile, int tid, int m) {
     constexpr int RPP = NTH / 16;                    // rows per pass
     static_assert(CC % RPP == 0 && RPP % 4 == 0, "whole passes with a fixed swizzle phase");
     const int q = tid & 15, r0 = tid >> 4;
     const int J = (m - 1) >> 1;
-    const float dc = 1.0f / sqrtf((float)m);
-    const float sq = sqrtf(2.0f / (float)m);
     const int pc = swz_elem(r0, 8 * q) - r0 * SWS;   // stored column of this thread's chunk
-    const bool sel_dec = kSel && s.ctl[2] != 0.f;     // uniform
     // rows one after another: interleaving them raises the register peak of the
     // fused kernel, which holds the carried states and the prefetched chunk here
 #pragma unroll 1
     for (int it = 0; it < CC / RPP; ++it) {
         const int r = r0 + RPP * it;
-        const float be = s.betas[r];
-        const float bac = be * sq;
-        const float wdec = kAd ? s.decw[r] : (kSel ? (sel_dec ? s.decw[r] : 1.f) : 0.f);
-        const float u = s.urev[r];
-        float s1, c1, sn, cs;
-        sincos_rev(u, &s1, &c1);
-        // start phase (4q+1) u mod 1 in fp32: u < 1 and 4q+1 <= 61, so its error is
-        // below 4e-6 revolutions, far under the bf16 / f16 rounding of A and the table
+        const float4 rec = s.bw[r];
+        const float amp = rec.x, u = rec.y, c1 = rec.z, s1 = rec.w;
+        float sn, cs;
         sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
-        bf16x8 a8, ad8;
+        bf16x8 a8;
         half8v cs8;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
@@ -295,17 +302,13 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
             const bool live = j <= J && j <= 63;
             const float cv = live ? cs : 0.f;
             const float sv = live ? sn : 0.f;
-            float a0 = bac * cv, a1 = -bac * sv;
+            float a0 = amp * cv, a1 = -amp * sv;
             if (jj == 3 && q == 15) {
-                a0 = be * dc;                        // internal column 126: DC
+                a0 = amp * 0.70710678118654752f;     // internal column 126: DC
                 a1 = 0.f;                            // 127: padding
             }
-            a8[2 * jj] = (__bf16)(kSel ? a0 * wdec : a0);
-            a8[2 * jj + 1] = (__bf16)(kSel ? a1 * wdec : a1);
-            if (kAd) {
-                ad8[2 * jj] = (__bf16)(a0 * wdec);
-                ad8[2 * jj + 1] = (__bf16)(a1 * wdec);
-            }
+            a8[2 * jj] = (__bf16)a0;
+            a8[2 * jj + 1] = (__bf16)a1;
             // table entry 63 (DC and padding) is (1, 0): the token-wise rotations
             // pass those columns through unchanged
             cs8[2 * jj] = (_Float16)(j == 64 ? 1.f : cv);
@@ -317,9 +320,8 @@ __device__ __forceinline__ void build_writes_swz(const Tiles &s, int tid, int m)
                 sn = ns;
             }
         }
-        if (kA) *reinterpret_cast<bf16x8 *>(s.As + r * SWS + pc) = a8;
+        *reinterpret_cast<bf16x8 *>(tile + r * SWS + pc) = a8;
         if (kTab) *reinterpret_cast<half8v *>(s.CS + r * CSW + 4 * q) = cs8;
-        if (kAd) *reinterpret_cast<bf16x8 *>(s.Ads + r * SWS + pc) = ad8;
     }
 }
 

@@ -56,12 +56,11 @@ struct Lay {
     static constexpr int A = V + STILE;                // A   (temporal writes, swizzled)
     static constexpr int S = A + STILE;                // scores [CC][SSC] bf16 / softmax partials
     static constexpr int RED = S;                      // (max, sum) per wave x row, middle step only
-    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][CSW] half pairs -> output staging [CC][QS]
+    static constexpr int CS = S + CC * SSC * 2;        // (cos, sin) [CC][CSW] half pairs
     static constexpr int MT = CS + CC * CSW * 4;       // readout matrix [128][SWS] bf16 (swizzled)
     static constexpr int SC = MT + 128 * SWS * 2;      // per-token scalars (CC entries each)
     static constexpr int BYTES = SC + scalar_bytes(CC);
     static_assert(4 * CC * 8 <= CC * SSC * 2, "softmax partials fit the score tile");
-    static_assert(CSW * 4 == QS * 2, "output staging fits the (cos, sin) table");
     static_assert(K % 256 == 0 && V % 256 == 0 && A % 256 == 0 && MT % 256 == 0,
                   "swizzled tiles start on a bank-window boundary");
     static_assert(CC != 32 || BYTES <= 80 * 1024, "two workgroups per compute unit");
@@ -500,13 +499,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const int rowb = opq(2 * (l32 * QS + 32 * w + h4));
     __bf16 *Wrow = lds_at<__bf16>(smem, Ly::Q + rowb);
     __bf16 *O2row = Wrow + TE;
-    // output staging: [CC][QS] bf16 in the (cos, sin) table, which is free from the
-    // O'' rotation until the next chunk's temporal writes
-    __bf16 *Strow = lds_at<__bf16>(smem, Ly::CS + rowb);
     const half2v *CSrow = lds_at<half2v>(smem, Ly::CS + rowb);
     float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
     const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
-    const __bf16 *Stg = lds_at<__bf16>(smem, opq(Ly::CS + 2 * ((tid >> 4) * QS + (tid & 15) * 8)));
 
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
@@ -535,32 +530,12 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     Prefetch<CC> pf;
     load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
-    // staged output tile of chunk tc -> o, 16-byte stores: uniform chunk base plus a
-    // 32-bit lane offset (opaque per call, so no 64-bit lane address lives across
-    // the loop)
-    auto flush_out = [&](int tc) {
-        const int tb = tc * CC, nn = min(CC, p.T - tb);
-        const int r0 = tid >> 4;
-        char *ob = reinterpret_cast<char *>(o + (((size_t)b * p.T + tb) * p.H + h) * D);
-        const unsigned loff = (unsigned)opq((r0 * p.H * D + (tid & 15) * 8) * 2);
-        const unsigned pass = (unsigned)(16 * p.H * D * 2);
-#pragma unroll
-        for (int it = 0; it < CC / 16; ++it)
-            if (r0 + 16 * it < nn)
-                *reinterpret_cast<uint4 *>(ob + it * pass + loff) = *reinterpret_cast<const uint4 *>(Stg + 16 * it * QS);
-    };
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
         const int n = min(CC, p.T - t0);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
-        // The previous chunk's output (staged at its end, intact until this chunk's
-        // temporal writes) goes out only now, after the wait for this chunk's
-        // prefetched data: one counter tracks vector loads and stores, so stores
-        // issued at the end of the previous chunk would have been waited for too.
-        __builtin_amdgcn_sched_barrier(0);
-        if (c > c_begin) flush_out(c - 1);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
@@ -780,13 +755,19 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) pacc[v] *= et;
         }
-        // output tile -> staging [token][column] for 16-byte global stores
+        // output: lane (token l32, half hl) stores its 16 columns 32w + 4hl + 8 v4 ..
+        // as four 8-byte pieces (uniform chunk base plus a 32-bit lane offset); the
+        // four waves' pieces of a token row merge in L2
+        if (l32 < n) {
+            char *ob = reinterpret_cast<char *>(o + (((size_t)b * p.T + t0) * p.H + h) * D);
+            const unsigned loff = (unsigned)opq((l32 * p.H * D + 32 * w + h4) * 2);
 #pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-            bf16x4 ov;
+            for (int v4 = 0; v4 < 4; ++v4) {
+                bf16x4 ov;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) ov[k] = (__bf16)pacc[4 * v4 + k];
-            *reinterpret_cast<bf16x4 *>(Strow + 8 * v4) = ov;
+                for (int k = 0; k < 4; ++k) ov[k] = (__bf16)pacc[4 * v4 + k];
+                *reinterpret_cast<bf16x4 *>(ob + loff + 16 * v4) = ov;
+            }
         }
         {
             // value state: Vbar' += A_dec^T V (decay kept in L)
@@ -809,7 +790,6 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
         __syncthreads();
     }
-    if (c_end > c_begin) flush_out(c_end - 1);
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));
         dump_state(a.fin_state + (size_t)bh * kStateFloats, w, lane, kacc, vacc);

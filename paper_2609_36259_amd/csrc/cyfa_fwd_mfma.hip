@@ -37,12 +37,12 @@ namespace {
 
 // ---- LDS maps (bytes) ---------------------------------------------------------
 // Fused kernel (32-token chunks).  Tiles read through the transpose read (K, V,
-// A and the readout matrix M) are swizzled rows of 128; Q (then X, W), O'' and
-// the output staging are padded to stride QS.  K's region switches to the
-// padded layout when O'' replaces K.  Two workgroups share a compute unit, so
-// the map stays within half of its 160 KiB: there is no A_dec tile (its row
-// scale is applied to the other operand of each state update) and the softmax
-// partials share the score tile.
+// A and the readout matrix M) are swizzled rows of 128; Q (then X, W) and O''
+// are padded to stride QS.  K's region switches to the padded layout when O''
+// replaces K.  Two workgroups share a compute unit, so the map stays within half
+// of its 160 KiB: one temporal-write tile (A_dec for a chunk whose decay factors
+// into a row scale, else A, whose state updates then decay the other operand),
+// and the softmax partials share the score tile.
 template <int CC>
 struct Lay {
     static constexpr int RB = CC / 32;                 // 32-row blocks per tile
@@ -492,9 +492,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const __bf16 *Sa = lds_at<__bf16>(smem, opq(Ly::S + 2 * (l32 * SSC + 8 * hl)));
     const __bf16 *At = lds_at<__bf16>(smem, Ly::A + trw);
     const __bf16 *Vt = lds_at<__bf16>(smem, Ly::V + trw);
-    // token-row base: row l32, columns 32w + 4hl (+ 8 v4) of the X / W, O'' and
-    // output-staging tiles, and the matching (cos, sin) pairs (the padded tile rows
-    // and the table rows are both 272 bytes)
+    // token-row base: row l32, columns 32w + 4hl (+ 8 v4) of the X / W and O''
+    // tiles, and the matching (cos, sin) pairs (the padded tile rows and the table
+    // rows are both 272 bytes)
     static_assert(QS * 2 == CSW * 4, "one token-row base for the padded tiles and the table");
     const int rowb = opq(2 * (l32 * QS + 32 * w + h4));
     __bf16 *Wrow = lds_at<__bf16>(smem, Ly::Q + rowb);

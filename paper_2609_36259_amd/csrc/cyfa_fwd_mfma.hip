@@ -64,9 +64,6 @@ struct Lay {
     static_assert(K % 256 == 0 && V % 256 == 0 && A % 256 == 0 && MT % 256 == 0,
                   "swizzled tiles start on a bank-window boundary");
     static_assert(CC != 32 || BYTES <= 80 * 1024, "two workgroups per compute unit");
-    // state pre-pass: K, V, A_dec (swizzled) and the scalars (64 entries)
-    static constexpr int PK = 0, PV = STILE, PAD = 2 * STILE, PSC = 3 * STILE;
-    static constexpr int PBYTES = PSC + scalar_bytes(64);
 };
 
 template <int CC>
@@ -88,51 +85,6 @@ __device__ __forceinline__ Tiles fused_tiles(char *smem) {
     t.Stage = reinterpret_cast<__bf16 *>(smem + L::CS);
     scalars_at(t, smem + L::SC, CC);
     return t;
-}
-
-template <int CC>
-__device__ __forceinline__ Tiles prepass_tiles(char *smem) {
-    using L = Lay<CC>;
-    Tiles t{};
-    t.Ks = reinterpret_cast<__bf16 *>(smem + L::PK);
-    t.Vs = reinterpret_cast<__bf16 *>(smem + L::PV);
-    t.Ads = reinterpret_cast<__bf16 *>(smem + L::PAD);
-    scalars_at(t, smem + L::PSC);
-    return t;
-}
-
-// Carried-state updates of one chunk (App. B):
-//   Kbar^T <- gamma^C Kbar^T + K^T A_dec,   Vbar <- gamma^C Vbar + A_dec^T V
-// Operands: K^T, A_dec and V come from swizzled row-major tiles through
-// transpose reads (column block x of a tile at the lane's offset ^ 64 x).
-template <int CC>
-__device__ __forceinline__ void update_states(const Tiles &s, char *smem, int w, int lane,
-                                              f32x16 (&kacc)[4], f32x16 (&vacc)[4]) {
-    using L = Lay<CC>;
-    const float sf = s.ctl[0];
-    if (sf != 1.f) {
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                kacc[x][v] *= sf;
-                vacc[x][v] *= sf;
-            }
-    }
-    const int trs = tr_off_swz(lane);
-    const int Kt = opq(L::PK + trs), Adt = opq(L::PAD + trs);
-    const __bf16 *Vt = lds_at<__bf16>(smem, opq(L::PV + (trs ^ (64 * w))));
-    const __bf16 *Adw = lds_at<__bf16>(smem, opq(L::PAD + (trs ^ (64 * w))));
-#pragma unroll
-    for (int ks = 0; ks < CC / 16; ++ks) {
-        const bf16x8 ad_w = lds8_tr(Adw + 16 * ks * SWS, SWS);
-        const bf16x8 v_w = lds8_tr(Vt + 16 * ks * SWS, SWS);
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Kt) ^ (64 * x)) + 16 * ks * SWS, SWS), ad_w, kacc[x]);
-            vacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, opq(Adt) ^ (64 * x)) + 16 * ks * SWS, SWS), v_w, vacc[x]);
-        }
-    }
 }
 
 // One 16 x 16 block (rb, sb) of the causal score tile -> Ss (bf16), k = 128 along
@@ -214,41 +166,151 @@ __device__ __forceinline__ void dump_state(T *st, int w, int lane, const f32x16 
 }
 
 // ---- 1. per-segment state contributions -------------------------------------
+// DeltaS_p = sum_t exp(G_end - G_t) a_t [k_t | v_t]^T over the segment's tokens,
+// with a_t = beta_t U(-lambda_t) b the temporal write (Eq. app-temporal-writes),
+// lambda_t the clock from the segment start and G_t the inclusive sum of log alpha
+// from the segment start (App. B, the carried-state recurrence unrolled from a
+// zero state).  G_end - G_t <= 0, so every weight lies in [0, 1].
+//
+// Wave w owns the 32 slot columns 32w .. 32w+31 of both contributions and builds
+// its own part of the decayed write matrix directly in MFMA operand registers:
+// lane l holds column 32w + l%32 at the 8 tokens 16ks + 8h + p (h = l/32), which
+// is the B operand of Kbar^T += K^T A_dec and the A operand of
+// Vbar += A_dec^T V alike.  K^T and V come from swizzled tiles through the
+// transpose read, double-buffered so that a chunk needs one barrier.  Each wave
+// runs the chunk's clock and decay scans itself (lane = token) and passes the
+// per-token phase and amplitude through a private LDS row.
 template <int CC>
 __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
-    __shared__ __attribute__((aligned(256))) char smem[Lay<CC>::PBYTES];
-    const Tiles s = prepass_tiles<CC>(smem);
+    constexpr int STILE = CC * SWS * 2;                // one swizzled K or V tile
+    constexpr int KIT = CC * 16 / NT;                  // 16-byte pieces per thread per tensor
+    constexpr int RPP = NT / 16;                       // tile rows per pass
+    constexpr int SCB = 4 * STILE;                     // per-wave (phase, amplitude) rows
+    __shared__ __attribute__((aligned(256))) char smem[SCB + 4 * 64 * 8 + 4 * 8];
+    const FwdParams &p = a.p;
     const int Pm1 = a.P - 1;
-    const int bh = blockIdx.x / Pm1, p = blockIdx.x % Pm1;
-    const int b = bh / a.p.H, h = bh % a.p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int c_begin = p * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
+    const int bh = blockIdx.x / Pm1, seg = blockIdx.x % Pm1;
+    const int b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5, l32 = lane & 31;
+    const int m = p.m;
+    const double inv_m = 1.0 / (double)m;
+    const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
+    const int t_begin = c_begin * CC, t_end = min(c_end * CC, p.T);
+    float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
+    double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
+
+    // this lane's write-matrix column: internal index cidx = 32w + l32 is the cosine
+    // (even) or minus sine (odd, a quarter turn later) of pair j = cidx/2 + 1, or the
+    // DC (126, amplitude 1/sqrt(2) of the pairs'), or padding / inactive pair (0)
+    const int cidx = 32 * w + l32;
+    const int J = (m - 1) >> 1;
+    const float jf = cidx < kDC ? (float)((cidx >> 1) + 1) : 0.f;
+    const float shift = (cidx < kDC && (cidx & 1)) ? 0.25f : 0.f;
+    const float mult = cidx < 2 * J ? 1.f : (cidx == kDC ? 0.70710678118654752f : 0.f);
+    const float amp0 = sqrtf(2.f / (float)m);
+
+    // segment total of log alpha (the decay reference G_end)
+    double gpart = 0.0;
+    if (p.log_alpha)
+        for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[((size_t)b * p.T + t) * p.H + h];
+    gpart = lane63(wave_incl_scan(gpart));
+    if (lane == 0) red[w] = gpart;
+
+    // K, V pieces: rows tid/16 + RPP it, 16-byte column block tid%16; scalars of
+    // token `lane` of the chunk on every wave
+    const size_t row_el = (size_t)p.H * D;
+    const unsigned loff = (unsigned)(((tid >> 4) * (int)row_el + (tid & 15) * 8) * 2);
+    const unsigned pass = (unsigned)(RPP * row_el * 2);
+    const int kvo = 2 * swz_elem(tid >> 4, (tid & 15) * 8);
+    uint4 pk[KIT], pv[KIT];
+    float dl, g, be;
+    auto load = [&](int c) {
+        const int t0 = c * CC;
+        const size_t base = (((size_t)b * p.T + t0) * row_el + (size_t)h * D) * 2;
+        const char *kb = reinterpret_cast<const char *>(p.k) + base;
+        const char *vb = reinterpret_cast<const char *>(p.v) + base;
+#pragma unroll
+        for (int it = 0; it < KIT; ++it) {
+            const bool in = t0 + (tid >> 4) + RPP * it < p.T;
+            pk[it] = in ? *reinterpret_cast<const uint4 *>(kb + loff + it * pass) : make_uint4(0, 0, 0, 0);
+            pv[it] = in ? *reinterpret_cast<const uint4 *>(vb + loff + it * pass) : make_uint4(0, 0, 0, 0);
+        }
+        const int t = t0 + lane;
+        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        const bool tin = lane < CC && t < p.T;
+        dl = tin ? p.delta[si] : 0.f;
+        g = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
+        be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+    };
+    if (c_begin < c_end) load(c_begin);
+    __syncthreads();
+    const double G_end = (red[0] + red[1]) + (red[2] + red[3]);
+
     f32x16 kacc[4], vacc[4];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
-        kacc[x] = f32x16{};
-        vacc[x] = f32x16{};
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
     }
     double carry = 0.0, gsum = 0.0;
-    float L = 0.f;
-    Prefetch<CC> pf;
-    load_chunk<CC, false>(a.p, b, h, c_begin * CC, tid, pf);
+    const int trs = tr_off_swz(lane);
     for (int c = c_begin; c < c_end; ++c) {
-        store_chunk<CC, false, NT, true>(s, tid, pf);
-        if (w == 0) chunk_scans<CC>(s, lane, a.p.m, pf, carry, gsum, L);
+        const int buf = (c - c_begin) & 1;
+        char *Kt = smem + 2 * buf * STILE;
+        char *Vt = Kt + STILE;
+#pragma unroll
+        for (int it = 0; it < KIT; ++it) {
+            *reinterpret_cast<uint4 *>(Kt + kvo + it * RPP * SWS * 2) = pk[it];
+            *reinterpret_cast<uint4 *>(Vt + kvo + it * RPP * SWS * 2) = pv[it];
+        }
+        {
+            // clock (fp64, from the segment start) and decay to the segment end
+            const double lam = carry + wave_incl_scan((double)dl);
+            const float Gl = wave_incl_scan(g);
+            const float rem = (float)(G_end - gsum);
+            const double q = lam * inv_m;
+            const float u = (float)(q - floor(q));
+            scw[lane] = make_float2(u, be * amp0 * __expf(rem - Gl));
+            carry = reduce_clock(lane63(lam), (double)m, inv_m);
+            gsum += (double)lane63(Gl);
+        }
+        if (c + 1 < c_end) load(c + 1);
         __syncthreads();
-        if (c + 1 < c_end) load_chunk<CC, false>(a.p, b, h, (c + 1) * CC, tid, pf);
-        build_writes_swz<CC, false, NT, 64>(s, s.Ads, tid, a.p.m);
-        __syncthreads();
-        update_states<CC>(s, smem, w, lane, kacc, vacc);
-        __syncthreads();
+        const int kt = opq(2 * buf * STILE + trs), vt = opq((2 * buf + 1) * STILE + trs);
+#pragma unroll
+        for (int ks = 0; ks < CC / 16; ++ks) {
+            const float4 *sp = reinterpret_cast<const float4 *>(scw + 16 * ks + 8 * hl);
+            bf16x8 af;
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) {
+                const float4 r = sp[q2];
+                af[2 * q2] = (__bf16)(__builtin_amdgcn_cosf(__builtin_amdgcn_fractf(fmaf(jf, r.x, shift))) *
+                                      (r.y * mult));
+                af[2 * q2 + 1] = (__bf16)(__builtin_amdgcn_cosf(__builtin_amdgcn_fractf(fmaf(jf, r.z, shift))) *
+                                          (r.w * mult));
+            }
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                kacc[x] = mma(lds8_tr(lds_at<__bf16>(smem, kt ^ (64 * x)) + 16 * ks * SWS, SWS), af, kacc[x]);
+                vacc[x] = mma(af, lds8_tr(lds_at<__bf16>(smem, vt ^ (64 * x)) + 16 * ks * SWS, SWS), vacc[x]);
+            }
+        }
     }
-    const size_t slot = (size_t)bh * a.P + p;
-    scale_states(kacc, vacc, __expf(s.ctl[1]));
-    dump_state(a.seg_state + slot * kStateFloats, w, lane, kacc, vacc);
+    // dump in the accumulator order of the fused kernel: key state as written
+    // (wave = slot block, x = d block); value state with the roles of wave and
+    // block exchanged (the fused kernel's wave owns a d_v block)
+    const size_t slot = (size_t)bh * a.P + seg;
+    __bf16 *st = a.seg_state + slot * kStateFloats;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            st[((w * 4 + x) * 16 + v) * 64 + lane] = (__bf16)kacc[x][v];
+            st[128 * 128 + ((x * 4 + w) * 16 + v) * 64 + lane] = (__bf16)vacc[x][v];
+        }
     if (tid == 0) {
         a.seg_span[slot] = carry;
-        a.seg_gsum[slot] = gsum;
+        a.seg_gsum[slot] = G_end;
     }
 }
 

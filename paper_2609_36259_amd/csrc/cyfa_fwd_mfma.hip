@@ -181,7 +181,7 @@ __device__ __forceinline__ void dump_state(T *st, int w, int lane, const f32x16 
 // runs the chunk's clock and decay scans itself (lane = token) and passes the
 // per-token phase and amplitude through a private LDS row.
 template <int CC>
-__global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float mz_scale) {
     constexpr int STILE = CC * SWS * 2;                // one swizzled K or V tile
     constexpr int KIT = CC * 16 / NT;                  // 16-byte pieces per thread per tensor
     constexpr int RPP = NT / 16;                       // tile rows per pass
@@ -198,6 +198,16 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a) {
     const int t_begin = c_begin * CC, t_end = min(c_end * CC, p.T);
     float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
     double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
+    {
+        // blocks past the segments form 32 rows of the bf16 readout matrix each
+        const int nseg = p.B * p.H * Pm1;
+        if ((int)blockIdx.x >= nseg) {
+            const int q = (int)blockIdx.x - nseg;
+            readout_prep_rows32(m, p.R, const_cast<__bf16 *>(a.Mz), mz_scale, q / (kStoreRows / kPrepRows32),
+                                q % (kStoreRows / kPrepRows32), tid, smem);
+            return;
+        }
+    }
 
     // this lane's write-matrix column: internal index cidx = 32w + l32 is the cosine
     // (even) or minus sine (odd, a quarter turn later) of pair j = cidx/2 + 1, or the
@@ -941,27 +951,30 @@ template <int CC>
 hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_start,
                      hipEvent_t ev_stop) {
     hipError_t e;
-    if (a.P > 1 && a.nchunks > 0) {
+    // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
+    const float mz_scale = a.p.scale * 1.4426950408889634f;
+    const bool prepass = a.P > 1 && a.nchunks > 0;
+    if (prepass) {
         // Only each segment's total contribution is needed, so the pre-pass may
         // step through a segment in 64-token chunks (fewer barriers and per-chunk
         // costs) whenever its length is a whole number of them.  Every segment but
-        // the last is full, and the last one is not pre-passed.
+        // the last is full, and the last one is not pre-passed.  Extra blocks of
+        // the same launch form the bf16 readout matrix, 32 rows each.
+        const int nblk = BH * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows32);
         if (CC == 32 && a.cps % 2 == 0) {
             MfmaArgs a64 = a;
             a64.chunk = 64;
             a64.cps = a.cps / 2;
             a64.nchunks = (a.p.T + 63) / 64;
-            hipLaunchKernelGGL(segment_state_kernel<64>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a64);
+            hipLaunchKernelGGL(segment_state_kernel<64>, dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
         } else {
-            hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(BH * (a.P - 1)), dim3(NT), 0, st, a);
+            hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(nblk), dim3(NT), 0, st, a, mz_scale);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
-    const float mz_scale = a.p.scale * 1.4426950408889634f;
     if (a.has_init) {
         const int nscan = BH * kScanBlocks;
-        const int nprep = a.p.H * (kStoreRows / kPrepRows);
+        const int nprep = prepass ? 0 : a.p.H * (kStoreRows / kPrepRows);
         hipLaunchKernelGGL(scan_prep_kernel, dim3(nscan + nprep), dim3(NT), 0, st, a, nscan, mz_scale);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else if ((e = launch_readout_prep(a.p.H, a.p.m, a.p.R, nullptr, const_cast<__bf16 *>(a.Mz),

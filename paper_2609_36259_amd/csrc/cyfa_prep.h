@@ -85,4 +85,65 @@ __device__ __forceinline__ void readout_prep_block(int m, const float *__restric
     }
 }
 
+// Rows [32 rb, 32 rb + 32) of the bf16 matrix Mz of head h (the matrix-core
+// kernels' copy only), in LDS the caller provides (at least 17 KiB, 16-byte
+// aligned): extra blocks of the segment pre-pass run this, so that the readout
+// matrix is formed while the pre-pass streams k and v.  Thread (j = tid % 128,
+// g = tid / 128) computes paper column j of rows 32 rb + 16 g .. + 15; R's rows
+// are staged zero-padded to 128 columns and read four columns at a time.
+constexpr int kPrepRows32 = 32;
+__device__ __forceinline__ void readout_prep_rows32(int m, const float *__restrict__ R,
+                                                    __bf16 *__restrict__ Mz, float mz_scale, int h,
+                                                    int rb, int tid, char *lds) {
+    float *tab = reinterpret_cast<float *>(lds);            // [2][128] cos, sin of 2 pi r / m
+    float *Rr = tab + 256;                                  // [32][128]
+    const int row0 = kPrepRows32 * rb;
+    if (tid < m) {
+        double sn, cs;
+        sincospi(2.0 * (double)tid / (double)m, &sn, &cs);
+        tab[tid] = (float)cs;
+        tab[128 + tid] = (float)sn;
+    }
+    const float *Rh = R ? R + (size_t)h * m * m : nullptr;
+    for (int e = tid; e < kPrepRows32 * 128; e += 256) {
+        const int r = e >> 7, sc = e & 127, i = row0 + r;
+        Rr[e] = (i < m && sc < m) ? (Rh ? Rh[(size_t)i * m + sc] : (sc == i ? 1.f : 0.f)) : 0.f;
+    }
+    __syncthreads();
+    const int j = tid & 127, g = tid >> 7;
+    // column j: DC (j = 0: constant 1), cosine (odd j) or sine (even j > 0) of
+    // frequency l = (j + 1) / 2; the table index l s mod m advances by l per step
+    const float *t = (j == 0 || (j & 1)) ? tab : tab + 128;
+    const int l = (j + 1) >> 1;
+    float acc[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    if (j < m) {
+        int idx = 0;
+        for (int s0 = 0; s0 < 128; s0 += 4) {
+            float ph[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                ph[q] = t[idx];
+                idx += l;
+                if (idx >= m) idx -= m;
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float4 rv = *reinterpret_cast<const float4 *>(Rr + (16 * g + r) * 128 + s0);
+                acc[r] = fmaf(rv.x, ph[0], fmaf(rv.y, ph[1], fmaf(rv.z, ph[2], fmaf(rv.w, ph[3], acc[r]))));
+            }
+        }
+    }
+    const float cscale = j == 0 ? (float)(1.0 / sqrt((double)m)) : (float)sqrt(2.0 / (double)m);
+    const int jint = j == 0 ? kStoreRows - 2 : (j == kStoreRows - 1 ? kStoreRows - 1 : j - 1);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int i = row0 + 16 * g + r;
+        const float val = (j < m && i < m) ? acc[r] * cscale : 0.f;
+        const float z = (j == kStoreRows - 1 && i >= m) ? kMaskLogit : mz_scale * val;
+        Mz[((size_t)h * kStoreRows + i) * kStoreRows + jint] = (__bf16)z;
+    }
+}
+
 }  // namespace cyfa

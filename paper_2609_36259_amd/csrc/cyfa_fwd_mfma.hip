@@ -142,26 +142,36 @@ __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4
 
 // Segment-boundary states travel in bf16 (the precision in which the chunk
 // products consume them); the carried states themselves accumulate in fp32.
+// Lane-major dump layout: two 16-byte loads per accumulator.
 __device__ __forceinline__ void load_state(const __bf16 *st, int w, int lane, f32x16 (&kacc)[4],
                                            f32x16 (&vacc)[4]) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int x = 0; x < 4; ++x) {
+        const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 0));
+        const bf16x8 k1 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 8));
+        const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 0));
+        const bf16x8 v1 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 8));
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            kacc[x][v] = (float)st[((w * 4 + x) * 16 + v) * 64 + lane];
-            vacc[x][v] = (float)st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane];
+        for (int v = 0; v < 8; ++v) {
+            kacc[x][v] = (float)k0[v];
+            kacc[x][v + 8] = (float)k1[v];
+            vacc[x][v] = (float)v0[v];
+            vacc[x][v + 8] = (float)v1[v];
         }
+    }
 }
 
-template <typename T>
-__device__ __forceinline__ void dump_state(T *st, int w, int lane, const f32x16 (&kacc)[4],
+// fp32 dump (the final state), four 16-byte stores per accumulator
+__device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32x16 (&kacc)[4],
                                            const f32x16 (&vacc)[4]) {
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            st[((w * 4 + x) * 16 + v) * 64 + lane] = (T)kacc[x][v];
-            st[128 * 128 + ((w * 4 + x) * 16 + v) * 64 + lane] = (T)vacc[x][v];
+        for (int q = 0; q < 4; ++q) {
+            *reinterpret_cast<float4 *>(st + dump_off(w, x, lane, 4 * q)) =
+                make_float4(kacc[x][4 * q], kacc[x][4 * q + 1], kacc[x][4 * q + 2], kacc[x][4 * q + 3]);
+            *reinterpret_cast<float4 *>(st + 128 * 128 + dump_off(w, x, lane, 4 * q)) =
+                make_float4(vacc[x][4 * q], vacc[x][4 * q + 1], vacc[x][4 * q + 2], vacc[x][4 * q + 3]);
         }
 }
 
@@ -314,9 +324,15 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            st[((w * 4 + x) * 16 + v) * 64 + lane] = (__bf16)kacc[x][v];
-            st[128 * 128 + ((x * 4 + w) * 16 + v) * 64 + lane] = (__bf16)vacc[x][v];
+        for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 kq, vq;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                kq[v] = (__bf16)kacc[x][8 * hf + v];
+                vq[v] = (__bf16)vacc[x][8 * hf + v];
+            }
+            *reinterpret_cast<bf16x8 *>(st + dump_off(w, x, lane, 8 * hf)) = kq;
+            *reinterpret_cast<bf16x8 *>(st + 128 * 128 + dump_off(x, w, lane, 8 * hf)) = vq;
         }
     if (tid == 0) {
         a.seg_span[slot] = carry;
@@ -325,10 +341,14 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
 }
 
 // ---- 2. states entering each segment ----------------------------------------
-// Element pairs that a rotation U(tau) mixes sit next to each other in the
-// accumulator-dump layout: key-state partners are adjacent lanes (offsets e,
-// e + 1), value-state partners are adjacent registers (offsets e, e + 64).
-// pair_ref(g) names pair g of a (b, h): g < 8192 key state, else value state.
+// Element pairs that a rotation U(tau) mixes, in the lane-major dump layout:
+// key-state partners are adjacent lanes (offsets e, e + 16), value-state
+// partners adjacent registers (offsets e, e + 1).  Pairs are numbered so that
+// thread t of the scan owns pairs 4t .. 4t+3 (g < 8192 key state, else value):
+//   key   t = (block wx, lane pair k, register quad q): lanes 2k, 2k+1, registers
+//         4q .. 4q+3 -- one slot pair, so the four share one frequency;
+//   value t = (block wx, lane, register half h8): registers 8 h8 .. 8 h8 + 7 of
+//         one lane, i.e. four consecutive slot pairs of one column.
 struct PairRef {
     int o0, o1;        // dump offsets of the (cos, sin) pair
     int i0;            // internal index of the first element (even)
@@ -339,23 +359,23 @@ struct PairRef {
 __device__ __forceinline__ PairRef pair_ref(int gidx) {
     PairRef r;
     if (gidx < 8192) {                                   // key state: lanes (2k, 2k+1)
-        const int e = 2 * gidx;
-        const int lane = e & 63, v = (e >> 6) & 15, blk = (e >> 10) & 3, w = e >> 12;
-        r.o0 = e;
-        r.o1 = e + 1;
-        r.i0 = 32 * w + (lane & 31);
-        const int h = lane >> 5;
-        r.col = 32 * blk + 8 * (v >> 2) + 4 * h + (v & 3);
+        const int t = gidx >> 2, e = gidx & 3;
+        const int q = t & 3, k = (t >> 2) & 31, wx = t >> 7;
+        const int w = wx >> 2, x = wx & 3, lane0 = 2 * k, h = lane0 >> 5;
+        r.o0 = dump_off(w, x, lane0, 4 * q + e);
+        r.o1 = r.o0 + 16;
+        r.i0 = 32 * w + (lane0 & 31);
+        r.col = 32 * x + 8 * q + 4 * h + e;
         r.value = false;
-    } else {                                             // value state: registers (2k, 2k+1)
+    } else {                                             // value state: registers (v, v+1)
         const int g = gidx - 8192;
-        const int lane = g & 63, vp = (g >> 6) & 7, blk = (g >> 9) & 3, w = g >> 11;
-        const int v = 2 * vp;
-        const int e = ((w * 4 + blk) * 16 + v) * 64 + lane;
-        r.o0 = 128 * 128 + e;
-        r.o1 = 128 * 128 + e + 64;
-        const int h = lane >> 5;
-        r.i0 = 32 * blk + 8 * (v >> 2) + 4 * h + (v & 3);
+        const int t = g >> 2, e = g & 3;
+        const int h8 = t & 1, lane = (t >> 1) & 63, wx = t >> 7;
+        const int w = wx >> 2, x = wx & 3, h = lane >> 5;
+        const int v = 8 * h8 + 2 * e;
+        r.o0 = 128 * 128 + dump_off(w, x, lane, v);
+        r.o1 = r.o0 + 1;
+        r.i0 = 32 * x + 8 * (v >> 2) + 4 * h + (v & 3);
         r.col = 32 * w + (lane & 31);
         r.value = true;
     }
@@ -369,42 +389,38 @@ __device__ __forceinline__ double ring_rev(double tau, int m) {
     const double inv_m = 1.0 / (double)m;
     return reduce_clock(tau, (double)m, inv_m) * inv_m;
 }
-__device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x1) {
+__device__ __forceinline__ void ring_sincos(double u, int j, float *sn, float *cs) {
     double rev = (double)j * u;
     rev -= floor(rev);
-    float sn, cs;
-    sincos_rev((float)rev, &sn, &cs);
+    sincos_rev((float)rev, sn, cs);
+}
+__device__ __forceinline__ void apply_rot(float sn, float cs, float &x0, float &x1) {
     const float y0 = cs * x0 - sn * x1;
     const float y1 = sn * x0 + cs * x1;
     x0 = y0;
     x1 = y1;
 }
+__device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x1) {
+    float sn, cs;
+    ring_sincos(u, j, &sn, &cs);
+    apply_rot(sn, cs, x0, x1);
+}
 
 // Thread = four rotation pairs moved with two 8-byte (4 x bf16) accesses per
-// segment: key state, 8 consecutive entries (pairs are adjacent lanes); value
-// state, 4 consecutive lanes of registers v and v + 1 (pairs are register
-// pairs, and the four share one frequency).  Blocks (bh, y < 16) of 256
-// threads: 2048 key and 2048 value threads per (b, h).
+// segment (see pair_ref): key state, four registers of each partner lane;
+// value state, eight consecutive registers of one lane.  Blocks (bh, y < 16)
+// of 256 threads: 2048 key and 2048 value threads per (b, h).
 constexpr int kScanBlocks = 4096 / NT;                   // blocks per (b, h)
 __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, int tid) {
     const int qi = y * NT + tid;                         // 0 .. 4095
     const int m = a.p.m;
     const bool value = qi >= 2048;
-    int off0, off1;                                      // dump offsets of the two float4
     PairRef pr[4];
-    if (!value) {
-        off0 = 8 * qi;
-        off1 = off0 + 4;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) pr[k] = pair_ref(4 * qi + k);
-    } else {
-        const int q = qi - 2048;
-        const int lane0 = 4 * (q & 15), vp = (q >> 4) & 7, blk = (q >> 7) & 3, w = q >> 9;
-        off0 = 128 * 128 + ((w * 4 + blk) * 16 + 2 * vp) * 64 + lane0;
-        off1 = off0 + 64;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) pr[k] = pair_ref(8192 + lane0 + k + 64 * (vp + 8 * (blk + 4 * w)));
-    }
+    for (int k = 0; k < 4; ++k) pr[k] = pair_ref(4 * qi + k);
+    // key: first elements of the four pairs, then the second elements; value: the
+    // four pairs' elements in register order
+    const int off0 = pr[0].o0, off1 = value ? pr[2].o0 : pr[0].o1;
     int jf[4];
     bool rot[4];
 #pragma unroll
@@ -460,11 +476,6 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
             float d0[4], d1[4];
             bf16x4 s0, s1;
             if (!value) {
-                s0[0] = (__bf16)x0[0]; s0[1] = (__bf16)x1[0]; s0[2] = (__bf16)x0[1]; s0[3] = (__bf16)x1[1];
-                s1[0] = (__bf16)x0[2]; s1[1] = (__bf16)x1[2]; s1[2] = (__bf16)x0[3]; s1[3] = (__bf16)x1[3];
-                d0[0] = (float)da[u][0]; d1[0] = (float)da[u][1]; d0[1] = (float)da[u][2]; d1[1] = (float)da[u][3];
-                d0[2] = (float)db[u][0]; d1[2] = (float)db[u][1]; d0[3] = (float)db[u][2]; d1[3] = (float)db[u][3];
-            } else {
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     s0[k] = (__bf16)x0[k];
@@ -472,6 +483,11 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
                     d0[k] = (float)da[u][k];
                     d1[k] = (float)db[u][k];
                 }
+            } else {
+                s0[0] = (__bf16)x0[0]; s0[1] = (__bf16)x1[0]; s0[2] = (__bf16)x0[1]; s0[3] = (__bf16)x1[1];
+                s1[0] = (__bf16)x0[2]; s1[1] = (__bf16)x1[2]; s1[2] = (__bf16)x0[3]; s1[3] = (__bf16)x1[3];
+                d0[0] = (float)da[u][0]; d1[0] = (float)da[u][1]; d0[1] = (float)da[u][2]; d1[1] = (float)da[u][3];
+                d0[2] = (float)db[u][0]; d1[2] = (float)db[u][1]; d0[3] = (float)db[u][2]; d1[3] = (float)db[u][3];
             }
             *reinterpret_cast<bf16x4 *>(st + off0) = s0;
             *reinterpret_cast<bf16x4 *>(st + off1) = s1;
@@ -483,7 +499,19 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
                 for (int k = 0; k < 4; ++k) {
                     x0[k] = fmaf(gdec, x0[k], d0[k]);
                     x1[k] = fmaf(gdec, x1[k], d1[k]);
-                    if (rot[k]) rotate_pair(u1, jf[k], x0[k], x1[k]);
+                }
+                if (!value) {
+                    // one slot pair: one rotation angle for all four
+                    if (rot[0]) {
+                        float sn, cs;
+                        ring_sincos(u1, jf[0], &sn, &cs);
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) apply_rot(sn, cs, x0[k], x1[k]);
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (rot[k]) rotate_pair(u1, jf[k], x0[k], x1[k]);
                 }
                 origin = reduce_clock(origin + span, (double)m, inv_m);
             }
@@ -575,6 +603,11 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     float2 *redw = lds_at<float2>(smem, opq(Ly::RED + 8 * (w * CC + l32)));
     const float2 *redr = lds_at<float2>(smem, opq(Ly::RED + 8 * l32));
 
+    // Issue order of the prologue's loads: the first chunk and the readout matrix
+    // (needed by the first stage), then the entering states, which the first
+    // chunk's products need only after its staging, scans and temporal writes.
+    Prefetch<CC> pf;
+    load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
         const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
@@ -599,8 +632,6 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     }
     double carry = 0.0, gsum = 0.0;
     float logf = 0.f;                                // carried states are exp(logf) x registers
-    Prefetch<CC> pf;
-    load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
 
     for (int c = c_begin; c < c_end; ++c) {

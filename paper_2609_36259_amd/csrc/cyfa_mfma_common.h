@@ -146,15 +146,21 @@ __host__ __device__ __forceinline__ int internal_to_paper(int i, int m) {
     return -1;
 }
 
-// Offsets of element (i, c) of a segment state in the accumulator-dump layout.
+// Segment states are stored in the "dump" layout of the fused kernel's
+// accumulators, lane-major: block (w, x) of a state (wave w's accumulator x) holds
+// 64 lanes x 16 registers, each lane's 16 registers consecutive, so that a lane
+// moves its part of a block with two 16-byte (bf16) or four (fp32) accesses.
+__host__ __device__ __forceinline__ constexpr int dump_off(int w, int x, int lane, int v) {
+    return ((w * 4 + x) * 64 + lane) * 16 + v;
+}
+// Offsets of element (i, c) of a segment state in that layout.
 // Key state: wave w = i / 32 owns columns i of Kbar^T (rows d = c), blocks db = c / 32.
 __host__ __device__ __forceinline__ int dump_index_K(int i, int c) {
     const int w = i >> 5, lane_lo = i & 31;
     const int db = c >> 5, cr = c & 31;
     const int h = (cr >> 2) & 1;
     const int v = ((cr >> 3) << 2) | (cr & 3);
-    const int lane = lane_lo + 32 * h;
-    return ((w * 4 + db) * 16 + v) * 64 + lane;
+    return dump_off(w, db, lane_lo + 32 * h, v);
 }
 // Value state: wave w = c / 32 owns columns c of Vbar (rows i), blocks ib = i / 32.
 __host__ __device__ __forceinline__ int dump_index_V(int i, int c) {
@@ -162,8 +168,7 @@ __host__ __device__ __forceinline__ int dump_index_V(int i, int c) {
     const int ib = i >> 5, ir = i & 31;
     const int h = (ir >> 2) & 1;
     const int v = ((ir >> 3) << 2) | (ir & 3);
-    const int lane = lane_lo + 32 * h;
-    return 128 * 128 + ((w * 4 + ib) * 16 + v) * 64 + lane;
+    return 128 * 128 + dump_off(w, ib, lane_lo + 32 * h, v);
 }
 
 // Value of lane l ^ 1 (DPP quad permutation [1,0,3,2]).

@@ -37,7 +37,7 @@ M_ACTIVE = 127
 # unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
 TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 118403 * 2 * 1024 + 65536 * 1024,
            "fetch_kib": 118403, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
-           "sources_sha256": "2b9a4345849edb5fa20e8927836fc543be82270965ff22d15f29d72cd904ddc4"}
+           "sources_sha256": "590d035b4f641a4639de5e832bc150d0d63ab9b88e5d896d52f314a1a71a2e13"}
 TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h",
                    "cyfa_prep.h")
 

@@ -27,10 +27,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     constexpr int VIT = kStoreRows * VQ / kThreads;  // float4 per thread (value state)
     constexpr int KROWS_PER_IT = kThreads / KQ;
     constexpr int VROWS_PER_IT = kThreads / VQ;
+    constexpr int MQ = kStoreRows / 4;               // float4 per readout-matrix row
+    constexpr int MIT = kStoreRows * MQ / kThreads;  // readout-matrix rows per thread
 
     __shared__ float qs[DK], ks[DK], vs[DV];
     __shared__ float a_s[kStoreRows], op[kStoreRows], xs[kStoreRows], ws[kStoreRows];
-    __shared__ float yp[2][kStoreRows];
+    __shared__ float zpart[kStoreRows][MQ + 1];
+    __shared__ float4 ypart[kThreads / MQ][MQ];
     __shared__ float2 cs[64];
     __shared__ float4 opart[kThreads / 64][VQ];
 
@@ -43,6 +46,23 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     const Tin *q = static_cast<const Tin *>(p.q);
     const Tin *k = static_cast<const Tin *>(p.k);
     const Tin *v = static_cast<const Tin *>(p.v);
+
+    // Both state streams are issued first (rows >= m are never touched): the
+    // value state arrives while the key state is updated and the readout runs.
+    float4 *K4 = reinterpret_cast<float4 *>(p.K + (size_t)nh * kStoreRows * DK);
+    float4 *V4 = reinterpret_cast<float4 *>(p.V + (size_t)nh * kStoreRows * DV);
+    const int ck = tid % KQ, cv = tid % VQ;
+    float4 kreg[KIT], vreg[VIT];
+#pragma unroll
+    for (int it = 0; it < KIT; ++it) {
+        const int row = it * KROWS_PER_IT + tid / KQ;
+        kreg[it] = row < m ? K4[(size_t)row * KQ + ck] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+        const int row = it * VROWS_PER_IT + tid / VQ;
+        vreg[it] = row < m ? V4[(size_t)row * VQ + cv] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
 
     const float alpha = p.log_alpha ? __expf(p.log_alpha[nh]) : 1.f;
     const float beta = p.beta ? p.beta[nh] : 1.f;
@@ -75,49 +95,43 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
 
     // ---- key state: update in place and form o' = Kbar q
     {
-        float4 *K4 = reinterpret_cast<float4 *>(p.K + (size_t)nh * kStoreRows * DK);
-        const int c4 = tid % KQ;
-        const float4 q4 = make_float4(qs[4 * c4], qs[4 * c4 + 1], qs[4 * c4 + 2], qs[4 * c4 + 3]);
-        const float4 k4 = make_float4(ks[4 * c4], ks[4 * c4 + 1], ks[4 * c4 + 2], ks[4 * c4 + 3]);
+        const float4 q4 = make_float4(qs[4 * ck], qs[4 * ck + 1], qs[4 * ck + 2], qs[4 * ck + 3]);
+        const float4 k4 = make_float4(ks[4 * ck], ks[4 * ck + 1], ks[4 * ck + 2], ks[4 * ck + 3]);
 #pragma unroll
         for (int it = 0; it < KIT; ++it) {
             const int row = it * KROWS_PER_IT + tid / KQ;
             float part = 0.f;
             if (row < m) {
-                float4 x = K4[(size_t)row * KQ + c4];
+                float4 x = kreg[it];
                 const float ar = a_s[row];
                 x.x = fmaf(alpha, x.x, ar * k4.x);
                 x.y = fmaf(alpha, x.y, ar * k4.y);
                 x.z = fmaf(alpha, x.z, ar * k4.z);
                 x.w = fmaf(alpha, x.w, ar * k4.w);
-                K4[(size_t)row * KQ + c4] = x;
+                K4[(size_t)row * KQ + ck] = x;
                 part = x.x * q4.x + x.y * q4.y + x.z * q4.z + x.w * q4.w;
             }
 #pragma unroll
             for (int off = 1; off < KQ; off <<= 1) part += __shfl_xor(part, off);
-            if (c4 == 0) op[row] = row < m ? part : 0.f;
+            if (ck == 0) op[row] = row < m ? part : 0.f;
         }
     }
     // ---- value state: update in place, keep the new values for the readout
-    float4 vreg[VIT];
     {
-        float4 *V4 = reinterpret_cast<float4 *>(p.V + (size_t)nh * kStoreRows * DV);
-        const int c4 = tid % VQ;
-        const float4 v4 = make_float4(vs[4 * c4], vs[4 * c4 + 1], vs[4 * c4 + 2], vs[4 * c4 + 3]);
+        const float4 v4 = make_float4(vs[4 * cv], vs[4 * cv + 1], vs[4 * cv + 2], vs[4 * cv + 3]);
 #pragma unroll
         for (int it = 0; it < VIT; ++it) {
             const int row = it * VROWS_PER_IT + tid / VQ;
-            float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
             if (row < m) {
-                x = V4[(size_t)row * VQ + c4];
+                float4 x = vreg[it];
                 const float ar = a_s[row];
                 x.x = fmaf(alpha, x.x, ar * v4.x);
                 x.y = fmaf(alpha, x.y, ar * v4.y);
                 x.z = fmaf(alpha, x.z, ar * v4.z);
                 x.w = fmaf(alpha, x.w, ar * v4.w);
-                V4[(size_t)row * VQ + c4] = x;
+                V4[(size_t)row * VQ + cv] = x;
+                vreg[it] = x;
             }
-            vreg[it] = x;
         }
     }
     __syncthreads();
@@ -135,26 +149,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
         }
         xs[i] = x;
     }
-    __syncthreads();
-    const float *Mh = Mg + (size_t)h * kStoreRows * kStoreRows;
-    {
-        // z_i = sum_j M_ij x_j: two threads per slot row, 64 columns each
-        const int i = tid >> 1, half = tid & 1;
-        float acc = 0.f;
-        if (i < m) {
-            const float4 *row4 = reinterpret_cast<const float4 *>(Mh + (size_t)i * kStoreRows) + half * 16;
+    // Thread (column quad cm = tid % 32, row group g = tid / 32) holds rows
+    // MIT g .. MIT g + MIT-1, columns 4 cm .. 4 cm + 3 of M (16-byte loads, a
+    // wave reading two whole rows per load); the same registers serve z = M x
+    // and y = M^T w.
+    const int cm = tid % MQ, g = tid / MQ;
+    const float4 *M4 = reinterpret_cast<const float4 *>(Mg + (size_t)h * kStoreRows * kStoreRows);
+    float4 mreg[MIT];
 #pragma unroll
-            for (int c = 0; c < 16; ++c) {
-                const float4 mm = row4[c];
-                const int j = half * 64 + 4 * c;
-                acc = fmaf(mm.x, xs[j], acc);
-                acc = fmaf(mm.y, xs[j + 1], acc);
-                acc = fmaf(mm.z, xs[j + 2], acc);
-                acc = fmaf(mm.w, xs[j + 3], acc);
-            }
+    for (int r = 0; r < MIT; ++r) mreg[r] = M4[(size_t)(MIT * g + r) * MQ + cm];
+    __syncthreads();
+    {
+        const float4 x4 = make_float4(xs[4 * cm], xs[4 * cm + 1], xs[4 * cm + 2], xs[4 * cm + 3]);
+#pragma unroll
+        for (int r = 0; r < MIT; ++r) {
+            const float4 mm = mreg[r];
+            zpart[MIT * g + r][cm] = mm.x * x4.x + mm.y * x4.y + mm.z * x4.z + mm.w * x4.w;
         }
-        acc += __shfl_xor(acc, 1);
-        if (half == 0) ws[i] = i < m ? acc : -INFINITY;
+    }
+    __syncthreads();
+    if (tid < kStoreRows) {
+        float z = 0.f;
+#pragma unroll 8
+        for (int c = 0; c < MQ; ++c) z += zpart[tid][c];
+        ws[tid] = tid < m ? z : -INFINITY;
     }
     __syncthreads();
     if (wave == 0) {
@@ -177,31 +195,43 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     }
     __syncthreads();
     {
-        // y_j = sum_i M_ij w_i: thread (j, half) sums 64 slot rows
-        const int j = tid & (kStoreRows - 1), half = tid >> 7;
-        float acc = 0.f;
-        for (int i = half * 64; i < half * 64 + 64 && i < m; ++i) acc = fmaf(Mh[(size_t)i * kStoreRows + j], ws[i], acc);
-        yp[half][j] = acc;
+        // y = M^T w: this thread's rows, then the row groups summed
+        float4 y4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int r = 0; r < MIT; ++r) {
+            const float wr = ws[MIT * g + r];
+            y4.x = fmaf(mreg[r].x, wr, y4.x);
+            y4.y = fmaf(mreg[r].y, wr, y4.y);
+            y4.z = fmaf(mreg[r].z, wr, y4.z);
+            y4.w = fmaf(mreg[r].w, wr, y4.w);
+        }
+        ypart[g][cm] = y4;
     }
     __syncthreads();
     if (tid < kStoreRows) {
+        float y[2] = {0.f, 0.f};
         const int i = tid;
+        // the rotation pairs paper columns (2jj+1, 2jj+2); column 0 is DC
+        const int c0 = i == 0 ? 0 : (i < m ? 2 * ((i - 1) >> 1) + 1 : 0);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int c = c0 + e;
+            const float *yp4 = reinterpret_cast<const float *>(&ypart[0][0]) + c;
+#pragma unroll
+            for (int gg = 0; gg < kThreads / MQ; ++gg) y[e] += yp4[gg * MQ * 4];
+        }
         float x = 0.f;
         if (i == 0) {
-            x = yp[0][0] + yp[1][0];
+            x = y[0];
         } else if (i < m) {
-            const int jj = (i - 1) >> 1;
-            const float2 t = cs[jj];
-            const float a0 = yp[0][2 * jj + 1] + yp[1][2 * jj + 1];
-            const float a1 = yp[0][2 * jj + 2] + yp[1][2 * jj + 2];
-            x = (i & 1) ? (t.x * a0 + t.y * a1) : (-t.y * a0 + t.x * a1);
+            const float2 t = cs[(i - 1) >> 1];
+            x = (i & 1) ? (t.x * y[0] + t.y * y[1]) : (-t.y * y[0] + t.x * y[1]);
         }
         xs[i] = x;   // o''
     }
     __syncthreads();
     // ---- o = Vbar^T o''
     {
-        const int c4 = tid % VQ;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int it = 0; it < VIT; ++it) {
@@ -212,7 +242,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
             acc.z = fmaf(vreg[it].z, w, acc.z);
             acc.w = fmaf(vreg[it].w, w, acc.w);
         }
-        // threads sharing c4 within a wave: lanes differing in the bits above log2(VQ)
+        // threads sharing cv within a wave: lanes differing in the bits above log2(VQ)
 #pragma unroll
         for (int off = VQ; off < 64; off <<= 1) {
             acc.x += __shfl_xor(acc.x, off);
@@ -220,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
             acc.z += __shfl_xor(acc.z, off);
             acc.w += __shfl_xor(acc.w, off);
         }
-        if (lane < VQ) opart[wave][c4] = acc;
+        if (lane < VQ) opart[wave][cv] = acc;
     }
     __syncthreads();
     if (tid < DV) {

@@ -35,6 +35,10 @@ using namespace mfma;
 
 namespace {
 
+// rows of the readout matrix per workgroup when extra blocks of the pre-pass or the
+// scan form it
+constexpr int kPrepRows = 32;
+
 // ---- LDS maps (bytes) ---------------------------------------------------------
 // Fused kernel (32-token chunks).  Tiles read through the transpose read (K, V,
 // A and the readout matrix M) are swizzled rows of 128; Q (then X, W) and O''
@@ -197,6 +201,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     constexpr int RPP = NT / 16;                       // tile rows per pass
     constexpr int SCB = 4 * STILE;                     // per-wave (phase, amplitude) rows
     __shared__ __attribute__((aligned(256))) char smem[SCB + 4 * 64 * 8 + 4 * 8];
+    static_assert(SCB + 4 * 64 * 8 + 4 * 8 >= prep_lds_bytes(kPrepRows), "readout-matrix blocks fit");
     const FwdParams &p = a.p;
     const int Pm1 = a.P - 1;
     const int bh = blockIdx.x / Pm1, seg = blockIdx.x % Pm1;
@@ -213,8 +218,8 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
         const int nseg = p.B * p.H * Pm1;
         if ((int)blockIdx.x >= nseg) {
             const int q = (int)blockIdx.x - nseg;
-            readout_prep_rows32(m, p.R, const_cast<__bf16 *>(a.Mz), mz_scale, q / (kStoreRows / kPrepRows32),
-                                q % (kStoreRows / kPrepRows32), tid, smem);
+            readout_prep_rows<kPrepRows>(m, p.R, nullptr, const_cast<__bf16 *>(a.Mz), mz_scale,
+                                          q / (kStoreRows / kPrepRows), q % (kStoreRows / kPrepRows), tid, smem);
             return;
         }
     }
@@ -519,16 +524,18 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
     }
 }
 
-// The segment scan and the readout preparation (needed only by the fused kernel)
-// in one launch: blocks [0, nscan) scan, the rest form M_h = R_h Phi.
+// The segment scan and, when no pre-pass formed it, the readout matrix (needed
+// only by the fused kernel) in one launch: blocks [0, nscan) scan, the rest form
+// 32 rows of M_h = R_h Phi each.
 __global__ __launch_bounds__(NT) void scan_prep_kernel(MfmaArgs a, int nscan, float mz_scale) {
+    __shared__ __attribute__((aligned(16))) char lds[prep_lds_bytes(kPrepRows)];
     const int b = blockIdx.x;
     if (b < nscan) {
         segment_scan(a, b / kScanBlocks, b % kScanBlocks, threadIdx.x);
     } else {
         const int q = b - nscan;
-        readout_prep_block(a.p.m, a.p.R, nullptr, const_cast<__bf16 *>(a.Mz), mz_scale,
-                           q / (kStoreRows / kPrepRows), q % (kStoreRows / kPrepRows), threadIdx.x);
+        readout_prep_rows<kPrepRows>(a.p.m, a.p.R, nullptr, const_cast<__bf16 *>(a.Mz), mz_scale,
+                                     q / (kStoreRows / kPrepRows), q % (kStoreRows / kPrepRows), threadIdx.x, lds);
     }
 }
 
@@ -991,7 +998,7 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
         // costs) whenever its length is a whole number of them.  Every segment but
         // the last is full, and the last one is not pre-passed.  Extra blocks of
         // the same launch form the bf16 readout matrix, 32 rows each.
-        const int nblk = BH * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows32);
+        const int nblk = BH * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows);
         if (CC == 32 && a.cps % 2 == 0) {
             MfmaArgs a64 = a;
             a64.chunk = 64;

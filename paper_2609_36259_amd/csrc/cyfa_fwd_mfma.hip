@@ -494,8 +494,10 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
                 d0[0] = (float)da[u][0]; d1[0] = (float)da[u][1]; d0[1] = (float)da[u][2]; d1[1] = (float)da[u][3];
                 d0[2] = (float)db[u][0]; d1[2] = (float)db[u][1]; d0[3] = (float)db[u][2]; d1[3] = (float)db[u][3];
             }
-            *reinterpret_cast<bf16x4 *>(st + off0) = s0;
-            *reinterpret_cast<bf16x4 *>(st + off1) = s1;
+            if (q > 0 || !a.zero_init) {
+                *reinterpret_cast<bf16x4 *>(st + off0) = s0;
+                *reinterpret_cast<bf16x4 *>(st + off1) = s1;
+            }
             if (q < a.P - 1) {
                 const float gdec = __expf((float)a.seg_gsum[slot]);
                 const double span = a.seg_span[slot];    // already reduced to [0, m)
@@ -628,7 +630,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     }
     f32x16 kacc[4], vacc[4];
     const __bf16 *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
-    if (a.has_init) {
+    if (a.has_init && !(seg == 0 && a.zero_init)) {
         load_state(slot_state, w, lane, kacc, vacc);
     } else {
 #pragma unroll
@@ -1076,6 +1078,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.final_lam = reinterpret_cast<double *>(base + L.flam);
     a.want_final = (p.K_out || p.V_out || p.clock_out) ? 1 : 0;
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
+    a.zero_init = (p.K0 || p.V0) ? 0 : 1;
     const int BH = p.B * p.H;
 
     hipError_t e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);

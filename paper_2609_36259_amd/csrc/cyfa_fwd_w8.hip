@@ -214,7 +214,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
     }
     f32x4 kacc[8], vacc[8];
     const __bf16 *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kStateFloats;
-    if (a.has_init) {
+    if (a.has_init && !(seg == 0 && a.zero_init)) {
         load_state16(slot_state, col, g4, kacc, vacc);
     } else {
 #pragma unroll

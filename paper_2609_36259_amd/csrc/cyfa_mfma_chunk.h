@@ -22,6 +22,8 @@ struct MfmaArgs {
     double *seg_origin;  // [B*H*P] absolute clock at each segment start (reduced)
     double *final_lam;   // [B*H] local clock after the last segment (reduced)
     int has_init;        // segment-entry states are read from seg_state
+    int zero_init;       // no initial state: the first segment starts from zero (its entry
+                         // state is neither written by the scan nor read)
     int want_final;      // last segment dumps its final state into fin_state
 };
 

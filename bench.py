@@ -37,7 +37,7 @@ M_ACTIVE = 127
 # unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
 TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 116370 * 2 * 1024 + 65536 * 1024,
            "fetch_kib": 116370, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
-           "sources_sha256": "119e049773f7c4a288d2a5788a67b3fe9a35e3b0363c06560c539b4f8986c999"}
+           "sources_sha256": "873451c5239b30dfd753015e629e3903174df82a3e6b5e069a9970ed5714be4c"}
 TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h",
                    "cyfa_prep.h")
 

@@ -98,9 +98,6 @@ __device__ __forceinline__ int tr_off(int stride, int lane) {
     const int s = lane & 15, g = lane >> 4;
     return (8 * (g >> 1) + (s >> 2)) * stride + 16 * (g & 1) + 4 * (s & 3);
 }
-__device__ __forceinline__ const __bf16 *tr_base(const __bf16 *tile, int stride, int lane) {
-    return tile + tr_off(stride, lane);
-}
 __device__ __forceinline__ bf16x8 lds8_tr(const __bf16 *p, int stride) {
     const bf16x4 lo = lds4_tr(p);
     const bf16x4 hi = lds4_tr(p + 4 * stride);
@@ -175,17 +172,6 @@ __host__ __device__ __forceinline__ int dump_index_V(int i, int c) {
 __device__ __forceinline__ float swap_pair(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
 }
-// Value of lane l ^ 2 (DPP quad permutation [2,3,0,1]).
-__device__ __forceinline__ float swap_halves4(float x) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
-}
-
-// Value of lane l ^ 7 within each group of 8 (DPP row_half_mirror); after the
-// two swaps above have made each quad uniform, this fetches the other quad.
-__device__ __forceinline__ float swap_quads8(float x) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
-}
-
 // ---- chunk-local prefix sums on one wave (lane = token row) --------------
 // DPP lane moves (no lane-address registers): row_shr:n within rows of 16 lanes
 // (sources outside the row read 0), then row_bcast:15 / row_bcast:31 carry the

@@ -17,7 +17,7 @@ namespace cyfa {
 
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;   // eight waves: 8 + 8 state float4 and 8 readout-matrix rows per thread
 
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const float *__restrict__ Mg) {

@@ -160,6 +160,24 @@ def forward_bench(args, torch, cyfa, w):
         hip.destroy(b)
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     kernel_ms = sum(kms) / len(kms)
+    # Cold steps: a 512 MiB write before each one evicts the 256 MB last-level
+    # cache and the L2s, so every input comes from HBM; events on the library's
+    # (torch's current) stream bracket the step alone.
+    cold_ms = None
+    if args.cold_steps > 0:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        pairs = []
+        for i in range(args.cold_steps):
+            flush.fill_(i & 0xFF)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            step()
+            e1.record()
+            pairs.append((e0, e1))
+        torch.cuda.synchronize()
+        cold = sorted(a.elapsed_time(b) for a, b in pairs)
+        cold_ms = cold[len(cold) // 2]
+        del flush
     in_bytes = 2 if w.dtype == "bf16" else 4
     chunk = args.chunk or cyfa.DEFAULT_CHUNK[cyfa.selected_kernel(desc)]
     flops = alg_flops_per_token_head(w.dk, w.dv, w.m, chunk) * w.B * w.T * w.H
@@ -168,7 +186,7 @@ def forward_bench(args, torch, cyfa, w):
     del t, ws, o
     torch.cuda.empty_cache()
     return dict(ms_per_step=ms_per_step, kernel_ms=kernel_ms, kernel_ms_min=min(kms),
-                flops=flops, bytes=nbytes_alg, kernel=plan_kernel, chunk=chunk)
+                flops=flops, bytes=nbytes_alg, kernel=plan_kernel, chunk=chunk, cold_ms=cold_ms)
 
 
 def decode_bench(args, torch, cyfa):
@@ -272,6 +290,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=20,
+                    help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (for scaling "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -333,6 +353,10 @@ def main():
                  "frac": tfl / PEAK_BF16_TFLOPS, "alg_flops_per_launch": fb["flops"]},
         "hbm": {"achieved": hbm, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": hbm / PEAK_HBM_GBS},
     }
+    if fb["cold_ms"] is not None:
+        line["cold"] = {"ms_per_step": fb["cold_ms"], "value": tokens / (fb["cold_ms"] * 1e-3),
+                        "unit": "tokens/s", "steps": args.cold_steps,
+                        "note": "median of single steps, each after a 512 MiB write (caches evicted)"}
     if not args.no_decode:
         line["decode"] = decode_bench(args, torch, cyfa)
     if not args.no_cpu_baseline:

@@ -37,7 +37,7 @@ M_ACTIVE = 127
 # unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
 TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 116370 * 2 * 1024 + 65536 * 1024,
            "fetch_kib": 116370, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
-           "sources_sha256": "873451c5239b30dfd753015e629e3903174df82a3e6b5e069a9970ed5714be4c"}
+           "sources_sha256": "8a415cf4b4428fe3ec44a82ffa874e02e30c6c106d834c88dcd259e191bc838c"}
 TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h",
                    "cyfa_prep.h")
 

@@ -9,8 +9,9 @@
 //   z = scale M U(lambda) o',  w = softmax(z),  o'' = U(-lambda) M^T w,  M = R Phi
 //   o = Vbar^T o''
 // The step reads and writes each state once; it is bound by HBM bandwidth.
-// Each workgroup streams its two 128 x d float states with 16-byte loads laid
-// out so that consecutive lanes touch consecutive addresses.
+// Each workgroup issues both of its 128 x d float states' loads at its start
+// (16-byte loads, consecutive lanes on consecutive addresses), so the value
+// state arrives while the key state is updated and the readout runs.
 #include "cyfa_internal.h"
 
 namespace cyfa {

@@ -6,6 +6,8 @@
 //      the carried states, DeltaS_p = sum_t (decay to segment end) a_t [k_t | v_t]^T,
 //      with the clock origin at the segment start, plus the segment's clock span
 //      and log-decay total.  App. B's state recurrence run from a zero state.
+//      Extra blocks of the same launch form the bf16 readout matrix
+//      M_h = R_h Phi (times scale log2 e) for step 3.
 //   2. scan_prep_kernel  (b, h): the states entering every segment,
 //      S'_{p+1} = U(span_p) (exp(gsum_p) S'_p + DeltaS_p), each expressed with its
 //      own segment-start clock origin.  Moving the origin rotates an
@@ -13,9 +15,8 @@
 //      (App. A.4, Prop. 6), which is what makes the segments independent.
 //      The recurrence runs in fp32; the contributions and entering states are
 //      stored in bf16, the precision in which the chunk products consume them.
-//      Extra blocks of the same launch form the bf16 readout matrix
-//      M_h = R_h Phi (times scale log2 e) for step 3.  (Without a scan the
-//      readout preparation is launched on its own.)
+//      (Without a pre-pass, extra blocks of this launch form the readout matrix,
+//      or, without a scan either, its own launch does.)
 //   3. chunk_forward_kernel  (b, h, p): the fused forward of App. B over the
 //      segment's chunks: clock/log-decay prefix sums, temporal write matrix
 //      A (Eq. app-temporal-writes), key pass (Eq. app-cyfa-key-chunk), token-wise

@@ -76,7 +76,7 @@ typedef enum {
  * Forward problem descriptor.
  *   B, T, H      batch, tokens, heads (B, H >= 1; T >= 0; T = 0 is a no-op that
  *                still writes the final state and clock when requested)
- *   d_k, d_v     head dims: 64 or 128 each (the matrix-core kernel: 128 only)
+ *   d_k, d_v     head dims: 64, 128 or 256 each (the matrix-core kernel: 128 only)
  *   m            active slots, odd, 3..127
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
  *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 32).
@@ -143,7 +143,7 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc,
 
 /*
  * Single-token decode descriptor: N independent streams, H heads each.
- *   d_k, d_v 64 or 128; m odd 3..127; dtype of q, k, v, o.
+ *   d_k, d_v 64, 128 or 256; m odd 3..127; dtype of q, k, v, o.
  */
 typedef struct {
     int32_t N, H, d_k, d_v;

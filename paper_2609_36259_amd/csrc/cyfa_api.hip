@@ -47,7 +47,7 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 constexpr size_t kWsAlign = 256;
 size_t round_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
-bool head_dim_ok(int d) { return d == 64 || d == 128; }
+bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
 
 struct FwdPlan {
     bool mfma;
@@ -66,7 +66,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     if (d->d_k <= 0 || d->d_v <= 0)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
     if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
-        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64 or 128 (got d_k=%d d_v=%d)",
+        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64, 128 or 256 (got d_k=%d d_v=%d)",
                     d->d_k, d->d_v);
     if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
         return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
@@ -125,7 +125,7 @@ cyfa_status check_dec(const cyfa_dec_desc *d) {
     if ((double)d->N * d->H > 2.0e9) return fail(CYFA_ERR_INVALID_ARGUMENT, "too many streams");
     if (d->d_k <= 0 || d->d_v <= 0) return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
     if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
-        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64 or 128");
+        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64, 128 or 256");
     if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
         return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
                                                                : CYFA_ERR_INVALID_ARGUMENT,

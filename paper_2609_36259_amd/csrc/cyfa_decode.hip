@@ -277,13 +277,19 @@ hipError_t launch_typed(const DecParams &p, const float *M, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int DK>
+hipError_t launch_dv(const DecParams &p, const float *M, hipStream_t s) {
+    if (p.dv == 64) return launch_typed<DK, 64>(p, M, s);
+    if (p.dv == 128) return launch_typed<DK, 128>(p, M, s);
+    return launch_typed<DK, 256>(p, M, s);
+}
+
 }  // namespace
 
 hipError_t launch_decode(const DecParams &p, const float *M, hipStream_t s) {
-    if (p.dk == 128 && p.dv == 128) return launch_typed<128, 128>(p, M, s);
-    if (p.dk == 64 && p.dv == 64) return launch_typed<64, 64>(p, M, s);
-    if (p.dk == 128 && p.dv == 64) return launch_typed<128, 64>(p, M, s);
-    return launch_typed<64, 128>(p, M, s);
+    if (p.dk == 64) return launch_dv<64>(p, M, s);
+    if (p.dk == 128) return launch_dv<128>(p, M, s);
+    return launch_dv<256>(p, M, s);
 }
 
 }  // namespace cyfa

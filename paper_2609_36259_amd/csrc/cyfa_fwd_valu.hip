@@ -20,7 +20,10 @@ namespace cyfa {
 namespace {
 
 constexpr int kValuChunkMax = 16;
-constexpr int kThreads = 256;
+// threads per workgroup: 256, or 512 when a head dimension is 256 (each thread
+// then holds at most 64 + 64 state values; with both dimensions at 256 some of
+// the kernel's temporaries spill, which this correctness-first fp32 path accepts)
+__host__ __device__ constexpr int valu_threads(int dk, int dv) { return (dk > 128 || dv > 128) ? 512 : 256; }
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
@@ -34,9 +37,11 @@ __device__ __forceinline__ float wave_sum(float x) {
 }
 
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(kThreads) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
+__global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
+    constexpr int kThreads = valu_threads(DK, DV);
     constexpr int CM = kValuChunkMax;
-    constexpr int KH = DK / 2;             // key-state columns per thread
+    constexpr int KP = kThreads / kStoreRows;  // threads sharing a key-state row
+    constexpr int KH = DK / KP;            // key-state columns per thread
     constexpr int VP = kThreads / DV;      // threads sharing a value-state column
     constexpr int VR = kStoreRows / VP;    // value-state rows per thread
 
@@ -68,7 +73,7 @@ __global__ __launch_bounds__(kThreads) void fwd_valu_kernel(FwdParams p, const f
     Tin *o = static_cast<Tin *>(p.o);
 
     // state ownership
-    const int ki = tid >> 1, kh = tid & 1;            // Kbar row ki, columns [kh*KH, kh*KH+KH)
+    const int ki = tid / KP, kh = tid % KP;           // Kbar row ki, columns [kh*KH, kh*KH+KH)
     const int vc = tid / VP, vpart = tid % VP;        // Vbar column vc, rows [vpart*VR, +VR)
     float kst[KH];
     float vst[VR];
@@ -156,7 +161,8 @@ __global__ __launch_bounds__(kThreads) void fwd_valu_kernel(FwdParams p, const f
             float part = 0.f;
 #pragma unroll
             for (int c = 0; c < KH; ++c) part = fmaf(Qs[r][kh * KH + c], kst[c], part);
-            part += __shfl_xor(part, 1);
+#pragma unroll
+            for (int off = 1; off < KP; off <<= 1) part += __shfl_xor(part, off);
             if (kh == 0) Ob[r][ki] = __expf(G_s[r]) * part;
         }
         __syncthreads();
@@ -299,7 +305,7 @@ __global__ __launch_bounds__(kThreads) void fwd_valu_kernel(FwdParams p, const f
 
 template <int DK, int DV>
 hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
-    const dim3 grid(p.B * p.H), block(kThreads);
+    const dim3 grid(p.B * p.H), block(valu_threads(DK, DV));
     if (p.dtype == 0)
         hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, float>), grid, block, 0, s, p, M);
     else
@@ -311,11 +317,17 @@ hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
 
 int valu_chunk_max() { return kValuChunkMax; }
 
+template <int DK>
+hipError_t launch_dv(const FwdParams &p, const float *M, hipStream_t s) {
+    if (p.dv == 64) return launch_typed<DK, 64>(p, M, s);
+    if (p.dv == 128) return launch_typed<DK, 128>(p, M, s);
+    return launch_typed<DK, 256>(p, M, s);
+}
+
 hipError_t launch_fwd_valu(const FwdParams &p, const float *M, hipStream_t s) {
-    if (p.dk == 128 && p.dv == 128) return launch_typed<128, 128>(p, M, s);
-    if (p.dk == 64 && p.dv == 64) return launch_typed<64, 64>(p, M, s);
-    if (p.dk == 128 && p.dv == 64) return launch_typed<128, 64>(p, M, s);
-    return launch_typed<64, 128>(p, M, s);
+    if (p.dk == 64) return launch_dv<64>(p, M, s);
+    if (p.dk == 128) return launch_dv<128>(p, M, s);
+    return launch_dv<256>(p, M, s);
 }
 
 }  // namespace cyfa

@@ -49,7 +49,7 @@ def test_tiny_f32_workload_full_parity():
 
 
 @pytest.mark.parametrize("variant", ["no_beta_no_R", "peaky", "small_m", "ragged_chunk8",
-                                     "d128_f32", "mixed_dims"])
+                                     "d128_f32", "mixed_dims", "d256_f32", "mixed_256"])
 def test_f32_variants(variant):
     kw = {}
     dk = dv = 64
@@ -60,6 +60,11 @@ def test_f32_variants(variant):
         T, kw = 77, {"chunk": 8}
     if variant == "d128_f32":
         dk = dv = 128
+    if variant == "d256_f32":          # the paper's head size (512-thread workgroups)
+        dk = dv = 256
+        T = 70
+    if variant == "mixed_256":
+        dk, dv, T = 256, 64, 70
     x = make_forward_inputs(B, T, H, dk, dv, seed=21, dtype="f32", m=m,
                             with_beta=variant != "no_beta_no_R", with_R=variant != "no_beta_no_R")
     if variant == "mixed_dims":
@@ -70,6 +75,13 @@ def test_f32_variants(variant):
     t = upload(x)
     res = _fwd(x, t, return_state=True, return_logits=True, **kw)
     _check_full(x, res, TOL_F32)
+
+
+def test_bf16_valu_kernel_d256():
+    x = make_forward_inputs(1, 45, 2, 256, 256, seed=24, dtype="bf16")
+    t = upload(x)
+    res = _fwd(x, t, return_state=True, return_logits=True)
+    _check_full(x, res, TOL_BF16)
 
 
 def test_bf16_valu_kernel():
@@ -167,7 +179,7 @@ def _decode_case(N, H, d, prefix, steps, seed, dtype="f32", with_logits=True):
     return e_o, e_z, e_K, e_c
 
 
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [64, 128, 256])
 def test_decode_steps_match_oracle_f32(d):
     e_o, e_z, e_K, e_c = _decode_case(3, 2, d, prefix=33, steps=6, seed=30 + d)
     assert e_o <= TOL_F32 and e_z <= TOL_F32 and e_K <= TOL_F32 and e_c <= 1e-9

@@ -142,6 +142,30 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc,
                          void *stream);
 
 /*
+ * Same as cyfa_forward for a padded batch of sequences of different lengths.
+ *   lens   [B] int32 device array: sequence b has lens[b] tokens (values are
+ *          clamped to [0, T]); NULL means every sequence has T tokens.
+ * Token t >= lens[b] of sequence b is treated like a position past the end of
+ * the sequence: it writes nothing into the states, decays nothing and does not
+ * advance the clock (App. B's chunk form with those rows masked), so K_out,
+ * V_out and clock_out are the states after lens[b] tokens, and rows t >= lens[b]
+ * of o (and of logits_out) are not written.  Every other argument, the
+ * workspace size (cyfa_forward_workspace_size) and the errors are those of
+ * cyfa_forward; lens must be 4-byte aligned.
+ */
+cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc,
+                              const void *q, const void *k, const void *v,
+                              const float *delta, const float *log_alpha, const float *beta,
+                              const float *R,
+                              const int32_t *lens,
+                              const float *K0, const float *V0, const double *clock0,
+                              void *o,
+                              float *K_out, float *V_out, double *clock_out,
+                              float *logits_out,
+                              void *workspace, size_t workspace_bytes,
+                              void *stream);
+
+/*
  * Single-token decode descriptor: N independent streams, H heads each.
  *   d_k, d_v 64, 128 or 256; m odd 3..127; dtype of q, k, v, o.
  */

@@ -155,6 +155,16 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
                          void *o, float *K_out, float *V_out, double *clock_out,
                          float *logits_out, void *workspace, size_t workspace_bytes,
                          void *stream) {
+    return cyfa_forward_lens(desc, q, k, v, delta, log_alpha, beta, R, nullptr, K0, V0, clock0, o, K_out,
+                             V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
+}
+
+cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                              const float *delta, const float *log_alpha, const float *beta,
+                              const float *R, const int32_t *lens, const float *K0, const float *V0,
+                              const double *clock0, void *o, float *K_out, float *V_out,
+                              double *clock_out, float *logits_out, void *workspace,
+                              size_t workspace_bytes, void *stream) {
     FwdPlan plan;
     cyfa_status st = plan_forward(desc, &plan);
     if (st != CYFA_OK) return st;
@@ -166,7 +176,7 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
     for (int i = 0; i < 8; ++i)
         if (vec[i] && !aligned(vec[i], 16))
             return fail(CYFA_ERR_INVALID_ARGUMENT, "%s must be 16-byte aligned", vec_names[i]);
-    const void *sc[] = {delta, log_alpha, beta, R, logits_out};
+    const void *sc[] = {delta, log_alpha, beta, R, logits_out, lens};
     for (const void *p : sc)
         if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
     if ((clock0 && !aligned(clock0, 8)) || (clock_out && !aligned(clock_out, 8)))
@@ -187,7 +197,7 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
     p.dtype = desc->dtype;
     p.q = q; p.k = k; p.v = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R;
     p.K0 = K0; p.V0 = V0; p.clock0 = clock0; p.o = o; p.K_out = K_out; p.V_out = V_out;
-    p.clock_out = clock_out; p.logits = logits_out;
+    p.clock_out = clock_out; p.logits = logits_out; p.lens = lens;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     char *ws = static_cast<char *>(workspace);

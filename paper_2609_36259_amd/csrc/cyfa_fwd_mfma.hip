@@ -210,10 +210,6 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5, l32 = lane & 31;
     const int m = p.m;
     const double inv_m = 1.0 / (double)m;
-    const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
-    const int t_begin = c_begin * CC, t_end = min(c_end * CC, p.T);
-    float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
-    double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
     {
         // blocks past the segments form 32 rows of the bf16 readout matrix each
         const int nseg = p.B * p.H * Pm1;
@@ -224,6 +220,11 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
             return;
         }
     }
+    const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
+    const int Tb = seq_tokens(p, b);
+    const int t_begin = c_begin * CC, t_end = min(c_end * CC, Tb);
+    float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
+    double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
 
     // this lane's write-matrix column: internal index cidx = 32w + l32 is the cosine
     // (even) or minus sine (odd, a quarter turn later) of pair j = cidx/2 + 1, or the
@@ -257,13 +258,13 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
         const char *vb = reinterpret_cast<const char *>(p.v) + base;
 #pragma unroll
         for (int it = 0; it < KIT; ++it) {
-            const bool in = t0 + (tid >> 4) + RPP * it < p.T;
+            const bool in = t0 + (tid >> 4) + RPP * it < Tb;
             pk[it] = in ? *reinterpret_cast<const uint4 *>(kb + loff + it * pass) : make_uint4(0, 0, 0, 0);
             pv[it] = in ? *reinterpret_cast<const uint4 *>(vb + loff + it * pass) : make_uint4(0, 0, 0, 0);
         }
         const int t = t0 + lane;
         const size_t si = ((size_t)b * p.T + t) * p.H + h;
-        const bool tin = lane < CC && t < p.T;
+        const bool tin = lane < CC && t < Tb;
         dl = tin ? p.delta[si] : 0.f;
         g = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
         be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
@@ -573,6 +574,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
     const int m = p.m;
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
+    const int Tb = seq_tokens(p, b);
     const int icol = 32 * w + l32;                   // this lane's slot (readout step)
     const int h4 = 4 * hl;
 
@@ -617,7 +619,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     // (needed by the first stage), then the entering states, which the first
     // chunk's products need only after its staging, scans and temporal writes.
     Prefetch<CC> pf;
-    load_chunk<CC, true>(p, b, h, c_begin * CC, tid, pf);
+    load_chunk<CC, true>(p, b, h, c_begin * CC, Tb, tid, pf);
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
         const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
@@ -646,12 +648,12 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
-        const int n = min(CC, p.T - t0);
+        const int n = min(CC, Tb - t0);          // <= 0 for chunks past the sequence
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
-        if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, tid, pf);
+        if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, Tb, tid, pf);
         // factor applied to the carried states this chunk, and whether the chunk's
         // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));

@@ -64,6 +64,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int m = p.m, C = p.chunk, T = p.T, H = p.H;
+    const int Tb = seq_tokens(p, b);                  // this sequence's tokens
     const int J = (m - 1) / 2;
     const float dc = 1.0f / sqrtf((float)m);
     const float ac = sqrtf(2.0f / (float)m);
@@ -92,8 +93,8 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
     if (tid == 0) lam_carry = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
     __syncthreads();
 
-    for (int t0 = 0; t0 < T; t0 += C) {
-        const int n = min(C, T - t0);
+    for (int t0 = 0; t0 < Tb; t0 += C) {
+        const int n = min(C, Tb - t0);
         // ---- load the chunk (rows past the end are zero: no write, no decay, no shift)
         for (int e = tid; e < C * DK; e += kThreads) {
             const int r = e / DK, c = e % DK;

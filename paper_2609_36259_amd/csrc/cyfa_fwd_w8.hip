@@ -161,6 +161,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
     const int l16 = lane & 15, g = lane >> 4, g4 = 4 * g;
     const int m = p.m;
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
+    const int Tb = seq_tokens(p, b);
     const int col = 16 * w + l16;                     // this lane's state / output column
     // U(theta) on a (cos, sin) column pair held by lanes (2k, 2k+1)
     const float sgn = (l16 & 1) ? 1.f : -1.f;
@@ -226,17 +227,17 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
     double carry = 0.0, gsum = 0.0;
     float logf = 0.f;                                 // carried states are exp(logf) x registers
     Prefetch<CK, W8> pf;
-    load_chunk<CK, true, W8>(p, b, h, c_begin * CK, tid, pf);
+    load_chunk<CK, true, W8>(p, b, h, c_begin * CK, Tb, tid, pf);
     __bf16 *o = static_cast<__bf16 *>(p.o);
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CK;
-        const int n = min(CK, p.T - t0);
+        const int n = min(CK, Tb - t0);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CK, true, W8>(s, tid, pf);
         if (w == 0) chunk_scans<CK, W8>(s, lane, m, pf, carry, gsum, logf);
         __syncthreads();
-        if (c + 1 < c_end) load_chunk<CK, true, W8>(p, b, h, t0 + CK, tid, pf);
+        if (c + 1 < c_end) load_chunk<CK, true, W8>(p, b, h, t0 + CK, Tb, tid, pf);
         build_writes<CK, true, true, W8>(s, tid, m);
         __syncthreads();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A

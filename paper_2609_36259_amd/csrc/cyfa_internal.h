@@ -24,6 +24,7 @@ struct FwdParams {
     float *K_out, *V_out;
     double *clock_out;
     float *logits;
+    const int *lens;                // [B] tokens of each sequence (clamped to [0, T]); NULL: all T
 };
 
 struct DecParams {
@@ -50,6 +51,12 @@ hipError_t launch_fwd_valu(const FwdParams &p, const float *M, hipStream_t s);
 hipError_t launch_decode(const DecParams &p, const float *M, hipStream_t s);
 
 // ---- device helpers --------------------------------------------------------
+// Tokens of sequence b: lens[b] clamped to [0, T], or T without lengths.  Tokens
+// t >= that count are treated like the tail past the end of a sequence: no
+// write, no decay, no clock shift, and their output rows are not written.
+__device__ __forceinline__ int seq_tokens(const FwdParams &p, int b) {
+    return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
+}
 __device__ __forceinline__ float load_as_float(const float *p, size_t i) { return p[i]; }
 __device__ __forceinline__ float load_as_float(const __hip_bfloat16 *p, size_t i) {
     return __bfloat162float(p[i]);

@@ -74,8 +74,9 @@ struct Prefetch {
     float g, dl, be;
 };
 
+// Tb: tokens of this sequence (rows at or past it read as zero, scalars as 0).
 template <int CC, bool kWithQ, int NTH = NT>
-__device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int tid,
+__device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int Tb, int tid,
                                            Prefetch<CC, NTH> &pf) {
     constexpr int kRows = NTH / 16;                  // rows per pass
     // Uniform chunk base (scalar registers) plus a fixed 32-bit per-lane byte offset:
@@ -92,7 +93,7 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     // (uniform part added first, so that the loads take a scalar base and a 32-bit
     // vector offset)
     auto ld = [&](const char *base_it) { return *reinterpret_cast<const uint4 *>(base_it + loff); };
-    if (t0 + CC <= p.T) {                            // whole chunk in range (uniform)
+    if (t0 + CC <= Tb) {                             // whole chunk in range (uniform)
 #pragma unroll
         for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
             if (kWithQ) pf.q[it] = ld(q + it * pass);
@@ -102,7 +103,7 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     } else {
 #pragma unroll
         for (int it = 0; it < Prefetch<CC, NTH>::kIt; ++it) {
-            const bool in = t0 + r0 + kRows * it < p.T;
+            const bool in = t0 + r0 + kRows * it < Tb;
             if (kWithQ) pf.q[it] = in ? ld(q + it * pass) : zero;
             pf.k[it] = in ? ld(k + it * pass) : zero;
             pf.v[it] = in ? ld(v + it * pass) : zero;
@@ -114,7 +115,7 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
         // opaque per chunk: otherwise base + lane offset is kept per lane (64-bit)
         // across the whole chunk loop
         const unsigned soff = (unsigned)opq(tid * p.H);
-        if (tid < CC && t < p.T) {
+        if (tid < CC && t < Tb) {
             pf.dl = (p.delta + sbase)[soff];
             pf.g = p.log_alpha ? (p.log_alpha + sbase)[soff] : 0.f;
             pf.be = p.beta ? (p.beta + sbase)[soff] : 1.f;

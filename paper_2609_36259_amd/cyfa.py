@@ -22,9 +22,9 @@ STATUS = {0: "CYFA_OK", 1: "CYFA_ERR_INVALID_ARGUMENT", 2: "CYFA_ERR_UNSUPPORTED
 STORE_ROWS = 128
 
 # Every symbol include/cyfa.h declares.
-EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_decode_workspace_size",
-            "cyfa_decode_step", "cyfa_set_timing_events", "cyfa_status_string",
-            "cyfa_last_error", "cyfa_version")
+EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
+            "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
+            "cyfa_status_string", "cyfa_last_error", "cyfa_version")
 
 
 class CyfaError(RuntimeError):
@@ -64,6 +64,8 @@ def load() -> ctypes.CDLL:
         lib.cyfa_forward_workspace_size.restype = ctypes.c_int
         lib.cyfa_forward.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 16 + [ctypes.c_size_t, _vp]
         lib.cyfa_forward.restype = ctypes.c_int
+        lib.cyfa_forward_lens.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 17 + [ctypes.c_size_t, _vp]
+        lib.cyfa_forward_lens.restype = ctypes.c_int
         lib.cyfa_decode_workspace_size.argtypes = [ctypes.POINTER(DecDesc),
                                                    ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_decode_workspace_size.restype = ctypes.c_int
@@ -152,9 +154,12 @@ DEFAULT_CHUNK = {"mfma": 32, "valu": 16}
 
 def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=127,
             chunk=0, segments=0, kernel=KERNEL_AUTO, K0=None, V0=None, clock0=None,
-            return_state=False, return_logits=False, out=None, workspace=None, stream=None):
+            lens=None, return_state=False, return_logits=False, out=None, workspace=None,
+            stream=None):
     """CyFA forward: q,k [B,T,H,dk], v [B,T,H,dv] (float32 or bfloat16), scalars [B,T,H] float32.
 
+    ``lens`` (optional int32 [B] device tensor): sequence b has lens[b] tokens
+    (cyfa_forward_lens); rows t >= lens[b] of the outputs are not written.
     Returns ``o`` [B,T,H,dv] (dtype of q) or a dict with ``o`` and, when requested,
     the final absolute-clock states ``K``/``V`` [B,H,128,d], ``clock`` [B,H] (float64)
     and the slot ``logits`` [B,T,H,m].
@@ -171,6 +176,7 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
     _need(K0, (B, H, STORE_ROWS, dk), torch.float32, "K0")
     _need(V0, (B, H, STORE_ROWS, dv), torch.float32, "V0")
     _need(clock0, (B, H), torch.float64, "clock0")
+    _need(lens, (B,), torch.int32, "lens")
     desc = forward_desc(B, T, H, dk, dv, m=m, chunk=chunk, segments=segments, scale=scale,
                         dtype=dt, kernel=kernel)
     nbytes = forward_workspace_size(desc)
@@ -183,11 +189,11 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
     V_out = torch.empty((B, H, STORE_ROWS, dv), dtype=torch.float32, device=dev) if return_state else None
     clk = torch.empty((B, H), dtype=torch.float64, device=dev) if return_state else None
     logits = torch.empty((B, T, H, m), dtype=torch.float32, device=dev) if return_logits else None
-    st = load().cyfa_forward(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
-                             _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(K0), _ptr(V0),
-                             _ptr(clock0), _ptr(o), _ptr(K_out), _ptr(V_out), _ptr(clk),
-                             _ptr(logits), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
-                             _stream_handle(stream))
+    st = load().cyfa_forward_lens(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
+                                  _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(lens), _ptr(K0),
+                                  _ptr(V0), _ptr(clock0), _ptr(o), _ptr(K_out), _ptr(V_out),
+                                  _ptr(clk), _ptr(logits), _ptr(workspace),
+                                  ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
     _check(st)
     if not (return_state or return_logits):
         return o

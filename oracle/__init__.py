@@ -9,6 +9,9 @@ Sec. 3.1 (Eqs. cyfa-physical-recurrence and cyfa-physical-readout) in double
 precision, one token at a time, with the fractional cyclic shift
 P(tau) = Phi U(tau) Phi^T of Eq. cyfa-fractional-shift rebuilt densely at every
 token (real Fourier basis of App. A.1, Eq. app-real-fourier).
+
+``oracle.backward`` gives the gradients of the same definition (reverse-mode
+differentiation of a float64 token-by-token evaluation with torch on the CPU).
 """
 from __future__ import annotations
 

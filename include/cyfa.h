@@ -166,6 +166,58 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc,
                               void *stream);
 
 /*
+ * Bytes of device workspace cyfa_backward needs for `desc` (host-only).  The
+ * backward keeps the states entering every 16-token chunk and the adjoint
+ * states at every chunk's end (2 x B H ceil(T/16) 128 (d_k + d_v) floats) and
+ * two 128-float rows per token and head; at B=4, T=4096, H=16, d=128 that is
+ * about 4.6 GB.
+ */
+cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes);
+
+/*
+ * Backward of cyfa_forward_lens: gradients of
+ *   L = sum_{b,t,h} <d_o[b,t,h], o[b,t,h]> + <dK_T, K_out> + <dV_T, V_out>
+ * with respect to every input, by reverse-mode differentiation of the
+ * absolute-clock recurrence and readout (Sec. 3.2, Eqs. cyfa-absolute-recurrence
+ * and cyfa-absolute-readout) evaluated chunk by chunk (App. B); the clock
+ * increments receive the reverse cumulative sum of the per-token clock
+ * gradients (Eq. app-clock-gradient-accumulation).  The forward is recomputed
+ * inside the call (only the inputs are needed).
+ *
+ * desc       as for cyfa_forward: d_k, d_v in {64, 128}; dtype F32 or BF16;
+ *            chunk 0 or 16; segments = chunk groups per sequence for the
+ *            parallel kernels (0 = automatic); kernel AUTO or VALU
+ * q .. lens, K0, V0, clock0   the forward's inputs, same layouts and NULL rules
+ * d_o        [B, T, H, d_v] dtype: dL/do (required)
+ * dK_T, dV_T [B, H, 128, d_k] / [B, H, 128, d_v] float: dL/dK_out, dL/dV_out,
+ *            or NULL (no loss on the final state)
+ * dq, dk     [B, T, H, d_k] dtype (required);  dv [B, T, H, d_v] dtype (required)
+ * d_delta    [B, T, H] float (required)
+ * d_log_alpha, d_beta   [B, T, H] float, or NULL; must be NULL when the
+ *            matching input is NULL
+ * d_R        [H, m, m] float, or NULL; must be NULL when R is NULL
+ * d_K0, d_V0 [B, H, 128, d] float gradients of the initial states (rows >= m
+ *            written as 0), or NULL
+ * d_clock0   [B, H] double gradient of the initial clock, or NULL
+ * Rows t >= lens[b] of every per-token gradient are written as 0.  Gradients
+ * are written, not accumulated.  Outputs must not alias inputs or each other.
+ * workspace  at least cyfa_backward_workspace_size bytes, 256-byte aligned.
+ * Arithmetic is fp32; bf16 gradients are rounded to nearest even.
+ */
+cyfa_status cyfa_backward(const cyfa_fwd_desc *desc,
+                          const void *q, const void *k, const void *v,
+                          const float *delta, const float *log_alpha, const float *beta,
+                          const float *R,
+                          const int32_t *lens,
+                          const float *K0, const float *V0, const double *clock0,
+                          const void *d_o, const float *dK_T, const float *dV_T,
+                          void *dq, void *dk, void *dv,
+                          float *d_delta, float *d_log_alpha, float *d_beta, float *d_R,
+                          float *d_K0, float *d_V0, double *d_clock0,
+                          void *workspace, size_t workspace_bytes,
+                          void *stream);
+
+/*
  * Single-token decode descriptor: N independent streams, H heads each.
  *   d_k, d_v 64, 128 or 256; m odd 3..127; dtype of q, k, v, o.
  */

@@ -7,6 +7,7 @@
 #include <cstring>
 
 #include "cyfa.h"
+#include "cyfa_bwd.h"
 #include "cyfa_internal.h"
 
 namespace cyfa {
@@ -119,6 +120,48 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     return CYFA_OK;
 }
 
+struct BwdPlan {
+    int groups;
+    size_t ws_bytes;
+};
+
+cyfa_status plan_backward(const cyfa_fwd_desc *d, BwdPlan *plan) {
+    if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
+    if (d->B < 1 || d->H < 1 || d->T < 0)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "need B >= 1, H >= 1, T >= 0 (got B=%d T=%d H=%d)",
+                    d->B, d->T, d->H);
+    if ((double)d->B * d->T * d->H * (d->d_k > d->d_v ? d->d_k : d->d_v) > 4.0e12)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "problem too large");
+    if (d->d_k <= 0 || d->d_v <= 0)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
+    if ((d->d_k != 64 && d->d_k != 128) || (d->d_v != 64 && d->d_v != 128))
+        return fail(CYFA_ERR_UNSUPPORTED, "backward head dims must be 64 or 128 (got d_k=%d d_v=%d)",
+                    d->d_k, d->d_v);
+    if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
+        return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
+                                                               : CYFA_ERR_INVALID_ARGUMENT,
+                    "m must be odd and in [3, 127] (got %d)", d->m);
+    if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
+    if (d->kernel != CYFA_KERNEL_AUTO && d->kernel != CYFA_KERNEL_VALU)
+        return fail(d->kernel == CYFA_KERNEL_MFMA ? CYFA_ERR_UNSUPPORTED : CYFA_ERR_INVALID_ARGUMENT,
+                    "backward runs the vector-ALU kernels (kernel AUTO or VALU)");
+    if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
+    if (d->chunk != 0 && d->chunk != cyfa::kBwdChunk)
+        return fail(CYFA_ERR_UNSUPPORTED, "backward chunk must be 0 or %d (got %d)", cyfa::kBwdChunk,
+                    d->chunk);
+    if (d->segments < 0 || d->segments > 1024)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "segments must be in [0, 1024]");
+    const int nc = (d->T + cyfa::kBwdChunk - 1) / cyfa::kBwdChunk;
+    int g = d->segments ? d->segments : cyfa::bwd_auto_groups(d->B, d->T, d->H);
+    if (g > nc) g = nc;
+    if (g < 1) g = 1;
+    const int cpg = nc > 0 ? (nc + g - 1) / g : 1;
+    plan->groups = nc > 0 ? (nc + cpg - 1) / cpg : 1;
+    plan->ws_bytes = cyfa::bwd_workspace_bytes(d->B, d->T, d->H, d->d_k, d->d_v, plan->groups);
+    return CYFA_OK;
+}
+
 cyfa_status check_dec(const cyfa_dec_desc *d) {
     if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
     if (d->N < 1 || d->H < 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "need N >= 1 and H >= 1");
@@ -214,6 +257,74 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
         if (e == hipSuccess) e = mark(g_ev_stop, s);
     }
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "forward launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes) {
+    if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    BwdPlan plan;
+    cyfa_status st = plan_backward(desc, &plan);
+    if (st != CYFA_OK) return st;
+    *bytes = plan.ws_bytes;
+    return ok();
+}
+
+cyfa_status cyfa_backward(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                          const float *delta, const float *log_alpha, const float *beta,
+                          const float *R, const int32_t *lens, const float *K0, const float *V0,
+                          const double *clock0, const void *d_o, const float *dK_T,
+                          const float *dV_T, void *dq, void *dk, void *dv, float *d_delta,
+                          float *d_log_alpha, float *d_beta, float *d_R, float *d_K0, float *d_V0,
+                          double *d_clock0, void *workspace, size_t workspace_bytes, void *stream) {
+    BwdPlan plan;
+    cyfa_status st = plan_backward(desc, &plan);
+    if (st != CYFA_OK) return st;
+    if (desc->T > 0 && (!q || !k || !v || !delta || !d_o || !dq || !dk || !dv || !d_delta))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "q, k, v, delta, d_o, dq, dk, dv and d_delta are required");
+    if ((d_log_alpha && !log_alpha) || (d_beta && !beta) || (d_R && !R))
+        return fail(CYFA_ERR_INVALID_ARGUMENT,
+                    "the gradient of an input passed as NULL must be NULL (d_log_alpha, d_beta, d_R)");
+    const void *vec[] = {q, k, v, d_o, K0, V0, dK_T, dV_T, dq, dk, dv, d_K0, d_V0};
+    for (const void *p : vec)
+        if (p && !aligned(p, 16)) return fail(CYFA_ERR_INVALID_ARGUMENT, "tensors must be 16-byte aligned");
+    const void *sc[] = {delta, log_alpha, beta, R, lens, d_delta, d_log_alpha, d_beta, d_R};
+    for (const void *p : sc)
+        if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    if ((clock0 && !aligned(clock0, 8)) || (d_clock0 && !aligned(d_clock0, 8)))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "clock arrays must be 8-byte aligned");
+    {
+        const void *outs[] = {dq, dk, dv, d_delta, d_log_alpha, d_beta, d_R, d_K0, d_V0, d_clock0};
+        const void *ins[] = {q, k, v, delta, log_alpha, beta, R, lens, K0, V0, clock0, d_o, dK_T, dV_T};
+        for (int a = 0; a < 10; ++a) {
+            if (!outs[a]) continue;
+            for (int c = a + 1; c < 10; ++c)
+                if (outs[a] == outs[c]) return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias each other");
+            for (const void *in : ins)
+                if (in == outs[a]) return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias inputs");
+        }
+    }
+    if (!workspace || workspace_bytes < plan.ws_bytes)
+        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required (got %zu)", plan.ws_bytes,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, kWsAlign))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+
+    cyfa::BwdParams p{};
+    p.B = desc->B; p.T = desc->T; p.H = desc->H; p.dk = desc->d_k; p.dv = desc->d_v; p.m = desc->m;
+    p.nc = (desc->T + cyfa::kBwdChunk - 1) / cyfa::kBwdChunk;
+    p.Tpad = p.nc * cyfa::kBwdChunk;
+    p.groups = plan.groups;
+    p.cpg = p.nc > 0 ? (p.nc + plan.groups - 1) / plan.groups : 1;
+    p.scale = desc->scale; p.dtype = desc->dtype;
+    p.q = q; p.k = k; p.v = v; p.dout = d_o;
+    p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R; p.lens = lens;
+    p.K0 = K0; p.V0 = V0; p.clock0 = clock0; p.dK_T = dK_T; p.dV_T = dV_T;
+    p.gq = dq; p.gk = dk; p.gv = dv;
+    p.gdelta = d_delta; p.glog_alpha = d_log_alpha; p.gbeta = d_beta; p.gR = d_R;
+    p.gK0 = d_K0; p.gV0 = d_V0; p.gclock0 = d_clock0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = cyfa::launch_bwd_valu(p, workspace, s);
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "backward launch: %s", hipGetErrorString(e));
     return ok();
 }
 

@@ -1,0 +1,42 @@
+// Internal declarations of the backward pass (not part of the public ABI).
+#pragma once
+
+#include "cyfa_internal.h"
+
+namespace cyfa {
+
+constexpr int kBwdChunk = 16;       // tokens per chunk of the backward kernels
+
+// Gradients of L = sum_t <do_t, o_t> + <dK_T, Kbar_T> + <dV_T, Vbar_T>.
+struct BwdParams {
+    int B, T, H, dk, dv, m;
+    int nc;                         // chunks per sequence, ceil(T / kBwdChunk)
+    int Tpad;                       // nc * kBwdChunk: rows of the per-token workspace arrays
+    int groups, cpg;                // chunk groups per sequence and chunks per group
+    float scale;
+    int dtype;
+    const void *q, *k, *v, *dout;
+    const float *delta, *log_alpha, *beta, *R;
+    const int *lens;
+    const float *K0, *V0;
+    const double *clock0;
+    const float *dK_T, *dV_T;
+    void *gq, *gk, *gv;             // dtype of q
+    float *gdelta, *glog_alpha, *gbeta, *gR, *gK0, *gV0;
+    double *gclock0;
+    // workspace (see bwd_workspace_bytes)
+    const float *M;                 // [H][128][128] readout matrix R Phi
+    float *Kst, *Vst;               // [BH][nc][128][d] states entering each chunk
+    double *clk;                    // [BH][nc] clock entering each chunk (reduced mod m)
+    float *DKe, *DVe;               // [BH][nc][128][d] adjoint states at each chunk's end
+    float *U, *dP;                  // [BH][Tpad][128] readout output u_t and key-pass adjoint dp_t
+    float *udu, *dlam, *dG;         // [BH][Tpad] <u_t, du_t>, dL/dlambda_t, dL/dG_t
+    float *dMp;                     // [BH][groups][128][128] partial dL/dM
+    float *fin;                     // [BH] <dK_T, Kbar_T> + <dV_T, Vbar_T>
+};
+
+size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups);
+int bwd_auto_groups(int B, int T, int H);
+hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s);
+
+}  // namespace cyfa

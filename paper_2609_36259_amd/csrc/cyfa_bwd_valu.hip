@@ -1,0 +1,897 @@
+// Vector-ALU backward of the chunk-wise CyFA forward (fp32 arithmetic).
+//
+// Gradients of L = sum_t <do_t, o_t> + <dK_T, Kbar_T> + <dV_T, Vbar_T> in the
+// absolute-clock form (Sec. 3.2, Eqs. cyfa-absolute-recurrence and
+// cyfa-absolute-readout), evaluated chunk by chunk as the forward is (App. B).
+// Forward per token: a_t = beta_t U(-lambda_t) b (Eq. app-temporal-writes),
+// Kbar_t = alpha_t Kbar_{t-1} + a_t k_t^T (Vbar likewise), p_t = Kbar_t q_t,
+// X_t = scale U(lambda_t) p_t, Z_t = M X_t, W_t = softmax over the m active
+// slots, u_t = U(-lambda_t) M^T W_t, o_t = Vbar_t^T u_t, with M = R Phi.
+// Reverse mode:
+//   du_t = Vbar_t do_t,  dY_t = U(lambda_t) du_t,  dW_t = M dY_t,
+//   dZ_t = W_t (.) (dW_t - <W_t, dW_t>),  dX_t = M^T dZ_t,  dp_t = scale U(-lambda_t) dX_t,
+//   dM = sum_t W_t dY_t^T + dZ_t X_t^T  and  dR = dM Phi^T,
+//   adjoint states DK_t = dp_t q_t^T + alpha_{t+1} DK_{t+1},  DV_t = u_t do_t^T + alpha_{t+1} DV_{t+1}
+//   (starting from dK_T, dV_T), dq_t = Kbar_t^T dp_t, dk_t = DK_t^T a_t, dv_t = DV_t^T a_t,
+//   da_t = DK_t k_t + DV_t v_t,  dbeta_t = <da_t, U(-lambda_t) b>.
+// Decay: with G_t = sum_{j<=t} log alpha_j every pair (t, s) of a pass carries
+// exp(G_t - G_s), so dL/dG_t = <q_t, dq_t> - <k_t, dk_t> + <u_t, du_t> - <a_t, DV_t v_t>
+// (plus <dK_T, Kbar_T> + <dV_T, Vbar_T> at the last token) and dlog_alpha_t is the
+// reverse cumulative sum of dL/dG.  Clock: U(+-lambda_t) acts on the (cos, sin)
+// pair j as a rotation by +-2 pi j lambda_t / m, whose derivative is the
+// rotation generator; dL/dlambda_t collects the three rotations of token t (a_t,
+// X_t, u_t) and ddelta_t = sum_{tau >= t} dL/dlambda_tau
+// (Eq. app-clock-gradient-accumulation); dclock0 is the full sum.
+//
+// Within a chunk (rows r, s; gamma_r = exp(G_r), Gamma_rs = exp(G_r - G_s) for
+// r >= s, rho_s = exp(G_C - G_s), entering states Kbar_c, Vbar_c, adjoints
+// DK', DV' at the chunk's end):
+//   p  = gamma (.) Q Kbar_c^T + (Q K^T (.) Gamma) A
+//   du = gamma (.) dO Vbar_c  + (dO V^T (.) Gamma) A
+//   dq = gamma (.) dP Kbar_c  + (dP A^T (.) Gamma) K
+//   dk = (dP A^T (.) Gamma)^T Q + (rho (.) A) DK'
+//   dv = (U A^T (.) Gamma)^T dO + (rho (.) A) DV'
+//   da = (Q K^T (.) Gamma)^T dP + rho (.) K DK'^T + (dO V^T (.) Gamma)^T U + rho (.) V DV'^T
+// Kernels: (1) states entering every chunk, per sequence; (2) readout
+// recomputation and its adjoint, per chunk group; (3) adjoint states at every
+// chunk's end, per sequence, in reverse; (4) token gradients, per chunk group;
+// (5) reverse cumulative sums, per sequence; (6) dR, per head.
+#include "cyfa_bwd.h"
+
+namespace cyfa {
+
+namespace {
+
+constexpr int kC = kBwdChunk;
+constexpr int kNT = 256;            // threads per workgroup
+constexpr int kLD = kStoreRows + 1; // padded row of a [token][basis] tile
+constexpr float kTwoPi = 6.283185307179586f;
+
+__device__ __forceinline__ float wsum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
+__device__ __forceinline__ float wmax(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+    return x;
+}
+
+__device__ __forceinline__ int bwd_tokens(const BwdParams &p, int b) {
+    return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
+}
+
+// Per-chunk scalar tables.
+struct ChunkTab {
+    double lam[kC];                 // clock after token r, reduced mod m
+    float G[kC];                    // sum of log alpha over the chunk's tokens 0..r
+    float beta[kC];
+    float2 cs[kC][64];              // (cos, sin) of 2 pi j lam_r / m at [r][j-1]
+};
+
+// Loads the chunk's scalars (rows at or past the sequence's end: no shift, no
+// decay, no write), forms the clock and log-decay prefix sums and the phase
+// table.  Ends with a barrier.
+__device__ void chunk_tables(const BwdParams &p, int b, int h, int t0, int Tb, double lam_in,
+                             ChunkTab &s, int tid) {
+    if (tid < kC) {
+        const int t = t0 + tid;
+        const bool live = t < Tb;
+        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        s.lam[tid] = live ? (double)p.delta[si] : 0.0;
+        s.G[tid] = (live && p.log_alpha) ? p.log_alpha[si] : 0.f;
+        s.beta[tid] = live ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double lam = lam_in;
+        float G = 0.f;
+        for (int r = 0; r < kC; ++r) {
+            lam = reduce_clock(lam + s.lam[r], p.m);
+            s.lam[r] = lam;
+            G += s.G[r];
+            s.G[r] = G;
+        }
+    }
+    __syncthreads();
+    const int J = (p.m - 1) / 2;
+    for (int e = tid; e < kC * 64; e += kNT) {
+        const int r = e >> 6, jj = e & 63;
+        float c = 1.f, sn = 0.f;
+        if (jj < J) clock_phase(s.lam[r], jj + 1, p.m, &c, &sn);
+        s.cs[r][jj] = make_float2(c, sn);
+    }
+    __syncthreads();
+}
+
+// Temporal write rows A_r = beta_r U(-lambda_r) b (Eq. app-temporal-writes);
+// with unit = true the same without beta (the direction dA is projected on for dbeta).
+__device__ __forceinline__ float write_entry(const ChunkTab &s, int m, int r, int i, float be) {
+    if (i == 0) return be * (1.f / sqrtf((float)m));
+    if (i >= m) return 0.f;
+    const float ac = sqrtf(2.f / (float)m);
+    const float2 cs = s.cs[r][(i - 1) >> 1];
+    return (i & 1) ? be * ac * cs.x : -be * ac * cs.y;
+}
+__device__ void build_writes(const ChunkTab &s, int m, float (*A)[kLD], int tid) {
+    for (int e = tid; e < kC * kStoreRows; e += kNT) {
+        const int r = e >> 7, i = e & 127;
+        A[r][i] = write_entry(s, m, r, i, s.beta[r]);
+    }
+}
+
+// Y_r <- mul * U(sign lambda_r) Y_r for every row, in place: element 0 is scaled,
+// pair (2j-1, 2j) rotated by sign * 2 pi j lambda_r / m; padding rows untouched.
+__device__ void rotate_rows(float (*Y)[kLD], const ChunkTab &s, int m, float sign, float mul, int tid) {
+    const int J = (m - 1) / 2;
+    for (int e = tid; e < kC * 64; e += kNT) {
+        const int r = e >> 6, j = e & 63;
+        if (j == 0) {
+            Y[r][0] *= mul;
+        } else if (j <= J) {
+            const float2 cs = s.cs[r][j - 1];
+            const float c = cs.x, sn = sign * cs.y;
+            const float a = Y[r][2 * j - 1], bb = Y[r][2 * j];
+            Y[r][2 * j - 1] = mul * (c * a - sn * bb);
+            Y[r][2 * j] = mul * (sn * a + c * bb);
+        }
+    }
+}
+
+// dL/dlambda of Z = U(sign lambda) y given dZ (one row, one wave): the pair j
+// contributes sign (2 pi j / m) (dZ_{2j} Z_{2j-1} - dZ_{2j-1} Z_{2j}).
+__device__ __forceinline__ float rot_grad(const float *dZ, const float *Z, int m, float sign, int lane) {
+    const int J = (m - 1) / 2, j = lane + 1;
+    float acc = 0.f;
+    if (j <= J) acc = (float)j * (dZ[2 * j] * Z[2 * j - 1] - dZ[2 * j - 1] * Z[2 * j]);
+    return sign * (kTwoPi / (float)m) * wsum(acc);
+}
+
+template <typename Tin>
+__device__ __forceinline__ float ld_row(const void *base, int b, int t, int h, int c, int T, int H, int D, bool live) {
+    return live ? load_as_float(static_cast<const Tin *>(base), (((size_t)b * T + t) * H + h) * D + c) : 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// (1) states entering every chunk.  Thread (i = tid / 2, part = tid % 2) keeps
+// row i, column half `part` of both states.
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
+    constexpr int KH = DK / 2, VH = DV / 2;
+    __shared__ float Ks[kC][DK];
+    __shared__ float Vs[kC][DV];
+    __shared__ float As[kC][kLD];
+    __shared__ ChunkTab tab;
+    __shared__ float red[kNT / 64];
+    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int Tb = bwd_tokens(p, b);
+    float kst[KH], vst[VH];
+#pragma unroll
+    for (int c = 0; c < KH; ++c)
+        kst[c] = (p.K0 && i < m) ? p.K0[((size_t)bh * kStoreRows + i) * DK + part * KH + c] : 0.f;
+#pragma unroll
+    for (int c = 0; c < VH; ++c)
+        vst[c] = (p.V0 && i < m) ? p.V0[((size_t)bh * kStoreRows + i) * DV + part * VH + c] : 0.f;
+    double lam = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
+    for (int c = 0; c < p.nc; ++c) {
+        const int t0 = c * kC;
+        float *Kd = p.Kst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
+        float *Vd = p.Vst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc) Kd[cc] = kst[cc];
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc) Vd[cc] = vst[cc];
+        if (tid == 0) p.clk[(size_t)bh * p.nc + c] = lam;
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            Ks[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
+        }
+        for (int e = tid; e < kC * DV; e += kNT) {
+            const int r = e / DV, cc = e % DV;
+            Vs[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
+        }
+        chunk_tables(p, b, h, t0, Tb, lam, tab, tid);
+        build_writes(tab, m, As, tid);
+        __syncthreads();
+        const float GC = tab.G[kC - 1], gC = __expf(GC);
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc) kst[cc] *= gC;
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc) vst[cc] *= gC;
+        for (int r = 0; r < kC; ++r) {
+            const float w = As[r][i] * __expf(GC - tab.G[r]);
+#pragma unroll
+            for (int cc = 0; cc < KH; ++cc) kst[cc] = fmaf(w, Ks[r][part * KH + cc], kst[cc]);
+#pragma unroll
+            for (int cc = 0; cc < VH; ++cc) vst[cc] = fmaf(w, Vs[r][part * VH + cc], vst[cc]);
+        }
+        lam = tab.lam[kC - 1];
+        __syncthreads();
+    }
+    // <dK_T, Kbar_T> + <dV_T, Vbar_T>: the final-state term of dL/dG at the last token
+    float acc = 0.f;
+    if (p.dK_T && i < m)
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc)
+            acc = fmaf(p.dK_T[((size_t)bh * kStoreRows + i) * DK + part * KH + cc], kst[cc], acc);
+    if (p.dV_T && i < m)
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc)
+            acc = fmaf(p.dV_T[((size_t)bh * kStoreRows + i) * DV + part * VH + cc], vst[cc], acc);
+    acc = wsum(acc);
+    if ((tid & 63) == 0) red[tid >> 6] = acc;
+    __syncthreads();
+    if (tid == 0) p.fin[bh] = red[0] + red[1] + red[2] + red[3];
+}
+
+// ---------------------------------------------------------------------------
+// (2) readout recomputation and its adjoint, per (sequence, chunk group).
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
+    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int DM = DK > DV ? DK : DV;
+    __shared__ float Ms[kStoreRows][kLD];
+    __shared__ float In0[kC][DM + 1];       // Q, then dO
+    __shared__ float In1[kC][DM + 1];       // K, then V
+    __shared__ float As[kC][kLD], Xs[kC][kLD], Ws[kC][kLD], Us[kC][kLD], dUs[kC][kLD], dWs[kC][kLD];
+    __shared__ float S1[kC][kC + 1], S2[kC][kC + 1];
+    __shared__ ChunkTab tab;
+    __shared__ float dlu[kC];
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int Tb = bwd_tokens(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    const float *Mh = p.M + (size_t)h * kStoreRows * kStoreRows;
+    for (int e = tid; e < kStoreRows * kStoreRows; e += kNT) Ms[e >> 7][e & 127] = Mh[e];
+    float dMacc[64];                        // dM[i][64 part .. 64 part + 63]
+#pragma unroll
+    for (int jj = 0; jj < 64; ++jj) dMacc[jj] = 0.f;
+
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * kC;
+        const size_t row0 = (size_t)bh * p.Tpad + t0;
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            const bool live = t0 + r < Tb;
+            In0[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, live);
+            In1[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, live);
+        }
+        chunk_tables(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
+        build_writes(tab, m, As, tid);
+        {   // S1 = (Q K^T) (.) Gamma
+            const int r = tid >> 4, s = tid & 15;
+            float acc = 0.f;
+            if (s <= r) {
+                for (int cc = 0; cc < DK; ++cc) acc = fmaf(In0[r][cc], In1[s][cc], acc);
+                acc *= __expf(tab.G[r] - tab.G[s]);
+            }
+            S1[r][s] = acc;
+        }
+        {   // p_r = gamma_r Kbar_c q_r (entering key state)
+            const float *Kc = p.Kst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
+            float kr[KH];
+#pragma unroll
+            for (int cc = 0; cc < KH; ++cc) kr[cc] = Kc[cc];
+            for (int r = 0; r < kC; ++r) {
+                float ps = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < KH; ++cc) ps = fmaf(In0[r][part * KH + cc], kr[cc], ps);
+                ps += __shfl_xor(ps, 1);
+                if (part == 0) Xs[r][i] = __expf(tab.G[r]) * ps;
+            }
+        }
+        __syncthreads();
+        // p += S1 A
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            float acc = Xs[r][ii];
+            for (int s = 0; s <= r; ++s) acc = fmaf(S1[r][s], As[s][ii], acc);
+            Xs[r][ii] = acc;
+        }
+        __syncthreads();
+        for (int e = tid; e < kC * DV; e += kNT) {
+            const int r = e / DV, cc = e % DV;
+            const bool live = t0 + r < Tb;
+            In0[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, live);
+            In1[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, live);
+        }
+        // X = scale U(lambda) p
+        rotate_rows(Xs, tab, m, 1.f, p.scale, tid);
+        __syncthreads();
+        // Z = M X (active slots), S2 = (dO V^T) (.) Gamma
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            float acc = 0.f;
+            if (ii < m)
+                for (int j = 0; j < m; ++j) acc = fmaf(Ms[ii][j], Xs[r][j], acc);
+            Ws[r][ii] = acc;
+        }
+        {
+            const int r = tid >> 4, s = tid & 15;
+            float acc = 0.f;
+            if (s <= r) {
+                for (int cc = 0; cc < DV; ++cc) acc = fmaf(In0[r][cc], In1[s][cc], acc);
+                acc *= __expf(tab.G[r] - tab.G[s]);
+            }
+            S2[r][s] = acc;
+        }
+        __syncthreads();
+        // W = softmax over the m active slots
+        for (int r = wave; r < kC; r += kNT / 64) {
+            const float z0 = lane < m ? Ws[r][lane] : -INFINITY;
+            const float z1 = lane + 64 < m ? Ws[r][lane + 64] : -INFINITY;
+            const float mx = wmax(fmaxf(z0, z1));
+            const float e0 = lane < m ? __expf(z0 - mx) : 0.f;
+            const float e1 = lane + 64 < m ? __expf(z1 - mx) : 0.f;
+            const float inv = 1.f / wsum(e0 + e1);
+            Ws[r][lane] = e0 * inv;
+            Ws[r][lane + 64] = e1 * inv;
+        }
+        __syncthreads();
+        // Y = M^T W
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, jj = e & 127;
+            float acc = 0.f;
+            if (jj < m)
+                for (int ii = 0; ii < m; ++ii) acc = fmaf(Ws[r][ii], Ms[ii][jj], acc);
+            Us[r][jj] = acc;
+        }
+        __syncthreads();
+        // u = U(-lambda) Y;  du_r = gamma_r Vbar_c do_r (entering value state)
+        rotate_rows(Us, tab, m, -1.f, 1.f, tid);
+        {
+            const float *Vc = p.Vst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+            float vr[VH];
+#pragma unroll
+            for (int cc = 0; cc < VH; ++cc) vr[cc] = Vc[cc];
+            for (int r = 0; r < kC; ++r) {
+                float ps = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < VH; ++cc) ps = fmaf(In0[r][part * VH + cc], vr[cc], ps);
+                ps += __shfl_xor(ps, 1);
+                if (part == 0) dUs[r][i] = __expf(tab.G[r]) * ps;
+            }
+        }
+        __syncthreads();
+        // store u; du += S2 A
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            p.U[(row0 + r) * kStoreRows + ii] = Us[r][ii];
+            float acc = dUs[r][ii];
+            for (int s = 0; s <= r; ++s) acc = fmaf(S2[r][s], As[s][ii], acc);
+            dUs[r][ii] = acc;
+        }
+        __syncthreads();
+        // <u, du> and the clock gradient of u = U(-lambda) Y
+        for (int r = wave; r < kC; r += kNT / 64) {
+            const float ud = wsum(Us[r][lane] * dUs[r][lane] + Us[r][lane + 64] * dUs[r][lane + 64]);
+            const float gl = rot_grad(dUs[r], Us[r], m, -1.f, lane);
+            if (lane == 0) {
+                p.udu[row0 + r] = ud;
+                dlu[r] = gl;
+            }
+        }
+        __syncthreads();
+        // dY = U(lambda) du
+        rotate_rows(dUs, tab, m, 1.f, 1.f, tid);
+        __syncthreads();
+        // dW = M dY;  dM += W dY^T
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            float acc = 0.f;
+            if (ii < m)
+                for (int j = 0; j < m; ++j) acc = fmaf(Ms[ii][j], dUs[r][j], acc);
+            dWs[r][ii] = acc;
+        }
+        for (int r = 0; r < kC; ++r) {
+            const float w = Ws[r][i];
+#pragma unroll
+            for (int jj = 0; jj < 64; ++jj) dMacc[jj] = fmaf(w, dUs[r][part * 64 + jj], dMacc[jj]);
+        }
+        __syncthreads();
+        // dZ = W (.) (dW - <W, dW>)
+        for (int r = wave; r < kC; r += kNT / 64) {
+            const float w0 = Ws[r][lane], w1 = Ws[r][lane + 64];
+            const float d0 = dWs[r][lane], d1 = dWs[r][lane + 64];
+            const float sd = wsum(w0 * d0 + w1 * d1);
+            dWs[r][lane] = w0 * (d0 - sd);
+            dWs[r][lane + 64] = w1 * (d1 - sd);
+        }
+        __syncthreads();
+        // dM += dZ X^T;  dX = M^T dZ (into the dY tile)
+        for (int r = 0; r < kC; ++r) {
+            const float dz = dWs[r][i];
+#pragma unroll
+            for (int jj = 0; jj < 64; ++jj) dMacc[jj] = fmaf(dz, Xs[r][part * 64 + jj], dMacc[jj]);
+        }
+        __syncthreads();
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, jj = e & 127;
+            float acc = 0.f;
+            if (jj < m)
+                for (int ii = 0; ii < m; ++ii) acc = fmaf(dWs[r][ii], Ms[ii][jj], acc);
+            dUs[r][jj] = acc;
+        }
+        __syncthreads();
+        // clock gradient of X = scale U(lambda) p, plus that of u
+        for (int r = wave; r < kC; r += kNT / 64) {
+            const float gl = rot_grad(dUs[r], Xs[r], m, 1.f, lane);
+            if (lane == 0) p.dlam[row0 + r] = dlu[r] + gl;
+        }
+        __syncthreads();
+        // dp = scale U(-lambda) dX
+        rotate_rows(dUs, tab, m, -1.f, p.scale, tid);
+        __syncthreads();
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            p.dP[(row0 + r) * kStoreRows + ii] = dUs[r][ii];
+        }
+        __syncthreads();
+    }
+    float *dMo = p.dMp + (((size_t)bh * p.groups + g) * kStoreRows + i) * kStoreRows + part * 64;
+#pragma unroll
+    for (int jj = 0; jj < 64; ++jj) dMo[jj] = dMacc[jj];
+}
+
+// ---------------------------------------------------------------------------
+// (3) adjoint states at every chunk's end, reverse over chunks; dK0, dV0.
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
+    constexpr int KH = DK / 2, VH = DV / 2;
+    __shared__ float Qs[kC][DK];
+    __shared__ float dOs[kC][DV];
+    __shared__ float dPs[kC][kStoreRows];
+    __shared__ float Us[kC][kStoreRows];
+    __shared__ float Gs[kC];
+    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int Tb = bwd_tokens(p, b);
+    float ak[KH], av[VH];
+#pragma unroll
+    for (int c = 0; c < KH; ++c)
+        ak[c] = (p.dK_T && i < m) ? p.dK_T[((size_t)bh * kStoreRows + i) * DK + part * KH + c] : 0.f;
+#pragma unroll
+    for (int c = 0; c < VH; ++c)
+        av[c] = (p.dV_T && i < m) ? p.dV_T[((size_t)bh * kStoreRows + i) * DV + part * VH + c] : 0.f;
+    for (int c = p.nc - 1; c >= 0; --c) {
+        const int t0 = c * kC;
+        const size_t row0 = (size_t)bh * p.Tpad + t0;
+        float *Kd = p.DKe + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
+        float *Vd = p.DVe + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc) Kd[cc] = ak[cc];
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc) Vd[cc] = av[cc];
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
+        }
+        for (int e = tid; e < kC * DV; e += kNT) {
+            const int r = e / DV, cc = e % DV;
+            dOs[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
+        }
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            dPs[r][ii] = p.dP[(row0 + r) * kStoreRows + ii];
+            Us[r][ii] = p.U[(row0 + r) * kStoreRows + ii];
+        }
+        if (tid < kC) {
+            const int t = t0 + tid;
+            Gs[tid] = (t < Tb && p.log_alpha) ? p.log_alpha[((size_t)b * p.T + t) * p.H + h] : 0.f;
+        }
+        __syncthreads();
+        if (tid == 0)
+            for (int r = 1; r < kC; ++r) Gs[r] += Gs[r - 1];
+        __syncthreads();
+        const float gC = __expf(Gs[kC - 1]);
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc) ak[cc] *= gC;
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc) av[cc] *= gC;
+        for (int r = 0; r < kC; ++r) {
+            const float gr = __expf(Gs[r]);
+            const float wk = gr * dPs[r][i], wv = gr * Us[r][i];
+#pragma unroll
+            for (int cc = 0; cc < KH; ++cc) ak[cc] = fmaf(wk, Qs[r][part * KH + cc], ak[cc]);
+#pragma unroll
+            for (int cc = 0; cc < VH; ++cc) av[cc] = fmaf(wv, dOs[r][part * VH + cc], av[cc]);
+        }
+        __syncthreads();
+    }
+    if (p.gK0)
+#pragma unroll
+        for (int cc = 0; cc < KH; ++cc)
+            p.gK0[((size_t)bh * kStoreRows + i) * DK + part * KH + cc] = i < m ? ak[cc] : 0.f;
+    if (p.gV0)
+#pragma unroll
+        for (int cc = 0; cc < VH; ++cc)
+            p.gV0[((size_t)bh * kStoreRows + i) * DV + part * VH + cc] = i < m ? av[cc] : 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// (4) token gradients, per (sequence, chunk group).
+// Column products (a sum over the 128 state rows) give thread (column cc, row
+// block ih) the partial sums for all kC tokens; row products (a sum over state
+// columns) give thread (row i, half part) one state row.
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
+    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int IHK = kNT / DK, IHV = kNT / DV;          // row blocks of the column products
+    __shared__ float Qs[kC][DK + 1], Ks[kC][DK + 1], gQ[kC][DK + 1], gK[kC][DK + 1];
+    __shared__ float Vs[kC][DV + 1], dOs[kC][DV + 1];
+    __shared__ float dPs[kC][kLD], Us[kC][kLD], As[kC][kLD], dAK[kC][kLD], dAV[kC][kLD];
+    __shared__ float Sqk[kC][kC + 1], Sdpa[kC][kC + 1], Suoa[kC][kC + 1], Sdov[kC][kC + 1];
+    __shared__ float red[kNT * kC];
+    __shared__ ChunkTab tab;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int Tb = bwd_tokens(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    Tin *gq = static_cast<Tin *>(p.gq);
+    Tin *gk = static_cast<Tin *>(p.gk);
+    Tin *gv = static_cast<Tin *>(p.gv);
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * kC;
+        const size_t row0 = (size_t)bh * p.Tpad + t0;
+        const size_t st = ((size_t)bh * p.nc + c) * kStoreRows;    // state row 0 of this chunk
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            const bool live = t0 + r < Tb;
+            Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, live);
+            Ks[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, live);
+        }
+        for (int e = tid; e < kC * DV; e += kNT) {
+            const int r = e / DV, cc = e % DV;
+            const bool live = t0 + r < Tb;
+            Vs[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, live);
+            dOs[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, live);
+        }
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            dPs[r][ii] = p.dP[(row0 + r) * kStoreRows + ii];
+            Us[r][ii] = p.U[(row0 + r) * kStoreRows + ii];
+        }
+        chunk_tables(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
+        build_writes(tab, m, As, tid);
+        __syncthreads();
+        const float GC = tab.G[kC - 1];
+        {   // the four masked score tiles
+            const int r = tid >> 4, s = tid & 15;
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+            if (s <= r) {
+                const float gam = __expf(tab.G[r] - tab.G[s]);
+                for (int cc = 0; cc < DK; ++cc) a0 = fmaf(Qs[r][cc], Ks[s][cc], a0);
+                for (int cc = 0; cc < DV; ++cc) a1 = fmaf(dOs[r][cc], Vs[s][cc], a1);
+                for (int ii = 0; ii < kStoreRows; ++ii) {
+                    a2 = fmaf(dPs[r][ii], As[s][ii], a2);
+                    a3 = fmaf(Us[r][ii], As[s][ii], a3);
+                }
+                a0 *= gam; a1 *= gam; a2 *= gam; a3 *= gam;
+            }
+            Sqk[r][s] = a0;
+            Sdov[r][s] = a1;
+            Sdpa[r][s] = a2;
+            Suoa[r][s] = a3;
+        }
+        // dq: gamma_r (dP Kbar_c)[r] + (Sdpa K)[r]
+        {
+            const int cc = tid % DK, ih = tid / DK;
+            constexpr int RB = kStoreRows / IHK;
+            float acc[kC];
+#pragma unroll
+            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                const float kb = p.Kst[(st + ii) * DK + cc];
+#pragma unroll
+                for (int r = 0; r < kC; ++r) acc[r] = fmaf(dPs[r][ii], kb, acc[r]);
+            }
+#pragma unroll
+            for (int r = 0; r < kC; ++r) red[(ih * kC + r) * DK + cc] = acc[r];
+        }
+        __syncthreads();
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            float sum = 0.f;
+            for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kC + r) * DK + cc];
+            float acc = __expf(tab.G[r]) * sum;
+            for (int s = 0; s <= r; ++s) acc = fmaf(Sdpa[r][s], Ks[s][cc], acc);
+            gQ[r][cc] = acc;
+        }
+        __syncthreads();
+        // dk: (Sdpa^T Q)[s] + rho_s (A DK')[s]
+        {
+            const int cc = tid % DK, ih = tid / DK;
+            constexpr int RB = kStoreRows / IHK;
+            float acc[kC];
+#pragma unroll
+            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                const float kb = p.DKe[(st + ii) * DK + cc];
+#pragma unroll
+                for (int s = 0; s < kC; ++s) acc[s] = fmaf(As[s][ii], kb, acc[s]);
+            }
+#pragma unroll
+            for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DK + cc] = acc[s];
+        }
+        __syncthreads();
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int s = e / DK, cc = e % DK;
+            float sum = 0.f;
+            for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kC + s) * DK + cc];
+            float acc = __expf(GC - tab.G[s]) * sum;
+            for (int r = s; r < kC; ++r) acc = fmaf(Sdpa[r][s], Qs[r][cc], acc);
+            gK[s][cc] = acc;
+        }
+        __syncthreads();
+        // dv: (Suoa^T dO)[s] + rho_s (A DV')[s], written out directly
+        {
+            const int cc = tid % DV, ih = tid / DV;
+            constexpr int RB = kStoreRows / IHV;
+            float acc[kC];
+#pragma unroll
+            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                const float vb = p.DVe[(st + ii) * DV + cc];
+#pragma unroll
+                for (int s = 0; s < kC; ++s) acc[s] = fmaf(As[s][ii], vb, acc[s]);
+            }
+#pragma unroll
+            for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DV + cc] = acc[s];
+        }
+        __syncthreads();
+        for (int e = tid; e < kC * DV; e += kNT) {
+            const int s = e / DV, cc = e % DV;
+            const int t = t0 + s;
+            if (t >= p.T) continue;
+            float sum = 0.f;
+            for (int ih = 0; ih < IHV; ++ih) sum += red[(ih * kC + s) * DV + cc];
+            float acc = __expf(GC - tab.G[s]) * sum;
+            for (int r = s; r < kC; ++r) acc = fmaf(Suoa[r][s], dOs[r][cc], acc);
+            store_from_float(gv, (((size_t)b * p.T + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
+        }
+        // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i]
+        {
+            float dk_r[KH];
+            const float *src = p.DKe + (st + i) * DK + part * KH;
+#pragma unroll
+            for (int cc = 0; cc < KH; ++cc) dk_r[cc] = src[cc];
+            for (int s = 0; s < kC; ++s) {
+                float ps = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < KH; ++cc) ps = fmaf(Ks[s][part * KH + cc], dk_r[cc], ps);
+                ps += __shfl_xor(ps, 1);
+                if (part == 0) dAK[s][i] = __expf(GC - tab.G[s]) * ps;
+            }
+        }
+        {
+            float dv_r[VH];
+            const float *src = p.DVe + (st + i) * DV + part * VH;
+#pragma unroll
+            for (int cc = 0; cc < VH; ++cc) dv_r[cc] = src[cc];
+            for (int s = 0; s < kC; ++s) {
+                float ps = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < VH; ++cc) ps = fmaf(Vs[s][part * VH + cc], dv_r[cc], ps);
+                ps += __shfl_xor(ps, 1);
+                if (part == 0) dAV[s][i] = __expf(GC - tab.G[s]) * ps;
+            }
+        }
+        __syncthreads();
+        // da, intra-chunk parts; dAK then holds the whole da
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int s = e >> 7, ii = e & 127;
+            float av = dAV[s][ii], ak = dAK[s][ii];
+            for (int r = s; r < kC; ++r) {
+                av = fmaf(Sdov[r][s], Us[r][ii], av);
+                ak = fmaf(Sqk[r][s], dPs[r][ii], ak);
+            }
+            dAV[s][ii] = av;
+            dAK[s][ii] = ak + av;
+        }
+        __syncthreads();
+        // per token: dbeta, clock gradient of a, dL/dG; dq and dk rows out
+        for (int s = wave; s < kC; s += kNT / 64) {
+            const int t = t0 + s;
+            float qdq = 0.f, kdk = 0.f;
+            for (int cc = lane; cc < DK; cc += 64) {
+                qdq = fmaf(Qs[s][cc], gQ[s][cc], qdq);
+                kdk = fmaf(Ks[s][cc], gK[s][cc], kdk);
+            }
+            const float adav = As[s][lane] * dAV[s][lane] + As[s][lane + 64] * dAV[s][lane + 64];
+            // <da, U(-lambda) b>: DC entry and the (cos, -sin) pairs
+            float db = 0.f;
+            {
+                const int J = (m - 1) / 2, j = lane + 1;
+                if (j <= J) {
+                    const float2 cs = tab.cs[s][j - 1];
+                    db = sqrtf(2.f / (float)m) * (cs.x * dAK[s][2 * j - 1] - cs.y * dAK[s][2 * j]);
+                }
+                if (lane == 0) db += dAK[s][0] / sqrtf((float)m);
+            }
+            const float gl = rot_grad(dAK[s], As[s], m, -1.f, lane);
+            const float sums = wsum(qdq - kdk - adav);
+            db = wsum(db);
+            if (lane == 0 && t < p.T) {
+                const size_t ti = row0 + s;
+                const bool live = t < Tb;
+                p.dG[ti] = live ? sums + p.udu[ti] : 0.f;
+                p.dlam[ti] = live ? p.dlam[ti] + gl : 0.f;
+                if (p.gbeta) p.gbeta[((size_t)b * p.T + t) * p.H + h] = live ? db : 0.f;
+            }
+        }
+        for (int e = tid; e < kC * DK; e += kNT) {
+            const int r = e / DK, cc = e % DK;
+            const int t = t0 + r;
+            if (t >= p.T) continue;
+            const size_t gi = (((size_t)b * p.T + t) * p.H + h) * DK + cc;
+            store_from_float(gq, gi, t < Tb ? gQ[r][cc] : 0.f);
+            store_from_float(gk, gi, t < Tb ? gK[r][cc] : 0.f);
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// (5) reverse cumulative sums per sequence: dlog_alpha_t = sum_{tau >= t} dG_tau
+// (with the final-state term at the last token), ddelta_t = sum_{tau >= t}
+// dlambda_tau, dclock0 = sum_t dlambda_t.
+__global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
+    __shared__ double sG[kNT], sL[kNT];
+    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int Tb = bwd_tokens(p, b);
+    const float *dG = p.dG + (size_t)bh * p.Tpad;
+    const float *dl = p.dlam + (size_t)bh * p.Tpad;
+    const float fin = p.fin[bh];
+    const int per = (Tb + kNT - 1) / kNT;
+    const int t_lo = min(tid * per, Tb), t_hi = min(t_lo + per, Tb);
+    double aG = 0.0, aL = 0.0;
+    for (int t = t_lo; t < t_hi; ++t) {
+        aG += dG[t] + (t == Tb - 1 ? fin : 0.f);
+        aL += dl[t];
+    }
+    sG[tid] = aG;
+    sL[tid] = aL;
+    __syncthreads();
+    if (tid == 0) {
+        // exclusive suffix sums over the thread ranges
+        double rg = 0.0, rl = 0.0;
+        for (int u = kNT - 1; u >= 0; --u) {
+            const double g = sG[u], l = sL[u];
+            sG[u] = rg;
+            sL[u] = rl;
+            rg += g;
+            rl += l;
+        }
+        if (p.gclock0) p.gclock0[bh] = rl;
+    }
+    __syncthreads();
+    double rg = sG[tid], rl = sL[tid];
+    for (int t = t_hi - 1; t >= t_lo; --t) {
+        rg += dG[t] + (t == Tb - 1 ? fin : 0.f);
+        rl += dl[t];
+        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        if (p.glog_alpha) p.glog_alpha[si] = (float)rg;
+        p.gdelta[si] = (float)rl;
+    }
+    for (int t = Tb + tid; t < p.T; t += kNT) {
+        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        if (p.glog_alpha) p.glog_alpha[si] = 0.f;
+        p.gdelta[si] = 0.f;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// (6) dR_h = (sum over sequences b and chunk groups of dM) Phi^T on the active
+// m x m block (M = R Phi, Phi the real Fourier basis of App. A.1).
+__global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
+    __shared__ float dM[kStoreRows][kLD];
+    __shared__ float tab[2][kStoreRows];
+    const int h = blockIdx.x, tid = threadIdx.x, m = p.m;
+    const int nb = p.B * p.groups;
+    for (int e = tid; e < kStoreRows * kStoreRows; e += kNT) {
+        float s = 0.f;
+        for (int u = 0; u < nb; ++u) {
+            const int b = u / p.groups, g = u % p.groups;
+            s += p.dMp[(((size_t)(b * p.H + h) * p.groups + g) * kStoreRows) * kStoreRows + e];
+        }
+        dM[e >> 7][e & 127] = s;
+    }
+    if (tid < m) {
+        double sn, cs;
+        sincospi(2.0 * (double)tid / (double)m, &sn, &cs);
+        tab[0][tid] = (float)cs;
+        tab[1][tid] = (float)sn;
+    }
+    __syncthreads();
+    const float dc = 1.f / sqrtf((float)m), ac = sqrtf(2.f / (float)m);
+    for (int e = tid; e < m * m; e += kNT) {
+        const int ii = e / m, s = e % m;
+        float acc = dM[ii][0] * dc;
+        for (int l = 1; 2 * l < m; ++l) {
+            const int n = (l * s) % m;
+            acc = fmaf(dM[ii][2 * l - 1], ac * tab[0][n], acc);
+            acc = fmaf(dM[ii][2 * l], ac * tab[1][n], acc);
+        }
+        p.gR[((size_t)h * m + ii) * m + s] = acc;
+    }
+}
+
+template <int DK, int DV, typename Tin>
+hipError_t launch_typed(const BwdParams &p, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const dim3 block(kNT), seq(BH), grp(BH, p.groups);
+    hipLaunchKernelGGL((bwd_states_kernel<DK, DV, Tin>), seq, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_readout_kernel<DK, DV, Tin>), grp, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV, Tin>), seq, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_grad_kernel<DK, DV, Tin>), grp, block, 0, s, p);
+    hipLaunchKernelGGL(bwd_scan_kernel, seq, block, 0, s, p);
+    if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H), block, 0, s, p);
+    return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t launch_dtype(const BwdParams &p, hipStream_t s) {
+    return p.dtype == 0 ? launch_typed<DK, DV, float>(p, s) : launch_typed<DK, DV, __hip_bfloat16>(p, s);
+}
+
+size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
+
+}  // namespace
+
+int bwd_auto_groups(int B, int T, int H) {
+    const int nc = (T + kC - 1) / kC;
+    const int BH = B * H;
+    int g = (512 + BH - 1) / BH;
+    if (g > nc) g = nc;
+    return g < 1 ? 1 : g;
+}
+
+// Layout (each piece 256-byte aligned): M, Kst, Vst, clk, DKe, DVe, U, dP, udu,
+// dlam, dG, dMp, fin.
+size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups) {
+    const size_t BH = (size_t)B * H, nc = ((size_t)T + kC - 1) / kC, Tpad = nc * kC;
+    const size_t st = BH * nc * kStoreRows * (size_t)(dk + dv) * 4;
+    size_t n = align_up(readout_f32_bytes(H));
+    n += align_up(st);                                   // Kst + Vst
+    n += align_up(BH * nc * 8);                          // clk
+    n += align_up(st);                                   // DKe + DVe
+    n += 2 * align_up(BH * Tpad * kStoreRows * 4);       // U, dP
+    n += 3 * align_up(BH * Tpad * 4);                    // udu, dlam, dG
+    n += align_up(BH * (size_t)groups * kStoreRows * kStoreRows * 4);
+    n += align_up(BH * 4);
+    return n;
+}
+
+hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s) {
+    const size_t BH = (size_t)p.B * p.H, nc = p.nc, Tpad = p.Tpad;
+    char *w = static_cast<char *>(ws);
+    auto take = [&w](size_t bytes) { char *r = w; w += align_up(bytes); return r; };
+    float *M = reinterpret_cast<float *>(take(readout_f32_bytes(p.H)));
+    char *st = take(BH * nc * kStoreRows * (size_t)(p.dk + p.dv) * 4);
+    p.Kst = reinterpret_cast<float *>(st);
+    p.Vst = p.Kst + BH * nc * kStoreRows * p.dk;
+    p.clk = reinterpret_cast<double *>(take(BH * nc * 8));
+    char *ad = take(BH * nc * kStoreRows * (size_t)(p.dk + p.dv) * 4);
+    p.DKe = reinterpret_cast<float *>(ad);
+    p.DVe = p.DKe + BH * nc * kStoreRows * p.dk;
+    p.U = reinterpret_cast<float *>(take(BH * Tpad * kStoreRows * 4));
+    p.dP = reinterpret_cast<float *>(take(BH * Tpad * kStoreRows * 4));
+    p.udu = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dlam = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dG = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dMp = reinterpret_cast<float *>(take(BH * (size_t)p.groups * kStoreRows * kStoreRows * 4));
+    p.fin = reinterpret_cast<float *>(take(BH * 4));
+    p.M = M;
+    hipError_t e = launch_readout_prep(p.H, p.m, p.R, M, nullptr, 1.f, s);
+    if (e != hipSuccess) return e;
+    if (p.dk == 64 && p.dv == 64) return launch_dtype<64, 64>(p, s);
+    if (p.dk == 64 && p.dv == 128) return launch_dtype<64, 128>(p, s);
+    if (p.dk == 128 && p.dv == 64) return launch_dtype<128, 64>(p, s);
+    return launch_dtype<128, 128>(p, s);
+}
+
+}  // namespace cyfa

@@ -23,7 +23,7 @@ STORE_ROWS = 128
 
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
-            "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
+            "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
             "cyfa_status_string", "cyfa_last_error", "cyfa_version")
 
 
@@ -66,6 +66,11 @@ def load() -> ctypes.CDLL:
         lib.cyfa_forward.restype = ctypes.c_int
         lib.cyfa_forward_lens.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 17 + [ctypes.c_size_t, _vp]
         lib.cyfa_forward_lens.restype = ctypes.c_int
+        lib.cyfa_backward_workspace_size.argtypes = [ctypes.POINTER(FwdDesc),
+                                                     ctypes.POINTER(ctypes.c_size_t)]
+        lib.cyfa_backward_workspace_size.restype = ctypes.c_int
+        lib.cyfa_backward.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 25 + [ctypes.c_size_t, _vp]
+        lib.cyfa_backward.restype = ctypes.c_int
         lib.cyfa_decode_workspace_size.argtypes = [ctypes.POINTER(DecDesc),
                                                    ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_decode_workspace_size.restype = ctypes.c_int
@@ -203,6 +208,63 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
     if return_logits:
         res["logits"] = logits
     return res
+
+
+def backward_workspace_size(desc: FwdDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().cyfa_backward_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def backward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, d_o, scale=None, m=127,
+             K0=None, V0=None, clock0=None, dK_T=None, dV_T=None, lens=None, groups=0,
+             want_state_grads=True, workspace=None, stream=None):
+    """Gradients of sum <d_o, o> + <dK_T, K_out> + <dV_T, V_out> (cyfa_backward).
+
+    Inputs as for ``forward``; ``d_o`` [B,T,H,dv] in q's dtype; ``dK_T``/``dV_T``
+    [B,H,128,d] float32 or None.  Returns a dict with dq, dk, dv (q's dtype),
+    d_delta, d_log_alpha / d_beta (None when the input is None), d_R (None without
+    R) and, with ``want_state_grads``, d_K0, d_V0 [B,H,128,d] and d_clock0 [B,H].
+    """
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = _dtype_code(q)
+    _need(q, (B, T, H, dk), q.dtype, "q")
+    _need(k, (B, T, H, dk), q.dtype, "k")
+    _need(v, (B, T, H, dv), q.dtype, "v")
+    _need(d_o, (B, T, H, dv), q.dtype, "d_o")
+    for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
+        _need(t, (B, T, H), torch.float32, name)
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(K0, (B, H, STORE_ROWS, dk), torch.float32, "K0")
+    _need(V0, (B, H, STORE_ROWS, dv), torch.float32, "V0")
+    _need(dK_T, (B, H, STORE_ROWS, dk), torch.float32, "dK_T")
+    _need(dV_T, (B, H, STORE_ROWS, dv), torch.float32, "dV_T")
+    _need(clock0, (B, H), torch.float64, "clock0")
+    _need(lens, (B,), torch.int32, "lens")
+    desc = forward_desc(B, T, H, dk, dv, m=m, chunk=0, segments=groups, scale=scale, dtype=dt,
+                        kernel=KERNEL_VALU)
+    nbytes = backward_workspace_size(desc)
+    dev = q.device
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    e = lambda *shape, dtype=torch.float32: torch.empty(shape, dtype=dtype, device=dev)  # noqa: E731
+    g = {"dq": e(B, T, H, dk, dtype=q.dtype), "dk": e(B, T, H, dk, dtype=q.dtype),
+         "dv": e(B, T, H, dv, dtype=q.dtype), "d_delta": e(B, T, H),
+         "d_log_alpha": e(B, T, H) if log_alpha is not None else None,
+         "d_beta": e(B, T, H) if beta is not None else None,
+         "d_R": e(H, m, m) if R is not None else None,
+         "d_K0": e(B, H, STORE_ROWS, dk) if want_state_grads else None,
+         "d_V0": e(B, H, STORE_ROWS, dv) if want_state_grads else None,
+         "d_clock0": e(B, H, dtype=torch.float64) if want_state_grads else None}
+    st = load().cyfa_backward(
+        ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta), _ptr(log_alpha), _ptr(beta),
+        _ptr(R), _ptr(lens), _ptr(K0), _ptr(V0), _ptr(clock0), _ptr(d_o), _ptr(dK_T), _ptr(dV_T),
+        _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["d_delta"]), _ptr(g["d_log_alpha"]),
+        _ptr(g["d_beta"]), _ptr(g["d_R"]), _ptr(g["d_K0"]), _ptr(g["d_V0"]), _ptr(g["d_clock0"]),
+        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
+    _check(st)
+    return g
 
 
 def decode_desc(N, H, dk, dv, *, m=127, scale=None, dtype=F32) -> DecDesc:

@@ -110,3 +110,43 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cyfa, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         cyfa.load()
+
+
+def _call_backward(desc, ptrs, ws=0, ws_bytes=0):
+    lib = cyfa.load()
+    names = ("q", "k", "v", "delta", "log_alpha", "beta", "R", "lens", "K0", "V0", "clock0", "d_o",
+             "dK_T", "dV_T", "dq", "dk", "dv", "d_delta", "d_log_alpha", "d_beta", "d_R", "d_K0",
+             "d_V0", "d_clock0")
+    args = [ptrs.get(k) for k in names]
+    return lib.cyfa_backward(ctypes.byref(desc), *[ctypes.c_void_p(a) if a else None for a in args],
+                             ctypes.c_void_p(ws) if ws else None, ctypes.c_size_t(ws_bytes), None)
+
+
+def test_backward_workspace_and_descriptor_checks():
+    d = cyfa.forward_desc(4, 4096, 16, 128, 128, dtype=cyfa.BF16)
+    n = cyfa.backward_workspace_size(d)
+    # entering and adjoint states per 16-token chunk dominate: ~4.3 GB at this shape
+    assert 4.0e9 < n < 5.0e9
+    for field, value in (("d_k", 256), ("kernel", cyfa.KERNEL_MFMA), ("chunk", 32), ("m", 255)):
+        d = cyfa.forward_desc(1, 64, 2, 64, 64, dtype=cyfa.F32)
+        setattr(d, field, value)
+        with pytest.raises(cyfa.CyfaError) as ei:
+            cyfa.backward_workspace_size(d)
+        assert ei.value.status == 2, (field, ei.value)
+
+
+def test_backward_rejects_before_launch():
+    base = 1 << 40
+    slot = iter(range(1, 64))
+    good = {k: base + (next(slot) << 20) for k in ("q", "k", "v", "delta", "d_o", "dq", "dk", "dv",
+                                                   "d_delta")}
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, dtype=cyfa.F32)
+    need = cyfa.backward_workspace_size(d)
+    assert _call_backward(d, {k: v for k, v in good.items() if k != "d_o"}, base, need) == 1
+    assert _call_backward(d, dict(good, d_beta=base + (40 << 20)), base, need) == 1   # no beta
+    assert _call_backward(d, dict(good, d_R=base + (41 << 20)), base, need) == 1      # no R
+    assert _call_backward(d, dict(good, dq=good["dk"]), base, need) == 1             # aliasing
+    assert _call_backward(d, dict(good, dq=good["q"]), base, need) == 1
+    assert _call_backward(d, dict(good, q=base + 8), base, need) == 1                # misaligned
+    assert _call_backward(d, good, 0, 0) == 3
+    assert _call_backward(d, good, base, need - 1) == 3

@@ -1,0 +1,155 @@
+"""GPU parity of the backward (cyfa_backward) against the backward oracle.
+
+Every gradient tensor is compared element by element with the oracle's float64
+reverse-mode gradients on the same seeded inputs, the same upstream gradient
+d_o and the same final-state adjoints.  Error per tensor: max |x - y| / max |y|.
+Bars: 1e-4 for float32 inputs, 2e-2 for bfloat16 inputs (fp32 arithmetic).
+"""
+import numpy as np
+import pytest
+
+from oracle import backward as ob
+from paper_2609_36259_amd.inputs import make_forward_inputs
+from tests.harness import TOL_BF16, TOL_F32, rel_err, upload
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _cyfa():
+    from paper_2609_36259_amd import cyfa
+    return cyfa
+
+
+def _round(a, dtype):
+    if dtype != "bf16":
+        return np.asarray(a, np.float32)
+    return torch.tensor(np.asarray(a, np.float32)).bfloat16().float().numpy()
+
+
+def _extras(x, seed, init=True, final=True):
+    """Upstream gradient, initial states/clock and final-state adjoints."""
+    B, T, H = x["delta"].shape
+    dk, dv, m = x["q"].shape[-1], x["v"].shape[-1], x["m"]
+    rng = np.random.default_rng(seed)
+    e = {"do": _round(rng.standard_normal((B, T, H, dv)), x["dtype"])}
+    if init:
+        K0 = np.zeros((B, H, 128, dk), np.float32)
+        V0 = np.zeros((B, H, 128, dv), np.float32)
+        K0[:, :, :m] = 0.3 * rng.standard_normal((B, H, m, dk))
+        V0[:, :, :m] = 0.3 * rng.standard_normal((B, H, m, dv))
+        e.update(K0=K0, V0=V0, clock0=rng.uniform(0, 2 * m, (B, H)))
+    if final:
+        dK = np.zeros((B, H, 128, dk), np.float32)
+        dV = np.zeros((B, H, 128, dv), np.float32)
+        dK[:, :, :m] = rng.standard_normal((B, H, m, dk))
+        dV[:, :, :m] = rng.standard_normal((B, H, m, dv))
+        e.update(dK_T=dK, dV_T=dV)
+    return e
+
+
+def _run(x, e, lens=None, groups=0):
+    cyfa = _cyfa()
+    t = upload(x)
+    dt = t["q"].dtype
+    dev = lambda a, dtype=torch.float32: None if a is None else torch.tensor(a, dtype=dtype, device="cuda")  # noqa: E731
+    g = cyfa.backward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                      d_o=dev(e["do"], dt), scale=x["scale"], m=x["m"],
+                      K0=dev(e.get("K0")), V0=dev(e.get("V0")),
+                      clock0=dev(e.get("clock0"), torch.float64),
+                      dK_T=dev(e.get("dK_T")), dV_T=dev(e.get("dV_T")),
+                      lens=None if lens is None else dev(lens, torch.int32), groups=groups)
+    torch.cuda.synchronize()
+    return {k: (None if v is None else v.float().cpu().numpy() if v.dtype != torch.float64
+                else v.cpu().numpy()) for k, v in g.items()}
+
+
+def _oracle(x, e, lens=None):
+    return ob.backward(x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"],
+                       do=e["do"], m=x["m"], scale=x["scale"], K0=e.get("K0"), V0=e.get("V0"),
+                       clock0=e.get("clock0"), dK_T=e.get("dK_T"), dV_T=e.get("dV_T"), lens=lens)
+
+
+PAIRS = {"dq": "dq", "dk": "dk", "dv": "dv", "d_delta": "ddelta", "d_log_alpha": "dlog_alpha",
+         "d_beta": "dbeta", "d_R": "dR", "d_K0": "dK0", "d_V0": "dV0", "d_clock0": "dclock0"}
+
+
+def _compare(g, ref, tol, skip=()):
+    errs = {}
+    for gk, rk in PAIRS.items():
+        if gk in skip or ref.get(rk) is None:
+            continue
+        assert g[gk] is not None, gk
+        errs[gk] = rel_err(g[gk], ref[rk])
+    print("errors", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= tol, (k, v)
+    return errs
+
+
+@pytest.mark.parametrize("m", [7, 127])
+def test_f32_d64_full_parity(m):
+    x = make_forward_inputs(2, 45, 2, 64, 64, seed=71, dtype="f32", m=m)
+    e = _extras(x, 1)
+    _compare(_run(x, e), _oracle(x, e), TOL_F32)
+
+
+@pytest.mark.parametrize("dk,dv", [(128, 128), (64, 128), (128, 64)])
+def test_f32_head_dims(dk, dv):
+    x = make_forward_inputs(1, 37, 2, dk, dv, seed=72, dtype="f32")
+    e = _extras(x, 2)
+    _compare(_run(x, e), _oracle(x, e), TOL_F32)
+
+
+def test_bf16_d128():
+    x = make_forward_inputs(2, 50, 2, 128, 128, seed=73, dtype="bf16")
+    e = _extras(x, 3)
+    _compare(_run(x, e), _oracle(x, e), TOL_BF16)
+
+
+def test_absent_gates_readout_and_states():
+    x = make_forward_inputs(1, 40, 2, 64, 64, seed=74, dtype="f32", with_beta=False, with_R=False)
+    x["log_alpha"] = None
+    e = _extras(x, 4, init=False, final=False)
+    g = _run(x, e)
+    assert g["d_log_alpha"] is None and g["d_beta"] is None and g["d_R"] is None
+    _compare(g, _oracle(x, e), TOL_F32)
+
+
+def test_ragged_lengths():
+    x = make_forward_inputs(3, 40, 2, 64, 64, seed=75, dtype="f32")
+    e = _extras(x, 5)
+    lens = [40, 19, 0]
+    g = _run(x, e, lens=lens)
+    ref = _oracle(x, e, lens=lens)
+    _compare(g, ref, TOL_F32)
+    for name in ("dq", "dk", "dv", "d_delta", "d_log_alpha", "d_beta"):
+        assert np.all(g[name][1, 19:] == 0) and np.all(g[name][2] == 0), name
+
+
+def test_chunk_groups_change_only_rounding():
+    x = make_forward_inputs(1, 16 * 7 + 3, 2, 64, 64, seed=76, dtype="f32")
+    e = _extras(x, 6)
+    a = _run(x, e, groups=1)
+    b = _run(x, e, groups=3)
+    for k in PAIRS:
+        assert rel_err(b[k], a[k]) <= 1e-5, k
+
+
+def test_peaky_logits():
+    """A large logit scale makes the softmax far from uniform, so errors in the
+    readout's adjoint are not hidden by near-constant weights."""
+    x = make_forward_inputs(1, 33, 2, 64, 64, seed=77, dtype="f32")
+    x["scale"] = 12.0
+    e = _extras(x, 7)
+    _compare(_run(x, e), _oracle(x, e), TOL_F32)
+
+
+def test_empty_sequence_passes_state_adjoints_through():
+    x = make_forward_inputs(1, 0, 2, 64, 64, seed=78, dtype="f32")
+    e = _extras(x, 8)
+    g = _run(x, e)
+    np.testing.assert_array_equal(g["d_K0"], e["dK_T"])
+    np.testing.assert_array_equal(g["d_V0"], e["dV_T"])
+    assert np.all(g["d_clock0"] == 0)

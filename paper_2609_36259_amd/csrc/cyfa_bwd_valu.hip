@@ -105,8 +105,7 @@ __device__ void chunk_tables(const BwdParams &p, int b, int h, int t0, int Tb, d
     __syncthreads();
 }
 
-// Temporal write rows A_r = beta_r U(-lambda_r) b (Eq. app-temporal-writes);
-// with unit = true the same without beta (the direction dA is projected on for dbeta).
+// Temporal write rows A_r = beta_r U(-lambda_r) b (Eq. app-temporal-writes).
 __device__ __forceinline__ float write_entry(const ChunkTab &s, int m, int r, int i, float be) {
     if (i == 0) return be * (1.f / sqrtf((float)m));
     if (i >= m) return 0.f;
@@ -148,41 +147,82 @@ __device__ __forceinline__ float rot_grad(const float *dZ, const float *Z, int m
     return sign * (kTwoPi / (float)m) * wsum(acc);
 }
 
+// Products with the readout matrix over the m active entries, register-blocked:
+// thread (column col = tid % 128, rows 8 (tid / 128) .. + 7) keeps eight
+// independent sums.  TRANS = false: out_r = M in_r (out[r][i] = sum_j M[i][j] in[r][j]);
+// TRANS = true: out_r = M^T in_r.  Entries >= m of out are 0.
+template <bool TRANS>
+__device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], float (*out)[kLD], int m,
+                                int tid) {
+    const int col = tid & 127, r0 = (tid >> 7) * 8;
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    if (col < m) {
+        for (int j = 0; j < m; ++j) {
+            const float mv = TRANS ? Ms[j][col] : Ms[col][j];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[q] = fmaf(mv, in[r0 + q][j], acc[q]);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) out[r0 + q][col] = acc[q];
+}
+
+// out[r][i] += sum_s S[r][s] A[s][i] for a causal (lower-triangular) score tile S.
+__device__ void add_scores_times(const float (*S)[kC + 1], const float (*A)[kLD], float (*out)[kLD], int tid) {
+    const int col = tid & 127, r0 = (tid >> 7) * 8;
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = out[r0 + q][col];
+    for (int s = 0; s < r0 + 8; ++s) {
+        const float a = A[s][col];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] = fmaf(S[r0 + q][s], a, acc[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) out[r0 + q][col] = acc[q];
+}
+
 template <typename Tin>
 __device__ __forceinline__ float ld_row(const void *base, int b, int t, int h, int c, int T, int H, int D, bool live) {
     return live ? load_as_float(static_cast<const Tin *>(base), (((size_t)b * T + t) * H + h) * D + c) : 0.f;
 }
 
 // ---------------------------------------------------------------------------
-// (1) states entering every chunk.  Thread (i = tid / 2, part = tid % 2) keeps
-// row i, column half `part` of both states.
+// (1) states entering every chunk.  Thread t keeps column t % D of a state
+// and its rows (t / D) NR .. + NR - 1 (NR = D / 2), for the key state (D = d_k)
+// and the value state (D = d_v): a wave shares its rows, so the write rows are
+// broadcast reads and the stored state rows are coalesced.
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
-    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int NRK = DK / 2, NRV = DV / 2;
     __shared__ float Ks[kC][DK];
     __shared__ float Vs[kC][DV];
-    __shared__ float As[kC][kLD];
+    __shared__ __attribute__((aligned(16))) float Aw[kC][kStoreRows];   // rho_r A_r
     __shared__ ChunkTab tab;
     __shared__ float red[kNT / 64];
     const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
-    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int ck = tid % DK, rk = (tid / DK) * NRK;
+    const int cv = tid % DV, rv = (tid / DV) * NRV;
+    const int m = p.m;
     const int Tb = bwd_tokens(p, b);
-    float kst[KH], vst[VH];
+    float kst[NRK], vst[NRV];
 #pragma unroll
-    for (int c = 0; c < KH; ++c)
-        kst[c] = (p.K0 && i < m) ? p.K0[((size_t)bh * kStoreRows + i) * DK + part * KH + c] : 0.f;
+    for (int ii = 0; ii < NRK; ++ii)
+        kst[ii] = (p.K0 && rk + ii < m) ? p.K0[((size_t)bh * kStoreRows + rk + ii) * DK + ck] : 0.f;
 #pragma unroll
-    for (int c = 0; c < VH; ++c)
-        vst[c] = (p.V0 && i < m) ? p.V0[((size_t)bh * kStoreRows + i) * DV + part * VH + c] : 0.f;
+    for (int ii = 0; ii < NRV; ++ii)
+        vst[ii] = (p.V0 && rv + ii < m) ? p.V0[((size_t)bh * kStoreRows + rv + ii) * DV + cv] : 0.f;
     double lam = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
     for (int c = 0; c < p.nc; ++c) {
         const int t0 = c * kC;
-        float *Kd = p.Kst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
-        float *Vd = p.Vst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+        float *Kd = p.Kst + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
+        float *Vd = p.Vst + ((size_t)bh * p.nc + c) * kStoreRows * DV + cv;
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc) Kd[cc] = kst[cc];
+        for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = kst[ii];
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc) Vd[cc] = vst[cc];
+        for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = vst[ii];
         if (tid == 0) p.clk[(size_t)bh * p.nc + c] = lam;
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
@@ -193,33 +233,36 @@ __global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
             Vs[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
         }
         chunk_tables(p, b, h, t0, Tb, lam, tab, tid);
-        build_writes(tab, m, As, tid);
-        __syncthreads();
         const float GC = tab.G[kC - 1], gC = __expf(GC);
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, i = e & 127;
+            Aw[r][i] = write_entry(tab, m, r, i, tab.beta[r]) * __expf(GC - tab.G[r]);
+        }
+        __syncthreads();
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc) kst[cc] *= gC;
+        for (int ii = 0; ii < NRK; ++ii) kst[ii] *= gC;
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc) vst[cc] *= gC;
+        for (int ii = 0; ii < NRV; ++ii) vst[ii] *= gC;
         for (int r = 0; r < kC; ++r) {
-            const float w = As[r][i] * __expf(GC - tab.G[r]);
+            const float kr = Ks[r][ck], vr = Vs[r][cv];
 #pragma unroll
-            for (int cc = 0; cc < KH; ++cc) kst[cc] = fmaf(w, Ks[r][part * KH + cc], kst[cc]);
+            for (int ii = 0; ii < NRK; ++ii) kst[ii] = fmaf(Aw[r][rk + ii], kr, kst[ii]);
 #pragma unroll
-            for (int cc = 0; cc < VH; ++cc) vst[cc] = fmaf(w, Vs[r][part * VH + cc], vst[cc]);
+            for (int ii = 0; ii < NRV; ++ii) vst[ii] = fmaf(Aw[r][rv + ii], vr, vst[ii]);
         }
         lam = tab.lam[kC - 1];
         __syncthreads();
     }
     // <dK_T, Kbar_T> + <dV_T, Vbar_T>: the final-state term of dL/dG at the last token
     float acc = 0.f;
-    if (p.dK_T && i < m)
+    if (p.dK_T)
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc)
-            acc = fmaf(p.dK_T[((size_t)bh * kStoreRows + i) * DK + part * KH + cc], kst[cc], acc);
-    if (p.dV_T && i < m)
+        for (int ii = 0; ii < NRK; ++ii)
+            if (rk + ii < m) acc = fmaf(p.dK_T[((size_t)bh * kStoreRows + rk + ii) * DK + ck], kst[ii], acc);
+    if (p.dV_T)
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc)
-            acc = fmaf(p.dV_T[((size_t)bh * kStoreRows + i) * DV + part * VH + cc], vst[cc], acc);
+        for (int ii = 0; ii < NRV; ++ii)
+            if (rv + ii < m) acc = fmaf(p.dV_T[((size_t)bh * kStoreRows + rv + ii) * DV + cv], vst[ii], acc);
     acc = wsum(acc);
     if ((tid & 63) == 0) red[tid >> 6] = acc;
     __syncthreads();
@@ -265,6 +308,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
             if (s <= r) {
+#pragma unroll 4
                 for (int cc = 0; cc < DK; ++cc) acc = fmaf(In0[r][cc], In1[s][cc], acc);
                 acc *= __expf(tab.G[r] - tab.G[s]);
             }
@@ -285,12 +329,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // p += S1 A
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, ii = e & 127;
-            float acc = Xs[r][ii];
-            for (int s = 0; s <= r; ++s) acc = fmaf(S1[r][s], As[s][ii], acc);
-            Xs[r][ii] = acc;
-        }
+        add_scores_times(S1, As, Xs, tid);
         __syncthreads();
         for (int e = tid; e < kC * DV; e += kNT) {
             const int r = e / DV, cc = e % DV;
@@ -302,17 +341,12 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         rotate_rows(Xs, tab, m, 1.f, p.scale, tid);
         __syncthreads();
         // Z = M X (active slots), S2 = (dO V^T) (.) Gamma
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, ii = e & 127;
-            float acc = 0.f;
-            if (ii < m)
-                for (int j = 0; j < m; ++j) acc = fmaf(Ms[ii][j], Xs[r][j], acc);
-            Ws[r][ii] = acc;
-        }
+        readout_product<false>(Ms, Xs, Ws, m, tid);
         {
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
             if (s <= r) {
+#pragma unroll 4
                 for (int cc = 0; cc < DV; ++cc) acc = fmaf(In0[r][cc], In1[s][cc], acc);
                 acc *= __expf(tab.G[r] - tab.G[s]);
             }
@@ -332,13 +366,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // Y = M^T W
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, jj = e & 127;
-            float acc = 0.f;
-            if (jj < m)
-                for (int ii = 0; ii < m; ++ii) acc = fmaf(Ws[r][ii], Ms[ii][jj], acc);
-            Us[r][jj] = acc;
-        }
+        readout_product<true>(Ms, Ws, Us, m, tid);
         __syncthreads();
         // u = U(-lambda) Y;  du_r = gamma_r Vbar_c do_r (entering value state)
         rotate_rows(Us, tab, m, -1.f, 1.f, tid);
@@ -360,10 +388,8 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         for (int e = tid; e < kC * kStoreRows; e += kNT) {
             const int r = e >> 7, ii = e & 127;
             p.U[(row0 + r) * kStoreRows + ii] = Us[r][ii];
-            float acc = dUs[r][ii];
-            for (int s = 0; s <= r; ++s) acc = fmaf(S2[r][s], As[s][ii], acc);
-            dUs[r][ii] = acc;
         }
+        add_scores_times(S2, As, dUs, tid);
         __syncthreads();
         // <u, du> and the clock gradient of u = U(-lambda) Y
         for (int r = wave; r < kC; r += kNT / 64) {
@@ -379,13 +405,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         rotate_rows(dUs, tab, m, 1.f, 1.f, tid);
         __syncthreads();
         // dW = M dY;  dM += W dY^T
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, ii = e & 127;
-            float acc = 0.f;
-            if (ii < m)
-                for (int j = 0; j < m; ++j) acc = fmaf(Ms[ii][j], dUs[r][j], acc);
-            dWs[r][ii] = acc;
-        }
+        readout_product<false>(Ms, dUs, dWs, m, tid);
         for (int r = 0; r < kC; ++r) {
             const float w = Ws[r][i];
 #pragma unroll
@@ -408,13 +428,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
             for (int jj = 0; jj < 64; ++jj) dMacc[jj] = fmaf(dz, Xs[r][part * 64 + jj], dMacc[jj]);
         }
         __syncthreads();
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, jj = e & 127;
-            float acc = 0.f;
-            if (jj < m)
-                for (int ii = 0; ii < m; ++ii) acc = fmaf(dWs[r][ii], Ms[ii][jj], acc);
-            dUs[r][jj] = acc;
-        }
+        readout_product<true>(Ms, dWs, dUs, m, tid);
         __syncthreads();
         // clock gradient of X = scale U(lambda) p, plus that of u
         for (int r = wave; r < kC; r += kNT / 64) {
@@ -438,33 +452,36 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
 
 // ---------------------------------------------------------------------------
 // (3) adjoint states at every chunk's end, reverse over chunks; dK0, dV0.
+// Thread layout as in (1).
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
-    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int NRK = DK / 2, NRV = DV / 2;
     __shared__ float Qs[kC][DK];
     __shared__ float dOs[kC][DV];
-    __shared__ float dPs[kC][kStoreRows];
-    __shared__ float Us[kC][kStoreRows];
+    __shared__ __attribute__((aligned(16))) float Wp[kC][kStoreRows];   // gamma_r dp_r
+    __shared__ __attribute__((aligned(16))) float Wu[kC][kStoreRows];   // gamma_r u_r
     __shared__ float Gs[kC];
     const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
-    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int ck = tid % DK, rk = (tid / DK) * NRK;
+    const int cv = tid % DV, rv = (tid / DV) * NRV;
+    const int m = p.m;
     const int Tb = bwd_tokens(p, b);
-    float ak[KH], av[VH];
+    float ak[NRK], av[NRV];
 #pragma unroll
-    for (int c = 0; c < KH; ++c)
-        ak[c] = (p.dK_T && i < m) ? p.dK_T[((size_t)bh * kStoreRows + i) * DK + part * KH + c] : 0.f;
+    for (int ii = 0; ii < NRK; ++ii)
+        ak[ii] = (p.dK_T && rk + ii < m) ? p.dK_T[((size_t)bh * kStoreRows + rk + ii) * DK + ck] : 0.f;
 #pragma unroll
-    for (int c = 0; c < VH; ++c)
-        av[c] = (p.dV_T && i < m) ? p.dV_T[((size_t)bh * kStoreRows + i) * DV + part * VH + c] : 0.f;
+    for (int ii = 0; ii < NRV; ++ii)
+        av[ii] = (p.dV_T && rv + ii < m) ? p.dV_T[((size_t)bh * kStoreRows + rv + ii) * DV + cv] : 0.f;
     for (int c = p.nc - 1; c >= 0; --c) {
         const int t0 = c * kC;
         const size_t row0 = (size_t)bh * p.Tpad + t0;
-        float *Kd = p.DKe + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
-        float *Vd = p.DVe + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+        float *Kd = p.DKe + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
+        float *Vd = p.DVe + ((size_t)bh * p.nc + c) * kStoreRows * DV + cv;
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc) Kd[cc] = ak[cc];
+        for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = ak[ii];
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc) Vd[cc] = av[cc];
+        for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = av[ii];
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
@@ -472,11 +489,6 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
         for (int e = tid; e < kC * DV; e += kNT) {
             const int r = e / DV, cc = e % DV;
             dOs[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
-        }
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
-            const int r = e >> 7, ii = e & 127;
-            dPs[r][ii] = p.dP[(row0 + r) * kStoreRows + ii];
-            Us[r][ii] = p.U[(row0 + r) * kStoreRows + ii];
         }
         if (tid < kC) {
             const int t = t0 + tid;
@@ -486,29 +498,35 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
         if (tid == 0)
             for (int r = 1; r < kC; ++r) Gs[r] += Gs[r - 1];
         __syncthreads();
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, ii = e & 127;
+            const float gr = __expf(Gs[r]);
+            Wp[r][ii] = gr * p.dP[(row0 + r) * kStoreRows + ii];
+            Wu[r][ii] = gr * p.U[(row0 + r) * kStoreRows + ii];
+        }
+        __syncthreads();
         const float gC = __expf(Gs[kC - 1]);
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc) ak[cc] *= gC;
+        for (int ii = 0; ii < NRK; ++ii) ak[ii] *= gC;
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc) av[cc] *= gC;
+        for (int ii = 0; ii < NRV; ++ii) av[ii] *= gC;
         for (int r = 0; r < kC; ++r) {
-            const float gr = __expf(Gs[r]);
-            const float wk = gr * dPs[r][i], wv = gr * Us[r][i];
+            const float qr = Qs[r][ck], dor = dOs[r][cv];
 #pragma unroll
-            for (int cc = 0; cc < KH; ++cc) ak[cc] = fmaf(wk, Qs[r][part * KH + cc], ak[cc]);
+            for (int ii = 0; ii < NRK; ++ii) ak[ii] = fmaf(Wp[r][rk + ii], qr, ak[ii]);
 #pragma unroll
-            for (int cc = 0; cc < VH; ++cc) av[cc] = fmaf(wv, dOs[r][part * VH + cc], av[cc]);
+            for (int ii = 0; ii < NRV; ++ii) av[ii] = fmaf(Wu[r][rv + ii], dor, av[ii]);
         }
         __syncthreads();
     }
     if (p.gK0)
 #pragma unroll
-        for (int cc = 0; cc < KH; ++cc)
-            p.gK0[((size_t)bh * kStoreRows + i) * DK + part * KH + cc] = i < m ? ak[cc] : 0.f;
+        for (int ii = 0; ii < NRK; ++ii)
+            p.gK0[((size_t)bh * kStoreRows + rk + ii) * DK + ck] = rk + ii < m ? ak[ii] : 0.f;
     if (p.gV0)
 #pragma unroll
-        for (int cc = 0; cc < VH; ++cc)
-            p.gV0[((size_t)bh * kStoreRows + i) * DV + part * VH + cc] = i < m ? av[cc] : 0.f;
+        for (int ii = 0; ii < NRV; ++ii)
+            p.gV0[((size_t)bh * kStoreRows + rv + ii) * DV + cv] = rv + ii < m ? av[ii] : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -564,8 +582,11 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
             if (s <= r) {
                 const float gam = __expf(tab.G[r] - tab.G[s]);
+#pragma unroll 4
                 for (int cc = 0; cc < DK; ++cc) a0 = fmaf(Qs[r][cc], Ks[s][cc], a0);
+#pragma unroll 4
                 for (int cc = 0; cc < DV; ++cc) a1 = fmaf(dOs[r][cc], Vs[s][cc], a1);
+#pragma unroll 4
                 for (int ii = 0; ii < kStoreRows; ++ii) {
                     a2 = fmaf(dPs[r][ii], As[s][ii], a2);
                     a3 = fmaf(Us[r][ii], As[s][ii], a3);
@@ -653,31 +674,44 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             for (int r = s; r < kC; ++r) acc = fmaf(Suoa[r][s], dOs[r][cc], acc);
             store_from_float(gv, (((size_t)b * p.T + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
         }
-        // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i]
+        // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i];
+        // thread (row i, half part) sums its half of the columns for every token s
         {
-            float dk_r[KH];
-            const float *src = p.DKe + (st + i) * DK + part * KH;
+            float ak[kC], av[kC];
 #pragma unroll
-            for (int cc = 0; cc < KH; ++cc) dk_r[cc] = src[cc];
-            for (int s = 0; s < kC; ++s) {
-                float ps = 0.f;
-#pragma unroll
-                for (int cc = 0; cc < KH; ++cc) ps = fmaf(Ks[s][part * KH + cc], dk_r[cc], ps);
-                ps += __shfl_xor(ps, 1);
-                if (part == 0) dAK[s][i] = __expf(GC - tab.G[s]) * ps;
+            for (int s2 = 0; s2 < kC; ++s2) {
+                ak[s2] = 0.f;
+                av[s2] = 0.f;
             }
-        }
-        {
-            float dv_r[VH];
-            const float *src = p.DVe + (st + i) * DV + part * VH;
+            const float *dkr = p.DKe + (st + i) * DK + part * KH;
+#pragma unroll 1
+            for (int cc = 0; cc < KH; cc += 4) {
+                const float4 d = *reinterpret_cast<const float4 *>(dkr + cc);
 #pragma unroll
-            for (int cc = 0; cc < VH; ++cc) dv_r[cc] = src[cc];
-            for (int s = 0; s < kC; ++s) {
-                float ps = 0.f;
+                for (int s2 = 0; s2 < kC; ++s2) {
+                    const float *kk = &Ks[s2][part * KH + cc];
+                    ak[s2] = fmaf(kk[0], d.x, fmaf(kk[1], d.y, fmaf(kk[2], d.z, fmaf(kk[3], d.w, ak[s2]))));
+                }
+            }
+            const float *dvr = p.DVe + (st + i) * DV + part * VH;
+#pragma unroll 1
+            for (int cc = 0; cc < VH; cc += 4) {
+                const float4 d = *reinterpret_cast<const float4 *>(dvr + cc);
 #pragma unroll
-                for (int cc = 0; cc < VH; ++cc) ps = fmaf(Vs[s][part * VH + cc], dv_r[cc], ps);
-                ps += __shfl_xor(ps, 1);
-                if (part == 0) dAV[s][i] = __expf(GC - tab.G[s]) * ps;
+                for (int s2 = 0; s2 < kC; ++s2) {
+                    const float *vv = &Vs[s2][part * VH + cc];
+                    av[s2] = fmaf(vv[0], d.x, fmaf(vv[1], d.y, fmaf(vv[2], d.z, fmaf(vv[3], d.w, av[s2]))));
+                }
+            }
+#pragma unroll
+            for (int s2 = 0; s2 < kC; ++s2) {
+                const float a = ak[s2] + __shfl_xor(ak[s2], 1);
+                const float bv = av[s2] + __shfl_xor(av[s2], 1);
+                if (part == 0) {
+                    const float rho = __expf(GC - tab.G[s2]);
+                    dAK[s2][i] = rho * a;
+                    dAV[s2][i] = rho * bv;
+                }
             }
         }
         __syncthreads();
@@ -786,19 +820,22 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
 
 // ---------------------------------------------------------------------------
 // (6) dR_h = (sum over sequences b and chunk groups of dM) Phi^T on the active
-// m x m block (M = R Phi, Phi the real Fourier basis of App. A.1).
+// m x m block (M = R Phi, Phi the real Fourier basis of App. A.1).  Workgroup
+// (h, row block) handles kDRRows rows of dR, which need the same rows of dM only.
+constexpr int kDRRows = 8;
 __global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
-    __shared__ float dM[kStoreRows][kLD];
+    __shared__ float dM[kDRRows][kLD];
     __shared__ float tab[2][kStoreRows];
-    const int h = blockIdx.x, tid = threadIdx.x, m = p.m;
+    const int h = blockIdx.x, i0 = blockIdx.y * kDRRows, tid = threadIdx.x, m = p.m;
     const int nb = p.B * p.groups;
-    for (int e = tid; e < kStoreRows * kStoreRows; e += kNT) {
+    for (int e = tid; e < kDRRows * kStoreRows; e += kNT) {
+        const int ii = e >> 7, j = e & 127;
         float s = 0.f;
         for (int u = 0; u < nb; ++u) {
             const int b = u / p.groups, g = u % p.groups;
-            s += p.dMp[(((size_t)(b * p.H + h) * p.groups + g) * kStoreRows) * kStoreRows + e];
+            s += p.dMp[(((size_t)(b * p.H + h) * p.groups + g) * kStoreRows + i0 + ii) * kStoreRows + j];
         }
-        dM[e >> 7][e & 127] = s;
+        dM[ii][j] = s;
     }
     if (tid < m) {
         double sn, cs;
@@ -808,15 +845,16 @@ __global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
     }
     __syncthreads();
     const float dc = 1.f / sqrtf((float)m), ac = sqrtf(2.f / (float)m);
-    for (int e = tid; e < m * m; e += kNT) {
+    for (int e = tid; e < kDRRows * m; e += kNT) {
         const int ii = e / m, s = e % m;
+        if (i0 + ii >= m) continue;
         float acc = dM[ii][0] * dc;
         for (int l = 1; 2 * l < m; ++l) {
             const int n = (l * s) % m;
             acc = fmaf(dM[ii][2 * l - 1], ac * tab[0][n], acc);
             acc = fmaf(dM[ii][2 * l], ac * tab[1][n], acc);
         }
-        p.gR[((size_t)h * m + ii) * m + s] = acc;
+        p.gR[((size_t)h * m + i0 + ii) * m + s] = acc;
     }
 }
 
@@ -829,7 +867,7 @@ hipError_t launch_typed(const BwdParams &p, hipStream_t s) {
     hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV, Tin>), seq, block, 0, s, p);
     hipLaunchKernelGGL((bwd_grad_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL(bwd_scan_kernel, seq, block, 0, s, p);
-    if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H), block, 0, s, p);
+    if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H, kStoreRows / kDRRows), block, 0, s, p);
     return hipGetLastError();
 }
 

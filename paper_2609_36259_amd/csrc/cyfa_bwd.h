@@ -26,13 +26,21 @@ struct BwdParams {
     double *gclock0;
     // workspace (see bwd_workspace_bytes)
     const float *M;                 // [H][128][128] readout matrix R Phi
-    float *Kst, *Vst;               // [BH][nc][128][d] states entering each chunk
+    // States entering chunk c of group g: Kst[c] + exp(Gin[c]) Ecar[g] (Kst from
+    // the group's own tokens, Ecar the state entering the group).  Adjoint states
+    // at chunk c's end: DKe[c] + exp(Gout[c]) Acar[g] (Acar: the adjoint at the
+    // group's end from later groups and the final-state loss).
+    float *Kst, *Vst;               // [BH][nc][128][d]
     double *clk;                    // [BH][nc] clock entering each chunk (reduced mod m)
-    float *DKe, *DVe;               // [BH][nc][128][d] adjoint states at each chunk's end
+    float *DKe, *DVe;               // [BH][nc][128][d]
+    float *EcK, *EcV;               // [BH][groups][128][d]
+    float *AcK, *AcV;               // [BH][groups][128][d]
+    float *Gin, *Gout;              // [BH][nc] log decay from the group start / to the group end
+    float *Gg;                      // [BH][groups] log decay over each group
     float *U, *dP;                  // [BH][Tpad][128] readout output u_t and key-pass adjoint dp_t
     float *udu, *dlam, *dG;         // [BH][Tpad] <u_t, du_t>, dL/dlambda_t, dL/dG_t
     float *dMp;                     // [BH][groups][128][128] partial dL/dM
-    float *fin;                     // [BH] <dK_T, Kbar_T> + <dV_T, Vbar_T>
+    float *fin;                     // [BH][8] partial sums of <dK_T, Kbar_T> + <dV_T, Vbar_T>
 };
 
 size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups);

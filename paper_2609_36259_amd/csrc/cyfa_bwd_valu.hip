@@ -32,10 +32,13 @@
 //   dk = (dP A^T (.) Gamma)^T Q + (rho (.) A) DK'
 //   dv = (U A^T (.) Gamma)^T dO + (rho (.) A) DV'
 //   da = (Q K^T (.) Gamma)^T dP + rho (.) K DK'^T + (dO V^T (.) Gamma)^T U + rho (.) V DV'^T
-// Kernels: (1) states entering every chunk, per sequence; (2) readout
-// recomputation and its adjoint, per chunk group; (3) adjoint states at every
-// chunk's end, per sequence, in reverse; (4) token gradients, per chunk group;
-// (5) reverse cumulative sums, per sequence; (6) dR, per head.
+// Kernels: (1a) states entering every chunk from the chunk group's own tokens,
+// per chunk group, and (1b) the states entering every group, per sequence; (2)
+// readout recomputation and its adjoint, per chunk group; (3a, 3b) the same
+// split for the adjoint states at every chunk's end, in reverse; (4) token
+// gradients, per chunk group; (5) reverse cumulative sums, per sequence; (6)
+// dR, per head.  The states are in absolute-clock coordinates, so a group's
+// entering state reaches its chunks through the decay alone.
 #include "cyfa_bwd.h"
 
 namespace cyfa {
@@ -44,8 +47,9 @@ namespace {
 
 constexpr int kC = kBwdChunk;
 constexpr int kNT = 256;            // threads per workgroup
-constexpr int kLD = kStoreRows + 1; // padded row of a [token][basis] tile
+constexpr int kLD = kStoreRows + 4; // padded row of a [token][basis] tile (16-byte rows)
 constexpr float kTwoPi = 6.283185307179586f;
+constexpr int kCombBlocks = 8;      // workgroups per sequence of the group-combine kernels
 
 __device__ __forceinline__ float wsum(float x) {
 #pragma unroll
@@ -159,10 +163,20 @@ __device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], 
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = 0.f;
     if (col < m) {
-        for (int j = 0; j < m; ++j) {
-            const float mv = TRANS ? Ms[j][col] : Ms[col][j];
+        // four entries per step (16-byte rows; entries m .. 127 of in are 0, and M
+        // is 0 outside its active block, so running to a multiple of four is exact)
+        for (int j = 0; j < m; j += 4) {
+            float4 mv;
+            if (TRANS) {
+                mv = make_float4(Ms[j][col], Ms[j + 1][col], Ms[j + 2][col], Ms[j + 3][col]);
+            } else {
+                mv = *reinterpret_cast<const float4 *>(&Ms[col][j]);
+            }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) acc[q] = fmaf(mv, in[r0 + q][j], acc[q]);
+            for (int q = 0; q < 8; ++q) {
+                const float4 x = *reinterpret_cast<const float4 *>(&in[r0 + q][j]);
+                acc[q] = fmaf(mv.x, x.x, fmaf(mv.y, x.y, fmaf(mv.z, x.z, fmaf(mv.w, x.w, acc[q]))));
+            }
         }
     }
 #pragma unroll
@@ -190,32 +204,46 @@ __device__ __forceinline__ float ld_row(const void *base, int b, int t, int h, i
 }
 
 // ---------------------------------------------------------------------------
-// (1) states entering every chunk.  Thread t keeps column t % D of a state
-// and its rows (t / D) NR .. + NR - 1 (NR = D / 2), for the key state (D = d_k)
-// and the value state (D = d_v): a wave shares its rows, so the write rows are
-// broadcast reads and the stored state rows are coalesced.
+// (1a) states entering every chunk from the chunk group's own tokens (the
+// group starts from zero), per (sequence, group).  Thread t keeps column t % D
+// of a state and its rows (t / D) NR .. + NR - 1 (NR = D / 2), for the key
+// state (D = d_k) and the value state (D = d_v): a wave shares its rows, so the
+// write rows are broadcast reads and the stored state rows are coalesced.  The
+// group's own final state goes to EcK/EcV[g], its total log decay to Gg.
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
+__global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
     constexpr int NRK = DK / 2, NRV = DV / 2;
     __shared__ float Ks[kC][DK];
     __shared__ float Vs[kC][DV];
     __shared__ __attribute__((aligned(16))) float Aw[kC][kStoreRows];   // rho_r A_r
     __shared__ ChunkTab tab;
-    __shared__ float red[kNT / 64];
-    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    __shared__ double dred[kNT];
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int ck = tid % DK, rk = (tid / DK) * NRK;
     const int cv = tid % DV, rv = (tid / DV) * NRV;
     const int m = p.m;
     const int Tb = bwd_tokens(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    // clock at the group's first token: lambda_0 plus the increments before it
+    {
+        const int t_start = min(c_begin * kC, Tb);
+        double ds = 0.0;
+        for (int t = tid; t < t_start; t += kNT) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
+        dred[tid] = ds;
+        __syncthreads();
+        for (int w = kNT / 2; w > 0; w >>= 1) {
+            if (tid < w) dred[tid] += dred[tid + w];
+            __syncthreads();
+        }
+    }
+    double lam = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + dred[0], m);
     float kst[NRK], vst[NRV];
 #pragma unroll
-    for (int ii = 0; ii < NRK; ++ii)
-        kst[ii] = (p.K0 && rk + ii < m) ? p.K0[((size_t)bh * kStoreRows + rk + ii) * DK + ck] : 0.f;
+    for (int ii = 0; ii < NRK; ++ii) kst[ii] = 0.f;
 #pragma unroll
-    for (int ii = 0; ii < NRV; ++ii)
-        vst[ii] = (p.V0 && rv + ii < m) ? p.V0[((size_t)bh * kStoreRows + rv + ii) * DV + cv] : 0.f;
-    double lam = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
-    for (int c = 0; c < p.nc; ++c) {
+    for (int ii = 0; ii < NRV; ++ii) vst[ii] = 0.f;
+    float Gl = 0.f;
+    for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC;
         float *Kd = p.Kst + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
         float *Vd = p.Vst + ((size_t)bh * p.nc + c) * kStoreRows * DV + cv;
@@ -223,7 +251,10 @@ __global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
         for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = kst[ii];
 #pragma unroll
         for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = vst[ii];
-        if (tid == 0) p.clk[(size_t)bh * p.nc + c] = lam;
+        if (tid == 0) {
+            p.clk[(size_t)bh * p.nc + c] = lam;
+            p.Gin[(size_t)bh * p.nc + c] = Gl;
+        }
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             Ks[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
@@ -251,22 +282,55 @@ __global__ __launch_bounds__(kNT) void bwd_states_kernel(BwdParams p) {
             for (int ii = 0; ii < NRV; ++ii) vst[ii] = fmaf(Aw[r][rv + ii], vr, vst[ii]);
         }
         lam = tab.lam[kC - 1];
+        Gl += GC;
         __syncthreads();
     }
-    // <dK_T, Kbar_T> + <dV_T, Vbar_T>: the final-state term of dL/dG at the last token
+    float *Ko = p.EcK + ((size_t)bh * p.groups + g) * kStoreRows * DK + ck;
+    float *Vo = p.EcV + ((size_t)bh * p.groups + g) * kStoreRows * DV + cv;
+#pragma unroll
+    for (int ii = 0; ii < NRK; ++ii) Ko[(size_t)(rk + ii) * DK] = kst[ii];
+#pragma unroll
+    for (int ii = 0; ii < NRV; ++ii) Vo[(size_t)(rv + ii) * DV] = vst[ii];
+    if (tid == 0) p.Gg[(size_t)bh * p.groups + g] = Gl;
+}
+
+// (1b) states entering each group, per sequence, in group order:
+// E_0 = (K0, V0), E_{g+1} = exp(Gg_g) E_g + (group g's own final state); EcK/EcV[g]
+// are overwritten with E_g.  The final state gives <dK_T, Kbar_T> + <dV_T, Vbar_T>,
+// the final-state term of dL/dG at the last token.
+template <int DK, int DV>
+__global__ __launch_bounds__(kNT) void bwd_states_combine_kernel(BwdParams p) {
+    __shared__ float red[kNT / 64];
+    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
+    const int e0 = blockIdx.y * kNT + tid, es = kCombBlocks * kNT;
+    const float *Gg = p.Gg + (size_t)bh * G;
     float acc = 0.f;
-    if (p.dK_T)
-#pragma unroll
-        for (int ii = 0; ii < NRK; ++ii)
-            if (rk + ii < m) acc = fmaf(p.dK_T[((size_t)bh * kStoreRows + rk + ii) * DK + ck], kst[ii], acc);
-    if (p.dV_T)
-#pragma unroll
-        for (int ii = 0; ii < NRV; ++ii)
-            if (rv + ii < m) acc = fmaf(p.dV_T[((size_t)bh * kStoreRows + rv + ii) * DV + cv], vst[ii], acc);
+    for (int e = e0; e < kStoreRows * DK; e += es) {
+        const bool act = e / DK < m;
+        float E = (p.K0 && act) ? p.K0[(size_t)bh * kStoreRows * DK + e] : 0.f;
+        for (int g = 0; g < G; ++g) {
+            float *slot = p.EcK + ((size_t)bh * G + g) * kStoreRows * DK + e;
+            const float own = *slot;
+            *slot = E;
+            E = fmaf(__expf(Gg[g]), E, own);
+        }
+        if (p.dK_T && act) acc = fmaf(p.dK_T[(size_t)bh * kStoreRows * DK + e], E, acc);
+    }
+    for (int e = e0; e < kStoreRows * DV; e += es) {
+        const bool act = e / DV < m;
+        float E = (p.V0 && act) ? p.V0[(size_t)bh * kStoreRows * DV + e] : 0.f;
+        for (int g = 0; g < G; ++g) {
+            float *slot = p.EcV + ((size_t)bh * G + g) * kStoreRows * DV + e;
+            const float own = *slot;
+            *slot = E;
+            E = fmaf(__expf(Gg[g]), E, own);
+        }
+        if (p.dV_T && act) acc = fmaf(p.dV_T[(size_t)bh * kStoreRows * DV + e], E, acc);
+    }
     acc = wsum(acc);
     if ((tid & 63) == 0) red[tid >> 6] = acc;
     __syncthreads();
-    if (tid == 0) p.fin[bh] = red[0] + red[1] + red[2] + red[3];
+    if (tid == 0) p.fin[(size_t)bh * kCombBlocks + blockIdx.y] = red[0] + red[1] + red[2] + red[3];
 }
 
 // ---------------------------------------------------------------------------
@@ -275,10 +339,11 @@ template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
     constexpr int KH = DK / 2, VH = DV / 2;
     constexpr int DM = DK > DV ? DK : DV;
-    __shared__ float Ms[kStoreRows][kLD];
+    __shared__ __attribute__((aligned(16))) float Ms[kStoreRows][kLD];
     __shared__ float In0[kC][DM + 1];       // Q, then dO
     __shared__ float In1[kC][DM + 1];       // K, then V
-    __shared__ float As[kC][kLD], Xs[kC][kLD], Ws[kC][kLD], Us[kC][kLD], dUs[kC][kLD], dWs[kC][kLD];
+    __shared__ __attribute__((aligned(16))) float As[kC][kLD], Xs[kC][kLD], Ws[kC][kLD], Us[kC][kLD],
+        dUs[kC][kLD], dWs[kC][kLD];
     __shared__ float S1[kC][kC + 1], S2[kC][kC + 1];
     __shared__ ChunkTab tab;
     __shared__ float dlu[kC];
@@ -316,9 +381,11 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         {   // p_r = gamma_r Kbar_c q_r (entering key state)
             const float *Kc = p.Kst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DK + part * KH;
+            const float *Ke = p.EcK + (((size_t)bh * p.groups + g) * kStoreRows + i) * DK + part * KH;
+            const float dec = __expf(p.Gin[(size_t)bh * p.nc + c]);
             float kr[KH];
 #pragma unroll
-            for (int cc = 0; cc < KH; ++cc) kr[cc] = Kc[cc];
+            for (int cc = 0; cc < KH; ++cc) kr[cc] = fmaf(dec, Ke[cc], Kc[cc]);
             for (int r = 0; r < kC; ++r) {
                 float ps = 0.f;
 #pragma unroll
@@ -372,9 +439,11 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         rotate_rows(Us, tab, m, -1.f, 1.f, tid);
         {
             const float *Vc = p.Vst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
+            const float *Ve = p.EcV + (((size_t)bh * p.groups + g) * kStoreRows + i) * DV + part * VH;
+            const float dec = __expf(p.Gin[(size_t)bh * p.nc + c]);
             float vr[VH];
 #pragma unroll
-            for (int cc = 0; cc < VH; ++cc) vr[cc] = Vc[cc];
+            for (int cc = 0; cc < VH; ++cc) vr[cc] = fmaf(dec, Ve[cc], Vc[cc]);
             for (int r = 0; r < kC; ++r) {
                 float ps = 0.f;
 #pragma unroll
@@ -451,29 +520,30 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// (3) adjoint states at every chunk's end, reverse over chunks; dK0, dV0.
-// Thread layout as in (1).
+// (3a) adjoint states at every chunk's end from the chunk group's own later
+// tokens (zero at the group's end), reverse over the group's chunks, per
+// (sequence, group).  Thread layout as in (1a).  The adjoint of the state
+// entering the group goes to AcK/AcV[g].
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
+__global__ __launch_bounds__(kNT) void bwd_adjoint_local_kernel(BwdParams p) {
     constexpr int NRK = DK / 2, NRV = DV / 2;
     __shared__ float Qs[kC][DK];
     __shared__ float dOs[kC][DV];
     __shared__ __attribute__((aligned(16))) float Wp[kC][kStoreRows];   // gamma_r dp_r
     __shared__ __attribute__((aligned(16))) float Wu[kC][kStoreRows];   // gamma_r u_r
     __shared__ float Gs[kC];
-    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int ck = tid % DK, rk = (tid / DK) * NRK;
     const int cv = tid % DV, rv = (tid / DV) * NRV;
-    const int m = p.m;
     const int Tb = bwd_tokens(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
     float ak[NRK], av[NRV];
 #pragma unroll
-    for (int ii = 0; ii < NRK; ++ii)
-        ak[ii] = (p.dK_T && rk + ii < m) ? p.dK_T[((size_t)bh * kStoreRows + rk + ii) * DK + ck] : 0.f;
+    for (int ii = 0; ii < NRK; ++ii) ak[ii] = 0.f;
 #pragma unroll
-    for (int ii = 0; ii < NRV; ++ii)
-        av[ii] = (p.dV_T && rv + ii < m) ? p.dV_T[((size_t)bh * kStoreRows + rv + ii) * DV + cv] : 0.f;
-    for (int c = p.nc - 1; c >= 0; --c) {
+    for (int ii = 0; ii < NRV; ++ii) av[ii] = 0.f;
+    float Go = 0.f;
+    for (int c = c_end - 1; c >= c_begin; --c) {
         const int t0 = c * kC;
         const size_t row0 = (size_t)bh * p.Tpad + t0;
         float *Kd = p.DKe + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
@@ -482,6 +552,7 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
         for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = ak[ii];
 #pragma unroll
         for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = av[ii];
+        if (tid == 0) p.Gout[(size_t)bh * p.nc + c] = Go;
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
@@ -517,16 +588,48 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_kernel(BwdParams p) {
 #pragma unroll
             for (int ii = 0; ii < NRV; ++ii) av[ii] = fmaf(Wu[r][rv + ii], dor, av[ii]);
         }
+        Go += Gs[kC - 1];
         __syncthreads();
     }
-    if (p.gK0)
+    float *Ko = p.AcK + ((size_t)bh * p.groups + g) * kStoreRows * DK + ck;
+    float *Vo = p.AcV + ((size_t)bh * p.groups + g) * kStoreRows * DV + cv;
 #pragma unroll
-        for (int ii = 0; ii < NRK; ++ii)
-            p.gK0[((size_t)bh * kStoreRows + rk + ii) * DK + ck] = rk + ii < m ? ak[ii] : 0.f;
-    if (p.gV0)
+    for (int ii = 0; ii < NRK; ++ii) Ko[(size_t)(rk + ii) * DK] = ak[ii];
 #pragma unroll
-        for (int ii = 0; ii < NRV; ++ii)
-            p.gV0[((size_t)bh * kStoreRows + rv + ii) * DV + cv] = rv + ii < m ? av[ii] : 0.f;
+    for (int ii = 0; ii < NRV; ++ii) Vo[(size_t)(rv + ii) * DV] = av[ii];
+}
+
+// (3b) adjoints at each group's end, per sequence, in reverse group order:
+// A_{G-1} = (dK_T, dV_T), A_{g-1} = exp(Gg_g) A_g + (group g's own adjoint of its
+// entering state); AcK/AcV[g] are overwritten with A_g, and the adjoint of the
+// initial state is dK0, dV0.
+template <int DK, int DV>
+__global__ __launch_bounds__(kNT) void bwd_adjoint_combine_kernel(BwdParams p) {
+    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
+    const int e0 = blockIdx.y * kNT + tid, es = kCombBlocks * kNT;
+    const float *Gg = p.Gg + (size_t)bh * G;
+    for (int e = e0; e < kStoreRows * DK; e += es) {
+        const bool act = e / DK < m;
+        float A = (p.dK_T && act) ? p.dK_T[(size_t)bh * kStoreRows * DK + e] : 0.f;
+        for (int g = G - 1; g >= 0; --g) {
+            float *slot = p.AcK + ((size_t)bh * G + g) * kStoreRows * DK + e;
+            const float own = *slot;
+            *slot = A;
+            A = fmaf(__expf(Gg[g]), A, own);
+        }
+        if (p.gK0) p.gK0[(size_t)bh * kStoreRows * DK + e] = act ? A : 0.f;
+    }
+    for (int e = e0; e < kStoreRows * DV; e += es) {
+        const bool act = e / DV < m;
+        float A = (p.dV_T && act) ? p.dV_T[(size_t)bh * kStoreRows * DV + e] : 0.f;
+        for (int g = G - 1; g >= 0; --g) {
+            float *slot = p.AcV + ((size_t)bh * G + g) * kStoreRows * DV + e;
+            const float own = *slot;
+            *slot = A;
+            A = fmaf(__expf(Gg[g]), A, own);
+        }
+        if (p.gV0) p.gV0[(size_t)bh * kStoreRows * DV + e] = act ? A : 0.f;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -541,6 +644,8 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
     __shared__ float Qs[kC][DK + 1], Ks[kC][DK + 1], gQ[kC][DK + 1], gK[kC][DK + 1];
     __shared__ float Vs[kC][DV + 1], dOs[kC][DV + 1];
     __shared__ float dPs[kC][kLD], Us[kC][kLD], As[kC][kLD], dAK[kC][kLD], dAV[kC][kLD];
+    __shared__ __attribute__((aligned(16))) float dPT[kStoreRows][kC];   // dp and A transposed:
+    __shared__ __attribute__((aligned(16))) float AT[kStoreRows][kC];    // all tokens of a row in 64 bytes
     __shared__ float Sqk[kC][kC + 1], Sdpa[kC][kC + 1], Suoa[kC][kC + 1], Sdov[kC][kC + 1];
     __shared__ float red[kNT * kC];
     __shared__ ChunkTab tab;
@@ -556,6 +661,9 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
         const int t0 = c * kC;
         const size_t row0 = (size_t)bh * p.Tpad + t0;
         const size_t st = ((size_t)bh * p.nc + c) * kStoreRows;    // state row 0 of this chunk
+        const size_t sg = ((size_t)bh * p.groups + g) * kStoreRows; // group carry row 0
+        const float dec_in = __expf(p.Gin[(size_t)bh * p.nc + c]);
+        const float dec_out = __expf(p.Gout[(size_t)bh * p.nc + c]);
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             const bool live = t0 + r < Tb;
@@ -570,11 +678,18 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
         }
         for (int e = tid; e < kC * kStoreRows; e += kNT) {
             const int r = e >> 7, ii = e & 127;
-            dPs[r][ii] = p.dP[(row0 + r) * kStoreRows + ii];
+            const float dp = p.dP[(row0 + r) * kStoreRows + ii];
+            dPs[r][ii] = dp;
+            dPT[ii][r] = dp;
             Us[r][ii] = p.U[(row0 + r) * kStoreRows + ii];
         }
         chunk_tables(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
-        build_writes(tab, m, As, tid);
+        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+            const int r = e >> 7, i = e & 127;
+            const float a = write_entry(tab, m, r, i, tab.beta[r]);
+            As[r][i] = a;
+            AT[i][r] = a;
+        }
         __syncthreads();
         const float GC = tab.G[kC - 1];
         {   // the four masked score tiles
@@ -606,9 +721,15 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float kb = p.Kst[(st + ii) * DK + cc];
+                const float kb = fmaf(dec_in, p.EcK[(sg + ii) * DK + cc], p.Kst[(st + ii) * DK + cc]);
 #pragma unroll
-                for (int r = 0; r < kC; ++r) acc[r] = fmaf(dPs[r][ii], kb, acc[r]);
+                for (int q4 = 0; q4 < kC / 4; ++q4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&dPT[ii][4 * q4]);
+                    acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
+                    acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
+                    acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
+                    acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                }
             }
 #pragma unroll
             for (int r = 0; r < kC; ++r) red[(ih * kC + r) * DK + cc] = acc[r];
@@ -631,9 +752,15 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float kb = p.DKe[(st + ii) * DK + cc];
+                const float kb = fmaf(dec_out, p.AcK[(sg + ii) * DK + cc], p.DKe[(st + ii) * DK + cc]);
 #pragma unroll
-                for (int s = 0; s < kC; ++s) acc[s] = fmaf(As[s][ii], kb, acc[s]);
+                for (int q4 = 0; q4 < kC / 4; ++q4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][4 * q4]);
+                    acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
+                    acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
+                    acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
+                    acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                }
             }
 #pragma unroll
             for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DK + cc] = acc[s];
@@ -656,9 +783,15 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float vb = p.DVe[(st + ii) * DV + cc];
+                const float vb = fmaf(dec_out, p.AcV[(sg + ii) * DV + cc], p.DVe[(st + ii) * DV + cc]);
 #pragma unroll
-                for (int s = 0; s < kC; ++s) acc[s] = fmaf(As[s][ii], vb, acc[s]);
+                for (int q4 = 0; q4 < kC / 4; ++q4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][4 * q4]);
+                    acc[4 * q4] = fmaf(x.x, vb, acc[4 * q4]);
+                    acc[4 * q4 + 1] = fmaf(x.y, vb, acc[4 * q4 + 1]);
+                    acc[4 * q4 + 2] = fmaf(x.z, vb, acc[4 * q4 + 2]);
+                    acc[4 * q4 + 3] = fmaf(x.w, vb, acc[4 * q4 + 3]);
+                }
             }
 #pragma unroll
             for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DV + cc] = acc[s];
@@ -684,9 +817,13 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 av[s2] = 0.f;
             }
             const float *dkr = p.DKe + (st + i) * DK + part * KH;
+            const float *dkc = p.AcK + (sg + i) * DK + part * KH;
 #pragma unroll 1
             for (int cc = 0; cc < KH; cc += 4) {
-                const float4 d = *reinterpret_cast<const float4 *>(dkr + cc);
+                const float4 d0 = *reinterpret_cast<const float4 *>(dkr + cc);
+                const float4 d1 = *reinterpret_cast<const float4 *>(dkc + cc);
+                const float4 d = make_float4(fmaf(dec_out, d1.x, d0.x), fmaf(dec_out, d1.y, d0.y),
+                                             fmaf(dec_out, d1.z, d0.z), fmaf(dec_out, d1.w, d0.w));
 #pragma unroll
                 for (int s2 = 0; s2 < kC; ++s2) {
                     const float *kk = &Ks[s2][part * KH + cc];
@@ -694,9 +831,13 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 }
             }
             const float *dvr = p.DVe + (st + i) * DV + part * VH;
+            const float *dvc = p.AcV + (sg + i) * DV + part * VH;
 #pragma unroll 1
             for (int cc = 0; cc < VH; cc += 4) {
-                const float4 d = *reinterpret_cast<const float4 *>(dvr + cc);
+                const float4 d0 = *reinterpret_cast<const float4 *>(dvr + cc);
+                const float4 d1 = *reinterpret_cast<const float4 *>(dvc + cc);
+                const float4 d = make_float4(fmaf(dec_out, d1.x, d0.x), fmaf(dec_out, d1.y, d0.y),
+                                             fmaf(dec_out, d1.z, d0.z), fmaf(dec_out, d1.w, d0.w));
 #pragma unroll
                 for (int s2 = 0; s2 < kC; ++s2) {
                     const float *vv = &Vs[s2][part * VH + cc];
@@ -779,7 +920,8 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
     const int Tb = bwd_tokens(p, b);
     const float *dG = p.dG + (size_t)bh * p.Tpad;
     const float *dl = p.dlam + (size_t)bh * p.Tpad;
-    const float fin = p.fin[bh];
+    float fin = 0.f;
+    for (int u = 0; u < kCombBlocks; ++u) fin += p.fin[(size_t)bh * kCombBlocks + u];
     const int per = (Tb + kNT - 1) / kNT;
     const int t_lo = min(tid * per, Tb), t_hi = min(t_lo + per, Tb);
     double aG = 0.0, aL = 0.0;
@@ -862,9 +1004,11 @@ template <int DK, int DV, typename Tin>
 hipError_t launch_typed(const BwdParams &p, hipStream_t s) {
     const int BH = p.B * p.H;
     const dim3 block(kNT), seq(BH), grp(BH, p.groups);
-    hipLaunchKernelGGL((bwd_states_kernel<DK, DV, Tin>), seq, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_states_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_states_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
     hipLaunchKernelGGL((bwd_readout_kernel<DK, DV, Tin>), grp, block, 0, s, p);
-    hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV, Tin>), seq, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_adjoint_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_adjoint_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
     hipLaunchKernelGGL((bwd_grad_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL(bwd_scan_kernel, seq, block, 0, s, p);
     if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H, kStoreRows / kDRRows), block, 0, s, p);
@@ -888,19 +1032,22 @@ int bwd_auto_groups(int B, int T, int H) {
     return g < 1 ? 1 : g;
 }
 
-// Layout (each piece 256-byte aligned): M, Kst, Vst, clk, DKe, DVe, U, dP, udu,
-// dlam, dG, dMp, fin.
+// Layout (each piece 256-byte aligned): M, Kst, Vst, clk, DKe, DVe, EcK, EcV,
+// AcK, AcV, Gin, Gout, Gg, U, dP, udu, dlam, dG, dMp, fin.
 size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups) {
     const size_t BH = (size_t)B * H, nc = ((size_t)T + kC - 1) / kC, Tpad = nc * kC;
     const size_t st = BH * nc * kStoreRows * (size_t)(dk + dv) * 4;
+    const size_t gc = BH * (size_t)groups * kStoreRows * (size_t)(dk + dv) * 4;
     size_t n = align_up(readout_f32_bytes(H));
     n += align_up(st);                                   // Kst + Vst
     n += align_up(BH * nc * 8);                          // clk
     n += align_up(st);                                   // DKe + DVe
+    n += 2 * align_up(gc);                               // EcK + EcV, AcK + AcV
+    n += 2 * align_up(BH * nc * 4) + align_up(BH * (size_t)groups * 4);   // Gin, Gout, Gg
     n += 2 * align_up(BH * Tpad * kStoreRows * 4);       // U, dP
     n += 3 * align_up(BH * Tpad * 4);                    // udu, dlam, dG
     n += align_up(BH * (size_t)groups * kStoreRows * kStoreRows * 4);
-    n += align_up(BH * 4);
+    n += align_up(BH * kCombBlocks * 4);
     return n;
 }
 
@@ -916,13 +1063,21 @@ hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s) {
     char *ad = take(BH * nc * kStoreRows * (size_t)(p.dk + p.dv) * 4);
     p.DKe = reinterpret_cast<float *>(ad);
     p.DVe = p.DKe + BH * nc * kStoreRows * p.dk;
+    const size_t gcar = BH * (size_t)p.groups * kStoreRows;
+    p.EcK = reinterpret_cast<float *>(take(gcar * (size_t)(p.dk + p.dv) * 4));
+    p.EcV = p.EcK + gcar * p.dk;
+    p.AcK = reinterpret_cast<float *>(take(gcar * (size_t)(p.dk + p.dv) * 4));
+    p.AcV = p.AcK + gcar * p.dk;
+    p.Gin = reinterpret_cast<float *>(take(BH * nc * 4));
+    p.Gout = reinterpret_cast<float *>(take(BH * nc * 4));
+    p.Gg = reinterpret_cast<float *>(take(BH * (size_t)p.groups * 4));
     p.U = reinterpret_cast<float *>(take(BH * Tpad * kStoreRows * 4));
     p.dP = reinterpret_cast<float *>(take(BH * Tpad * kStoreRows * 4));
     p.udu = reinterpret_cast<float *>(take(BH * Tpad * 4));
     p.dlam = reinterpret_cast<float *>(take(BH * Tpad * 4));
     p.dG = reinterpret_cast<float *>(take(BH * Tpad * 4));
     p.dMp = reinterpret_cast<float *>(take(BH * (size_t)p.groups * kStoreRows * kStoreRows * 4));
-    p.fin = reinterpret_cast<float *>(take(BH * 4));
+    p.fin = reinterpret_cast<float *>(take(BH * kCombBlocks * 4));
     p.M = M;
     hipError_t e = launch_readout_prep(p.H, p.m, p.R, M, nullptr, 1.f, s);
     if (e != hipSuccess) return e;

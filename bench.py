@@ -9,8 +9,9 @@ whole batch.  Prints one JSON line.
 Extra fields: ``roofline`` of the dominant kernel (the fused chunk kernel, timed
 alone with HIP events the library records on its launch stream), ``mfma``
 (algorithmic TFLOP/s against the bf16 dense MFMA peak), ``cpu_baseline`` (the
-fp64 CPU oracle timed on a bounded sample of the same workload on this host)
-and ``decode`` (the single-token decode step at 256 streams x 16 heads).
+fp64 CPU oracle timed on a bounded sample of the same workload on this host),
+``decode`` (the single-token decode step at 256 streams x 16 heads) and
+``backward`` (cyfa_backward on the same workload).
 """
 from __future__ import annotations
 
@@ -28,6 +29,7 @@ if ROOT not in sys.path:
 METRIC = "CyFA fwd tokens/s + TFLOP/s (% MFMA peak) at 1.4B shape, 1 MI355X"
 PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2516.6       # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
+PEAK_F32_TFLOPS = 157.3         # MI355X fp32 vector ALU (256 CU x 2.4 GHz x 256 FLOP/clk)
 M_ACTIVE = 127
 
 # Measured HBM bytes per launch of the fused 32-token kernel on the 1.4B-layer
@@ -249,6 +251,53 @@ def decode_bench(args, torch, cyfa):
     return res
 
 
+def bwd_flops_per_token_head(dk: int, dv: int, m: int = M_ACTIVE, C: int = 16) -> float:
+    """Algorithmic FLOPs of the chunk-wise backward per token and head: carried-state
+    products 4m(dk+dv) (entering states, adjoint states, dk/dv and da carried parts),
+    the recomputed key-pass output, du and the dq carried part m(2dk+dv), the four
+    readout products and dM 6m^2, and the causal half of the intra-chunk score tiles
+    and products ((C+1)/2)(4dk+3dv+6m); times 2 for FMA."""
+    return 2.0 * (4 * m * (dk + dv) + m * (2 * dk + dv) + 6 * m * m
+                  + (C + 1) / 2.0 * (4 * dk + 3 * dv + 6 * m))
+
+
+def backward_bench(args, torch, cyfa, w):
+    """cyfa_backward on the benchmark workload (upstream gradient d_o ~ N(0, 1))."""
+    from paper_2609_36259_amd.inputs import workload_inputs
+    dev = torch.device("cuda:0")
+    x = workload_inputs(w)
+    t = upload_inputs(torch, x, dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    do = torch.randn((w.B, w.T, w.H, w.dv), device=dev, generator=g).to(t["q"].dtype)
+    desc = cyfa.forward_desc(w.B, w.T, w.H, w.dk, w.dv, m=w.m, scale=x["scale"],
+                             dtype=cyfa.BF16 if w.dtype == "bf16" else cyfa.F32,
+                             kernel=cyfa.KERNEL_VALU)
+    ws = torch.empty(cyfa.backward_workspace_size(desc), dtype=torch.uint8, device=dev)
+
+    def step():
+        return cyfa.backward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                             d_o=do, scale=x["scale"], m=w.m, workspace=ws)
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    steps = 10
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1000 / steps
+    flops = bwd_flops_per_token_head(w.dk, w.dv, w.m) * w.B * w.T * w.H
+    tfl = flops / (ms * 1e-3) / 1e12
+    del ws
+    torch.cuda.empty_cache()
+    return dict(workload=w.name, steps=steps, ms_per_step=ms, tokens_per_s=w.B * w.T / (ms * 1e-3),
+                arithmetic="fp32 vector ALU", alg_flops_per_step=flops,
+                roofline={"bound": "alu", "achieved": tfl, "peak": PEAK_F32_TFLOPS, "unit": "TFLOP/s",
+                          "frac": tfl / PEAK_F32_TFLOPS})
+
+
 def cpu_baseline(w, budget_s: float):
     """Time the CPU oracle on a bounded sample of the workload (leading (b, h)
     sequences, leading tokens), sized to about `budget_s` seconds."""
@@ -290,6 +339,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -359,6 +409,8 @@ def main():
                         "note": "median of single steps, each after a 512 MiB write (caches evicted)"}
     if not args.no_decode:
         line["decode"] = decode_bench(args, torch, cyfa)
+    if not args.no_backward:
+        line["backward"] = backward_bench(args, torch, cyfa, w)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -46,7 +46,9 @@ namespace cyfa {
 namespace {
 
 constexpr int kC = kBwdChunk;
-constexpr int kNT = 256;            // threads per workgroup
+constexpr int kNT = 512;            // threads per workgroup (two waves per SIMD)
+constexpr int kRP = kNT / kStoreRows; // threads sharing one state row in the row layouts
+constexpr int kRQ = kC * kStoreRows / kNT;   // token rows per thread in the readout products
 constexpr int kLD = kStoreRows + 4; // padded row of a [token][basis] tile (16-byte rows)
 constexpr float kTwoPi = 6.283185307179586f;
 constexpr int kCombBlocks = 8;      // workgroups per sequence of the group-combine kernels
@@ -152,19 +154,20 @@ __device__ __forceinline__ float rot_grad(const float *dZ, const float *Z, int m
 }
 
 // Products with the readout matrix over the m active entries, register-blocked:
-// thread (column col = tid % 128, rows 8 (tid / 128) .. + 7) keeps eight
+// thread (column col = tid % 128, rows kRQ (tid / 128) .. + kRQ - 1) keeps kRQ
 // independent sums.  TRANS = false: out_r = M in_r (out[r][i] = sum_j M[i][j] in[r][j]);
 // TRANS = true: out_r = M^T in_r.  Entries >= m of out are 0.
 template <bool TRANS>
 __device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], float (*out)[kLD], int m,
                                 int tid) {
-    const int col = tid & 127, r0 = (tid >> 7) * 8;
-    float acc[8];
+    const int col = tid & 127, r0 = (tid >> 7) * kRQ;
+    float acc[kRQ];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int q = 0; q < kRQ; ++q) acc[q] = 0.f;
     if (col < m) {
         // four entries per step (16-byte rows; entries m .. 127 of in are 0, and M
         // is 0 outside its active block, so running to a multiple of four is exact)
+#pragma unroll 2
         for (int j = 0; j < m; j += 4) {
             float4 mv;
             if (TRANS) {
@@ -173,29 +176,29 @@ __device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], 
                 mv = *reinterpret_cast<const float4 *>(&Ms[col][j]);
             }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < kRQ; ++q) {
                 const float4 x = *reinterpret_cast<const float4 *>(&in[r0 + q][j]);
                 acc[q] = fmaf(mv.x, x.x, fmaf(mv.y, x.y, fmaf(mv.z, x.z, fmaf(mv.w, x.w, acc[q]))));
             }
         }
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) out[r0 + q][col] = acc[q];
+    for (int q = 0; q < kRQ; ++q) out[r0 + q][col] = acc[q];
 }
 
 // out[r][i] += sum_s S[r][s] A[s][i] for a causal (lower-triangular) score tile S.
 __device__ void add_scores_times(const float (*S)[kC + 1], const float (*A)[kLD], float (*out)[kLD], int tid) {
-    const int col = tid & 127, r0 = (tid >> 7) * 8;
-    float acc[8];
+    const int col = tid & 127, r0 = (tid >> 7) * kRQ;
+    float acc[kRQ];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = out[r0 + q][col];
-    for (int s = 0; s < r0 + 8; ++s) {
+    for (int q = 0; q < kRQ; ++q) acc[q] = out[r0 + q][col];
+    for (int s = 0; s < r0 + kRQ; ++s) {
         const float a = A[s][col];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] = fmaf(S[r0 + q][s], a, acc[q]);
+        for (int q = 0; q < kRQ; ++q) acc[q] = fmaf(S[r0 + q][s], a, acc[q]);
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) out[r0 + q][col] = acc[q];
+    for (int q = 0; q < kRQ; ++q) out[r0 + q][col] = acc[q];
 }
 
 template <typename Tin>
@@ -206,13 +209,13 @@ __device__ __forceinline__ float ld_row(const void *base, int b, int t, int h, i
 // ---------------------------------------------------------------------------
 // (1a) states entering every chunk from the chunk group's own tokens (the
 // group starts from zero), per (sequence, group).  Thread t keeps column t % D
-// of a state and its rows (t / D) NR .. + NR - 1 (NR = D / 2), for the key
+// of a state and its rows (t / D) NR .. + NR - 1 (NR = 128 D / threads), for the key
 // state (D = d_k) and the value state (D = d_v): a wave shares its rows, so the
 // write rows are broadcast reads and the stored state rows are coalesced.  The
 // group's own final state goes to EcK/EcV[g], its total log decay to Gg.
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
-    constexpr int NRK = DK / 2, NRV = DV / 2;
+    constexpr int NRK = DK * kStoreRows / kNT, NRV = DV * kStoreRows / kNT;
     __shared__ float Ks[kC][DK];
     __shared__ float Vs[kC][DV];
     __shared__ __attribute__((aligned(16))) float Aw[kC][kStoreRows];   // rho_r A_r
@@ -274,6 +277,7 @@ __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
         for (int ii = 0; ii < NRK; ++ii) kst[ii] *= gC;
 #pragma unroll
         for (int ii = 0; ii < NRV; ++ii) vst[ii] *= gC;
+#pragma unroll 1
         for (int r = 0; r < kC; ++r) {
             const float kr = Ks[r][ck], vr = Vs[r][cv];
 #pragma unroll
@@ -330,14 +334,18 @@ __global__ __launch_bounds__(kNT) void bwd_states_combine_kernel(BwdParams p) {
     acc = wsum(acc);
     if ((tid & 63) == 0) red[tid >> 6] = acc;
     __syncthreads();
-    if (tid == 0) p.fin[(size_t)bh * kCombBlocks + blockIdx.y] = red[0] + red[1] + red[2] + red[3];
+    if (tid == 0) {
+        float t = 0.f;
+        for (int w = 0; w < kNT / 64; ++w) t += red[w];
+        p.fin[(size_t)bh * kCombBlocks + blockIdx.y] = t;
+    }
 }
 
 // ---------------------------------------------------------------------------
 // (2) readout recomputation and its adjoint, per (sequence, chunk group).
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
-    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int KH = DK / kRP, VH = DV / kRP, MH = kStoreRows / kRP;
     constexpr int DM = DK > DV ? DK : DV;
     __shared__ __attribute__((aligned(16))) float Ms[kStoreRows][kLD];
     __shared__ float In0[kC][DM + 1];       // Q, then dO
@@ -349,14 +357,14 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
     __shared__ float dlu[kC];
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int i = tid / kRP, part = tid % kRP, m = p.m;
     const int Tb = bwd_tokens(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
     const float *Mh = p.M + (size_t)h * kStoreRows * kStoreRows;
     for (int e = tid; e < kStoreRows * kStoreRows; e += kNT) Ms[e >> 7][e & 127] = Mh[e];
-    float dMacc[64];                        // dM[i][64 part .. 64 part + 63]
+    float dMacc[MH];                        // dM[i][MH part .. MH part + MH - 1]
 #pragma unroll
-    for (int jj = 0; jj < 64; ++jj) dMacc[jj] = 0.f;
+    for (int jj = 0; jj < MH; ++jj) dMacc[jj] = 0.f;
 
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC;
@@ -369,7 +377,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         chunk_tables(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
         build_writes(tab, m, As, tid);
-        {   // S1 = (Q K^T) (.) Gamma
+        if (tid < kC * kC) {   // S1 = (Q K^T) (.) Gamma
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
             if (s <= r) {
@@ -386,11 +394,13 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
             float kr[KH];
 #pragma unroll
             for (int cc = 0; cc < KH; ++cc) kr[cc] = fmaf(dec, Ke[cc], Kc[cc]);
+#pragma unroll 1
             for (int r = 0; r < kC; ++r) {
                 float ps = 0.f;
 #pragma unroll
                 for (int cc = 0; cc < KH; ++cc) ps = fmaf(In0[r][part * KH + cc], kr[cc], ps);
                 ps += __shfl_xor(ps, 1);
+                ps += __shfl_xor(ps, 2);
                 if (part == 0) Xs[r][i] = __expf(tab.G[r]) * ps;
             }
         }
@@ -409,7 +419,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         __syncthreads();
         // Z = M X (active slots), S2 = (dO V^T) (.) Gamma
         readout_product<false>(Ms, Xs, Ws, m, tid);
-        {
+        if (tid < kC * kC) {
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
             if (s <= r) {
@@ -444,11 +454,13 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
             float vr[VH];
 #pragma unroll
             for (int cc = 0; cc < VH; ++cc) vr[cc] = fmaf(dec, Ve[cc], Vc[cc]);
+#pragma unroll 1
             for (int r = 0; r < kC; ++r) {
                 float ps = 0.f;
 #pragma unroll
                 for (int cc = 0; cc < VH; ++cc) ps = fmaf(In0[r][part * VH + cc], vr[cc], ps);
                 ps += __shfl_xor(ps, 1);
+                ps += __shfl_xor(ps, 2);
                 if (part == 0) dUs[r][i] = __expf(tab.G[r]) * ps;
             }
         }
@@ -475,10 +487,11 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         __syncthreads();
         // dW = M dY;  dM += W dY^T
         readout_product<false>(Ms, dUs, dWs, m, tid);
+#pragma unroll 1
         for (int r = 0; r < kC; ++r) {
             const float w = Ws[r][i];
 #pragma unroll
-            for (int jj = 0; jj < 64; ++jj) dMacc[jj] = fmaf(w, dUs[r][part * 64 + jj], dMacc[jj]);
+            for (int jj = 0; jj < MH; ++jj) dMacc[jj] = fmaf(w, dUs[r][part * MH + jj], dMacc[jj]);
         }
         __syncthreads();
         // dZ = W (.) (dW - <W, dW>)
@@ -491,10 +504,11 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // dM += dZ X^T;  dX = M^T dZ (into the dY tile)
+#pragma unroll 1
         for (int r = 0; r < kC; ++r) {
             const float dz = dWs[r][i];
 #pragma unroll
-            for (int jj = 0; jj < 64; ++jj) dMacc[jj] = fmaf(dz, Xs[r][part * 64 + jj], dMacc[jj]);
+            for (int jj = 0; jj < MH; ++jj) dMacc[jj] = fmaf(dz, Xs[r][part * MH + jj], dMacc[jj]);
         }
         __syncthreads();
         readout_product<true>(Ms, dWs, dUs, m, tid);
@@ -514,9 +528,9 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
     }
-    float *dMo = p.dMp + (((size_t)bh * p.groups + g) * kStoreRows + i) * kStoreRows + part * 64;
+    float *dMo = p.dMp + (((size_t)bh * p.groups + g) * kStoreRows + i) * kStoreRows + part * MH;
 #pragma unroll
-    for (int jj = 0; jj < 64; ++jj) dMo[jj] = dMacc[jj];
+    for (int jj = 0; jj < MH; ++jj) dMo[jj] = dMacc[jj];
 }
 
 // ---------------------------------------------------------------------------
@@ -526,7 +540,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
 // entering the group goes to AcK/AcV[g].
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_adjoint_local_kernel(BwdParams p) {
-    constexpr int NRK = DK / 2, NRV = DV / 2;
+    constexpr int NRK = DK * kStoreRows / kNT, NRV = DV * kStoreRows / kNT;
     __shared__ float Qs[kC][DK];
     __shared__ float dOs[kC][DV];
     __shared__ __attribute__((aligned(16))) float Wp[kC][kStoreRows];   // gamma_r dp_r
@@ -581,6 +595,7 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_local_kernel(BwdParams p) {
         for (int ii = 0; ii < NRK; ++ii) ak[ii] *= gC;
 #pragma unroll
         for (int ii = 0; ii < NRV; ++ii) av[ii] *= gC;
+#pragma unroll 1
         for (int r = 0; r < kC; ++r) {
             const float qr = Qs[r][ck], dor = dOs[r][cv];
 #pragma unroll
@@ -639,7 +654,7 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_combine_kernel(BwdParams p) {
 // columns) give thread (row i, half part) one state row.
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
-    constexpr int KH = DK / 2, VH = DV / 2;
+    constexpr int KH = DK / kRP, VH = DV / kRP;
     constexpr int IHK = kNT / DK, IHV = kNT / DV;          // row blocks of the column products
     __shared__ float Qs[kC][DK + 1], Ks[kC][DK + 1], gQ[kC][DK + 1], gK[kC][DK + 1];
     __shared__ float Vs[kC][DV + 1], dOs[kC][DV + 1];
@@ -651,7 +666,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
     __shared__ ChunkTab tab;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int i = tid >> 1, part = tid & 1, m = p.m;
+    const int i = tid / kRP, part = tid % kRP, m = p.m;
     const int Tb = bwd_tokens(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
     Tin *gq = static_cast<Tin *>(p.gq);
@@ -692,26 +707,35 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
         }
         __syncthreads();
         const float GC = tab.G[kC - 1];
-        {   // the four masked score tiles
-            const int r = tid >> 4, s = tid & 15;
-            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+        {   // the four masked score tiles: threads 0..255 the (q, k) and (do, v) tiles,
+            // threads 256..511 the (dp, a) and (u, a) tiles
+            const int half = tid / (kC * kC), e = tid % (kC * kC);
+            const int r = e >> 4, s = e & 15;
+            float a0 = 0.f, a1 = 0.f;
             if (s <= r) {
                 const float gam = __expf(tab.G[r] - tab.G[s]);
+                if (half == 0) {
 #pragma unroll 4
-                for (int cc = 0; cc < DK; ++cc) a0 = fmaf(Qs[r][cc], Ks[s][cc], a0);
+                    for (int cc = 0; cc < DK; ++cc) a0 = fmaf(Qs[r][cc], Ks[s][cc], a0);
 #pragma unroll 4
-                for (int cc = 0; cc < DV; ++cc) a1 = fmaf(dOs[r][cc], Vs[s][cc], a1);
+                    for (int cc = 0; cc < DV; ++cc) a1 = fmaf(dOs[r][cc], Vs[s][cc], a1);
+                } else {
 #pragma unroll 4
-                for (int ii = 0; ii < kStoreRows; ++ii) {
-                    a2 = fmaf(dPs[r][ii], As[s][ii], a2);
-                    a3 = fmaf(Us[r][ii], As[s][ii], a3);
+                    for (int ii = 0; ii < kStoreRows; ++ii) {
+                        a0 = fmaf(dPs[r][ii], As[s][ii], a0);
+                        a1 = fmaf(Us[r][ii], As[s][ii], a1);
+                    }
                 }
-                a0 *= gam; a1 *= gam; a2 *= gam; a3 *= gam;
+                a0 *= gam;
+                a1 *= gam;
             }
-            Sqk[r][s] = a0;
-            Sdov[r][s] = a1;
-            Sdpa[r][s] = a2;
-            Suoa[r][s] = a3;
+            if (half == 0) {
+                Sqk[r][s] = a0;
+                Sdov[r][s] = a1;
+            } else {
+                Sdpa[r][s] = a0;
+                Suoa[r][s] = a1;
+            }
         }
         // dq: gamma_r (dP Kbar_c)[r] + (Sdpa K)[r]
         {
@@ -720,6 +744,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             float acc[kC];
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+#pragma unroll 2
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
                 const float kb = fmaf(dec_in, p.EcK[(sg + ii) * DK + cc], p.Kst[(st + ii) * DK + cc]);
 #pragma unroll
@@ -751,6 +776,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             float acc[kC];
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+#pragma unroll 2
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
                 const float kb = fmaf(dec_out, p.AcK[(sg + ii) * DK + cc], p.DKe[(st + ii) * DK + cc]);
 #pragma unroll
@@ -782,6 +808,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             float acc[kC];
 #pragma unroll
             for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+#pragma unroll 2
             for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
                 const float vb = fmaf(dec_out, p.AcV[(sg + ii) * DV + cc], p.DVe[(st + ii) * DV + cc]);
 #pragma unroll
@@ -846,8 +873,10 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             }
 #pragma unroll
             for (int s2 = 0; s2 < kC; ++s2) {
-                const float a = ak[s2] + __shfl_xor(ak[s2], 1);
-                const float bv = av[s2] + __shfl_xor(av[s2], 1);
+                float a = ak[s2] + __shfl_xor(ak[s2], 1);
+                float bv = av[s2] + __shfl_xor(av[s2], 1);
+                a += __shfl_xor(a, 2);
+                bv += __shfl_xor(bv, 2);
                 if (part == 0) {
                     const float rho = __expf(GC - tab.G[s2]);
                     dAK[s2][i] = rho * a;

@@ -153,3 +153,28 @@ def test_empty_sequence_passes_state_adjoints_through():
     np.testing.assert_array_equal(g["d_K0"], e["dK_T"])
     np.testing.assert_array_equal(g["d_V0"], e["dV_T"])
     assert np.all(g["d_clock0"] == 0)
+
+
+@pytest.mark.timeout(400)
+def test_full_size_sampled_sequence():
+    """The 1.4B-scale workload (B=4, T=4096, H=16, d=128, bf16) in the launch
+    configuration the benchmark times (automatic chunk groups); one sampled
+    (b, h) sequence's gradients, all tokens, against the oracle run on that
+    sequence alone (dR sums over every sequence and is covered by the small cases)."""
+    from paper_2609_36259_amd.inputs import FWD_1P4B, workload_inputs
+    x = workload_inputs(FWD_1P4B)
+    B, T, H = x["delta"].shape
+    rng = np.random.default_rng(9)
+    e = {"do": _round(rng.standard_normal((B, T, H, 128)), "bf16")}
+    print("full-size backward", flush=True)
+    g = _run(x, e)
+    b, h = 2, 11
+    sl = lambda a: None if a is None else np.ascontiguousarray(a[b:b + 1, :, h:h + 1])  # noqa: E731
+    y = dict(x, q=sl(x["q"]), k=sl(x["k"]), v=sl(x["v"]), delta=sl(x["delta"]),
+             log_alpha=sl(x["log_alpha"]), beta=sl(x["beta"]), R=x["R"][h:h + 1])
+    print("oracle on sequence", (b, h), flush=True)
+    ref = _oracle(y, {"do": sl(e["do"])})
+    pick = {k: (v[b:b + 1, :, h:h + 1] if k in ("dq", "dk", "dv", "d_delta", "d_log_alpha", "d_beta")
+                else v[b:b + 1, h:h + 1] if k in ("d_K0", "d_V0", "d_clock0") else v)
+            for k, v in g.items() if v is not None}
+    _compare(pick, ref, TOL_BF16, skip=("d_R",))

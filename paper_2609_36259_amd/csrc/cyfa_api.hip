@@ -9,6 +9,7 @@
 #include "cyfa.h"
 #include "cyfa_bwd.h"
 #include "cyfa_internal.h"
+#include "cyfa_rows.h"
 
 namespace cyfa {
 int valu_chunk_max();
@@ -69,10 +70,13 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
         return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64, 128 or 256 (got d_k=%d d_v=%d)",
                     d->d_k, d->d_v);
-    if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
-        return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
-                                                               : CYFA_ERR_INVALID_ARGUMENT,
-                    "m must be odd and in [3, 127] (got %d)", d->m);
+    if (d->m < 3 || d->m > cyfa::kMaxActiveWide || (d->m % 2) == 0)
+        return fail(d->m > cyfa::kMaxActiveWide && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
+                                                                   : CYFA_ERR_INVALID_ARGUMENT,
+                    "m must be odd and in [3, 255] (got %d)", d->m);
+    const bool wide = d->m > cyfa::kMaxActive;
+    if (wide && (d->d_k > 128 || d->d_v > 128))
+        return fail(CYFA_ERR_UNSUPPORTED, "m > 127 (256 storage rows) supports head dims 64 and 128");
     if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
     if (d->kernel < CYFA_KERNEL_AUTO || d->kernel > CYFA_KERNEL_MFMA)
@@ -86,12 +90,12 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     probe.B = d->B; probe.T = d->T; probe.H = d->H; probe.dk = d->d_k; probe.dv = d->d_v;
     probe.m = d->m; probe.dtype = d->dtype;
     probe.chunk = d->chunk ? d->chunk : cyfa::mfma_default_chunk();
-    const bool mfma_ok = cyfa::mfma_supported(probe);
+    const bool mfma_ok = !wide && cyfa::mfma_supported(probe);
     bool use_mfma;
     if (d->kernel == CYFA_KERNEL_MFMA) {
         if (!mfma_ok)
             return fail(CYFA_ERR_UNSUPPORTED,
-                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 and chunk 32 or 64");
+                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128, m <= 127 and chunk 32 or 64");
         use_mfma = true;
     } else if (d->kernel == CYFA_KERNEL_VALU) {
         use_mfma = false;
@@ -99,7 +103,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
         use_mfma = mfma_ok;          // chunk 0, 32 or 64 with bf16 and d = 128
     }
     plan->mfma = use_mfma;
-    size_t ws = round_up(cyfa::readout_f32_bytes(d->H));
+    size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
     if (use_mfma) {
         plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
@@ -140,7 +144,7 @@ cyfa_status plan_backward(const cyfa_fwd_desc *d, BwdPlan *plan) {
     if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
         return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
                                                                : CYFA_ERR_INVALID_ARGUMENT,
-                    "m must be odd and in [3, 127] (got %d)", d->m);
+                    "backward: m must be odd and in [3, 127] (got %d)", d->m);
     if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
     if (d->kernel != CYFA_KERNEL_AUTO && d->kernel != CYFA_KERNEL_VALU)
@@ -172,7 +176,7 @@ cyfa_status check_dec(const cyfa_dec_desc *d) {
     if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
         return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
                                                                : CYFA_ERR_INVALID_ARGUMENT,
-                    "m must be odd and in [3, 127] (got %d)", d->m);
+                    "decode: m must be odd and in [3, 127] (got %d)", d->m);
     if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
     if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
@@ -250,7 +254,8 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
         // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else {
-        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
+        e = p.m > cyfa::kMaxActive ? cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s)
+                                   : cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
         if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
         e = mark(g_ev_start, s);
         if (e == hipSuccess) e = cyfa::launch_fwd_valu(p, M, s);

@@ -13,17 +13,20 @@
 // gamma^r = exp(G_r), Gamma_rs = exp(G_r - G_s) for r >= s (Eq. app-chunk-decay).
 // The basis order inside the kernel is the one of App. A.1 (0 = DC, 2j-1 =
 // cos_j, 2j = sin_j); rows m..127 are padding and stay zero.
-#include "cyfa_internal.h"
+#include "cyfa_rows.h"
 
 namespace cyfa {
 
 namespace {
 
 constexpr int kValuChunkMax = 16;
-// threads per workgroup: 256, or 512 when a head dimension is 256 (each thread
-// then holds at most 64 + 64 state values; with both dimensions at 256 some of
-// the kernel's temporaries spill, which this correctness-first fp32 path accepts)
-__host__ __device__ constexpr int valu_threads(int dk, int dv) { return (dk > 128 || dv > 128) ? 512 : 256; }
+// threads per workgroup: 256, or 512 when a head dimension is 256 or the states
+// have 256 storage rows (each thread then holds at most 64 + 64 state values;
+// with both dimensions at 256 some of the kernel's temporaries spill, which this
+// correctness-first fp32 path accepts)
+__host__ __device__ constexpr int valu_threads(int dk, int dv, int rows) {
+    return (dk > 128 || dv > 128 || rows > kStoreRows) ? 512 : 256;
+}
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
@@ -36,24 +39,28 @@ __device__ __forceinline__ float wave_sum(float x) {
     return x;
 }
 
-template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
-    constexpr int kThreads = valu_threads(DK, DV);
+// ROWS: storage rows of the states (128, or 256 for m > 127).  The readout
+// matrix sits in LDS with 128 rows and is read from global memory (L2) with 256.
+template <int DK, int DV, int ROWS, typename Tin>
+__global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
+    constexpr int kThreads = valu_threads(DK, DV, ROWS);
     constexpr int CM = kValuChunkMax;
-    constexpr int KP = kThreads / kStoreRows;  // threads sharing a key-state row
+    constexpr int KP = kThreads / ROWS;    // threads sharing a key-state row
     constexpr int KH = DK / KP;            // key-state columns per thread
     constexpr int VP = kThreads / DV;      // threads sharing a value-state column
-    constexpr int VR = kStoreRows / VP;    // value-state rows per thread
+    constexpr int VR = ROWS / VP;          // value-state rows per thread
+    constexpr int MSR = ROWS == kStoreRows ? kStoreRows : 1;   // LDS copy of M (128 rows only)
+    constexpr int NJ = ROWS / 2;           // phase-table entries per token
 
     __shared__ float Qs[CM][DK + 1];
     __shared__ float Ks[CM][DK + 1];
     __shared__ float Vs[CM][DV];
-    __shared__ float As[CM][kStoreRows + 1];
-    __shared__ float Ob[CM][kStoreRows];
-    __shared__ float Xb[CM][kStoreRows];
+    __shared__ float As[CM][ROWS + 1];
+    __shared__ float Ob[CM][ROWS];
+    __shared__ float Xb[CM][ROWS];
     __shared__ float Ss[CM][CM];
-    __shared__ float Ms[kStoreRows][kStoreRows + 1];
-    __shared__ float2 CSs[CM][64];
+    __shared__ float Ms[MSR][kStoreRows + 1];
+    __shared__ float2 CSs[CM][NJ];
     __shared__ double lam_s[CM];
     __shared__ float G_s[CM];
     __shared__ float beta_s[CM];
@@ -79,17 +86,24 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
     float kst[KH];
     float vst[VR];
     {
-        const size_t kbase = ((size_t)bh * kStoreRows + ki) * DK + kh * KH;
+        const size_t kbase = ((size_t)bh * ROWS + ki) * DK + kh * KH;
 #pragma unroll
         for (int c = 0; c < KH; ++c) kst[c] = (p.K0 && ki < m) ? p.K0[kbase + c] : 0.f;
 #pragma unroll
         for (int ii = 0; ii < VR; ++ii) {
             const int row = vpart * VR + ii;
-            vst[ii] = (p.V0 && row < m) ? p.V0[((size_t)bh * kStoreRows + row) * DV + vc] : 0.f;
+            vst[ii] = (p.V0 && row < m) ? p.V0[((size_t)bh * ROWS + row) * DV + vc] : 0.f;
         }
     }
-    for (int e = tid; e < kStoreRows * kStoreRows; e += kThreads)
-        Ms[e / kStoreRows][e % kStoreRows] = Mg[(size_t)h * kStoreRows * kStoreRows + e];
+    const float *Mh = Mg + (size_t)h * ROWS * ROWS;
+    if constexpr (ROWS == kStoreRows) {
+        for (int e = tid; e < kStoreRows * kStoreRows; e += kThreads)
+            Ms[e / kStoreRows][e % kStoreRows] = Mh[e];
+    }
+    auto Mv = [&](int i, int j) -> float {
+        if constexpr (ROWS == kStoreRows) return Ms[i][j];
+        else return Mh[i * ROWS + j];
+    };
     if (tid == 0) lam_carry = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
     __syncthreads();
 
@@ -133,6 +147,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
             clock_phase(lam_s[r], jj + 1, m, &c, &s);
             CSs[r][jj] = make_float2(c, s);
         }
+        static_assert(NJ >= kMaxActiveWide / 2 || ROWS == kStoreRows, "phase table holds every pair");
         // S = (Q K^T) (.) Gamma
         for (int e = tid; e < C * C; e += kThreads) {
             const int r = e / C, s = e % C;
@@ -145,8 +160,8 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
         }
         __syncthreads();
         // temporal write matrix A_r = beta_r U(-lambda_r) b
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, i = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, i = e % ROWS;
             const float be = beta_s[r];
             float val = 0.f;
             if (i == 0) {
@@ -168,8 +183,8 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
         }
         __syncthreads();
         // key pass, intra-chunk part: O' += S A
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, i = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, i = e % ROWS;
             float acc = Ob[r][i];
             for (int s = 0; s <= r; ++s) acc = fmaf(Ss[r][s], As[s][i], acc);
             Ob[r][i] = acc;
@@ -188,8 +203,8 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
         }
         __syncthreads();
         // middle step: X_r = U(lambda_r) (scale O'_r)
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, i = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, i = e % ROWS;
             float x = 0.f;
             if (i == 0) {
                 x = p.scale * Ob[r][0];
@@ -203,11 +218,11 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
         }
         __syncthreads();
         // slot logits Z_r = M X_r
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, i = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, i = e % ROWS;
             float acc = 0.f;
             if (i < m) {
-                for (int j = 0; j < m; ++j) acc = fmaf(Ms[i][j], Xb[r][j], acc);
+                for (int j = 0; j < m; ++j) acc = fmaf(Mv(i, j), Xb[r][j], acc);
                 if (p.logits && r < n)
                     p.logits[(((size_t)b * T + t0 + r) * H + h) * m + i] = acc;
             }
@@ -216,28 +231,38 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
         __syncthreads();
         // softmax over the m active slots (padding slots excluded)
         for (int r = wave; r < C; r += kThreads / 64) {
-            const float z0 = lane < m ? Ob[r][lane] : -INFINITY;
-            const float z1 = lane + 64 < m ? Ob[r][lane + 64] : -INFINITY;
-            const float mx = wave_max(fmaxf(z0, z1));
-            const float e0 = lane < m ? __expf(z0 - mx) : 0.f;
-            const float e1 = lane + 64 < m ? __expf(z1 - mx) : 0.f;
-            const float inv = 1.f / wave_sum(e0 + e1);
-            Ob[r][lane] = e0 * inv;
-            Ob[r][lane + 64] = e1 * inv;
+            constexpr int NQ = ROWS / 64;
+            float z[NQ];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                z[q] = lane + 64 * q < m ? Ob[r][lane + 64 * q] : -INFINITY;
+                mx = fmaxf(mx, z[q]);
+            }
+            mx = wave_max(mx);
+            float sum = 0.f;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                z[q] = lane + 64 * q < m ? __expf(z[q] - mx) : 0.f;
+                sum += z[q];
+            }
+            const float inv = 1.f / wave_sum(sum);
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) Ob[r][lane + 64 * q] = z[q] * inv;
         }
         __syncthreads();
         // Y_r = M^T W_r
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, j = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, j = e % ROWS;
             float acc = 0.f;
             if (j < m)
-                for (int i = 0; i < m; ++i) acc = fmaf(Ob[r][i], Ms[i][j], acc);
+                for (int i = 0; i < m; ++i) acc = fmaf(Ob[r][i], Mv(i, j), acc);
             Xb[r][j] = acc;
         }
         __syncthreads();
         // O''_r = U(-lambda_r) Y_r
-        for (int e = tid; e < C * kStoreRows; e += kThreads) {
-            const int r = e / kStoreRows, i = e % kStoreRows;
+        for (int e = tid; e < C * ROWS; e += kThreads) {
+            const int r = e / ROWS, i = e % ROWS;
             float x = 0.f;
             if (i == 0) {
                 x = Xb[r][0];
@@ -290,7 +315,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
     }
 
     if (p.K_out) {
-        const size_t kbase = ((size_t)bh * kStoreRows + ki) * DK + kh * KH;
+        const size_t kbase = ((size_t)bh * ROWS + ki) * DK + kh * KH;
 #pragma unroll
         for (int c = 0; c < KH; ++c) p.K_out[kbase + c] = ki < m ? kst[c] : 0.f;
     }
@@ -298,20 +323,29 @@ __global__ __launch_bounds__(valu_threads(DK, DV)) void fwd_valu_kernel(FwdParam
 #pragma unroll
         for (int ii = 0; ii < VR; ++ii) {
             const int row = vpart * VR + ii;
-            p.V_out[((size_t)bh * kStoreRows + row) * DV + vc] = row < m ? vst[ii] : 0.f;
+            p.V_out[((size_t)bh * ROWS + row) * DV + vc] = row < m ? vst[ii] : 0.f;
         }
     }
     if (p.clock_out && tid == 0) p.clock_out[bh] = lam_carry;
 }
 
+template <int DK, int DV, int ROWS>
+hipError_t launch_rows(const FwdParams &p, const float *M, hipStream_t s) {
+    const dim3 grid(p.B * p.H), block(valu_threads(DK, DV, ROWS));
+    if (p.dtype == 0)
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M);
+    else
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M);
+    return hipGetLastError();
+}
+
+// 256 storage rows are built for head dims up to 128
 template <int DK, int DV>
 hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
-    const dim3 grid(p.B * p.H), block(valu_threads(DK, DV));
-    if (p.dtype == 0)
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, float>), grid, block, 0, s, p, M);
-    else
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, __hip_bfloat16>), grid, block, 0, s, p, M);
-    return hipGetLastError();
+    if constexpr (DK <= 128 && DV <= 128) {
+        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, s);
+    }
+    return launch_rows<DK, DV, kStoreRows>(p, M, s);
 }
 
 }  // namespace

@@ -1,0 +1,25 @@
+// Storage rows of the states for larger slot counts (not part of the public ABI).
+//
+// m <= 127 active slots keep the m* = 128 storage rows of App. A.7; m up to 255
+// (the largest slot count of the paper's ablation) uses m* = 256 rows, with the
+// same basis order (0 = DC, 2j-1 = cos_j, 2j = sin_j) and zero padding.
+#pragma once
+
+#include "cyfa_internal.h"
+
+namespace cyfa {
+
+constexpr int kWideRows = 256;
+constexpr int kMaxActiveWide = 255;
+
+__host__ __device__ inline int store_rows(int m) { return m > kMaxActive ? kWideRows : kStoreRows; }
+inline size_t readout_bytes(int H, int m) {
+    const size_t r = (size_t)store_rows(m);
+    return (size_t)H * r * r * 4;
+}
+
+// M_h = R_h Phi as float [H][256][256] for 127 < m <= 255 (slot row, basis
+// column in the order of App. A.1, zero outside the active m x m block).
+hipError_t launch_readout_prep_wide(int H, int m, const float *R, float *M, hipStream_t s);
+
+}  // namespace cyfa

@@ -21,6 +21,11 @@ STATUS = {0: "CYFA_OK", 1: "CYFA_ERR_INVALID_ARGUMENT", 2: "CYFA_ERR_UNSUPPORTED
           3: "CYFA_ERR_WORKSPACE", 4: "CYFA_ERR_LAUNCH"}
 STORE_ROWS = 128
 
+
+def store_rows(m: int) -> int:
+    """Storage rows of the states: 128 for m <= 127, 256 for 127 < m <= 255."""
+    return STORE_ROWS if m <= 127 else 2 * STORE_ROWS
+
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
             "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
@@ -166,7 +171,7 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
     ``lens`` (optional int32 [B] device tensor): sequence b has lens[b] tokens
     (cyfa_forward_lens); rows t >= lens[b] of the outputs are not written.
     Returns ``o`` [B,T,H,dv] (dtype of q) or a dict with ``o`` and, when requested,
-    the final absolute-clock states ``K``/``V`` [B,H,128,d], ``clock`` [B,H] (float64)
+    the final absolute-clock states ``K``/``V`` [B,H,S,d] (S = store_rows(m)), ``clock`` [B,H] (float64)
     and the slot ``logits`` [B,T,H,m].
     """
     B, T, H, dk = q.shape
@@ -178,8 +183,9 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
     for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
         _need(t, (B, T, H), torch.float32, name)
     _need(R, (H, m, m), torch.float32, "R")
-    _need(K0, (B, H, STORE_ROWS, dk), torch.float32, "K0")
-    _need(V0, (B, H, STORE_ROWS, dv), torch.float32, "V0")
+    S = store_rows(m)
+    _need(K0, (B, H, S, dk), torch.float32, "K0")
+    _need(V0, (B, H, S, dv), torch.float32, "V0")
     _need(clock0, (B, H), torch.float64, "clock0")
     _need(lens, (B,), torch.int32, "lens")
     desc = forward_desc(B, T, H, dk, dv, m=m, chunk=chunk, segments=segments, scale=scale,
@@ -190,8 +196,8 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     o = out if out is not None else torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
     _need(o, (B, T, H, dv), q.dtype, "out")
-    K_out = torch.empty((B, H, STORE_ROWS, dk), dtype=torch.float32, device=dev) if return_state else None
-    V_out = torch.empty((B, H, STORE_ROWS, dv), dtype=torch.float32, device=dev) if return_state else None
+    K_out = torch.empty((B, H, S, dk), dtype=torch.float32, device=dev) if return_state else None
+    V_out = torch.empty((B, H, S, dv), dtype=torch.float32, device=dev) if return_state else None
     clk = torch.empty((B, H), dtype=torch.float64, device=dev) if return_state else None
     logits = torch.empty((B, T, H, m), dtype=torch.float32, device=dev) if return_logits else None
     st = load().cyfa_forward_lens(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),

@@ -48,10 +48,16 @@ def state_view(t, pairs, H):
     return np.stack([a[p // H, p % H] for p in pairs])
 
 
+def store_rows(m: int) -> int:
+    """Storage rows of the operator's states: 128 for m <= 127, 256 up to m = 255."""
+    return 128 if m <= 127 else 256
+
+
 def oracle_states_abs(ref: dict, m: int):
-    """Oracle relative-time final states -> padded absolute-clock storage [n, 128, d]."""
-    K = np.stack([oracle.absolute_storage(m, lam, Kr) for lam, Kr in zip(ref["lam"], ref["K"])])
-    V = np.stack([oracle.absolute_storage(m, lam, Vr) for lam, Vr in zip(ref["lam"], ref["V"])])
+    """Oracle relative-time final states -> padded absolute-clock storage [n, rows, d]."""
+    rows = store_rows(m)
+    K = np.stack([oracle.absolute_storage(m, lam, Kr, rows) for lam, Kr in zip(ref["lam"], ref["K"])])
+    V = np.stack([oracle.absolute_storage(m, lam, Vr, rows) for lam, Vr in zip(ref["lam"], ref["V"])])
     return K, V
 
 

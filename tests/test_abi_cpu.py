@@ -42,7 +42,7 @@ def test_workspace_sizes_and_kernel_selection():
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("m", 128, cyfa.CyfaError), ("m", 1, cyfa.CyfaError), ("m", 129, cyfa.CyfaError),
+    ("m", 128, cyfa.CyfaError), ("m", 1, cyfa.CyfaError), ("m", 257, cyfa.CyfaError),
     ("d_k", 96, cyfa.CyfaError), ("d_v", 0, cyfa.CyfaError), ("B", 0, cyfa.CyfaError),
     ("H", 0, cyfa.CyfaError), ("T", -1, cyfa.CyfaError), ("dtype", 5, cyfa.CyfaError),
     ("kernel", 7, cyfa.CyfaError), ("segments", -1, cyfa.CyfaError), ("chunk", 48, cyfa.CyfaError),
@@ -59,9 +59,19 @@ def test_status_codes():
     n = ctypes.c_size_t(0)
     d = cyfa.forward_desc(1, 16, 1, 64, 64, m=128)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 1
-    d = cyfa.forward_desc(1, 16, 1, 64, 64, m=255)
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, m=257)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
-    assert b"127" in lib.cyfa_last_error()
+    assert b"255" in lib.cyfa_last_error()
+    # 127 < m <= 255: 256 storage rows on the vector-ALU kernel only
+    d = cyfa.forward_desc(1, 16, 1, 64, 64, m=255)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert n.value == 256 * 256 * 4
+    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    d = cyfa.forward_desc(1, 16, 1, 256, 64, m=255)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16)
+    assert cyfa.selected_kernel(d) == "valu"
     d = cyfa.forward_desc(1, 16, 1, 96, 64)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     assert lib.cyfa_forward_workspace_size(None, ctypes.byref(n)) == 1

@@ -49,7 +49,8 @@ def test_tiny_f32_workload_full_parity():
 
 
 @pytest.mark.parametrize("variant", ["no_beta_no_R", "peaky", "small_m", "ragged_chunk8",
-                                     "d128_f32", "mixed_dims", "d256_f32", "mixed_256"])
+                                     "d128_f32", "mixed_dims", "d256_f32", "mixed_256",
+                                     "m255_d64", "m255_d128", "m255_mixed", "m129"])
 def test_f32_variants(variant):
     kw = {}
     dk = dv = 64
@@ -65,6 +66,11 @@ def test_f32_variants(variant):
         T = 70
     if variant == "mixed_256":
         dk, dv, T = 256, 64, 70
+    if variant.startswith("m255"):     # the largest slot count of the paper's ablation
+        m, T = 255, 70
+        dk, dv = {"m255_d64": (64, 64), "m255_d128": (128, 128), "m255_mixed": (128, 64)}[variant]
+    if variant == "m129":              # smallest slot count with 256 storage rows
+        m, T = 129, 53
     x = make_forward_inputs(B, T, H, dk, dv, seed=21, dtype="f32", m=m,
                             with_beta=variant != "no_beta_no_R", with_R=variant != "no_beta_no_R")
     if variant == "mixed_dims":
@@ -82,6 +88,29 @@ def test_bf16_valu_kernel_d256():
     t = upload(x)
     res = _fwd(x, t, return_state=True, return_logits=True)
     _check_full(x, res, TOL_BF16)
+
+
+def test_bf16_m255_and_resume():
+    """m = 255 (256 storage rows) with bf16 inputs; split-and-resume through the
+    256-row states equals one pass."""
+    cyfa = _cyfa()
+    x = make_forward_inputs(2, 60, 2, 128, 128, seed=25, dtype="bf16", m=255)
+    t = upload(x)
+    full = _fwd(x, t, return_state=True, return_logits=True)
+    assert full["K"].shape == (2, 2, 256, 128)
+    _check_full(x, full, TOL_BF16)
+    t1 = 29
+    a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    first = _fwd(x, a, return_state=True)
+    second = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
+                          scale=x["scale"], m=255, K0=first["K"], V0=first["V"], clock0=first["clock"],
+                          return_state=True)
+    torch.cuda.synchronize()
+    o_split = torch.cat([first["o"], second["o"]], dim=1).float().cpu().numpy()
+    assert rel_err(o_split, full["o"].float().cpu().numpy()) <= 1e-2
+    assert rel_err(second["K"].cpu().numpy(), full["K"].cpu().numpy()) <= 1e-5
+    assert clock_err(second["clock"].cpu().numpy(), full["clock"].cpu().numpy(), 255) <= 1e-9
 
 
 def test_bf16_valu_kernel():

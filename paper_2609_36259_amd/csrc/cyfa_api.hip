@@ -173,10 +173,12 @@ cyfa_status check_dec(const cyfa_dec_desc *d) {
     if (d->d_k <= 0 || d->d_v <= 0) return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
     if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
         return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64, 128 or 256");
-    if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
-        return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
-                                                               : CYFA_ERR_INVALID_ARGUMENT,
-                    "decode: m must be odd and in [3, 127] (got %d)", d->m);
+    if (d->m < 3 || d->m > cyfa::kMaxActiveWide || (d->m % 2) == 0)
+        return fail(d->m > cyfa::kMaxActiveWide && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
+                                                                   : CYFA_ERR_INVALID_ARGUMENT,
+                    "m must be odd and in [3, 255] (got %d)", d->m);
+    if (d->m > cyfa::kMaxActive && (d->d_k > 128 || d->d_v > 128))
+        return fail(CYFA_ERR_UNSUPPORTED, "m > 127 (256 storage rows) supports head dims 64 and 128");
     if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
     if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
@@ -337,7 +339,7 @@ cyfa_status cyfa_decode_workspace_size(const cyfa_dec_desc *desc, size_t *bytes)
     if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
     cyfa_status st = check_dec(desc);
     if (st != CYFA_OK) return st;
-    *bytes = round_up(cyfa::readout_f32_bytes(desc->H));
+    *bytes = round_up(cyfa::readout_bytes(desc->H, desc->m));
     return ok();
 }
 
@@ -359,7 +361,7 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     if (!aligned(clock, 8)) return fail(CYFA_ERR_INVALID_ARGUMENT, "clock must be 8-byte aligned");
     if (K == V || o == (void *)K || o == (void *)V)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias each other");
-    const size_t need = round_up(cyfa::readout_f32_bytes(desc->H));
+    const size_t need = round_up(cyfa::readout_bytes(desc->H, desc->m));
     if (!workspace || workspace_bytes < need)
         return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
     if (!aligned(workspace, kWsAlign))
@@ -372,7 +374,8 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     p.K = K; p.V = V; p.clock = clock; p.o = o; p.logits = logits_out;
     hipStream_t s = static_cast<hipStream_t>(stream);
     float *M = static_cast<float *>(workspace);
-    hipError_t e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
+    hipError_t e = p.m > cyfa::kMaxActive ? cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s)
+                                          : cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
     if (e == hipSuccess) e = mark(g_ev_start, s);
     if (e == hipSuccess) e = cyfa::launch_decode(p, M, s);
     if (e == hipSuccess) e = mark(g_ev_stop, s);

@@ -9,33 +9,37 @@
 //   z = scale M U(lambda) o',  w = softmax(z),  o'' = U(-lambda) M^T w,  M = R Phi
 //   o = Vbar^T o''
 // The step reads and writes each state once; it is bound by HBM bandwidth.
-// Each workgroup issues both of its 128 x d float states' loads at its start
+// Each workgroup issues both of its rows x d float states' loads at its start
 // (16-byte loads, consecutive lanes on consecutive addresses), so the value
 // state arrives while the key state is updated and the readout runs.
-#include "cyfa_internal.h"
+#include "cyfa_rows.h"
 
 namespace cyfa {
 
 namespace {
 
-constexpr int kThreads = 512;   // eight waves: 8 + 8 state float4 and 8 readout-matrix rows per thread
+// Threads per workgroup: eight waves for 128 storage rows (8 + 8 state float4 and
+// 8 readout-matrix rows per thread at d = 128), sixteen for 256 rows.
+__host__ __device__ constexpr int dec_threads(int rows) { return rows > kStoreRows ? 1024 : 512; }
 
-template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const float *__restrict__ Mg) {
+template <int DK, int DV, int ROWS, typename Tin>
+__global__ __launch_bounds__(dec_threads(ROWS)) void decode_kernel(DecParams p, const float *__restrict__ Mg) {
+    constexpr int kThreads = dec_threads(ROWS);
     constexpr int KQ = DK / 4;                       // float4 per key-state row
     constexpr int VQ = DV / 4;                       // float4 per value-state row
-    constexpr int KIT = kStoreRows * KQ / kThreads;  // float4 per thread (key state)
-    constexpr int VIT = kStoreRows * VQ / kThreads;  // float4 per thread (value state)
+    constexpr int KIT = ROWS * KQ / kThreads;        // float4 per thread (key state)
+    constexpr int VIT = ROWS * VQ / kThreads;        // float4 per thread (value state)
     constexpr int KROWS_PER_IT = kThreads / KQ;
     constexpr int VROWS_PER_IT = kThreads / VQ;
-    constexpr int MQ = kStoreRows / 4;               // float4 per readout-matrix row
-    constexpr int MIT = kStoreRows * MQ / kThreads;  // readout-matrix rows per thread
+    constexpr int MQ = ROWS / 4;                     // float4 per readout-matrix row
+    constexpr int MIT = ROWS * MQ / kThreads;        // readout-matrix rows per thread
+    constexpr int NQ = ROWS / 64;                    // slots per lane in the softmax
 
     __shared__ float qs[DK], ks[DK], vs[DV];
-    __shared__ float a_s[kStoreRows], op[kStoreRows], xs[kStoreRows], ws[kStoreRows];
-    __shared__ float zpart[kStoreRows][MQ + 1];
+    __shared__ float a_s[ROWS], op[ROWS], xs[ROWS], ws[ROWS];
+    __shared__ float zpart[ROWS][MQ + 1];
     __shared__ float4 ypart[kThreads / MQ][MQ];
-    __shared__ float2 cs[64];
+    __shared__ float2 cs[ROWS / 2];
     __shared__ float4 opart[kThreads / 64][VQ];
 
     const int nh = blockIdx.x;
@@ -50,8 +54,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
 
     // Both state streams are issued first (rows >= m are never touched): the
     // value state arrives while the key state is updated and the readout runs.
-    float4 *K4 = reinterpret_cast<float4 *>(p.K + (size_t)nh * kStoreRows * DK);
-    float4 *V4 = reinterpret_cast<float4 *>(p.V + (size_t)nh * kStoreRows * DV);
+    float4 *K4 = reinterpret_cast<float4 *>(p.K + (size_t)nh * ROWS * DK);
+    float4 *V4 = reinterpret_cast<float4 *>(p.V + (size_t)nh * ROWS * DV);
     const int ck = tid % KQ, cv = tid % VQ;
     float4 kreg[KIT], vreg[VIT];
 #pragma unroll
@@ -80,7 +84,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
         cs[tid] = make_float2(c, s);
     }
     __syncthreads();
-    if (tid < kStoreRows) {
+    if (tid < ROWS) {
         const int i = tid;
         float val = 0.f;
         if (i == 0) {
@@ -137,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     }
     __syncthreads();
     // ---- middle step
-    if (tid < kStoreRows) {
+    if (tid < ROWS) {
         const int i = tid;
         float x = 0.f;
         if (i == 0) {
@@ -155,7 +159,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     // wave reading two whole rows per load); the same registers serve z = M x
     // and y = M^T w.
     const int cm = tid % MQ, g = tid / MQ;
-    const float4 *M4 = reinterpret_cast<const float4 *>(Mg + (size_t)h * kStoreRows * kStoreRows);
+    const float4 *M4 = reinterpret_cast<const float4 *>(Mg + (size_t)h * ROWS * ROWS);
     float4 mreg[MIT];
 #pragma unroll
     for (int r = 0; r < MIT; ++r) mreg[r] = M4[(size_t)(MIT * g + r) * MQ + cm];
@@ -169,7 +173,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
         }
     }
     __syncthreads();
-    if (tid < kStoreRows) {
+    if (tid < ROWS) {
         float z = 0.f;
 #pragma unroll 8
         for (int c = 0; c < MQ; ++c) z += zpart[tid][c];
@@ -177,22 +181,27 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     }
     __syncthreads();
     if (wave == 0) {
-        const float z0 = ws[lane], z1 = ws[lane + 64];
-        if (p.logits) {
-            if (lane < m) p.logits[(size_t)nh * m + lane] = z0;
-            if (lane + 64 < m) p.logits[(size_t)nh * m + lane + 64] = z1;
+        float zq[NQ];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int qq = 0; qq < NQ; ++qq) {
+            zq[qq] = ws[lane + 64 * qq];
+            if (p.logits && lane + 64 * qq < m) p.logits[(size_t)nh * m + lane + 64 * qq] = zq[qq];
+            mx = fmaxf(mx, zq[qq]);
         }
-        float mx = fmaxf(z0, z1);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-        const float e0 = lane < m ? __expf(z0 - mx) : 0.f;
-        const float e1 = lane + 64 < m ? __expf(z1 - mx) : 0.f;
-        float sum = e0 + e1;
+        float sum = 0.f;
+#pragma unroll
+        for (int qq = 0; qq < NQ; ++qq) {
+            zq[qq] = lane + 64 * qq < m ? __expf(zq[qq] - mx) : 0.f;
+            sum += zq[qq];
+        }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
         const float inv = 1.f / sum;
-        ws[lane] = e0 * inv;
-        ws[lane + 64] = e1 * inv;
+#pragma unroll
+        for (int qq = 0; qq < NQ; ++qq) ws[lane + 64 * qq] = zq[qq] * inv;
     }
     __syncthreads();
     {
@@ -209,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
         ypart[g][cm] = y4;
     }
     __syncthreads();
-    if (tid < kStoreRows) {
+    if (tid < ROWS) {
         float y[2] = {0.f, 0.f};
         const int i = tid;
         // the rotation pairs paper columns (2jj+1, 2jj+2); column 0 is DC
@@ -267,14 +276,23 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecParams p, const flo
     if (tid == 0) p.clock[nh] = lam;
 }
 
+template <int DK, int DV, int ROWS>
+hipError_t launch_rows(const DecParams &p, const float *M, hipStream_t s) {
+    const dim3 grid(p.N * p.H), block(dec_threads(ROWS));
+    if (p.dtype == 0)
+        hipLaunchKernelGGL((decode_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M);
+    else
+        hipLaunchKernelGGL((decode_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M);
+    return hipGetLastError();
+}
+
+// 256 storage rows are built for head dims up to 128
 template <int DK, int DV>
 hipError_t launch_typed(const DecParams &p, const float *M, hipStream_t s) {
-    const dim3 grid(p.N * p.H), block(kThreads);
-    if (p.dtype == 0)
-        hipLaunchKernelGGL((decode_kernel<DK, DV, float>), grid, block, 0, s, p, M);
-    else
-        hipLaunchKernelGGL((decode_kernel<DK, DV, __hip_bfloat16>), grid, block, 0, s, p, M);
-    return hipGetLastError();
+    if constexpr (DK <= 128 && DV <= 128) {
+        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, s);
+    }
+    return launch_rows<DK, DV, kStoreRows>(p, M, s);
 }
 
 template <int DK>

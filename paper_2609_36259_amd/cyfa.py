@@ -286,7 +286,7 @@ def decode_workspace_size(desc: DecDesc) -> int:
 def decode_step(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, *, scale=None,
                 m=127, return_logits=False, out=None, workspace=None, stream=None):
     """One in-place decode step: q,k [N,H,dk], v [N,H,dv]; scalars [N,H] float32;
-    states K [N,H,128,dk], V [N,H,128,dv] float32 and clock [N,H] float64 (updated)."""
+    states K [N,H,S,dk], V [N,H,S,dv] float32 (S = store_rows(m)) and clock [N,H] float64 (updated)."""
     N, H, dk = q.shape
     dv = v.shape[-1]
     dt = _dtype_code(q)
@@ -295,8 +295,8 @@ def decode_step(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, 
     for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
         _need(t, (N, H), torch.float32, name)
     _need(R, (H, m, m), torch.float32, "R")
-    _need(K, (N, H, STORE_ROWS, dk), torch.float32, "K")
-    _need(V, (N, H, STORE_ROWS, dv), torch.float32, "V")
+    _need(K, (N, H, store_rows(m), dk), torch.float32, "K")
+    _need(V, (N, H, store_rows(m), dv), torch.float32, "V")
     _need(clock, (N, H), torch.float64, "clock")
     desc = decode_desc(N, H, dk, dv, m=m, scale=scale, dtype=dt)
     nbytes = decode_workspace_size(desc)

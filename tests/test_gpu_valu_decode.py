@@ -175,21 +175,21 @@ def test_nan_input_propagates_without_fault():
     assert np.isfinite(o[0, :10]).all()
 
 
-def _decode_case(N, H, d, prefix, steps, seed, dtype="f32", with_logits=True):
+def _decode_case(N, H, d, prefix, steps, seed, dtype="f32", with_logits=True, m=127):
     cyfa = _cyfa()
-    x = make_forward_inputs(N, prefix + steps, H, d, d, seed=seed, dtype=dtype)
+    x = make_forward_inputs(N, prefix + steps, H, d, d, seed=seed, dtype=dtype, m=m)
     ref = run_oracle(x)
     t = upload(x)
     pre = {k: (v[:, :prefix].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
     st = cyfa.forward(pre["q"], pre["k"], pre["v"], pre["delta"], pre["log_alpha"], pre["beta"],
-                      pre["R"], scale=x["scale"], return_state=True)
+                      pre["R"], scale=x["scale"], m=m, return_state=True)
     K, V, clk = st["K"], st["V"], st["clock"]
     outs, logits = [], []
     for s in range(steps):
         tok = {k: (v[:, prefix + s].contiguous() if v is not None and k != "R" else v)
                for k, v in t.items()}
         o, z = cyfa.decode_step(tok["q"], tok["k"], tok["v"], tok["delta"], K, V, clk,
-                                tok["log_alpha"], tok["beta"], t["R"], scale=x["scale"],
+                                tok["log_alpha"], tok["beta"], t["R"], scale=x["scale"], m=m,
                                 return_logits=True)
         outs.append(o.float().cpu().numpy())
         logits.append(z.cpu().numpy())
@@ -211,6 +211,13 @@ def _decode_case(N, H, d, prefix, steps, seed, dtype="f32", with_logits=True):
 @pytest.mark.parametrize("d", [64, 128, 256])
 def test_decode_steps_match_oracle_f32(d):
     e_o, e_z, e_K, e_c = _decode_case(3, 2, d, prefix=33, steps=6, seed=30 + d)
+    assert e_o <= TOL_F32 and e_z <= TOL_F32 and e_K <= TOL_F32 and e_c <= 1e-9
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_steps_match_oracle_m255(d):
+    """256 storage rows (m = 255): forward prefix, then decode steps, against the oracle."""
+    e_o, e_z, e_K, e_c = _decode_case(2, 2, d, prefix=21, steps=5, seed=40 + d, m=255)
     assert e_o <= TOL_F32 and e_z <= TOL_F32 and e_K <= TOL_F32 and e_c <= 1e-9
 
 

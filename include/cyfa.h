@@ -30,11 +30,14 @@
  *     default stream) with no host synchronisation.  The library holds no
  *     global mutable state (only the per-thread error text and timing hook)
  *     and may be called from several threads.
- *   - m is the number of active relative-time slots (odd, 3..127).  States are
- *     stored with 128 rows (m* = 128): rows 0..m-1 hold the absolute-clock
- *     coordinates in the basis order of App. A.1 (row 0 = DC component, row
- *     2j-1 = cosine of frequency j, row 2j = its sine) and rows m..127 are
- *     padding (App. A.7): ignored on input, written as zero on output.
+ *   - m is the number of active relative-time slots (odd, 3..255).  States are
+ *     stored with S rows, S = 128 for m <= 127 and S = 256 for 127 < m <= 255
+ *     (m* of App. A.7): rows 0..m-1 hold the absolute-clock coordinates in the
+ *     basis order of App. A.1 (row 0 = DC component, row 2j-1 = cosine of
+ *     frequency j, row 2j = its sine) and rows m..S-1 are padding: ignored on
+ *     input, written as zero on output.  Below, "128" in a state shape reads
+ *     S.  m > 127 runs the vector-ALU forward and the decode step with head
+ *     dims 64 or 128; the matrix-core kernel and the backward take m <= 127.
  *   - Clocks are double precision and are reported reduced modulo m, which is
  *     exact because U(tau + m) = U(tau) (App. A.1, Prop. 1) and the output
  *     depends only on clock differences (App. A.4, Prop. 6).
@@ -77,7 +80,7 @@ typedef enum {
  *   B, T, H      batch, tokens, heads (B, H >= 1; T >= 0; T = 0 is a no-op that
  *                still writes the final state and clock when requested)
  *   d_k, d_v     head dims: 64, 128 or 256 each (the matrix-core kernel: 128 only)
- *   m            active slots, odd, 3..127
+ *   m            active slots, odd, 3..255 (see above for m > 127)
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
  *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 32).
  *                Results do not depend on it beyond rounding (App. B: the
@@ -219,7 +222,7 @@ cyfa_status cyfa_backward(const cyfa_fwd_desc *desc,
 
 /*
  * Single-token decode descriptor: N independent streams, H heads each.
- *   d_k, d_v 64, 128 or 256; m odd 3..127; dtype of q, k, v, o.
+ *   d_k, d_v 64, 128 or 256; m odd 3..255 (m > 127: d_k, d_v <= 128); dtype of q, k, v, o.
  */
 typedef struct {
     int32_t N, H, d_k, d_v;

@@ -221,6 +221,62 @@ cyfa_status cyfa_backward(const cyfa_fwd_desc *desc,
                           void *stream);
 
 /*
+ * Mixer around the operator (Sec. 4, network design): what a CyFA layer does
+ * between its projection GEMMs and the operator, and after it.
+ *   B, T, H, d_k, d_v   shapes as for cyfa_forward (d in {64, 128, 256})
+ *   conv_size  ShortConv width K, 1..4
+ *   conv_act   0: none (the paper omits a feature map on q and k), 1: SiLU after
+ *              the convolution
+ *   eps        RMSNorm epsilon (> 0)
+ *   dtype      type of the q, k, v, o, gate inputs and of the q, k, v, out outputs
+ */
+typedef struct {
+    int32_t B, T, H, d_k, d_v;
+    int32_t conv_size;
+    int32_t conv_act;
+    float eps;
+    cyfa_dtype dtype;
+} cyfa_mixer_desc;
+
+/*
+ * Prologue: produces cyfa_forward's inputs from the raw projections.
+ *   q_in, k_in [B, T, H, d_k], v_in [B, T, H, d_v] dtype (required)
+ *   conv_q, conv_k [H*d_k, K], conv_v [H*d_v, K] float depthwise causal ShortConv
+ *              weights, y_t = sum_j w[c][j] x_{t-K+1+j} (zero before the sequence
+ *              start); NULL skips that convolution
+ *   norm_q, norm_k [d_k] float RMSNorm weights of the QK normalisation
+ *              (per head vector: x / sqrt(mean(x^2) + eps) * w); NULL skips it
+ *   z_delta, z_alpha, z_beta [B, T, H] float gate projections; b_delta,
+ *              b_alpha, A [H] float (b may be NULL: zero; A required with z_alpha):
+ *              delta = sigmoid(z_delta + b_delta) (Eq. clock_gradient_stabilization),
+ *              log_alpha = -A softplus(z_alpha + b_alpha), beta = sigmoid(z_beta);
+ *              an output is written when its projection is given
+ *   lens       [B] int32 or NULL: rows t >= lens[b] are padding (outputs 0)
+ *   q, k, v    [B, T, H, d] dtype outputs (required); must not alias the inputs
+ *   delta, log_alpha, beta   [B, T, H] float outputs
+ * 16-byte aligned tensors, 4-byte aligned scalar arrays.
+ */
+cyfa_status cyfa_mixer_prologue(const cyfa_mixer_desc *desc,
+                                const void *q_in, const void *k_in, const void *v_in,
+                                const float *conv_q, const float *conv_k, const float *conv_v,
+                                const float *norm_q, const float *norm_k,
+                                const float *z_delta, const float *b_delta,
+                                const float *z_alpha, const float *b_alpha, const float *A,
+                                const float *z_beta, const int32_t *lens,
+                                void *q, void *k, void *v,
+                                float *delta, float *log_alpha, float *beta,
+                                void *stream);
+
+/*
+ * Epilogue: out = RMSNorm(o) * norm_o * sigmoid(gate), per head vector of d_v.
+ *   o, gate, out [B, T, H, d_v] dtype (gate NULL: no gating; norm_o [d_v] float
+ *   or NULL: unit weights); rows t >= lens[b] of out are written as 0; out must
+ *   not alias o or gate.
+ */
+cyfa_status cyfa_mixer_epilogue(const cyfa_mixer_desc *desc, const void *o, const void *gate,
+                                const float *norm_o, const int32_t *lens, void *out, void *stream);
+
+/*
  * Single-token decode descriptor: N independent streams, H heads each.
  *   d_k, d_v 64, 128 or 256; m odd 3..255 (m > 127: d_k, d_v <= 128); dtype of q, k, v, o.
  */

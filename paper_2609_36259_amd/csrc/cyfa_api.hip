@@ -8,6 +8,7 @@
 
 #include "cyfa.h"
 #include "cyfa_bwd.h"
+#include "cyfa_mixer.h"
 #include "cyfa_internal.h"
 #include "cyfa_rows.h"
 
@@ -187,6 +188,32 @@ cyfa_status check_dec(const cyfa_dec_desc *d) {
 
 }  // namespace
 
+namespace {
+cyfa_status check_mixer(const cyfa_mixer_desc *d) {
+    if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
+    if (d->B < 1 || d->H < 1 || d->T < 0)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "need B >= 1, H >= 1, T >= 0");
+    if ((double)d->B * d->T * d->H * (d->d_k > d->d_v ? d->d_k : d->d_v) > 4.0e12)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "problem too large");
+    if (!head_dim_ok(d->d_k) || !head_dim_ok(d->d_v))
+        return fail(CYFA_ERR_UNSUPPORTED, "head dims must be 64, 128 or 256");
+    if (d->conv_size < 1 || d->conv_size > cyfa::kMixMaxConv)
+        return fail(CYFA_ERR_UNSUPPORTED, "conv_size must be in [1, %d]", cyfa::kMixMaxConv);
+    if (d->conv_act != 0 && d->conv_act != 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "conv_act must be 0 or 1");
+    if (!(d->eps > 0.f) || !std::isfinite(d->eps)) return fail(CYFA_ERR_INVALID_ARGUMENT, "eps must be > 0");
+    if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
+    return CYFA_OK;
+}
+
+cyfa::MixParams mixer_params(const cyfa_mixer_desc *d) {
+    cyfa::MixParams p{};
+    p.B = d->B; p.T = d->T; p.H = d->H; p.dk = d->d_k; p.dv = d->d_v;
+    p.K = d->conv_size; p.act = d->conv_act; p.eps = d->eps; p.dtype = d->dtype;
+    return p;
+}
+}  // namespace
+
 extern "C" {
 
 cyfa_status cyfa_forward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes) {
@@ -332,6 +359,68 @@ cyfa_status cyfa_backward(const cyfa_fwd_desc *desc, const void *q, const void *
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = cyfa::launch_bwd_valu(p, workspace, s);
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "backward launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+
+cyfa_status cyfa_mixer_prologue(const cyfa_mixer_desc *desc, const void *q_in, const void *k_in,
+                                const void *v_in, const float *conv_q, const float *conv_k,
+                                const float *conv_v, const float *norm_q, const float *norm_k,
+                                const float *z_delta, const float *b_delta, const float *z_alpha,
+                                const float *b_alpha, const float *A, const float *z_beta,
+                                const int32_t *lens, void *q, void *k, void *v, float *delta,
+                                float *log_alpha, float *beta, void *stream) {
+    cyfa_status st = check_mixer(desc);
+    if (st != CYFA_OK) return st;
+    if (desc->T > 0 && (!q_in || !k_in || !v_in || !q || !k || !v))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "q_in, k_in, v_in, q, k and v are required");
+    if ((z_delta && !delta) || (z_alpha && (!log_alpha || !A)) || (z_beta && !beta))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "a gate projection needs its output (and A for z_alpha)");
+    const void *vec[] = {q_in, k_in, v_in, q, k, v};
+    for (const void *p : vec)
+        if (p && !aligned(p, 16)) return fail(CYFA_ERR_INVALID_ARGUMENT, "tensors must be 16-byte aligned");
+    const void *sc[] = {conv_q, conv_k, conv_v, norm_q, norm_k, z_delta, b_delta, z_alpha, b_alpha, A,
+                        z_beta, lens, delta, log_alpha, beta};
+    for (const void *p : sc)
+        if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    {
+        const void *outs[] = {q, k, v, delta, log_alpha, beta};
+        const void *ins[] = {q_in, k_in, v_in, conv_q, conv_k, conv_v, norm_q, norm_k, z_delta, b_delta,
+                             z_alpha, b_alpha, A, z_beta, lens};
+        for (int a = 0; a < 6; ++a) {
+            if (!outs[a]) continue;
+            for (int c = a + 1; c < 6; ++c)
+                if (outs[a] == outs[c]) return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias each other");
+            for (const void *in : ins)
+                if (in == outs[a]) return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias inputs");
+        }
+    }
+    cyfa::MixParams p = mixer_params(desc);
+    p.q_in = q_in; p.k_in = k_in; p.v_in = v_in;
+    p.wq = conv_q; p.wk = conv_k; p.wv = conv_v; p.gq = norm_q; p.gk = norm_k;
+    p.z_delta = z_delta; p.b_delta = b_delta; p.z_alpha = z_alpha; p.b_alpha = b_alpha; p.A = A;
+    p.z_beta = z_beta; p.lens = lens;
+    p.q_out = q; p.k_out = k; p.v_out = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta;
+    hipError_t e = cyfa::launch_mixer_prologue(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "mixer prologue launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+cyfa_status cyfa_mixer_epilogue(const cyfa_mixer_desc *desc, const void *o, const void *gate,
+                                const float *norm_o, const int32_t *lens, void *out, void *stream) {
+    cyfa_status st = check_mixer(desc);
+    if (st != CYFA_OK) return st;
+    if (desc->T > 0 && (!o || !out)) return fail(CYFA_ERR_INVALID_ARGUMENT, "o and out are required");
+    const void *vec[] = {o, gate, out};
+    for (const void *p : vec)
+        if (p && !aligned(p, 16)) return fail(CYFA_ERR_INVALID_ARGUMENT, "tensors must be 16-byte aligned");
+    if ((norm_o && !aligned(norm_o, 4)) || (lens && !aligned(lens, 4)))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    if (out && (out == o || out == gate)) return fail(CYFA_ERR_INVALID_ARGUMENT, "out must not alias o or gate");
+    cyfa::MixParams p = mixer_params(desc);
+    p.lens = lens;
+    hipError_t e = cyfa::launch_mixer_epilogue(p, o, gate, norm_o, out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "mixer epilogue launch: %s", hipGetErrorString(e));
     return ok();
 }
 

@@ -1,0 +1,256 @@
+// Mixer prologue and epilogue around the CyFA operator (Sec. 4, network design).
+//
+// Prologue, per token t and head h:
+//   ShortConv  y_t[c] = sum_{j<K} w[c][j] x_{t-K+1+j}[c]   (causal, depthwise; zero
+//              before the sequence start), optionally SiLU, on q, k and v;
+//   QK RMSNorm q_t <- q_t / sqrt(mean(q_t^2) + eps) * g_q  (and k);
+//   gates      delta = sigmoid(z_delta + b_delta)           (Eq. clock_gradient_stabilization)
+//              log alpha = -A softplus(z_alpha + b_alpha)   (the forget-gate parameterization)
+//              beta = sigmoid(z_beta)
+// Epilogue: out_t = RMSNorm(o_t) * g_o * sigmoid(gate_t)     (head-wise RMSNorm, output gate)
+//
+// Both are streaming kernels bound by HBM bandwidth.  Thread layout: each thread
+// owns eight consecutive channels (one 16-byte bf16 load or two float4 loads per
+// token) of one head; the D / 8 threads of a head are consecutive lanes, so the
+// RMSNorm sum is a shuffle reduction inside the wave.  A workgroup walks a run of
+// kTokens consecutive tokens of one sequence, keeping the convolution's K - 1
+// previous inputs in registers.
+#include <algorithm>
+#include "cyfa_mixer.h"
+
+namespace cyfa {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kCh = 8;              // channels per thread
+constexpr int kTokens = 16;         // tokens per workgroup
+
+__device__ __forceinline__ float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
+__device__ __forceinline__ float softplus_f(float x) { return x > 20.f ? x : log1pf(__expf(x)); }
+
+__device__ __forceinline__ int mix_tokens(const int *lens, int b, int T) {
+    return lens ? min(max(lens[b], 0), T) : T;
+}
+
+__device__ __forceinline__ void load8(const float *p, float *x) {
+    const float4 a = *reinterpret_cast<const float4 *>(p);
+    const float4 b = *reinterpret_cast<const float4 *>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void load8(const __hip_bfloat16 *p, float *x) {
+    const uint4 u = *reinterpret_cast<const uint4 *>(p);
+    const unsigned w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void store8(float *p, const float *y) {
+    *reinterpret_cast<float4 *>(p) = make_float4(y[0], y[1], y[2], y[3]);
+    *reinterpret_cast<float4 *>(p + 4) = make_float4(y[4], y[5], y[6], y[7]);
+}
+__device__ __forceinline__ void store8(__hip_bfloat16 *p, const float *y) {
+    __hip_bfloat16 t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
+    *reinterpret_cast<uint4 *>(p) = *reinterpret_cast<const uint4 *>(t);
+}
+
+// sum over the D / 8 consecutive lanes of one head
+template <int D>
+__device__ __forceinline__ float head_sum(float s) {
+#pragma unroll
+    for (int o = 1; o < D / kCh; o <<= 1) s += __shfl_xor(s, o);
+    return s;
+}
+
+// ShortConv (+ SiLU) (+ RMSNorm) of one [B, T, H, D] tensor.
+template <int D, int KMAX, typename Tin>
+__global__ __launch_bounds__(kThreads) void conv_norm_kernel(const Tin *__restrict__ x, const float *__restrict__ w,
+                                                             const float *__restrict__ g, Tin *__restrict__ y,
+                                                             int T, int H, int K, int act, float eps,
+                                                             const int *__restrict__ lens) {
+    const int b = blockIdx.z, t_begin = blockIdx.y * kTokens;
+    const int c0 = (blockIdx.x * kThreads + threadIdx.x) * kCh;    // first channel of this thread
+    const int HD = H * D;
+    const bool active = c0 < HD;                                    // whole heads are active or not
+    const int Tb = mix_tokens(lens, b, T);
+    const int t_end = min(t_begin + kTokens, T);
+    // wr[i][s]: weight of x_{t-s} (tap K - 1 - s), zero for s >= K; win[s] = x_{t-s}
+    float wr[kCh][KMAX], gr[kCh], win[KMAX][kCh];
+#pragma unroll
+    for (int i = 0; i < kCh; ++i) {
+#pragma unroll
+        for (int s = 0; s < KMAX; ++s)
+            wr[i][s] = (w && active && s < K) ? w[(size_t)(c0 + i) * K + (K - 1 - s)] : 0.f;
+        gr[i] = (g && active) ? g[(c0 + i) % D] : 1.f;
+    }
+    // inputs before the run, zero before the sequence start
+#pragma unroll
+    for (int s = 1; s < KMAX; ++s) {
+        const int t = t_begin - s;
+        if (w && active && s < K && t >= 0 && t < Tb) {
+            load8(x + ((size_t)b * T + t) * HD + c0, win[s]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) win[s][i] = 0.f;
+        }
+    }
+    for (int t = t_begin; t < t_end; ++t) {
+        const bool live = t < Tb;
+        float yt[kCh];
+        if (active && live) {
+            load8(x + ((size_t)b * T + t) * HD + c0, win[0]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) win[0][i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < kCh; ++i) {
+            float acc = w ? 0.f : win[0][i];
+            if (w)
+#pragma unroll
+                for (int s = 0; s < KMAX; ++s) acc = fmaf(wr[i][s], win[s][i], acc);
+            yt[i] = act ? acc * sigm(acc) : acc;
+        }
+        if (g) {
+            float ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) ss = fmaf(yt[i], yt[i], ss);
+            const float r = rsqrtf(head_sum<D>(ss) / (float)D + eps);
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) yt[i] *= r * gr[i];
+        }
+        if (!live)
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) yt[i] = 0.f;
+        if (active) store8(y + ((size_t)b * T + t) * HD + c0, yt);
+        // slide the window: win[s] <- win[s - 1]
+#pragma unroll
+        for (int s = KMAX - 1; s >= 1; --s)
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) win[s][i] = win[s - 1][i];
+    }
+}
+
+// Scalar gates, elementwise over [B, T, H].
+__global__ __launch_bounds__(kThreads) void gates_kernel(MixParams p) {
+    const size_t n = (size_t)p.B * p.T * p.H;
+    for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += (size_t)gridDim.x * kThreads) {
+        const int h = (int)(e % p.H);
+        const int t = (int)((e / p.H) % p.T);
+        const int b = (int)(e / ((size_t)p.H * p.T));
+        const bool live = t < mix_tokens(p.lens, b, p.T);
+        if (p.z_delta) p.delta[e] = live ? sigm(p.z_delta[e] + (p.b_delta ? p.b_delta[h] : 0.f)) : 0.f;
+        if (p.z_alpha)
+            p.log_alpha[e] = live ? -p.A[h] * softplus_f(p.z_alpha[e] + (p.b_alpha ? p.b_alpha[h] : 0.f)) : 0.f;
+        if (p.z_beta) p.beta[e] = live ? sigm(p.z_beta[e]) : 0.f;
+    }
+}
+
+// Epilogue: head-wise RMSNorm and sigmoid output gate.
+template <int D, typename Tin>
+__global__ __launch_bounds__(kThreads) void norm_gate_kernel(const Tin *__restrict__ o, const Tin *__restrict__ gate,
+                                                             const float *__restrict__ g, Tin *__restrict__ out,
+                                                             int T, int H, float eps, const int *__restrict__ lens) {
+    const int b = blockIdx.z, t_begin = blockIdx.y * kTokens;
+    const int c0 = (blockIdx.x * kThreads + threadIdx.x) * kCh;
+    const int HD = H * D;
+    const bool active = c0 < HD;
+    const int Tb = mix_tokens(lens, b, T);
+    const int t_end = min(t_begin + kTokens, T);
+    float gr[kCh];
+#pragma unroll
+    for (int i = 0; i < kCh; ++i) gr[i] = (g && active) ? g[(c0 + i) % D] : 1.f;
+    for (int t = t_begin; t < t_end; ++t) {
+        const bool live = t < Tb;
+        const size_t base = ((size_t)b * T + t) * HD + c0;
+        float yt[kCh], gt[kCh];
+        if (active && live) {
+            load8(o + base, yt);
+            if (gate) load8(gate + base, gt);
+        } else {
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) yt[i] = 0.f;
+        }
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < kCh; ++i) ss = fmaf(yt[i], yt[i], ss);
+        const float r = rsqrtf(head_sum<D>(ss) / (float)D + eps);
+#pragma unroll
+        for (int i = 0; i < kCh; ++i) {
+            float v = yt[i] * r * gr[i];
+            if (gate && active && live) v *= sigm(gt[i]);
+            yt[i] = live ? v : 0.f;
+        }
+        if (active) store8(out + base, yt);
+    }
+}
+
+template <int D, typename Tin>
+hipError_t launch_conv(const MixParams &p, const void *x, const float *w, const float *g, void *y, hipStream_t s) {
+    const int HD = p.H * D;
+    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens, p.B);
+    hipLaunchKernelGGL((conv_norm_kernel<D, kMixMaxConv, Tin>), grid, dim3(kThreads), 0, s,
+                       static_cast<const Tin *>(x), w, g, static_cast<Tin *>(y), p.T, p.H, p.K, p.act, p.eps, p.lens);
+    return hipGetLastError();
+}
+
+template <typename Tin>
+hipError_t launch_conv_d(const MixParams &p, int D, const void *x, const float *w, const float *g, void *y,
+                         hipStream_t s) {
+    if (D == 64) return launch_conv<64, Tin>(p, x, w, g, y, s);
+    if (D == 128) return launch_conv<128, Tin>(p, x, w, g, y, s);
+    return launch_conv<256, Tin>(p, x, w, g, y, s);
+}
+
+template <int D, typename Tin>
+hipError_t launch_epi(const MixParams &p, const void *o, const void *gate, const float *g, void *out, hipStream_t s) {
+    const int HD = p.H * D;
+    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens, p.B);
+    hipLaunchKernelGGL((norm_gate_kernel<D, Tin>), grid, dim3(kThreads), 0, s, static_cast<const Tin *>(o),
+                       static_cast<const Tin *>(gate), g, static_cast<Tin *>(out), p.T, p.H, p.eps, p.lens);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_mixer_prologue(const MixParams &p, hipStream_t s) {
+    if (p.T == 0) return hipSuccess;
+    hipError_t e;
+    if (p.dtype == 0) {
+        e = launch_conv_d<float>(p, p.dk, p.q_in, p.wq, p.gq, p.q_out, s);
+        if (e == hipSuccess) e = launch_conv_d<float>(p, p.dk, p.k_in, p.wk, p.gk, p.k_out, s);
+        if (e == hipSuccess) e = launch_conv_d<float>(p, p.dv, p.v_in, p.wv, nullptr, p.v_out, s);
+    } else {
+        e = launch_conv_d<__hip_bfloat16>(p, p.dk, p.q_in, p.wq, p.gq, p.q_out, s);
+        if (e == hipSuccess) e = launch_conv_d<__hip_bfloat16>(p, p.dk, p.k_in, p.wk, p.gk, p.k_out, s);
+        if (e == hipSuccess) e = launch_conv_d<__hip_bfloat16>(p, p.dv, p.v_in, p.wv, nullptr, p.v_out, s);
+    }
+    if (e != hipSuccess) return e;
+    if (p.z_delta || p.z_alpha || p.z_beta) {
+        const size_t n = (size_t)p.B * p.T * p.H;
+        const int blocks = (int)std::min<size_t>((n + kThreads - 1) / kThreads, 4096);
+        hipLaunchKernelGGL(gates_kernel, dim3(blocks), dim3(kThreads), 0, s, p);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+hipError_t launch_mixer_epilogue(const MixParams &p, const void *o, const void *gate, const float *g, void *out,
+                                 hipStream_t s) {
+    if (p.T == 0) return hipSuccess;
+    const int D = p.dv;
+    if (p.dtype == 0) {
+        if (D == 64) return launch_epi<64, float>(p, o, gate, g, out, s);
+        if (D == 128) return launch_epi<128, float>(p, o, gate, g, out, s);
+        return launch_epi<256, float>(p, o, gate, g, out, s);
+    }
+    if (D == 64) return launch_epi<64, __hip_bfloat16>(p, o, gate, g, out, s);
+    if (D == 128) return launch_epi<128, __hip_bfloat16>(p, o, gate, g, out, s);
+    return launch_epi<256, __hip_bfloat16>(p, o, gate, g, out, s);
+}
+
+}  // namespace cyfa

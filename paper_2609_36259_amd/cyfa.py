@@ -28,7 +28,8 @@ def store_rows(m: int) -> int:
 
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
-            "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
+            "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_mixer_prologue",
+            "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
             "cyfa_status_string", "cyfa_last_error", "cyfa_version")
 
 
@@ -44,6 +45,12 @@ class FwdDesc(ctypes.Structure):
                 ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("m", ctypes.c_int32),
                 ("chunk", ctypes.c_int32), ("segments", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("dtype", ctypes.c_int32), ("kernel", ctypes.c_int32)]
+
+
+class MixDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("conv_size", ctypes.c_int32),
+                ("conv_act", ctypes.c_int32), ("eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
 
 
 class DecDesc(ctypes.Structure):
@@ -76,6 +83,10 @@ def load() -> ctypes.CDLL:
         lib.cyfa_backward_workspace_size.restype = ctypes.c_int
         lib.cyfa_backward.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 25 + [ctypes.c_size_t, _vp]
         lib.cyfa_backward.restype = ctypes.c_int
+        lib.cyfa_mixer_prologue.argtypes = [ctypes.POINTER(MixDesc)] + [_vp] * 22
+        lib.cyfa_mixer_prologue.restype = ctypes.c_int
+        lib.cyfa_mixer_epilogue.argtypes = [ctypes.POINTER(MixDesc)] + [_vp] * 6
+        lib.cyfa_mixer_epilogue.restype = ctypes.c_int
         lib.cyfa_decode_workspace_size.argtypes = [ctypes.POINTER(DecDesc),
                                                    ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_decode_workspace_size.restype = ctypes.c_int
@@ -271,6 +282,54 @@ def backward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, d_o, scale=No
         _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
     _check(st)
     return g
+
+
+def mixer_prologue(q_in, k_in, v_in, *, conv_q=None, conv_k=None, conv_v=None, norm_q=None,
+                   norm_k=None, z_delta=None, b_delta=None, z_alpha=None, b_alpha=None, A=None,
+                   z_beta=None, lens=None, conv_size=4, conv_act=0, eps=1e-6, stream=None):
+    """ShortConv (+ SiLU) of q, k, v, RMSNorm of q and k, and the gate activations
+    (cyfa_mixer_prologue).  Returns q, k, v and delta / log_alpha / beta (None where
+    the projection is None)."""
+    B, T, H, dk = q_in.shape
+    dv = v_in.shape[-1]
+    _need(k_in, (B, T, H, dk), q_in.dtype, "k_in")
+    _need(v_in, (B, T, H, dv), q_in.dtype, "v_in")
+    for name, t, d in (("conv_q", conv_q, dk), ("conv_k", conv_k, dk), ("conv_v", conv_v, dv)):
+        _need(t, (H * d, conv_size), torch.float32, name)
+    _need(norm_q, (dk,), torch.float32, "norm_q")
+    _need(norm_k, (dk,), torch.float32, "norm_k")
+    for name, t in (("z_delta", z_delta), ("z_alpha", z_alpha), ("z_beta", z_beta)):
+        _need(t, (B, T, H), torch.float32, name)
+    for name, t in (("b_delta", b_delta), ("b_alpha", b_alpha), ("A", A)):
+        _need(t, (H,), torch.float32, name)
+    _need(lens, (B,), torch.int32, "lens")
+    desc = MixDesc(B, T, H, dk, dv, conv_size, conv_act, eps, _dtype_code(q_in))
+    dev = q_in.device
+    out = {"q": torch.empty_like(q_in), "k": torch.empty_like(k_in), "v": torch.empty_like(v_in)}
+    for name, z in (("delta", z_delta), ("log_alpha", z_alpha), ("beta", z_beta)):
+        out[name] = torch.empty((B, T, H), dtype=torch.float32, device=dev) if z is not None else None
+    st = load().cyfa_mixer_prologue(
+        ctypes.byref(desc), _ptr(q_in), _ptr(k_in), _ptr(v_in), _ptr(conv_q), _ptr(conv_k),
+        _ptr(conv_v), _ptr(norm_q), _ptr(norm_k), _ptr(z_delta), _ptr(b_delta), _ptr(z_alpha),
+        _ptr(b_alpha), _ptr(A), _ptr(z_beta), _ptr(lens), _ptr(out["q"]), _ptr(out["k"]),
+        _ptr(out["v"]), _ptr(out["delta"]), _ptr(out["log_alpha"]), _ptr(out["beta"]),
+        _stream_handle(stream))
+    _check(st)
+    return out
+
+
+def mixer_epilogue(o, gate=None, norm_o=None, *, lens=None, eps=1e-6, out=None, stream=None):
+    """RMSNorm(o) * norm_o * sigmoid(gate) per head vector (cyfa_mixer_epilogue)."""
+    B, T, H, dv = o.shape
+    _need(gate, (B, T, H, dv), o.dtype, "gate")
+    _need(norm_o, (dv,), torch.float32, "norm_o")
+    _need(lens, (B,), torch.int32, "lens")
+    res = out if out is not None else torch.empty_like(o)
+    _need(res, (B, T, H, dv), o.dtype, "out")
+    desc = MixDesc(B, T, H, dv, dv, 1, 0, eps, _dtype_code(o))
+    _check(load().cyfa_mixer_epilogue(ctypes.byref(desc), _ptr(o), _ptr(gate), _ptr(norm_o),
+                                      _ptr(lens), _ptr(res), _stream_handle(stream)))
+    return res
 
 
 def decode_desc(N, H, dk, dv, *, m=127, scale=None, dtype=F32) -> DecDesc:

@@ -10,8 +10,9 @@ Extra fields: ``roofline`` of the dominant kernel (the fused chunk kernel, timed
 alone with HIP events the library records on its launch stream), ``mfma``
 (algorithmic TFLOP/s against the bf16 dense MFMA peak), ``cpu_baseline`` (the
 fp64 CPU oracle timed on a bounded sample of the same workload on this host),
-``decode`` (the single-token decode step at 256 streams x 16 heads) and
-``backward`` (cyfa_backward on the same workload).
+``decode`` (the single-token decode step at 256 streams x 16 heads),
+``backward`` (cyfa_backward on the same workload) and ``mixer`` (the mixer
+prologue and epilogue kernels at the same shape).
 """
 from __future__ import annotations
 
@@ -298,6 +299,52 @@ def backward_bench(args, torch, cyfa, w):
                           "frac": tfl / PEAK_F32_TFLOPS})
 
 
+def mixer_bench(args, torch, cyfa, w):
+    """cyfa_mixer_prologue and cyfa_mixer_epilogue on the benchmark workload's shape
+    (bf16 projections, ShortConv width 4, QK RMSNorm, all three gates; synthetic
+    weights), each timed alone with HIP events over 50 launches."""
+    dev = torch.device("cuda:0")
+    B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+    g = torch.Generator(device=dev)
+    g.manual_seed(6)
+    rnd = lambda *s, dt=torch.float32: torch.randn(s, device=dev, generator=g).to(dt)  # noqa: E731
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    q, k, v = rnd(B, T, H, dk, dt=dt), rnd(B, T, H, dk, dt=dt), rnd(B, T, H, dv, dt=dt)
+    wq, wk, wv = 0.5 * rnd(H * dk, 4), 0.5 * rnd(H * dk, 4), 0.5 * rnd(H * dv, 4)
+    nq, nk, no = rnd(dk) + 1, rnd(dk) + 1, rnd(dv) + 1
+    zd, za, zb = rnd(B, T, H), rnd(B, T, H), rnd(B, T, H)
+    bd, ba, A = rnd(H), rnd(H), rnd(H).exp()
+    o, gate = rnd(B, T, H, dv, dt=dt), rnd(B, T, H, dv, dt=dt)
+    out = torch.empty_like(o)
+
+    def pro():
+        return cyfa.mixer_prologue(q, k, v, conv_q=wq, conv_k=wk, conv_v=wv, norm_q=nq, norm_k=nk,
+                                   z_delta=zd, b_delta=bd, z_alpha=za, b_alpha=ba, A=A, z_beta=zb)
+
+    def epi():
+        return cyfa.mixer_epilogue(o, gate, no, out=out)
+
+    res = {"workload": w.name}
+    es = 2 if dt == torch.bfloat16 else 4
+    nbytes = {"prologue": 2 * (2 * dk + dv) * B * T * H * es + 6 * B * T * H * 4,
+              "epilogue": 3 * dv * B * T * H * es}
+    for name, fn in (("prologue", pro), ("epilogue", epi)):
+        for _ in range(5):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        n = 50
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / n
+        gbs = nbytes[name] / (ms * 1e-3) / 1e9
+        res[name] = {"ms": ms, "bytes": nbytes[name], "achieved_gbs": gbs, "peak_gbs": PEAK_HBM_GBS,
+                     "frac": gbs / PEAK_HBM_GBS}
+    return res
+
+
 def cpu_baseline(w, budget_s: float):
     """Time the CPU oracle on a bounded sample of the workload (leading (b, h)
     sequences, leading tokens), sized to about `budget_s` seconds."""
@@ -340,6 +387,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
+    ap.add_argument("--no-mixer", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -411,6 +459,8 @@ def main():
         line["decode"] = decode_bench(args, torch, cyfa)
     if not args.no_backward:
         line["backward"] = backward_bench(args, torch, cyfa, w)
+    if not args.no_mixer:
+        line["mixer"] = mixer_bench(args, torch, cyfa, w)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)

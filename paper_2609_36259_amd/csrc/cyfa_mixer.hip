@@ -25,6 +25,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCh = 8;              // channels per thread
 constexpr int kTokens = 16;         // tokens per workgroup
+static_assert(kMixMaxConv % 4 == 0, "16-byte tap loads");
 
 __device__ __forceinline__ float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
 __device__ __forceinline__ float softplus_f(float x) { return x > 20.f ? x : log1pf(__expf(x)); }
@@ -66,13 +67,23 @@ __device__ __forceinline__ float head_sum(float s) {
     return s;
 }
 
-// ShortConv (+ SiLU) (+ RMSNorm) of one [B, T, H, D] tensor.
+// Up to three [B, T, H, D] tensors (q, k, v) in one launch: blockIdx.z = tensor * B + b.
+struct ConvSet {
+    const void *x[3];
+    const float *w[3];
+    const float *g[3];
+    void *y[3];
+};
+
+// ShortConv (+ SiLU) (+ RMSNorm) of the tensors of a ConvSet.
 template <int D, int KMAX, typename Tin>
-__global__ __launch_bounds__(kThreads) void conv_norm_kernel(const Tin *__restrict__ x, const float *__restrict__ w,
-                                                             const float *__restrict__ g, Tin *__restrict__ y,
-                                                             int T, int H, int K, int act, float eps,
-                                                             const int *__restrict__ lens) {
-    const int b = blockIdx.z, t_begin = blockIdx.y * kTokens;
+__global__ __launch_bounds__(kThreads) void conv_norm_kernel(ConvSet cs, int B, int T, int H, int K, int act,
+                                                             float eps, const int *__restrict__ lens) {
+    const int tensor = blockIdx.z / B, b = blockIdx.z % B, t_begin = blockIdx.y * kTokens;
+    const Tin *__restrict__ x = static_cast<const Tin *>(cs.x[tensor]);
+    const float *__restrict__ w = cs.w[tensor];
+    const float *__restrict__ g = cs.g[tensor];
+    Tin *__restrict__ y = static_cast<Tin *>(cs.y[tensor]);
     const int c0 = (blockIdx.x * kThreads + threadIdx.x) * kCh;    // first channel of this thread
     const int HD = H * D;
     const bool active = c0 < HD;                                    // whole heads are active or not
@@ -80,13 +91,29 @@ __global__ __launch_bounds__(kThreads) void conv_norm_kernel(const Tin *__restri
     const int t_end = min(t_begin + kTokens, T);
     // wr[i][s]: weight of x_{t-s} (tap K - 1 - s), zero for s >= K; win[s] = x_{t-s}
     float wr[kCh][KMAX], gr[kCh], win[KMAX][kCh];
+    if (w && active && K == KMAX) {
+        // the eight channels' taps are KMAX * 8 consecutive floats: 16-byte loads
+        const float4 *w4 = reinterpret_cast<const float4 *>(w + (size_t)c0 * KMAX);
 #pragma unroll
-    for (int i = 0; i < kCh; ++i) {
+        for (int i = 0; i < kCh; ++i) {
+            float tap[KMAX];
 #pragma unroll
-        for (int s = 0; s < KMAX; ++s)
-            wr[i][s] = (w && active && s < K) ? w[(size_t)(c0 + i) * K + (K - 1 - s)] : 0.f;
-        gr[i] = (g && active) ? g[(c0 + i) % D] : 1.f;
+            for (int q = 0; q < KMAX / 4; ++q) {
+                const float4 f = w4[i * (KMAX / 4) + q];
+                tap[4 * q] = f.x; tap[4 * q + 1] = f.y; tap[4 * q + 2] = f.z; tap[4 * q + 3] = f.w;
+            }
+#pragma unroll
+            for (int s = 0; s < KMAX; ++s) wr[i][s] = tap[KMAX - 1 - s];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kCh; ++i)
+#pragma unroll
+            for (int s = 0; s < KMAX; ++s)
+                wr[i][s] = (w && active && s < K) ? w[(size_t)(c0 + i) * K + (K - 1 - s)] : 0.f;
     }
+#pragma unroll
+    for (int i = 0; i < kCh; ++i) gr[i] = (g && active) ? g[(c0 + i) % D] : 1.f;
     // inputs before the run, zero before the sequence start
 #pragma unroll
     for (int s = 1; s < KMAX; ++s) {
@@ -98,40 +125,54 @@ __global__ __launch_bounds__(kThreads) void conv_norm_kernel(const Tin *__restri
             for (int i = 0; i < kCh; ++i) win[s][i] = 0.f;
         }
     }
-    for (int t = t_begin; t < t_end; ++t) {
-        const bool live = t < Tb;
-        float yt[kCh];
-        if (active && live) {
-            load8(x + ((size_t)b * T + t) * HD + c0, win[0]);
-        } else {
+    // four tokens per step: their loads are issued together
+    constexpr int kU = 4;
+    for (int t0 = t_begin; t0 < t_end; t0 += kU) {
+        float xin[kU][kCh];
 #pragma unroll
-            for (int i = 0; i < kCh; ++i) win[0][i] = 0.f;
+        for (int u = 0; u < kU; ++u) {
+            const int t = t0 + u;
+            if (active && t < t_end && t < Tb) {
+                load8(x + ((size_t)b * T + t) * HD + c0, xin[u]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < kCh; ++i) xin[u][i] = 0.f;
+            }
         }
 #pragma unroll
-        for (int i = 0; i < kCh; ++i) {
-            float acc = w ? 0.f : win[0][i];
-            if (w)
+        for (int u = 0; u < kU; ++u) {
+            const int t = t0 + u;
+            if (t >= t_end) break;
+            const bool live = t < Tb;
+            float yt[kCh];
 #pragma unroll
-                for (int s = 0; s < KMAX; ++s) acc = fmaf(wr[i][s], win[s][i], acc);
-            yt[i] = act ? acc * sigm(acc) : acc;
+            for (int i = 0; i < kCh; ++i) win[0][i] = xin[u][i];
+#pragma unroll
+            for (int i = 0; i < kCh; ++i) {
+                float acc = w ? 0.f : win[0][i];
+                if (w)
+#pragma unroll
+                    for (int s = 0; s < KMAX; ++s) acc = fmaf(wr[i][s], win[s][i], acc);
+                yt[i] = act ? acc * sigm(acc) : acc;
+            }
+            if (g) {
+                float ss = 0.f;
+#pragma unroll
+                for (int i = 0; i < kCh; ++i) ss = fmaf(yt[i], yt[i], ss);
+                const float r = rsqrtf(head_sum<D>(ss) / (float)D + eps);
+#pragma unroll
+                for (int i = 0; i < kCh; ++i) yt[i] *= r * gr[i];
+            }
+            if (!live)
+#pragma unroll
+                for (int i = 0; i < kCh; ++i) yt[i] = 0.f;
+            if (active) store8(y + ((size_t)b * T + t) * HD + c0, yt);
+            // slide the window: win[s] <- win[s - 1]
+#pragma unroll
+            for (int s = KMAX - 1; s >= 1; --s)
+#pragma unroll
+                for (int i = 0; i < kCh; ++i) win[s][i] = win[s - 1][i];
         }
-        if (g) {
-            float ss = 0.f;
-#pragma unroll
-            for (int i = 0; i < kCh; ++i) ss = fmaf(yt[i], yt[i], ss);
-            const float r = rsqrtf(head_sum<D>(ss) / (float)D + eps);
-#pragma unroll
-            for (int i = 0; i < kCh; ++i) yt[i] *= r * gr[i];
-        }
-        if (!live)
-#pragma unroll
-            for (int i = 0; i < kCh; ++i) yt[i] = 0.f;
-        if (active) store8(y + ((size_t)b * T + t) * HD + c0, yt);
-        // slide the window: win[s] <- win[s - 1]
-#pragma unroll
-        for (int s = KMAX - 1; s >= 1; --s)
-#pragma unroll
-            for (int i = 0; i < kCh; ++i) win[s][i] = win[s - 1][i];
     }
 }
 
@@ -190,20 +231,30 @@ __global__ __launch_bounds__(kThreads) void norm_gate_kernel(const Tin *__restri
 }
 
 template <int D, typename Tin>
-hipError_t launch_conv(const MixParams &p, const void *x, const float *w, const float *g, void *y, hipStream_t s) {
+hipError_t launch_conv(const MixParams &p, const ConvSet &cs, int n, hipStream_t s) {
     const int HD = p.H * D;
-    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens, p.B);
-    hipLaunchKernelGGL((conv_norm_kernel<D, kMixMaxConv, Tin>), grid, dim3(kThreads), 0, s,
-                       static_cast<const Tin *>(x), w, g, static_cast<Tin *>(y), p.T, p.H, p.K, p.act, p.eps, p.lens);
+    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens, n * p.B);
+    hipLaunchKernelGGL((conv_norm_kernel<D, kMixMaxConv, Tin>), grid, dim3(kThreads), 0, s, cs, p.B, p.T, p.H,
+                       p.K, p.act, p.eps, p.lens);
     return hipGetLastError();
 }
 
 template <typename Tin>
-hipError_t launch_conv_d(const MixParams &p, int D, const void *x, const float *w, const float *g, void *y,
-                         hipStream_t s) {
-    if (D == 64) return launch_conv<64, Tin>(p, x, w, g, y, s);
-    if (D == 128) return launch_conv<128, Tin>(p, x, w, g, y, s);
-    return launch_conv<256, Tin>(p, x, w, g, y, s);
+hipError_t launch_conv_d(const MixParams &p, int D, const ConvSet &cs, int n, hipStream_t s) {
+    if (D == 64) return launch_conv<64, Tin>(p, cs, n, s);
+    if (D == 128) return launch_conv<128, Tin>(p, cs, n, s);
+    return launch_conv<256, Tin>(p, cs, n, s);
+}
+
+// q, k and v in one launch when d_k = d_v, else q and k together and v alone
+template <typename Tin>
+hipError_t launch_qkv(const MixParams &p, hipStream_t s) {
+    ConvSet qkv{{p.q_in, p.k_in, p.v_in}, {p.wq, p.wk, p.wv}, {p.gq, p.gk, nullptr}, {p.q_out, p.k_out, p.v_out}};
+    if (p.dk == p.dv) return launch_conv_d<Tin>(p, p.dk, qkv, 3, s);
+    hipError_t e = launch_conv_d<Tin>(p, p.dk, qkv, 2, s);
+    if (e != hipSuccess) return e;
+    ConvSet v{{p.v_in, nullptr, nullptr}, {p.wv, nullptr, nullptr}, {nullptr, nullptr, nullptr}, {p.v_out, nullptr, nullptr}};
+    return launch_conv_d<Tin>(p, p.dv, v, 1, s);
 }
 
 template <int D, typename Tin>
@@ -219,16 +270,7 @@ hipError_t launch_epi(const MixParams &p, const void *o, const void *gate, const
 
 hipError_t launch_mixer_prologue(const MixParams &p, hipStream_t s) {
     if (p.T == 0) return hipSuccess;
-    hipError_t e;
-    if (p.dtype == 0) {
-        e = launch_conv_d<float>(p, p.dk, p.q_in, p.wq, p.gq, p.q_out, s);
-        if (e == hipSuccess) e = launch_conv_d<float>(p, p.dk, p.k_in, p.wk, p.gk, p.k_out, s);
-        if (e == hipSuccess) e = launch_conv_d<float>(p, p.dv, p.v_in, p.wv, nullptr, p.v_out, s);
-    } else {
-        e = launch_conv_d<__hip_bfloat16>(p, p.dk, p.q_in, p.wq, p.gq, p.q_out, s);
-        if (e == hipSuccess) e = launch_conv_d<__hip_bfloat16>(p, p.dk, p.k_in, p.wk, p.gk, p.k_out, s);
-        if (e == hipSuccess) e = launch_conv_d<__hip_bfloat16>(p, p.dv, p.v_in, p.wv, nullptr, p.v_out, s);
-    }
+    hipError_t e = p.dtype == 0 ? launch_qkv<float>(p, s) : launch_qkv<__hip_bfloat16>(p, s);
     if (e != hipSuccess) return e;
     if (p.z_delta || p.z_alpha || p.z_beta) {
         const size_t n = (size_t)p.B * p.T * p.H;

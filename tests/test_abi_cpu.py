@@ -160,3 +160,33 @@ def test_backward_rejects_before_launch():
     assert _call_backward(d, dict(good, q=base + 8), base, need) == 1                # misaligned
     assert _call_backward(d, good, 0, 0) == 3
     assert _call_backward(d, good, base, need - 1) == 3
+
+
+def _call_prologue(desc, ptrs):
+    lib = cyfa.load()
+    names = ("q_in", "k_in", "v_in", "conv_q", "conv_k", "conv_v", "norm_q", "norm_k", "z_delta",
+             "b_delta", "z_alpha", "b_alpha", "A", "z_beta", "lens", "q", "k", "v", "delta",
+             "log_alpha", "beta")
+    args = [ptrs.get(k) for k in names]
+    return lib.cyfa_mixer_prologue(ctypes.byref(desc), *[ctypes.c_void_p(a) if a else None for a in args], None)
+
+
+def test_mixer_rejects_before_launch():
+    base = 1 << 40
+    slot = iter(range(1, 64))
+    good = {k: base + (next(slot) << 20) for k in ("q_in", "k_in", "v_in", "q", "k", "v")}
+    d = cyfa.MixDesc(1, 16, 2, 64, 64, 4, 0, 1e-6, cyfa.F32)
+    assert _call_prologue(d, {k: v for k, v in good.items() if k != "q"}) == 1
+    assert _call_prologue(d, dict(good, z_alpha=base + (40 << 20), log_alpha=base + (41 << 20))) == 1  # no A
+    assert _call_prologue(d, dict(good, z_delta=base + (42 << 20))) == 1                            # no output
+    assert _call_prologue(d, dict(good, q=good["q_in"])) == 1                                       # aliasing
+    assert _call_prologue(d, dict(good, q_in=base + 8)) == 1                                        # misaligned
+    for field, value, status in (("conv_size", 5, 2), ("conv_size", 0, 2), ("conv_act", 2, 1),
+                                 ("eps", 0.0, 1), ("d_k", 96, 2), ("dtype", 7, 1)):
+        bad = cyfa.MixDesc(1, 16, 2, 64, 64, 4, 0, 1e-6, cyfa.F32)
+        setattr(bad, field, value)
+        assert _call_prologue(bad, good) == status, field
+    lib = cyfa.load()
+    out = base + (50 << 20)
+    assert lib.cyfa_mixer_epilogue(ctypes.byref(d), ctypes.c_void_p(out), None, None, None,
+                                   ctypes.c_void_p(out), None) == 1                             # out aliases o

@@ -398,7 +398,7 @@ def main():
         ap.error("--steps must be at least 1 and --warmup at least 0")
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}, "
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}, "
               f"WORLD_SIZE={world}); the operator's multi-GPU sharding is a design, not "
               "built here", file=sys.stderr)
         sys.exit(2)

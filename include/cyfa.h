@@ -56,7 +56,7 @@ extern "C" {
 typedef enum {
     CYFA_OK = 0,
     CYFA_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, bad size, bad enum   */
-    CYFA_ERR_UNSUPPORTED = 2,      /* valid request this build does not implement   */
+    CYFA_ERR_UNSUPPORTED = 2,      /* valid request the library does not implement  */
     CYFA_ERR_WORKSPACE = 3,        /* workspace missing or smaller than required     */
     CYFA_ERR_LAUNCH = 4            /* the HIP runtime refused a launch               */
 } cyfa_status;

@@ -49,6 +49,7 @@ constexpr int kC = kBwdChunk;
 constexpr int kNT = 512;            // threads per workgroup (two waves per SIMD)
 constexpr int kRP = kNT / kStoreRows; // threads sharing one state row in the row layouts
 constexpr int kRQ = kC * kStoreRows / kNT;   // token rows per thread in the readout products
+constexpr int kReadoutThreads = kNT;           // the readout kernel (1024 measured slower: spills)
 constexpr int kLD = kStoreRows + 4; // padded row of a [token][basis] tile (16-byte rows)
 constexpr float kTwoPi = 6.283185307179586f;
 constexpr int kCombBlocks = 8;      // workgroups per sequence of the group-combine kernels
@@ -79,6 +80,7 @@ struct ChunkTab {
 // Loads the chunk's scalars (rows at or past the sequence's end: no shift, no
 // decay, no write), forms the clock and log-decay prefix sums and the phase
 // table.  Ends with a barrier.
+template <int NT = kNT>
 __device__ void chunk_tables(const BwdParams &p, int b, int h, int t0, int Tb, double lam_in,
                              ChunkTab &s, int tid) {
     if (tid < kC) {
@@ -102,7 +104,7 @@ __device__ void chunk_tables(const BwdParams &p, int b, int h, int t0, int Tb, d
     }
     __syncthreads();
     const int J = (p.m - 1) / 2;
-    for (int e = tid; e < kC * 64; e += kNT) {
+    for (int e = tid; e < kC * 64; e += NT) {
         const int r = e >> 6, jj = e & 63;
         float c = 1.f, sn = 0.f;
         if (jj < J) clock_phase(s.lam[r], jj + 1, p.m, &c, &sn);
@@ -119,8 +121,9 @@ __device__ __forceinline__ float write_entry(const ChunkTab &s, int m, int r, in
     const float2 cs = s.cs[r][(i - 1) >> 1];
     return (i & 1) ? be * ac * cs.x : -be * ac * cs.y;
 }
+template <int NT = kNT>
 __device__ void build_writes(const ChunkTab &s, int m, float (*A)[kLD], int tid) {
-    for (int e = tid; e < kC * kStoreRows; e += kNT) {
+    for (int e = tid; e < kC * kStoreRows; e += NT) {
         const int r = e >> 7, i = e & 127;
         A[r][i] = write_entry(s, m, r, i, s.beta[r]);
     }
@@ -128,9 +131,10 @@ __device__ void build_writes(const ChunkTab &s, int m, float (*A)[kLD], int tid)
 
 // Y_r <- mul * U(sign lambda_r) Y_r for every row, in place: element 0 is scaled,
 // pair (2j-1, 2j) rotated by sign * 2 pi j lambda_r / m; padding rows untouched.
+template <int NT = kNT>
 __device__ void rotate_rows(float (*Y)[kLD], const ChunkTab &s, int m, float sign, float mul, int tid) {
     const int J = (m - 1) / 2;
-    for (int e = tid; e < kC * 64; e += kNT) {
+    for (int e = tid; e < kC * 64; e += NT) {
         const int r = e >> 6, j = e & 63;
         if (j == 0) {
             Y[r][0] *= mul;
@@ -154,16 +158,17 @@ __device__ __forceinline__ float rot_grad(const float *dZ, const float *Z, int m
 }
 
 // Products with the readout matrix over the m active entries, register-blocked:
-// thread (column col = tid % 128, rows kRQ (tid / 128) .. + kRQ - 1) keeps kRQ
-// independent sums.  TRANS = false: out_r = M in_r (out[r][i] = sum_j M[i][j] in[r][j]);
+// thread (column col = tid % 128, rows RQ (tid / 128) .. + RQ - 1, RQ = 16 * 128 /
+// threads) keeps RQ independent sums.  TRANS = false: out_r = M in_r (out[r][i] = sum_j M[i][j] in[r][j]);
 // TRANS = true: out_r = M^T in_r.  Entries >= m of out are 0.
-template <bool TRANS>
+template <bool TRANS, int NT = kNT>
 __device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], float (*out)[kLD], int m,
                                 int tid) {
-    const int col = tid & 127, r0 = (tid >> 7) * kRQ;
-    float acc[kRQ];
+    constexpr int RQ = kC * kStoreRows / NT;
+    const int col = tid & 127, r0 = (tid >> 7) * RQ;
+    float acc[RQ];
 #pragma unroll
-    for (int q = 0; q < kRQ; ++q) acc[q] = 0.f;
+    for (int q = 0; q < RQ; ++q) acc[q] = 0.f;
     if (col < m) {
         // four entries per step (16-byte rows; entries m .. 127 of in are 0, and M
         // is 0 outside its active block, so running to a multiple of four is exact)
@@ -176,29 +181,31 @@ __device__ void readout_product(const float (*Ms)[kLD], const float (*in)[kLD], 
                 mv = *reinterpret_cast<const float4 *>(&Ms[col][j]);
             }
 #pragma unroll
-            for (int q = 0; q < kRQ; ++q) {
+            for (int q = 0; q < RQ; ++q) {
                 const float4 x = *reinterpret_cast<const float4 *>(&in[r0 + q][j]);
                 acc[q] = fmaf(mv.x, x.x, fmaf(mv.y, x.y, fmaf(mv.z, x.z, fmaf(mv.w, x.w, acc[q]))));
             }
         }
     }
 #pragma unroll
-    for (int q = 0; q < kRQ; ++q) out[r0 + q][col] = acc[q];
+    for (int q = 0; q < RQ; ++q) out[r0 + q][col] = acc[q];
 }
 
 // out[r][i] += sum_s S[r][s] A[s][i] for a causal (lower-triangular) score tile S.
+template <int NT = kNT>
 __device__ void add_scores_times(const float (*S)[kC + 1], const float (*A)[kLD], float (*out)[kLD], int tid) {
-    const int col = tid & 127, r0 = (tid >> 7) * kRQ;
-    float acc[kRQ];
+    constexpr int RQ = kC * kStoreRows / NT;
+    const int col = tid & 127, r0 = (tid >> 7) * RQ;
+    float acc[RQ];
 #pragma unroll
-    for (int q = 0; q < kRQ; ++q) acc[q] = out[r0 + q][col];
-    for (int s = 0; s < r0 + kRQ; ++s) {
+    for (int q = 0; q < RQ; ++q) acc[q] = out[r0 + q][col];
+    for (int s = 0; s < r0 + RQ; ++s) {
         const float a = A[s][col];
 #pragma unroll
-        for (int q = 0; q < kRQ; ++q) acc[q] = fmaf(S[r0 + q][s], a, acc[q]);
+        for (int q = 0; q < RQ; ++q) acc[q] = fmaf(S[r0 + q][s], a, acc[q]);
     }
 #pragma unroll
-    for (int q = 0; q < kRQ; ++q) out[r0 + q][col] = acc[q];
+    for (int q = 0; q < RQ; ++q) out[r0 + q][col] = acc[q];
 }
 
 template <typename Tin>
@@ -344,8 +351,9 @@ __global__ __launch_bounds__(kNT) void bwd_states_combine_kernel(BwdParams p) {
 // ---------------------------------------------------------------------------
 // (2) readout recomputation and its adjoint, per (sequence, chunk group).
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
-    constexpr int KH = DK / kRP, VH = DV / kRP, MH = kStoreRows / kRP;
+__global__ __launch_bounds__(kReadoutThreads) void bwd_readout_kernel(BwdParams p) {
+    constexpr int NT = kReadoutThreads, RP = NT / kStoreRows;
+    constexpr int KH = DK / RP, VH = DV / RP, MH = kStoreRows / RP;
     constexpr int DM = DK > DV ? DK : DV;
     __shared__ __attribute__((aligned(16))) float Ms[kStoreRows][kLD];
     __shared__ float In0[kC][DM + 1];       // Q, then dO
@@ -357,11 +365,11 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
     __shared__ float dlu[kC];
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int i = tid / kRP, part = tid % kRP, m = p.m;
+    const int i = tid / RP, part = tid % RP, m = p.m;
     const int Tb = bwd_tokens(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
     const float *Mh = p.M + (size_t)h * kStoreRows * kStoreRows;
-    for (int e = tid; e < kStoreRows * kStoreRows; e += kNT) Ms[e >> 7][e & 127] = Mh[e];
+    for (int e = tid; e < kStoreRows * kStoreRows; e += NT) Ms[e >> 7][e & 127] = Mh[e];
     float dMacc[MH];                        // dM[i][MH part .. MH part + MH - 1]
 #pragma unroll
     for (int jj = 0; jj < MH; ++jj) dMacc[jj] = 0.f;
@@ -369,14 +377,14 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC;
         const size_t row0 = (size_t)bh * p.Tpad + t0;
-        for (int e = tid; e < kC * DK; e += kNT) {
+        for (int e = tid; e < kC * DK; e += NT) {
             const int r = e / DK, cc = e % DK;
             const bool live = t0 + r < Tb;
             In0[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, live);
             In1[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, live);
         }
-        chunk_tables(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
-        build_writes(tab, m, As, tid);
+        chunk_tables<NT>(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
+        build_writes<NT>(tab, m, As, tid);
         if (tid < kC * kC) {   // S1 = (Q K^T) (.) Gamma
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
@@ -399,26 +407,26 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
                 float ps = 0.f;
 #pragma unroll
                 for (int cc = 0; cc < KH; ++cc) ps = fmaf(In0[r][part * KH + cc], kr[cc], ps);
-                ps += __shfl_xor(ps, 1);
-                ps += __shfl_xor(ps, 2);
+#pragma unroll
+                for (int o = 1; o < RP; o <<= 1) ps += __shfl_xor(ps, o);
                 if (part == 0) Xs[r][i] = __expf(tab.G[r]) * ps;
             }
         }
         __syncthreads();
         // p += S1 A
-        add_scores_times(S1, As, Xs, tid);
+        add_scores_times<NT>(S1, As, Xs, tid);
         __syncthreads();
-        for (int e = tid; e < kC * DV; e += kNT) {
+        for (int e = tid; e < kC * DV; e += NT) {
             const int r = e / DV, cc = e % DV;
             const bool live = t0 + r < Tb;
             In0[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, live);
             In1[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, live);
         }
         // X = scale U(lambda) p
-        rotate_rows(Xs, tab, m, 1.f, p.scale, tid);
+        rotate_rows<NT>(Xs, tab, m, 1.f, p.scale, tid);
         __syncthreads();
         // Z = M X (active slots), S2 = (dO V^T) (.) Gamma
-        readout_product<false>(Ms, Xs, Ws, m, tid);
+        readout_product<false, NT>(Ms, Xs, Ws, m, tid);
         if (tid < kC * kC) {
             const int r = tid >> 4, s = tid & 15;
             float acc = 0.f;
@@ -431,7 +439,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // W = softmax over the m active slots
-        for (int r = wave; r < kC; r += kNT / 64) {
+        for (int r = wave; r < kC; r += NT / 64) {
             const float z0 = lane < m ? Ws[r][lane] : -INFINITY;
             const float z1 = lane + 64 < m ? Ws[r][lane + 64] : -INFINITY;
             const float mx = wmax(fmaxf(z0, z1));
@@ -443,10 +451,10 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // Y = M^T W
-        readout_product<true>(Ms, Ws, Us, m, tid);
+        readout_product<true, NT>(Ms, Ws, Us, m, tid);
         __syncthreads();
         // u = U(-lambda) Y;  du_r = gamma_r Vbar_c do_r (entering value state)
-        rotate_rows(Us, tab, m, -1.f, 1.f, tid);
+        rotate_rows<NT>(Us, tab, m, -1.f, 1.f, tid);
         {
             const float *Vc = p.Vst + (((size_t)bh * p.nc + c) * kStoreRows + i) * DV + part * VH;
             const float *Ve = p.EcV + (((size_t)bh * p.groups + g) * kStoreRows + i) * DV + part * VH;
@@ -459,21 +467,21 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
                 float ps = 0.f;
 #pragma unroll
                 for (int cc = 0; cc < VH; ++cc) ps = fmaf(In0[r][part * VH + cc], vr[cc], ps);
-                ps += __shfl_xor(ps, 1);
-                ps += __shfl_xor(ps, 2);
+#pragma unroll
+                for (int o = 1; o < RP; o <<= 1) ps += __shfl_xor(ps, o);
                 if (part == 0) dUs[r][i] = __expf(tab.G[r]) * ps;
             }
         }
         __syncthreads();
         // store u; du += S2 A
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+        for (int e = tid; e < kC * kStoreRows; e += NT) {
             const int r = e >> 7, ii = e & 127;
             p.U[(row0 + r) * kStoreRows + ii] = Us[r][ii];
         }
-        add_scores_times(S2, As, dUs, tid);
+        add_scores_times<NT>(S2, As, dUs, tid);
         __syncthreads();
         // <u, du> and the clock gradient of u = U(-lambda) Y
-        for (int r = wave; r < kC; r += kNT / 64) {
+        for (int r = wave; r < kC; r += NT / 64) {
             const float ud = wsum(Us[r][lane] * dUs[r][lane] + Us[r][lane + 64] * dUs[r][lane + 64]);
             const float gl = rot_grad(dUs[r], Us[r], m, -1.f, lane);
             if (lane == 0) {
@@ -483,10 +491,10 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // dY = U(lambda) du
-        rotate_rows(dUs, tab, m, 1.f, 1.f, tid);
+        rotate_rows<NT>(dUs, tab, m, 1.f, 1.f, tid);
         __syncthreads();
         // dW = M dY;  dM += W dY^T
-        readout_product<false>(Ms, dUs, dWs, m, tid);
+        readout_product<false, NT>(Ms, dUs, dWs, m, tid);
 #pragma unroll 1
         for (int r = 0; r < kC; ++r) {
             const float w = Ws[r][i];
@@ -495,7 +503,7 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
         }
         __syncthreads();
         // dZ = W (.) (dW - <W, dW>)
-        for (int r = wave; r < kC; r += kNT / 64) {
+        for (int r = wave; r < kC; r += NT / 64) {
             const float w0 = Ws[r][lane], w1 = Ws[r][lane + 64];
             const float d0 = dWs[r][lane], d1 = dWs[r][lane + 64];
             const float sd = wsum(w0 * d0 + w1 * d1);
@@ -511,18 +519,18 @@ __global__ __launch_bounds__(kNT) void bwd_readout_kernel(BwdParams p) {
             for (int jj = 0; jj < MH; ++jj) dMacc[jj] = fmaf(dz, Xs[r][part * MH + jj], dMacc[jj]);
         }
         __syncthreads();
-        readout_product<true>(Ms, dWs, dUs, m, tid);
+        readout_product<true, NT>(Ms, dWs, dUs, m, tid);
         __syncthreads();
         // clock gradient of X = scale U(lambda) p, plus that of u
-        for (int r = wave; r < kC; r += kNT / 64) {
+        for (int r = wave; r < kC; r += NT / 64) {
             const float gl = rot_grad(dUs[r], Xs[r], m, 1.f, lane);
             if (lane == 0) p.dlam[row0 + r] = dlu[r] + gl;
         }
         __syncthreads();
         // dp = scale U(-lambda) dX
-        rotate_rows(dUs, tab, m, -1.f, p.scale, tid);
+        rotate_rows<NT>(dUs, tab, m, -1.f, p.scale, tid);
         __syncthreads();
-        for (int e = tid; e < kC * kStoreRows; e += kNT) {
+        for (int e = tid; e < kC * kStoreRows; e += NT) {
             const int r = e >> 7, ii = e & 127;
             p.dP[(row0 + r) * kStoreRows + ii] = dUs[r][ii];
         }
@@ -1035,7 +1043,7 @@ hipError_t launch_typed(const BwdParams &p, hipStream_t s) {
     const dim3 block(kNT), seq(BH), grp(BH, p.groups);
     hipLaunchKernelGGL((bwd_states_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL((bwd_states_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
-    hipLaunchKernelGGL((bwd_readout_kernel<DK, DV, Tin>), grp, block, 0, s, p);
+    hipLaunchKernelGGL((bwd_readout_kernel<DK, DV, Tin>), grp, dim3(kReadoutThreads), 0, s, p);
     hipLaunchKernelGGL((bwd_adjoint_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL((bwd_adjoint_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
     hipLaunchKernelGGL((bwd_grad_kernel<DK, DV, Tin>), grp, block, 0, s, p);

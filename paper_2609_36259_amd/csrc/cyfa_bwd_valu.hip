@@ -659,7 +659,7 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_combine_kernel(BwdParams p) {
 // (4) token gradients, per (sequence, chunk group).
 // Column products (a sum over the 128 state rows) give thread (column cc, row
 // block ih) the partial sums for all kC tokens; row products (a sum over state
-// columns) give thread (row i, half part) one state row.
+// columns) give the kRP threads (row i, part) one state row, each a kRP-th of its columns.
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
     constexpr int KH = DK / kRP, VH = DV / kRP;
@@ -843,7 +843,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             store_from_float(gv, (((size_t)b * p.T + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
         }
         // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i];
-        // thread (row i, half part) sums its half of the columns for every token s
+        // thread (row i, part) sums its share of the columns for every token s
         {
             float ak[kC], av[kC];
 #pragma unroll

@@ -116,10 +116,13 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
         const int c = d->chunk ? d->chunk : cyfa::valu_chunk_max();
         if (c != 8 && c != 16)
             return fail(CYFA_ERR_UNSUPPORTED, "vector-ALU kernel supports chunk 8 or 16 (got %d)", c);
-        if (d->segments > 1)
-            return fail(CYFA_ERR_UNSUPPORTED, "vector-ALU kernel runs one segment per sequence");
+        probe.chunk = c;
+        if (d->segments > 1 && !cyfa::valu_groups_supported(probe))
+            return fail(CYFA_ERR_UNSUPPORTED,
+                        "vector-ALU kernel runs several segments only for d_k, d_v <= 128 and m <= 127");
         plan->chunk = c;
-        plan->segments = 1;
+        plan->segments = d->segments ? d->segments : cyfa::valu_auto_groups(probe);
+        ws += round_up(cyfa::valu_group_workspace_bytes(probe, plan->segments));
     }
     plan->ws_bytes = ws;
     return CYFA_OK;
@@ -287,7 +290,8 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
                                    : cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
         if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
         e = mark(g_ev_start, s);
-        if (e == hipSuccess) e = cyfa::launch_fwd_valu(p, M, s);
+        if (e == hipSuccess)
+            e = cyfa::launch_fwd_valu(p, M, plan.segments, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s);
         if (e == hipSuccess) e = mark(g_ev_stop, s);
     }
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "forward launch: %s", hipGetErrorString(e));

@@ -44,6 +44,13 @@ struct BwdParams {
 };
 
 size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups);
+
+// The forward's chunk groups: the state entering each group of cpg 16-token
+// chunks (d_k, d_v in {64, 128}, m <= 127), from the groups' own contributions
+// and a combine in group order.  *EcK / *EcV point into ws at [BH][groups][128][d].
+size_t group_states_bytes(int B, int H, int dk, int dv, int groups);
+hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws, const float **EcK,
+                               const float **EcV, hipStream_t s);
 int bwd_auto_groups(int B, int T, int H);
 hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s);
 

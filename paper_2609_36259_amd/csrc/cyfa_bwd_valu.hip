@@ -39,6 +39,8 @@
 // gradients, per chunk group; (5) reverse cumulative sums, per sequence; (6)
 // dR, per head.  The states are in absolute-clock coordinates, so a group's
 // entering state reaches its chunks through the decay alone.
+#include <type_traits>
+
 #include "cyfa_bwd.h"
 
 namespace cyfa {
@@ -255,15 +257,17 @@ __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
     float Gl = 0.f;
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC;
-        float *Kd = p.Kst + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
-        float *Vd = p.Vst + ((size_t)bh * p.nc + c) * kStoreRows * DV + cv;
+        if (p.Kst) {        // the forward's group pre-pass keeps only the group totals
+            float *Kd = p.Kst + ((size_t)bh * p.nc + c) * kStoreRows * DK + ck;
+            float *Vd = p.Vst + ((size_t)bh * p.nc + c) * kStoreRows * DV + cv;
 #pragma unroll
-        for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = kst[ii];
+            for (int ii = 0; ii < NRK; ++ii) Kd[(size_t)(rk + ii) * DK] = kst[ii];
 #pragma unroll
-        for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = vst[ii];
-        if (tid == 0) {
-            p.clk[(size_t)bh * p.nc + c] = lam;
-            p.Gin[(size_t)bh * p.nc + c] = Gl;
+            for (int ii = 0; ii < NRV; ++ii) Vd[(size_t)(rv + ii) * DV] = vst[ii];
+            if (tid == 0) {
+                p.clk[(size_t)bh * p.nc + c] = lam;
+                p.Gin[(size_t)bh * p.nc + c] = Gl;
+            }
         }
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
@@ -1086,6 +1090,53 @@ size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups) {
     n += align_up(BH * (size_t)groups * kStoreRows * kStoreRows * 4);
     n += align_up(BH * kCombBlocks * 4);
     return n;
+}
+
+size_t group_states_bytes(int B, int H, int dk, int dv, int groups) {
+    const size_t BH = (size_t)B * H;
+    return align_up(BH * (size_t)groups * kStoreRows * (size_t)(dk + dv) * 4) +
+           align_up(BH * (size_t)groups * 4) + align_up(BH * kCombBlocks * 4);
+}
+
+hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws, const float **EcK,
+                               const float **EcV, hipStream_t s) {
+    BwdParams p{};
+    p.B = f.B; p.T = f.T; p.H = f.H; p.dk = f.dk; p.dv = f.dv; p.m = f.m;
+    p.nc = (f.T + kC - 1) / kC;
+    p.Tpad = p.nc * kC;
+    p.groups = groups;
+    p.cpg = cpg;
+    p.scale = f.scale; p.dtype = f.dtype;
+    p.q = f.q; p.k = f.k; p.v = f.v;
+    p.delta = f.delta; p.log_alpha = f.log_alpha; p.beta = f.beta; p.lens = f.lens;
+    p.K0 = f.K0; p.V0 = f.V0; p.clock0 = f.clock0;
+    const size_t BH = (size_t)f.B * f.H;
+    char *w = static_cast<char *>(ws);
+    auto take = [&w](size_t bytes) { char *r = w; w += align_up(bytes); return r; };
+    const size_t gcar = BH * (size_t)groups * kStoreRows;
+    p.EcK = reinterpret_cast<float *>(take(gcar * (size_t)(f.dk + f.dv) * 4));
+    p.EcV = p.EcK + gcar * f.dk;
+    p.Gg = reinterpret_cast<float *>(take(BH * (size_t)groups * 4));
+    p.fin = reinterpret_cast<float *>(take(BH * kCombBlocks * 4));
+    *EcK = p.EcK;
+    *EcV = p.EcV;
+    const dim3 block(kNT), grp(f.B * f.H, groups), comb(f.B * f.H, kCombBlocks);
+    auto go = [&](auto dk_tag, auto dv_tag) {
+        constexpr int DK = decltype(dk_tag)::value, DV = decltype(dv_tag)::value;
+        if (f.dtype == 0) {
+            hipLaunchKernelGGL((bwd_states_local_kernel<DK, DV, float>), grp, block, 0, s, p);
+        } else {
+            hipLaunchKernelGGL((bwd_states_local_kernel<DK, DV, __hip_bfloat16>), grp, block, 0, s, p);
+        }
+        hipLaunchKernelGGL((bwd_states_combine_kernel<DK, DV>), comb, block, 0, s, p);
+    };
+    using I64 = std::integral_constant<int, 64>;
+    using I128 = std::integral_constant<int, 128>;
+    if (f.dk == 64 && f.dv == 64) go(I64{}, I64{});
+    else if (f.dk == 64) go(I64{}, I128{});
+    else if (f.dv == 64) go(I128{}, I64{});
+    else go(I128{}, I128{});
+    return hipGetLastError();
 }
 
 hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s) {

@@ -13,6 +13,7 @@
 // gamma^r = exp(G_r), Gamma_rs = exp(G_r - G_s) for r >= s (Eq. app-chunk-decay).
 // The basis order inside the kernel is the one of App. A.1 (0 = DC, 2j-1 =
 // cos_j, 2j = sin_j); rows m..127 are padding and stay zero.
+#include "cyfa_bwd.h"
 #include "cyfa_rows.h"
 
 namespace cyfa {
@@ -41,8 +42,15 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 // ROWS: storage rows of the states (128, or 256 for m > 127).  The readout
 // matrix sits in LDS with 128 rows and is read from global memory (L2) with 256.
+// Chunk groups (gridDim.y > 1): workgroup (b h, g) runs the 16-token chunks
+// [g cpg, (g + 1) cpg) starting from the state entering its group (EcK / EcV slot
+// g, formed by a pre-pass over the earlier groups' own contributions) and the
+// clock lambda_0 + the increments before the group; the last group writes the
+// final state and clock.  With one group EcK / EcV are unused.
 template <int DK, int DV, int ROWS, typename Tin>
-__global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg) {
+__global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg,
+                                                                             const float *__restrict__ EcK,
+                                                                             const float *__restrict__ EcV, int cpg) {
     constexpr int kThreads = valu_threads(DK, DV, ROWS);
     constexpr int CM = kValuChunkMax;
     constexpr int KP = kThreads / ROWS;    // threads sharing a key-state row
@@ -65,13 +73,17 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
     __shared__ float G_s[CM];
     __shared__ float beta_s[CM];
     __shared__ double lam_carry;
+    __shared__ double dred[kThreads];
 
-    const int bh = blockIdx.x;
+    const int bh = blockIdx.x, grp = blockIdx.y, G = gridDim.y;
     const int b = bh / p.H, h = bh % p.H;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int m = p.m, C = p.chunk, T = p.T, H = p.H;
     const int Tb = seq_tokens(p, b);                  // this sequence's tokens
+    const int t_lo = G > 1 ? min(grp * cpg * 16, Tb) : 0;
+    const int t_hi = G > 1 ? min((grp + 1) * cpg * 16, Tb) : Tb;
+    const bool last = grp == G - 1;
     const int J = (m - 1) / 2;
     const float dc = 1.0f / sqrtf((float)m);
     const float ac = sqrtf(2.0f / (float)m);
@@ -86,13 +98,29 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
     float kst[KH];
     float vst[VR];
     {
-        const size_t kbase = ((size_t)bh * ROWS + ki) * DK + kh * KH;
+        // entering state rows: the initial state [BH][rows][d], or this group's slot of
+        // [BH][groups][rows][d]
+        const float *K0 = G > 1 ? EcK + ((size_t)bh * G + grp) * ROWS * DK
+                                : (p.K0 ? p.K0 + (size_t)bh * ROWS * DK : nullptr);
+        const float *V0 = G > 1 ? EcV + ((size_t)bh * G + grp) * ROWS * DV
+                                : (p.V0 ? p.V0 + (size_t)bh * ROWS * DV : nullptr);
 #pragma unroll
-        for (int c = 0; c < KH; ++c) kst[c] = (p.K0 && ki < m) ? p.K0[kbase + c] : 0.f;
+        for (int c = 0; c < KH; ++c) kst[c] = (K0 && ki < m) ? K0[(size_t)ki * DK + kh * KH + c] : 0.f;
 #pragma unroll
         for (int ii = 0; ii < VR; ++ii) {
             const int row = vpart * VR + ii;
-            vst[ii] = (p.V0 && row < m) ? p.V0[((size_t)bh * ROWS + row) * DV + vc] : 0.f;
+            vst[ii] = (V0 && row < m) ? V0[(size_t)row * DV + vc] : 0.f;
+        }
+    }
+    // clock at the group's first token: lambda_0 plus the increments before it
+    {
+        double ds = 0.0;
+        for (int t = tid; t < t_lo; t += kThreads) ds += (double)p.delta[((size_t)b * T + t) * H + h];
+        dred[tid] = ds;
+        __syncthreads();
+        for (int w = kThreads / 2; w > 0; w >>= 1) {
+            if (tid < w) dred[tid] += dred[tid + w];
+            __syncthreads();
         }
     }
     const float *Mh = Mg + (size_t)h * ROWS * ROWS;
@@ -104,11 +132,11 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
         if constexpr (ROWS == kStoreRows) return Ms[i][j];
         else return Mh[i * ROWS + j];
     };
-    if (tid == 0) lam_carry = p.clock0 ? reduce_clock(p.clock0[bh], m) : 0.0;
+    if (tid == 0) lam_carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + dred[0], m);
     __syncthreads();
 
-    for (int t0 = 0; t0 < Tb; t0 += C) {
-        const int n = min(C, Tb - t0);
+    for (int t0 = t_lo; t0 < t_hi; t0 += C) {
+        const int n = min(C, t_hi - t0);
         // ---- load the chunk (rows past the end are zero: no write, no decay, no shift)
         for (int e = tid; e < C * DK; e += kThreads) {
             const int r = e / DK, c = e % DK;
@@ -314,38 +342,40 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
         __syncthreads();
     }
 
-    if (p.K_out) {
+    if (p.K_out && last) {
         const size_t kbase = ((size_t)bh * ROWS + ki) * DK + kh * KH;
 #pragma unroll
         for (int c = 0; c < KH; ++c) p.K_out[kbase + c] = ki < m ? kst[c] : 0.f;
     }
-    if (p.V_out) {
+    if (p.V_out && last) {
 #pragma unroll
         for (int ii = 0; ii < VR; ++ii) {
             const int row = vpart * VR + ii;
             p.V_out[((size_t)bh * ROWS + row) * DV + vc] = row < m ? vst[ii] : 0.f;
         }
     }
-    if (p.clock_out && tid == 0) p.clock_out[bh] = lam_carry;
+    if (p.clock_out && last && tid == 0) p.clock_out[bh] = lam_carry;
 }
 
 template <int DK, int DV, int ROWS>
-hipError_t launch_rows(const FwdParams &p, const float *M, hipStream_t s) {
-    const dim3 grid(p.B * p.H), block(valu_threads(DK, DV, ROWS));
+hipError_t launch_rows(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
+                       hipStream_t s) {
+    const dim3 grid(p.B * p.H, groups), block(valu_threads(DK, DV, ROWS));
     if (p.dtype == 0)
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M);
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M, EcK, EcV, cpg);
     else
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M);
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M, EcK, EcV, cpg);
     return hipGetLastError();
 }
 
 // 256 storage rows are built for head dims up to 128
 template <int DK, int DV>
-hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
+hipError_t launch_typed(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
+                        hipStream_t s) {
     if constexpr (DK <= 128 && DV <= 128) {
-        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, s);
+        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, EcK, EcV, groups, cpg, s);
     }
-    return launch_rows<DK, DV, kStoreRows>(p, M, s);
+    return launch_rows<DK, DV, kStoreRows>(p, M, EcK, EcV, groups, cpg, s);
 }
 
 }  // namespace
@@ -353,16 +383,48 @@ hipError_t launch_typed(const FwdParams &p, const float *M, hipStream_t s) {
 int valu_chunk_max() { return kValuChunkMax; }
 
 template <int DK>
-hipError_t launch_dv(const FwdParams &p, const float *M, hipStream_t s) {
-    if (p.dv == 64) return launch_typed<DK, 64>(p, M, s);
-    if (p.dv == 128) return launch_typed<DK, 128>(p, M, s);
-    return launch_typed<DK, 256>(p, M, s);
+hipError_t launch_dv(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
+                     hipStream_t s) {
+    if (p.dv == 64) return launch_typed<DK, 64>(p, M, EcK, EcV, groups, cpg, s);
+    if (p.dv == 128) return launch_typed<DK, 128>(p, M, EcK, EcV, groups, cpg, s);
+    return launch_typed<DK, 256>(p, M, EcK, EcV, groups, cpg, s);
 }
 
-hipError_t launch_fwd_valu(const FwdParams &p, const float *M, hipStream_t s) {
-    if (p.dk == 64) return launch_dv<64>(p, M, s);
-    if (p.dk == 128) return launch_dv<128>(p, M, s);
-    return launch_dv<256>(p, M, s);
+bool valu_groups_supported(const FwdParams &p) {
+    return p.dk <= 128 && p.dv <= 128 && p.m <= kMaxActive;
+}
+
+int valu_auto_groups(const FwdParams &p) {
+    if (!valu_groups_supported(p)) return 1;
+    const int nc16 = (p.T + 15) / 16;
+    const int BH = p.B * p.H;
+    int g = (512 + BH - 1) / BH;
+    if (g > nc16) g = nc16;
+    return g < 1 ? 1 : g;
+}
+
+size_t valu_group_workspace_bytes(const FwdParams &p, int groups) {
+    return groups > 1 ? group_states_bytes(p.B, p.H, p.dk, p.dv, groups) : 0;
+}
+
+// groups > 1: chunk groups of cpg 16-token chunks, their entering states formed in ws
+hipError_t launch_fwd_valu(const FwdParams &p, const float *M, int groups, void *ws, hipStream_t s) {
+    const float *EcK = nullptr, *EcV = nullptr;
+    const int nc16 = (p.T + 15) / 16;
+    int cpg = 1;
+    if (groups > 1) {
+        cpg = (nc16 + groups - 1) / groups;
+        groups = (nc16 + cpg - 1) / cpg;
+    }
+    if (groups > 1) {
+        hipError_t e = launch_group_states(p, groups, cpg, ws, &EcK, &EcV, s);
+        if (e != hipSuccess) return e;
+    } else {
+        groups = 1;
+    }
+    if (p.dk == 64) return launch_dv<64>(p, M, EcK, EcV, groups, cpg, s);
+    if (p.dk == 128) return launch_dv<128>(p, M, EcK, EcV, groups, cpg, s);
+    return launch_dv<256>(p, M, EcK, EcV, groups, cpg, s);
 }
 
 }  // namespace cyfa

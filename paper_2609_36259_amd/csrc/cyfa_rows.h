@@ -22,4 +22,12 @@ inline size_t readout_bytes(int H, int m) {
 // column in the order of App. A.1, zero outside the active m x m block).
 hipError_t launch_readout_prep_wide(int H, int m, const float *R, float *M, hipStream_t s);
 
+// Vector-ALU forward over chunk groups (d_k, d_v <= 128 and m <= 127; other
+// shapes run one group per sequence): groups > 1 forms the state entering each
+// group in ws (valu_group_workspace_bytes) before the chunk kernel.
+bool valu_groups_supported(const FwdParams &p);
+int valu_auto_groups(const FwdParams &p);
+size_t valu_group_workspace_bytes(const FwdParams &p, int groups);
+hipError_t launch_fwd_valu(const FwdParams &p, const float *M, int groups, void *ws, hipStream_t s);
+
 }  // namespace cyfa

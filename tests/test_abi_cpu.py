@@ -35,8 +35,13 @@ def _ws(desc):
 def test_workspace_sizes_and_kernel_selection():
     d = cyfa.forward_desc(4, 4096, 16, 128, 128, dtype=cyfa.BF16)
     assert _ws(d) >= 16 * 128 * 128 * 4
+    d = cyfa.forward_desc(1, 256, 2, 64, 64, dtype=cyfa.F32, segments=1)
+    assert _ws(d) == 2 * 128 * 128 * 4            # one chunk group: the readout matrices only
     d = cyfa.forward_desc(1, 256, 2, 64, 64, dtype=cyfa.F32)
-    assert _ws(d) == 2 * 128 * 128 * 4
+    assert _ws(d) > 2 * 128 * 128 * 4             # automatic chunk groups: their entering states
+    d = cyfa.forward_desc(1, 256, 2, 256, 64, dtype=cyfa.F32, segments=4)
+    with pytest.raises(cyfa.CyfaError):
+        _ws(d)                                    # groups need d <= 128
     dd = cyfa.decode_desc(256, 16, 128, 128)
     assert cyfa.decode_workspace_size(dd) == 16 * 128 * 128 * 4
 

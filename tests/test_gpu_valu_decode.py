@@ -1,6 +1,7 @@
 """GPU parity of the vector-ALU forward kernel and of the decode step against the oracle."""
 import numpy as np
 import pytest
+import oracle
 
 from paper_2609_36259_amd.inputs import (DECODE, FWD_TINY, make_decode_inputs, make_forward_inputs,
                                          workload_inputs)
@@ -298,3 +299,37 @@ def oracle_forward_decode(x, pairs):
     import oracle
     return oracle.forward(x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"],
                           m=x["m"], scale=x["scale"], pairs=np.array(pairs, np.int32), want_z=False)
+
+
+@pytest.mark.parametrize("segments,chunk", [(1, 16), (3, 16), (5, 8), (0, 16)])
+def test_valu_chunk_groups(segments, chunk):
+    """The vector-ALU forward over chunk groups (each group's entering state from a
+    pre-pass over the earlier groups) against the oracle, with an initial state."""
+    cyfa = _cyfa()
+    x = make_forward_inputs(2, 16 * 9 + 5, 2, 64, 128, seed=26, dtype="f32")
+    t = upload(x)
+    g = torch.Generator().manual_seed(3)
+    K0 = torch.randn(2, 2, 128, 64, generator=g) * 0.2
+    V0 = torch.randn(2, 2, 128, 128, generator=g) * 0.2
+    K0[:, :, 127:] = 0
+    V0[:, :, 127:] = 0
+    c0 = torch.rand(2, 2, generator=g, dtype=torch.float64) * 127
+    res = _fwd(x, t, return_state=True, return_logits=True, kernel=cyfa.KERNEL_VALU, segments=segments,
+               chunk=chunk, K0=K0.cuda(), V0=V0.cuda(), clock0=c0.cuda())
+    torch.cuda.synchronize()
+    B, T, H = x["delta"].shape
+    pairs = list(range(B * H))
+    Kr = np.stack([oracle.relative_from_storage(127, c0.reshape(-1)[p].item(), K0.reshape(4, 128, 64)[p].numpy())
+                   for p in pairs])
+    Vr = np.stack([oracle.relative_from_storage(127, c0.reshape(-1)[p].item(), V0.reshape(4, 128, 128)[p].numpy())
+                   for p in pairs])
+    ref = run_oracle(x, K0=Kr, V0=Vr, lam0=c0.reshape(-1).numpy())
+    errs = {"o": rel_err(pairs_view(res["o"], pairs, H), ref["o"]),
+            "z": rel_err(pairs_view(res["logits"], pairs, H), ref["z"])}
+    Kref, Vref = oracle_states_abs(ref, 127)
+    errs["K"] = rel_err(state_view(res["K"], pairs, H), Kref)
+    errs["V"] = rel_err(state_view(res["V"], pairs, H), Vref)
+    errs["clock"] = clock_err(res["clock"].cpu().numpy().reshape(-1), ref["lam"], 127)
+    print("errors", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= (1e-9 if k == "clock" else TOL_F32), (k, v)

@@ -86,9 +86,10 @@ typedef enum {
  *                Results do not depend on it beyond rounding (App. B: the
  *                chunk form is exact).
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
- *                else 1..1024 (MFMA kernel only; the VALU kernel uses 1).  The
- *                state entering a segment is obtained from a pre-pass over the
- *                earlier segments.  Results do not depend on it beyond rounding.
+ *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
+ *                than one only for d_k, d_v <= 128 and m <= 127).  The state
+ *                entering a segment is obtained from a pre-pass over the earlier
+ *                segments.  Results do not depend on it beyond rounding.
  *   scale        logit scale (the paper leaves the dot-product scaling out of
  *                its notation, Sec. 3.1 footnote); multiplies R K_t q_t
  *   dtype        storage type of q, k, v and o

@@ -9,7 +9,8 @@
 //              beta = sigmoid(z_beta)
 // Epilogue: out_t = RMSNorm(o_t) * g_o * sigmoid(gate_t)     (head-wise RMSNorm, output gate)
 //
-// Both are streaming kernels bound by HBM bandwidth.  Thread layout: each thread
+// Both are streaming kernels bound by HBM bandwidth; the gates are computed by
+// extra workgroups of the convolution launch.  Thread layout: each thread
 // owns eight consecutive channels (one 16-byte bf16 load or two float4 loads per
 // token) of one head; the D / 8 threads of a head are consecutive lanes, so the
 // RMSNorm sum is a shuffle reduction inside the wave.  A workgroup walks a run of
@@ -73,13 +74,35 @@ struct ConvSet {
     const float *w[3];
     const float *g[3];
     void *y[3];
+    int n;                          // tensors in the set; blockIdx.z >= n B runs the gates
+    const float *z_delta, *b_delta, *z_alpha, *b_alpha, *A, *z_beta;
+    float *delta, *log_alpha, *beta;
 };
+
 
 // ShortConv (+ SiLU) (+ RMSNorm) of the tensors of a ConvSet.
 template <int D, int KMAX, typename Tin>
 __global__ __launch_bounds__(kThreads) void conv_norm_kernel(ConvSet cs, int B, int T, int H, int K, int act,
                                                              float eps, const int *__restrict__ lens) {
     const int tensor = blockIdx.z / B, b = blockIdx.z % B, t_begin = blockIdx.y * kTokens;
+    if (tensor >= cs.n) {
+        // the scalar gates of tokens [t_begin, t_begin + kTokens) of sequence b, all heads
+        if (blockIdx.x != 0) return;
+        const int Tg = mix_tokens(lens, b, T);
+        for (int e = threadIdx.x; e < kTokens * H; e += kThreads) {
+            const int t = t_begin + e / H, h = e % H;
+            if (t >= T) continue;
+            const size_t i = ((size_t)b * T + t) * H + h;
+            const bool live = t < Tg;
+            if (cs.z_delta) cs.delta[i] = live ? sigm(cs.z_delta[i] + (cs.b_delta ? cs.b_delta[h] : 0.f)) : 0.f;
+            if (cs.z_alpha) {
+                const float za = cs.z_alpha[i] + (cs.b_alpha ? cs.b_alpha[h] : 0.f);
+                cs.log_alpha[i] = live ? -cs.A[h] * softplus_f(za) : 0.f;
+            }
+            if (cs.z_beta) cs.beta[i] = live ? sigm(cs.z_beta[i]) : 0.f;
+        }
+        return;
+    }
     const Tin *__restrict__ x = static_cast<const Tin *>(cs.x[tensor]);
     const float *__restrict__ w = cs.w[tensor];
     const float *__restrict__ g = cs.g[tensor];
@@ -176,21 +199,6 @@ __global__ __launch_bounds__(kThreads) void conv_norm_kernel(ConvSet cs, int B, 
     }
 }
 
-// Scalar gates, elementwise over [B, T, H].
-__global__ __launch_bounds__(kThreads) void gates_kernel(MixParams p) {
-    const size_t n = (size_t)p.B * p.T * p.H;
-    for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += (size_t)gridDim.x * kThreads) {
-        const int h = (int)(e % p.H);
-        const int t = (int)((e / p.H) % p.T);
-        const int b = (int)(e / ((size_t)p.H * p.T));
-        const bool live = t < mix_tokens(p.lens, b, p.T);
-        if (p.z_delta) p.delta[e] = live ? sigm(p.z_delta[e] + (p.b_delta ? p.b_delta[h] : 0.f)) : 0.f;
-        if (p.z_alpha)
-            p.log_alpha[e] = live ? -p.A[h] * softplus_f(p.z_alpha[e] + (p.b_alpha ? p.b_alpha[h] : 0.f)) : 0.f;
-        if (p.z_beta) p.beta[e] = live ? sigm(p.z_beta[e]) : 0.f;
-    }
-}
-
 // Epilogue: head-wise RMSNorm and sigmoid output gate.
 template <int D, typename Tin>
 __global__ __launch_bounds__(kThreads) void norm_gate_kernel(const Tin *__restrict__ o, const Tin *__restrict__ gate,
@@ -232,8 +240,11 @@ __global__ __launch_bounds__(kThreads) void norm_gate_kernel(const Tin *__restri
 
 template <int D, typename Tin>
 hipError_t launch_conv(const MixParams &p, const ConvSet &cs, int n, hipStream_t s) {
+    (void)n;
     const int HD = p.H * D;
-    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens, n * p.B);
+    const bool gates = p.z_delta || p.z_alpha || p.z_beta;
+    const dim3 grid((HD / kCh + kThreads - 1) / kThreads, (p.T + kTokens - 1) / kTokens,
+                    (cs.n + (gates ? 1 : 0)) * p.B);
     hipLaunchKernelGGL((conv_norm_kernel<D, kMixMaxConv, Tin>), grid, dim3(kThreads), 0, s, cs, p.B, p.T, p.H,
                        p.K, p.act, p.eps, p.lens);
     return hipGetLastError();
@@ -249,12 +260,19 @@ hipError_t launch_conv_d(const MixParams &p, int D, const ConvSet &cs, int n, hi
 // q, k and v in one launch when d_k = d_v, else q and k together and v alone
 template <typename Tin>
 hipError_t launch_qkv(const MixParams &p, hipStream_t s) {
-    ConvSet qkv{{p.q_in, p.k_in, p.v_in}, {p.wq, p.wk, p.wv}, {p.gq, p.gk, nullptr}, {p.q_out, p.k_out, p.v_out}};
+    // the gates ride along with the launch that carries q and k
+    ConvSet qkv{{p.q_in, p.k_in, p.v_in}, {p.wq, p.wk, p.wv}, {p.gq, p.gk, nullptr}, {p.q_out, p.k_out, p.v_out},
+                p.dk == p.dv ? 3 : 2, p.z_delta, p.b_delta, p.z_alpha, p.b_alpha, p.A, p.z_beta,
+                p.delta, p.log_alpha, p.beta};
     if (p.dk == p.dv) return launch_conv_d<Tin>(p, p.dk, qkv, 3, s);
     hipError_t e = launch_conv_d<Tin>(p, p.dk, qkv, 2, s);
     if (e != hipSuccess) return e;
-    ConvSet v{{p.v_in, nullptr, nullptr}, {p.wv, nullptr, nullptr}, {nullptr, nullptr, nullptr}, {p.v_out, nullptr, nullptr}};
-    return launch_conv_d<Tin>(p, p.dv, v, 1, s);
+    ConvSet v{{p.v_in, nullptr, nullptr}, {p.wv, nullptr, nullptr}, {nullptr, nullptr, nullptr},
+              {p.v_out, nullptr, nullptr}, 1, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+              nullptr, nullptr, nullptr};
+    MixParams pv = p;
+    pv.z_delta = pv.z_alpha = pv.z_beta = nullptr;
+    return launch_conv_d<Tin>(pv, p.dv, v, 1, s);
 }
 
 template <int D, typename Tin>
@@ -270,15 +288,7 @@ hipError_t launch_epi(const MixParams &p, const void *o, const void *gate, const
 
 hipError_t launch_mixer_prologue(const MixParams &p, hipStream_t s) {
     if (p.T == 0) return hipSuccess;
-    hipError_t e = p.dtype == 0 ? launch_qkv<float>(p, s) : launch_qkv<__hip_bfloat16>(p, s);
-    if (e != hipSuccess) return e;
-    if (p.z_delta || p.z_alpha || p.z_beta) {
-        const size_t n = (size_t)p.B * p.T * p.H;
-        const int blocks = (int)std::min<size_t>((n + kThreads - 1) / kThreads, 4096);
-        hipLaunchKernelGGL(gates_kernel, dim3(blocks), dim3(kThreads), 0, s, p);
-        e = hipGetLastError();
-    }
-    return e;
+    return p.dtype == 0 ? launch_qkv<float>(p, s) : launch_qkv<__hip_bfloat16>(p, s);
 }
 
 hipError_t launch_mixer_epilogue(const MixParams &p, const void *o, const void *gate, const float *g, void *out,

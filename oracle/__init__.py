@@ -23,7 +23,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cyfa_oracle.c")
-_LIB = os.path.join(_HERE, "libcyfa_oracle.so")
+# CYFA_ORACLE_LIB points the wrapper at another build of the same source (the
+# mutation check of tests/test_oracle_mutations.py loads deliberately broken copies)
+_LIB = os.environ.get("CYFA_ORACLE_LIB") or os.path.join(_HERE, "libcyfa_oracle.so")
 _lib = None
 
 _dp = ctypes.POINTER(ctypes.c_double)

@@ -37,6 +37,8 @@ struct BwdParams {
     float *AcK, *AcV;               // [BH][groups][128][d]
     float *Gin, *Gout;              // [BH][nc] log decay from the group start / to the group end
     float *Gg;                      // [BH][groups] log decay over each group
+    double *gclk;                   // [BH][groups] clock entering each group (reduced mod m),
+                                    // written by the forward's group pre-pass only
     float *U, *dP;                  // [BH][Tpad][128] readout output u_t and key-pass adjoint dp_t
     float *udu, *dlam, *dG;         // [BH][Tpad] <u_t, du_t>, dL/dlambda_t, dL/dG_t
     float *dMp;                     // [BH][groups][128][128] partial dL/dM
@@ -47,10 +49,14 @@ size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups);
 
 // The forward's chunk groups: the state entering each group of cpg 16-token
 // chunks (d_k, d_v in {64, 128}, m <= 127), from the groups' own contributions
-// and a combine in group order.  *EcK / *EcV point into ws at [BH][groups][128][d].
+// and a combine in group order.  *EcK / *EcV point into ws at [BH][groups][128][d],
+// *Eclk at [BH][groups]: the clock entering each group (reduced mod m).  The
+// forward's chunk kernel reads the clock from there rather than from clock0, so
+// that clock_out may alias clock0 (the last group writes it while earlier groups
+// are still running).
 size_t group_states_bytes(int B, int H, int dk, int dv, int groups);
 hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws, const float **EcK,
-                               const float **EcV, hipStream_t s);
+                               const float **EcV, const double **Eclk, hipStream_t s);
 int bwd_auto_groups(int B, int T, int H);
 hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s);
 

@@ -249,6 +249,7 @@ __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
         }
     }
     double lam = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + dred[0], m);
+    if (p.gclk && tid == 0) p.gclk[(size_t)bh * p.groups + g] = lam;
     float kst[NRK], vst[NRV];
 #pragma unroll
     for (int ii = 0; ii < NRK; ++ii) kst[ii] = 0.f;
@@ -1095,11 +1096,12 @@ size_t bwd_workspace_bytes(int B, int T, int H, int dk, int dv, int groups) {
 size_t group_states_bytes(int B, int H, int dk, int dv, int groups) {
     const size_t BH = (size_t)B * H;
     return align_up(BH * (size_t)groups * kStoreRows * (size_t)(dk + dv) * 4) +
-           align_up(BH * (size_t)groups * 4) + align_up(BH * kCombBlocks * 4);
+           align_up(BH * (size_t)groups * 4) + align_up(BH * kCombBlocks * 4) +
+           align_up(BH * (size_t)groups * 8);
 }
 
 hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws, const float **EcK,
-                               const float **EcV, hipStream_t s) {
+                               const float **EcV, const double **Eclk, hipStream_t s) {
     BwdParams p{};
     p.B = f.B; p.T = f.T; p.H = f.H; p.dk = f.dk; p.dv = f.dv; p.m = f.m;
     p.nc = (f.T + kC - 1) / kC;
@@ -1118,8 +1120,10 @@ hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws
     p.EcV = p.EcK + gcar * f.dk;
     p.Gg = reinterpret_cast<float *>(take(BH * (size_t)groups * 4));
     p.fin = reinterpret_cast<float *>(take(BH * kCombBlocks * 4));
+    p.gclk = reinterpret_cast<double *>(take(BH * (size_t)groups * 8));
     *EcK = p.EcK;
     *EcV = p.EcV;
+    *Eclk = p.gclk;
     const dim3 block(kNT), grp(f.B * f.H, groups), comb(f.B * f.H, kCombBlocks);
     auto go = [&](auto dk_tag, auto dv_tag) {
         constexpr int DK = decltype(dk_tag)::value, DV = decltype(dv_tag)::value;

@@ -45,12 +45,16 @@ __device__ __forceinline__ float wave_sum(float x) {
 // Chunk groups (gridDim.y > 1): workgroup (b h, g) runs the 16-token chunks
 // [g cpg, (g + 1) cpg) starting from the state entering its group (EcK / EcV slot
 // g, formed by a pre-pass over the earlier groups' own contributions) and the
-// clock lambda_0 + the increments before the group; the last group writes the
-// final state and clock.  With one group EcK / EcV are unused.
+// clock entering the group (Eclk slot g, lambda_0 plus the increments before the
+// group, from the same pre-pass); the last group writes the final state and
+// clock.  No group reads clock0, K0 or V0 itself, so the final state and clock
+// may overwrite them in place.  With one group EcK / EcV / Eclk are unused.
 template <int DK, int DV, int ROWS, typename Tin>
 __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(FwdParams p, const float *__restrict__ Mg,
                                                                              const float *__restrict__ EcK,
-                                                                             const float *__restrict__ EcV, int cpg) {
+                                                                             const float *__restrict__ EcV,
+                                                                             const double *__restrict__ Eclk,
+                                                                             int cpg) {
     constexpr int kThreads = valu_threads(DK, DV, ROWS);
     constexpr int CM = kValuChunkMax;
     constexpr int KP = kThreads / ROWS;    // threads sharing a key-state row
@@ -73,7 +77,6 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
     __shared__ float G_s[CM];
     __shared__ float beta_s[CM];
     __shared__ double lam_carry;
-    __shared__ double dred[kThreads];
 
     const int bh = blockIdx.x, grp = blockIdx.y, G = gridDim.y;
     const int b = bh / p.H, h = bh % p.H;
@@ -112,17 +115,6 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
             vst[ii] = (V0 && row < m) ? V0[(size_t)row * DV + vc] : 0.f;
         }
     }
-    // clock at the group's first token: lambda_0 plus the increments before it
-    {
-        double ds = 0.0;
-        for (int t = tid; t < t_lo; t += kThreads) ds += (double)p.delta[((size_t)b * T + t) * H + h];
-        dred[tid] = ds;
-        __syncthreads();
-        for (int w = kThreads / 2; w > 0; w >>= 1) {
-            if (tid < w) dred[tid] += dred[tid + w];
-            __syncthreads();
-        }
-    }
     const float *Mh = Mg + (size_t)h * ROWS * ROWS;
     if constexpr (ROWS == kStoreRows) {
         for (int e = tid; e < kStoreRows * kStoreRows; e += kThreads)
@@ -132,7 +124,8 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
         if constexpr (ROWS == kStoreRows) return Ms[i][j];
         else return Mh[i * ROWS + j];
     };
-    if (tid == 0) lam_carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + dred[0], m);
+    // clock at the group's first token (with groups: from the pre-pass)
+    if (tid == 0) lam_carry = G > 1 ? Eclk[(size_t)bh * G + grp] : reduce_clock(p.clock0 ? p.clock0[bh] : 0.0, m);
     __syncthreads();
 
     for (int t0 = t_lo; t0 < t_hi; t0 += C) {
@@ -358,24 +351,24 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
 }
 
 template <int DK, int DV, int ROWS>
-hipError_t launch_rows(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
-                       hipStream_t s) {
+hipError_t launch_rows(const FwdParams &p, const float *M, const float *EcK, const float *EcV, const double *Eclk,
+                       int groups, int cpg, hipStream_t s) {
     const dim3 grid(p.B * p.H, groups), block(valu_threads(DK, DV, ROWS));
     if (p.dtype == 0)
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M, EcK, EcV, cpg);
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, float>), grid, block, 0, s, p, M, EcK, EcV, Eclk, cpg);
     else
-        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M, EcK, EcV, cpg);
+        hipLaunchKernelGGL((fwd_valu_kernel<DK, DV, ROWS, __hip_bfloat16>), grid, block, 0, s, p, M, EcK, EcV, Eclk, cpg);
     return hipGetLastError();
 }
 
 // 256 storage rows are built for head dims up to 128
 template <int DK, int DV>
-hipError_t launch_typed(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
-                        hipStream_t s) {
+hipError_t launch_typed(const FwdParams &p, const float *M, const float *EcK, const float *EcV, const double *Eclk,
+                        int groups, int cpg, hipStream_t s) {
     if constexpr (DK <= 128 && DV <= 128) {
-        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, EcK, EcV, groups, cpg, s);
+        if (p.m > kMaxActive) return launch_rows<DK, DV, kWideRows>(p, M, EcK, EcV, Eclk, groups, cpg, s);
     }
-    return launch_rows<DK, DV, kStoreRows>(p, M, EcK, EcV, groups, cpg, s);
+    return launch_rows<DK, DV, kStoreRows>(p, M, EcK, EcV, Eclk, groups, cpg, s);
 }
 
 }  // namespace
@@ -383,11 +376,11 @@ hipError_t launch_typed(const FwdParams &p, const float *M, const float *EcK, co
 int valu_chunk_max() { return kValuChunkMax; }
 
 template <int DK>
-hipError_t launch_dv(const FwdParams &p, const float *M, const float *EcK, const float *EcV, int groups, int cpg,
-                     hipStream_t s) {
-    if (p.dv == 64) return launch_typed<DK, 64>(p, M, EcK, EcV, groups, cpg, s);
-    if (p.dv == 128) return launch_typed<DK, 128>(p, M, EcK, EcV, groups, cpg, s);
-    return launch_typed<DK, 256>(p, M, EcK, EcV, groups, cpg, s);
+hipError_t launch_dv(const FwdParams &p, const float *M, const float *EcK, const float *EcV, const double *Eclk,
+                     int groups, int cpg, hipStream_t s) {
+    if (p.dv == 64) return launch_typed<DK, 64>(p, M, EcK, EcV, Eclk, groups, cpg, s);
+    if (p.dv == 128) return launch_typed<DK, 128>(p, M, EcK, EcV, Eclk, groups, cpg, s);
+    return launch_typed<DK, 256>(p, M, EcK, EcV, Eclk, groups, cpg, s);
 }
 
 bool valu_groups_supported(const FwdParams &p) {
@@ -410,6 +403,7 @@ size_t valu_group_workspace_bytes(const FwdParams &p, int groups) {
 // groups > 1: chunk groups of cpg 16-token chunks, their entering states formed in ws
 hipError_t launch_fwd_valu(const FwdParams &p, const float *M, int groups, void *ws, hipStream_t s) {
     const float *EcK = nullptr, *EcV = nullptr;
+    const double *Eclk = nullptr;
     const int nc16 = (p.T + 15) / 16;
     int cpg = 1;
     if (groups > 1) {
@@ -417,14 +411,14 @@ hipError_t launch_fwd_valu(const FwdParams &p, const float *M, int groups, void 
         groups = (nc16 + cpg - 1) / cpg;
     }
     if (groups > 1) {
-        hipError_t e = launch_group_states(p, groups, cpg, ws, &EcK, &EcV, s);
+        hipError_t e = launch_group_states(p, groups, cpg, ws, &EcK, &EcV, &Eclk, s);
         if (e != hipSuccess) return e;
     } else {
         groups = 1;
     }
-    if (p.dk == 64) return launch_dv<64>(p, M, EcK, EcV, groups, cpg, s);
-    if (p.dk == 128) return launch_dv<128>(p, M, EcK, EcV, groups, cpg, s);
-    return launch_dv<256>(p, M, EcK, EcV, groups, cpg, s);
+    if (p.dk == 64) return launch_dv<64>(p, M, EcK, EcV, Eclk, groups, cpg, s);
+    if (p.dk == 128) return launch_dv<128>(p, M, EcK, EcV, Eclk, groups, cpg, s);
+    return launch_dv<256>(p, M, EcK, EcV, Eclk, groups, cpg, s);
 }
 
 }  // namespace cyfa

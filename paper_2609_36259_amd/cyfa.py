@@ -176,14 +176,16 @@ DEFAULT_CHUNK = {"mfma": 32, "valu": 16}
 def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=127,
             chunk=0, segments=0, kernel=KERNEL_AUTO, K0=None, V0=None, clock0=None,
             lens=None, return_state=False, return_logits=False, out=None, workspace=None,
-            stream=None):
+            K_out=None, V_out=None, clock_out=None, stream=None):
     """CyFA forward: q,k [B,T,H,dk], v [B,T,H,dv] (float32 or bfloat16), scalars [B,T,H] float32.
 
     ``lens`` (optional int32 [B] device tensor): sequence b has lens[b] tokens
     (cyfa_forward_lens); rows t >= lens[b] of the outputs are not written.
     Returns ``o`` [B,T,H,dv] (dtype of q) or a dict with ``o`` and, when requested,
     the final absolute-clock states ``K``/``V`` [B,H,S,d] (S = store_rows(m)), ``clock`` [B,H] (float64)
-    and the slot ``logits`` [B,T,H,m].
+    and the slot ``logits`` [B,T,H,m].  ``K_out``/``V_out``/``clock_out``, when given, receive
+    the final state (they may be ``K0``/``V0``/``clock0`` themselves: resume in place) and
+    imply ``return_state``.
     """
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -207,9 +209,19 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     o = out if out is not None else torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
     _need(o, (B, T, H, dv), q.dtype, "out")
-    K_out = torch.empty((B, H, S, dk), dtype=torch.float32, device=dev) if return_state else None
-    V_out = torch.empty((B, H, S, dv), dtype=torch.float32, device=dev) if return_state else None
-    clk = torch.empty((B, H), dtype=torch.float64, device=dev) if return_state else None
+    if K_out is not None or V_out is not None or clock_out is not None:
+        return_state = True
+    _need(K_out, (B, H, S, dk), torch.float32, "K_out")
+    _need(V_out, (B, H, S, dv), torch.float32, "V_out")
+    _need(clock_out, (B, H), torch.float64, "clock_out")
+    if return_state:
+        if K_out is None:
+            K_out = torch.empty((B, H, S, dk), dtype=torch.float32, device=dev)
+        if V_out is None:
+            V_out = torch.empty((B, H, S, dv), dtype=torch.float32, device=dev)
+    clk = clock_out
+    if return_state and clk is None:
+        clk = torch.empty((B, H), dtype=torch.float64, device=dev)
     logits = torch.empty((B, T, H, m), dtype=torch.float32, device=dev) if return_logits else None
     st = load().cyfa_forward_lens(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
                                   _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(lens), _ptr(K0),

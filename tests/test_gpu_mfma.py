@@ -203,20 +203,45 @@ def test_peaky_logits_diagnostic():
     res = _fwd(x, t, return_logits=True)
     err = _errors(x, res)
     assert err["z"] <= TOL_BF16, err
-    assert err["o"] <= 5e-2, err
+    assert err["o"] <= TOL_BF16, err
 
 
-@pytest.mark.parametrize("w,npairs", [(FWD_400M, 4), (FWD_1P4B, 4), (FWD_LONG, 3)],
-                         ids=["400M", "1.4B", "long"])
-def test_full_size_sampled_parity(w, npairs):
-    """Full-size workload in the benchmark's launch configuration; sampled (b, h)
-    sequences (first, last and interior pairs) compared over all tokens."""
+@pytest.mark.parametrize("w", [FWD_400M, FWD_1P4B, FWD_LONG], ids=["400M", "1.4B", "long"])
+def test_full_size_parity(w):
+    """Full-size workload in the benchmark's launch configuration; every (b, h)
+    sequence compared with the oracle over all tokens (outputs, slot logits, final
+    states and clocks)."""
     x = workload_inputs(w)
     t = upload(x)
     res = _fwd(x, t, kernel=_cyfa().KERNEL_AUTO, return_state=True, return_logits=True)
     torch.cuda.synchronize()
-    BH = w.B * w.H
-    pairs = list(dict.fromkeys([0, BH - 1, BH // 2, (BH // 3) | 1]))[:npairs]
     o = res["o"]
     assert torch.isfinite(o.float()).all()
-    _assert_ok(_errors(x, res, pairs=pairs))
+    _assert_ok(_errors(x, res))
+
+
+@pytest.mark.parametrize("kernel,segments", [("mfma", 3), ("valu", 4)])
+def test_resume_in_place(kernel, segments):
+    """The final state and clock written over the initial ones (K_out = K0,
+    V_out = V0, clock_out = clock0) with several segments / chunk groups: every
+    workgroup must have read its entering clock and state before any writes them."""
+    cyfa = _cyfa()
+    kern = cyfa.KERNEL_MFMA if kernel == "mfma" else cyfa.KERNEL_VALU
+    x = make_forward_inputs(2, 300, 2, 128, 128, seed=53, dtype="bf16")
+    t = upload(x)
+    t1 = 137
+    a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    first = cyfa.forward(a["q"], a["k"], a["v"], a["delta"], a["log_alpha"], a["beta"], a["R"],
+                         scale=x["scale"], return_state=True, kernel=kern, segments=segments)
+    K, V, clk = first["K"], first["V"], first["clock"]
+    ref = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
+                       scale=x["scale"], K0=K.clone(), V0=V.clone(), clock0=clk.clone(),
+                       return_state=True, kernel=kern, segments=segments)
+    got = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
+                       scale=x["scale"], K0=K, V0=V, clock0=clk, K_out=K, V_out=V, clock_out=clk,
+                       kernel=kern, segments=segments)
+    torch.cuda.synchronize()
+    assert torch.equal(got["o"], ref["o"])
+    assert torch.equal(K, ref["K"]) and torch.equal(V, ref["V"])
+    assert torch.equal(clk, ref["clock"])

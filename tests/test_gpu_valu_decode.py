@@ -259,8 +259,9 @@ def test_decode_consistent_with_forward():
 
 def test_decode_full_size_sampled():
     """256 streams x 16 heads, d = 128: 512-token prefix (GPU forward), then 64
-    decode steps; sampled stream-heads compared with the oracle stepped token by
-    token over all 576 tokens."""
+    decode steps; every stream of one head (256 stream-heads, all sharing that
+    head's readout matrix) plus stream-heads of the other heads compared with the
+    oracle stepped token by token over all 576 tokens."""
     cyfa = _cyfa()
     N, H, d = DECODE.B, DECODE.H, DECODE.dk
     prefix, steps = DECODE.extra["prefix"], DECODE.extra["steps"]
@@ -283,7 +284,8 @@ def test_decode_full_size_sampled():
                                   workspace=ws)
         outs[:, s_] = o_step
     torch.cuda.synchronize()
-    pairs = [0, N * H - 1, 1000, 2050, 3333]
+    head = 5
+    pairs = [n * H + head for n in range(N)] + [0, N * H - 1, 1000, 2050, 3333, 17 * H + 11]
     ref = oracle_forward_decode(x, pairs)
     got = outs.cpu().numpy()
     got = np.stack([got[p // H, :, p % H] for p in pairs])
@@ -330,6 +332,31 @@ def test_valu_chunk_groups(segments, chunk):
     errs["K"] = rel_err(state_view(res["K"], pairs, H), Kref)
     errs["V"] = rel_err(state_view(res["V"], pairs, H), Vref)
     errs["clock"] = clock_err(res["clock"].cpu().numpy().reshape(-1), ref["lam"], 127)
+    print("errors", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= (1e-9 if k == "clock" else TOL_F32), (k, v)
+
+
+def test_valu_full_size_f32_chunk_groups():
+    """The vector-ALU forward at the 1.4B layer shape (B4 T4096 H16 d128) with fp32
+    inputs, in its automatic chunk-group split (the fp32 path of that shape);
+    eight (b, h) sequences, first, last and interior, compared over all tokens."""
+    from paper_2609_36259_amd.inputs import FWD_1P4B
+    cyfa = _cyfa()
+    w = FWD_1P4B
+    x = make_forward_inputs(w.B, w.T, w.H, w.dk, w.dv, seed=w.seed, dtype="f32")
+    t = upload(x)
+    res = _fwd(x, t, kernel=cyfa.KERNEL_VALU, return_state=True, return_logits=True)
+    torch.cuda.synchronize()
+    B, T, H = x["delta"].shape
+    pairs = [0, 1, 17, 31, 32, 46, 62, B * H - 1]
+    ref = run_oracle(x, pairs=np.array(pairs, np.int32))
+    errs = {"o": rel_err(pairs_view(res["o"], pairs, H), ref["o"]),
+            "z": rel_err(pairs_view(res["logits"], pairs, H), ref["z"])}
+    Kref, Vref = oracle_states_abs(ref, x["m"])
+    errs["K"] = rel_err(state_view(res["K"], pairs, H), Kref)
+    errs["V"] = rel_err(state_view(res["V"], pairs, H), Vref)
+    errs["clock"] = clock_err(res["clock"].cpu().numpy().reshape(-1)[pairs], ref["lam"], x["m"])
     print("errors", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     for k, v in errs.items():
         assert v <= (1e-9 if k == "clock" else TOL_F32), (k, v)

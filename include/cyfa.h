@@ -320,6 +320,34 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc,
                              void *stream);
 
 /*
+ * cyfa_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, results and errors as
+ * cyfa_decode_step (bit-identical outputs and states), except that the step's
+ * scratch -- the readout matrices R_h Phi, H x rows x rows floats with rows =
+ * 128 (m <= 127) or 256 -- lives in a fixed device array of
+ * CYFA_DECODE_NOALLOC_SCRATCH_BYTES inside the library (4 MiB: H <= 64 at
+ * m <= 127, H <= 16 at m > 127).  A larger need returns CYFA_ERR_UNSUPPORTED
+ * before anything is launched.  Nothing is allocated: no hipMalloc, hipFree or
+ * allocating library call, on the first call or later.  Each GPU holds its own
+ * copy of the array for the life of the process; its address is looked up once
+ * per device, on the first call made with that device current.  `stream` must
+ * belong to the calling thread's current device (else
+ * CYFA_ERR_INVALID_ARGUMENT).  Every call on one GPU shares that GPU's array
+ * (each call overwrites all of it before reading it): calls that overlap on one
+ * GPU (on different streams, or from several threads) race and must be
+ * serialised by the caller.
+ */
+#define CYFA_DECODE_NOALLOC_SCRATCH_BYTES (4u << 20)
+cyfa_status cyfa_decode_step_noalloc(const cyfa_dec_desc *desc,
+                                     const void *q, const void *k, const void *v,
+                                     const float *delta, const float *log_alpha, const float *beta,
+                                     const float *R,
+                                     float *K, float *V, double *clock,
+                                     void *o, float *logits_out,
+                                     void *stream);
+
+/*
  * Optional timing hook for profilers and benchmarks.  When both events are
  * non-NULL (hipEvent_t handles), every later cyfa_forward / cyfa_decode_step
  * call made from the calling thread records `start` and `stop` around its main

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "cyfa.h"
 #include "cyfa_bwd.h"
@@ -428,19 +429,19 @@ cyfa_status cyfa_mixer_epilogue(const cyfa_mixer_desc *desc, const void *o, cons
     return ok();
 }
 
-cyfa_status cyfa_decode_workspace_size(const cyfa_dec_desc *desc, size_t *bytes) {
-    if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
-    cyfa_status st = check_dec(desc);
-    if (st != CYFA_OK) return st;
-    *bytes = round_up(cyfa::readout_bytes(desc->H, desc->m));
-    return ok();
-}
+}  // extern "C"
 
-cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
-                             const float *delta, const float *log_alpha, const float *beta,
-                             const float *R, float *K, float *V, double *clock, void *o,
-                             float *logits_out, void *workspace, size_t workspace_bytes,
-                             void *stream) {
+// Scratch of cyfa_decode_step_noalloc: one copy per GPU, for the life of the
+// process.  In host code `scratch` names a host-side stand-in, never the device
+// memory: its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[CYFA_DECODE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+cyfa_status check_decode_args(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
+                              const float *delta, const float *log_alpha, const float *beta,
+                              const float *R, float *K, float *V, double *clock, void *o,
+                              float *logits_out) {
     cyfa_status st = check_dec(desc);
     if (st != CYFA_OK) return st;
     if (!q || !k || !v || !delta || !K || !V || !clock || !o)
@@ -454,19 +455,20 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     if (!aligned(clock, 8)) return fail(CYFA_ERR_INVALID_ARGUMENT, "clock must be 8-byte aligned");
     if (K == V || o == (void *)K || o == (void *)V)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "outputs must not alias each other");
-    const size_t need = round_up(cyfa::readout_bytes(desc->H, desc->m));
-    if (!workspace || workspace_bytes < need)
-        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
-    if (!aligned(workspace, kWsAlign))
-        return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+    return CYFA_OK;
+}
 
+// Both decode entry points: readout matrices into M (every entry written), then
+// the step.
+cyfa_status run_decode(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
+                       const float *delta, const float *log_alpha, const float *beta, const float *R,
+                       float *K, float *V, double *clock, void *o, float *logits_out, float *M,
+                       hipStream_t s) {
     cyfa::DecParams p{};
     p.N = desc->N; p.H = desc->H; p.dk = desc->d_k; p.dv = desc->d_v; p.m = desc->m;
     p.scale = desc->scale; p.dtype = desc->dtype;
     p.q = q; p.k = k; p.v = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R;
     p.K = K; p.V = V; p.clock = clock; p.o = o; p.logits = logits_out;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    float *M = static_cast<float *>(workspace);
     hipError_t e = p.m > cyfa::kMaxActive ? cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s)
                                           : cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
     if (e == hipSuccess) e = mark(g_ev_start, s);
@@ -474,6 +476,82 @@ cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const voi
     if (e == hipSuccess) e = mark(g_ev_stop, s);
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "decode launch: %s", hipGetErrorString(e));
     return ok();
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of `scratch` (looked up on first use).
+cyfa_status scratch_for_stream(hipStream_t s, float **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(CYFA_ERR_LAUNCH, "no usable current device");
+    if (s) {
+        int sdev = -1;
+        if (hipStreamGetDevice(s, &sdev) != hipSuccess)
+            return fail(CYFA_ERR_INVALID_ARGUMENT, "cannot query the stream's device");
+        if (sdev != dev)
+            return fail(CYFA_ERR_INVALID_ARGUMENT,
+                        "stream belongs to device %d but device %d is current", sdev, dev);
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(CYFA_ERR_LAUNCH, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = static_cast<float *>(g_scratch_ptr[dev]);
+    return CYFA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cyfa_status cyfa_decode_workspace_size(const cyfa_dec_desc *desc, size_t *bytes) {
+    if (!bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    cyfa_status st = check_dec(desc);
+    if (st != CYFA_OK) return st;
+    *bytes = round_up(cyfa::readout_bytes(desc->H, desc->m));
+    return ok();
+}
+
+cyfa_status cyfa_decode_step(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
+                             const float *delta, const float *log_alpha, const float *beta,
+                             const float *R, float *K, float *V, double *clock, void *o,
+                             float *logits_out, void *workspace, size_t workspace_bytes,
+                             void *stream) {
+    cyfa_status st = check_decode_args(desc, q, k, v, delta, log_alpha, beta, R, K, V, clock, o, logits_out);
+    if (st != CYFA_OK) return st;
+    const size_t need = round_up(cyfa::readout_bytes(desc->H, desc->m));
+    if (!workspace || workspace_bytes < need)
+        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (!aligned(workspace, kWsAlign))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+    return run_decode(desc, q, k, v, delta, log_alpha, beta, R, K, V, clock, o, logits_out,
+                      static_cast<float *>(workspace), static_cast<hipStream_t>(stream));
+}
+
+cyfa_status cyfa_decode_step_noalloc(const cyfa_dec_desc *desc, const void *q, const void *k, const void *v,
+                                     const float *delta, const float *log_alpha, const float *beta,
+                                     const float *R, float *K, float *V, double *clock, void *o,
+                                     float *logits_out, void *stream) {
+    cyfa_status st = check_decode_args(desc, q, k, v, delta, log_alpha, beta, R, K, V, clock, o, logits_out);
+    if (st != CYFA_OK) return st;
+    const size_t need = cyfa::readout_bytes(desc->H, desc->m);
+    if (need > CYFA_DECODE_NOALLOC_SCRATCH_BYTES)
+        return fail(CYFA_ERR_UNSUPPORTED,
+                    "decode scratch of %zu bytes (H = %d, m = %d) exceeds the fixed %u-byte array of the "
+                    "no-allocation entry point; use cyfa_decode_step with a workspace",
+                    need, desc->H, desc->m, (unsigned)CYFA_DECODE_NOALLOC_SCRATCH_BYTES);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    float *M = nullptr;
+    st = scratch_for_stream(s, &M);
+    if (st != CYFA_OK) return st;
+    return run_decode(desc, q, k, v, delta, log_alpha, beta, R, K, V, clock, o, logits_out, M, s);
 }
 
 const char *cyfa_status_string(cyfa_status status) {

@@ -29,7 +29,8 @@ def store_rows(m: int) -> int:
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
             "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_mixer_prologue",
-            "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step", "cyfa_set_timing_events",
+            "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step",
+            "cyfa_decode_step_noalloc", "cyfa_set_timing_events",
             "cyfa_status_string", "cyfa_last_error", "cyfa_version")
 
 
@@ -92,6 +93,8 @@ def load() -> ctypes.CDLL:
         lib.cyfa_decode_workspace_size.restype = ctypes.c_int
         lib.cyfa_decode_step.argtypes = [ctypes.POINTER(DecDesc)] + [_vp] * 13 + [ctypes.c_size_t, _vp]
         lib.cyfa_decode_step.restype = ctypes.c_int
+        lib.cyfa_decode_step_noalloc.argtypes = [ctypes.POINTER(DecDesc)] + [_vp] * 13
+        lib.cyfa_decode_step_noalloc.restype = ctypes.c_int
         lib.cyfa_status_string.argtypes = [ctypes.c_int]
         lib.cyfa_status_string.restype = ctypes.c_char_p
         lib.cyfa_last_error.argtypes = []
@@ -382,3 +385,34 @@ def decode_step(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, 
                                  ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
     _check(st)
     return (o, logits) if return_logits else o
+
+
+DECODE_NOALLOC_SCRATCH_BYTES = 4 << 20
+
+
+def decode_step_noalloc(q, k, v, delta, K, V, clock, log_alpha=None, beta=None, R=None, *,
+                        scale=None, m=127, out, logits_out=None, stream=None):
+    """``decode_step`` through cyfa_decode_step_noalloc: no workspace, the library's
+    fixed per-GPU scratch array instead.  The caller passes every output (``out``
+    [N,H,dv] in q's dtype, optional ``logits_out`` [N,H,m] float32), so this call
+    allocates nothing either.  Returns ``out``."""
+    N, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = _dtype_code(q)
+    _need(k, (N, H, dk), q.dtype, "k")
+    _need(v, (N, H, dv), q.dtype, "v")
+    for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
+        _need(t, (N, H), torch.float32, name)
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(K, (N, H, store_rows(m), dk), torch.float32, "K")
+    _need(V, (N, H, store_rows(m), dv), torch.float32, "V")
+    _need(clock, (N, H), torch.float64, "clock")
+    _need(out, (N, H, dv), q.dtype, "out")
+    _need(logits_out, (N, H, m), torch.float32, "logits_out")
+    desc = decode_desc(N, H, dk, dv, m=m, scale=scale, dtype=dt)
+    st = load().cyfa_decode_step_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
+                                         _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(K), _ptr(V),
+                                         _ptr(clock), _ptr(out), _ptr(logits_out),
+                                         _stream_handle(stream))
+    _check(st)
+    return out

@@ -120,6 +120,27 @@ def test_decode_rejects_before_launch():
     assert st == 1
 
 
+def test_decode_noalloc_rejects_before_launch():
+    """The no-allocation decode step validates like cyfa_decode_step and refuses a
+    readout scratch larger than its fixed array, all before any HIP call."""
+    lib = cyfa.load()
+    d = cyfa.decode_desc(2, 2, 64, 64)
+    assert lib.cyfa_decode_step_noalloc(ctypes.byref(d), *([None] * 13)) == 1
+    d = cyfa.decode_desc(2, 2, 64, 64, m=4)
+    assert lib.cyfa_decode_step_noalloc(ctypes.byref(d), *([None] * 13)) == 1
+    base = 1 << 30                                   # fake, aligned, never dereferenced
+    ptr = lambda i: ctypes.c_void_p(base + (i << 24))  # noqa: E731
+    args = [ptr(i) for i in range(4)] + [None, None, None] + [ptr(i) for i in range(4, 8)] + [None]
+    for H, m in ((65, 127), (17, 255)):              # 4 MiB + 64 KiB, 4 MiB + 256 KiB of readout matrices
+        d = cyfa.decode_desc(1, H, 128, 128, m=m)
+        assert lib.cyfa_decode_step_noalloc(ctypes.byref(d), *args, None) == 2
+        assert b"exceeds" in lib.cyfa_last_error()
+    bad = list(args)
+    bad[0] = ctypes.c_void_p(base + 8)               # misaligned q
+    d = cyfa.decode_desc(1, 4, 128, 128)
+    assert lib.cyfa_decode_step_noalloc(ctypes.byref(d), *bad, None) == 1
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cyfa, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(cyfa, "_lib", None)

@@ -302,7 +302,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
             gsum += (double)lane63(Gl);
         }
         if (c + 1 < c_end) load(c + 1);
-        __syncthreads();
+        lds_barrier();
         const int kt = opq(2 * buf * STILE + trs), vt = opq((2 * buf + 1) * STILE + trs);
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks) {
@@ -652,14 +652,14 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
-        __syncthreads();
+        lds_barrier();
         if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, Tb, tid, pf);
         // factor applied to the carried states this chunk, and whether the chunk's
         // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
         const bool fac = __builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[2])) != 0;
         build_writes_swz<CC, true, NT, CSW>(s, s.As, tid, m);
-        __syncthreads();
+        lds_barrier();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A.  With the
         //    tile holding A_dec (rows times the right decay), Gamma_rs = gam_r decw_s
         //    and O' = eps (.) (Q Kbar'^T + S A_dec), S the causal Q K^T and Kbar' the
@@ -685,7 +685,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) oacc[v] *= gt;
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks)
             oacc = mma(lds8_tr(At + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), oacc);
@@ -735,7 +735,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             if (v4 == 3 && w == 3 && hl) xv[3] = (__bf16)1.f;
             *reinterpret_cast<bf16x4 *>(Wrow + 8 * v4) = xv;
         }
-        __syncthreads();
+        lds_barrier();
         // -- middle step 2: slot logits, transposed: Z^T = M X^T.  Wave w owns slots
         //    32w .. 32w+31; lane (token 32 nb + l32, half hl) holds 16 of them.
         f32x16 zacc[RB];
@@ -789,7 +789,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             sm += __shfl_xor(sm, 32);
             if (hl == 0) redw[32 * nb] = make_float2(mx, sm);
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int nb = 0; nb < RB; ++nb) {
             float2 pr[4];
@@ -812,7 +812,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 *reinterpret_cast<bf16x4 *>(wrow + 8 * v4) = wv;
             }
         }
-        __syncthreads();
+        lds_barrier();
         // -- middle step 4: O''_r = U(-lambda_r) M^T W_r, transposed: Y^T = M^T W^T.
         //    Wave w owns basis rows 32w .. 32w+31; each (cos, sin) pair sits in two
         //    consecutive registers of one lane, so the rotation is in-lane.
@@ -840,7 +840,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                 *reinterpret_cast<bf16x4 *>(O2row + 8 * v4) = ov;
             }
         }
-        __syncthreads();
+        lds_barrier();
         // -- D: value pass.  O = gamma (.) O'' Vbar + (O'' A^T (.) Gamma) V, as the key
         //    pass: O = eps (.) (O'' Vbar' + S2 V) with S2 the causal O'' A_dec^T (a
         //    chunk that is not factored as before); computed transposed, lane (token
@@ -861,7 +861,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) pacc[v] *= gt;
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks)
             pacc = mma(lds8_tr(Vt + 16 * ks * SWS, SWS), lds8(Sa + 16 * ks), pacc);
@@ -903,7 +903,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
                                   vacc[x]);
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));

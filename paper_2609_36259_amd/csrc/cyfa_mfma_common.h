@@ -168,6 +168,18 @@ __host__ __device__ __forceinline__ int dump_index_V(int i, int c) {
     return 128 * 128 + dump_off(w, ib, lane_lo + 32 * h, v);
 }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() is a full
+// workgroup fence: every wave first waits for all of its outstanding global loads,
+// so a chunk prefetch issued just before a barrier would expose the whole memory
+// latency there.  Here only the LDS operations are waited for; a prefetch stays in
+// flight across the barrier and is waited for where its registers are used.  No
+// wave reads another wave's global-memory results inside these kernels.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Value of lane l ^ 1 (DPP quad permutation [1,0,3,2]).
 __device__ __forceinline__ float swap_pair(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));

@@ -170,6 +170,34 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc,
                               void *stream);
 
 /*
+ * Same as cyfa_forward for packed (concatenated) sequences of different lengths:
+ * B sequences stored back to back, with no padding rows.
+ *   cu_seqlens  [B + 1] int32 device array of row offsets, cu_seqlens[0] = 0 and
+ *               nondecreasing: sequence b is rows cu_seqlens[b] .. cu_seqlens[b+1]-1
+ *               (its length is clamped to [0, T]; desc->T is the longest length,
+ *               which sizes the workspace and the segment plan)
+ *   q, k        [total, H, d_k];  v, o [total, H, d_v];  delta, log_alpha, beta
+ *               [total, H];  logits_out [total, H, m]  (total = cu_seqlens[B])
+ *   K0, V0, clock0, K_out, V_out, clock_out: per sequence, as for cyfa_forward
+ * Each sequence evolves from its own initial state and clock (Sec. 3.1, Eqs.
+ * cyfa-physical-recurrence / cyfa-physical-readout, one recurrence per sequence);
+ * the result equals cyfa_forward_lens on the same sequences padded to T rows.
+ * Workspace size (cyfa_forward_workspace_size with desc) and errors as for
+ * cyfa_forward; cu_seqlens is required and must be 4-byte aligned.
+ */
+cyfa_status cyfa_forward_varlen(const cyfa_fwd_desc *desc,
+                                const void *q, const void *k, const void *v,
+                                const float *delta, const float *log_alpha, const float *beta,
+                                const float *R,
+                                const int32_t *cu_seqlens,
+                                const float *K0, const float *V0, const double *clock0,
+                                void *o,
+                                float *K_out, float *V_out, double *clock_out,
+                                float *logits_out,
+                                void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/*
  * Bytes of device workspace cyfa_backward needs for `desc` (host-only).  The
  * backward keeps the states entering every 16-token chunk and the adjoint
  * states at every chunk's end (2 x B H ceil(T/16) 128 (d_k + d_v) floats) and

@@ -239,12 +239,15 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
                              V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
 }
 
-cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
-                              const float *delta, const float *log_alpha, const float *beta,
-                              const float *R, const int32_t *lens, const float *K0, const float *V0,
-                              const double *clock0, void *o, float *K_out, float *V_out,
-                              double *clock_out, float *logits_out, void *workspace,
-                              size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+// cyfa_forward_lens (lens or nothing) and cyfa_forward_varlen (cu_seqlens)
+cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                         const float *delta, const float *log_alpha, const float *beta, const float *R,
+                         const int32_t *lens, const int32_t *cu, const float *K0, const float *V0,
+                         const double *clock0, void *o, float *K_out, float *V_out, double *clock_out,
+                         float *logits_out, void *workspace, size_t workspace_bytes, void *stream) {
     FwdPlan plan;
     cyfa_status st = plan_forward(desc, &plan);
     if (st != CYFA_OK) return st;
@@ -256,7 +259,7 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
     for (int i = 0; i < 8; ++i)
         if (vec[i] && !aligned(vec[i], 16))
             return fail(CYFA_ERR_INVALID_ARGUMENT, "%s must be 16-byte aligned", vec_names[i]);
-    const void *sc[] = {delta, log_alpha, beta, R, logits_out, lens};
+    const void *sc[] = {delta, log_alpha, beta, R, logits_out, lens, cu};
     for (const void *p : sc)
         if (p && !aligned(p, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
     if ((clock0 && !aligned(clock0, 8)) || (clock_out && !aligned(clock_out, 8)))
@@ -277,7 +280,7 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
     p.dtype = desc->dtype;
     p.q = q; p.k = k; p.v = v; p.delta = delta; p.log_alpha = log_alpha; p.beta = beta; p.R = R;
     p.K0 = K0; p.V0 = V0; p.clock0 = clock0; p.o = o; p.K_out = K_out; p.V_out = V_out;
-    p.clock_out = clock_out; p.logits = logits_out; p.lens = lens;
+    p.clock_out = clock_out; p.logits = logits_out; p.lens = lens; p.cu = cu;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     char *ws = static_cast<char *>(workspace);
@@ -297,6 +300,30 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
     }
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "forward launch: %s", hipGetErrorString(e));
     return ok();
+}
+}  // namespace
+
+extern "C" {
+
+cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                              const float *delta, const float *log_alpha, const float *beta,
+                              const float *R, const int32_t *lens, const float *K0, const float *V0,
+                              const double *clock0, void *o, float *K_out, float *V_out,
+                              double *clock_out, float *logits_out, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    return forward_impl(desc, q, k, v, delta, log_alpha, beta, R, lens, nullptr, K0, V0, clock0, o, K_out,
+                        V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
+}
+
+cyfa_status cyfa_forward_varlen(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
+                                const float *delta, const float *log_alpha, const float *beta,
+                                const float *R, const int32_t *cu_seqlens, const float *K0, const float *V0,
+                                const double *clock0, void *o, float *K_out, float *V_out,
+                                double *clock_out, float *logits_out, void *workspace,
+                                size_t workspace_bytes, void *stream) {
+    if (!cu_seqlens) return fail(CYFA_ERR_INVALID_ARGUMENT, "cu_seqlens is required");
+    return forward_impl(desc, q, k, v, delta, log_alpha, beta, R, nullptr, cu_seqlens, K0, V0, clock0, o, K_out,
+                        V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
 }
 
 cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes) {

@@ -18,6 +18,7 @@ struct BwdParams {
     const void *q, *k, *v, *dout;
     const float *delta, *log_alpha, *beta, *R;
     const int *lens;
+    const int *cu;                  // packed sequences (the forward's group pre-pass only; see FwdParams)
     const float *K0, *V0;
     const double *clock0;
     const float *dK_T, *dV_T;

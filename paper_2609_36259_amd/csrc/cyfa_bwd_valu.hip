@@ -68,7 +68,12 @@ __device__ __forceinline__ float wmax(float x) {
 }
 
 __device__ __forceinline__ int bwd_tokens(const BwdParams &p, int b) {
+    if (p.cu) return min(max(p.cu[b + 1] - p.cu[b], 0), p.T);
     return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
+}
+// first row of sequence b in the [rows, H, ...] tensors
+__device__ __forceinline__ size_t brow0(const BwdParams &p, int b) {
+    return p.cu ? (size_t)p.cu[b] : (size_t)b * p.T;
 }
 
 // Per-chunk scalar tables.
@@ -88,7 +93,7 @@ __device__ void chunk_tables(const BwdParams &p, int b, int h, int t0, int Tb, d
     if (tid < kC) {
         const int t = t0 + tid;
         const bool live = t < Tb;
-        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        const size_t si = (brow0(p, b) + t) * p.H + h;
         s.lam[tid] = live ? (double)p.delta[si] : 0.0;
         s.G[tid] = (live && p.log_alpha) ? p.log_alpha[si] : 0.f;
         s.beta[tid] = live ? (p.beta ? p.beta[si] : 1.f) : 0.f;
@@ -211,8 +216,8 @@ __device__ void add_scores_times(const float (*S)[kC + 1], const float (*A)[kLD]
 }
 
 template <typename Tin>
-__device__ __forceinline__ float ld_row(const void *base, int b, int t, int h, int c, int T, int H, int D, bool live) {
-    return live ? load_as_float(static_cast<const Tin *>(base), (((size_t)b * T + t) * H + h) * D + c) : 0.f;
+__device__ __forceinline__ float ld_row(const void *base, size_t row0, int t, int h, int c, int H, int D, bool live) {
+    return live ? load_as_float(static_cast<const Tin *>(base), ((row0 + t) * H + h) * D + c) : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -240,7 +245,7 @@ __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
     {
         const int t_start = min(c_begin * kC, Tb);
         double ds = 0.0;
-        for (int t = tid; t < t_start; t += kNT) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
+        for (int t = tid; t < t_start; t += kNT) ds += (double)p.delta[(brow0(p, b) + t) * p.H + h];
         dred[tid] = ds;
         __syncthreads();
         for (int w = kNT / 2; w > 0; w >>= 1) {
@@ -272,11 +277,11 @@ __global__ __launch_bounds__(kNT) void bwd_states_local_kernel(BwdParams p) {
         }
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
-            Ks[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
+            Ks[r][cc] = ld_row<Tin>(p.k, brow0(p, b), t0 + r, h, cc, p.H, DK, t0 + r < Tb);
         }
         for (int e = tid; e < kC * DV; e += kNT) {
             const int r = e / DV, cc = e % DV;
-            Vs[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
+            Vs[r][cc] = ld_row<Tin>(p.v, brow0(p, b), t0 + r, h, cc, p.H, DV, t0 + r < Tb);
         }
         chunk_tables(p, b, h, t0, Tb, lam, tab, tid);
         const float GC = tab.G[kC - 1], gC = __expf(GC);
@@ -385,8 +390,8 @@ __global__ __launch_bounds__(kReadoutThreads) void bwd_readout_kernel(BwdParams 
         for (int e = tid; e < kC * DK; e += NT) {
             const int r = e / DK, cc = e % DK;
             const bool live = t0 + r < Tb;
-            In0[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, live);
-            In1[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, live);
+            In0[r][cc] = ld_row<Tin>(p.q, brow0(p, b), t0 + r, h, cc, p.H, DK, live);
+            In1[r][cc] = ld_row<Tin>(p.k, brow0(p, b), t0 + r, h, cc, p.H, DK, live);
         }
         chunk_tables<NT>(p, b, h, t0, Tb, p.clk[(size_t)bh * p.nc + c], tab, tid);
         build_writes<NT>(tab, m, As, tid);
@@ -424,8 +429,8 @@ __global__ __launch_bounds__(kReadoutThreads) void bwd_readout_kernel(BwdParams 
         for (int e = tid; e < kC * DV; e += NT) {
             const int r = e / DV, cc = e % DV;
             const bool live = t0 + r < Tb;
-            In0[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, live);
-            In1[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, live);
+            In0[r][cc] = ld_row<Tin>(p.dout, brow0(p, b), t0 + r, h, cc, p.H, DV, live);
+            In1[r][cc] = ld_row<Tin>(p.v, brow0(p, b), t0 + r, h, cc, p.H, DV, live);
         }
         // X = scale U(lambda) p
         rotate_rows<NT>(Xs, tab, m, 1.f, p.scale, tid);
@@ -582,15 +587,15 @@ __global__ __launch_bounds__(kNT) void bwd_adjoint_local_kernel(BwdParams p) {
         if (tid == 0) p.Gout[(size_t)bh * p.nc + c] = Go;
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
-            Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, t0 + r < Tb);
+            Qs[r][cc] = ld_row<Tin>(p.q, brow0(p, b), t0 + r, h, cc, p.H, DK, t0 + r < Tb);
         }
         for (int e = tid; e < kC * DV; e += kNT) {
             const int r = e / DV, cc = e % DV;
-            dOs[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, t0 + r < Tb);
+            dOs[r][cc] = ld_row<Tin>(p.dout, brow0(p, b), t0 + r, h, cc, p.H, DV, t0 + r < Tb);
         }
         if (tid < kC) {
             const int t = t0 + tid;
-            Gs[tid] = (t < Tb && p.log_alpha) ? p.log_alpha[((size_t)b * p.T + t) * p.H + h] : 0.f;
+            Gs[tid] = (t < Tb && p.log_alpha) ? p.log_alpha[(brow0(p, b) + t) * p.H + h] : 0.f;
         }
         __syncthreads();
         if (tid == 0)
@@ -695,14 +700,14 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             const bool live = t0 + r < Tb;
-            Qs[r][cc] = ld_row<Tin>(p.q, b, t0 + r, h, cc, p.T, p.H, DK, live);
-            Ks[r][cc] = ld_row<Tin>(p.k, b, t0 + r, h, cc, p.T, p.H, DK, live);
+            Qs[r][cc] = ld_row<Tin>(p.q, brow0(p, b), t0 + r, h, cc, p.H, DK, live);
+            Ks[r][cc] = ld_row<Tin>(p.k, brow0(p, b), t0 + r, h, cc, p.H, DK, live);
         }
         for (int e = tid; e < kC * DV; e += kNT) {
             const int r = e / DV, cc = e % DV;
             const bool live = t0 + r < Tb;
-            Vs[r][cc] = ld_row<Tin>(p.v, b, t0 + r, h, cc, p.T, p.H, DV, live);
-            dOs[r][cc] = ld_row<Tin>(p.dout, b, t0 + r, h, cc, p.T, p.H, DV, live);
+            Vs[r][cc] = ld_row<Tin>(p.v, brow0(p, b), t0 + r, h, cc, p.H, DV, live);
+            dOs[r][cc] = ld_row<Tin>(p.dout, brow0(p, b), t0 + r, h, cc, p.H, DV, live);
         }
         for (int e = tid; e < kC * kStoreRows; e += kNT) {
             const int r = e >> 7, ii = e & 127;
@@ -845,7 +850,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
             for (int ih = 0; ih < IHV; ++ih) sum += red[(ih * kC + s) * DV + cc];
             float acc = __expf(GC - tab.G[s]) * sum;
             for (int r = s; r < kC; ++r) acc = fmaf(Suoa[r][s], dOs[r][cc], acc);
-            store_from_float(gv, (((size_t)b * p.T + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
+            store_from_float(gv, ((brow0(p, b) + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
         }
         // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i];
         // thread (row i, part) sums its share of the columns for every token s
@@ -937,14 +942,14 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 const bool live = t < Tb;
                 p.dG[ti] = live ? sums + p.udu[ti] : 0.f;
                 p.dlam[ti] = live ? p.dlam[ti] + gl : 0.f;
-                if (p.gbeta) p.gbeta[((size_t)b * p.T + t) * p.H + h] = live ? db : 0.f;
+                if (p.gbeta) p.gbeta[(brow0(p, b) + t) * p.H + h] = live ? db : 0.f;
             }
         }
         for (int e = tid; e < kC * DK; e += kNT) {
             const int r = e / DK, cc = e % DK;
             const int t = t0 + r;
             if (t >= p.T) continue;
-            const size_t gi = (((size_t)b * p.T + t) * p.H + h) * DK + cc;
+            const size_t gi = ((brow0(p, b) + t) * p.H + h) * DK + cc;
             store_from_float(gq, gi, t < Tb ? gQ[r][cc] : 0.f);
             store_from_float(gk, gi, t < Tb ? gK[r][cc] : 0.f);
         }
@@ -991,12 +996,12 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
     for (int t = t_hi - 1; t >= t_lo; --t) {
         rg += dG[t] + (t == Tb - 1 ? fin : 0.f);
         rl += dl[t];
-        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        const size_t si = (brow0(p, b) + t) * p.H + h;
         if (p.glog_alpha) p.glog_alpha[si] = (float)rg;
         p.gdelta[si] = (float)rl;
     }
     for (int t = Tb + tid; t < p.T; t += kNT) {
-        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        const size_t si = (brow0(p, b) + t) * p.H + h;
         if (p.glog_alpha) p.glog_alpha[si] = 0.f;
         p.gdelta[si] = 0.f;
     }
@@ -1110,7 +1115,7 @@ hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws
     p.cpg = cpg;
     p.scale = f.scale; p.dtype = f.dtype;
     p.q = f.q; p.k = f.k; p.v = f.v;
-    p.delta = f.delta; p.log_alpha = f.log_alpha; p.beta = f.beta; p.lens = f.lens;
+    p.delta = f.delta; p.log_alpha = f.log_alpha; p.beta = f.beta; p.lens = f.lens; p.cu = f.cu;
     p.K0 = f.K0; p.V0 = f.V0; p.clock0 = f.clock0;
     const size_t BH = (size_t)f.B * f.H;
     char *w = static_cast<char *>(ws);

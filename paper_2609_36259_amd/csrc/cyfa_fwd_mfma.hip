@@ -239,7 +239,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     // segment total of log alpha (the decay reference G_end)
     double gpart = 0.0;
     if (p.log_alpha)
-        for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[((size_t)b * p.T + t) * p.H + h];
+        for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[(seq_row0(p, b) + t) * p.H + h];
     gpart = lane63(wave_incl_scan(gpart));
     if (lane == 0) red[w] = gpart;
 
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     float dl, g, be;
     auto load = [&](int c) {
         const int t0 = c * CC;
-        const size_t base = (((size_t)b * p.T + t0) * row_el + (size_t)h * D) * 2;
+        const size_t base = ((seq_row0(p, b) + t0) * row_el + (size_t)h * D) * 2;
         const char *kb = reinterpret_cast<const char *>(p.k) + base;
         const char *vb = reinterpret_cast<const char *>(p.v) + base;
 #pragma unroll
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
             pv[it] = in ? *reinterpret_cast<const uint4 *>(vb + loff + it * pass) : make_uint4(0, 0, 0, 0);
         }
         const int t = t0 + lane;
-        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        const size_t si = (seq_row0(p, b) + t) * p.H + h;
         const bool tin = lane < CC && t < Tb;
         dl = tin ? p.delta[si] : 0.f;
         g = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
@@ -766,7 +766,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             const int r = 32 * nb + l32;
             if (p.logits && r < n) {
                 // the logit accumulators hold log2(e) z; report z
-                float *lg = p.logits + (((size_t)b * p.T + t0 + r) * p.H + h) * m;
+                float *lg = p.logits + ((seq_row0(p, b) + t0 + r) * p.H + h) * m;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int slot = icol - l32 + 8 * (v >> 2) + h4 + (v & 3);
@@ -874,7 +874,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // as four 8-byte pieces (uniform chunk base plus a 32-bit lane offset); the
         // four waves' pieces of a token row merge in L2
         if (l32 < n) {
-            char *ob = reinterpret_cast<char *>(o + (((size_t)b * p.T + t0) * p.H + h) * D);
+            char *ob = reinterpret_cast<char *>(o + ((seq_row0(p, b) + t0) * p.H + h) * D);
             const unsigned loff = (unsigned)opq((l32 * p.H * D + 32 * w + h4) * 2);
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4) {

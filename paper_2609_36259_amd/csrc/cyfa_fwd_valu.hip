@@ -84,6 +84,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
     const int lane = tid & 63, wave = tid >> 6;
     const int m = p.m, C = p.chunk, T = p.T, H = p.H;
     const int Tb = seq_tokens(p, b);                  // this sequence's tokens
+    const size_t row0 = seq_row0(p, b);               // its first row
     const int t_lo = G > 1 ? min(grp * cpg * 16, Tb) : 0;
     const int t_hi = G > 1 ? min((grp + 1) * cpg * 16, Tb) : Tb;
     const bool last = grp == G - 1;
@@ -133,17 +134,17 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
         // ---- load the chunk (rows past the end are zero: no write, no decay, no shift)
         for (int e = tid; e < C * DK; e += kThreads) {
             const int r = e / DK, c = e % DK;
-            const size_t gi = (((size_t)b * T + t0 + r) * H + h) * DK + c;
+            const size_t gi = ((row0 + t0 + r) * H + h) * DK + c;
             Qs[r][c] = r < n ? load_as_float(q, gi) : 0.f;
             Ks[r][c] = r < n ? load_as_float(k, gi) : 0.f;
         }
         for (int e = tid; e < C * DV; e += kThreads) {
             const int r = e / DV, c = e % DV;
-            Vs[r][c] = r < n ? load_as_float(v, (((size_t)b * T + t0 + r) * H + h) * DV + c) : 0.f;
+            Vs[r][c] = r < n ? load_as_float(v, ((row0 + t0 + r) * H + h) * DV + c) : 0.f;
         }
         if (tid < C) {
             const int r = tid;
-            const size_t si = ((size_t)b * T + t0 + r) * H + h;
+            const size_t si = (row0 + t0 + r) * H + h;
             lam_s[r] = r < n ? (double)p.delta[si] : 0.0;
             G_s[r] = (r < n && p.log_alpha) ? p.log_alpha[si] : 0.f;
             beta_s[r] = r < n ? (p.beta ? p.beta[si] : 1.f) : 0.f;
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
             if (i < m) {
                 for (int j = 0; j < m; ++j) acc = fmaf(Mv(i, j), Xb[r][j], acc);
                 if (p.logits && r < n)
-                    p.logits[(((size_t)b * T + t0 + r) * H + h) * m + i] = acc;
+                    p.logits[((row0 + t0 + r) * H + h) * m + i] = acc;
             }
             Ob[r][i] = acc;
         }
@@ -317,7 +318,7 @@ __global__ __launch_bounds__(valu_threads(DK, DV, ROWS)) void fwd_valu_kernel(Fw
             if (vpart == 0 && r < n) {
                 float acc = __expf(G_s[r]) * part;
                 for (int s = 0; s <= r; ++s) acc = fmaf(Ss[r][s], Vs[s][vc], acc);
-                store_from_float(o, (((size_t)b * T + t0 + r) * H + h) * DV + vc, acc);
+                store_from_float(o, ((row0 + t0 + r) * H + h) * DV + vc, acc);
             }
         }
         // value state carry: Vbar <- gamma^C Vbar + A^T (right-rescaled V)

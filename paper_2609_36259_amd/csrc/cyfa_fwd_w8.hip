@@ -325,7 +325,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
             if (g == 0) redw[16 * rt] = make_float2(mx, sm);
             if (p.logits && tok < n) {
                 // the accumulators hold log2(e) z; report z
-                float *lg = p.logits + (((size_t)b * p.T + t0 + tok) * p.H + h) * m;
+                float *lg = p.logits + ((seq_row0(p, b) + t0 + tok) * p.H + h) * m;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int slot = 16 * w + g4 + r;
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(W8, 1) void chunk64_w8_kernel(MfmaArgs a) {
             for (int it = 0; it < 2; ++it) {
                 const int r = r0 + 32 * it;
                 if (r < n)
-                    *reinterpret_cast<uint4 *>(o + (((size_t)b * p.T + t0 + r) * p.H + h) * D + d0) =
+                    *reinterpret_cast<uint4 *>(o + ((seq_row0(p, b) + t0 + r) * p.H + h) * D + d0) =
                         *reinterpret_cast<const uint4 *>(Stg + 32 * it * QS);
             }
         }

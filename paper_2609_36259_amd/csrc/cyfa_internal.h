@@ -25,6 +25,8 @@ struct FwdParams {
     double *clock_out;
     float *logits;
     const int *lens;                // [B] tokens of each sequence (clamped to [0, T]); NULL: all T
+    const int *cu;                  // [B+1] packed sequences: sequence b is rows cu[b] .. cu[b+1]-1 of
+                                    // [total, H, d] tensors (count clamped to [0, T]); NULL: [B, T, H, d]
 };
 
 struct DecParams {
@@ -55,7 +57,13 @@ hipError_t launch_decode(const DecParams &p, const float *M, hipStream_t s);
 // t >= that count are treated like the tail past the end of a sequence: no
 // write, no decay, no clock shift, and their output rows are not written.
 __device__ __forceinline__ int seq_tokens(const FwdParams &p, int b) {
+    if (p.cu) return min(max(p.cu[b + 1] - p.cu[b], 0), p.T);
     return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
+}
+// Row (token index over the whole [rows, H, ...] tensor) of token 0 of sequence b:
+// b T for the padded layout, cu[b] for packed sequences.
+__device__ __forceinline__ size_t seq_row0(const FwdParams &p, int b) {
+    return p.cu ? (size_t)p.cu[b] : (size_t)b * p.T;
 }
 __device__ __forceinline__ float load_as_float(const float *p, size_t i) { return p[i]; }
 __device__ __forceinline__ float load_as_float(const __hip_bfloat16 *p, size_t i) {

@@ -82,7 +82,7 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     // Uniform chunk base (scalar registers) plus a fixed 32-bit per-lane byte offset:
     // no per-lane 64-bit address arithmetic.  Rows past the sequence read as zero.
     const size_t row_el = (size_t)p.H * D;           // elements between consecutive tokens
-    const size_t base = ((size_t)b * p.T + t0) * row_el + (size_t)h * D;
+    const size_t base = (seq_row0(p, b) + t0) * row_el + (size_t)h * D;
     const char *q = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.q) + base);
     const char *k = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.k) + base);
     const char *v = reinterpret_cast<const char *>(static_cast<const __bf16 *>(p.v) + base);
@@ -111,7 +111,7 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
     }
     if (tid < 64) {
         const int t = t0 + tid;
-        const size_t sbase = ((size_t)b * p.T + t0) * p.H + h;
+        const size_t sbase = (seq_row0(p, b) + t0) * p.H + h;
         // opaque per chunk: otherwise base + lane offset is kept per lane (64-bit)
         // across the whole chunk loop
         const unsigned soff = (unsigned)opq(tid * p.H);

@@ -27,7 +27,7 @@ def store_rows(m: int) -> int:
     return STORE_ROWS if m <= 127 else 2 * STORE_ROWS
 
 # Every symbol include/cyfa.h declares.
-EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens",
+EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens", "cyfa_forward_varlen",
             "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_mixer_prologue",
             "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step",
             "cyfa_decode_step_noalloc", "cyfa_set_timing_events",
@@ -79,6 +79,8 @@ def load() -> ctypes.CDLL:
         lib.cyfa_forward.restype = ctypes.c_int
         lib.cyfa_forward_lens.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 17 + [ctypes.c_size_t, _vp]
         lib.cyfa_forward_lens.restype = ctypes.c_int
+        lib.cyfa_forward_varlen.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 17 + [ctypes.c_size_t, _vp]
+        lib.cyfa_forward_varlen.restype = ctypes.c_int
         lib.cyfa_backward_workspace_size.argtypes = [ctypes.POINTER(FwdDesc),
                                                      ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_backward_workspace_size.restype = ctypes.c_int
@@ -231,6 +233,57 @@ def forward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, scale=None, m=
                                   _ptr(V0), _ptr(clock0), _ptr(o), _ptr(K_out), _ptr(V_out),
                                   _ptr(clk), _ptr(logits), _ptr(workspace),
                                   ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
+    _check(st)
+    if not (return_state or return_logits):
+        return o
+    res = {"o": o}
+    if return_state:
+        res.update(K=K_out, V=V_out, clock=clk)
+    if return_logits:
+        res["logits"] = logits
+    return res
+
+
+def forward_varlen(q, k, v, delta, cu_seqlens, log_alpha=None, beta=None, R=None, *, max_len,
+                   scale=None, m=127, chunk=0, segments=0, kernel=KERNEL_AUTO, K0=None, V0=None,
+                   clock0=None, return_state=False, return_logits=False, out=None, workspace=None,
+                   stream=None):
+    """CyFA forward over packed sequences (cyfa_forward_varlen): q,k [total,H,dk],
+    v [total,H,dv], scalars [total,H]; ``cu_seqlens`` int32 [B+1] device offsets;
+    ``max_len`` the longest sequence.  States are per sequence ([B,H,S,d], clock [B,H]).
+    Returns ``o`` [total,H,dv] or a dict as ``forward``."""
+    total, H, dk = q.shape
+    dv = v.shape[-1]
+    B = cu_seqlens.shape[0] - 1
+    dt = _dtype_code(q)
+    _need(q, (total, H, dk), q.dtype, "q")
+    _need(k, (total, H, dk), q.dtype, "k")
+    _need(v, (total, H, dv), q.dtype, "v")
+    for name, t in (("delta", delta), ("log_alpha", log_alpha), ("beta", beta)):
+        _need(t, (total, H), torch.float32, name)
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(cu_seqlens, (B + 1,), torch.int32, "cu_seqlens")
+    S = store_rows(m)
+    _need(K0, (B, H, S, dk), torch.float32, "K0")
+    _need(V0, (B, H, S, dv), torch.float32, "V0")
+    _need(clock0, (B, H), torch.float64, "clock0")
+    desc = forward_desc(B, int(max_len), H, dk, dv, m=m, chunk=chunk, segments=segments, scale=scale,
+                        dtype=dt, kernel=kernel)
+    nbytes = forward_workspace_size(desc)
+    dev = q.device
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    o = out if out is not None else torch.empty((total, H, dv), dtype=q.dtype, device=dev)
+    _need(o, (total, H, dv), q.dtype, "out")
+    K_out = torch.empty((B, H, S, dk), dtype=torch.float32, device=dev) if return_state else None
+    V_out = torch.empty((B, H, S, dv), dtype=torch.float32, device=dev) if return_state else None
+    clk = torch.empty((B, H), dtype=torch.float64, device=dev) if return_state else None
+    logits = torch.empty((total, H, m), dtype=torch.float32, device=dev) if return_logits else None
+    st = load().cyfa_forward_varlen(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(delta),
+                                    _ptr(log_alpha), _ptr(beta), _ptr(R), _ptr(cu_seqlens), _ptr(K0),
+                                    _ptr(V0), _ptr(clock0), _ptr(o), _ptr(K_out), _ptr(V_out),
+                                    _ptr(clk), _ptr(logits), _ptr(workspace),
+                                    ctypes.c_size_t(workspace.numel()), _stream_handle(stream))
     _check(st)
     if not (return_state or return_logits):
         return o

@@ -82,9 +82,9 @@ typedef enum {
  *   d_k, d_v     head dims: 64, 128 or 256 each (the matrix-core kernel: 128 only)
  *   m            active slots, odd, 3..255 (see above for m > 127)
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
- *                8 or 16 (default 16); MFMA kernel: 32 or 64 (default 32).
- *                Results do not depend on it beyond rounding (App. B: the
- *                chunk form is exact).
+ *                8 or 16 (default 16); MFMA kernel: 32 or 64, evaluated in
+ *                32-token chunks (64 = two of them).  Results do not depend on
+ *                it beyond rounding (App. B: the chunk form is exact).
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
  *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
  *                than one only for d_k, d_v <= 128 and m <= 127).  The state

@@ -107,6 +107,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     plan->mfma = use_mfma;
     size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
     if (use_mfma) {
+        probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
         const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;

@@ -557,9 +557,8 @@ __device__ __forceinline__ bf16x8 decay_rows(bf16x8 v, const float *dw) {
 }
 
 // ---- 3. fused chunk forward, 32-token chunks ------------------------------------
-// (64-token chunks run the eight-wave kernel of cyfa_fwd_w8.hip.)  Two
-// workgroups share a compute unit; the readout matrix sits in LDS and the next
-// chunk is prefetched into registers.
+// Two workgroups share a compute unit; the readout matrix sits in LDS and the
+// next chunk is prefetched into registers.
 template <int CC>
 __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
@@ -955,13 +954,18 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
 }  // namespace
 
 // ---- host side --------------------------------------------------------------
-constexpr int kMfmaDefaultChunk = 32;
+// The matrix-core path evaluates App. B's chunk form in 32-token chunks.  A
+// requested chunk length of 64 is accepted and run as two 32-token chunks: the
+// chunk form is exact for any chunk length (the carried states after 64 tokens
+// are those after two steps of 32), so only the rounding order differs from a
+// 64-token evaluation.
+constexpr int kMfmaChunk = 32;
 
 bool mfma_supported(const FwdParams &p) {
     return p.dtype == 1 && p.dk == 128 && p.dv == 128 && (p.chunk == 32 || p.chunk == 64);
 }
 
-int mfma_default_chunk() { return kMfmaDefaultChunk; }
+int mfma_default_chunk() { return kMfmaChunk; }
 
 namespace {
 struct WsLayout {
@@ -1027,13 +1031,8 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
     // Timing events, when given, are taken by the fused kernel's own dispatch: they
     // bracket the kernel alone and add no gap between launches.
     if (a.nchunks > 0) {
-        if constexpr (CC == 64) {
-            if ((e = launch_chunk64_w8(a, BH * a.P, st, ev_start, ev_stop)) != hipSuccess) return e;
-        } else {
-            hipExtLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, ev_start,
-                                  ev_stop, 0, a);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
+        hipExtLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, ev_start, ev_stop, 0, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
         if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
@@ -1048,10 +1047,10 @@ size_t mfma_workspace_bytes(const FwdParams &p, int segments) {
 }
 
 int mfma_auto_segments(const FwdParams &p) {
-    // workgroups resident per compute unit: 2 with 32-token chunks, 1 with 64;
-    // split sequences until B*H*P fills 256 compute units
-    const int C = p.chunk;
-    const int slots = 256 * (C == 32 ? 2 : 1);
+    // two workgroups are resident per compute unit: split sequences until B*H*P
+    // fills the 256 compute units twice
+    const int C = kMfmaChunk;
+    const int slots = 256 * 2;
     const int seqs = p.B * p.H;
     int P = (slots + seqs - 1) / seqs;
     const int nchunks = (p.T + C - 1) / C;
@@ -1063,7 +1062,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop) {
     char *base = static_cast<char *>(ws);
     const WsLayout L = ws_layout(p, P);
-    const int C = p.chunk;
+    const int C = kMfmaChunk;
     MfmaArgs a{};
     a.p = p;
     a.chunk = C;
@@ -1084,7 +1083,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.zero_init = (p.K0 || p.V0) ? 0 : 1;
     const int BH = p.B * p.H;
 
-    hipError_t e = C == 32 ? launch_cc<32>(a, BH, st, ev_start, ev_stop) : launch_cc<64>(a, BH, st, ev_start, ev_stop);
+    hipError_t e = launch_cc<32>(a, BH, st, ev_start, ev_stop);
     if (e != hipSuccess) return e;
     if (a.want_final) {
         hipLaunchKernelGGL(state_out_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);

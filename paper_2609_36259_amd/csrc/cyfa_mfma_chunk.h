@@ -27,10 +27,6 @@ struct MfmaArgs {
     int want_final;      // last segment dumps its final state into fin_state
 };
 
-// fused forward for 64-token chunks on eight waves (one workgroup per (b, h, p));
-// optional events are taken by the kernel's dispatch
-hipError_t launch_chunk64_w8(const MfmaArgs &a, int groups, hipStream_t st, hipEvent_t ev_start,
-                             hipEvent_t ev_stop);
 
 namespace mfma {
 

@@ -60,6 +60,9 @@ FWD_LONG = Workload("long-ctx B1 T32768 H16 d128 slow-clock", 1, 32768, 16, 128,
                     seed=3, delta_mu=-1.0)
 DECODE = Workload("decode N256 H16 d128 prefix512 steps64", 256, 512 + 64, 16, 128, 128,
                   seed=4, dtype="f32", extra={"prefix": 512, "steps": 64})
+# The paper's own operator benchmark shape (its 400M model's layer at 2K tokens:
+# 4 heads of 256 channels, 32 sequences), with the value distributions above.
+FWD_PAPER_OP = Workload("paper-op B32 T2048 H4 d256", 32, 2048, 4, 256, 256, seed=5)
 
 FORWARD_WORKLOADS = (FWD_TINY, FWD_400M, FWD_1P4B, FWD_LONG)
 

@@ -67,19 +67,22 @@ typedef enum {
 } cyfa_dtype;
 
 typedef enum {
-    CYFA_KERNEL_AUTO = 0,  /* BF16 with d_k = d_v = 128: matrix-core kernel;
-                              anything else: the vector-ALU kernel            */
+    CYFA_KERNEL_AUTO = 0,  /* BF16 with d_k = d_v = 128 or d_k = d_v = 256 and
+                              m <= 127: matrix-core kernel; anything else: the
+                              vector-ALU kernel                               */
     CYFA_KERNEL_VALU = 1,  /* vector-ALU chunk kernel, fp32 arithmetic, any
                               supported shape and dtype                        */
     CYFA_KERNEL_MFMA = 2   /* matrix-core (bf16 MFMA) chunk kernel: BF16,
-                              d_k = d_v = 128, chunk 32 or 64                   */
+                              d_k = d_v = 128 or d_k = d_v = 256, m <= 127,
+                              chunk 32 or 64                                   */
 } cyfa_kernel;
 
 /*
  * Forward problem descriptor.
  *   B, T, H      batch, tokens, heads (B, H >= 1; T >= 0; T = 0 is a no-op that
  *                still writes the final state and clock when requested)
- *   d_k, d_v     head dims: 64, 128 or 256 each (the matrix-core kernel: 128 only)
+ *   d_k, d_v     head dims: 64, 128 or 256 each (the matrix-core kernel: both
+ *                128 or both 256)
  *   m            active slots, odd, 3..255 (see above for m > 127)
  *   chunk        chunk length C: 0 selects the kernel's default.  VALU kernel:
  *                8 or 16 (default 16); MFMA kernel: 32 or 64, evaluated in
@@ -89,7 +92,9 @@ typedef enum {
  *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
  *                than one only for d_k, d_v <= 128 and m <= 127).  The state
  *                entering a segment is obtained from a pre-pass over the earlier
- *                segments.  Results do not depend on it beyond rounding.
+ *                segments; the matrix-core kernel at d_k = d_v = 256 always runs
+ *                one segment per sequence.  Results do not depend on it beyond
+ *                rounding.
  *   scale        logit scale (the paper leaves the dot-product scaling out of
  *                its notation, Sec. 3.1 footnote); multiplies R K_t q_t
  *   dtype        storage type of q, k, v and o

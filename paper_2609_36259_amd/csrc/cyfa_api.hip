@@ -97,12 +97,13 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     if (d->kernel == CYFA_KERNEL_MFMA) {
         if (!mfma_ok)
             return fail(CYFA_ERR_UNSUPPORTED,
-                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128, m <= 127 and chunk 32 or 64");
+                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 or d_k=d_v=256, m <= 127 and "
+                        "chunk 32 or 64");
         use_mfma = true;
     } else if (d->kernel == CYFA_KERNEL_VALU) {
         use_mfma = false;
     } else {
-        use_mfma = mfma_ok;          // chunk 0, 32 or 64 with bf16 and d = 128
+        use_mfma = mfma_ok;          // chunk 0, 32 or 64 with bf16 and d = 128 or 256
     }
     plan->mfma = use_mfma;
     size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
@@ -110,6 +111,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
         probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
+        if (d->d_k == 256) plan->segments = 1;       // one segment per sequence at d = 256
         const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
         if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
         if (plan->segments < 1) plan->segments = 1;

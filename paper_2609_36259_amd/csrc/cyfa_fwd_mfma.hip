@@ -961,8 +961,15 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
 // 64-token evaluation.
 constexpr int kMfmaChunk = 32;
 
+// Head dimension 256 (both d_k and d_v) runs on an eight-wave variant of the fused
+// kernel, one segment per sequence (cyfa_fwd_mfma256.hip).
+size_t mfma256_workspace_bytes(const FwdParams &p);
+hipError_t launch_fwd_mfma256(const FwdParams &p, void *ws, hipStream_t st, hipEvent_t ev_start,
+                              hipEvent_t ev_stop);
+
 bool mfma_supported(const FwdParams &p) {
-    return p.dtype == 1 && p.dk == 128 && p.dv == 128 && (p.chunk == 32 || p.chunk == 64);
+    const bool dims = (p.dk == 128 && p.dv == 128) || (p.dk == 256 && p.dv == 256);
+    return p.dtype == 1 && dims && (p.chunk == 32 || p.chunk == 64);
 }
 
 int mfma_default_chunk() { return kMfmaChunk; }
@@ -1042,11 +1049,13 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
 }  // namespace
 
 size_t mfma_workspace_bytes(const FwdParams &p, int segments) {
+    if (p.dk == 256) return mfma256_workspace_bytes(p);
     // bytes beyond the float readout block the host API reserves first
     return ws_layout(p, segments).total - (readout_f32_bytes(p.H) + 255) / 256 * 256;
 }
 
 int mfma_auto_segments(const FwdParams &p) {
+    if (p.dk == 256) return 1;
     // two workgroups are resident per compute unit: split sequences until B*H*P
     // fills the 256 compute units twice
     const int C = kMfmaChunk;
@@ -1060,6 +1069,7 @@ int mfma_auto_segments(const FwdParams &p) {
 
 hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop) {
+    if (p.dk == 256) return launch_fwd_mfma256(p, ws, st, ev_start, ev_stop);
     char *base = static_cast<char *>(ws);
     const WsLayout L = ws_layout(p, P);
     const int C = kMfmaChunk;

@@ -82,6 +82,27 @@ def test_status_codes():
     assert lib.cyfa_forward_workspace_size(None, ctypes.byref(n)) == 1
 
 
+def test_matrix_core_head_dims():
+    """bf16 with d_k = d_v = 128 or 256 (m <= 127) selects the matrix-core kernel;
+    mixed head dims, m > 127 or fp32 inputs do not, and asking for it there fails
+    with CYFA_ERR_UNSUPPORTED.  At 256 it runs one segment per sequence, so the
+    requested segment count does not change the workspace."""
+    lib = cyfa.load()
+    n = ctypes.c_size_t(0)
+    assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 256, 256, dtype=cyfa.BF16)) == "mfma"
+    assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 128, 128, dtype=cyfa.BF16)) == "mfma"
+    assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 256, 128, dtype=cyfa.BF16)) == "valu"
+    assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 256, 256, dtype=cyfa.F32)) == "valu"
+    assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 256, 256, m=255, dtype=cyfa.BF16)) == "valu"
+    for dk, dv, m, dt in ((256, 128, 127, cyfa.BF16), (128, 256, 127, cyfa.BF16),
+                          (256, 256, 255, cyfa.BF16), (256, 256, 127, cyfa.F32), (64, 64, 127, cyfa.BF16)):
+        d = cyfa.forward_desc(1, 64, 2, dk, dv, m=m, dtype=dt, kernel=cyfa.KERNEL_MFMA)
+        assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2, (dk, dv, m, dt)
+    sizes = {_ws(cyfa.forward_desc(4, 4096, 4, 256, 256, segments=s, kernel=cyfa.KERNEL_MFMA))
+             for s in (0, 1, 7, 64)}
+    assert len(sizes) == 1
+
+
 def _call_forward(desc, ptrs, ws=0, ws_bytes=0):
     lib = cyfa.load()
     args = [ptrs.get(k) for k in ("q", "k", "v", "delta", "log_alpha", "beta", "R", "K0", "V0",

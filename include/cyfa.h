@@ -92,9 +92,7 @@ typedef enum {
  *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
  *                than one only for d_k, d_v <= 128 and m <= 127).  The state
  *                entering a segment is obtained from a pre-pass over the earlier
- *                segments; the matrix-core kernel at d_k = d_v = 256 always runs
- *                one segment per sequence.  Results do not depend on it beyond
- *                rounding.
+ *                segments.  Results do not depend on it beyond rounding.
  *   scale        logit scale (the paper leaves the dot-product scaling out of
  *                its notation, Sec. 3.1 footnote); multiplies R K_t q_t
  *   dtype        storage type of q, k, v and o

@@ -111,7 +111,6 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
         probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
-        if (d->d_k == 256) plan->segments = 1;       // one segment per sequence at d = 256
         const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
         if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
         if (plan->segments < 1) plan->segments = 1;

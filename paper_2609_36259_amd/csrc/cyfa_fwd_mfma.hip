@@ -145,41 +145,6 @@ __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4
         }
 }
 
-// Segment-boundary states travel in bf16 (the precision in which the chunk
-// products consume them); the carried states themselves accumulate in fp32.
-// Lane-major dump layout: two 16-byte loads per accumulator.
-__device__ __forceinline__ void load_state(const __bf16 *st, int w, int lane, f32x16 (&kacc)[4],
-                                           f32x16 (&vacc)[4]) {
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 0));
-        const bf16x8 k1 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 8));
-        const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 0));
-        const bf16x8 v1 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 8));
-#pragma unroll
-        for (int v = 0; v < 8; ++v) {
-            kacc[x][v] = (float)k0[v];
-            kacc[x][v + 8] = (float)k1[v];
-            vacc[x][v] = (float)v0[v];
-            vacc[x][v + 8] = (float)v1[v];
-        }
-    }
-}
-
-// fp32 dump (the final state), four 16-byte stores per accumulator
-__device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32x16 (&kacc)[4],
-                                           const f32x16 (&vacc)[4]) {
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            *reinterpret_cast<float4 *>(st + dump_off(w, x, lane, 4 * q)) =
-                make_float4(kacc[x][4 * q], kacc[x][4 * q + 1], kacc[x][4 * q + 2], kacc[x][4 * q + 3]);
-            *reinterpret_cast<float4 *>(st + 128 * 128 + dump_off(w, x, lane, 4 * q)) =
-                make_float4(vacc[x][4 * q], vacc[x][4 * q + 1], vacc[x][4 * q + 2], vacc[x][4 * q + 3]);
-        }
-}
-
 // ---- 1. per-segment state contributions -------------------------------------
 // DeltaS_p = sum_t exp(G_end - G_t) a_t [k_t | v_t]^T over the segment's tokens,
 // with a_t = beta_t U(-lambda_t) b the temporal write (Eq. app-temporal-writes),
@@ -205,14 +170,16 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     static_assert(SCB + 4 * 64 * 8 + 4 * 8 >= prep_lds_bytes(kPrepRows), "readout-matrix blocks fit");
     const FwdParams &p = a.p;
     const int Pm1 = a.P - 1;
+    const int Hv = p.H * a.hv;                         // (virtual) heads of 128 channels
     const int bh = blockIdx.x / Pm1, seg = blockIdx.x % Pm1;
-    const int b = bh / p.H, h = bh % p.H;
+    const int b = bh / Hv, hv = bh % Hv;               // k, v column block hv
+    const int h = hv / a.hv;                           // head of the per-token scalars
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5, l32 = lane & 31;
     const int m = p.m;
     const double inv_m = 1.0 / (double)m;
     {
         // blocks past the segments form 32 rows of the bf16 readout matrix each
-        const int nseg = p.B * p.H * Pm1;
+        const int nseg = p.B * Hv * Pm1;
         if ((int)blockIdx.x >= nseg) {
             const int q = (int)blockIdx.x - nseg;
             readout_prep_rows<kPrepRows>(m, p.R, nullptr, const_cast<__bf16 *>(a.Mz), mz_scale,
@@ -245,7 +212,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
 
     // K, V pieces: rows tid/16 + RPP it, 16-byte column block tid%16; scalars of
     // token `lane` of the chunk on every wave
-    const size_t row_el = (size_t)p.H * D;
+    const size_t row_el = (size_t)Hv * D;
     const unsigned loff = (unsigned)(((tid >> 4) * (int)row_el + (tid & 15) * 8) * 2);
     const unsigned pass = (unsigned)(RPP * row_el * 2);
     const int kvo = 2 * swz_elem(tid >> 4, (tid & 15) * 8);
@@ -253,7 +220,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     float dl, g, be;
     auto load = [&](int c) {
         const int t0 = c * CC;
-        const size_t base = ((seq_row0(p, b) + t0) * row_el + (size_t)h * D) * 2;
+        const size_t base = ((seq_row0(p, b) + t0) * row_el + (size_t)hv * D) * 2;
         const char *kb = reinterpret_cast<const char *>(p.k) + base;
         const char *vb = reinterpret_cast<const char *>(p.v) + base;
 #pragma unroll
@@ -416,11 +383,14 @@ __device__ __forceinline__ void rotate_pair(double u, int j, float &x0, float &x
 // Thread = four rotation pairs moved with two 8-byte (4 x bf16) accesses per
 // segment (see pair_ref): key state, four registers of each partner lane;
 // value state, eight consecutive registers of one lane.  Blocks (bh, y < 16)
-// of 256 threads: 2048 key and 2048 value threads per (b, h).
-constexpr int kScanBlocks = 4096 / NT;                   // blocks per (b, h)
+// of 256 threads: 2048 key and 2048 value threads per (virtual) head bh.
+constexpr int kScanBlocks = 4096 / NT;                   // blocks per (virtual) head
 __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, int tid) {
     const int qi = y * NT + tid;                         // 0 .. 4095
     const int m = a.p.m;
+    // ABI state [B][H][128][128 hv]: column block bh mod hv of head bh / hv
+    const int dabi = 128 * a.hv;
+    const size_t sbase = (size_t)(bh / a.hv) * 128 * dabi + 128 * (bh % a.hv);
     const bool value = qi >= 2048;
     PairRef pr[4];
 #pragma unroll
@@ -436,15 +406,15 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
         rot[k] = pr[k].i0 < kDC && jf[k] <= (m - 1) / 2;
     }
     const float *init = value ? a.p.V0 : a.p.K0;
-    const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
+    const double c0 = a.p.clock0 ? a.p.clock0[bh / a.hv] : 0.0;
     float x0[4] = {0.f, 0.f, 0.f, 0.f}, x1[4] = {0.f, 0.f, 0.f, 0.f};
     if (init) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int p0 = internal_to_paper(pr[k].i0, m), p1 = internal_to_paper(pr[k].i0 + 1, m);
-            const size_t base = (size_t)bh * 128 * 128 + pr[k].col;
-            x0[k] = p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
-            x1[k] = p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
+            const size_t base = sbase + pr[k].col;
+            x0[k] = p0 >= 0 ? init[base + (size_t)p0 * dabi] : 0.f;
+            x1[k] = p1 >= 0 ? init[base + (size_t)p1 * dabi] : 0.f;
         }
     }
     {
@@ -914,7 +884,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 // ---- 4. final state in the ABI layout ------------------------------------------
 // grid (B*H, 32): thread = one rotation pair of the key or value state.
 __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
-    const int bh = blockIdx.x;
+    const int bh = blockIdx.x;                           // (virtual) head
     const int gidx = blockIdx.y * NT + threadIdx.x;
     const int m = a.p.m;
     const PairRef pr = pair_ref(gidx);
@@ -922,7 +892,9 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     const size_t slot = (size_t)bh * a.P + (a.P - 1);
     const float *st = a.fin_state + (size_t)bh * kStateFloats;
     const double origin = a.seg_origin[slot];
-    const size_t base = (size_t)bh * 128 * 128 + pr.col;
+    // ABI state [B][H][128][128 hv]: column block bh mod hv of head bh / hv
+    const int dabi = 128 * a.hv;
+    const size_t base = (size_t)(bh / a.hv) * 128 * dabi + 128 * (bh % a.hv) + pr.col;
     const int p0 = internal_to_paper(pr.i0, m), p1 = internal_to_paper(pr.i0 + 1, m);
     float x0, x1;
     if (a.nchunks > 0) {
@@ -933,21 +905,21 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
     } else {
         // no tokens: the final state is the initial state (zero when none is given)
         const float *init = pr.value ? a.p.V0 : a.p.K0;
-        x0 = init && p0 >= 0 ? init[base + (size_t)p0 * 128] : 0.f;
-        x1 = init && p1 >= 0 ? init[base + (size_t)p1 * 128] : 0.f;
+        x0 = init && p0 >= 0 ? init[base + (size_t)p0 * dabi] : 0.f;
+        x1 = init && p1 >= 0 ? init[base + (size_t)p1 * dabi] : 0.f;
     }
     float *out = pr.value ? a.p.V_out : a.p.K_out;
     if (out) {
-        if (p0 >= 0) out[base + (size_t)p0 * 128] = x0;
-        if (p1 >= 0) out[base + (size_t)p1 * 128] = x1;
+        if (p0 >= 0) out[base + (size_t)p0 * dabi] = x0;
+        if (p1 >= 0) out[base + (size_t)p1 * dabi] = x1;
         // padding rows m..127 of the ABI layout are written as zero (one writer per row)
         const int ip = pr.i0 >> 1;
-        for (int row = m + ip; row < 128; row += 64) out[base + (size_t)row * 128] = 0.f;
+        for (int row = m + ip; row < 128; row += 64) out[base + (size_t)row * dabi] = 0.f;
     }
-    if (gidx == 0 && a.p.clock_out) {
+    if (gidx == 0 && bh % a.hv == 0 && a.p.clock_out) {
         // with no tokens the final state is the initial one and the local clock is 0
         const double fl = a.nchunks > 0 ? a.final_lam[bh] : 0.0;
-        a.p.clock_out[bh] = reduce_clock(origin + fl, m);
+        a.p.clock_out[bh / a.hv] = reduce_clock(origin + fl, m);
     }
 }
 
@@ -961,11 +933,10 @@ __global__ __launch_bounds__(NT) void state_out_kernel(MfmaArgs a) {
 // 64-token evaluation.
 constexpr int kMfmaChunk = 32;
 
-// Head dimension 256 (both d_k and d_v) runs on an eight-wave variant of the fused
-// kernel, one segment per sequence (cyfa_fwd_mfma256.hip).
-size_t mfma256_workspace_bytes(const FwdParams &p);
-hipError_t launch_fwd_mfma256(const FwdParams &p, void *ws, hipStream_t st, hipEvent_t ev_start,
-                              hipEvent_t ev_stop);
+// Head dimension 256 (both d_k and d_v): the fused chunk kernel is an eight-wave
+// variant (cyfa_fwd_mfma256.hip); the pre-pass, the segment scan and the
+// final-state conversion run unchanged on 128-channel virtual heads.
+hipError_t launch_chunk256(const MfmaArgs &a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop);
 
 bool mfma_supported(const FwdParams &p) {
     const bool dims = (p.dk == 128 && p.dv == 128) || (p.dk == 256 && p.dv == 256);
@@ -975,20 +946,24 @@ bool mfma_supported(const FwdParams &p) {
 int mfma_default_chunk() { return kMfmaChunk; }
 
 namespace {
+// 128-channel column blocks per head: d = 256 states are two 128 x 128 pairs
+int virtual_heads(const FwdParams &p) { return p.dk == 256 ? 2 : 1; }
+
 struct WsLayout {
     size_t mz, state, fin, span, gsum, origin, flam, total;
 };
 WsLayout ws_layout(const FwdParams &p, int P) {
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
     WsLayout L{};
+    const size_t BHv = (size_t)p.B * p.H * virtual_heads(p);
     size_t off = up(readout_f32_bytes(p.H));
     L.mz = off;
     off += up((size_t)p.H * 128 * 128 * 2);
-    const size_t nseg = (size_t)p.B * p.H * P;
+    const size_t nseg = BHv * P;
     L.state = off;
     off += up(nseg * kStateFloats * 2);
     L.fin = off;
-    off += up((size_t)p.B * p.H * kStateFloats * 4);
+    off += up(BHv * kStateFloats * 4);
     L.span = off;
     off += up(nseg * 8);
     L.gsum = off;
@@ -996,13 +971,14 @@ WsLayout ws_layout(const FwdParams &p, int P) {
     L.origin = off;
     off += up(nseg * 8);
     L.flam = off;
-    off += up((size_t)p.B * p.H * 8);
+    off += up(BHv * 8);
     L.total = off;
     return L;
 }
 
+// BHv: (virtual) heads of the pre-pass and the scan, B H hv
 template <int CC>
-hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_start,
+hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_start,
                      hipEvent_t ev_stop) {
     hipError_t e;
     // the bf16 readout matrix carries the logit scale in log2 units, scale log2(e)
@@ -1014,7 +990,7 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
         // costs) whenever its length is a whole number of them.  Every segment but
         // the last is full, and the last one is not pre-passed.  Extra blocks of
         // the same launch form the bf16 readout matrix, 32 rows each.
-        const int nblk = BH * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows);
+        const int nblk = BHv * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows);
         if (CC == 32 && a.cps % 2 == 0) {
             MfmaArgs a64 = a;
             a64.chunk = 64;
@@ -1027,7 +1003,7 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.has_init) {
-        const int nscan = BH * kScanBlocks;
+        const int nscan = BHv * kScanBlocks;
         const int nprep = prepass ? 0 : a.p.H * (kStoreRows / kPrepRows);
         hipLaunchKernelGGL(scan_prep_kernel, dim3(nscan + nprep), dim3(NT), 0, st, a, nscan, mz_scale);
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1037,8 +1013,11 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
     }
     // Timing events, when given, are taken by the fused kernel's own dispatch: they
     // bracket the kernel alone and add no gap between launches.
-    if (a.nchunks > 0) {
-        hipExtLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BH * a.P), dim3(NT), 0, st, ev_start, ev_stop, 0, a);
+    if (a.nchunks > 0 && a.hv == 2) {
+        if ((e = launch_chunk256(a, st, ev_start, ev_stop)) != hipSuccess) return e;
+    } else if (a.nchunks > 0) {
+        hipExtLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BHv * a.P), dim3(NT), 0, st, ev_start, ev_stop, 0,
+                              a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
@@ -1049,17 +1028,16 @@ hipError_t launch_cc(const MfmaArgs &a, int BH, hipStream_t st, hipEvent_t ev_st
 }  // namespace
 
 size_t mfma_workspace_bytes(const FwdParams &p, int segments) {
-    if (p.dk == 256) return mfma256_workspace_bytes(p);
     // bytes beyond the float readout block the host API reserves first
     return ws_layout(p, segments).total - (readout_f32_bytes(p.H) + 255) / 256 * 256;
 }
 
 int mfma_auto_segments(const FwdParams &p) {
-    if (p.dk == 256) return 1;
-    // two workgroups are resident per compute unit: split sequences until B*H*P
-    // fills the 256 compute units twice
+    // two workgroups of the four-wave kernel are resident per compute unit, one of
+    // the eight-wave kernel (d = 256): split sequences until B*H*P fills the 256
+    // compute units with them
     const int C = kMfmaChunk;
-    const int slots = 256 * 2;
+    const int slots = p.dk == 256 ? 256 : 256 * 2;
     const int seqs = p.B * p.H;
     int P = (slots + seqs - 1) / seqs;
     const int nchunks = (p.T + C - 1) / C;
@@ -1069,7 +1047,6 @@ int mfma_auto_segments(const FwdParams &p) {
 
 hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop) {
-    if (p.dk == 256) return launch_fwd_mfma256(p, ws, st, ev_start, ev_stop);
     char *base = static_cast<char *>(ws);
     const WsLayout L = ws_layout(p, P);
     const int C = kMfmaChunk;
@@ -1091,12 +1068,13 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.want_final = (p.K_out || p.V_out || p.clock_out) ? 1 : 0;
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     a.zero_init = (p.K0 || p.V0) ? 0 : 1;
-    const int BH = p.B * p.H;
+    a.hv = virtual_heads(p);
+    const int BHv = p.B * p.H * a.hv;
 
-    hipError_t e = launch_cc<32>(a, BH, st, ev_start, ev_stop);
+    hipError_t e = launch_cc<32>(a, BHv, st, ev_start, ev_stop);
     if (e != hipSuccess) return e;
     if (a.want_final) {
-        hipLaunchKernelGGL(state_out_kernel, dim3(BH, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
+        hipLaunchKernelGGL(state_out_kernel, dim3(BHv, 2 * 64 * 128 / NT), dim3(NT), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

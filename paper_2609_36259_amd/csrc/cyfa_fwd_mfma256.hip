@@ -4,7 +4,7 @@
 // The same computation as the 128-channel fused kernel (App. B: clock and
 // log-decay prefix sums, temporal writes, key pass Eq. app-cyfa-key-chunk,
 // token-wise softmax readout Eq. cyfa-two-pass (middle line), value pass
-// Eq. app-cyfa-value-chunk), on one eight-wave workgroup per sequence.  Both
+// Eq. app-cyfa-value-chunk), on one eight-wave workgroup per segment.  Both
 // 256 x 128 carried states stay in MFMA accumulators:
 //   wave w = (slot block sb = w mod 4, channel half dh = w div 4) holds
 //     Kbar^T[d in 128 dh .. + 127][slots 32 sb .. + 31]   (4 accumulators), and
@@ -20,12 +20,15 @@
 // Layout in LDS: q, k, v of a chunk as two 128-channel tiles each (low, high);
 // the temporal writes, the (cos, sin) table, the readout matrix, X / W and O''
 // exactly as in the 128-channel kernel (they live in the 128-dim slot / basis
-// space).  One workgroup per compute unit (~118 KB of LDS).
+// space).  One workgroup per compute unit (~118 KB of LDS); a sequence is cut
+// into segments of whole chunks as in the 128-channel path.
 //
-// Carried states across calls: the state entering the sequence (the initial
-// state turned into the chunk kernel's frame and layout) and the final state
-// (back to the ABI layout) are converted by two small kernels; each sequence
-// runs as one segment.
+// Segments: the states of a 256-channel head are two independent 128 x 128
+// pairs (one per 128-channel block of k and v; the clock, the gates and the
+// writes are shared), so the segment pre-pass, the scan of the entering states
+// and the final-state conversion of the 128-channel path run on "virtual heads"
+// of 128 channels, and this kernel reads and writes those heads' pairs.  Wave
+// (sb, dh) holds what wave sb of the 128-channel kernel holds for block dh.
 #include "cyfa_mfma_chunk.h"
 #include "cyfa_prep.h"
 
@@ -40,7 +43,6 @@ namespace {
 constexpr int kNT8 = 512;                              // eight waves
 constexpr int kCC = 32;                                // chunk length
 constexpr int kD2 = 256;                               // head dimension
-constexpr int kState2 = 2 * kD2 * 128;                 // one state pair: K part then V part
 
 struct Lay2 {
     static constexpr int SSC = kCC + 8;                // score tile row stride
@@ -243,23 +245,13 @@ __global__ __launch_bounds__(kNT8, 1) void chunk_forward256_kernel(MfmaArgs a) {
             *reinterpret_cast<uint4 *>(s.Mt + swz_elem(row, c0)) = *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
         }
     }
+    // Wave (sb, dh) holds exactly what wave sb of the 128-channel kernel holds for
+    // the 128-channel block dh of this head: its entering and final states are
+    // that virtual head's pairs (index 2 bh + dh), in the same dump layout.
     f32x16 kacc[4], vacc[4];
-    const __bf16 *slot_state = a.seg_state + ((size_t)bh * a.P + seg) * kState2;
-    if (a.has_init) {
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(slot_state + dump_off(w8, x, lane, 0));
-            const bf16x8 k1 = *reinterpret_cast<const bf16x8 *>(slot_state + dump_off(w8, x, lane, 8));
-            const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(slot_state + kD2 * 128 + dump_off(w8, x, lane, 0));
-            const bf16x8 v1 = *reinterpret_cast<const bf16x8 *>(slot_state + kD2 * 128 + dump_off(w8, x, lane, 8));
-#pragma unroll
-            for (int v = 0; v < 8; ++v) {
-                kacc[x][v] = (float)k0[v];
-                kacc[x][v + 8] = (float)k1[v];
-                vacc[x][v] = (float)v0[v];
-                vacc[x][v + 8] = (float)v1[v];
-            }
-        }
+    const size_t vh = (size_t)bh * 2 + dh;
+    if (a.has_init && !(seg == 0 && a.zero_init)) {
+        load_state(a.seg_state + (vh * a.P + seg) * kStateFloats, sb, lane, kacc, vacc);
     } else {
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
@@ -489,179 +481,21 @@ __global__ __launch_bounds__(kNT8, 1) void chunk_forward256_kernel(MfmaArgs a) {
         const float f = __expf(s.ctl[1]);
         scale4(kacc, f);
         scale4(vacc, f);
-        float *st = a.fin_state + (size_t)bh * kState2;
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<float4 *>(st + dump_off(w8, x, lane, 4 * q)) =
-                    make_float4(kacc[x][4 * q], kacc[x][4 * q + 1], kacc[x][4 * q + 2], kacc[x][4 * q + 3]);
-                *reinterpret_cast<float4 *>(st + kD2 * 128 + dump_off(w8, x, lane, 4 * q)) =
-                    make_float4(vacc[x][4 * q], vacc[x][4 * q + 1], vacc[x][4 * q + 2], vacc[x][4 * q + 3]);
-            }
-        if (tid == 0) a.final_lam[bh] = carry;
+        dump_state(a.fin_state + vh * kStateFloats, sb, lane, kacc, vacc);
+        if (tid == 0) {
+            // the clock runs on wave 0; both virtual heads carry it
+            a.final_lam[2 * bh] = carry;
+            a.final_lam[2 * bh + 1] = carry;
+        }
     }
-}
-
-// ---- state conversion between the ABI layout and the chunk kernel's ---------
-// Element (internal slot i, channel d) of the key state sits with wave
-// (i / 32) + 4 (d / 128), accumulator (d / 32) mod 4, row d mod 32, column i mod
-// 32; of the value state with wave d / 32, accumulator i / 32, row i mod 32,
-// column d mod 32 (D layout of v_mfma_f32_32x32x16: row r of column n is lane
-// n + 32 ((r / 4) mod 2), register 4 (r / 8) + r mod 4).
-__device__ __forceinline__ int acc_pos(int w, int x, int r, int n) {
-    return dump_off(w, x, n + 32 * ((r >> 2) & 1), ((r >> 3) << 2) | (r & 3));
-}
-__device__ __forceinline__ int key_pos(int i, int d) { return acc_pos((i >> 5) + 4 * (d >> 7), (d >> 5) & 3, d & 31, i & 31); }
-__device__ __forceinline__ int val_pos(int i, int d) { return kD2 * 128 + acc_pos(d >> 5, i >> 5, i & 31, d & 31); }
-
-__device__ __forceinline__ void rot_by(double tau, int j, int m, float &x0, float &x1) {
-    // U(tau) on the (cos, sin) pair j: rotation by 2 pi j tau / m
-    double rev = (double)j * reduce_clock(tau, m) / (double)m;
-    rev -= floor(rev);
-    float sn, cs;
-    sincos_rev((float)rev, &sn, &cs);
-    const float y0 = cs * x0 - sn * x1, y1 = sn * x0 + cs * x1;
-    x0 = y0;
-    x1 = y1;
-}
-
-// The state entering the sequence in the chunk kernel's frame (origin at the
-// initial clock, Prop. 6: U(clock0) applied to the initial state) and layout,
-// bf16; grid (B*H, 2*64*256/256): thread = one slot pair of one channel of
-// the key or the value state.
-__global__ __launch_bounds__(256) void init_state256_kernel(MfmaArgs a) {
-    const int bh = blockIdx.x;
-    const int e = blockIdx.y * 256 + threadIdx.x;       // 0 .. 2*64*256-1
-    const bool value = e >= 64 * kD2;
-    const int pair = (e % (64 * kD2)) / kD2, d = e % kD2;
-    const int m = a.p.m;
-    const int i0 = 2 * pair;                            // internal slots i0, i0 + 1
-    const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
-    const float *init = value ? a.p.V0 : a.p.K0;
-    const int p0 = internal_to_paper(i0, m), p1 = internal_to_paper(i0 + 1, m);
-    const size_t base = (size_t)bh * 128 * kD2 + d;
-    float x0 = (init && p0 >= 0) ? init[base + (size_t)p0 * kD2] : 0.f;
-    float x1 = (init && p1 >= 0) ? init[base + (size_t)p1 * kD2] : 0.f;
-    const int j = pair + 1;
-    if (i0 < kDC && j <= (m - 1) / 2) rot_by(c0, j, m, x0, x1);
-    __bf16 *st = a.seg_state + (size_t)bh * a.P * kState2;
-    st[value ? val_pos(i0, d) : key_pos(i0, d)] = (__bf16)x0;
-    st[value ? val_pos(i0 + 1, d) : key_pos(i0 + 1, d)] = (__bf16)x1;
-}
-
-// Final state back to the absolute clock (U(-origin)) and the ABI layout, and the
-// final clock; with no tokens, the initial state and clock.
-__global__ __launch_bounds__(256) void state_out256_kernel(MfmaArgs a) {
-    const int bh = blockIdx.x;
-    const int e = blockIdx.y * 256 + threadIdx.x;
-    const bool value = e >= 64 * kD2;
-    const int pair = (e % (64 * kD2)) / kD2, d = e % kD2;
-    const int m = a.p.m;
-    const int i0 = 2 * pair;
-    const int p0 = internal_to_paper(i0, m), p1 = internal_to_paper(i0 + 1, m);
-    const size_t base = (size_t)bh * 128 * kD2 + d;
-    const double c0 = a.p.clock0 ? a.p.clock0[bh] : 0.0;
-    const double origin = reduce_clock(c0, m);
-    float x0, x1;
-    if (a.nchunks > 0) {
-        const float *st = a.fin_state + (size_t)bh * kState2;
-        x0 = st[value ? val_pos(i0, d) : key_pos(i0, d)];
-        x1 = st[value ? val_pos(i0 + 1, d) : key_pos(i0 + 1, d)];
-        const int j = pair + 1;
-        if (i0 < kDC && j <= (m - 1) / 2) rot_by(-origin, j, m, x0, x1);
-    } else {
-        const float *init = value ? a.p.V0 : a.p.K0;
-        x0 = (init && p0 >= 0) ? init[base + (size_t)p0 * kD2] : 0.f;
-        x1 = (init && p1 >= 0) ? init[base + (size_t)p1 * kD2] : 0.f;
-    }
-    float *out = value ? a.p.V_out : a.p.K_out;
-    if (out) {
-        if (p0 >= 0) out[base + (size_t)p0 * kD2] = x0;
-        if (p1 >= 0) out[base + (size_t)p1 * kD2] = x1;
-        // padding rows m .. 127 (one writer per row)
-        for (int row = m + pair; row < 128; row += 64) out[base + (size_t)row * kD2] = 0.f;
-    }
-    if (e == 0 && a.p.clock_out) {
-        const double fl = a.nchunks > 0 ? a.final_lam[bh] : 0.0;
-        a.p.clock_out[bh] = reduce_clock(origin + fl, m);
-    }
-}
-
-struct Ws2 {
-    size_t mz, state, fin, span, gsum, origin, flam, total;
-};
-Ws2 ws2_layout(const FwdParams &p) {
-    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
-    const size_t BH = (size_t)p.B * p.H;
-    Ws2 L{};
-    size_t off = up(readout_f32_bytes(p.H));            // the host API's float readout block comes first
-    L.mz = off;
-    off += up((size_t)p.H * 128 * 128 * 2);
-    L.state = off;
-    off += up(BH * kState2 * 2);
-    L.fin = off;
-    off += up(BH * kState2 * 4);
-    L.span = off;
-    off += up(BH * 8);
-    L.gsum = off;
-    off += up(BH * 8);
-    L.origin = off;
-    off += up(BH * 8);
-    L.flam = off;
-    off += up(BH * 8);
-    L.total = off;
-    return L;
 }
 
 }  // namespace
 
-size_t mfma256_workspace_bytes(const FwdParams &p) {
-    return ws2_layout(p).total - (readout_f32_bytes(p.H) + 255) / 256 * 256;
-}
-
-hipError_t launch_fwd_mfma256(const FwdParams &p, void *ws, hipStream_t st, hipEvent_t ev_start,
-                              hipEvent_t ev_stop) {
-    char *base = static_cast<char *>(ws);
-    const Ws2 L = ws2_layout(p);
-    MfmaArgs a{};
-    a.p = p;
-    a.chunk = kCC;
-    a.nchunks = (p.T + kCC - 1) / kCC;
-    a.P = 1;
-    a.cps = a.nchunks;
-    a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
-    a.seg_state = reinterpret_cast<__bf16 *>(base + L.state);
-    a.fin_state = reinterpret_cast<float *>(base + L.fin);
-    a.seg_span = reinterpret_cast<double *>(base + L.span);
-    a.seg_gsum = reinterpret_cast<double *>(base + L.gsum);
-    a.seg_origin = reinterpret_cast<double *>(base + L.origin);
-    a.final_lam = reinterpret_cast<double *>(base + L.flam);
-    a.want_final = (p.K_out || p.V_out || p.clock_out) ? 1 : 0;
-    a.has_init = (p.K0 || p.V0) ? 1 : 0;
-    a.zero_init = (p.K0 || p.V0) ? 0 : 1;
-    const int BH = p.B * p.H;
-    hipError_t e;
-    if ((e = launch_readout_prep(p.H, p.m, p.R, nullptr, const_cast<__bf16 *>(a.Mz), p.scale * 1.4426950408889634f,
-                                 st)) != hipSuccess)
-        return e;
-    const dim3 conv_grid(BH, 2 * 64 * kD2 / 256);
-    if (a.has_init) {
-        hipLaunchKernelGGL(init_state256_kernel, conv_grid, dim3(256), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (a.nchunks > 0) {
-        hipExtLaunchKernelGGL(chunk_forward256_kernel, dim3(BH), dim3(kNT8), 0, st, ev_start, ev_stop, 0, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    } else {
-        if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
-        if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
-    }
-    if (a.want_final) {
-        hipLaunchKernelGGL(state_out256_kernel, conv_grid, dim3(256), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    return hipSuccess;
+hipError_t launch_chunk256(const MfmaArgs &a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+    hipExtLaunchKernelGGL(chunk_forward256_kernel, dim3(a.p.B * a.p.H * a.P), dim3(kNT8), 0, st, ev_start,
+                          ev_stop, 0, a);
+    return hipGetLastError();
 }
 
 }  // namespace cyfa

@@ -25,6 +25,11 @@ struct MfmaArgs {
     int zero_init;       // no initial state: the first segment starts from zero (its entry
                          // state is neither written by the scan nor read)
     int want_final;      // last segment dumps its final state into fin_state
+    int hv;              // 128-channel column blocks per head (1: d = 128, 2: d = 256).  The
+                         // pre-pass, the segment scan and the final-state conversion treat
+                         // each block as a head of its own (a "virtual head", index
+                         // hv h + block): the states of a 256-channel head are two 128 x 128
+                         // pairs, and the per-token scalars are shared by its blocks.
 };
 
 
@@ -59,6 +64,42 @@ __device__ __forceinline__ void scalars_at(Tiles &t, char *base, int n = 64) {
     t.bw = reinterpret_cast<float4 *>(t.ctl + 4);      // 16-byte aligned for n a multiple of 4
 }
 __host__ __device__ constexpr int scalar_bytes(int n) { return n * (4 + 4 + 4 + 4 + 4 + 16) + 16; }
+
+// Segment-boundary states travel in bf16 (the precision in which the chunk
+// products consume them); the carried states themselves accumulate in fp32.
+// Lane-major dump layout, one (virtual) head's pair per kStateFloats block: two
+// 16-byte loads per accumulator.
+__device__ __forceinline__ void load_state(const __bf16 *st, int w, int lane, f32x16 (&kacc)[4],
+                                           f32x16 (&vacc)[4]) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 0));
+        const bf16x8 k1 = *reinterpret_cast<const bf16x8 *>(st + dump_off(w, x, lane, 8));
+        const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 0));
+        const bf16x8 v1 = *reinterpret_cast<const bf16x8 *>(st + 128 * 128 + dump_off(w, x, lane, 8));
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+            kacc[x][v] = (float)k0[v];
+            kacc[x][v + 8] = (float)k1[v];
+            vacc[x][v] = (float)v0[v];
+            vacc[x][v + 8] = (float)v1[v];
+        }
+    }
+}
+
+// fp32 dump (the final state), four 16-byte stores per accumulator
+__device__ __forceinline__ void dump_state(float *st, int w, int lane, const f32x16 (&kacc)[4],
+                                           const f32x16 (&vacc)[4]) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            *reinterpret_cast<float4 *>(st + dump_off(w, x, lane, 4 * q)) =
+                make_float4(kacc[x][4 * q], kacc[x][4 * q + 1], kacc[x][4 * q + 2], kacc[x][4 * q + 3]);
+            *reinterpret_cast<float4 *>(st + 128 * 128 + dump_off(w, x, lane, 4 * q)) =
+                make_float4(vacc[x][4 * q], vacc[x][4 * q + 1], vacc[x][4 * q + 2], vacc[x][4 * q + 3]);
+        }
+}
 
 // Global -> register prefetch of one chunk: CC NTH/16 x 16-byte pieces per thread
 // per tensor (rows (NTH/16) it + tid / 16, columns 8 (tid % 16)), plus one

@@ -85,8 +85,8 @@ def test_status_codes():
 def test_matrix_core_head_dims():
     """bf16 with d_k = d_v = 128 or 256 (m <= 127) selects the matrix-core kernel;
     mixed head dims, m > 127 or fp32 inputs do not, and asking for it there fails
-    with CYFA_ERR_UNSUPPORTED.  At 256 it runs one segment per sequence, so the
-    requested segment count does not change the workspace."""
+    with CYFA_ERR_UNSUPPORTED.  At 256 the workspace holds two 128 x 128 state
+    pairs per head and segment."""
     lib = cyfa.load()
     n = ctypes.c_size_t(0)
     assert cyfa.selected_kernel(cyfa.forward_desc(2, 100, 2, 256, 256, dtype=cyfa.BF16)) == "mfma"
@@ -98,9 +98,12 @@ def test_matrix_core_head_dims():
                           (256, 256, 255, cyfa.BF16), (256, 256, 127, cyfa.F32), (64, 64, 127, cyfa.BF16)):
         d = cyfa.forward_desc(1, 64, 2, dk, dv, m=m, dtype=dt, kernel=cyfa.KERNEL_MFMA)
         assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2, (dk, dv, m, dt)
-    sizes = {_ws(cyfa.forward_desc(4, 4096, 4, 256, 256, segments=s, kernel=cyfa.KERNEL_MFMA))
-             for s in (0, 1, 7, 64)}
-    assert len(sizes) == 1
+    w1 = _ws(cyfa.forward_desc(4, 4096, 4, 256, 256, segments=1, kernel=cyfa.KERNEL_MFMA))
+    w8 = _ws(cyfa.forward_desc(4, 4096, 4, 256, 256, segments=8, kernel=cyfa.KERNEL_MFMA))
+    # bf16 entering states: 2 pairs x 2 x 128 x 128 x 2 bytes per head and extra segment
+    assert w8 - w1 >= 7 * 16 * 2 * 2 * 128 * 128 * 2
+    h1 = _ws(cyfa.forward_desc(4, 4096, 4, 128, 128, segments=8, kernel=cyfa.KERNEL_MFMA))
+    assert w8 > h1
 
 
 def _call_forward(desc, ptrs, ws=0, ws_bytes=0):

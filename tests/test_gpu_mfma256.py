@@ -2,7 +2,8 @@
 256, the paper's head size) against the oracle.
 
 Small cases compare every output element, slot logit, final state and clock
-with the oracle over several 32-token chunks and a ragged tail; the paper's
+with the oracle over several 32-token chunks and a ragged tail, with sequences
+cut into one or several segments; the paper's
 operator shape (B 32, T 2048, H 4, d 256) runs in the benchmark's launch
 configuration and is compared on sampled (b, h) sequences over all tokens.
 Bar: max relative error 2e-2 (bf16 inputs, fp32 accumulation), clocks 1e-9.
@@ -94,10 +95,42 @@ def test_small_full_parity(chunk):
 def test_chunk_64_is_two_chunks_of_32():
     x = make_forward_inputs(1, 64 * 3 + 9, 2, D, D, seed=72, dtype="bf16")
     t = upload(x)
-    a = _fwd(x, t, chunk=32, return_state=True)
-    b = _fwd(x, t, chunk=64, segments=5, return_state=True)      # segments: one per sequence at d = 256
+    for sgm in (1, 3):
+        a = _fwd(x, t, chunk=32, segments=sgm, return_state=True)
+        b = _fwd(x, t, chunk=64, segments=sgm, return_state=True)
+        torch.cuda.synchronize()
+        assert torch.equal(a["o"], b["o"]) and torch.equal(a["K"], b["K"]) and torch.equal(a["V"], b["V"])
+
+
+@pytest.mark.parametrize("segments", [1, 2, 3, 7])
+@pytest.mark.parametrize("with_init", [False, True])
+def test_segments_against_oracle(segments, with_init):
+    """Sequences cut into segments: the pre-pass and the scan of the entering
+    states run on the two 128-channel blocks of each head; every output, logit,
+    final state and clock against the oracle, with and without an initial state."""
+    m = 127
+    x = make_forward_inputs(2, 32 * 9 + 13, 2, D, D, seed=87, dtype="bf16", m=m)
+    t = upload(x)
+    if with_init:
+        K0, V0, c0 = _init_states(2, 2, m, 88)
+        res = _fwd(x, t, segments=segments, K0=K0, V0=V0, clock0=c0, return_state=True, return_logits=True)
+        _assert_ok(_errors(x, res, **_oracle_init(m, K0, V0, c0)))
+    else:
+        res = _fwd(x, t, segments=segments, return_state=True, return_logits=True)
+        _assert_ok(_errors(x, res))
+
+
+def test_segment_count_changes_only_rounding():
+    x = make_forward_inputs(1, 32 * 11 + 5, 2, D, D, seed=89, dtype="bf16")
+    t = upload(x)
+    outs = [_fwd(x, t, segments=sgm, return_state=True) for sgm in (1, 2, 5, 12)]
     torch.cuda.synchronize()
-    assert torch.equal(a["o"], b["o"]) and torch.equal(a["K"], b["K"]) and torch.equal(a["V"], b["V"])
+    base = outs[0]["o"].float().cpu().numpy()
+    for r in outs[1:]:
+        assert rel_err(r["o"].float().cpu().numpy(), base) <= 1e-2
+        assert rel_err(r["K"].cpu().numpy(), outs[0]["K"].cpu().numpy()) <= 1e-2
+        assert rel_err(r["V"].cpu().numpy(), outs[0]["V"].cpu().numpy()) <= 1e-2
+        assert clock_err(r["clock"].cpu().numpy(), outs[0]["clock"].cpu().numpy(), 127) <= 1e-9
 
 
 @pytest.mark.parametrize("variant", ["no_beta_no_R", "small_m", "m63", "short", "one_token"])
@@ -127,12 +160,13 @@ def test_extreme_and_mixed_gates():
     g[:, 200:330] = 0.0
     g[:, 400:410] = -40.0
     t = upload(x)
-    res = _fwd(x, t, return_state=True, return_logits=True)
-    _assert_ok(_errors(x, res))
+    for sgm in (1, 3):
+        res = _fwd(x, t, segments=sgm, return_state=True, return_logits=True)
+        _assert_ok(_errors(x, res))
     y = make_forward_inputs(1, 300, 2, D, D, seed=75, dtype="bf16")
     y["log_alpha"] = None
     y["beta"] = None
-    res = _fwd(y, upload(y), return_state=True)
+    res = _fwd(y, upload(y), segments=2, return_state=True)
     _assert_ok(_errors(y, res))
 
 
@@ -143,7 +177,7 @@ def test_eager_rescale_paths(gate):
     tiles."""
     x = make_forward_inputs(1, 431, 2, D, D, seed=76, dtype="bf16")
     x["log_alpha"][:, 40:360] = gate
-    res = _fwd(x, upload(x), return_state=True, return_logits=True)
+    res = _fwd(x, upload(x), segments=2, return_state=True, return_logits=True)
     _assert_ok(_errors(x, res))
 
 
@@ -176,22 +210,25 @@ def test_resume_matches_one_call():
     _assert_ok(_errors(x, full))
 
 
-def test_resume_in_place():
-    """Final state and clock written over the initial ones."""
+@pytest.mark.parametrize("segments", [1, 3])
+def test_resume_in_place(segments):
+    """Final state and clock written over the initial ones; with several segments
+    every workgroup must have read its entering clock and state before any writes
+    them."""
     cyfa = _cyfa()
     x = make_forward_inputs(2, 300, 2, D, D, seed=80, dtype="bf16")
     t = upload(x)
     t1 = 137
     a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
     b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
-    first = _fwd(x, a, return_state=True)
+    first = _fwd(x, a, return_state=True, segments=segments)
     K, V, clk = first["K"], first["V"], first["clock"]
     ref = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
                        scale=x["scale"], K0=K.clone(), V0=V.clone(), clock0=clk.clone(),
-                       return_state=True, kernel=cyfa.KERNEL_MFMA)
+                       return_state=True, kernel=cyfa.KERNEL_MFMA, segments=segments)
     got = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
                        scale=x["scale"], K0=K, V0=V, clock0=clk, K_out=K, V_out=V, clock_out=clk,
-                       kernel=cyfa.KERNEL_MFMA)
+                       kernel=cyfa.KERNEL_MFMA, segments=segments)
     torch.cuda.synchronize()
     assert torch.equal(got["o"], ref["o"])
     assert torch.equal(K, ref["K"]) and torch.equal(V, ref["V"])
@@ -213,8 +250,9 @@ def test_empty_sequence():
     np.testing.assert_allclose(res["clock"].cpu().numpy(), [[5.25, 3.5]], atol=1e-9)
 
 
+@pytest.mark.parametrize("segments", [1, 3])
 @pytest.mark.parametrize("with_init", [False, True])
-def test_ragged_lengths_and_packed(with_init):
+def test_ragged_lengths_and_packed(with_init, segments):
     """Per-sequence lengths (empty, one token, partial and whole chunks) through
     cyfa_forward_lens, each sequence against the oracle on its own tokens, and the
     same sequences packed (cyfa_forward_varlen), bit-identical."""
@@ -226,13 +264,14 @@ def test_ragged_lengths_and_packed(with_init):
     lens = torch.tensor(lens_l, dtype=torch.int32, device="cuda")
     init = _init_states(B, H, m, 83) if with_init else (None, None, None)
     pad = _fwd(x, t, lens=lens, K0=init[0], V0=init[1], clock0=init[2], return_state=True,
-               return_logits=True)
+               return_logits=True, segments=segments)
     tp = {k: (torch.cat([a[b, :n] for b, n in enumerate(lens_l)], 0).contiguous()
               if a is not None and k != "R" else a) for k, a in t.items()}
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens_l)]), dtype=torch.int32, device="cuda")
     pk = cyfa.forward_varlen(tp["q"], tp["k"], tp["v"], tp["delta"], cu, tp["log_alpha"], tp["beta"],
                              t["R"], max_len=T, scale=x["scale"], kernel=cyfa.KERNEL_MFMA, K0=init[0],
-                             V0=init[1], clock0=init[2], return_state=True, return_logits=True)
+                             V0=init[1], clock0=init[2], return_state=True, return_logits=True,
+                             segments=segments)
     torch.cuda.synchronize()
     assert torch.equal(pk["o"], torch.cat([pad["o"][b, :n] for b, n in enumerate(lens_l)], 0))
     assert torch.equal(pk["logits"], torch.cat([pad["logits"][b, :n] for b, n in enumerate(lens_l)], 0))
@@ -250,6 +289,7 @@ def test_ragged_lengths_and_packed(with_init):
         ref = oracle.forward(xs["q"], xs["k"], xs["v"], xs["delta"], xs["log_alpha"], xs["beta"], x["R"],
                              m=m, scale=x["scale"], T_run=n, **kw)
         if n > 0:
+            print("sequence", b, "tokens", n, "o error", f"{rel_err(o_all[b, :n].transpose(1, 0, 2), ref['o']):.2e}")
             worst["o"] = max(worst.get("o", 0), rel_err(o_all[b, :n].transpose(1, 0, 2), ref["o"]))
             worst["z"] = max(worst.get("z", 0), rel_err(z_all[b, :n].transpose(1, 0, 2), ref["z"]))
         Kref, Vref = oracle_states_abs(ref, m)
@@ -296,7 +336,8 @@ def test_peaky_logits_diagnostic():
 
 def test_paper_op_shape_sampled():
     """B 32, T 2048, H 4, d 256 in the benchmark's configuration (automatic kernel
-    choice); six sampled (b, h) sequences against the oracle over all tokens."""
+    choice and segment count); six sampled (b, h) sequences against the oracle over
+    all tokens."""
     cyfa = _cyfa()
     x = workload_inputs(FWD_PAPER_OP)
     t = upload(x)

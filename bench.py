@@ -6,16 +6,17 @@ H=16, d_k=d_v=128, chunk 32, bf16 inputs, fp32 accumulation) on synthetic
 seeded inputs already resident in HBM.  One step = one cyfa_forward over the
 whole batch.  Prints one JSON line.
 
-The decode, backward and mixer legs run before the headline forward, so that
-the forward is timed at the GPU's settled clock.
+The other legs run before the headline forward, so that the forward is timed
+at the GPU's settled clock.
 
 Extra fields: ``roofline`` of the dominant kernel (the fused chunk kernel, timed
 alone with HIP events the library records on its launch stream), ``mfma``
 (algorithmic TFLOP/s against the bf16 dense MFMA peak), ``cpu_baseline`` (the
 fp64 CPU oracle timed on a bounded sample of the same workload on this host),
 ``decode`` (the single-token decode step at 256 streams x 16 heads),
-``backward`` (cyfa_backward on the same workload) and ``mixer`` (the mixer
-prologue and epilogue kernels at the same shape).
+``backward`` (cyfa_backward on the same workload), ``mixer`` (the mixer
+prologue and epilogue kernels at the same shape) and ``paper_op`` (the forward
+at the paper's operator-benchmark shape, B 32, T 2048, H 4, d 256).
 """
 from __future__ import annotations
 
@@ -355,6 +356,25 @@ def mixer_bench(args, torch, cyfa, w):
     return res
 
 
+def paper_op_bench(args, torch, cyfa):
+    """The forward at the paper's own operator-benchmark shape (B 32, T 2048, H 4,
+    d_k = d_v = 256, bf16), automatic kernel and segments, fused kernel timed
+    with HIP events as for the headline."""
+    import argparse as _ap
+    from paper_2609_36259_amd.inputs import FWD_PAPER_OP as w
+    sub = _ap.Namespace(kernel="auto", chunk=0, segments=0, steps=200, warmup=100, cold_steps=0)
+    fb = forward_bench(sub, torch, cyfa, w, forward_inputs(sub, torch, w))
+    ks = fb["kernel_ms"] * 1e-3
+    torch.cuda.empty_cache()
+    return dict(workload=w.name, kernel=fb["kernel"], chunk=fb["chunk"], steps=sub.steps,
+                ms_per_step=fb["ms_per_step"], tokens_per_s=w.B * w.T / (fb["ms_per_step"] * 1e-3),
+                fused_kernel_ms=fb["kernel_ms"],
+                mfma={"achieved": fb["flops"] / ks / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                      "frac": fb["flops"] / ks / 1e12 / PEAK_BF16_TFLOPS},
+                hbm={"achieved": fb["bytes"] / ks / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": fb["bytes"] / ks / 1e9 / PEAK_HBM_GBS})
+
+
 def cpu_baseline(w, budget_s: float):
     """Time the CPU oracle on a bounded sample of the workload (leading (b, h)
     sequences, leading tokens), sized to about `budget_s` seconds."""
@@ -398,6 +418,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-mixer", action="store_true")
+    ap.add_argument("--no-paper-op", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -433,10 +454,13 @@ def main():
 
     # The other legs run first: they keep the GPU busy for a few hundred
     # milliseconds, so the headline forward is timed at the clock the chip holds
-    # under sustained load rather than while it is still ramping up; its inputs
-    # are generated before them, so no host-side pause comes in between.
-    prepared = forward_inputs(args, torch, w)
+    # under sustained load rather than while it is still ramping up.  The headline's
+    # inputs are generated after the paper-shape leg (which makes its own) and
+    # before the rest, so no host-side pause comes just before the timed steps.
     extra = {}
+    if not args.no_paper_op and args.workload != "paper-op":
+        extra["paper_op"] = paper_op_bench(args, torch, cyfa)
+    prepared = forward_inputs(args, torch, w)
     if not args.no_decode:
         extra["decode"] = decode_bench(args, torch, cyfa)
     if not args.no_backward and w.dk <= 128 and w.dv <= 128:

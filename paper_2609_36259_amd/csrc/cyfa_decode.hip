@@ -11,12 +11,21 @@
 // The step reads and writes each state once; it is bound by HBM bandwidth.
 // Each workgroup issues both of its rows x d float states' loads at its start
 // (16-byte loads, consecutive lanes on consecutive addresses), so the value
-// state arrives while the key state is updated and the readout runs.
+// state arrives while the key state is updated and the readout runs.  The
+// updated states are written back with nontemporal (streaming) stores: nothing
+// reads them again within the step, and on this memory system a read-modify-write
+// stream with ordinary stores tops out well below one with streaming stores.
 #include "cyfa_rows.h"
 
 namespace cyfa {
 
 namespace {
+
+typedef float f32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store_stream(float4 *p, float4 v) {
+    const f32x4_nt t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<f32x4_nt *>(p));
+}
 
 // Threads per workgroup: eight waves for 128 storage rows (8 + 8 state float4 and
 // 8 readout-matrix rows per thread at d = 128), sixteen for 256 rows.
@@ -113,7 +122,7 @@ __global__ __launch_bounds__(dec_threads(ROWS)) void decode_kernel(DecParams p, 
                 x.y = fmaf(alpha, x.y, ar * k4.y);
                 x.z = fmaf(alpha, x.z, ar * k4.z);
                 x.w = fmaf(alpha, x.w, ar * k4.w);
-                K4[(size_t)row * KQ + ck] = x;
+                store_stream(&K4[(size_t)row * KQ + ck], x);
                 part = x.x * q4.x + x.y * q4.y + x.z * q4.z + x.w * q4.w;
             }
 #pragma unroll
@@ -134,7 +143,7 @@ __global__ __launch_bounds__(dec_threads(ROWS)) void decode_kernel(DecParams p, 
                 x.y = fmaf(alpha, x.y, ar * v4.y);
                 x.z = fmaf(alpha, x.z, ar * v4.z);
                 x.w = fmaf(alpha, x.w, ar * v4.w);
-                V4[(size_t)row * VQ + cv] = x;
+                store_stream(&V4[(size_t)row * VQ + cv], x);
                 vreg[it] = x;
             }
         }

@@ -59,6 +59,25 @@ __device__ __forceinline__ void store8(__hip_bfloat16 *p, const float *y) {
     for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
     *reinterpret_cast<uint4 *>(p) = *reinterpret_cast<const uint4 *>(t);
 }
+// The same as nontemporal (streaming) stores.  The prologue's outputs are whole
+// 16-byte pieces of consecutive lanes, read back only by a later launch; streaming
+// them measured ~15 % faster than ordinary stores for that kernel (the epilogue,
+// which reads two tensors per written one, measured no gain).
+typedef unsigned u32x4_nt __attribute__((ext_vector_type(4)));
+typedef float f32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store8_stream(float *p, const float *y) {
+    const f32x4_nt a = {y[0], y[1], y[2], y[3]}, b = {y[4], y[5], y[6], y[7]};
+    __builtin_nontemporal_store(a, reinterpret_cast<f32x4_nt *>(p));
+    __builtin_nontemporal_store(b, reinterpret_cast<f32x4_nt *>(p + 4));
+}
+__device__ __forceinline__ void store8_stream(__hip_bfloat16 *p, const float *y) {
+    __hip_bfloat16 t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
+    const uint4 u = *reinterpret_cast<const uint4 *>(t);
+    const u32x4_nt v = {u.x, u.y, u.z, u.w};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt *>(p));
+}
 
 // sum over the D / 8 consecutive lanes of one head
 template <int D>
@@ -189,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void conv_norm_kernel(ConvSet cs, int B, 
             if (!live)
 #pragma unroll
                 for (int i = 0; i < kCh; ++i) yt[i] = 0.f;
-            if (active) store8(y + ((size_t)b * T + t) * HD + c0, yt);
+            if (active) store8_stream(y + ((size_t)b * T + t) * HD + c0, yt);
             // slide the window: win[s] <- win[s - 1]
 #pragma unroll
             for (int s = KMAX - 1; s >= 1; --s)

@@ -309,6 +309,51 @@ cyfa_status cyfa_mixer_epilogue(const cyfa_mixer_desc *desc, const void *o, cons
                                 const float *norm_o, const int32_t *lens, void *out, void *stream);
 
 /*
+ * Mixer weights of the layer forward (cyfa_forward_mixer); each field means what
+ * the same-named argument of cyfa_mixer_prologue / cyfa_mixer_epilogue means.
+ * z_delta is required; z_alpha NULL means no decay (log alpha = 0), z_beta NULL
+ * beta = 1, gate NULL no output gate, norm_o NULL unit weights.
+ */
+typedef struct {
+    int32_t conv_size;               /* 1..4 */
+    int32_t conv_act;                /* 0 or 1 (SiLU) */
+    float eps;                       /* RMSNorm epsilon (> 0) */
+    const float *conv_q, *conv_k, *conv_v;   /* [H*d, conv_size] or NULL */
+    const float *norm_q, *norm_k;    /* [d] or NULL */
+    const float *z_delta, *b_delta;  /* [B, T, H], [H] (b may be NULL) */
+    const float *z_alpha, *b_alpha, *A;      /* [B, T, H], [H], [H] (A required with z_alpha) */
+    const float *z_beta;             /* [B, T, H] or NULL */
+    const void *gate;                /* [B, T, H, d] dtype or NULL */
+    const float *norm_o;             /* [d] or NULL */
+} cyfa_mixer_weights;
+
+/*
+ * Layer forward: cyfa_mixer_prologue -> cyfa_forward -> cyfa_mixer_epilogue in
+ * one pass over the sequence (Sec. 4, network design, around the operator of
+ * Sec. 3.3, Eq. cyfa-two-pass).  The ShortConv, the QK RMSNorm and the gate
+ * activations run in the matrix-core kernel's chunk staging, and the output
+ * RMSNorm and gate on its output tile, so the operator's q, k, v, gates and o
+ * never go to memory; the arithmetic is the standalone kernels', and `out` is
+ * bit-identical to the three calls in sequence.
+ *   desc       as for cyfa_forward; BF16, d_k = d_v = 128, m <= 127 (the
+ *              matrix-core kernel); desc->kernel AUTO or MFMA
+ *   mw         mixer weights and gate inputs (above)
+ *   q_in, k_in, v_in   [B, T, H, 128] bf16 raw projections
+ *   lens       [B] int32 or NULL, as for cyfa_forward_lens (rows t >= lens[b]
+ *              of `out` are written as 0, as the epilogue writes them)
+ *   out        [B, T, H, 128] bf16 layer output (must not alias an input)
+ *   R, K0, V0, clock0, K_out, V_out, clock_out, logits_out, workspace (size from
+ *              cyfa_forward_workspace_size(desc)), stream: as for cyfa_forward.
+ */
+cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw,
+                               const void *q_in, const void *k_in, const void *v_in,
+                               const float *R, const int32_t *lens,
+                               const float *K0, const float *V0, const double *clock0,
+                               void *out, float *K_out, float *V_out, double *clock_out,
+                               float *logits_out, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
+/*
  * Single-token decode descriptor: N independent streams, H heads each.
  *   d_k, d_v 64, 128 or 256; m odd 3..255 (m > 127: d_k, d_v <= 128); dtype of q, k, v, o.
  */

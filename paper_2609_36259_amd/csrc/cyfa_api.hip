@@ -20,7 +20,7 @@ size_t mfma_workspace_bytes(const FwdParams &p, int segments);
 int mfma_auto_segments(const FwdParams &p);
 int mfma_default_chunk();
 hipError_t launch_fwd_mfma(const FwdParams &p, int segments, void *ws, hipStream_t s,
-                           hipEvent_t ev_start, hipEvent_t ev_stop);
+                           hipEvent_t ev_start, hipEvent_t ev_stop, const MixIn *mix = nullptr);
 }  // namespace cyfa
 
 namespace {
@@ -245,16 +245,19 @@ cyfa_status cyfa_forward(const cyfa_fwd_desc *desc, const void *q, const void *k
 
 namespace {
 // cyfa_forward_lens (lens or nothing) and cyfa_forward_varlen (cu_seqlens)
+// mix: the layer forward (cyfa_forward_mixer): q, k, v are the raw projections,
+// the gates come from mix, and o receives the layer output.
 cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,
                          const float *delta, const float *log_alpha, const float *beta, const float *R,
                          const int32_t *lens, const int32_t *cu, const float *K0, const float *V0,
                          const double *clock0, void *o, float *K_out, float *V_out, double *clock_out,
-                         float *logits_out, void *workspace, size_t workspace_bytes, void *stream) {
+                         float *logits_out, void *workspace, size_t workspace_bytes, void *stream,
+                         const cyfa::MixIn *mix = nullptr) {
     FwdPlan plan;
     cyfa_status st = plan_forward(desc, &plan);
     if (st != CYFA_OK) return st;
     const bool has_tokens = desc->T > 0;
-    if (has_tokens && (!q || !k || !v || !delta || !o))
+    if (has_tokens && (!q || !k || !v || (!delta && !mix) || !o))
         return fail(CYFA_ERR_INVALID_ARGUMENT, "q, k, v, delta and o are required");
     const void *vec[] = {q, k, v, o, K0, V0, K_out, V_out};
     const char *vec_names[] = {"q", "k", "v", "o", "K0", "V0", "K_out", "V_out"};
@@ -290,7 +293,7 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
     hipError_t e;
     if (plan.mfma) {
         // forms its own bf16 readout matrix
-        e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
+        e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop, mix);
     } else {
         e = p.m > cyfa::kMaxActive ? cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s)
                                    : cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
@@ -315,6 +318,43 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
                               size_t workspace_bytes, void *stream) {
     return forward_impl(desc, q, k, v, delta, log_alpha, beta, R, lens, nullptr, K0, V0, clock0, o, K_out,
                         V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
+}
+
+cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw, const void *q_in,
+                               const void *k_in, const void *v_in, const float *R, const int32_t *lens,
+                               const float *K0, const float *V0, const double *clock0, void *out,
+                               float *K_out, float *V_out, double *clock_out, float *logits_out,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+    if (!desc || !mw) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc and mw are required");
+    if (desc->dtype != CYFA_BF16 || desc->d_k != 128 || desc->d_v != 128 || desc->m > cyfa::kMaxActive ||
+        desc->kernel == CYFA_KERNEL_VALU)
+        return fail(CYFA_ERR_UNSUPPORTED,
+                    "the layer forward runs on the matrix-core kernel: BF16, d_k = d_v = 128, m <= 127");
+    if (mw->conv_size < 1 || mw->conv_size > cyfa::kMixMaxConv)
+        return fail(CYFA_ERR_UNSUPPORTED, "conv_size must be in [1, %d]", cyfa::kMixMaxConv);
+    if (mw->conv_act != 0 && mw->conv_act != 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "conv_act must be 0 or 1");
+    if (!(mw->eps > 0.f) || !std::isfinite(mw->eps)) return fail(CYFA_ERR_INVALID_ARGUMENT, "eps must be > 0");
+    if (desc->T > 0 && !mw->z_delta) return fail(CYFA_ERR_INVALID_ARGUMENT, "z_delta is required");
+    if (mw->z_alpha && !mw->A) return fail(CYFA_ERR_INVALID_ARGUMENT, "A is required with z_alpha");
+    const void *sc[] = {mw->conv_q, mw->conv_k, mw->conv_v, mw->norm_q, mw->norm_k, mw->z_delta, mw->b_delta,
+                        mw->z_alpha, mw->b_alpha, mw->A, mw->z_beta, mw->norm_o};
+    for (const void *ptr : sc)
+        if (ptr && !aligned(ptr, 4)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scalar arrays must be 4-byte aligned");
+    if (mw->gate && !aligned(mw->gate, 16)) return fail(CYFA_ERR_INVALID_ARGUMENT, "gate must be 16-byte aligned");
+    {
+        const void *ins[] = {q_in, k_in, v_in, mw->gate, mw->z_delta, mw->z_alpha, mw->z_beta, R, K0, V0, lens};
+        for (const void *in : ins)
+            if (out && in == out) return fail(CYFA_ERR_INVALID_ARGUMENT, "out must not alias an input");
+    }
+    cyfa::MixIn mix{};
+    mix.wq = mw->conv_q; mix.wk = mw->conv_k; mix.wv = mw->conv_v; mix.gq = mw->norm_q; mix.gk = mw->norm_k;
+    mix.z_delta = mw->z_delta; mix.b_delta = mw->b_delta; mix.z_alpha = mw->z_alpha; mix.b_alpha = mw->b_alpha;
+    mix.A = mw->A; mix.z_beta = mw->z_beta; mix.gate = mw->gate; mix.g_o = mw->norm_o;
+    mix.K = mw->conv_size; mix.act = mw->conv_act; mix.eps = mw->eps;
+    cyfa_fwd_desc d2 = *desc;
+    d2.kernel = CYFA_KERNEL_MFMA;
+    return forward_impl(&d2, q_in, k_in, v_in, nullptr, nullptr, nullptr, R, lens, nullptr, K0, V0, clock0, out,
+                        K_out, V_out, clock_out, logits_out, workspace, workspace_bytes, stream, &mix);
 }
 
 cyfa_status cyfa_forward_varlen(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,

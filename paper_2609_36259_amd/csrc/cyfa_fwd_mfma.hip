@@ -526,16 +526,241 @@ __device__ __forceinline__ bf16x8 decay_rows(bf16x8 v, const float *dw) {
     return r;
 }
 
+// ---- mixer pieces of the fused layer forward ----------------------------------
+// The layer forward (cyfa_forward_mixer) runs the mixer prologue inside the fused
+// kernel's chunk staging and the epilogue on its output tile, with the standalone
+// kernels' arithmetic (cyfa_mixer.hip) in the same order, so that its output is
+// the bits of prologue -> forward -> epilogue.  Thread (tid) of the staging owns
+// channel block cb = tid % 16 (channels 8 cb .. 8 cb + 7) of rows tid / 16 and
+// tid / 16 + 16 of each tile -- the positions store_chunk writes -- and the 16
+// threads of a row are consecutive lanes of one wave.  In the mixer variant the
+// (cos, sin) table's LDS holds the convolution taps and three raw rows before
+// the chunk (the halo); the rotations compute their table entries on the fly.
+constexpr int kMixHead = 128;                             // channels per head
+constexpr int kMixTapBytes = 3 * kMixHead * 4 * 4;        // [q, k, v][s][channel]: weight of x_{t-s}
+constexpr int kMixHaloBytes = 3 * 3 * kMixHead * 2;       // [q, k, v][row -3 .. -1][channel] bf16
+constexpr int kMixNormBytes = 3 * kMixHead * 4;           // g_q, g_k, g_o
+
+struct MixLds {
+    int taps, halo, norm;                                 // byte offsets in the workgroup's LDS
+};
+
+__device__ __forceinline__ void bf16x8_to_float(uint4 u, float *x) {
+    const unsigned w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ uint4 float_to_bf16x8(const float *y) {
+    __hip_bfloat16 t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
+    return *reinterpret_cast<const uint4 *>(t);
+}
+// sum over the 16 lanes of one row (the standalone kernels' head reduction)
+__device__ __forceinline__ float mix_row_sum(float s) {
+#pragma unroll
+    for (int o = 1; o < kMixHead / 8; o <<= 1) s += __shfl_xor(s, o);
+    return s;
+}
+
+// Per-segment set-up: taps (zero past the width, reversed so that s indexes
+// x_{t-s}), RMSNorm weights, and the halo of the segment's first chunk (raw rows
+// t0-3 .. t0-1 of the sequence, zero before its start).
+__device__ __forceinline__ void mix_setup(const MfmaArgs &a, const MixLds &L, char *smem, int b, int h, int t0,
+                                          int tid, int nth) {
+    const FwdParams &p = a.p;
+    const MixIn &mx = a.mix;
+    const int K = mx.K;
+    for (int e = tid; e < 3 * kMixHead * 4; e += nth) {
+        const int tensor = e / (kMixHead * 4), s = (e / kMixHead) % 4, ch = e % kMixHead;
+        const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
+        const float w = (W && s < K) ? W[((size_t)h * kMixHead + ch) * K + (K - 1 - s)] : 0.f;
+        lds_at<float>(smem, L.taps)[e] = w;
+    }
+    for (int e = tid; e < 3 * kMixHead; e += nth) {
+        const int which = e / kMixHead, ch = e % kMixHead;
+        const float *g = which == 0 ? mx.gq : (which == 1 ? mx.gk : mx.g_o);
+        lds_at<float>(smem, L.norm)[e] = g ? g[ch] : 1.f;
+    }
+    const int Tb = seq_tokens(p, b);
+    for (int e = tid; e < 3 * 3 * 16; e += nth) {
+        const int tensor = e / 48, hr = (e / 16) % 3, cb = e % 16;
+        const int t = t0 - 3 + hr;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (t >= 0 && t < Tb) {
+            const void *X = tensor == 0 ? p.q : (tensor == 1 ? p.k : p.v);
+            v = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(X) +
+                                                 ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb);
+        }
+        *reinterpret_cast<uint4 *>(smem + L.halo + ((tensor * 3 + hr) * kMixHead + 8 * cb) * 2) = v;
+    }
+}
+
+// ShortConv (+ SiLU) (+ RMSNorm for q, k) of this thread's two rows of one tensor,
+// from the raw tile (rows >= 0) and the halo (rows < 0), as bf16.  Rows past the
+// sequence come out as 0.  tensor 0: q (padded tile), 1: k, 2: v (swizzled).
+template <int CC>
+__device__ __forceinline__ void mix_conv_rows(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int tensor,
+                                              int tid, int live0, int live1, uint4 *outv) {
+    const MixIn &mx = a.mix;
+    // opaque per call: the addresses below are formed here, not held across the chunk loop
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
+    const bool conv = W != nullptr;
+    const float *g = tensor == 0 ? mx.gq : (tensor == 1 ? mx.gk : nullptr);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it;
+        // x_{t-s} for s = 0 .. 3 in the standalone kernel's order of products
+        float y[8];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s > 0 && !conv) break;                     // uniform: only x_t is used
+            const int rr = r - s;
+            uint4 u;
+            if (rr >= 0) {
+                const int off = tensor == 0 ? 2 * (rr * QS + 8 * cb) : 2 * swz_elem(rr, 8 * cb);
+                u = *reinterpret_cast<const uint4 *>(smem + tile + off);
+            } else {
+                u = *reinterpret_cast<const uint4 *>(smem + L.halo + ((tensor * 3 + rr + 3) * kMixHead + 8 * cb) * 2);
+            }
+            float x[8];
+            bf16x8_to_float(u, x);
+            if (!conv) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) y[i] = x[i];
+            } else {
+                const float *tp = lds_at<float>(smem, L.taps + ((tensor * 4 + s) * kMixHead + 8 * cb) * 4);
+                const float4 w0 = *reinterpret_cast<const float4 *>(tp);
+                const float4 w1 = *reinterpret_cast<const float4 *>(tp + 4);
+                const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+                for (int i = 0; i < 8; ++i) y[i] = fmaf(wv[i], x[i], s == 0 ? 0.f : y[i]);
+            }
+        }
+        if (mx.act)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] = y[i] * mix_sigm(y[i]);
+        if (g) {
+            float ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ss = fmaf(y[i], y[i], ss);
+            const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
+            const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb) * 4);
+            const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb + 4) * 4);
+            const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] *= rn * gr[i];
+        }
+        if (!(it == 0 ? live0 : live1))
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] = 0.f;
+        outv[it] = float_to_bf16x8(y);
+    }
+}
+
+// The (cos, sin) table entry of pair q*4 + jj for a token (its builder record
+// rec), computed exactly as build_writes_swz computes it.
+__device__ __forceinline__ half2v mix_cs_entry(float4 rec, int q, int jj, int J) {
+    const float u = rec.y, c1 = rec.z, s1 = rec.w;
+    float sn, cs;
+    sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k >= jj) break;
+        const float nc = cs * c1 - sn * s1;
+        const float ns = sn * c1 + cs * s1;
+        cs = nc;
+        sn = ns;
+    }
+    const int j = 4 * q + 1 + jj;
+    const bool live = j <= J && j <= 63;
+    const float cv = live ? cs : 0.f;
+    const float sv = live ? sn : 0.f;
+    half2v e;
+    e[0] = (_Float16)(j == 64 ? 1.f : cv);
+    e[1] = (_Float16)sv;
+    return e;
+}
+
+// Epilogue of one chunk: out = RMSNorm(o) g_o sigmoid(gate) for this thread's
+// rows of the staged output tile (padded, in the Q tile's place).
+template <int CC>
+__device__ __forceinline__ void mix_epilogue(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int b, int h,
+                                             int t0, int Tb, int tid, const uint4 *gpf) {
+    const FwdParams &p = a.p;
+    const MixIn &mx = a.mix;
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb) * 4);
+    const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb + 4) * 4);
+    const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    __bf16 *out = static_cast<__bf16 *>(p.o);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it, t = t0 + r;
+        const bool live = t < Tb;
+        float yt[8], gt[8];
+        if (live) {
+            bf16x8_to_float(*reinterpret_cast<const uint4 *>(smem + tile + 2 * (r * QS + 8 * cb)), yt);
+            if (mx.gate) bf16x8_to_float(gpf[it], gt);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) yt[i] = 0.f;
+        }
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fmaf(yt[i], yt[i], ss);
+        const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float v = yt[i] * rn * gr[i];
+            if (mx.gate && live) v *= mix_sigm(gt[i]);
+            yt[i] = live ? v : 0.f;
+        }
+        if (t < p.T)
+            *reinterpret_cast<uint4 *>(out + ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb) =
+                float_to_bf16x8(yt);
+    }
+}
+
+// Gate rows of this thread for a chunk (zero past the sequence), loaded during the
+// chunk so that its epilogue does not wait for them.
+__device__ __forceinline__ void mix_load_gate(const MfmaArgs &a, int b, int h, int t0, int Tb, int tid, uint4 *gpf) {
+    const FwdParams &p = a.p;
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const int avail = Tb - t0;
+    gpf[0] = make_uint4(0, 0, 0, 0);
+    gpf[1] = gpf[0];
+    if (!a.mix.gate || avail <= 0) return;                 // uniform
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = min(r0 + 16 * it, avail - 1);        // rows past the sequence re-read its last
+        gpf[it] = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.mix.gate) +
+                                                   ((seq_row0(p, b) + t0 + r) * p.H + h) * kMixHead + 8 * cb);
+    }
+}
+
 // ---- 3. fused chunk forward, 32-token chunks ------------------------------------
 // Two workgroups share a compute unit; the readout matrix sits in LDS and the
 // next chunk is prefetched into registers.
-template <int CC>
+// kMix: the layer forward (the mixer prologue in the chunk staging, the
+// epilogue on the output tile; see the mixer pieces above).
+template <int CC, bool kMix>
 __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
     using Ly = Lay<CC>;
     constexpr int RB = Ly::RB;
     constexpr int SSC = Ly::SSC;
-    __shared__ __attribute__((aligned(256))) char smem[Ly::BYTES];
+    static_assert(kMixTapBytes + kMixHaloBytes <= CC * Ly::CSW * 4, "taps and halo fit the table's place");
+    static_assert(!kMix || Ly::BYTES + kMixNormBytes <= 80 * 1024, "two workgroups per compute unit");
+    __shared__ __attribute__((aligned(256))) char smem[Ly::BYTES + (kMix ? kMixNormBytes : 0)];
+    const MixLds ML{Ly::CS, Ly::CS + kMixTapBytes, Ly::BYTES};
     const Tiles s = fused_tiles<CC>(smem);
     const FwdParams &p = a.p;
     const int bh = blockIdx.x / a.P, seg = blockIdx.x % a.P;
@@ -588,7 +813,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     // (needed by the first stage), then the entering states, which the first
     // chunk's products need only after its staging, scans and temporal writes.
     Prefetch<CC> pf;
-    load_chunk<CC, true>(p, b, h, c_begin * CC, Tb, tid, pf);
+    load_chunk<CC, true, NT, kMix>(p, b, h, c_begin * CC, Tb, tid, pf, &a.mix);
+    if constexpr (kMix) mix_setup(a, ML, smem, b, h, c_begin * CC, tid, NT);
+    uint4 gpf[2];                                    // kMix: the chunk's gate rows
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
         const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
@@ -618,16 +845,52 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * CC;
         const int n = min(CC, Tb - t0);          // <= 0 for chunks past the sequence
+        // kMix: the previous chunk's epilogue, from its output tile in Q's place; each
+        // thread reads exactly the positions it overwrites next
+        if constexpr (kMix)
+            if (c > c_begin) mix_epilogue<CC>(a, ML, smem, Ly::Q, b, h, t0 - CC, Tb, tid, gpf);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         lds_barrier();
-        if (c + 1 < c_end) load_chunk<CC, true>(p, b, h, t0 + CC, Tb, tid, pf);
+        if constexpr (kMix) {
+            // the staged rows are raw projections: ShortConv, RMSNorm, then the
+            // operator's q, k, v replace them (one more barrier: the convolution
+            // reads three rows above each row)
+            const int r0 = tid >> 4;
+            const bool live0 = t0 + r0 < Tb, live1 = t0 + r0 + 16 < Tb;
+            uint4 fq[2], fk[2], fv[2];
+            mix_conv_rows<CC>(a, ML, smem, Ly::Q, 0, tid, live0, live1, fq);
+            mix_conv_rows<CC>(a, ML, smem, Ly::K, 1, tid, live0, live1, fk);
+            mix_conv_rows<CC>(a, ML, smem, Ly::V, 2, tid, live0, live1, fv);
+            lds_barrier();
+            const int tq = opq(tid);
+            const int cb = tq & 15, rq = tq >> 4;
+            const int offq = 2 * (rq * QS + 8 * cb), offs = 2 * swz_elem(rq, 8 * cb);
+            const int offq1 = offq + 2 * 16 * QS, offs1 = offs + 2 * 16 * SWS;
+            if (rq + 16 >= CC - 3) {
+                // raw rows CC-3 .. CC-1: the next chunk's halo
+                const int hr = rq + 16 - (CC - 3);
+                *reinterpret_cast<uint4 *>(smem + ML.halo + ((0 * 3 + hr) * kMixHead + 8 * cb) * 2) =
+                    *reinterpret_cast<const uint4 *>(smem + Ly::Q + offq1);
+                *reinterpret_cast<uint4 *>(smem + ML.halo + ((1 * 3 + hr) * kMixHead + 8 * cb) * 2) =
+                    *reinterpret_cast<const uint4 *>(smem + Ly::K + offs1);
+                *reinterpret_cast<uint4 *>(smem + ML.halo + ((2 * 3 + hr) * kMixHead + 8 * cb) * 2) =
+                    *reinterpret_cast<const uint4 *>(smem + Ly::V + offs1);
+            }
+            *reinterpret_cast<uint4 *>(smem + Ly::Q + offq) = fq[0];
+            *reinterpret_cast<uint4 *>(smem + Ly::Q + offq1) = fq[1];
+            *reinterpret_cast<uint4 *>(smem + Ly::K + offs) = fk[0];
+            *reinterpret_cast<uint4 *>(smem + Ly::K + offs1) = fk[1];
+            *reinterpret_cast<uint4 *>(smem + Ly::V + offs) = fv[0];
+            *reinterpret_cast<uint4 *>(smem + Ly::V + offs1) = fv[1];
+        }
+        if (c + 1 < c_end) load_chunk<CC, true, NT, kMix>(p, b, h, t0 + CC, Tb, tid, pf, &a.mix);
         // factor applied to the carried states this chunk, and whether the chunk's
         // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
         const bool fac = __builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[2])) != 0;
-        build_writes_swz<CC, true, NT, CSW>(s, s.As, tid, m);
+        build_writes_swz<CC, !kMix, NT, CSW>(s, s.As, tid, m);
         lds_barrier();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A.  With the
         //    tile holding A_dec (rows times the right decay), Gamma_rs = gam_r decw_s
@@ -687,7 +950,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4)
 #pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2) csx[2 * v4 + k2] = CSrow[4 * v4 + k2];
+            for (int k2 = 0; k2 < 2; ++k2)
+                csx[2 * v4 + k2] = kMix ? mix_cs_entry(s.bw[l32], 4 * w + v4, 2 * hl + k2, (m - 1) >> 1)
+                                        : CSrow[4 * v4 + k2];
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
             bf16x4 xv;
@@ -791,7 +1056,9 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4)
 #pragma unroll
-                for (int k2 = 0; k2 < 2; ++k2) csy[2 * v4 + k2] = CSrow[4 * v4 + k2];
+                for (int k2 = 0; k2 < 2; ++k2)
+                    csy[2 * v4 + k2] = kMix ? mix_cs_entry(s.bw[l32], 4 * w + v4, 2 * hl + k2, (m - 1) >> 1)
+                                            : CSrow[4 * v4 + k2];
             f32x16 yacc = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) yacc = mma(lds8_tr(Myt + 16 * ks * SWS, SWS), lds8(Xa + 16 * ks), yacc);
@@ -820,6 +1087,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) vacc[x][v] *= sf;
         }
+        if constexpr (kMix) mix_load_gate(a, b, h, t0, Tb, tid, gpf);
         score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane, fac);
         f32x16 pacc = zero_acc();
 #pragma unroll
@@ -842,7 +1110,17 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // output: lane (token l32, half hl) stores its 16 columns 32w + 4hl + 8 v4 ..
         // as four 8-byte pieces (uniform chunk base plus a 32-bit lane offset); the
         // four waves' pieces of a token row merge in L2
-        if (l32 < n) {
+        if constexpr (kMix) {
+            // the operator's output tile goes to Q's place (free since the readout) for
+            // the epilogue at the start of the next chunk
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+                bf16x4 ov;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) ov[k] = (__bf16)pacc[4 * v4 + k];
+                *reinterpret_cast<bf16x4 *>(Wrow + 8 * v4) = ov;
+            }
+        } else if (l32 < n) {
             char *ob = reinterpret_cast<char *>(o + ((seq_row0(p, b) + t0) * p.H + h) * D);
             const unsigned loff = (unsigned)opq((l32 * p.H * D + 32 * w + h4) * 2);
 #pragma unroll
@@ -874,6 +1152,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
         lds_barrier();
     }
+    if constexpr (kMix)
+        if (c_end > c_begin) mix_epilogue<CC>(a, ML, smem, Ly::Q, b, h, (c_end - 1) * CC, Tb, tid, gpf);
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));
         dump_state(a.fin_state + (size_t)bh * kStateFloats, w, lane, kacc, vacc);
@@ -1016,8 +1296,12 @@ hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_s
     if (a.nchunks > 0 && a.hv == 2) {
         if ((e = launch_chunk256(a, st, ev_start, ev_stop)) != hipSuccess) return e;
     } else if (a.nchunks > 0) {
-        hipExtLaunchKernelGGL(chunk_forward_kernel<CC>, dim3(BHv * a.P), dim3(NT), 0, st, ev_start, ev_stop, 0,
-                              a);
+        if (a.mix.z_delta)
+            hipExtLaunchKernelGGL((chunk_forward_kernel<CC, true>), dim3(BHv * a.P), dim3(NT), 0, st, ev_start,
+                                  ev_stop, 0, a);
+        else
+            hipExtLaunchKernelGGL((chunk_forward_kernel<CC, false>), dim3(BHv * a.P), dim3(NT), 0, st, ev_start,
+                                  ev_stop, 0, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
@@ -1046,8 +1330,9 @@ int mfma_auto_segments(const FwdParams &p) {
 }
 
 hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
-                           hipEvent_t ev_start, hipEvent_t ev_stop) {
+                           hipEvent_t ev_start, hipEvent_t ev_stop, const MixIn *mix) {
     char *base = static_cast<char *>(ws);
+    if (mix) P = 1;
     const WsLayout L = ws_layout(p, P);
     const int C = kMfmaChunk;
     MfmaArgs a{};
@@ -1069,6 +1354,7 @@ hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
     a.has_init = (a.P > 1 || p.K0 || p.V0 || p.clock0 || a.want_final) ? 1 : 0;
     a.zero_init = (p.K0 || p.V0) ? 0 : 1;
     a.hv = virtual_heads(p);
+    if (mix) a.mix = *mix;
     const int BHv = p.B * p.H * a.hv;
 
     hipError_t e = launch_cc<32>(a, BHv, st, ev_start, ev_stop);

@@ -4,6 +4,7 @@
 #pragma once
 
 #include "cyfa_mfma_common.h"
+#include "cyfa_mixer.h"
 
 namespace cyfa {
 
@@ -30,6 +31,8 @@ struct MfmaArgs {
                          // each block as a head of its own (a "virtual head", index
                          // hv h + block): the states of a 256-channel head are two 128 x 128
                          // pairs, and the per-token scalars are shared by its blocks.
+    MixIn mix;           // fused layer forward only: the mixer's weights and gate inputs (p.q,
+                         // p.k, p.v are then the raw projections and p.o the layer output)
 };
 
 
@@ -112,9 +115,11 @@ struct Prefetch {
 };
 
 // Tb: tokens of this sequence (rows at or past it read as zero, scalars as 0).
-template <int CC, bool kWithQ, int NTH = NT>
+// kMix: the per-token scalars are the gate activations of the mixer's projections
+// (mx), computed as the standalone prologue computes them.
+template <int CC, bool kWithQ, int NTH = NT, bool kMix = false>
 __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int t0, int Tb, int tid,
-                                           Prefetch<CC, NTH> &pf) {
+                                           Prefetch<CC, NTH> &pf, const MixIn *mx = nullptr) {
     constexpr int kRows = NTH / 16;                  // rows per pass
     // Uniform chunk base (scalar registers) plus a fixed 32-bit per-lane byte offset:
     // no per-lane 64-bit address arithmetic.  Rows past the sequence read as zero.
@@ -153,9 +158,17 @@ __device__ __forceinline__ void load_chunk(const FwdParams &p, int b, int h, int
         // across the whole chunk loop
         const unsigned soff = (unsigned)opq(tid * p.H);
         if (tid < CC && t < Tb) {
-            pf.dl = (p.delta + sbase)[soff];
-            pf.g = p.log_alpha ? (p.log_alpha + sbase)[soff] : 0.f;
-            pf.be = p.beta ? (p.beta + sbase)[soff] : 1.f;
+            if constexpr (kMix) {
+                pf.dl = mix_sigm((mx->z_delta + sbase)[soff] + (mx->b_delta ? mx->b_delta[h] : 0.f));
+                pf.g = mx->z_alpha ? -mx->A[h] * mix_softplus((mx->z_alpha + sbase)[soff] +
+                                                              (mx->b_alpha ? mx->b_alpha[h] : 0.f))
+                                   : 0.f;
+                pf.be = mx->z_beta ? mix_sigm((mx->z_beta + sbase)[soff]) : 1.f;
+            } else {
+                pf.dl = (p.delta + sbase)[soff];
+                pf.g = p.log_alpha ? (p.log_alpha + sbase)[soff] : 0.f;
+                pf.be = p.beta ? (p.beta + sbase)[soff] : 1.f;
+            }
         } else {
             pf.dl = 0.f;   // rows past the chunk or the sequence: no shift, no decay, no write
             pf.g = 0.f;

@@ -22,6 +22,27 @@ struct MixParams {
     float *delta, *log_alpha, *beta;
 };
 
+// Gate activations of the prologue (Eq. clock_gradient_stabilization and the
+// forget-gate parameterisation); shared by the standalone prologue and the
+// matrix-core forward that runs the prologue inside its chunk staging, so that
+// both produce the same bits.
+__device__ __forceinline__ float mix_sigm(float x) { return 1.f / (1.f + __expf(-x)); }
+__device__ __forceinline__ float mix_softplus(float x) { return x > 20.f ? x : log1pf(__expf(x)); }
+
+// Mixer inputs of the fused layer forward (cyfa_forward_mixer): the raw
+// projections come in through FwdParams q, k, v; these are the rest.
+struct MixIn {
+    const float *wq, *wk, *wv;      // [H*128][K] ShortConv taps or NULL (no convolution)
+    const float *gq, *gk;           // [128] RMSNorm weights or NULL (no normalisation)
+    const float *z_delta, *b_delta; // delta = sigmoid(z_delta + b_delta); z_delta required
+    const float *z_alpha, *b_alpha, *A;  // log alpha = -A softplus(z_alpha + b_alpha); NULL: 0
+    const float *z_beta;            // beta = sigmoid(z_beta); NULL: 1
+    const void *gate;               // [B, T, H, 128] output gate or NULL
+    const float *g_o;               // [128] output RMSNorm weights or NULL (unit)
+    int K, act;                     // ShortConv width 1..kMixMaxConv, SiLU after it
+    float eps;                      // RMSNorm epsilon
+};
+
 hipError_t launch_mixer_prologue(const MixParams &p, hipStream_t s);
 hipError_t launch_mixer_epilogue(const MixParams &p, const void *o, const void *gate, const float *g, void *out,
                                  hipStream_t s);

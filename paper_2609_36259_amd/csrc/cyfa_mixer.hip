@@ -28,8 +28,8 @@ constexpr int kCh = 8;              // channels per thread
 constexpr int kTokens = 16;         // tokens per workgroup
 static_assert(kMixMaxConv % 4 == 0, "16-byte tap loads");
 
-__device__ __forceinline__ float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
-__device__ __forceinline__ float softplus_f(float x) { return x > 20.f ? x : log1pf(__expf(x)); }
+__device__ __forceinline__ float sigm(float x) { return mix_sigm(x); }
+__device__ __forceinline__ float softplus_f(float x) { return mix_softplus(x); }
 
 __device__ __forceinline__ int mix_tokens(const int *lens, int b, int T) {
     return lens ? min(max(lens[b], 0), T) : T;

@@ -28,6 +28,7 @@ def store_rows(m: int) -> int:
 
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens", "cyfa_forward_varlen",
+            "cyfa_forward_mixer",
             "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_mixer_prologue",
             "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step",
             "cyfa_decode_step_noalloc", "cyfa_set_timing_events",
@@ -52,6 +53,12 @@ class MixDesc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("conv_size", ctypes.c_int32),
                 ("conv_act", ctypes.c_int32), ("eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class MixWeights(ctypes.Structure):
+    _fields_ = [("conv_size", ctypes.c_int32), ("conv_act", ctypes.c_int32), ("eps", ctypes.c_float)] + \
+        [(n, ctypes.c_void_p) for n in ("conv_q", "conv_k", "conv_v", "norm_q", "norm_k", "z_delta", "b_delta",
+                                         "z_alpha", "b_alpha", "A", "z_beta", "gate", "norm_o")]
 
 
 class DecDesc(ctypes.Structure):
@@ -81,6 +88,9 @@ def load() -> ctypes.CDLL:
         lib.cyfa_forward_lens.restype = ctypes.c_int
         lib.cyfa_forward_varlen.argtypes = [ctypes.POINTER(FwdDesc)] + [_vp] * 17 + [ctypes.c_size_t, _vp]
         lib.cyfa_forward_varlen.restype = ctypes.c_int
+        lib.cyfa_forward_mixer.argtypes = [ctypes.POINTER(FwdDesc), ctypes.POINTER(MixWeights)] + \
+            [_vp] * 14 + [ctypes.c_size_t, _vp]
+        lib.cyfa_forward_mixer.restype = ctypes.c_int
         lib.cyfa_backward_workspace_size.argtypes = [ctypes.POINTER(FwdDesc),
                                                      ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_backward_workspace_size.restype = ctypes.c_int
@@ -397,6 +407,65 @@ def mixer_epilogue(o, gate=None, norm_o=None, *, lens=None, eps=1e-6, out=None, 
     desc = MixDesc(B, T, H, dv, dv, 1, 0, eps, _dtype_code(o))
     _check(load().cyfa_mixer_epilogue(ctypes.byref(desc), _ptr(o), _ptr(gate), _ptr(norm_o),
                                       _ptr(lens), _ptr(res), _stream_handle(stream)))
+    return res
+
+
+def forward_mixer(q_in, k_in, v_in, z_delta, *, conv_q=None, conv_k=None, conv_v=None, norm_q=None,
+                  norm_k=None, b_delta=None, z_alpha=None, b_alpha=None, A=None, z_beta=None, gate=None,
+                  norm_o=None, R=None, scale=None, m=127, segments=0, lens=None, conv_size=4, conv_act=0,
+                  eps=1e-6, K0=None, V0=None, clock0=None, return_state=False, return_logits=False,
+                  out=None, workspace=None, stream=None):
+    """Layer forward (cyfa_forward_mixer): mixer prologue, the operator and the mixer
+    epilogue in one pass; bf16 q_in, k_in, v_in [B,T,H,128].  Returns ``out``
+    [B,T,H,128] bf16, or a dict with ``out`` and the final state / logits as
+    ``forward`` returns them."""
+    B, T, H, d = q_in.shape
+    if q_in.dtype != torch.bfloat16:
+        raise CyfaError(2, "the layer forward takes bf16 projections")
+    _need(k_in, (B, T, H, d), q_in.dtype, "k_in")
+    _need(v_in, (B, T, H, d), q_in.dtype, "v_in")
+    for name, t in (("conv_q", conv_q), ("conv_k", conv_k), ("conv_v", conv_v)):
+        _need(t, (H * d, conv_size), torch.float32, name)
+    for name, t in (("norm_q", norm_q), ("norm_k", norm_k), ("norm_o", norm_o)):
+        _need(t, (d,), torch.float32, name)
+    for name, t in (("z_delta", z_delta), ("z_alpha", z_alpha), ("z_beta", z_beta)):
+        _need(t, (B, T, H), torch.float32, name)
+    for name, t in (("b_delta", b_delta), ("b_alpha", b_alpha), ("A", A)):
+        _need(t, (H,), torch.float32, name)
+    _need(gate, (B, T, H, d), q_in.dtype, "gate")
+    _need(R, (H, m, m), torch.float32, "R")
+    _need(lens, (B,), torch.int32, "lens")
+    S = store_rows(m)
+    _need(K0, (B, H, S, d), torch.float32, "K0")
+    _need(V0, (B, H, S, d), torch.float32, "V0")
+    _need(clock0, (B, H), torch.float64, "clock0")
+    desc = forward_desc(B, T, H, d, d, m=m, segments=segments, scale=scale, dtype=BF16, kernel=KERNEL_MFMA)
+    nbytes = forward_workspace_size(desc)
+    dev = q_in.device
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    res_out = out if out is not None else torch.empty_like(q_in)
+    _need(res_out, (B, T, H, d), q_in.dtype, "out")
+    mw = MixWeights(conv_size, conv_act, eps, *[_ptr(t) for t in (conv_q, conv_k, conv_v, norm_q, norm_k, z_delta,
+                                                                 b_delta, z_alpha, b_alpha, A, z_beta, gate,
+                                                                 norm_o)])
+    K_out = V_out = clk = None
+    if return_state:
+        K_out = torch.empty((B, H, S, d), dtype=torch.float32, device=dev)
+        V_out = torch.empty((B, H, S, d), dtype=torch.float32, device=dev)
+        clk = torch.empty((B, H), dtype=torch.float64, device=dev)
+    logits = torch.empty((B, T, H, m), dtype=torch.float32, device=dev) if return_logits else None
+    _check(load().cyfa_forward_mixer(ctypes.byref(desc), ctypes.byref(mw), _ptr(q_in), _ptr(k_in), _ptr(v_in),
+                                     _ptr(R), _ptr(lens), _ptr(K0), _ptr(V0), _ptr(clock0), _ptr(res_out),
+                                     _ptr(K_out), _ptr(V_out), _ptr(clk), _ptr(logits), _ptr(workspace),
+                                     ctypes.c_size_t(workspace.numel()), _stream_handle(stream)))
+    if not (return_state or return_logits):
+        return res_out
+    res = {"out": res_out}
+    if return_state:
+        res.update(K=K_out, V=V_out, clock=clk)
+    if return_logits:
+        res["logits"] = logits
     return res
 
 

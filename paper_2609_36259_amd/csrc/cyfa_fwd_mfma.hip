@@ -145,6 +145,227 @@ __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4
         }
 }
 
+// ---- mixer pieces of the fused layer forward ----------------------------------
+// The layer forward (cyfa_forward_mixer) runs the mixer prologue inside the fused
+// kernel's chunk staging and the epilogue on its output tile, with the standalone
+// kernels' arithmetic (cyfa_mixer.hip) in the same order, so that its output is
+// the bits of prologue -> forward -> epilogue.  Thread (tid) of the staging owns
+// channel block cb = tid % 16 (channels 8 cb .. 8 cb + 7) of rows tid / 16 and
+// tid / 16 + 16 of each tile -- the positions store_chunk writes -- and the 16
+// threads of a row are consecutive lanes of one wave.  In the mixer variant the
+// (cos, sin) table's LDS holds the convolution taps and three raw rows before
+// the chunk (the halo); the rotations compute their table entries on the fly.
+constexpr int kMixHead = 128;                             // channels per head
+constexpr int kMixTapBytes = 3 * kMixHead * 4 * 4;        // [q, k, v][s][channel]: weight of x_{t-s}
+constexpr int kMixHaloBytes = 3 * 3 * kMixHead * 2;       // [q, k, v][row -3 .. -1][channel] bf16
+constexpr int kMixNormBytes = 3 * kMixHead * 4;           // g_q, g_k, g_o
+
+struct MixLds {
+    int taps, halo, norm;                                 // byte offsets in the workgroup's LDS
+};
+
+__device__ __forceinline__ void bf16x8_to_float(uint4 u, float *x) {
+    const unsigned w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ uint4 float_to_bf16x8(const float *y) {
+    __hip_bfloat16 t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
+    return *reinterpret_cast<const uint4 *>(t);
+}
+// sum over the 16 lanes of one row (the standalone kernels' head reduction)
+__device__ __forceinline__ float mix_row_sum(float s) {
+#pragma unroll
+    for (int o = 1; o < kMixHead / 8; o <<= 1) s += __shfl_xor(s, o);
+    return s;
+}
+
+// Per-segment set-up: taps (zero past the width, reversed so that s indexes
+// x_{t-s}), RMSNorm weights, and the halo of the segment's first chunk (raw rows
+// t0-3 .. t0-1 of the sequence, zero before its start).
+__device__ __forceinline__ void mix_setup(const MfmaArgs &a, const MixLds &L, char *smem, int b, int h, int t0,
+                                          int tid, int nth) {
+    const FwdParams &p = a.p;
+    const MixIn &mx = a.mix;
+    const int K = mx.K;
+    for (int e = tid; e < 3 * kMixHead * 4; e += nth) {
+        const int tensor = e / (kMixHead * 4), s = (e / kMixHead) % 4, ch = e % kMixHead;
+        const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
+        const float w = (W && s < K) ? W[((size_t)h * kMixHead + ch) * K + (K - 1 - s)] : 0.f;
+        lds_at<float>(smem, L.taps)[e] = w;
+    }
+    for (int e = tid; e < 3 * kMixHead; e += nth) {
+        const int which = e / kMixHead, ch = e % kMixHead;
+        const float *g = which == 0 ? mx.gq : (which == 1 ? mx.gk : mx.g_o);
+        lds_at<float>(smem, L.norm)[e] = g ? g[ch] : 1.f;
+    }
+    const int Tb = seq_tokens(p, b);
+    for (int e = tid; e < 3 * 3 * 16; e += nth) {
+        const int tensor = e / 48, hr = (e / 16) % 3, cb = e % 16;
+        const int t = t0 - 3 + hr;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (t >= 0 && t < Tb) {
+            const void *X = tensor == 0 ? p.q : (tensor == 1 ? p.k : p.v);
+            v = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(X) +
+                                                 ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb);
+        }
+        *reinterpret_cast<uint4 *>(smem + L.halo + ((tensor * 3 + hr) * kMixHead + 8 * cb) * 2) = v;
+    }
+}
+
+// ShortConv (+ SiLU) (+ RMSNorm for q, k) of this thread's rows tid/16 + 16 it
+// (it < CC/16) of one tensor, from the raw tile (rows >= 0) and the halo (rows <
+// 0), as bf16.  Rows past the sequence (tokens t0 + row >= Tb) come out as 0.
+// tensor 0: q (padded tile), 1: k, 2: v (swizzled).
+template <int CC>
+__device__ __forceinline__ void mix_conv_rows(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int tensor,
+                                              int tid, int t0, int Tb, uint4 *outv) {
+    const MixIn &mx = a.mix;
+    // opaque per call: the addresses below are formed here, not held across the chunk loop
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
+    const bool conv = W != nullptr;
+    const float *g = tensor == 0 ? mx.gq : (tensor == 1 ? mx.gk : nullptr);
+#pragma unroll
+    for (int it = 0; it < CC / 16; ++it) {
+        const int r = r0 + 16 * it;
+        // x_{t-s} for s = 0 .. 3 in the standalone kernel's order of products
+        float y[8];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s > 0 && !conv) break;                     // uniform: only x_t is used
+            const int rr = r - s;
+            uint4 u;
+            if (rr >= 0) {
+                const int off = tensor == 0 ? 2 * (rr * QS + 8 * cb) : 2 * swz_elem(rr, 8 * cb);
+                u = *reinterpret_cast<const uint4 *>(smem + tile + off);
+            } else {
+                u = *reinterpret_cast<const uint4 *>(smem + L.halo + ((tensor * 3 + rr + 3) * kMixHead + 8 * cb) * 2);
+            }
+            float x[8];
+            bf16x8_to_float(u, x);
+            if (!conv) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) y[i] = x[i];
+            } else {
+                const float *tp = lds_at<float>(smem, L.taps + ((tensor * 4 + s) * kMixHead + 8 * cb) * 4);
+                const float4 w0 = *reinterpret_cast<const float4 *>(tp);
+                const float4 w1 = *reinterpret_cast<const float4 *>(tp + 4);
+                const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+                for (int i = 0; i < 8; ++i) y[i] = fmaf(wv[i], x[i], s == 0 ? 0.f : y[i]);
+            }
+        }
+        if (mx.act)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] = y[i] * mix_sigm(y[i]);
+        if (g) {
+            float ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ss = fmaf(y[i], y[i], ss);
+            const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
+            const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb) * 4);
+            const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb + 4) * 4);
+            const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] *= rn * gr[i];
+        }
+        if (t0 + r >= Tb)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) y[i] = 0.f;
+        outv[it] = float_to_bf16x8(y);
+    }
+}
+
+// The (cos, sin) table entry of pair q*4 + jj for a token (its builder record
+// rec), computed exactly as build_writes_swz computes it.
+__device__ __forceinline__ half2v mix_cs_entry(float4 rec, int q, int jj, int J) {
+    const float u = rec.y, c1 = rec.z, s1 = rec.w;
+    float sn, cs;
+    sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k >= jj) break;
+        const float nc = cs * c1 - sn * s1;
+        const float ns = sn * c1 + cs * s1;
+        cs = nc;
+        sn = ns;
+    }
+    const int j = 4 * q + 1 + jj;
+    const bool live = j <= J && j <= 63;
+    const float cv = live ? cs : 0.f;
+    const float sv = live ? sn : 0.f;
+    half2v e;
+    e[0] = (_Float16)(j == 64 ? 1.f : cv);
+    e[1] = (_Float16)sv;
+    return e;
+}
+
+// Epilogue of one chunk: out = RMSNorm(o) g_o sigmoid(gate) for this thread's
+// rows of the staged output tile (padded, in the Q tile's place).
+template <int CC>
+__device__ __forceinline__ void mix_epilogue(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int b, int h,
+                                             int t0, int Tb, int tid, const uint4 *gpf) {
+    const FwdParams &p = a.p;
+    const MixIn &mx = a.mix;
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb) * 4);
+    const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb + 4) * 4);
+    const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    __bf16 *out = static_cast<__bf16 *>(p.o);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it, t = t0 + r;
+        const bool live = t < Tb;
+        float yt[8], gt[8];
+        if (live) {
+            bf16x8_to_float(*reinterpret_cast<const uint4 *>(smem + tile + 2 * (r * QS + 8 * cb)), yt);
+            if (mx.gate) bf16x8_to_float(gpf[it], gt);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) yt[i] = 0.f;
+        }
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fmaf(yt[i], yt[i], ss);
+        const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float v = yt[i] * rn * gr[i];
+            if (mx.gate && live) v *= mix_sigm(gt[i]);
+            yt[i] = live ? v : 0.f;
+        }
+        if (t < p.T)
+            *reinterpret_cast<uint4 *>(out + ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb) =
+                float_to_bf16x8(yt);
+    }
+}
+
+// Gate rows of this thread for a chunk (zero past the sequence), loaded during the
+// chunk so that its epilogue does not wait for them.
+__device__ __forceinline__ void mix_load_gate(const MfmaArgs &a, int b, int h, int t0, int Tb, int tid, uint4 *gpf) {
+    const FwdParams &p = a.p;
+    const int tq = opq(tid);
+    const int cb = tq & 15, r0 = tq >> 4;
+    const int avail = Tb - t0;
+    gpf[0] = make_uint4(0, 0, 0, 0);
+    gpf[1] = gpf[0];
+    if (!a.mix.gate || avail <= 0) return;                 // uniform
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = min(r0 + 16 * it, avail - 1);        // rows past the sequence re-read its last
+        gpf[it] = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.mix.gate) +
+                                                   ((seq_row0(p, b) + t0 + r) * p.H + h) * kMixHead + 8 * cb);
+    }
+}
+
 // ---- 1. per-segment state contributions -------------------------------------
 // DeltaS_p = sum_t exp(G_end - G_t) a_t [k_t | v_t]^T over the segment's tokens,
 // with a_t = beta_t U(-lambda_t) b the temporal write (Eq. app-temporal-writes),
@@ -160,13 +381,19 @@ __device__ __forceinline__ void scale_states(f32x16 (&kacc)[4], f32x16 (&vacc)[4
 // transpose read, double-buffered so that a chunk needs one barrier.  Each wave
 // runs the chunk's clock and decay scans itself (lane = token) and passes the
 // per-token phase and amplitude through a private LDS row.
-template <int CC>
+// kMix (layer forward, 32-token steps): the staged k and v rows are the raw
+// projections; the mixer's ShortConv and k's RMSNorm turn them into the operator's
+// k and v in LDS first, and the gates come from their projections.
+template <int CC, bool kMix = false>
 __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float mz_scale) {
     constexpr int STILE = CC * SWS * 2;                // one swizzled K or V tile
     constexpr int KIT = CC * 16 / NT;                  // 16-byte pieces per thread per tensor
     constexpr int RPP = NT / 16;                       // tile rows per pass
     constexpr int SCB = 4 * STILE;                     // per-wave (phase, amplitude) rows
-    __shared__ __attribute__((aligned(256))) char smem[SCB + 4 * 64 * 8 + 4 * 8];
+    constexpr int MIX0 = SCB + 4 * 64 * 8 + 4 * 8;     // kMix: taps, halo, RMSNorm weights
+    __shared__ __attribute__((aligned(256)))
+    char smem[MIX0 + (kMix ? kMixTapBytes + kMixHaloBytes + kMixNormBytes : 0)];
+    const MixLds ML{MIX0, MIX0 + kMixTapBytes, MIX0 + kMixTapBytes + kMixHaloBytes};
     static_assert(SCB + 4 * 64 * 8 + 4 * 8 >= prep_lds_bytes(kPrepRows), "readout-matrix blocks fit");
     const FwdParams &p = a.p;
     const int Pm1 = a.P - 1;
@@ -190,6 +417,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
     const int Tb = seq_tokens(p, b);
     const int t_begin = c_begin * CC, t_end = min(c_end * CC, Tb);
+    if constexpr (kMix) mix_setup(a, ML, smem, b, h, t_begin, tid, NT);
     float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
     double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
 
@@ -205,8 +433,15 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
 
     // segment total of log alpha (the decay reference G_end)
     double gpart = 0.0;
-    if (p.log_alpha)
+    if constexpr (kMix) {
+        const MixIn &mx = a.mix;
+        if (mx.z_alpha)
+            for (int t = t_begin + tid; t < t_end; t += NT)
+                gpart += (double)(-mx.A[h] * mix_softplus(mx.z_alpha[(seq_row0(p, b) + t) * p.H + h] +
+                                                          (mx.b_alpha ? mx.b_alpha[h] : 0.f)));
+    } else if (p.log_alpha) {
         for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[(seq_row0(p, b) + t) * p.H + h];
+    }
     gpart = lane63(wave_incl_scan(gpart));
     if (lane == 0) red[w] = gpart;
 
@@ -232,9 +467,17 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
         const int t = t0 + lane;
         const size_t si = (seq_row0(p, b) + t) * p.H + h;
         const bool tin = lane < CC && t < Tb;
-        dl = tin ? p.delta[si] : 0.f;
-        g = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
-        be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+        if constexpr (kMix) {
+            const MixIn &mx = a.mix;
+            dl = tin ? mix_sigm(mx.z_delta[si] + (mx.b_delta ? mx.b_delta[h] : 0.f)) : 0.f;
+            g = (tin && mx.z_alpha) ? -mx.A[h] * mix_softplus(mx.z_alpha[si] + (mx.b_alpha ? mx.b_alpha[h] : 0.f))
+                                    : 0.f;
+            be = tin ? (mx.z_beta ? mix_sigm(mx.z_beta[si]) : 1.f) : 0.f;
+        } else {
+            dl = tin ? p.delta[si] : 0.f;
+            g = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
+            be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+        }
     };
     if (c_begin < c_end) load(c_begin);
     __syncthreads();
@@ -270,6 +513,32 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
         }
         if (c + 1 < c_end) load(c + 1);
         lds_barrier();
+        if constexpr (kMix) {
+            // raw rows -> the operator's k and v (ShortConv, k's RMSNorm), in place; the
+            // raw rows CC-3 .. CC-1 become the next chunk's halo
+            uint4 fk[KIT], fv[KIT];
+            const int kto = 2 * buf * STILE, vto = kto + STILE;
+            mix_conv_rows<CC>(a, ML, smem, kto, 1, tid, c * CC, Tb, fk);
+            mix_conv_rows<CC>(a, ML, smem, vto, 2, tid, c * CC, Tb, fv);
+            lds_barrier();
+            const int tq = opq(tid);
+            const int cb = tq & 15, rq = tq >> 4;
+            const int offs = 2 * swz_elem(rq, 8 * cb);
+            if (rq + RPP * (KIT - 1) >= CC - 3) {
+                const int hr = rq + RPP * (KIT - 1) - (CC - 3);
+                const int offl = offs + RPP * (KIT - 1) * SWS * 2;
+                *reinterpret_cast<uint4 *>(smem + ML.halo + ((1 * 3 + hr) * kMixHead + 8 * cb) * 2) =
+                    *reinterpret_cast<const uint4 *>(smem + kto + offl);
+                *reinterpret_cast<uint4 *>(smem + ML.halo + ((2 * 3 + hr) * kMixHead + 8 * cb) * 2) =
+                    *reinterpret_cast<const uint4 *>(smem + vto + offl);
+            }
+#pragma unroll
+            for (int it = 0; it < KIT; ++it) {
+                *reinterpret_cast<uint4 *>(smem + kto + offs + it * RPP * SWS * 2) = fk[it];
+                *reinterpret_cast<uint4 *>(smem + vto + offs + it * RPP * SWS * 2) = fv[it];
+            }
+            lds_barrier();
+        }
         const int kt = opq(2 * buf * STILE + trs), vt = opq((2 * buf + 1) * STILE + trs);
 #pragma unroll
         for (int ks = 0; ks < CC / 16; ++ks) {
@@ -526,226 +795,6 @@ __device__ __forceinline__ bf16x8 decay_rows(bf16x8 v, const float *dw) {
     return r;
 }
 
-// ---- mixer pieces of the fused layer forward ----------------------------------
-// The layer forward (cyfa_forward_mixer) runs the mixer prologue inside the fused
-// kernel's chunk staging and the epilogue on its output tile, with the standalone
-// kernels' arithmetic (cyfa_mixer.hip) in the same order, so that its output is
-// the bits of prologue -> forward -> epilogue.  Thread (tid) of the staging owns
-// channel block cb = tid % 16 (channels 8 cb .. 8 cb + 7) of rows tid / 16 and
-// tid / 16 + 16 of each tile -- the positions store_chunk writes -- and the 16
-// threads of a row are consecutive lanes of one wave.  In the mixer variant the
-// (cos, sin) table's LDS holds the convolution taps and three raw rows before
-// the chunk (the halo); the rotations compute their table entries on the fly.
-constexpr int kMixHead = 128;                             // channels per head
-constexpr int kMixTapBytes = 3 * kMixHead * 4 * 4;        // [q, k, v][s][channel]: weight of x_{t-s}
-constexpr int kMixHaloBytes = 3 * 3 * kMixHead * 2;       // [q, k, v][row -3 .. -1][channel] bf16
-constexpr int kMixNormBytes = 3 * kMixHead * 4;           // g_q, g_k, g_o
-
-struct MixLds {
-    int taps, halo, norm;                                 // byte offsets in the workgroup's LDS
-};
-
-__device__ __forceinline__ void bf16x8_to_float(uint4 u, float *x) {
-    const unsigned w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        x[2 * i] = __uint_as_float(w[i] << 16);
-        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
-}
-__device__ __forceinline__ uint4 float_to_bf16x8(const float *y) {
-    __hip_bfloat16 t[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
-    return *reinterpret_cast<const uint4 *>(t);
-}
-// sum over the 16 lanes of one row (the standalone kernels' head reduction)
-__device__ __forceinline__ float mix_row_sum(float s) {
-#pragma unroll
-    for (int o = 1; o < kMixHead / 8; o <<= 1) s += __shfl_xor(s, o);
-    return s;
-}
-
-// Per-segment set-up: taps (zero past the width, reversed so that s indexes
-// x_{t-s}), RMSNorm weights, and the halo of the segment's first chunk (raw rows
-// t0-3 .. t0-1 of the sequence, zero before its start).
-__device__ __forceinline__ void mix_setup(const MfmaArgs &a, const MixLds &L, char *smem, int b, int h, int t0,
-                                          int tid, int nth) {
-    const FwdParams &p = a.p;
-    const MixIn &mx = a.mix;
-    const int K = mx.K;
-    for (int e = tid; e < 3 * kMixHead * 4; e += nth) {
-        const int tensor = e / (kMixHead * 4), s = (e / kMixHead) % 4, ch = e % kMixHead;
-        const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
-        const float w = (W && s < K) ? W[((size_t)h * kMixHead + ch) * K + (K - 1 - s)] : 0.f;
-        lds_at<float>(smem, L.taps)[e] = w;
-    }
-    for (int e = tid; e < 3 * kMixHead; e += nth) {
-        const int which = e / kMixHead, ch = e % kMixHead;
-        const float *g = which == 0 ? mx.gq : (which == 1 ? mx.gk : mx.g_o);
-        lds_at<float>(smem, L.norm)[e] = g ? g[ch] : 1.f;
-    }
-    const int Tb = seq_tokens(p, b);
-    for (int e = tid; e < 3 * 3 * 16; e += nth) {
-        const int tensor = e / 48, hr = (e / 16) % 3, cb = e % 16;
-        const int t = t0 - 3 + hr;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (t >= 0 && t < Tb) {
-            const void *X = tensor == 0 ? p.q : (tensor == 1 ? p.k : p.v);
-            v = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(X) +
-                                                 ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb);
-        }
-        *reinterpret_cast<uint4 *>(smem + L.halo + ((tensor * 3 + hr) * kMixHead + 8 * cb) * 2) = v;
-    }
-}
-
-// ShortConv (+ SiLU) (+ RMSNorm for q, k) of this thread's two rows of one tensor,
-// from the raw tile (rows >= 0) and the halo (rows < 0), as bf16.  Rows past the
-// sequence come out as 0.  tensor 0: q (padded tile), 1: k, 2: v (swizzled).
-template <int CC>
-__device__ __forceinline__ void mix_conv_rows(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int tensor,
-                                              int tid, int live0, int live1, uint4 *outv) {
-    const MixIn &mx = a.mix;
-    // opaque per call: the addresses below are formed here, not held across the chunk loop
-    const int tq = opq(tid);
-    const int cb = tq & 15, r0 = tq >> 4;
-    const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
-    const bool conv = W != nullptr;
-    const float *g = tensor == 0 ? mx.gq : (tensor == 1 ? mx.gk : nullptr);
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-        const int r = r0 + 16 * it;
-        // x_{t-s} for s = 0 .. 3 in the standalone kernel's order of products
-        float y[8];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if (s > 0 && !conv) break;                     // uniform: only x_t is used
-            const int rr = r - s;
-            uint4 u;
-            if (rr >= 0) {
-                const int off = tensor == 0 ? 2 * (rr * QS + 8 * cb) : 2 * swz_elem(rr, 8 * cb);
-                u = *reinterpret_cast<const uint4 *>(smem + tile + off);
-            } else {
-                u = *reinterpret_cast<const uint4 *>(smem + L.halo + ((tensor * 3 + rr + 3) * kMixHead + 8 * cb) * 2);
-            }
-            float x[8];
-            bf16x8_to_float(u, x);
-            if (!conv) {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) y[i] = x[i];
-            } else {
-                const float *tp = lds_at<float>(smem, L.taps + ((tensor * 4 + s) * kMixHead + 8 * cb) * 4);
-                const float4 w0 = *reinterpret_cast<const float4 *>(tp);
-                const float4 w1 = *reinterpret_cast<const float4 *>(tp + 4);
-                const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-#pragma unroll
-                for (int i = 0; i < 8; ++i) y[i] = fmaf(wv[i], x[i], s == 0 ? 0.f : y[i]);
-            }
-        }
-        if (mx.act)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) y[i] = y[i] * mix_sigm(y[i]);
-        if (g) {
-            float ss = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) ss = fmaf(y[i], y[i], ss);
-            const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
-            const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb) * 4);
-            const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (tensor * kMixHead + 8 * cb + 4) * 4);
-            const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-#pragma unroll
-            for (int i = 0; i < 8; ++i) y[i] *= rn * gr[i];
-        }
-        if (!(it == 0 ? live0 : live1))
-#pragma unroll
-            for (int i = 0; i < 8; ++i) y[i] = 0.f;
-        outv[it] = float_to_bf16x8(y);
-    }
-}
-
-// The (cos, sin) table entry of pair q*4 + jj for a token (its builder record
-// rec), computed exactly as build_writes_swz computes it.
-__device__ __forceinline__ half2v mix_cs_entry(float4 rec, int q, int jj, int J) {
-    const float u = rec.y, c1 = rec.z, s1 = rec.w;
-    float sn, cs;
-    sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
-#pragma unroll
-    for (int k = 0; k < 3; ++k) {
-        if (k >= jj) break;
-        const float nc = cs * c1 - sn * s1;
-        const float ns = sn * c1 + cs * s1;
-        cs = nc;
-        sn = ns;
-    }
-    const int j = 4 * q + 1 + jj;
-    const bool live = j <= J && j <= 63;
-    const float cv = live ? cs : 0.f;
-    const float sv = live ? sn : 0.f;
-    half2v e;
-    e[0] = (_Float16)(j == 64 ? 1.f : cv);
-    e[1] = (_Float16)sv;
-    return e;
-}
-
-// Epilogue of one chunk: out = RMSNorm(o) g_o sigmoid(gate) for this thread's
-// rows of the staged output tile (padded, in the Q tile's place).
-template <int CC>
-__device__ __forceinline__ void mix_epilogue(const MfmaArgs &a, const MixLds &L, char *smem, int tile, int b, int h,
-                                             int t0, int Tb, int tid, const uint4 *gpf) {
-    const FwdParams &p = a.p;
-    const MixIn &mx = a.mix;
-    const int tq = opq(tid);
-    const int cb = tq & 15, r0 = tq >> 4;
-    const float4 g0 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb) * 4);
-    const float4 g1 = *reinterpret_cast<const float4 *>(smem + L.norm + (2 * kMixHead + 8 * cb + 4) * 4);
-    const float gr[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-    __bf16 *out = static_cast<__bf16 *>(p.o);
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-        const int r = r0 + 16 * it, t = t0 + r;
-        const bool live = t < Tb;
-        float yt[8], gt[8];
-        if (live) {
-            bf16x8_to_float(*reinterpret_cast<const uint4 *>(smem + tile + 2 * (r * QS + 8 * cb)), yt);
-            if (mx.gate) bf16x8_to_float(gpf[it], gt);
-        } else {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) yt[i] = 0.f;
-        }
-        float ss = 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) ss = fmaf(yt[i], yt[i], ss);
-        const float rn = rsqrtf(mix_row_sum(ss) / (float)kMixHead + mx.eps);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            float v = yt[i] * rn * gr[i];
-            if (mx.gate && live) v *= mix_sigm(gt[i]);
-            yt[i] = live ? v : 0.f;
-        }
-        if (t < p.T)
-            *reinterpret_cast<uint4 *>(out + ((seq_row0(p, b) + t) * p.H + h) * kMixHead + 8 * cb) =
-                float_to_bf16x8(yt);
-    }
-}
-
-// Gate rows of this thread for a chunk (zero past the sequence), loaded during the
-// chunk so that its epilogue does not wait for them.
-__device__ __forceinline__ void mix_load_gate(const MfmaArgs &a, int b, int h, int t0, int Tb, int tid, uint4 *gpf) {
-    const FwdParams &p = a.p;
-    const int tq = opq(tid);
-    const int cb = tq & 15, r0 = tq >> 4;
-    const int avail = Tb - t0;
-    gpf[0] = make_uint4(0, 0, 0, 0);
-    gpf[1] = gpf[0];
-    if (!a.mix.gate || avail <= 0) return;                 // uniform
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-        const int r = min(r0 + 16 * it, avail - 1);        // rows past the sequence re-read its last
-        gpf[it] = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.mix.gate) +
-                                                   ((seq_row0(p, b) + t0 + r) * p.H + h) * kMixHead + 8 * cb);
-    }
-}
-
 // ---- 3. fused chunk forward, 32-token chunks ------------------------------------
 // Two workgroups share a compute unit; the readout matrix sits in LDS and the
 // next chunk is prefetched into registers.
@@ -857,12 +906,10 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             // the staged rows are raw projections: ShortConv, RMSNorm, then the
             // operator's q, k, v replace them (one more barrier: the convolution
             // reads three rows above each row)
-            const int r0 = tid >> 4;
-            const bool live0 = t0 + r0 < Tb, live1 = t0 + r0 + 16 < Tb;
             uint4 fq[2], fk[2], fv[2];
-            mix_conv_rows<CC>(a, ML, smem, Ly::Q, 0, tid, live0, live1, fq);
-            mix_conv_rows<CC>(a, ML, smem, Ly::K, 1, tid, live0, live1, fk);
-            mix_conv_rows<CC>(a, ML, smem, Ly::V, 2, tid, live0, live1, fv);
+            mix_conv_rows<CC>(a, ML, smem, Ly::Q, 0, tid, t0, Tb, fq);
+            mix_conv_rows<CC>(a, ML, smem, Ly::K, 1, tid, t0, Tb, fk);
+            mix_conv_rows<CC>(a, ML, smem, Ly::V, 2, tid, t0, Tb, fv);
             lds_barrier();
             const int tq = opq(tid);
             const int cb = tq & 15, rq = tq >> 4;
@@ -1271,14 +1318,20 @@ hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_s
         // the last is full, and the last one is not pre-passed.  Extra blocks of
         // the same launch form the bf16 readout matrix, 32 rows each.
         const int nblk = BHv * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows);
+        const bool mix = a.mix.z_delta != nullptr;
         if (CC == 32 && a.cps % 2 == 0) {
             MfmaArgs a64 = a;
             a64.chunk = 64;
             a64.cps = a.cps / 2;
             a64.nchunks = (a.p.T + 63) / 64;
-            hipLaunchKernelGGL(segment_state_kernel<64>, dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
+            if (mix)
+                hipLaunchKernelGGL((segment_state_kernel<64, true>), dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
+            else
+                hipLaunchKernelGGL((segment_state_kernel<64, false>), dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
+        } else if (mix) {
+            hipLaunchKernelGGL((segment_state_kernel<CC, true>), dim3(nblk), dim3(NT), 0, st, a, mz_scale);
         } else {
-            hipLaunchKernelGGL(segment_state_kernel<CC>, dim3(nblk), dim3(NT), 0, st, a, mz_scale);
+            hipLaunchKernelGGL((segment_state_kernel<CC, false>), dim3(nblk), dim3(NT), 0, st, a, mz_scale);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
@@ -1332,7 +1385,6 @@ int mfma_auto_segments(const FwdParams &p) {
 hipError_t launch_fwd_mfma(const FwdParams &p, int P, void *ws, hipStream_t st,
                            hipEvent_t ev_start, hipEvent_t ev_stop, const MixIn *mix) {
     char *base = static_cast<char *>(ws);
-    if (mix) P = 1;
     const WsLayout L = ws_layout(p, P);
     const int C = kMfmaChunk;
     MfmaArgs a{};

@@ -15,8 +15,10 @@ alone with HIP events the library records on its launch stream), ``mfma``
 fp64 CPU oracle timed on a bounded sample of the same workload on this host),
 ``decode`` (the single-token decode step at 256 streams x 16 heads),
 ``backward`` (cyfa_backward on the same workload), ``mixer`` (the mixer
-prologue and epilogue kernels at the same shape) and ``paper_op`` (the forward
-at the paper's operator-benchmark shape, B 32, T 2048, H 4, d 256).
+prologue and epilogue kernels at the same shape), ``layer`` (prologue, forward
+and epilogue as three calls against the layer forward cyfa_forward_mixer) and
+``paper_op`` (the forward at the paper's operator-benchmark shape, B 32, T 2048,
+H 4, d 256).
 """
 from __future__ import annotations
 
@@ -356,6 +358,65 @@ def mixer_bench(args, torch, cyfa, w):
     return res
 
 
+def layer_bench(args, torch, cyfa, w):
+    """The operator with its mixer at the benchmark workload's shape (ShortConv width
+    4, QK RMSNorm, all gates, output RMSNorm and gate; synthetic weights): the three
+    standalone calls (cyfa_mixer_prologue -> cyfa_forward -> cyfa_mixer_epilogue)
+    against the layer forward cyfa_forward_mixer, which produces the same bits in
+    one pass (``fused``: ShortConv in its own streaming kernel, then one forward
+    with the gates and the epilogue in its staging; ``fused_conv``: the ShortConv in
+    the forward kernels' staging too).  HIP events around 100 launches of each,
+    after 30 warm-up launches."""
+    dev = torch.device("cuda:0")
+    B, T, H, d = w.B, w.T, w.H, w.dk
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    rnd = lambda *s, dt=torch.float32: torch.randn(s, device=dev, generator=g).to(dt)  # noqa: E731
+    bf = torch.bfloat16
+    q, k, v, gate = (rnd(B, T, H, d, dt=bf) for _ in range(4))
+    wq, wk, wv = (0.5 * rnd(H * d, 4) for _ in range(3))
+    nq, nk, no = (rnd(d) * 0.1 + 1 for _ in range(3))
+    zd, za, zb = (rnd(B, T, H) for _ in range(3))
+    bd, ba, A = rnd(H), rnd(H) + 2, (rnd(H) - 1).exp()
+    R = torch.eye(w.m, device=dev).expand(H, w.m, w.m).contiguous() + 0.1 * rnd(H, w.m, w.m)
+    scale = d ** -0.5
+    desc = cyfa.forward_desc(B, T, H, d, d, m=w.m, scale=scale, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
+    ws = torch.empty(cyfa.forward_workspace_size(desc), dtype=torch.uint8, device=dev)
+    o = torch.empty((B, T, H, d), dtype=bf, device=dev)
+    out_c = torch.empty_like(o)
+    out_f = torch.empty_like(o)
+
+    def chain():
+        pro = cyfa.mixer_prologue(q, k, v, conv_q=wq, conv_k=wk, conv_v=wv, norm_q=nq, norm_k=nk, z_delta=zd,
+                                  b_delta=bd, z_alpha=za, b_alpha=ba, A=A, z_beta=zb)
+        cyfa.forward(pro["q"], pro["k"], pro["v"], pro["delta"], pro["log_alpha"], pro["beta"], R, scale=scale,
+                     m=w.m, kernel=cyfa.KERNEL_MFMA, out=o, workspace=ws)
+        cyfa.mixer_epilogue(o, gate, no, out=out_c)
+
+    def fused(fuse_conv):
+        return lambda: cyfa.forward_mixer(q, k, v, zd, conv_q=wq, conv_k=wk, conv_v=wv, norm_q=nq, norm_k=nk,
+                                          b_delta=bd, z_alpha=za, b_alpha=ba, A=A, z_beta=zb, gate=gate,
+                                          norm_o=no, R=R, scale=scale, m=w.m, out=out_f, fuse_conv=fuse_conv)
+
+    res = {"workload": w.name}
+    for name, fn in (("chain", chain), ("fused_conv", fused(1)), ("fused", fused(0))):
+        for _ in range(30):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        n = 100
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[f"{name}_ms"] = e0.elapsed_time(e1) / n
+    res["same_bits"] = bool(torch.equal(out_c, out_f))
+    res["fused_tokens_per_s"] = B * T / (res["fused_ms"] * 1e-3)
+    del ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def paper_op_bench(args, torch, cyfa):
     """The forward at the paper's own operator-benchmark shape (B 32, T 2048, H 4,
     d_k = d_v = 256, bf16), automatic kernel and segments, fused kernel timed
@@ -419,6 +480,7 @@ def main():
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-mixer", action="store_true")
     ap.add_argument("--no-paper-op", action="store_true")
+    ap.add_argument("--no-layer", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -469,6 +531,8 @@ def main():
         extra["backward"] = {"skipped": "cyfa_backward supports head dims 64 and 128"}
     if not args.no_mixer:
         extra["mixer"] = mixer_bench(args, torch, cyfa, w)
+    if not args.no_layer and w.dk == 128 and w.dv == 128 and w.dtype == "bf16":
+        extra["layer"] = layer_bench(args, torch, cyfa, w)
 
     fb = forward_bench(args, torch, cyfa, w, prepared)
     del prepared

@@ -318,6 +318,10 @@ typedef struct {
     int32_t conv_size;               /* 1..4 */
     int32_t conv_act;                /* 0 or 1 (SiLU) */
     float eps;                       /* RMSNorm epsilon (> 0) */
+    int32_t fuse_conv;               /* 1: ShortConv and QK RMSNorm run in the forward
+                                        kernels' chunk staging too; 0: in a streaming
+                                        kernel first, into the workspace (faster at the
+                                        1.4B-layer shape) */
     const float *conv_q, *conv_k, *conv_v;   /* [H*d, conv_size] or NULL */
     const float *norm_q, *norm_k;    /* [d] or NULL */
     const float *z_delta, *b_delta;  /* [B, T, H], [H] (b may be NULL) */
@@ -328,13 +332,14 @@ typedef struct {
 } cyfa_mixer_weights;
 
 /*
- * Layer forward: cyfa_mixer_prologue -> cyfa_forward -> cyfa_mixer_epilogue in
- * one pass over the sequence (Sec. 4, network design, around the operator of
- * Sec. 3.3, Eq. cyfa-two-pass).  The ShortConv, the QK RMSNorm and the gate
- * activations run in the matrix-core kernel's chunk staging, and the output
- * RMSNorm and gate on its output tile, so the operator's q, k, v, gates and o
- * never go to memory; the arithmetic is the standalone kernels', and `out` is
- * bit-identical to the three calls in sequence.
+ * Layer forward: cyfa_mixer_prologue -> cyfa_forward -> cyfa_mixer_epilogue
+ * (Sec. 4, network design, around the operator of Sec. 3.3, Eq. cyfa-two-pass)
+ * with the matrix-core kernels doing the mixer's work in their chunk staging: the
+ * gate activations from their projections and the output RMSNorm and gate on the
+ * output tile always, the ShortConv and QK RMSNorm too with mw->fuse_conv = 1, so
+ * the operator's gates and o (and with fuse_conv its q, k, v) never go to memory.
+ * The arithmetic is the standalone kernels', and `out` is bit-identical to the
+ * three calls in sequence.
  *   desc       as for cyfa_forward; BF16, d_k = d_v = 128, m <= 127 (the
  *              matrix-core kernel); desc->kernel AUTO or MFMA
  *   mw         mixer weights and gate inputs (above)
@@ -342,9 +347,12 @@ typedef struct {
  *   lens       [B] int32 or NULL, as for cyfa_forward_lens (rows t >= lens[b]
  *              of `out` are written as 0, as the epilogue writes them)
  *   out        [B, T, H, 128] bf16 layer output (must not alias an input)
- *   R, K0, V0, clock0, K_out, V_out, clock_out, logits_out, workspace (size from
- *              cyfa_forward_workspace_size(desc)), stream: as for cyfa_forward.
+ *   workspace  cyfa_forward_mixer_workspace_size(desc, mw) bytes, 256-byte aligned
+ *   R, K0, V0, clock0, K_out, V_out, clock_out, logits_out, stream: as for
+ *              cyfa_forward.
  */
+cyfa_status cyfa_forward_mixer_workspace_size(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw,
+                                              size_t *bytes);
 cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw,
                                const void *q_in, const void *k_in, const void *v_in,
                                const float *R, const int32_t *lens,

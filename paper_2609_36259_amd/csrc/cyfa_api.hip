@@ -212,6 +212,13 @@ cyfa_status check_mixer(const cyfa_mixer_desc *d) {
     return CYFA_OK;
 }
 
+// workspace of the layer forward beyond the forward's: the prologue's q, k, v when the
+// ShortConv runs in its own kernel
+size_t mixer_qkv_bytes(const cyfa_fwd_desc *d, const cyfa_mixer_weights *mw) {
+    if (mw->fuse_conv) return 0;
+    return 3 * round_up((size_t)d->B * d->T * d->H * 128 * 2);
+}
+
 cyfa::MixParams mixer_params(const cyfa_mixer_desc *d) {
     cyfa::MixParams p{};
     p.B = d->B; p.T = d->T; p.H = d->H; p.dk = d->d_k; p.dv = d->d_v;
@@ -320,6 +327,18 @@ cyfa_status cyfa_forward_lens(const cyfa_fwd_desc *desc, const void *q, const vo
                         V_out, clock_out, logits_out, workspace, workspace_bytes, stream);
 }
 
+cyfa_status cyfa_forward_mixer_workspace_size(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw,
+                                              size_t *bytes) {
+    if (!desc || !mw || !bytes) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc, mw and bytes are required");
+    cyfa_fwd_desc d2 = *desc;
+    d2.kernel = CYFA_KERNEL_MFMA;
+    FwdPlan plan;
+    cyfa_status st = plan_forward(&d2, &plan);
+    if (st != CYFA_OK) return st;
+    *bytes = plan.ws_bytes + mixer_qkv_bytes(desc, mw);
+    return ok();
+}
+
 cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weights *mw, const void *q_in,
                                const void *k_in, const void *v_in, const float *R, const int32_t *lens,
                                const float *K0, const float *V0, const double *clock0, void *out,
@@ -333,6 +352,7 @@ cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weigh
     if (mw->conv_size < 1 || mw->conv_size > cyfa::kMixMaxConv)
         return fail(CYFA_ERR_UNSUPPORTED, "conv_size must be in [1, %d]", cyfa::kMixMaxConv);
     if (mw->conv_act != 0 && mw->conv_act != 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "conv_act must be 0 or 1");
+    if (mw->fuse_conv != 0 && mw->fuse_conv != 1) return fail(CYFA_ERR_INVALID_ARGUMENT, "fuse_conv must be 0 or 1");
     if (!(mw->eps > 0.f) || !std::isfinite(mw->eps)) return fail(CYFA_ERR_INVALID_ARGUMENT, "eps must be > 0");
     if (desc->T > 0 && !mw->z_delta) return fail(CYFA_ERR_INVALID_ARGUMENT, "z_delta is required");
     if (mw->z_alpha && !mw->A) return fail(CYFA_ERR_INVALID_ARGUMENT, "A is required with z_alpha");
@@ -346,15 +366,42 @@ cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weigh
         for (const void *in : ins)
             if (out && in == out) return fail(CYFA_ERR_INVALID_ARGUMENT, "out must not alias an input");
     }
+    cyfa_fwd_desc d2 = *desc;
+    d2.kernel = CYFA_KERNEL_MFMA;
+    FwdPlan plan;
+    cyfa_status st = plan_forward(&d2, &plan);
+    if (st != CYFA_OK) return st;
+    const size_t need = plan.ws_bytes + mixer_qkv_bytes(desc, mw);
+    if (!workspace || workspace_bytes < need)
+        return fail(CYFA_ERR_WORKSPACE, "workspace of %zu bytes required (got %zu)", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, kWsAlign)) return fail(CYFA_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+    if (desc->T > 0 && (!q_in || !k_in || !v_in || !out))
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "q_in, k_in, v_in and out are required");
     cyfa::MixIn mix{};
     mix.wq = mw->conv_q; mix.wk = mw->conv_k; mix.wv = mw->conv_v; mix.gq = mw->norm_q; mix.gk = mw->norm_k;
     mix.z_delta = mw->z_delta; mix.b_delta = mw->b_delta; mix.z_alpha = mw->z_alpha; mix.b_alpha = mw->b_alpha;
     mix.A = mw->A; mix.z_beta = mw->z_beta; mix.gate = mw->gate; mix.g_o = mw->norm_o;
-    mix.K = mw->conv_size; mix.act = mw->conv_act; mix.eps = mw->eps;
-    cyfa_fwd_desc d2 = *desc;
-    d2.kernel = CYFA_KERNEL_MFMA;
-    return forward_impl(&d2, q_in, k_in, v_in, nullptr, nullptr, nullptr, R, lens, nullptr, K0, V0, clock0, out,
-                        K_out, V_out, clock_out, logits_out, workspace, workspace_bytes, stream, &mix);
+    mix.K = mw->conv_size; mix.act = mw->conv_act; mix.eps = mw->eps; mix.fuse_conv = mw->fuse_conv;
+    const void *q = q_in, *k = k_in, *v = v_in;
+    if (!mw->fuse_conv && desc->T > 0) {
+        // ShortConv and QK RMSNorm in the streaming kernel, into the workspace past the
+        // forward's own part
+        char *buf = static_cast<char *>(workspace) + plan.ws_bytes;
+        const size_t one = mixer_qkv_bytes(desc, mw) / 3;
+        cyfa::MixParams mp{};
+        mp.B = desc->B; mp.T = desc->T; mp.H = desc->H; mp.dk = 128; mp.dv = 128;
+        mp.K = mw->conv_size; mp.act = mw->conv_act; mp.eps = mw->eps; mp.dtype = CYFA_BF16;
+        mp.q_in = q_in; mp.k_in = k_in; mp.v_in = v_in;
+        mp.wq = mw->conv_q; mp.wk = mw->conv_k; mp.wv = mw->conv_v; mp.gq = mw->norm_q; mp.gk = mw->norm_k;
+        mp.lens = lens;
+        mp.q_out = buf; mp.k_out = buf + one; mp.v_out = buf + 2 * one;
+        hipError_t e = cyfa::launch_mixer_prologue(mp, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "mixer prologue launch: %s", hipGetErrorString(e));
+        q = mp.q_out; k = mp.k_out; v = mp.v_out;
+    }
+    return forward_impl(&d2, q, k, v, nullptr, nullptr, nullptr, R, lens, nullptr, K0, V0, clock0, out,
+                        K_out, V_out, clock_out, logits_out, workspace, plan.ws_bytes, stream, &mix);
 }
 
 cyfa_status cyfa_forward_varlen(const cyfa_fwd_desc *desc, const void *q, const void *k, const void *v,

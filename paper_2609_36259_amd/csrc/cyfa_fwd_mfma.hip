@@ -172,12 +172,7 @@ __device__ __forceinline__ void bf16x8_to_float(uint4 u, float *x) {
         x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
     }
 }
-__device__ __forceinline__ uint4 float_to_bf16x8(const float *y) {
-    __hip_bfloat16 t[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
-    return *reinterpret_cast<const uint4 *>(t);
-}
+__device__ __forceinline__ uint4 float_to_bf16x8(const float *y) { return mix_pack_bf16x8(y); }
 // sum over the 16 lanes of one row (the standalone kernels' head reduction)
 __device__ __forceinline__ float mix_row_sum(float s) {
 #pragma unroll
@@ -188,21 +183,23 @@ __device__ __forceinline__ float mix_row_sum(float s) {
 // Per-segment set-up: taps (zero past the width, reversed so that s indexes
 // x_{t-s}), RMSNorm weights, and the halo of the segment's first chunk (raw rows
 // t0-3 .. t0-1 of the sequence, zero before its start).
+template <bool kConv>
 __device__ __forceinline__ void mix_setup(const MfmaArgs &a, const MixLds &L, char *smem, int b, int h, int t0,
                                           int tid, int nth) {
     const FwdParams &p = a.p;
     const MixIn &mx = a.mix;
     const int K = mx.K;
+    for (int e = tid; e < 3 * kMixHead; e += nth) {
+        const int which = e / kMixHead, ch = e % kMixHead;
+        const float *g = which == 0 ? mx.gq : (which == 1 ? mx.gk : mx.g_o);
+        lds_at<float>(smem, L.norm)[e] = g ? g[ch] : 1.f;
+    }
+    if (!kConv) return;
     for (int e = tid; e < 3 * kMixHead * 4; e += nth) {
         const int tensor = e / (kMixHead * 4), s = (e / kMixHead) % 4, ch = e % kMixHead;
         const float *W = tensor == 0 ? mx.wq : (tensor == 1 ? mx.wk : mx.wv);
         const float w = (W && s < K) ? W[((size_t)h * kMixHead + ch) * K + (K - 1 - s)] : 0.f;
         lds_at<float>(smem, L.taps)[e] = w;
-    }
-    for (int e = tid; e < 3 * kMixHead; e += nth) {
-        const int which = e / kMixHead, ch = e % kMixHead;
-        const float *g = which == 0 ? mx.gq : (which == 1 ? mx.gk : mx.g_o);
-        lds_at<float>(smem, L.norm)[e] = g ? g[ch] : 1.f;
     }
     const int Tb = seq_tokens(p, b);
     for (int e = tid; e < 3 * 3 * 16; e += nth) {
@@ -283,8 +280,9 @@ __device__ __forceinline__ void mix_conv_rows(const MfmaArgs &a, const MixLds &L
     }
 }
 
-// The (cos, sin) table entry of pair q*4 + jj for a token (its builder record
-// rec), computed exactly as build_writes_swz computes it.
+// The (cos, sin) table entries of pairs 4q + jj0 and 4q + jj0 + 1 for a token (its
+// builder record rec), computed exactly as build_writes_swz computes them: the
+// start phase of pair 4q, then jj angle-addition steps for entry jj.
 __device__ __forceinline__ half2v mix_cs_entry(float4 rec, int q, int jj, int J) {
     const float u = rec.y, c1 = rec.z, s1 = rec.w;
     float sn, cs;
@@ -305,6 +303,10 @@ __device__ __forceinline__ half2v mix_cs_entry(float4 rec, int q, int jj, int J)
     e[0] = (_Float16)(j == 64 ? 1.f : cv);
     e[1] = (_Float16)sv;
     return e;
+}
+__device__ __forceinline__ void mix_cs_pair(float4 rec, int q, int jj0, int J, half2v &e0, half2v &e1) {
+    e0 = mix_cs_entry(rec, q, jj0, J);
+    e1 = mix_cs_entry(rec, q, jj0 + 1, J);
 }
 
 // Epilogue of one chunk: out = RMSNorm(o) g_o sigmoid(gate) for this thread's
@@ -381,10 +383,11 @@ __device__ __forceinline__ void mix_load_gate(const MfmaArgs &a, int b, int h, i
 // transpose read, double-buffered so that a chunk needs one barrier.  Each wave
 // runs the chunk's clock and decay scans itself (lane = token) and passes the
 // per-token phase and amplitude through a private LDS row.
-// kMix (layer forward, 32-token steps): the staged k and v rows are the raw
-// projections; the mixer's ShortConv and k's RMSNorm turn them into the operator's
-// k and v in LDS first, and the gates come from their projections.
-template <int CC, bool kMix = false>
+// kMix (layer forward): 0 the plain operator; otherwise the gates come from their
+// projections, and with kMix = 1 the staged k and v rows are the raw projections,
+// which the mixer's ShortConv and k's RMSNorm turn into the operator's k and v in
+// LDS first (kMix = 2: k and v are the standalone prologue's).
+template <int CC, int kMix = 0>
 __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float mz_scale) {
     constexpr int STILE = CC * SWS * 2;                // one swizzled K or V tile
     constexpr int KIT = CC * 16 / NT;                  // 16-byte pieces per thread per tensor
@@ -392,7 +395,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     constexpr int SCB = 4 * STILE;                     // per-wave (phase, amplitude) rows
     constexpr int MIX0 = SCB + 4 * 64 * 8 + 4 * 8;     // kMix: taps, halo, RMSNorm weights
     __shared__ __attribute__((aligned(256)))
-    char smem[MIX0 + (kMix ? kMixTapBytes + kMixHaloBytes + kMixNormBytes : 0)];
+    char smem[MIX0 + (kMix == 1 ? kMixTapBytes + kMixHaloBytes + kMixNormBytes : 0)];
     const MixLds ML{MIX0, MIX0 + kMixTapBytes, MIX0 + kMixTapBytes + kMixHaloBytes};
     static_assert(SCB + 4 * 64 * 8 + 4 * 8 >= prep_lds_bytes(kPrepRows), "readout-matrix blocks fit");
     const FwdParams &p = a.p;
@@ -417,7 +420,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     const int c_begin = seg * a.cps, c_end = min(c_begin + a.cps, a.nchunks);
     const int Tb = seq_tokens(p, b);
     const int t_begin = c_begin * CC, t_end = min(c_end * CC, Tb);
-    if constexpr (kMix) mix_setup(a, ML, smem, b, h, t_begin, tid, NT);
+    if constexpr (kMix == 1) mix_setup<true>(a, ML, smem, b, h, t_begin, tid, NT);
     float2 *scw = lds_at<float2>(smem, SCB + w * 64 * 8);
     double *red = lds_at<double>(smem, SCB + 4 * 64 * 8);
 
@@ -513,7 +516,7 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
         }
         if (c + 1 < c_end) load(c + 1);
         lds_barrier();
-        if constexpr (kMix) {
+        if constexpr (kMix == 1) {
             // raw rows -> the operator's k and v (ShortConv, k's RMSNorm), in place; the
             // raw rows CC-3 .. CC-1 become the next chunk's halo
             uint4 fk[KIT], fv[KIT];
@@ -798,17 +801,21 @@ __device__ __forceinline__ bf16x8 decay_rows(bf16x8 v, const float *dw) {
 // ---- 3. fused chunk forward, 32-token chunks ------------------------------------
 // Two workgroups share a compute unit; the readout matrix sits in LDS and the
 // next chunk is prefetched into registers.
-// kMix: the layer forward (the mixer prologue in the chunk staging, the
-// epilogue on the output tile; see the mixer pieces above).
-template <int CC, bool kMix>
+// kMix: 0 the plain operator; 1 the layer forward with the mixer prologue in the
+// chunk staging and the epilogue on the output tile; 2 the layer forward after
+// the standalone prologue's ShortConv and RMSNorm (gates and epilogue fused here).
+// See the mixer pieces above.
+template <int CC, int kMix>
 __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     static_assert(CC == 32, "four-wave fused kernel: 32-token chunks");
     using Ly = Lay<CC>;
     constexpr int RB = Ly::RB;
     constexpr int SSC = Ly::SSC;
     static_assert(kMixTapBytes + kMixHaloBytes <= CC * Ly::CSW * 4, "taps and halo fit the table's place");
-    static_assert(!kMix || Ly::BYTES + kMixNormBytes <= 80 * 1024, "two workgroups per compute unit");
-    __shared__ __attribute__((aligned(256))) char smem[Ly::BYTES + (kMix ? kMixNormBytes : 0)];
+    static_assert(Ly::BYTES + kMixNormBytes <= 80 * 1024, "two workgroups per compute unit");
+    constexpr bool kConv = kMix == 1;                // convolution in the staging; the table's
+                                                     // place then holds taps and halo
+    __shared__ __attribute__((aligned(256))) char smem[Ly::BYTES + (kMix != 0 ? kMixNormBytes : 0)];
     const MixLds ML{Ly::CS, Ly::CS + kMixTapBytes, Ly::BYTES};
     const Tiles s = fused_tiles<CC>(smem);
     const FwdParams &p = a.p;
@@ -862,8 +869,8 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
     // (needed by the first stage), then the entering states, which the first
     // chunk's products need only after its staging, scans and temporal writes.
     Prefetch<CC> pf;
-    load_chunk<CC, true, NT, kMix>(p, b, h, c_begin * CC, Tb, tid, pf, &a.mix);
-    if constexpr (kMix) mix_setup(a, ML, smem, b, h, c_begin * CC, tid, NT);
+    load_chunk<CC, true, NT, kMix != 0>(p, b, h, c_begin * CC, Tb, tid, pf, &a.mix);
+    if constexpr (kMix != 0) mix_setup<kConv>(a, ML, smem, b, h, c_begin * CC, tid, NT);
     uint4 gpf[2];                                    // kMix: the chunk's gate rows
     {
         // readout matrix M_h (slot rows, internal basis columns), resident for the segment
@@ -896,13 +903,13 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         const int n = min(CC, Tb - t0);          // <= 0 for chunks past the sequence
         // kMix: the previous chunk's epilogue, from its output tile in Q's place; each
         // thread reads exactly the positions it overwrites next
-        if constexpr (kMix)
+        if constexpr (kMix != 0)
             if (c > c_begin) mix_epilogue<CC>(a, ML, smem, Ly::Q, b, h, t0 - CC, Tb, tid, gpf);
         // -- A: stage the chunk, prefix sums, temporal writes; prefetch the next chunk
         store_chunk<CC, true, NT, true>(s, tid, pf);
         if (w == 0) chunk_scans<CC, NT, CC, true>(s, lane, m, pf, carry, gsum, logf);
         lds_barrier();
-        if constexpr (kMix) {
+        if constexpr (kConv) {
             // the staged rows are raw projections: ShortConv, RMSNorm, then the
             // operator's q, k, v replace them (one more barrier: the convolution
             // reads three rows above each row)
@@ -932,12 +939,12 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             *reinterpret_cast<uint4 *>(smem + Ly::V + offs) = fv[0];
             *reinterpret_cast<uint4 *>(smem + Ly::V + offs1) = fv[1];
         }
-        if (c + 1 < c_end) load_chunk<CC, true, NT, kMix>(p, b, h, t0 + CC, Tb, tid, pf, &a.mix);
+        if (c + 1 < c_end) load_chunk<CC, true, NT, kMix != 0>(p, b, h, t0 + CC, Tb, tid, pf, &a.mix);
         // factor applied to the carried states this chunk, and whether the chunk's
         // decay is factored (the A tile then holds A_dec); uniform: scalar registers
         const float sf = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[0])));
         const bool fac = __builtin_amdgcn_readfirstlane(__float_as_int(s.ctl[2])) != 0;
-        build_writes_swz<CC, !kMix, NT, CSW>(s, s.As, tid, m);
+        build_writes_swz<CC, !kConv, NT, CSW>(s, s.As, tid, m);
         lds_barrier();
         // -- B: key pass.  O' = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A.  With the
         //    tile holding A_dec (rows times the right decay), Gamma_rs = gam_r decw_s
@@ -995,11 +1002,14 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // -- middle step 1: X_r = U(lambda_r) O'_r -> X tile [token][basis] (reuses Q's)
         half2v csx[8];
 #pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4)
+        for (int v4 = 0; v4 < 4; ++v4) {
+            if constexpr (kConv) {
+                mix_cs_pair(s.bw[l32], 4 * w + v4, 2 * hl, (m - 1) >> 1, csx[2 * v4], csx[2 * v4 + 1]);
+            } else {
 #pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2)
-                csx[2 * v4 + k2] = kMix ? mix_cs_entry(s.bw[l32], 4 * w + v4, 2 * hl + k2, (m - 1) >> 1)
-                                        : CSrow[4 * v4 + k2];
+                for (int k2 = 0; k2 < 2; ++k2) csx[2 * v4 + k2] = CSrow[4 * v4 + k2];
+            }
+        }
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
             bf16x4 xv;
@@ -1101,11 +1111,14 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
             // the (cos, sin) pairs are read first: they do not depend on the products
             half2v csy[8];
 #pragma unroll
-            for (int v4 = 0; v4 < 4; ++v4)
+            for (int v4 = 0; v4 < 4; ++v4) {
+                if constexpr (kConv) {
+                    mix_cs_pair(s.bw[l32], 4 * w + v4, 2 * hl, (m - 1) >> 1, csy[2 * v4], csy[2 * v4 + 1]);
+                } else {
 #pragma unroll
-                for (int k2 = 0; k2 < 2; ++k2)
-                    csy[2 * v4 + k2] = kMix ? mix_cs_entry(s.bw[l32], 4 * w + v4, 2 * hl + k2, (m - 1) >> 1)
-                                            : CSrow[4 * v4 + k2];
+                    for (int k2 = 0; k2 < 2; ++k2) csy[2 * v4 + k2] = CSrow[4 * v4 + k2];
+                }
+            }
             f32x16 yacc = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) yacc = mma(lds8_tr(Myt + 16 * ks * SWS, SWS), lds8(Xa + 16 * ks), yacc);
@@ -1134,7 +1147,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) vacc[x][v] *= sf;
         }
-        if constexpr (kMix) mix_load_gate(a, b, h, t0, Tb, tid, gpf);
+        if constexpr (kMix != 0) mix_load_gate(a, b, h, t0, Tb, tid, gpf);
         score_tiles<CC>(s, s.Os, smem, Ly::A, w, lane, fac);
         f32x16 pacc = zero_acc();
 #pragma unroll
@@ -1157,7 +1170,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         // output: lane (token l32, half hl) stores its 16 columns 32w + 4hl + 8 v4 ..
         // as four 8-byte pieces (uniform chunk base plus a 32-bit lane offset); the
         // four waves' pieces of a token row merge in L2
-        if constexpr (kMix) {
+        if constexpr (kMix != 0) {
             // the operator's output tile goes to Q's place (free since the readout) for
             // the epilogue at the start of the next chunk
 #pragma unroll
@@ -1199,7 +1212,7 @@ __global__ __launch_bounds__(NT, 2) void chunk_forward_kernel(MfmaArgs a) {
         }
         lds_barrier();
     }
-    if constexpr (kMix)
+    if constexpr (kMix != 0)
         if (c_end > c_begin) mix_epilogue<CC>(a, ML, smem, Ly::Q, b, h, (c_end - 1) * CC, Tb, tid, gpf);
     if (a.want_final && seg == a.P - 1) {
         scale_states(kacc, vacc, __expf(s.ctl[1]));
@@ -1303,6 +1316,10 @@ WsLayout ws_layout(const FwdParams &p, int P) {
     return L;
 }
 
+// 0: the plain operator; 1, 2: the layer forward with the ShortConv in the
+// staging or before it (the kernels' kMix)
+int mix_mode(const MfmaArgs &a) { return a.mix.z_delta ? (a.mix.fuse_conv ? 1 : 2) : 0; }
+
 // BHv: (virtual) heads of the pre-pass and the scan, B H hv
 template <int CC>
 hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_start,
@@ -1318,20 +1335,22 @@ hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_s
         // the last is full, and the last one is not pre-passed.  Extra blocks of
         // the same launch form the bf16 readout matrix, 32 rows each.
         const int nblk = BHv * (a.P - 1) + a.p.H * (kStoreRows / kPrepRows);
-        const bool mix = a.mix.z_delta != nullptr;
+        const int mode = mix_mode(a);
+        auto pre = [&](auto kern, const MfmaArgs &args) {
+            hipLaunchKernelGGL(kern, dim3(nblk), dim3(NT), 0, st, args, mz_scale);
+        };
         if (CC == 32 && a.cps % 2 == 0) {
             MfmaArgs a64 = a;
             a64.chunk = 64;
             a64.cps = a.cps / 2;
             a64.nchunks = (a.p.T + 63) / 64;
-            if (mix)
-                hipLaunchKernelGGL((segment_state_kernel<64, true>), dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
-            else
-                hipLaunchKernelGGL((segment_state_kernel<64, false>), dim3(nblk), dim3(NT), 0, st, a64, mz_scale);
-        } else if (mix) {
-            hipLaunchKernelGGL((segment_state_kernel<CC, true>), dim3(nblk), dim3(NT), 0, st, a, mz_scale);
+            if (mode == 1) pre(segment_state_kernel<64, 1>, a64);
+            else if (mode == 2) pre(segment_state_kernel<64, 2>, a64);
+            else pre(segment_state_kernel<64, 0>, a64);
         } else {
-            hipLaunchKernelGGL((segment_state_kernel<CC, false>), dim3(nblk), dim3(NT), 0, st, a, mz_scale);
+            if (mode == 1) pre(segment_state_kernel<CC, 1>, a);
+            else if (mode == 2) pre(segment_state_kernel<CC, 2>, a);
+            else pre(segment_state_kernel<CC, 0>, a);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
@@ -1349,12 +1368,13 @@ hipError_t launch_cc(const MfmaArgs &a, int BHv, hipStream_t st, hipEvent_t ev_s
     if (a.nchunks > 0 && a.hv == 2) {
         if ((e = launch_chunk256(a, st, ev_start, ev_stop)) != hipSuccess) return e;
     } else if (a.nchunks > 0) {
-        if (a.mix.z_delta)
-            hipExtLaunchKernelGGL((chunk_forward_kernel<CC, true>), dim3(BHv * a.P), dim3(NT), 0, st, ev_start,
-                                  ev_stop, 0, a);
-        else
-            hipExtLaunchKernelGGL((chunk_forward_kernel<CC, false>), dim3(BHv * a.P), dim3(NT), 0, st, ev_start,
-                                  ev_stop, 0, a);
+        const int mode = mix_mode(a);
+        auto fused = [&](auto kern) {
+            hipExtLaunchKernelGGL(kern, dim3(BHv * a.P), dim3(NT), 0, st, ev_start, ev_stop, 0, a);
+        };
+        if (mode == 1) fused(chunk_forward_kernel<CC, 1>);
+        else if (mode == 2) fused(chunk_forward_kernel<CC, 2>);
+        else fused(chunk_forward_kernel<CC, 0>);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;

@@ -26,7 +26,17 @@ struct MixParams {
 // forget-gate parameterisation); shared by the standalone prologue and the
 // matrix-core forward that runs the prologue inside its chunk staging, so that
 // both produce the same bits.
-__device__ __forceinline__ float mix_sigm(float x) { return 1.f / (1.f + __expf(-x)); }
+// (the reciprocal is the hardware one, within 1 ulp; the fused and the standalone
+// paths both use this function, so they agree bit for bit)
+__device__ __forceinline__ float mix_sigm(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+// fp32 -> bf16, round to nearest even (the hardware conversion)
+__device__ __forceinline__ uint4 mix_pack_bf16x8(const float *y) {
+    typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+    bf16x8_t t;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = (__bf16)y[i];
+    return *reinterpret_cast<const uint4 *>(&t);
+}
 __device__ __forceinline__ float mix_softplus(float x) { return x > 20.f ? x : log1pf(__expf(x)); }
 
 // Mixer inputs of the fused layer forward (cyfa_forward_mixer): the raw
@@ -41,6 +51,8 @@ struct MixIn {
     const float *g_o;               // [128] output RMSNorm weights or NULL (unit)
     int K, act;                     // ShortConv width 1..kMixMaxConv, SiLU after it
     float eps;                      // RMSNorm epsilon
+    int fuse_conv;                  // 1: ShortConv and QK RMSNorm in the forward kernels' staging;
+                                    // 0: q, k, v arrive already through them (standalone prologue)
 };
 
 hipError_t launch_mixer_prologue(const MixParams &p, hipStream_t s);

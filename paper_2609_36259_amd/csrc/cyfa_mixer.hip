@@ -54,10 +54,7 @@ __device__ __forceinline__ void store8(float *p, const float *y) {
     *reinterpret_cast<float4 *>(p + 4) = make_float4(y[4], y[5], y[6], y[7]);
 }
 __device__ __forceinline__ void store8(__hip_bfloat16 *p, const float *y) {
-    __hip_bfloat16 t[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
-    *reinterpret_cast<uint4 *>(p) = *reinterpret_cast<const uint4 *>(t);
+    *reinterpret_cast<uint4 *>(p) = mix_pack_bf16x8(y);            // round to nearest even
 }
 // The same as nontemporal (streaming) stores.  The prologue's outputs are whole
 // 16-byte pieces of consecutive lanes, read back only by a later launch; streaming
@@ -71,10 +68,7 @@ __device__ __forceinline__ void store8_stream(float *p, const float *y) {
     __builtin_nontemporal_store(b, reinterpret_cast<f32x4_nt *>(p + 4));
 }
 __device__ __forceinline__ void store8_stream(__hip_bfloat16 *p, const float *y) {
-    __hip_bfloat16 t[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) t[i] = __float2bfloat16(y[i]);     // round to nearest even
-    const uint4 u = *reinterpret_cast<const uint4 *>(t);
+    const uint4 u = mix_pack_bf16x8(y);                               // round to nearest even
     const u32x4_nt v = {u.x, u.y, u.z, u.w};
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt *>(p));
 }

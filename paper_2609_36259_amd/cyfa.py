@@ -28,7 +28,7 @@ def store_rows(m: int) -> int:
 
 # Every symbol include/cyfa.h declares.
 EXPORTED = ("cyfa_forward_workspace_size", "cyfa_forward", "cyfa_forward_lens", "cyfa_forward_varlen",
-            "cyfa_forward_mixer",
+            "cyfa_forward_mixer", "cyfa_forward_mixer_workspace_size",
             "cyfa_backward_workspace_size", "cyfa_backward", "cyfa_mixer_prologue",
             "cyfa_mixer_epilogue", "cyfa_decode_workspace_size", "cyfa_decode_step",
             "cyfa_decode_step_noalloc", "cyfa_set_timing_events",
@@ -56,7 +56,8 @@ class MixDesc(ctypes.Structure):
 
 
 class MixWeights(ctypes.Structure):
-    _fields_ = [("conv_size", ctypes.c_int32), ("conv_act", ctypes.c_int32), ("eps", ctypes.c_float)] + \
+    _fields_ = [("conv_size", ctypes.c_int32), ("conv_act", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("fuse_conv", ctypes.c_int32)] + \
         [(n, ctypes.c_void_p) for n in ("conv_q", "conv_k", "conv_v", "norm_q", "norm_k", "z_delta", "b_delta",
                                          "z_alpha", "b_alpha", "A", "z_beta", "gate", "norm_o")]
 
@@ -91,6 +92,9 @@ def load() -> ctypes.CDLL:
         lib.cyfa_forward_mixer.argtypes = [ctypes.POINTER(FwdDesc), ctypes.POINTER(MixWeights)] + \
             [_vp] * 14 + [ctypes.c_size_t, _vp]
         lib.cyfa_forward_mixer.restype = ctypes.c_int
+        lib.cyfa_forward_mixer_workspace_size.argtypes = [ctypes.POINTER(FwdDesc), ctypes.POINTER(MixWeights),
+                                                          ctypes.POINTER(ctypes.c_size_t)]
+        lib.cyfa_forward_mixer_workspace_size.restype = ctypes.c_int
         lib.cyfa_backward_workspace_size.argtypes = [ctypes.POINTER(FwdDesc),
                                                      ctypes.POINTER(ctypes.c_size_t)]
         lib.cyfa_backward_workspace_size.restype = ctypes.c_int
@@ -413,8 +417,8 @@ def mixer_epilogue(o, gate=None, norm_o=None, *, lens=None, eps=1e-6, out=None, 
 def forward_mixer(q_in, k_in, v_in, z_delta, *, conv_q=None, conv_k=None, conv_v=None, norm_q=None,
                   norm_k=None, b_delta=None, z_alpha=None, b_alpha=None, A=None, z_beta=None, gate=None,
                   norm_o=None, R=None, scale=None, m=127, segments=0, lens=None, conv_size=4, conv_act=0,
-                  eps=1e-6, K0=None, V0=None, clock0=None, return_state=False, return_logits=False,
-                  out=None, workspace=None, stream=None):
+                  eps=1e-6, fuse_conv=0, K0=None, V0=None, clock0=None, return_state=False,
+                  return_logits=False, out=None, workspace=None, stream=None):
     """Layer forward (cyfa_forward_mixer): mixer prologue, the operator and the mixer
     epilogue in one pass; bf16 q_in, k_in, v_in [B,T,H,128].  Returns ``out``
     [B,T,H,128] bf16, or a dict with ``out`` and the final state / logits as
@@ -440,15 +444,17 @@ def forward_mixer(q_in, k_in, v_in, z_delta, *, conv_q=None, conv_k=None, conv_v
     _need(V0, (B, H, S, d), torch.float32, "V0")
     _need(clock0, (B, H), torch.float64, "clock0")
     desc = forward_desc(B, T, H, d, d, m=m, segments=segments, scale=scale, dtype=BF16, kernel=KERNEL_MFMA)
-    nbytes = forward_workspace_size(desc)
+    mw = MixWeights(conv_size, conv_act, eps, int(fuse_conv),
+                    *[_ptr(t) for t in (conv_q, conv_k, conv_v, norm_q, norm_k, z_delta, b_delta, z_alpha, b_alpha,
+                                        A, z_beta, gate, norm_o)])
+    n = ctypes.c_size_t(0)
+    _check(load().cyfa_forward_mixer_workspace_size(ctypes.byref(desc), ctypes.byref(mw), ctypes.byref(n)))
+    nbytes = n.value
     dev = q_in.device
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     res_out = out if out is not None else torch.empty_like(q_in)
     _need(res_out, (B, T, H, d), q_in.dtype, "out")
-    mw = MixWeights(conv_size, conv_act, eps, *[_ptr(t) for t in (conv_q, conv_k, conv_v, norm_q, norm_k, z_delta,
-                                                                 b_delta, z_alpha, b_alpha, A, z_beta, gate,
-                                                                 norm_o)])
     K_out = V_out = clk = None
     if return_state:
         K_out = torch.empty((B, H, S, d), dtype=torch.float32, device=dev)

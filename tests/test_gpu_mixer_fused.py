@@ -1,7 +1,8 @@
 """GPU parity of the layer forward (cyfa_forward_mixer: mixer prologue, operator and
 mixer epilogue in one pass of the matrix-core kernel).
 
-The fused call runs the standalone kernels' arithmetic in the same order, so its
+The fused call (ShortConv in the staging or in its own streaming kernel,
+``fuse_conv`` 1 or 0) runs the standalone kernels' arithmetic in the same order, so its
 output, final states, clocks and slot logits must be bit-identical to
 cyfa_mixer_prologue -> cyfa_forward -> cyfa_mixer_epilogue on the same inputs and
 segment plan; the layer output is also compared with the chain of the oracles
@@ -67,14 +68,14 @@ def _chain(t, x, segments, act=0, lens=None, K0=None, V0=None, clock0=None, logi
     return out, res
 
 
-def _fused(t, x, segments, act=0, lens=None, K0=None, V0=None, clock0=None, logits=False):
+def _fused(t, x, segments, act=0, lens=None, K0=None, V0=None, clock0=None, logits=False, fuse_conv=0):
     cyfa = _cyfa()
     return cyfa.forward_mixer(t["q"], t["k"], t["v"], t["z_delta"], conv_q=t["wq"], conv_k=t["wk"],
                               conv_v=t["wv"], norm_q=t["gq"], norm_k=t["gk"], b_delta=t["b_delta"],
                               z_alpha=t["z_alpha"], b_alpha=t["b_alpha"], A=t["A"], z_beta=t["z_beta"],
                               gate=t["gate"], norm_o=t["go"], R=t["R"], scale=D ** -0.5, m=x["m"],
                               segments=segments, lens=lens, conv_size=x["K"], conv_act=act, K0=K0, V0=V0,
-                              clock0=clock0, return_state=True, return_logits=logits)
+                              clock0=clock0, return_state=True, return_logits=logits, fuse_conv=fuse_conv)
 
 
 def _assert_same(f, out, res, logits=False):
@@ -88,13 +89,14 @@ def _assert_same(f, out, res, logits=False):
         assert torch.equal(f["logits"], res["logits"])
 
 
+@pytest.mark.parametrize("fuse_conv", [0, 1])
 @pytest.mark.parametrize("segments", [1, 3])
-def test_bit_identical_with_chain_and_oracle(segments):
+def test_bit_identical_with_chain_and_oracle(segments, fuse_conv):
     B, T, H = 2, 32 * 5 + 11, 2
     x = _inputs(B, T, H, 201)
     t = _dev(x)
     out, res = _chain(t, x, segments, logits=True)
-    f = _fused(t, x, segments, logits=True)
+    f = _fused(t, x, segments, logits=True, fuse_conv=fuse_conv)
     _assert_same(f, out, res, logits=True)
     # the layer output against the chained oracles
     ref_pro = mixer.prologue(x["q"], x["k"], x["v"], x["wq"], x["wk"], x["wv"], x["gq"], x["gk"],
@@ -110,9 +112,10 @@ def test_bit_identical_with_chain_and_oracle(segments):
     assert err <= TOL_BF16
 
 
+@pytest.mark.parametrize("fuse_conv", [0, 1])
 @pytest.mark.parametrize("variant", ["no_conv", "no_norm", "no_gates", "width1", "width2_silu", "width3",
                                      "no_out_gate"])
-def test_optional_parts(variant):
+def test_optional_parts(variant, fuse_conv):
     B, T, H = 1, 32 * 3 + 7, 2
     K = {"width1": 1, "width2_silu": 2, "width3": 3}.get(variant, 4)
     x = _inputs(B, T, H, 202, K=K)
@@ -122,12 +125,13 @@ def test_optional_parts(variant):
     t = _dev(x, drop)
     act = 1 if variant == "width2_silu" else 0
     out, res = _chain(t, x, 1, act=act)
-    f = _fused(t, x, 1, act=act)
+    f = _fused(t, x, 1, act=act, fuse_conv=fuse_conv)
     _assert_same(f, out, res)
 
 
+@pytest.mark.parametrize("fuse_conv", [0, 1])
 @pytest.mark.parametrize("segments", [1, 2])
-def test_ragged_and_initial_state(segments):
+def test_ragged_and_initial_state(segments, fuse_conv):
     B, T, H, m = 4, 32 * 4 + 5, 2, 127
     x = _inputs(B, T, H, 203)
     t = _dev(x)
@@ -140,7 +144,7 @@ def test_ragged_and_initial_state(segments):
     K0, V0 = K0.cuda(), V0.cuda()
     c0 = (torch.rand(B, H, generator=g, dtype=torch.float64) * 2 * m).cuda()
     out, res = _chain(t, x, segments, lens=lens, K0=K0, V0=V0, clock0=c0)
-    f = _fused(t, x, segments, lens=lens, K0=K0, V0=V0, clock0=c0)
+    f = _fused(t, x, segments, lens=lens, K0=K0, V0=V0, clock0=c0, fuse_conv=fuse_conv)
     _assert_same(f, out, res)
     assert torch.count_nonzero(f["out"][1]) == 0 and torch.count_nonzero(f["out"][2, 37:]) == 0
 
@@ -152,3 +156,35 @@ def test_rejects_unsupported():
     with pytest.raises(cyfa.CyfaError) as ei:
         cyfa.forward_mixer(q, q, q, z, m=127)
     assert ei.value.status == 2
+
+
+@pytest.mark.parametrize("fuse_conv", [0, 1])
+def test_full_size_bit_identical(fuse_conv):
+    """The 1.4B-layer shape (B 4, T 4096, H 16) in the benchmark's launch
+    configuration (automatic segment count): the layer forward against the three
+    standalone calls, every output element and the final states."""
+    B, T, H = 4, 4096, 16
+    g = torch.Generator(device="cuda")
+    g.manual_seed(205)
+    rnd = lambda *s, dt=torch.float32: torch.randn(s, device="cuda", generator=g).to(dt)  # noqa: E731
+    bf = torch.bfloat16
+    t = dict(q=rnd(B, T, H, D, dt=bf), k=rnd(B, T, H, D, dt=bf), v=rnd(B, T, H, D, dt=bf),
+             gate=rnd(B, T, H, D, dt=bf), wq=0.5 * rnd(H * D, 4), wk=0.5 * rnd(H * D, 4), wv=0.5 * rnd(H * D, 4),
+             gq=1 + 0.1 * rnd(D), gk=1 + 0.1 * rnd(D), go=1 + 0.1 * rnd(D), z_delta=rnd(B, T, H), b_delta=rnd(H),
+             z_alpha=rnd(B, T, H), b_alpha=rnd(H) + 2, A=(rnd(H) - 1).exp(), z_beta=rnd(B, T, H),
+             R=torch.eye(127, device="cuda").expand(H, 127, 127).contiguous() + 0.1 * rnd(H, 127, 127))
+    x = {"K": 4, "m": 127}
+    out, res = _chain(t, x, 0)
+    f = _fused(t, x, 0, fuse_conv=fuse_conv)
+    _assert_same(f, out, res)
+    assert torch.isfinite(f["out"].float()).all()
+
+
+def test_deterministic():
+    B, T, H = 2, 32 * 6 + 3, 2
+    x = _inputs(B, T, H, 206)
+    t = _dev(x)
+    a = _fused(t, x, 3, fuse_conv=1)
+    b = _fused(t, x, 3, fuse_conv=1)
+    torch.cuda.synchronize()
+    assert torch.equal(a["out"], b["out"]) and torch.equal(a["K"], b["K"])

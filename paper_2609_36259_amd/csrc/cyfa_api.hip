@@ -133,6 +133,8 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
 
 struct BwdPlan {
     int groups;
+    int mfma;       // matrix-core backward (32-token chunks) rather than the vector-ALU one
+    int chunk;
     size_t ws_bytes;
 };
 
@@ -154,22 +156,31 @@ cyfa_status plan_backward(const cyfa_fwd_desc *d, BwdPlan *plan) {
                     "backward: m must be odd and in [3, 127] (got %d)", d->m);
     if (d->dtype != CYFA_F32 && d->dtype != CYFA_BF16)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "bad dtype %d", d->dtype);
-    if (d->kernel != CYFA_KERNEL_AUTO && d->kernel != CYFA_KERNEL_VALU)
-        return fail(d->kernel == CYFA_KERNEL_MFMA ? CYFA_ERR_UNSUPPORTED : CYFA_ERR_INVALID_ARGUMENT,
-                    "backward runs the vector-ALU kernels (kernel AUTO or VALU)");
+    if (d->kernel != CYFA_KERNEL_AUTO && d->kernel != CYFA_KERNEL_VALU && d->kernel != CYFA_KERNEL_MFMA)
+        return fail(CYFA_ERR_INVALID_ARGUMENT, "bad kernel %d", d->kernel);
     if (!std::isfinite(d->scale)) return fail(CYFA_ERR_INVALID_ARGUMENT, "scale must be finite");
-    if (d->chunk != 0 && d->chunk != cyfa::kBwdChunk)
-        return fail(CYFA_ERR_UNSUPPORTED, "backward chunk must be 0 or %d (got %d)", cyfa::kBwdChunk,
-                    d->chunk);
+    const bool mfma_ok = d->dtype == CYFA_BF16 && d->d_k == 128 && d->d_v == 128;
+    if (d->kernel == CYFA_KERNEL_MFMA && !mfma_ok)
+        return fail(CYFA_ERR_UNSUPPORTED, "matrix-core backward: BF16 with d_k = d_v = 128");
+    const bool mfma = d->kernel == CYFA_KERNEL_MFMA ||
+                      (d->kernel == CYFA_KERNEL_AUTO && mfma_ok && d->chunk != cyfa::kBwdChunk);
+    const int chunk = mfma ? cyfa::kBwdMfmaChunk : cyfa::kBwdChunk;
+    if (d->chunk != 0 && d->chunk != chunk)
+        return fail(CYFA_ERR_UNSUPPORTED, "backward chunk must be 0 or %d on the %s kernels (got %d)", chunk,
+                    mfma ? "matrix-core" : "vector-ALU", d->chunk);
     if (d->segments < 0 || d->segments > 1024)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "segments must be in [0, 1024]");
-    const int nc = (d->T + cyfa::kBwdChunk - 1) / cyfa::kBwdChunk;
-    int g = d->segments ? d->segments : cyfa::bwd_auto_groups(d->B, d->T, d->H);
+    const int nc = (d->T + chunk - 1) / chunk;
+    int g = d->segments ? d->segments
+                        : (mfma ? cyfa::bwd_mfma_auto_groups(d->B, d->T, d->H) : cyfa::bwd_auto_groups(d->B, d->T, d->H));
     if (g > nc) g = nc;
     if (g < 1) g = 1;
     const int cpg = nc > 0 ? (nc + g - 1) / g : 1;
     plan->groups = nc > 0 ? (nc + cpg - 1) / cpg : 1;
-    plan->ws_bytes = cyfa::bwd_workspace_bytes(d->B, d->T, d->H, d->d_k, d->d_v, plan->groups);
+    plan->mfma = mfma;
+    plan->chunk = chunk;
+    plan->ws_bytes = mfma ? cyfa::bwd_mfma_workspace_bytes(d->B, d->T, d->H, plan->groups)
+                          : cyfa::bwd_workspace_bytes(d->B, d->T, d->H, d->d_k, d->d_v, plan->groups);
     return CYFA_OK;
 }
 
@@ -466,8 +477,8 @@ cyfa_status cyfa_backward(const cyfa_fwd_desc *desc, const void *q, const void *
 
     cyfa::BwdParams p{};
     p.B = desc->B; p.T = desc->T; p.H = desc->H; p.dk = desc->d_k; p.dv = desc->d_v; p.m = desc->m;
-    p.nc = (desc->T + cyfa::kBwdChunk - 1) / cyfa::kBwdChunk;
-    p.Tpad = p.nc * cyfa::kBwdChunk;
+    p.nc = (desc->T + plan.chunk - 1) / plan.chunk;
+    p.Tpad = p.nc * plan.chunk;
     p.groups = plan.groups;
     p.cpg = p.nc > 0 ? (p.nc + plan.groups - 1) / plan.groups : 1;
     p.scale = desc->scale; p.dtype = desc->dtype;
@@ -478,7 +489,7 @@ cyfa_status cyfa_backward(const cyfa_fwd_desc *desc, const void *q, const void *
     p.gdelta = d_delta; p.glog_alpha = d_log_alpha; p.gbeta = d_beta; p.gR = d_R;
     p.gK0 = d_K0; p.gV0 = d_V0; p.gclock0 = d_clock0;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = cyfa::launch_bwd_valu(p, workspace, s);
+    hipError_t e = plan.mfma ? cyfa::launch_bwd_mfma(p, workspace, s) : cyfa::launch_bwd_valu(p, workspace, s);
     if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "backward launch: %s", hipGetErrorString(e));
     return ok();
 }

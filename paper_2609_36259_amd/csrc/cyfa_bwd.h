@@ -5,7 +5,9 @@
 
 namespace cyfa {
 
-constexpr int kBwdChunk = 16;       // tokens per chunk of the backward kernels
+constexpr int kBwdChunk = 16;       // tokens per chunk of the vector-ALU backward kernels
+constexpr int kBwdMfmaChunk = 32;   // tokens per chunk of the matrix-core backward kernels
+constexpr int kBwdFinParts = 8;     // partial sums of the final-state loss per (b, h)
 
 // Gradients of L = sum_t <do_t, o_t> + <dK_T, Kbar_T> + <dV_T, Vbar_T>.
 struct BwdParams {
@@ -60,5 +62,15 @@ hipError_t launch_group_states(const FwdParams &f, int groups, int cpg, void *ws
                                const float **EcV, const double **Eclk, hipStream_t s);
 int bwd_auto_groups(int B, int T, int H);
 hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s);
+// The last two kernels of either backward: reverse cumulative sums of p.dG and
+// p.dlam (plus the final-state loss p.fin at the last token) into dlog_alpha,
+// ddelta, dclock0; dR from the partial dM of every (b, h, group) in p.dMp.
+hipError_t launch_bwd_tail(const BwdParams &p, hipStream_t s);
+
+// Matrix-core backward (bf16, d_k = d_v = 128, m <= 127, 32-token chunks, p.nc and
+// p.Tpad counted in those chunks).
+int bwd_mfma_auto_groups(int B, int T, int H);
+size_t bwd_mfma_workspace_bytes(int B, int T, int H, int groups);
+hipError_t launch_bwd_mfma(BwdParams p, void *ws, hipStream_t s);
 
 }  // namespace cyfa

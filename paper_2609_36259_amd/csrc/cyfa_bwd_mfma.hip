@@ -1,0 +1,1101 @@
+// Matrix-core (bf16 MFMA) backward of the chunk-wise CyFA forward: bf16 inputs,
+// d_k = d_v = 128, m <= 127, 32-token chunks.
+//
+// The gradients are those of the vector-ALU backward (reverse mode of the
+// absolute-clock recurrence and readout, Sec. 3.2 Eqs. cyfa-absolute-recurrence
+// and cyfa-absolute-readout, chunk by chunk as in App. B; the clock increments
+// receive the reverse cumulative sum of the per-token clock gradients, Eq.
+// app-clock-gradient-accumulation; the per-token formulas are written out at
+// the top of cyfa_bwd_valu.hip).  Here every dense product runs on bf16
+// matrix-core tiles with fp32 accumulation, and the states stay in MFMA
+// accumulators while a workgroup walks its chunk group:
+//   (1) fwd_contrib_kernel (b, h, group): the group's own contribution to the
+//       states at its end (zero entering state), the clock entering the group
+//       and the group's total log decay.
+//   (2) fwd_combine_kernel (b, h): the states entering every group, in group
+//       order from (K0, V0), and the final-state loss <dK_T, Kbar_T> + <dV_T, Vbar_T>.
+//   (3) readout_kernel (b, h, group): walks the group's chunks forward with both
+//       states in accumulators, recomputes the key pass p, X, the slot weights W
+//       and u, and forms du, the readout's adjoint (dY, dW, dZ, dX, dp), dq, the
+//       group's part of dM, <q, dq> + <u, du> and the clock gradients of X and u.
+//       u and dp go to the workspace in bf16 for (4) and (6).
+//   (4) adj_contrib_kernel (b, h, group): the group's own contribution to the
+//       adjoint states entering it from its tokens (zero adjoint at its end).
+//   (5) adj_combine_kernel (b, h): the adjoint states at every group's end, in
+//       reverse group order from (dK_T, dV_T); dK0 and dV0.
+//   (6) grad_kernel (b, h, group): walks the group's chunks in reverse with both
+//       adjoint states in accumulators: dk, dv, da and from da the gradient of
+//       beta and the clock gradient of the write a_t, and dL/dG.
+// The reverse cumulative sums (dlog_alpha, ddelta, dclock0) and dR = dM Phi^T
+// are the vector-ALU backward's last two kernels (launch_bwd_tail).
+//
+// Within a chunk (token rows r, s; G_r the chunk-local inclusive sum of log
+// alpha; gamma_r = exp(G_r); rho_s = exp(G_C - G_s); Gamma_rs = exp(G_r - G_s)
+// for s <= r, else 0; Kbar, Vbar the states entering the chunk; DK', DV' the
+// adjoint states at its end):
+//   p  = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A      du = gamma (.) dO Vbar^T + (dO V^T (.) Gamma) A
+//   dq = gamma (.) dP Kbar  + (dP A^T (.) Gamma) K
+//   dk = rho (.) A DK' + (dP A^T (.) Gamma)^T Q         dv = rho (.) A DV' + (U A^T (.) Gamma)^T dO
+//   da = rho (.) (K DK'^T + V DV'^T) + (Q K^T (.) Gamma)^T dP + (dO V^T (.) Gamma)^T U
+//   Kbar <- exp(G_C) Kbar + (rho (.) A)^T K,   DK'_prev = exp(G_C) DK' + (gamma (.) dP)^T Q
+// (Vbar, DV' likewise with V and (gamma (.) U)^T dO).
+//
+// Basis order inside: the matrix-core kernels' internal order (pair j at
+// (2j-2, 2j-1), DC at 126, padding 127), so a rotation acts on two consecutive
+// accumulator registers of one lane.  The ABI's state arrays (paper order) are
+// converted where they are read or written; dM leaves in paper column order.
+//
+// State accumulators, four per wave (x = 0..3): wave w holds basis rows
+// i = 32 w + lane % 32 and columns c = 32 x + 8 (v / 4) + 4 (lane / 32) + v % 4 of
+// a 128 x 128 state in register v, i.e. the transposed product D[c][i]; the key
+// and the value state (and their adjoints) alike.  Fed back as an A operand
+// (acc_to_operand) it supplies rows i and the permuted k indices c (the other
+// operand is then read with lds8_perm).  The workspace copies use the same
+// lane-major dump layout (dump_off).
+#include "cyfa_bwd.h"
+#include "cyfa_mfma_common.h"
+#include "cyfa_prep.h"
+
+namespace cyfa {
+
+using namespace mfma;
+
+namespace {
+
+constexpr int kC = kBwdMfmaChunk;   // tokens per chunk
+constexpr int kNT = 256;            // threads per workgroup (four waves)
+constexpr int kT32 = kC * QS * 2;   // bytes of a padded [32][128] bf16 tile
+constexpr int kT128 = 128 * QS * 2; // bytes of a padded [128][128] bf16 tile
+constexpr int SSB = 40;             // row stride (bf16) of a [32][32] score tile
+constexpr int kTS = kC * SSB * 2;   // bytes of a score tile
+constexpr int kSE = 128 * 128;      // floats of one 128 x 128 state
+constexpr int kCombBlocks = kBwdFinParts;
+constexpr float kTwoPi = 6.283185307179586f;
+
+struct Args {
+    BwdParams p;        // shapes, inputs and outputs; nc / Tpad count 32-token chunks;
+                        // p.udu, p.dlam, p.dG, p.dMp, p.fin as for the shared last kernels
+    const __bf16 *Mz;   // [H][128][128] readout matrix times zs = scale log2 e (internal columns)
+    float *Ef;          // [BH][G][2][kSE] forward states: group contributions, then entering states
+    float *Ea;          // [BH][G][2][kSE] adjoint states: group contributions, then the adjoints at
+                        // each group's end
+    float *Gg;          // [BH][G] total log decay of each group
+    double *gclk;       // [BH][G] clock entering each group (reduced mod m)
+    double *cclk;       // [BH][nc] clock entering each chunk (reduced mod m)
+    __bf16 *U, *dP;     // [BH][Tpad][128] u_t and dp_t, internal basis order
+};
+
+__device__ __forceinline__ int tokens_of(const BwdParams &p, int b) {
+    return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
+}
+
+// internal basis index -> paper row (a bijection of 0..127; rows i < m-1 and DC are active)
+__device__ __forceinline__ int paper_row(int i) { return i < 126 ? i + 1 : (i == 126 ? 0 : 127); }
+__device__ __forceinline__ bool row_active(int i, int m) { return i < m - 1 || i == 126; }
+
+// element e of the dump layout -> (internal row i, column c)
+__device__ __forceinline__ void dump_coords(int e, int &i, int &c) {
+    const int w = e >> 12, x = (e >> 10) & 3, lane = (e >> 4) & 63, v = e & 15;
+    i = 32 * w + (lane & 31);
+    c = 32 * x + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+__device__ __forceinline__ void load_acc(const float *E, int w, int lane, f32x16 (&acc)[4]) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 f = *reinterpret_cast<const float4 *>(E + dump_off(w, x, lane, 4 * q));
+            acc[x][4 * q] = f.x;
+            acc[x][4 * q + 1] = f.y;
+            acc[x][4 * q + 2] = f.z;
+            acc[x][4 * q + 3] = f.w;
+        }
+}
+__device__ __forceinline__ void store_acc(float *E, int w, int lane, const f32x16 (&acc)[4]) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<float4 *>(E + dump_off(w, x, lane, 4 * q)) =
+                make_float4(acc[x][4 * q], acc[x][4 * q + 1], acc[x][4 * q + 2], acc[x][4 * q + 3]);
+}
+__device__ __forceinline__ void scale_acc(f32x16 (&acc)[4], float f) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[x][v] *= f;
+}
+// accumulators as bf16 rows of a [128][QS] tile: row i, columns c .. c+3 per store
+__device__ __forceinline__ void dump_tile(__bf16 *T, int w, int l32, int h4, const f32x16 (&acc)[4]) {
+    __bf16 *row = T + (32 * w + l32) * QS + h4;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+            bf16x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[x][4 * g4 + e];
+            *reinterpret_cast<bf16x4 *>(row + 32 * x + 8 * g4) = o;
+        }
+}
+
+// A 32 x 32 output block D[m][n] in registers (lane: n = lane % 32; register v:
+// m = 8 (v / 4) + 4 (lane / 32) + v % 4) stored as bf16 rows of a [32][QS] tile
+// at row n, columns col0 + m.
+__device__ __forceinline__ void store_block(__bf16 *T, int l32, int col0, int h4, const f32x16 &acc) {
+    __bf16 *row = T + l32 * QS + col0 + h4;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[4 * g4 + e];
+        *reinterpret_cast<bf16x4 *>(row + 8 * g4) = o;
+    }
+}
+
+// Transposed operand from a padded tile: element [k0 + 8 (lane/32) + p][n0 + lane % 32].
+__device__ __forceinline__ bf16x8 rd_tr(const __bf16 *T, int trl, int k0, int n0) {
+    return lds8_tr(T + trl + k0 * QS + n0, QS);
+}
+// Row operand: element [row][k0 + 8 (lane/32) + p] of a tile with row stride `stride`.
+__device__ __forceinline__ bf16x8 rd_row(const __bf16 *T, int stride, int row, int k0, int hl) {
+    return lds8(T + row * stride + k0 + 8 * hl);
+}
+// The operand's eight k indices k0 + 8 (lane/32) + p scaled by f[p] (f points at entry k0 + 8 (lane/32)).
+__device__ __forceinline__ bf16x8 scale_k(bf16x8 v, const float *f) {
+    const float4 a = *reinterpret_cast<const float4 *>(f);
+    const float4 b = *reinterpret_cast<const float4 *>(f + 4);
+    const float d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    bf16x8 r;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = (__bf16)((float)v[q] * d[q]);
+    return r;
+}
+
+// ---- chunk staging ---------------------------------------------------------
+// 32 rows x 128 bf16 (two 16-byte pieces per thread: rows tid/16 and tid/16 + 16,
+// columns 8 (tid % 16)); rows at or past n read as zero.
+struct Rows2 {
+    uint4 r[2];
+};
+__device__ __forceinline__ void load_rows(const __bf16 *base, size_t row_stride, int n, int tid, Rows2 &o) {
+    const int r0 = tid >> 4, c8 = (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it;
+        o.r[it] = make_uint4(0, 0, 0, 0);
+        if (r < n) o.r[it] = *reinterpret_cast<const uint4 *>(base + (size_t)r * row_stride + c8);
+    }
+}
+__device__ __forceinline__ void store_rows(__bf16 *T, int tid, const Rows2 &o) {
+    const int r0 = tid >> 4, c8 = (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) *reinterpret_cast<uint4 *>(T + (r0 + 16 * it) * QS + c8) = o.r[it];
+}
+
+// Per-token scalars of a chunk (lanes 0..31 of wave 0; zero elsewhere and past the
+// sequence: no shift, no decay, no write).
+struct Tok {
+    float g, dl, be;
+};
+__device__ __forceinline__ void load_tok(const BwdParams &p, int b, int h, int t0, int Tb, int tid, Tok &k) {
+    k.g = 0.f;
+    k.dl = 0.f;
+    k.be = 0.f;
+    const int t = t0 + tid;
+    if (tid < kC && t < Tb) {
+        const size_t si = ((size_t)b * p.T + t) * p.H + h;
+        k.g = p.log_alpha ? p.log_alpha[si] : 0.f;
+        k.dl = p.delta[si];
+        k.be = p.beta ? p.beta[si] : 1.f;
+    }
+}
+
+// Chunk scalars in LDS.
+struct Sc {
+    float G[kC];      // chunk-local inclusive sums of log alpha
+    float gam[kC];    // exp(G_r)
+    float rho[kC];    // exp(G_C - G_r)
+    float urev[kC];   // clock after token r over m, mod 1 (revolutions)
+    float4 bw[kC];    // write-builder record: amplitude, urev, cos and sin of 2 pi urev
+};
+static_assert(sizeof(Sc) == 1024, "scalar block");
+
+// Wave 0: prefix sums of the chunk and the builder records; carry is the clock
+// entering the chunk (reduced), advanced past it.  dec_amp: the write rows carry
+// their right decay rho_r (A_dec).
+__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, bool dec_amp) {
+    const double inv_m = 1.0 / (double)m;
+    const float G = wave_incl_scan(k.g);
+    const double lam = carry + wave_incl_scan((double)k.dl);
+    const float GC = lane63(G);
+    if (lane < kC) {
+        s.G[lane] = G;
+        s.gam[lane] = __expf(G);
+        const float rho = __expf(GC - G);
+        s.rho[lane] = rho;
+        const double q = lam * inv_m;
+        const float u = (float)(q - floor(q));
+        s.urev[lane] = u;
+        float s1, c1;
+        sincos_rev(u, &s1, &c1);
+        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? rho : 1.f), u, c1, s1);
+    }
+    carry = reduce_clock(lane63(lam), (double)m, inv_m);
+}
+
+// Temporal write rows (Eq. app-temporal-writes) into a padded [32][QS] tile:
+// amp_r [cos th_j, -sin th_j] on pair j (internal columns 2j-2, 2j-1), amp_r /
+// sqrt 2 = beta_r / sqrt m on DC (126), 0 on 127.  Thread (row tid/16 + 16 it,
+// q = tid % 16) fills columns 8q .. 8q+7 (pairs 4q+1 .. 4q+4); the phases advance
+// by angle addition from a start reduced in revolutions.
+__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) {
+    const int q = tid & 15, r0 = tid >> 4;
+    const int J = (m - 1) >> 1;
+#pragma unroll 1
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it;
+        const float4 rec = s.bw[r];
+        const float amp = rec.x, u = rec.y, c1 = rec.z, s1 = rec.w;
+        float sn, cs;
+        sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
+        bf16x8 a8;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int j = 4 * q + 1 + jj;
+            const bool live = j <= J;
+            float a0 = live ? amp * cs : 0.f, a1 = live ? -amp * sn : 0.f;
+            if (jj == 3 && q == 15) {
+                a0 = amp * 0.70710678118654752f;
+                a1 = 0.f;
+            }
+            a8[2 * jj] = (__bf16)a0;
+            a8[2 * jj + 1] = (__bf16)a1;
+            if (jj < 3) {
+                const float nc = cs * c1 - sn * s1;
+                const float ns = sn * c1 + cs * s1;
+                cs = nc;
+                sn = ns;
+            }
+        }
+        *reinterpret_cast<bf16x8 *>(T + r * QS + 8 * q) = a8;
+    }
+}
+
+// (cos, sin) of 2 pi j urev for the eight pairs of a lane's 16 rows in wave w's
+// 32-row block: pair e (registers 2e, 2e+1) is internal rows 32w + 8(e/2) + 4hl +
+// 2(e%2) (+1), frequency j = 16w + 4(e/2) + 2hl + e%2 + 1.  Inactive pairs, DC and
+// padding get (1, 0).
+__device__ __forceinline__ int pair_freq(int w, int hl, int e) { return 16 * w + 4 * (e >> 1) + 2 * hl + (e & 1) + 1; }
+__device__ __forceinline__ void lane_phases(float u, int w, int hl, int m, float (&c)[8], float (&s)[8]) {
+    const int J = (m - 1) >> 1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int j = pair_freq(w, hl, e);
+        c[e] = 1.f;
+        s[e] = 0.f;
+        if (j <= J) sincos_rev(__builtin_amdgcn_fractf((float)j * u), &s[e], &c[e]);
+    }
+}
+// acc <- mul U(SIGN lambda) acc on a lane's pairs (U(tau): rotation by +2 pi j tau / m
+// of the (cos, sin) pair); DC and padding are multiplied by mul.
+template <int SIGN>
+__device__ __forceinline__ void rotate(f32x16 &a, const float (&c)[8], const float (&s)[8], float mul) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float x0 = a[2 * e], x1 = a[2 * e + 1];
+        const float sn = SIGN > 0 ? s[e] : -s[e];
+        a[2 * e] = mul * (c[e] * x0 - sn * x1);
+        a[2 * e + 1] = mul * (sn * x0 + c[e] * x1);
+    }
+}
+// Clock-gradient part of Z = U(+-lambda) y over a lane's active pairs:
+// sum_j j (dZ_sin Z_cos - dZ_cos Z_sin); the gradient is +-(2 pi / m) times its
+// sum over all pairs.
+__device__ __forceinline__ float rot_part(const f32x16 &dz, const f32x16 &z, int w, int hl, int m) {
+    const int J = (m - 1) >> 1;
+    float acc = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int j = pair_freq(w, hl, e);
+        if (j <= J) acc = fmaf((float)j, dz[2 * e + 1] * z[2 * e] - dz[2 * e] * z[2 * e + 1], acc);
+    }
+    return acc;
+}
+
+// Masked score tile into S (bf16, [32][SSB]): D[mr][nr] = sum_k Am[mr][k] Bn[nr][k]
+// over 128 columns (lane: nr = lane % 32; registers: mr), times Gamma and stored at
+// S[nr][mr .. mr+3].  kLaneLater: the lane's token nr is the later one (Gamma_{nr,mr},
+// mr <= nr); otherwise mr is (Gamma_{mr,nr}, mr >= nr).
+template <bool kLaneLater>
+__device__ __forceinline__ void score_tile(const __bf16 *Am, const __bf16 *Bn, __bf16 *S, const Sc &sc,
+                                           int l32, int hl) {
+    f32x16 acc = zero_acc();
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) acc = mma(rd_row(Am, QS, l32, 16 * ks, hl), rd_row(Bn, QS, l32, 16 * ks, hl), acc);
+    const float Gn = sc.G[l32];
+    __bf16 *row = S + l32 * SSB + 4 * hl;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int mr = 8 * g4 + 4 * hl + e;
+            const float Gm = sc.G[mr];
+            float val = 0.f;
+            if (kLaneLater ? mr <= l32 : mr >= l32)
+                val = acc[4 * g4 + e] * __expf(kLaneLater ? Gn - Gm : Gm - Gn);
+            o[e] = (__bf16)val;
+        }
+        *reinterpret_cast<bf16x4 *>(row + 8 * g4) = o;
+    }
+}
+
+// Per-token output row: token l32 of the chunk, columns 32w + 4hl + 8 g4 .. +3.
+__device__ __forceinline__ void store_out(__bf16 *dst, const f32x16 &acc, bool live) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)(live ? acc[4 * g4 + e] : 0.f);
+        *reinterpret_cast<bf16x4 *>(dst + 8 * g4) = o;
+    }
+}
+// <row of a bf16 tile, accumulator> over the lane's 16 columns
+__device__ __forceinline__ float dot_row(const __bf16 *row, const f32x16 &acc) {
+    float s = 0.f;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        const bf16x4 x = *reinterpret_cast<const bf16x4 *>(row + 8 * g4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s = fmaf((float)x[e], acc[4 * g4 + e], s);
+    }
+    return s;
+}
+
+// ---------------------------------------------------------------------------
+// (1) group contributions to the forward states and the group's clock entry.
+struct CLay {
+    static constexpr int K = 0, V = kT32, A = 2 * kT32, SC = 3 * kT32, RED = SC + 1024;
+    static constexpr int BYTES = RED + kNT * 8;
+};
+__global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
+    using L = CLay;
+    __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int m = p.m;
+    const int Tb = tokens_of(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    Sc &sc = *lds_at<Sc>(smem, L::SC);
+    __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V), *At = lds_at<__bf16>(smem, L::A);
+    // clock entering the group: clock0 plus every increment before it (double)
+    double carry;
+    {
+        double *red = lds_at<double>(smem, L::RED);
+        const int t_start = min(c_begin * kC, Tb);
+        double ds = 0.0;
+        for (int t = tid; t < t_start; t += kNT) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
+        red[tid] = ds;
+        __syncthreads();
+        for (int s = kNT / 2; s > 0; s >>= 1) {
+            if (tid < s) red[tid] += red[tid + s];
+            __syncthreads();
+        }
+        carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + red[0], (double)m, 1.0 / (double)m);
+        __syncthreads();
+    }
+    if (tid == 0) a.gclk[(size_t)bh * p.groups + g] = carry;
+    const int trl = tr_off(QS, lane);
+    f32x16 kacc[4], vacc[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
+    }
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
+    double gsum = 0.0;
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        {
+            Rows2 rk, rv;
+            const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+            load_rows(kin + base, rs, n, tid, rk);
+            load_rows(vin + base, rs, n, tid, rv);
+            Tok tk;
+            load_tok(p, b, h, t0, Tb, tid, tk);
+            store_rows(Kt, tid, rk);
+            store_rows(Vt, tid, rv);
+            if (w == 0) chunk_scalars(sc, lane, m, tk, carry, true);
+        }
+        lds_barrier();
+        build_A(sc, At, tid, m);
+        lds_barrier();
+        const float gC = sc.gam[kC - 1];
+        gsum += (double)sc.G[kC - 1];
+        scale_acc(kacc, gC);
+        scale_acc(vacc, gC);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 ad = rd_tr(At, trl, 16 * ks, 32 * w);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                kacc[x] = mma(rd_tr(Kt, trl, 16 * ks, 32 * x), ad, kacc[x]);
+                vacc[x] = mma(rd_tr(Vt, trl, 16 * ks, 32 * x), ad, vacc[x]);
+            }
+        }
+        lds_barrier();
+    }
+    float *E = a.Ef + ((size_t)bh * p.groups + g) * 2 * kSE;
+    store_acc(E, w, lane, kacc);
+    store_acc(E + kSE, w, lane, vacc);
+    if (tid == 0) a.Gg[(size_t)bh * p.groups + g] = (float)gsum;
+}
+
+// (2) states entering each group, from (K0, V0) in group order; the final-state
+// loss <dK_T, Kbar_T> + <dV_T, Vbar_T> in kCombBlocks partial sums.
+__global__ __launch_bounds__(kNT) void fwd_combine_kernel(Args a) {
+    __shared__ float red[kNT / 64];
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
+    const float *Gg = a.Gg + (size_t)bh * G;
+    float acc = 0.f;
+    for (int e = blockIdx.y * kNT + tid; e < 2 * kSE; e += kCombBlocks * kNT) {
+        const int st = e / kSE, f = e % kSE;
+        int i, c;
+        dump_coords(f, i, c);
+        const bool act = row_active(i, m);
+        const size_t ai = ((size_t)bh * kStoreRows + paper_row(i)) * 128 + c;
+        const float *init = st ? p.V0 : p.K0;
+        const float *fin = st ? p.dV_T : p.dK_T;
+        float E = (init && act) ? init[ai] : 0.f;
+        for (int q = 0; q < G; ++q) {
+            float *slot = a.Ef + (((size_t)bh * G + q) * 2 + st) * kSE + f;
+            const float own = *slot;
+            *slot = E;
+            E = fmaf(__expf(Gg[q]), E, own);
+        }
+        if (fin && act) acc = fmaf(fin[ai], E, acc);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+    if ((tid & 63) == 0) red[tid >> 6] = acc;
+    __syncthreads();
+    if (tid == 0) p.fin[(size_t)bh * kCombBlocks + blockIdx.y] = red[0] + red[1] + red[2] + red[3];
+}
+
+// ---------------------------------------------------------------------------
+// (3) readout recomputation and its adjoint, per (sequence, chunk group).
+// LDS: padded [32][QS] tiles Q, K, V, dO, A, X, W (later dp), dY (later scale dZ);
+// [128][QS] tiles of the entering key state (bf16) and the readout matrix; three
+// score tiles; chunk scalars; per-token reduction slots.
+struct RLay {
+    static constexpr int Q = 0, K = kT32, V = 2 * kT32, O = 3 * kT32, A = 4 * kT32;
+    static constexpr int X = 5 * kT32, W = 6 * kT32, Y = 7 * kT32;
+    static constexpr int KB = 8 * kT32, MZ = KB + kT128;
+    static constexpr int S1 = MZ + kT128, S2 = S1 + kTS, S3 = S2 + kTS;
+    static constexpr int SC = S3 + kTS;
+    static constexpr int R1 = SC + 1024, R2 = R1 + 4 * kC * 8, R3 = R2 + 4 * kC * 4;
+    static constexpr int BYTES = R3 + 4 * kC * 8;
+    static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
+};
+__global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
+    using L = RLay;
+    __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5, h4 = 4 * hl;
+    const int m = p.m;
+    const int Tb = tokens_of(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    Sc &sc = *lds_at<Sc>(smem, L::SC);
+    __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
+    __bf16 *Ot = lds_at<__bf16>(smem, L::O), *At = lds_at<__bf16>(smem, L::A), *Xt = lds_at<__bf16>(smem, L::X);
+    __bf16 *Wt = lds_at<__bf16>(smem, L::W), *Yt = lds_at<__bf16>(smem, L::Y);
+    __bf16 *KB = lds_at<__bf16>(smem, L::KB), *MZ = lds_at<__bf16>(smem, L::MZ);
+    __bf16 *S1 = lds_at<__bf16>(smem, L::S1), *S2 = lds_at<__bf16>(smem, L::S2), *S3 = lds_at<__bf16>(smem, L::S3);
+    float2 *red1 = lds_at<float2>(smem, L::R1);
+    float *red2 = lds_at<float>(smem, L::R2);
+    float2 *red3 = lds_at<float2>(smem, L::R3);
+    const int trl = tr_off(QS, lane);
+    const float scale = p.scale;
+    const float zs = scale * 1.4426950408889634f;   // the LDS readout matrix is zs M
+    const float inv_zs = 1.f / zs;
+
+    {
+        const __bf16 *Mh = a.Mz + (size_t)h * 128 * 128;
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int e = it * kNT + tid, row = e >> 4, c0 = (e & 15) * 8;
+            *reinterpret_cast<uint4 *>(MZ + row * QS + c0) = *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
+        }
+    }
+    f32x16 kacc[4], vacc[4], macc[4];
+    {
+        const float *E = a.Ef + ((size_t)bh * p.groups + g) * 2 * kSE;
+        load_acc(E, w, lane, kacc);
+        load_acc(E + kSE, w, lane, vacc);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) macc[x] = zero_acc();
+    }
+    double carry = a.gclk[(size_t)bh * p.groups + g];
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
+    const __bf16 *vin = static_cast<const __bf16 *>(p.v), *oin = static_cast<const __bf16 *>(p.dout);
+    __bf16 *gq = static_cast<__bf16 *>(p.gq);
+    Rows2 pq, pk, pv, po;
+    Tok tk;
+    auto prefetch = [&](int c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+        load_rows(qin + base, rs, n, tid, pq);
+        load_rows(kin + base, rs, n, tid, pk);
+        load_rows(vin + base, rs, n, tid, pv);
+        load_rows(oin + base, rs, n, tid, po);
+        load_tok(p, b, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_begin);
+
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        // -- A: stage the chunk, scalars, entering key state in bf16; prefetch the next
+        store_rows(Qt, tid, pq);
+        store_rows(Kt, tid, pk);
+        store_rows(Vt, tid, pv);
+        store_rows(Ot, tid, po);
+        if (w == 0) {
+            if (lane == 0) a.cclk[(size_t)bh * p.nc + c] = carry;
+            chunk_scalars(sc, lane, m, tk, carry, false);
+        }
+        dump_tile(KB, w, l32, h4, kacc);
+        if (c + 1 < c_end) prefetch(c + 1);
+        lds_barrier();
+        build_A(sc, At, tid, m);
+        lds_barrier();
+        // -- B: scores, inter-chunk terms of p and du, state update
+        const float gr = sc.gam[l32];
+        float pc[8], ps[8];
+        lane_phases(sc.urev[l32], w, hl, m, pc, ps);
+        if (w == 0) score_tile<true>(Kt, Qt, S1, sc, l32, hl);   // S1[r][s] = Gamma (q_r . k_s)
+        if (w == 1) score_tile<true>(Vt, Ot, S2, sc, l32, hl);   // S2[r][s] = Gamma (do_r . v_s)
+        f32x16 pacc = zero_acc(), dacc = zero_acc();
+        const __bf16 *qrow = Qt + l32 * QS, *orow = Ot + l32 * QS;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            pacc = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(qrow, 16 * ks, hl), pacc);
+            dacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(orow, 16 * ks, hl), dacc);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            pacc[v] *= gr;
+            dacc[v] *= gr;
+        }
+        {
+            const float gC = sc.gam[kC - 1];
+            scale_acc(kacc, gC);
+            scale_acc(vacc, gC);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 ad = scale_k(rd_tr(At, trl, 16 * ks, 32 * w), sc.rho + 16 * ks + 8 * hl);
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    kacc[x] = mma(rd_tr(Kt, trl, 16 * ks, 32 * x), ad, kacc[x]);
+                    vacc[x] = mma(rd_tr(Vt, trl, 16 * ks, 32 * x), ad, vacc[x]);
+                }
+            }
+        }
+        lds_barrier();
+        // -- C: intra-chunk terms; X = U(lambda) p (scale folded into M); slot logits
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 at = rd_tr(At, trl, 16 * ks, 32 * w);
+            pacc = mma(at, rd_row(S1, SSB, l32, 16 * ks, hl), pacc);
+            dacc = mma(at, rd_row(S2, SSB, l32, 16 * ks, hl), dacc);
+        }
+        rotate<1>(pacc, pc, ps, 1.f);                 // X' = U(lambda) p;  X = scale X'
+        {
+            f32x16 xs = pacc;
+            if (w == 3 && hl == 1) xs[15] = 1.f;      // column 127 = 1: inactive slots get the mask logit
+            store_block(Xt, l32, 32 * w, h4, xs);
+        }
+        lds_barrier();
+        f32x16 wr = zero_acc();                       // slot logits (log2 units), then W
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) wr = mma(rd_row(MZ, QS, 32 * w + l32, 16 * ks, hl), rd_row(Xt, QS, l32, 16 * ks, hl), wr);
+        {
+            float mx = wr[0];
+#pragma unroll
+            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, wr[v]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+#pragma unroll
+            for (int v = 0; v < 16; ++v) wr[v] = __builtin_amdgcn_exp2f(wr[v] - mx);
+            float sm = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sm += wr[v];
+            sm += __shfl_xor(sm, 32);
+            if (hl == 0) red1[w * kC + l32] = make_float2(mx, sm);
+            lds_barrier();
+            float2 pr[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) pr[x] = red1[x * kC + l32];
+            const float M = fmaxf(fmaxf(pr[0].x, pr[1].x), fmaxf(pr[2].x, pr[3].x));
+            float Ls = 0.f;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) Ls += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
+            const float f = __builtin_amdgcn_exp2f(mx - M) / Ls;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) wr[v] *= f;
+        }
+        store_block(Wt, l32, 32 * w, h4, wr);
+        {
+            f32x16 dy = dacc;                          // dY = U(lambda) du
+            rotate<1>(dy, pc, ps, 1.f);
+            if (w == 3 && hl == 1) dy[15] = 0.f;
+            store_block(Yt, l32, 32 * w, h4, dy);
+        }
+        lds_barrier();
+        // -- D: u = U(-lambda) M^T W; dW = M dY; dM += W dY^T
+        float tsum, tclk;
+        {
+            f32x16 ya = zero_acc();
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) ya = mma(rd_tr(MZ, trl, 16 * ks, 32 * w), rd_row(Wt, QS, l32, 16 * ks, hl), ya);
+            rotate<-1>(ya, pc, ps, inv_zs);
+            store_out(a.U + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, ya, true);
+            float ud = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) ud = fmaf(ya[v], dacc[v], ud);
+            tsum = ud;
+            tclk = -rot_part(dacc, ya, w, hl, m);
+        }
+        f32x16 dw = zero_acc();
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) dw = mma(rd_row(MZ, QS, 32 * w + l32, 16 * ks, hl), rd_row(Yt, QS, l32, 16 * ks, hl), dw);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 wa = rd_tr(Wt, trl, 16 * ks, 32 * w);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) macc[x] = mma(wa, rd_tr(Yt, trl, 16 * ks, 32 * x), macc[x]);
+        }
+        {
+            float sw = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                dw[v] *= inv_zs;
+                sw = fmaf(wr[v], dw[v], sw);
+            }
+            sw += __shfl_xor(sw, 32);
+            if (hl == 0) red2[w * kC + l32] = sw;
+        }
+        lds_barrier();
+        {
+            const float sW = (red2[l32] + red2[kC + l32]) + (red2[2 * kC + l32] + red2[3 * kC + l32]);
+            // dZ = W (.) (dW - <W, dW>), stored times scale in the dY tile's place
+#pragma unroll
+            for (int v = 0; v < 16; ++v) dw[v] = wr[v] * (dw[v] - sW) * scale;
+            store_block(Yt, l32, 32 * w, h4, dw);
+        }
+        lds_barrier();
+        // -- E: dX = M^T dZ; dM += dZ X^T; dp = scale U(-lambda) dX
+        {
+            f32x16 xa = zero_acc();
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) xa = mma(rd_tr(MZ, trl, 16 * ks, 32 * w), rd_row(Yt, QS, l32, 16 * ks, hl), xa);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 za = rd_tr(Yt, trl, 16 * ks, 32 * w);
+#pragma unroll
+                for (int x = 0; x < 4; ++x) macc[x] = mma(za, rd_tr(Xt, trl, 16 * ks, 32 * x), macc[x]);
+            }
+            const float fx = inv_zs / scale;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) xa[v] *= fx;
+            tclk += scale * rot_part(xa, pacc, w, hl, m);
+            rotate<-1>(xa, pc, ps, scale);
+            store_block(Wt, l32, 32 * w, h4, xa);
+            store_out(a.dP + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, xa, true);
+        }
+        lds_barrier();
+        // -- F: dq = gamma (.) dP Kbar + (dP A^T (.) Gamma) K
+        if (w == 0) score_tile<true>(At, Wt, S3, sc, l32, hl);   // S3[r][s] = Gamma (dp_r . a_s)
+        f32x16 qa = zero_acc();
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) qa = mma(rd_tr(KB, trl, 16 * ks, 32 * w), rd_row(Wt, QS, l32, 16 * ks, hl), qa);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) qa[v] *= gr;
+        lds_barrier();
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) qa = mma(rd_tr(Kt, trl, 16 * ks, 32 * w), rd_row(S3, SSB, l32, 16 * ks, hl), qa);
+        const bool live = l32 < n;
+        if (t0 + l32 < p.T) store_out(gq + (((size_t)b * p.T + t0 + l32) * p.H + h) * 128 + 32 * w + h4, qa, live);
+        tsum += dot_row(Qt + l32 * QS + 32 * w + h4, qa);
+        tsum += __shfl_xor(tsum, 32);
+        tclk += __shfl_xor(tclk, 32);
+        if (hl == 0) red3[w * kC + l32] = make_float2(tsum, tclk);
+        lds_barrier();
+        if (w == 0 && lane < kC) {
+            float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                const float2 v = red3[x * kC + lane];
+                s1 += v.x;
+                s2 += v.y;
+            }
+            const size_t ti = (size_t)bh * p.Tpad + t0 + lane;
+            const bool lv = lane < n;
+            p.udu[ti] = lv ? s1 : 0.f;
+            p.dlam[ti] = lv ? s2 * (kTwoPi / (float)m) : 0.f;
+        }
+    }
+    // the group's dM in paper column order
+    float *dMo = p.dMp + ((size_t)bh * p.groups + g) * 128 * 128;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        const int col = paper_row(32 * x + l32);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int j = 32 * w + 8 * (v >> 2) + h4 + (v & 3);
+            dMo[j * 128 + col] = macc[x][v];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// (4) group contributions to the adjoint states (reverse over the group's chunks,
+// zero adjoint at its end): DK <- exp(G_C) DK + (gamma (.) dP)^T Q, DV likewise
+// with (gamma (.) U)^T dO.
+struct ALay {
+    static constexpr int Q = 0, O = kT32, U = 2 * kT32, P = 3 * kT32, SC = 4 * kT32;
+    static constexpr int BYTES = SC + 1024;
+};
+__global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
+    using L = ALay;
+    __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int Tb = tokens_of(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    Sc &sc = *lds_at<Sc>(smem, L::SC);
+    __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Ot = lds_at<__bf16>(smem, L::O);
+    __bf16 *Ut = lds_at<__bf16>(smem, L::U), *Pt = lds_at<__bf16>(smem, L::P);
+    const int trl = tr_off(QS, lane);
+    f32x16 kacc[4], vacc[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
+    }
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *qin = static_cast<const __bf16 *>(p.q), *oin = static_cast<const __bf16 *>(p.dout);
+    for (int c = c_end - 1; c >= c_begin; --c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        {
+            Rows2 rq, ro, ru, rp;
+            const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+            const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
+            load_rows(qin + base, rs, n, tid, rq);
+            load_rows(oin + base, rs, n, tid, ro);
+            load_rows(a.U + wb, 128, kC, tid, ru);
+            load_rows(a.dP + wb, 128, kC, tid, rp);
+            float lg = 0.f;
+            if (tid < kC && t0 + tid < Tb && p.log_alpha)
+                lg = p.log_alpha[((size_t)b * p.T + t0 + tid) * p.H + h];
+            store_rows(Qt, tid, rq);
+            store_rows(Ot, tid, ro);
+            store_rows(Ut, tid, ru);
+            store_rows(Pt, tid, rp);
+            if (w == 0) {
+                const float G = wave_incl_scan(lg);
+                if (lane < kC) sc.gam[lane] = __expf(G);
+            }
+        }
+        lds_barrier();
+        const float gC = sc.gam[kC - 1];
+        scale_acc(kacc, gC);
+        scale_acc(vacc, gC);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const float *gk = sc.gam + 16 * ks + 8 * hl;
+            const bf16x8 bp = scale_k(rd_tr(Pt, trl, 16 * ks, 32 * w), gk);
+            const bf16x8 bu = scale_k(rd_tr(Ut, trl, 16 * ks, 32 * w), gk);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                kacc[x] = mma(rd_tr(Qt, trl, 16 * ks, 32 * x), bp, kacc[x]);
+                vacc[x] = mma(rd_tr(Ot, trl, 16 * ks, 32 * x), bu, vacc[x]);
+            }
+        }
+        lds_barrier();
+    }
+    float *E = a.Ea + ((size_t)bh * p.groups + g) * 2 * kSE;
+    store_acc(E, w, lane, kacc);
+    store_acc(E + kSE, w, lane, vacc);
+}
+
+// (5) adjoint states at each group's end, in reverse group order from (dK_T, dV_T);
+// the adjoint of the initial state is dK0, dV0 (paper row order, rows >= m zero).
+__global__ __launch_bounds__(kNT) void adj_combine_kernel(Args a) {
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
+    const float *Gg = a.Gg + (size_t)bh * G;
+    for (int e = blockIdx.y * kNT + tid; e < 2 * kSE; e += kCombBlocks * kNT) {
+        const int st = e / kSE, f = e % kSE;
+        int i, c;
+        dump_coords(f, i, c);
+        const bool act = row_active(i, m);
+        const size_t ai = ((size_t)bh * kStoreRows + paper_row(i)) * 128 + c;
+        const float *fin = st ? p.dV_T : p.dK_T;
+        float *g0 = st ? p.gV0 : p.gK0;
+        float A = (fin && act) ? fin[ai] : 0.f;
+        for (int q = G - 1; q >= 0; --q) {
+            float *slot = a.Ea + (((size_t)bh * G + q) * 2 + st) * kSE + f;
+            const float own = *slot;
+            *slot = A;
+            A = fmaf(__expf(Gg[q]), A, own);
+        }
+        if (g0) g0[ai] = act ? A : 0.f;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// (6) token gradients, per (sequence, chunk group), chunks in reverse.
+// LDS: padded [32][QS] tiles Q, K, V, dO, U, dP, A; [128][QS] tiles of the adjoint
+// states at the chunk's end (bf16); four score tiles stored [s][r]; scalars;
+// per-token reduction slots.
+struct GLay {
+    static constexpr int Q = 0, K = kT32, V = 2 * kT32, O = 3 * kT32, U = 4 * kT32, P = 5 * kT32, A = 6 * kT32;
+    static constexpr int DK = 7 * kT32, DV = DK + kT128;
+    static constexpr int T1 = DV + kT128, T2 = T1 + kTS, T3 = T2 + kTS, T4 = T3 + kTS;
+    static constexpr int SC = T4 + kTS, RED = SC + 1024;
+    static constexpr int BYTES = RED + 4 * kC * 16;
+    static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
+};
+__global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
+    using L = GLay;
+    __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
+    const BwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5, h4 = 4 * hl;
+    const int m = p.m;
+    const int Tb = tokens_of(p, b);
+    const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
+    Sc &sc = *lds_at<Sc>(smem, L::SC);
+    __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
+    __bf16 *Ot = lds_at<__bf16>(smem, L::O), *Ut = lds_at<__bf16>(smem, L::U), *Pt = lds_at<__bf16>(smem, L::P);
+    __bf16 *At = lds_at<__bf16>(smem, L::A), *DKt = lds_at<__bf16>(smem, L::DK), *DVt = lds_at<__bf16>(smem, L::DV);
+    __bf16 *T1 = lds_at<__bf16>(smem, L::T1), *T2 = lds_at<__bf16>(smem, L::T2);
+    __bf16 *T3 = lds_at<__bf16>(smem, L::T3), *T4 = lds_at<__bf16>(smem, L::T4);
+    float4 *red = lds_at<float4>(smem, L::RED);
+    const int trl = tr_off(QS, lane);
+    f32x16 kacc[4], vacc[4];
+    {
+        const float *E = a.Ea + ((size_t)bh * p.groups + g) * 2 * kSE;
+        load_acc(E, w, lane, kacc);
+        load_acc(E + kSE, w, lane, vacc);
+    }
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
+    const __bf16 *vin = static_cast<const __bf16 *>(p.v), *oin = static_cast<const __bf16 *>(p.dout);
+    __bf16 *gk = static_cast<__bf16 *>(p.gk), *gv = static_cast<__bf16 *>(p.gv);
+    Rows2 pq, pk, pv, po, pu, pp;
+    Tok tk;
+    auto prefetch = [&](int c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+        const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
+        load_rows(qin + base, rs, n, tid, pq);
+        load_rows(kin + base, rs, n, tid, pk);
+        load_rows(vin + base, rs, n, tid, pv);
+        load_rows(oin + base, rs, n, tid, po);
+        load_rows(a.U + wb, 128, kC, tid, pu);
+        load_rows(a.dP + wb, 128, kC, tid, pp);
+        load_tok(p, b, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_end - 1);
+    const float sq2m = sqrtf(2.f / (float)m), dcw = 1.f / sqrtf((float)m);
+    const int J = (m - 1) >> 1;
+
+    for (int c = c_end - 1; c >= c_begin; --c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        // -- A: stage, scalars (clock entering the chunk from the forward walk), adjoint
+        //    states at the chunk's end in bf16; prefetch the previous chunk
+        store_rows(Qt, tid, pq);
+        store_rows(Kt, tid, pk);
+        store_rows(Vt, tid, pv);
+        store_rows(Ot, tid, po);
+        store_rows(Ut, tid, pu);
+        store_rows(Pt, tid, pp);
+        if (w == 0) {
+            double carry = a.cclk[(size_t)bh * p.nc + c];
+            chunk_scalars(sc, lane, m, tk, carry, false);
+        }
+        dump_tile(DKt, w, l32, h4, kacc);
+        dump_tile(DVt, w, l32, h4, vacc);
+        if (c > c_begin) prefetch(c - 1);
+        lds_barrier();
+        build_A(sc, At, tid, m);
+        lds_barrier();
+        // -- B: score tiles (one per wave, stored [s][r]); inter-chunk terms of da, dk,
+        //    dv; adjoint update
+        if (w == 0) score_tile<false>(Qt, Kt, T1, sc, l32, hl);   // T1[s][r] = Gamma (q_r . k_s)
+        if (w == 1) score_tile<false>(Ot, Vt, T2, sc, l32, hl);   // T2[s][r] = Gamma (do_r . v_s)
+        if (w == 2) score_tile<false>(Pt, At, T3, sc, l32, hl);   // T3[s][r] = Gamma (dp_r . a_s)
+        if (w == 3) score_tile<false>(Ut, At, T4, sc, l32, hl);   // T4[s][r] = Gamma (u_r . a_s)
+        const float rs_ = sc.rho[l32];
+        f32x16 da = zero_acc(), dka = zero_acc(), dva = zero_acc();
+        {
+            const __bf16 *krow = Kt + l32 * QS, *vrow = Vt + l32 * QS;
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) {
+                da = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(krow, 16 * ks, hl), da);
+                da = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(vrow, 16 * ks, hl), da);
+            }
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) {
+                const bf16x8 ar = rd_row(At, QS, l32, 16 * ks, hl);
+                dka = mma(rd_tr(DKt, trl, 16 * ks, 32 * w), ar, dka);
+                dva = mma(rd_tr(DVt, trl, 16 * ks, 32 * w), ar, dva);
+            }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                da[v] *= rs_;
+                dka[v] *= rs_;
+                dva[v] *= rs_;
+            }
+        }
+        {
+            const float gC = sc.gam[kC - 1];
+            scale_acc(kacc, gC);
+            scale_acc(vacc, gC);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const float *gk8 = sc.gam + 16 * ks + 8 * hl;
+                const bf16x8 bp = scale_k(rd_tr(Pt, trl, 16 * ks, 32 * w), gk8);
+                const bf16x8 bu = scale_k(rd_tr(Ut, trl, 16 * ks, 32 * w), gk8);
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    kacc[x] = mma(rd_tr(Qt, trl, 16 * ks, 32 * x), bp, kacc[x]);
+                    vacc[x] = mma(rd_tr(Ot, trl, 16 * ks, 32 * x), bu, vacc[x]);
+                }
+            }
+        }
+        lds_barrier();
+        // -- C: intra-chunk terms
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            da = mma(rd_tr(Pt, trl, 16 * ks, 32 * w), rd_row(T1, SSB, l32, 16 * ks, hl), da);
+            da = mma(rd_tr(Ut, trl, 16 * ks, 32 * w), rd_row(T2, SSB, l32, 16 * ks, hl), da);
+            dka = mma(rd_tr(Qt, trl, 16 * ks, 32 * w), rd_row(T3, SSB, l32, 16 * ks, hl), dka);
+            dva = mma(rd_tr(Ot, trl, 16 * ks, 32 * w), rd_row(T4, SSB, l32, 16 * ks, hl), dva);
+        }
+        const bool live = l32 < n;
+        if (t0 + l32 < p.T) {
+            const size_t go = (((size_t)b * p.T + t0 + l32) * p.H + h) * 128 + 32 * w + h4;
+            store_out(gk + go, dka, live);
+            store_out(gv + go, dva, live);
+        }
+        float r1 = dot_row(Kt + l32 * QS + 32 * w + h4, dka) + dot_row(Vt + l32 * QS + 32 * w + h4, dva);
+        // dbeta = <da, U(-lambda) b>; clock gradient of a = beta U(-lambda) b
+        float r2 = 0.f, r3 = 0.f;
+        {
+            float pc[8], ps[8];
+            lane_phases(sc.urev[l32], w, hl, m, pc, ps);
+            const float amp = sc.bw[l32].x;            // beta sqrt(2/m)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int j = pair_freq(w, hl, e);
+                if (j <= J) {
+                    r2 = fmaf(sq2m, pc[e] * da[2 * e] - ps[e] * da[2 * e + 1], r2);
+                    // j (da_sin a_cos - da_cos a_sin) with a_cos = amp c, a_sin = -amp s
+                    r3 = fmaf((float)j * amp, da[2 * e + 1] * pc[e] + da[2 * e] * ps[e], r3);
+                }
+            }
+            if (w == 3 && hl == 1) r2 = fmaf(dcw, da[14], r2);   // DC (internal row 126)
+        }
+        r1 += __shfl_xor(r1, 32);
+        r2 += __shfl_xor(r2, 32);
+        r3 += __shfl_xor(r3, 32);
+        if (hl == 0) red[w * kC + l32] = make_float4(r1, r2, r3, 0.f);
+        lds_barrier();
+        if (w == 0 && lane < kC) {
+            float s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                const float4 v = red[x * kC + lane];
+                s1 += v.x;
+                s2 += v.y;
+                s3 += v.z;
+            }
+            const size_t ti = (size_t)bh * p.Tpad + t0 + lane;
+            const bool lv = lane < n;
+            p.dG[ti] = lv ? p.udu[ti] - s1 : 0.f;
+            p.dlam[ti] = lv ? p.dlam[ti] - s3 * (kTwoPi / (float)m) : 0.f;
+            if (p.gbeta && t0 + lane < p.T) p.gbeta[((size_t)b * p.T + t0 + lane) * p.H + h] = lv ? s2 : 0.f;
+        }
+    }
+}
+
+}  // namespace
+
+int bwd_mfma_auto_groups(int B, int T, int H) {
+    const int nc = (T + kC - 1) / kC;
+    const int BH = B * H;
+    int g = (256 + BH - 1) / BH;
+    if (g > nc) g = nc;
+    return g < 1 ? 1 : g;
+}
+
+// Layout (each piece 256-byte aligned): Mz, Ef, Ea, Gg, gclk, cclk, U, dP, udu, dlam,
+// dG, dMp, fin.
+size_t bwd_mfma_workspace_bytes(int B, int T, int H, int groups) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t BH = (size_t)B * H, nc = ((size_t)T + kC - 1) / kC, Tpad = nc * kC, G = groups;
+    size_t n = al((size_t)H * 128 * 128 * 2);
+    n += 2 * al(BH * G * 2 * kSE * 4);
+    n += al(BH * G * 4) + al(BH * G * 8) + al(BH * nc * 8);
+    n += 2 * al(BH * Tpad * 128 * 2);
+    n += 3 * al(BH * Tpad * 4);
+    n += al(BH * G * 128 * 128 * 4);
+    n += al(BH * kCombBlocks * 4);
+    return n;
+}
+
+hipError_t launch_bwd_mfma(BwdParams p, void *ws, hipStream_t s) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t BH = (size_t)p.B * p.H, nc = p.nc, Tpad = p.Tpad, G = p.groups;
+    char *w = static_cast<char *>(ws);
+    auto take = [&](size_t bytes) { char *r = w; w += al(bytes); return r; };
+    Args a{};
+    __bf16 *Mz = reinterpret_cast<__bf16 *>(take((size_t)p.H * 128 * 128 * 2));
+    a.Mz = Mz;
+    a.Ef = reinterpret_cast<float *>(take(BH * G * 2 * kSE * 4));
+    a.Ea = reinterpret_cast<float *>(take(BH * G * 2 * kSE * 4));
+    a.Gg = reinterpret_cast<float *>(take(BH * G * 4));
+    a.gclk = reinterpret_cast<double *>(take(BH * G * 8));
+    a.cclk = reinterpret_cast<double *>(take(BH * nc * 8));
+    a.U = reinterpret_cast<__bf16 *>(take(BH * Tpad * 128 * 2));
+    a.dP = reinterpret_cast<__bf16 *>(take(BH * Tpad * 128 * 2));
+    p.udu = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dlam = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dG = reinterpret_cast<float *>(take(BH * Tpad * 4));
+    p.dMp = reinterpret_cast<float *>(take(BH * G * 128 * 128 * 4));
+    p.fin = reinterpret_cast<float *>(take(BH * kCombBlocks * 4));
+    a.p = p;
+    hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, Mz, p.scale * 1.4426950408889634f, s);
+    if (e != hipSuccess) return e;
+    const dim3 block(kNT), grp(BH, G), comb(BH, kCombBlocks);
+    hipLaunchKernelGGL(fwd_contrib_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(fwd_combine_kernel, comb, block, 0, s, a);
+    hipLaunchKernelGGL(readout_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(adj_contrib_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(adj_combine_kernel, comb, block, 0, s, a);
+    hipLaunchKernelGGL(grad_kernel, grp, block, 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_bwd_tail(p, s);
+}
+
+}  // namespace cyfa

@@ -54,7 +54,7 @@ constexpr int kRQ = kC * kStoreRows / kNT;   // token rows per thread in the rea
 constexpr int kReadoutThreads = kNT;           // the readout kernel (1024 measured slower: spills)
 constexpr int kLD = kStoreRows + 4; // padded row of a [token][basis] tile (16-byte rows)
 constexpr float kTwoPi = 6.283185307179586f;
-constexpr int kCombBlocks = 8;      // workgroups per sequence of the group-combine kernels
+constexpr int kCombBlocks = kBwdFinParts;   // workgroups per sequence of the group-combine kernels
 
 __device__ __forceinline__ float wsum(float x) {
 #pragma unroll
@@ -1050,16 +1050,14 @@ __global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
 template <int DK, int DV, typename Tin>
 hipError_t launch_typed(const BwdParams &p, hipStream_t s) {
     const int BH = p.B * p.H;
-    const dim3 block(kNT), seq(BH), grp(BH, p.groups);
+    const dim3 block(kNT), grp(BH, p.groups);
     hipLaunchKernelGGL((bwd_states_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL((bwd_states_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
     hipLaunchKernelGGL((bwd_readout_kernel<DK, DV, Tin>), grp, dim3(kReadoutThreads), 0, s, p);
     hipLaunchKernelGGL((bwd_adjoint_local_kernel<DK, DV, Tin>), grp, block, 0, s, p);
     hipLaunchKernelGGL((bwd_adjoint_combine_kernel<DK, DV>), dim3(BH, kCombBlocks), block, 0, s, p);
     hipLaunchKernelGGL((bwd_grad_kernel<DK, DV, Tin>), grp, block, 0, s, p);
-    hipLaunchKernelGGL(bwd_scan_kernel, seq, block, 0, s, p);
-    if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H, kStoreRows / kDRRows), block, 0, s, p);
-    return hipGetLastError();
+    return launch_bwd_tail(p, s);
 }
 
 template <int DK, int DV>
@@ -1070,6 +1068,12 @@ hipError_t launch_dtype(const BwdParams &p, hipStream_t s) {
 size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
 
 }  // namespace
+
+hipError_t launch_bwd_tail(const BwdParams &p, hipStream_t s) {
+    hipLaunchKernelGGL(bwd_scan_kernel, dim3(p.B * p.H), dim3(kNT), 0, s, p);
+    if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H, kStoreRows / kDRRows), dim3(kNT), 0, s, p);
+    return hipGetLastError();
+}
 
 int bwd_auto_groups(int B, int T, int H) {
     const int nc = (T + kC - 1) / kC;

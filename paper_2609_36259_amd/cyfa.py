@@ -317,13 +317,15 @@ def backward_workspace_size(desc: FwdDesc) -> int:
 
 def backward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, d_o, scale=None, m=127,
              K0=None, V0=None, clock0=None, dK_T=None, dV_T=None, lens=None, groups=0,
-             want_state_grads=True, workspace=None, stream=None):
+             want_state_grads=True, kernel=KERNEL_AUTO, workspace=None, stream=None):
     """Gradients of sum <d_o, o> + <dK_T, K_out> + <dV_T, V_out> (cyfa_backward).
 
     Inputs as for ``forward``; ``d_o`` [B,T,H,dv] in q's dtype; ``dK_T``/``dV_T``
     [B,H,128,d] float32 or None.  Returns a dict with dq, dk, dv (q's dtype),
     d_delta, d_log_alpha / d_beta (None when the input is None), d_R (None without
     R) and, with ``want_state_grads``, d_K0, d_V0 [B,H,128,d] and d_clock0 [B,H].
+    ``kernel``: KERNEL_AUTO (the matrix-core backward for bf16 with d = 128, else
+    the vector-ALU one), KERNEL_VALU or KERNEL_MFMA.
     """
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -342,7 +344,7 @@ def backward(q, k, v, delta, log_alpha=None, beta=None, R=None, *, d_o, scale=No
     _need(clock0, (B, H), torch.float64, "clock0")
     _need(lens, (B,), torch.int32, "lens")
     desc = forward_desc(B, T, H, dk, dv, m=m, chunk=0, segments=groups, scale=scale, dtype=dt,
-                        kernel=KERNEL_VALU)
+                        kernel=kernel)
     nbytes = backward_workspace_size(desc)
     dev = q.device
     if workspace is None or workspace.numel() < nbytes:

@@ -1,4 +1,5 @@
-"""GPU parity of the backward (cyfa_backward) against the backward oracle.
+"""GPU parity of the vector-ALU backward (cyfa_backward, kernel VALU) against the
+backward oracle.
 
 Every gradient tensor is compared element by element with the oracle's float64
 reverse-mode gradients on the same seeded inputs, the same upstream gradient
@@ -50,6 +51,7 @@ def _extras(x, seed, init=True, final=True):
 
 
 def _run(x, e, lens=None, groups=0):
+    """The vector-ALU backward (fp32 arithmetic); the matrix-core one has its own file."""
     cyfa = _cyfa()
     t = upload(x)
     dt = t["q"].dtype
@@ -59,7 +61,8 @@ def _run(x, e, lens=None, groups=0):
                       K0=dev(e.get("K0")), V0=dev(e.get("V0")),
                       clock0=dev(e.get("clock0"), torch.float64),
                       dK_T=dev(e.get("dK_T")), dV_T=dev(e.get("dV_T")),
-                      lens=None if lens is None else dev(lens, torch.int32), groups=groups)
+                      lens=None if lens is None else dev(lens, torch.int32), groups=groups,
+                      kernel=cyfa.KERNEL_VALU)
     torch.cuda.synchronize()
     return {k: (None if v is None else v.float().cpu().numpy() if v.dtype != torch.float64
                 else v.cpu().numpy()) for k, v in g.items()}

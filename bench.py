@@ -277,39 +277,66 @@ def bwd_flops_per_token_head(dk: int, dv: int, m: int = M_ACTIVE, C: int = 16) -
                   + (C + 1) / 2.0 * (4 * dk + 3 * dv + 6 * m))
 
 
+def bwd_mfma_flops_per_token_head(d: int = 128, C: int = 32, R: int = 128) -> float:
+    """Matrix-core FLOPs of the bf16 backward per token and head (R = 128 state rows,
+    d = d_k = d_v, C-token chunks), as its kernels issue them: state and adjoint-state
+    products 15 R d (group pre-passes 2+2, the forward walk's key pass, du, dq and state
+    update 5, the reverse walk's da, dk, dv and adjoint update 6), the readout's four
+    products and dM 6 R^2, and the full C x C score tiles and their products
+    7 C (d + R); times 2 for multiply-add."""
+    return 2.0 * (15 * R * d + 6 * R * R + 7 * C * (d + R))
+
+
 def backward_bench(args, torch, cyfa, w, prepared):
-    """cyfa_backward on the benchmark workload (upstream gradient d_o ~ N(0, 1))."""
+    """cyfa_backward on the benchmark workload (upstream gradient d_o ~ N(0, 1)): the
+    matrix-core backward (bf16 with d = 128; the automatic choice there) and the
+    vector-ALU one on the same inputs."""
     dev = torch.device("cuda:0")
     scale, io_dtype, t = prepared
     g = torch.Generator(device=dev)
     g.manual_seed(5)
     do = torch.randn((w.B, w.T, w.H, w.dv), device=dev, generator=g).to(t["q"].dtype)
-    desc = cyfa.forward_desc(w.B, w.T, w.H, w.dk, w.dv, m=w.m, scale=scale,
-                             dtype=cyfa.BF16 if io_dtype == "bf16" else cyfa.F32,
-                             kernel=cyfa.KERNEL_VALU)
-    ws = torch.empty(cyfa.backward_workspace_size(desc), dtype=torch.uint8, device=dev)
 
-    def step():
-        return cyfa.backward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
-                             d_o=do, scale=scale, m=w.m, workspace=ws)
+    def timed(kernel, steps):
+        desc = cyfa.forward_desc(w.B, w.T, w.H, w.dk, w.dv, m=w.m, scale=scale,
+                                 dtype=cyfa.BF16 if io_dtype == "bf16" else cyfa.F32, kernel=kernel)
+        ws = torch.empty(cyfa.backward_workspace_size(desc), dtype=torch.uint8, device=dev)
 
-    for _ in range(2):
-        step()
-    torch.cuda.synchronize()
-    steps = 10
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1000 / steps
-    flops = bwd_flops_per_token_head(w.dk, w.dv, w.m) * w.B * w.T * w.H
+        def step():
+            return cyfa.backward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                                 d_o=do, scale=scale, m=w.m, workspace=ws, kernel=kernel)
+
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1000 / steps
+        del ws
+        torch.cuda.empty_cache()
+        return ms
+
+    tokens = w.B * w.T
+    ms_v = timed(cyfa.KERNEL_VALU, 10)
+    flops_v = bwd_flops_per_token_head(w.dk, w.dv, w.m) * tokens * w.H
+    tfl_v = flops_v / (ms_v * 1e-3) / 1e12
+    valu = dict(ms_per_step=ms_v, tokens_per_s=tokens / (ms_v * 1e-3), arithmetic="fp32 vector ALU",
+                alg_flops_per_step=flops_v,
+                roofline={"bound": "alu", "achieved": tfl_v, "peak": PEAK_F32_VALU_TFLOPS, "unit": "TFLOP/s",
+                          "frac": tfl_v / PEAK_F32_VALU_TFLOPS})
+    if not (io_dtype == "bf16" and w.dk == 128 and w.dv == 128):
+        return dict(workload=w.name, steps=10, **valu)
+    steps = 20
+    ms = timed(cyfa.KERNEL_MFMA, steps)
+    flops = bwd_mfma_flops_per_token_head(w.dk) * tokens * w.H
     tfl = flops / (ms * 1e-3) / 1e12
-    del ws
-    torch.cuda.empty_cache()
-    return dict(workload=w.name, steps=steps, ms_per_step=ms, tokens_per_s=w.B * w.T / (ms * 1e-3),
-                arithmetic="fp32 vector ALU", alg_flops_per_step=flops,
-                roofline={"bound": "alu", "achieved": tfl, "peak": PEAK_F32_VALU_TFLOPS, "unit": "TFLOP/s",
-                          "frac": tfl / PEAK_F32_VALU_TFLOPS})
+    return dict(workload=w.name, steps=steps, ms_per_step=ms, tokens_per_s=tokens / (ms * 1e-3),
+                arithmetic="bf16 MFMA, fp32 accumulation", mfma_flops_per_step=flops,
+                roofline={"bound": "mfma", "achieved": tfl, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                          "frac": tfl / PEAK_BF16_TFLOPS},
+                valu=valu)
 
 
 def mixer_bench(args, torch, cyfa, w):

@@ -85,6 +85,16 @@ struct Args {
     __bf16 *U, *dP;     // [BH][Tpad][128] u_t and dp_t, internal basis order
 };
 
+// a value every lane holds alike, moved to a scalar register
+__device__ __forceinline__ float uniform(float x) {
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+// opaque copy: a value recomputed from it is not merged with an earlier computation
+__device__ __forceinline__ float opqf(float x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 __device__ __forceinline__ int tokens_of(const BwdParams &p, int b) {
     return p.lens ? min(max(p.lens[b], 0), p.T) : p.T;
 }
@@ -179,13 +189,16 @@ __device__ __forceinline__ bf16x8 scale_k(bf16x8 v, const float *f) {
 struct Rows2 {
     uint4 r[2];
 };
+// (Rows past n are read from a clamped row of the chunk, which exists: the chunk
+// starts inside the tensor, and then set to zero.)
 __device__ __forceinline__ void load_rows(const __bf16 *base, size_t row_stride, int n, int tid, Rows2 &o) {
     const int r0 = tid >> 4, c8 = (tid & 15) * 8;
+    const int last = max(n - 1, 0);
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
         const int r = r0 + 16 * it;
-        o.r[it] = make_uint4(0, 0, 0, 0);
-        if (r < n) o.r[it] = *reinterpret_cast<const uint4 *>(base + (size_t)r * row_stride + c8);
+        const uint4 v = *reinterpret_cast<const uint4 *>(base + (size_t)min(r, last) * row_stride + c8);
+        o.r[it] = r < n ? v : make_uint4(0, 0, 0, 0);
     }
 }
 __device__ __forceinline__ void store_rows(__bf16 *T, int tid, const Rows2 &o) {
@@ -215,34 +228,75 @@ __device__ __forceinline__ void load_tok(const BwdParams &p, int b, int h, int t
 // Chunk scalars in LDS.
 struct Sc {
     float G[kC];      // chunk-local inclusive sums of log alpha
-    float gam[kC];    // exp(G_r)
-    float rho[kC];    // exp(G_C - G_r)
+    float gam[kC];    // exp(G_r) (times the carried states' scale where a kernel keeps one)
+    float rho[kC];    // exp(G_C - G_r) (likewise)
     float urev[kC];   // clock after token r over m, mod 1 (revolutions)
     float4 bw[kC];    // write-builder record: amplitude, urev, cos and sin of 2 pi urev
+    float ctl[4];     // lazily scaled kernels: [0] factor applied to the carried states
+                      // before the chunk, [1] factor applied before their update
 };
-static_assert(sizeof(Sc) == 1024, "scalar block");
+constexpr int kScBytes = sizeof(Sc);
+static_assert(kScBytes % 16 == 0, "scalar block");
 
 // Wave 0: prefix sums of the chunk and the builder records; carry is the clock
 // entering the chunk (reduced), advanced past it.  dec_amp: the write rows carry
 // their right decay rho_r (A_dec).
-__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, bool dec_amp) {
+//
+// Lazily scaled carried states (kLazy: the forward walk's states, kLazyAdj: the
+// reverse walk's adjoint states) are held as exp(Ls) times the registers, so that a
+// chunk's decay changes Ls instead of every accumulator.  Forward walk: gam_r =
+// exp(G_r + Ls) scales the inter-chunk terms and rho_s = exp(-Ls - G_s) the update
+// operand, then Ls += G_C.  Reverse walk: rho_s = exp(G_C - G_s + Ls) scales the
+// inter-chunk terms and gam_r = exp(G_r - G_C - Ls) the update operand, then Ls +=
+// G_C.  When an exponent could leave [-60, 60] the chunk is eager: the registers
+// are first multiplied by exp(Ls) (ctl[0]), Ls restarts at 0, gam and rho take their
+// plain values and the registers are multiplied by exp(G_C) (ctl[1]) before the
+// update.  Every thread tracks Ls itself from the same LDS values.
+enum { kPlain = 0, kLazy = 1, kLazyAdj = 2 };
+template <int kMode>
+__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, bool dec_amp,
+                                              float Ls = 0.f) {
     const double inv_m = 1.0 / (double)m;
     const float G = wave_incl_scan(k.g);
     const double lam = carry + wave_incl_scan((double)k.dl);
     const float GC = lane63(G);
+    bool lazy = false;
+    if (kMode != kPlain) {
+        const float gabs = wave_max_nonneg(fabsf(G));
+        lazy = fabsf(Ls) + (kMode == kLazyAdj ? 2.f : 1.f) * gabs <= 60.f;
+    }
     if (lane < kC) {
         s.G[lane] = G;
-        s.gam[lane] = __expf(G);
-        const float rho = __expf(GC - G);
+        float gam = __expf(G), rho = __expf(GC - G);
+        const float amp_dec = rho;
+        if (lazy) {
+            if (kMode == kLazy) {
+                gam = __expf(G + Ls);
+                rho = __expf(-Ls - G);
+            } else {
+                rho = __expf(GC - G + Ls);
+                gam = __expf(G - GC - Ls);
+            }
+        }
+        s.gam[lane] = gam;
         s.rho[lane] = rho;
         const double q = lam * inv_m;
         const float u = (float)(q - floor(q));
         s.urev[lane] = u;
         float s1, c1;
         sincos_rev(u, &s1, &c1);
-        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? rho : 1.f), u, c1, s1);
+        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? amp_dec : 1.f), u, c1, s1);
+    }
+    if (kMode != kPlain && lane == 0) {
+        s.ctl[0] = lazy ? 1.f : __expf(Ls);
+        s.ctl[1] = lazy ? 1.f : __expf(GC);
+        s.ctl[2] = lazy ? 1.f : 0.f;
     }
     carry = reduce_clock(lane63(lam), (double)m, inv_m);
+}
+// Every thread: the carried log scale after the chunk (from the chunk's control words).
+__device__ __forceinline__ float next_scale(const Sc &s, float Ls) {
+    return s.ctl[2] != 0.f ? Ls + s.G[kC - 1] : 0.f;
 }
 
 // Temporal write rows (Eq. app-temporal-writes) into a padded [32][QS] tile:
@@ -377,7 +431,7 @@ __device__ __forceinline__ float dot_row(const __bf16 *row, const f32x16 &acc) {
 // ---------------------------------------------------------------------------
 // (1) group contributions to the forward states and the group's clock entry.
 struct CLay {
-    static constexpr int K = 0, V = kT32, A = 2 * kT32, SC = 3 * kT32, RED = SC + 1024;
+    static constexpr int K = 0, V = kT32, A = 2 * kT32, SC = 3 * kT32, RED = SC + kScBytes;
     static constexpr int BYTES = RED + kNT * 8;
 };
 __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
@@ -429,7 +483,7 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
             load_tok(p, b, h, t0, Tb, tid, tk);
             store_rows(Kt, tid, rk);
             store_rows(Vt, tid, rv);
-            if (w == 0) chunk_scalars(sc, lane, m, tk, carry, true);
+            if (w == 0) chunk_scalars<kPlain>(sc, lane, m, tk, carry, true);
         }
         lds_barrier();
         build_A(sc, At, tid, m);
@@ -498,7 +552,7 @@ struct RLay {
     static constexpr int KB = 8 * kT32, MZ = KB + kT128;
     static constexpr int S1 = MZ + kT128, S2 = S1 + kTS, S3 = S2 + kTS;
     static constexpr int SC = S3 + kTS;
-    static constexpr int R1 = SC + 1024, R2 = R1 + 4 * kC * 8, R3 = R2 + 4 * kC * 4;
+    static constexpr int R1 = SC + kScBytes, R2 = R1 + 4 * kC * 8, R3 = R2 + 4 * kC * 4;
     static constexpr int BYTES = R3 + 4 * kC * 8;
     static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
 };
@@ -559,34 +613,41 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
     };
     if (c_begin < c_end) prefetch(c_begin);
 
+    float Ls = 0.f;                                   // carried states: exp(Ls) x registers
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
-        // -- A: stage the chunk, scalars, entering key state in bf16; prefetch the next
+        // -- A: stage the chunk and its scalars; entering key state in bf16; writes
         store_rows(Qt, tid, pq);
         store_rows(Kt, tid, pk);
         store_rows(Vt, tid, pv);
         store_rows(Ot, tid, po);
         if (w == 0) {
             if (lane == 0) a.cclk[(size_t)bh * p.nc + c] = carry;
-            chunk_scalars(sc, lane, m, tk, carry, false);
+            chunk_scalars<kLazy>(sc, lane, m, tk, carry, false, Ls);
+        }
+        lds_barrier();
+        {
+            const float pre = uniform(sc.ctl[0]);
+            if (pre != 1.f) {
+                scale_acc(kacc, pre);
+                scale_acc(vacc, pre);
+            }
         }
         dump_tile(KB, w, l32, h4, kacc);
-        if (c + 1 < c_end) prefetch(c + 1);
-        lds_barrier();
         build_A(sc, At, tid, m);
         lds_barrier();
-        // -- B: scores, inter-chunk terms of p and du, state update
+        // -- B: scores, inter-chunk terms of p and du, state update; prefetch the next chunk
         const float gr = sc.gam[l32];
-        float pc[8], ps[8];
-        lane_phases(sc.urev[l32], w, hl, m, pc, ps);
         if (w == 0) score_tile<true>(Kt, Qt, S1, sc, l32, hl);   // S1[r][s] = Gamma (q_r . k_s)
         if (w == 1) score_tile<true>(Vt, Ot, S2, sc, l32, hl);   // S2[r][s] = Gamma (do_r . v_s)
         f32x16 pacc = zero_acc(), dacc = zero_acc();
-        const __bf16 *qrow = Qt + l32 * QS, *orow = Ot + l32 * QS;
+        {
+            const __bf16 *orow = Ot + l32 * QS;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            pacc = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(qrow, 16 * ks, hl), pacc);
-            dacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(orow, 16 * ks, hl), dacc);
+            for (int ks = 0; ks < 8; ++ks) {
+                pacc = mma(rd_row(KB, QS, 32 * w + l32, 16 * ks, hl), rd_row(Qt, QS, l32, 16 * ks, hl), pacc);
+                dacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(orow, 16 * ks, hl), dacc);
+            }
         }
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
@@ -594,9 +655,11 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
             dacc[v] *= gr;
         }
         {
-            const float gC = sc.gam[kC - 1];
-            scale_acc(kacc, gC);
-            scale_acc(vacc, gC);
+            const float post = uniform(sc.ctl[1]);
+            if (post != 1.f) {
+                scale_acc(kacc, post);
+                scale_acc(vacc, post);
+            }
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const bf16x8 ad = scale_k(rd_tr(At, trl, 16 * ks, 32 * w), sc.rho + 16 * ks + 8 * hl);
@@ -607,6 +670,8 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
                 }
             }
         }
+        Ls = next_scale(sc, Ls);
+        if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
         // -- C: intra-chunk terms; X = U(lambda) p (scale folded into M); slot logits
 #pragma unroll
@@ -615,6 +680,8 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
             pacc = mma(at, rd_row(S1, SSB, l32, 16 * ks, hl), pacc);
             dacc = mma(at, rd_row(S2, SSB, l32, 16 * ks, hl), dacc);
         }
+        float pc[8], ps[8];
+        lane_phases(opqf(sc.urev[l32]), w, hl, m, pc, ps);
         rotate<1>(pacc, pc, ps, 1.f);                 // X' = U(lambda) p;  X = scale X'
         {
             f32x16 xs = pacc;
@@ -642,10 +709,10 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 #pragma unroll
             for (int x = 0; x < 4; ++x) pr[x] = red1[x * kC + l32];
             const float M = fmaxf(fmaxf(pr[0].x, pr[1].x), fmaxf(pr[2].x, pr[3].x));
-            float Ls = 0.f;
+            float Lsum = 0.f;
 #pragma unroll
-            for (int x = 0; x < 4; ++x) Ls += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
-            const float f = __builtin_amdgcn_exp2f(mx - M) / Ls;
+            for (int x = 0; x < 4; ++x) Lsum += pr[x].y * __builtin_amdgcn_exp2f(pr[x].x - M);
+            const float f = __builtin_amdgcn_exp2f(mx - M) / Lsum;
 #pragma unroll
             for (int v = 0; v < 16; ++v) wr[v] *= f;
         }
@@ -659,11 +726,13 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
         lds_barrier();
         // -- D: u = U(-lambda) M^T W; dW = M dY; dM += W dY^T
         float tsum, tclk;
+        float qc[8], qs[8];                            // the phases again (short live ranges)
+        lane_phases(opqf(sc.urev[l32]), w, hl, m, qc, qs);
         {
             f32x16 ya = zero_acc();
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) ya = mma(rd_tr(MZ, trl, 16 * ks, 32 * w), rd_row(Wt, QS, l32, 16 * ks, hl), ya);
-            rotate<-1>(ya, pc, ps, inv_zs);
+            rotate<-1>(ya, qc, qs, inv_zs);
             store_out(a.U + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, ya, true);
             float ud = 0.f;
 #pragma unroll
@@ -714,7 +783,7 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) xa[v] *= fx;
             tclk += scale * rot_part(xa, pacc, w, hl, m);
-            rotate<-1>(xa, pc, ps, scale);
+            rotate<-1>(xa, qc, qs, scale);
             store_block(Wt, l32, 32 * w, h4, xa);
             store_out(a.dP + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, xa, true);
         }
@@ -769,7 +838,7 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 // with (gamma (.) U)^T dO.
 struct ALay {
     static constexpr int Q = 0, O = kT32, U = 2 * kT32, P = 3 * kT32, SC = 4 * kT32;
-    static constexpr int BYTES = SC + 1024;
+    static constexpr int BYTES = SC + kScBytes;
 };
 __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     using L = ALay;
@@ -869,7 +938,7 @@ struct GLay {
     static constexpr int Q = 0, K = kT32, V = 2 * kT32, O = 3 * kT32, U = 4 * kT32, P = 5 * kT32, A = 6 * kT32;
     static constexpr int DK = 7 * kT32, DV = DK + kT128;
     static constexpr int T1 = DV + kT128, T2 = T1 + kTS, T3 = T2 + kTS, T4 = T3 + kTS;
-    static constexpr int SC = T4 + kTS, RED = SC + 1024;
+    static constexpr int SC = T4 + kTS, RED = SC + kScBytes;
     static constexpr int BYTES = RED + 4 * kC * 16;
     static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
 };
@@ -918,10 +987,11 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     const float sq2m = sqrtf(2.f / (float)m), dcw = 1.f / sqrtf((float)m);
     const int J = (m - 1) >> 1;
 
+    float Ls = 0.f;                                   // adjoint states: exp(Ls) x registers
     for (int c = c_end - 1; c >= c_begin; --c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         // -- A: stage, scalars (clock entering the chunk from the forward walk), adjoint
-        //    states at the chunk's end in bf16; prefetch the previous chunk
+        //    states at the chunk's end in bf16, writes
         store_rows(Qt, tid, pq);
         store_rows(Kt, tid, pk);
         store_rows(Vt, tid, pv);
@@ -930,16 +1000,22 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         store_rows(Pt, tid, pp);
         if (w == 0) {
             double carry = a.cclk[(size_t)bh * p.nc + c];
-            chunk_scalars(sc, lane, m, tk, carry, false);
+            chunk_scalars<kLazyAdj>(sc, lane, m, tk, carry, false, Ls);
+        }
+        lds_barrier();
+        {
+            const float pre = uniform(sc.ctl[0]);
+            if (pre != 1.f) {
+                scale_acc(kacc, pre);
+                scale_acc(vacc, pre);
+            }
         }
         dump_tile(DKt, w, l32, h4, kacc);
         dump_tile(DVt, w, l32, h4, vacc);
-        if (c > c_begin) prefetch(c - 1);
-        lds_barrier();
         build_A(sc, At, tid, m);
         lds_barrier();
         // -- B: score tiles (one per wave, stored [s][r]); inter-chunk terms of da, dk,
-        //    dv; adjoint update
+        //    dv; adjoint update; prefetch the previous chunk
         if (w == 0) score_tile<false>(Qt, Kt, T1, sc, l32, hl);   // T1[s][r] = Gamma (q_r . k_s)
         if (w == 1) score_tile<false>(Ot, Vt, T2, sc, l32, hl);   // T2[s][r] = Gamma (do_r . v_s)
         if (w == 2) score_tile<false>(Pt, At, T3, sc, l32, hl);   // T3[s][r] = Gamma (dp_r . a_s)
@@ -947,11 +1023,10 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         const float rs_ = sc.rho[l32];
         f32x16 da = zero_acc(), dka = zero_acc(), dva = zero_acc();
         {
-            const __bf16 *krow = Kt + l32 * QS, *vrow = Vt + l32 * QS;
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                da = mma(acc_to_operand(kacc[ks >> 1], ks & 1), lds8_perm(krow, 16 * ks, hl), da);
-                da = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(vrow, 16 * ks, hl), da);
+                da = mma(rd_row(DKt, QS, 32 * w + l32, 16 * ks, hl), rd_row(Kt, QS, l32, 16 * ks, hl), da);
+                da = mma(rd_row(DVt, QS, 32 * w + l32, 16 * ks, hl), rd_row(Vt, QS, l32, 16 * ks, hl), da);
             }
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
@@ -967,9 +1042,11 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
             }
         }
         {
-            const float gC = sc.gam[kC - 1];
-            scale_acc(kacc, gC);
-            scale_acc(vacc, gC);
+            const float post = uniform(sc.ctl[1]);
+            if (post != 1.f) {
+                scale_acc(kacc, post);
+                scale_acc(vacc, post);
+            }
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const float *gk8 = sc.gam + 16 * ks + 8 * hl;
@@ -982,6 +1059,8 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
                 }
             }
         }
+        Ls = next_scale(sc, Ls);
+        if (c > c_begin) prefetch(c - 1);
         lds_barrier();
         // -- C: intra-chunk terms
 #pragma unroll

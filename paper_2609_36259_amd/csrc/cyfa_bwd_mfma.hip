@@ -12,20 +12,21 @@
 //   (1) fwd_contrib_kernel (b, h, group): the group's own contribution to the
 //       states at its end (zero entering state), the clock entering the group
 //       and the group's total log decay.
-//   (2) fwd_combine_kernel (b, h): the states entering every group, in group
-//       order from (K0, V0), and the final-state loss <dK_T, Kbar_T> + <dV_T, Vbar_T>.
-//   (3) readout_kernel (b, h, group): walks the group's chunks forward with both
-//       states in accumulators, recomputes the key pass p, X, the slot weights W
-//       and u, and forms du, the readout's adjoint (dY, dW, dZ, dX, dp), dq, the
-//       group's part of dM, <q, dq> + <u, du> and the clock gradients of X and u.
-//       u and dp go to the workspace in bf16 for (4) and (6).
-//   (4) adj_contrib_kernel (b, h, group): the group's own contribution to the
+//   (2) readout_kernel (b, h, group): forms the state entering its group from
+//       (K0, V0) and the earlier groups' contributions, then walks the group's
+//       chunks forward with both states in accumulators, recomputes the key
+//       pass p, X, the slot weights W and u, and forms du, the readout's adjoint
+//       (dY, dW, dZ, dX, dp), dq, the group's part of dM, <q, dq> + <u, du> and
+//       the clock gradients of X and u; u and dp go to the workspace in bf16 for
+//       (3) and (4).  The last group ends with the final states and forms the
+//       final-state loss <dK_T, Kbar_T> + <dV_T, Vbar_T>.
+//   (3) adj_contrib_kernel (b, h, group): the group's own contribution to the
 //       adjoint states entering it from its tokens (zero adjoint at its end).
-//   (5) adj_combine_kernel (b, h): the adjoint states at every group's end, in
-//       reverse group order from (dK_T, dV_T); dK0 and dV0.
-//   (6) grad_kernel (b, h, group): walks the group's chunks in reverse with both
-//       adjoint states in accumulators: dk, dv, da and from da the gradient of
-//       beta and the clock gradient of the write a_t, and dL/dG.
+//   (4) grad_kernel (b, h, group): forms the adjoint at its group's end from
+//       (dK_T, dV_T) and the later groups' contributions, then walks the group's
+//       chunks in reverse with both adjoint states in accumulators: dk, dv, da and
+//       from da the gradient of beta and the clock gradient of the write a_t, and
+//       dL/dG.  The first group ends at the sequence start: dK0, dV0.
 // The reverse cumulative sums (dlog_alpha, ddelta, dclock0) and dR = dM Phi^T
 // are the vector-ALU backward's last two kernels (launch_bwd_tail).
 //
@@ -136,6 +137,68 @@ __device__ __forceinline__ void scale_acc(f32x16 (&acc)[4], float f) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[x][v] *= f;
 }
+// acc += f * (a state in the ABI layout [128 paper rows][128], active rows only)
+__device__ __forceinline__ void add_abi_state(f32x16 (&acc)[4], const float *S, float f, int w, int lane, int m) {
+    const int i = 32 * w + (lane & 31);
+    if (!row_active(i, m)) return;
+    const float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
+            acc[x][4 * v4] = fmaf(f, q.x, acc[x][4 * v4]);
+            acc[x][4 * v4 + 1] = fmaf(f, q.y, acc[x][4 * v4 + 1]);
+            acc[x][4 * v4 + 2] = fmaf(f, q.z, acc[x][4 * v4 + 2]);
+            acc[x][4 * v4 + 3] = fmaf(f, q.w, acc[x][4 * v4 + 3]);
+        }
+}
+// acc += f * (a state in the dump layout)
+__device__ __forceinline__ void add_dump_state(f32x16 (&acc)[4], const float *E, float f, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 e = *reinterpret_cast<const float4 *>(E + dump_off(w, x, lane, 4 * q));
+            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
+            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
+            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
+            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+        }
+}
+// sum over the lane's elements of S (ABI layout, active rows) times acc
+__device__ __forceinline__ float dot_abi_state(const f32x16 (&acc)[4], const float *S, int w, int lane, int m) {
+    const int i = 32 * w + (lane & 31);
+    if (!S || !row_active(i, m)) return 0.f;
+    const float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
+    float t = 0.f;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
+            t = fmaf(q.x, acc[x][4 * v4], t);
+            t = fmaf(q.y, acc[x][4 * v4 + 1], t);
+            t = fmaf(q.z, acc[x][4 * v4 + 2], t);
+            t = fmaf(q.w, acc[x][4 * v4 + 3], t);
+        }
+    return t;
+}
+// f * acc into a state in the ABI layout (rows that are not active written as 0)
+__device__ __forceinline__ void store_abi_state(float *S, const f32x16 (&acc)[4], float f, int w, int lane, int m) {
+    const int i = 32 * w + (lane & 31);
+    const bool act = row_active(i, m);
+    float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4)
+            *reinterpret_cast<float4 *>(row + 32 * x + 8 * v4) =
+                act ? make_float4(f * acc[x][4 * v4], f * acc[x][4 * v4 + 1], f * acc[x][4 * v4 + 2],
+                                  f * acc[x][4 * v4 + 3])
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 // accumulators as bf16 rows of a [128][QS] tile: row i, columns c .. c+3 per store
 __device__ __forceinline__ void dump_tile(__bf16 *T, int w, int l32, int h4, const f32x16 (&acc)[4]) {
     __bf16 *row = T + (32 * w + l32) * QS + h4;
@@ -268,7 +331,6 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
     if (lane < kC) {
         s.G[lane] = G;
         float gam = __expf(G), rho = __expf(GC - G);
-        const float amp_dec = rho;
         if (lazy) {
             if (kMode == kLazy) {
                 gam = __expf(G + Ls);
@@ -285,7 +347,7 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
         s.urev[lane] = u;
         float s1, c1;
         sincos_rev(u, &s1, &c1);
-        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? amp_dec : 1.f), u, c1, s1);
+        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? rho : 1.f), u, c1, s1);
     }
     if (kMode != kPlain && lane == 0) {
         s.ctl[0] = lazy ? 1.f : __expf(Ls);
@@ -471,27 +533,35 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
-    double gsum = 0.0;
-    for (int c = c_begin; c < c_end; ++c) {
+    Rows2 rk, rv;
+    Tok tk;
+    auto prefetch = [&](int c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
-        {
-            Rows2 rk, rv;
-            const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
-            load_rows(kin + base, rs, n, tid, rk);
-            load_rows(vin + base, rs, n, tid, rv);
-            Tok tk;
-            load_tok(p, b, h, t0, Tb, tid, tk);
-            store_rows(Kt, tid, rk);
-            store_rows(Vt, tid, rv);
-            if (w == 0) chunk_scalars<kPlain>(sc, lane, m, tk, carry, true);
-        }
+        const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+        load_rows(kin + base, rs, n, tid, rk);
+        load_rows(vin + base, rs, n, tid, rv);
+        load_tok(p, b, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_begin);
+    double gsum = 0.0;
+    float Ls = 0.f;                                   // states: exp(Ls) x registers
+    for (int c = c_begin; c < c_end; ++c) {
+        store_rows(Kt, tid, rk);
+        store_rows(Vt, tid, rv);
+        if (w == 0) chunk_scalars<kLazy>(sc, lane, m, tk, carry, true, Ls);
+        if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
         build_A(sc, At, tid, m);
-        lds_barrier();
-        const float gC = sc.gam[kC - 1];
         gsum += (double)sc.G[kC - 1];
-        scale_acc(kacc, gC);
-        scale_acc(vacc, gC);
+        {
+            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
+            if (f != 1.f) {
+                scale_acc(kacc, f);
+                scale_acc(vacc, f);
+            }
+        }
+        Ls = next_scale(sc, Ls);
+        lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const bf16x8 ad = rd_tr(At, trl, 16 * ks, 32 * w);
@@ -503,42 +573,12 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
         }
         lds_barrier();
     }
+    scale_acc(kacc, __expf(Ls));
+    scale_acc(vacc, __expf(Ls));
     float *E = a.Ef + ((size_t)bh * p.groups + g) * 2 * kSE;
     store_acc(E, w, lane, kacc);
     store_acc(E + kSE, w, lane, vacc);
     if (tid == 0) a.Gg[(size_t)bh * p.groups + g] = (float)gsum;
-}
-
-// (2) states entering each group, from (K0, V0) in group order; the final-state
-// loss <dK_T, Kbar_T> + <dV_T, Vbar_T> in kCombBlocks partial sums.
-__global__ __launch_bounds__(kNT) void fwd_combine_kernel(Args a) {
-    __shared__ float red[kNT / 64];
-    const BwdParams &p = a.p;
-    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
-    const float *Gg = a.Gg + (size_t)bh * G;
-    float acc = 0.f;
-    for (int e = blockIdx.y * kNT + tid; e < 2 * kSE; e += kCombBlocks * kNT) {
-        const int st = e / kSE, f = e % kSE;
-        int i, c;
-        dump_coords(f, i, c);
-        const bool act = row_active(i, m);
-        const size_t ai = ((size_t)bh * kStoreRows + paper_row(i)) * 128 + c;
-        const float *init = st ? p.V0 : p.K0;
-        const float *fin = st ? p.dV_T : p.dK_T;
-        float E = (init && act) ? init[ai] : 0.f;
-        for (int q = 0; q < G; ++q) {
-            float *slot = a.Ef + (((size_t)bh * G + q) * 2 + st) * kSE + f;
-            const float own = *slot;
-            *slot = E;
-            E = fmaf(__expf(Gg[q]), E, own);
-        }
-        if (fin && act) acc = fmaf(fin[ai], E, acc);
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-    if ((tid & 63) == 0) red[tid >> 6] = acc;
-    __syncthreads();
-    if (tid == 0) p.fin[(size_t)bh * kCombBlocks + blockIdx.y] = red[0] + red[1] + red[2] + red[3];
 }
 
 // ---------------------------------------------------------------------------
@@ -589,11 +629,26 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
     }
     f32x16 kacc[4], vacc[4], macc[4];
     {
-        const float *E = a.Ef + ((size_t)bh * p.groups + g) * 2 * kSE;
-        load_acc(E, w, lane, kacc);
-        load_acc(E + kSE, w, lane, vacc);
+        // state entering the group: (K0, V0) decayed through the earlier groups, plus each
+        // earlier group's contribution decayed through the groups after it
 #pragma unroll
-        for (int x = 0; x < 4; ++x) macc[x] = zero_acc();
+        for (int x = 0; x < 4; ++x) {
+            kacc[x] = zero_acc();
+            vacc[x] = zero_acc();
+            macc[x] = zero_acc();
+        }
+        const float *Gg = a.Gg + (size_t)bh * p.groups;
+        float tail = 0.f;                         // log decay of groups q+1 .. g-1
+        for (int q = g - 1; q >= 0; --q) {
+            const float f = __expf(tail);
+            const float *E = a.Ef + ((size_t)bh * p.groups + q) * 2 * kSE;
+            add_dump_state(kacc, E, f, w, lane);
+            add_dump_state(vacc, E + kSE, f, w, lane);
+            tail += Gg[q];
+        }
+        const size_t sb = (size_t)bh * kStoreRows * 128;
+        if (p.K0) add_abi_state(kacc, p.K0 + sb, __expf(tail), w, lane, m);
+        if (p.V0) add_abi_state(vacc, p.V0 + sb, __expf(tail), w, lane, m);
     }
     double carry = a.gclk[(size_t)bh * p.groups + g];
     const size_t rs = (size_t)p.H * 128;
@@ -819,6 +874,18 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
             p.dlam[ti] = lv ? s2 * (kTwoPi / (float)m) : 0.f;
         }
     }
+    // the last group holds the final states: the loss <dK_T, Kbar_T> + <dV_T, Vbar_T>
+    if (g == p.groups - 1) {
+        const size_t sb = (size_t)bh * kStoreRows * 128;
+        float t = __expf(Ls) * (dot_abi_state(kacc, p.dK_T ? p.dK_T + sb : nullptr, w, lane, m) +
+                                dot_abi_state(vacc, p.dV_T ? p.dV_T + sb : nullptr, w, lane, m));
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
+        if (lane == 0) {
+            p.fin[(size_t)bh * kCombBlocks + w] = t;
+            p.fin[(size_t)bh * kCombBlocks + 4 + w] = 0.f;
+        }
+    }
     // the group's dM in paper column order
     float *dMo = p.dMp + ((size_t)bh * p.groups + g) * 128 * 128;
 #pragma unroll
@@ -860,32 +927,39 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *qin = static_cast<const __bf16 *>(p.q), *oin = static_cast<const __bf16 *>(p.dout);
-    for (int c = c_end - 1; c >= c_begin; --c) {
+    Rows2 rq, ro, ru, rp;
+    Tok tk;
+    auto prefetch = [&](int c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
+        const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
+        load_rows(qin + base, rs, n, tid, rq);
+        load_rows(oin + base, rs, n, tid, ro);
+        load_rows(a.U + wb, 128, kC, tid, ru);
+        load_rows(a.dP + wb, 128, kC, tid, rp);
+        tk.g = 0.f;
+        tk.dl = 0.f;
+        tk.be = 0.f;
+        if (tid < kC && t0 + tid < Tb && p.log_alpha) tk.g = p.log_alpha[((size_t)b * p.T + t0 + tid) * p.H + h];
+    };
+    if (c_begin < c_end) prefetch(c_end - 1);
+    float Ls = 0.f;                                   // adjoint states: exp(Ls) x registers
+    double clk = 0.0;                                 // (the clock is not used here)
+    for (int c = c_end - 1; c >= c_begin; --c) {
+        store_rows(Qt, tid, rq);
+        store_rows(Ot, tid, ro);
+        store_rows(Ut, tid, ru);
+        store_rows(Pt, tid, rp);
+        if (w == 0) chunk_scalars<kLazyAdj>(sc, lane, 3, tk, clk, false, Ls);
+        if (c > c_begin) prefetch(c - 1);
+        lds_barrier();
         {
-            Rows2 rq, ro, ru, rp;
-            const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
-            const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
-            load_rows(qin + base, rs, n, tid, rq);
-            load_rows(oin + base, rs, n, tid, ro);
-            load_rows(a.U + wb, 128, kC, tid, ru);
-            load_rows(a.dP + wb, 128, kC, tid, rp);
-            float lg = 0.f;
-            if (tid < kC && t0 + tid < Tb && p.log_alpha)
-                lg = p.log_alpha[((size_t)b * p.T + t0 + tid) * p.H + h];
-            store_rows(Qt, tid, rq);
-            store_rows(Ot, tid, ro);
-            store_rows(Ut, tid, ru);
-            store_rows(Pt, tid, rp);
-            if (w == 0) {
-                const float G = wave_incl_scan(lg);
-                if (lane < kC) sc.gam[lane] = __expf(G);
+            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
+            if (f != 1.f) {
+                scale_acc(kacc, f);
+                scale_acc(vacc, f);
             }
         }
-        lds_barrier();
-        const float gC = sc.gam[kC - 1];
-        scale_acc(kacc, gC);
-        scale_acc(vacc, gC);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const float *gk = sc.gam + 16 * ks + 8 * hl;
@@ -897,36 +971,14 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
                 vacc[x] = mma(rd_tr(Ot, trl, 16 * ks, 32 * x), bu, vacc[x]);
             }
         }
+        Ls = next_scale(sc, Ls);
         lds_barrier();
     }
+    scale_acc(kacc, __expf(Ls));
+    scale_acc(vacc, __expf(Ls));
     float *E = a.Ea + ((size_t)bh * p.groups + g) * 2 * kSE;
     store_acc(E, w, lane, kacc);
     store_acc(E + kSE, w, lane, vacc);
-}
-
-// (5) adjoint states at each group's end, in reverse group order from (dK_T, dV_T);
-// the adjoint of the initial state is dK0, dV0 (paper row order, rows >= m zero).
-__global__ __launch_bounds__(kNT) void adj_combine_kernel(Args a) {
-    const BwdParams &p = a.p;
-    const int bh = blockIdx.x, tid = threadIdx.x, m = p.m, G = p.groups;
-    const float *Gg = a.Gg + (size_t)bh * G;
-    for (int e = blockIdx.y * kNT + tid; e < 2 * kSE; e += kCombBlocks * kNT) {
-        const int st = e / kSE, f = e % kSE;
-        int i, c;
-        dump_coords(f, i, c);
-        const bool act = row_active(i, m);
-        const size_t ai = ((size_t)bh * kStoreRows + paper_row(i)) * 128 + c;
-        const float *fin = st ? p.dV_T : p.dK_T;
-        float *g0 = st ? p.gV0 : p.gK0;
-        float A = (fin && act) ? fin[ai] : 0.f;
-        for (int q = G - 1; q >= 0; --q) {
-            float *slot = a.Ea + (((size_t)bh * G + q) * 2 + st) * kSE + f;
-            const float own = *slot;
-            *slot = A;
-            A = fmaf(__expf(Gg[q]), A, own);
-        }
-        if (g0) g0[ai] = act ? A : 0.f;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -961,9 +1013,25 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     const int trl = tr_off(QS, lane);
     f32x16 kacc[4], vacc[4];
     {
-        const float *E = a.Ea + ((size_t)bh * p.groups + g) * 2 * kSE;
-        load_acc(E, w, lane, kacc);
-        load_acc(E + kSE, w, lane, vacc);
+        // adjoint at the group's end: (dK_T, dV_T) decayed through the later groups, plus
+        // each later group's own contribution decayed through the groups before it
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            kacc[x] = zero_acc();
+            vacc[x] = zero_acc();
+        }
+        const float *Gg = a.Gg + (size_t)bh * p.groups;
+        float head = 0.f;                         // log decay of groups g+1 .. q-1
+        for (int q = g + 1; q < p.groups; ++q) {
+            const float f = __expf(head);
+            const float *E = a.Ea + ((size_t)bh * p.groups + q) * 2 * kSE;
+            add_dump_state(kacc, E, f, w, lane);
+            add_dump_state(vacc, E + kSE, f, w, lane);
+            head += Gg[q];
+        }
+        const size_t sb = (size_t)bh * kStoreRows * 128;
+        if (p.dK_T) add_abi_state(kacc, p.dK_T + sb, __expf(head), w, lane, m);
+        if (p.dV_T) add_abi_state(vacc, p.dV_T + sb, __expf(head), w, lane, m);
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
@@ -1115,6 +1183,13 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
             if (p.gbeta && t0 + lane < p.T) p.gbeta[((size_t)b * p.T + t0 + lane) * p.H + h] = lv ? s2 : 0.f;
         }
     }
+    // the first group ends at the sequence start: its adjoints are dK0, dV0
+    if (g == 0) {
+        const size_t sb = (size_t)bh * kStoreRows * 128;
+        const float f = __expf(Ls);
+        if (p.gK0) store_abi_state(p.gK0 + sb, kacc, f, w, lane, m);
+        if (p.gV0) store_abi_state(p.gV0 + sb, vacc, f, w, lane, m);
+    }
 }
 
 }  // namespace
@@ -1165,12 +1240,10 @@ hipError_t launch_bwd_mfma(BwdParams p, void *ws, hipStream_t s) {
     a.p = p;
     hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, Mz, p.scale * 1.4426950408889634f, s);
     if (e != hipSuccess) return e;
-    const dim3 block(kNT), grp(BH, G), comb(BH, kCombBlocks);
+    const dim3 block(kNT), grp(BH, G);
     hipLaunchKernelGGL(fwd_contrib_kernel, grp, block, 0, s, a);
-    hipLaunchKernelGGL(fwd_combine_kernel, comb, block, 0, s, a);
     hipLaunchKernelGGL(readout_kernel, grp, block, 0, s, a);
     hipLaunchKernelGGL(adj_contrib_kernel, grp, block, 0, s, a);
-    hipLaunchKernelGGL(adj_combine_kernel, comb, block, 0, s, a);
     hipLaunchKernelGGL(grad_kernel, grp, block, 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

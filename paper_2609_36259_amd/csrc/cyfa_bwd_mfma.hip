@@ -65,8 +65,8 @@ namespace {
 
 constexpr int kC = kBwdMfmaChunk;   // tokens per chunk
 constexpr int kNT = 256;            // threads per workgroup (four waves)
-constexpr int kT32 = kC * QS * 2;   // bytes of a padded [32][128] bf16 tile
-constexpr int kT128 = 128 * QS * 2; // bytes of a padded [128][128] bf16 tile
+constexpr int kT32 = kC * 288;      // bytes of a padded [32][128] bf16 tile (row stride 144)
+constexpr int kT128 = 128 * 288;    // bytes of a padded [128][128] bf16 tile
 constexpr int SSB = 40;             // row stride (bf16) of a [32][32] score tile
 constexpr int kTS = kC * SSB * 2;   // bytes of a score tile
 constexpr int kSE = 128 * 128;      // floats of one 128 x 128 state
@@ -199,9 +199,57 @@ __device__ __forceinline__ void store_abi_state(float *S, const f32x16 (&acc)[4]
                     : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// accumulators as bf16 rows of a [128][QS] tile: row i, columns c .. c+3 per store
-__device__ __forceinline__ void dump_tile(__bf16 *T, int w, int l32, int h4, const f32x16 (&acc)[4]) {
-    __bf16 *row = T + (32 * w + l32) * QS + h4;
+// ---- padded tiles ----------------------------------------------------------------
+// [rows][128] bf16 tiles with a row stride of PS = 144 elements (288 bytes: each row
+// starts 8 banks after the previous one).  Transposed operands (sixteen lanes read 32
+// bytes from each of four consecutive rows) and row operands (eight lanes read 16 bytes
+// from each of eight consecutive rows) are then free of bank conflicts; 8-byte
+// accesses of sixteen consecutive rows at one column meet rows r and r + 8 in the same
+// banks.  Every offset is a lane constant plus a compile-time term, which the LDS
+// instructions take as their immediate offset.
+constexpr int PS = 144;
+constexpr int PSB = PS * 2;                 // row stride in bytes
+
+struct Sw {
+    int row;    // row operand: row lane%32, columns 8 (lane/32) ..          (+ 32 ks bytes)
+    int st;     // 8-byte pieces: row lane%32, columns 4 (lane/32) ..        (+ 2 col bytes)
+    int tr;     // transposed operand (tr_off)                               (+ rows, columns)
+    int cp;     // 16-byte pieces of whole rows: row tid/16, columns 8 (tid%16) ..
+};
+__device__ __forceinline__ Sw make_sw(int tid) {
+    const int lane = tid & 63, l32 = lane & 31, hl = lane >> 5;
+    Sw z;
+    z.row = l32 * PSB + 16 * hl;
+    z.st = l32 * PSB + 8 * hl;
+    z.tr = 2 * tr_off(PS, lane);
+    z.cp = (tid >> 4) * PSB + (tid & 15) * 16;
+    return z;
+}
+__device__ __forceinline__ const char *cbyte(const __bf16 *T) { return reinterpret_cast<const char *>(T); }
+__device__ __forceinline__ char *cbyte(__bf16 *T) { return reinterpret_cast<char *>(T); }
+
+// Row operand: element [r0 + lane%32][16 ks + 8 (lane/32) + p].
+__device__ __forceinline__ bf16x8 srow(const __bf16 *T, int r0, int ks, const Sw &z) {
+    return *reinterpret_cast<const bf16x8 *>(cbyte(T) + z.row + r0 * PSB + 32 * ks);
+}
+// Row operand in the permuted k order of a fed-back accumulator: columns
+// 16 ks + 4 (lane/32) .. +3 and 16 ks + 8 + 4 (lane/32) .. +3 of row lane%32.
+__device__ __forceinline__ bf16x8 sperm(const __bf16 *T, int ks, const Sw &z) {
+    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(cbyte(T) + z.st + 32 * ks);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(cbyte(T) + z.st + 32 * ks + 16);
+    bf16x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+}
+// Transposed operand: element [k0 + 8 (lane/32) + p][n0 + lane % 32].
+__device__ __forceinline__ bf16x8 stro(const __bf16 *T, int k0, int n0, const Sw &z) {
+    return lds8_tr(reinterpret_cast<const __bf16 *>(cbyte(T) + z.tr) + k0 * PS + n0, PS);
+}
+// Accumulators as bf16 rows of a [128][PS] tile: row 32 w + lane%32, columns
+// 32 x + 8 g4 + 4 (lane/32) .. +3 per store.
+__device__ __forceinline__ void dump_tile(__bf16 *T, int w, const f32x16 (&acc)[4], const Sw &z) {
+    char *b = cbyte(T) + z.st + 32 * w * PSB;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -209,29 +257,31 @@ __device__ __forceinline__ void dump_tile(__bf16 *T, int w, int l32, int h4, con
             bf16x4 o;
 #pragma unroll
             for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[x][4 * g4 + e];
-            *reinterpret_cast<bf16x4 *>(row + 32 * x + 8 * g4) = o;
+            *reinterpret_cast<bf16x4 *>(b + 2 * (32 * x + 8 * g4)) = o;
         }
 }
-
 // A 32 x 32 output block D[m][n] in registers (lane: n = lane % 32; register v:
-// m = 8 (v / 4) + 4 (lane / 32) + v % 4) stored as bf16 rows of a [32][QS] tile
-// at row n, columns col0 + m.
-__device__ __forceinline__ void store_block(__bf16 *T, int l32, int col0, int h4, const f32x16 &acc) {
-    __bf16 *row = T + l32 * QS + col0 + h4;
+// m = 8 (v / 4) + 4 (lane / 32) + v % 4) stored as bf16 rows of a [32][PS] tile at
+// row n, columns col0 + m.
+__device__ __forceinline__ void store_block(__bf16 *T, int col0, const f32x16 &acc, const Sw &z) {
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
         bf16x4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[4 * g4 + e];
-        *reinterpret_cast<bf16x4 *>(row + 8 * g4) = o;
+        *reinterpret_cast<bf16x4 *>(cbyte(T) + z.st + 2 * (col0 + 8 * g4)) = o;
     }
 }
-
-// Transposed operand from a padded tile: element [k0 + 8 (lane/32) + p][n0 + lane % 32].
-__device__ __forceinline__ bf16x8 rd_tr(const __bf16 *T, int trl, int k0, int n0) {
-    return lds8_tr(T + trl + k0 * QS + n0, QS);
+// The same block read back as floats.
+__device__ __forceinline__ void load_block(const __bf16 *T, int col0, f32x16 &acc, const Sw &z) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        const bf16x4 x4 = *reinterpret_cast<const bf16x4 *>(cbyte(T) + z.st + 2 * (col0 + 8 * g4));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[4 * g4 + e] = (float)x4[e];
+    }
 }
-// Row operand: element [row][k0 + 8 (lane/32) + p] of a tile with row stride `stride`.
+// Row operand of a padded score tile (row stride SSB): element [row][k0 + 8 (lane/32) + p].
 __device__ __forceinline__ bf16x8 rd_row(const __bf16 *T, int stride, int row, int k0, int hl) {
     return lds8(T + row * stride + k0 + 8 * hl);
 }
@@ -264,10 +314,9 @@ __device__ __forceinline__ void load_rows(const __bf16 *base, size_t row_stride,
         o.r[it] = r < n ? v : make_uint4(0, 0, 0, 0);
     }
 }
-__device__ __forceinline__ void store_rows(__bf16 *T, int tid, const Rows2 &o) {
-    const int r0 = tid >> 4, c8 = (tid & 15) * 8;
+__device__ __forceinline__ void store_rows(__bf16 *T, const Rows2 &o, const Sw &z) {
 #pragma unroll
-    for (int it = 0; it < 2; ++it) *reinterpret_cast<uint4 *>(T + (r0 + 16 * it) * QS + c8) = o.r[it];
+    for (int it = 0; it < 2; ++it) *reinterpret_cast<uint4 *>(cbyte(T) + 16 * PSB * it + z.cp) = o.r[it];
 }
 
 // Per-token scalars of a chunk (lanes 0..31 of wave 0; zero elsewhere and past the
@@ -295,8 +344,11 @@ struct Sc {
     float rho[kC];    // exp(G_C - G_r) (likewise)
     float urev[kC];   // clock after token r over m, mod 1 (revolutions)
     float4 bw[kC];    // write-builder record: amplitude, urev, cos and sin of 2 pi urev
+    float ea[kC];     // exp(G_r) and exp(-G_r): Gamma_rs = ea_r eb_s when every |G_r| <= 60
+    float eb[kC];
     float ctl[4];     // lazily scaled kernels: [0] factor applied to the carried states
-                      // before the chunk, [1] factor applied before their update
+                      // before the chunk, [1] factor applied before their update; [3]: 1 when
+                      // Gamma factors into ea, eb
 };
 constexpr int kScBytes = sizeof(Sc);
 static_assert(kScBytes % 16 == 0, "scalar block");
@@ -323,13 +375,13 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
     const float G = wave_incl_scan(k.g);
     const double lam = carry + wave_incl_scan((double)k.dl);
     const float GC = lane63(G);
+    const float gabs = wave_max_nonneg(fabsf(G));
     bool lazy = false;
-    if (kMode != kPlain) {
-        const float gabs = wave_max_nonneg(fabsf(G));
-        lazy = fabsf(Ls) + (kMode == kLazyAdj ? 2.f : 1.f) * gabs <= 60.f;
-    }
+    if (kMode != kPlain) lazy = fabsf(Ls) + (kMode == kLazyAdj ? 2.f : 1.f) * gabs <= 60.f;
     if (lane < kC) {
         s.G[lane] = G;
+        s.ea[lane] = __expf(G);
+        s.eb[lane] = __expf(-G);
         float gam = __expf(G), rho = __expf(GC - G);
         if (lazy) {
             if (kMode == kLazy) {
@@ -349,10 +401,11 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
         sincos_rev(u, &s1, &c1);
         s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m) * (dec_amp ? rho : 1.f), u, c1, s1);
     }
-    if (kMode != kPlain && lane == 0) {
+    if (lane == 0) {
         s.ctl[0] = lazy ? 1.f : __expf(Ls);
         s.ctl[1] = lazy ? 1.f : __expf(GC);
         s.ctl[2] = lazy ? 1.f : 0.f;
+        s.ctl[3] = gabs <= 60.f ? 1.f : 0.f;
     }
     carry = reduce_clock(lane63(lam), (double)m, inv_m);
 }
@@ -361,12 +414,12 @@ __device__ __forceinline__ float next_scale(const Sc &s, float Ls) {
     return s.ctl[2] != 0.f ? Ls + s.G[kC - 1] : 0.f;
 }
 
-// Temporal write rows (Eq. app-temporal-writes) into a padded [32][QS] tile:
+// Temporal write rows (Eq. app-temporal-writes) into a padded [32][PS] tile:
 // amp_r [cos th_j, -sin th_j] on pair j (internal columns 2j-2, 2j-1), amp_r /
 // sqrt 2 = beta_r / sqrt m on DC (126), 0 on 127.  Thread (row tid/16 + 16 it,
 // q = tid % 16) fills columns 8q .. 8q+7 (pairs 4q+1 .. 4q+4); the phases advance
 // by angle addition from a start reduced in revolutions.
-__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) {
+__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m, const Sw &z) {
     const int q = tid & 15, r0 = tid >> 4;
     const int J = (m - 1) >> 1;
 #pragma unroll 1
@@ -395,7 +448,7 @@ __device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) 
                 sn = ns;
             }
         }
-        *reinterpret_cast<bf16x8 *>(T + r * QS + 8 * q) = a8;
+        *reinterpret_cast<bf16x8 *>(cbyte(T) + 16 * PSB * it + z.cp) = a8;
     }
 }
 
@@ -440,31 +493,49 @@ __device__ __forceinline__ float rot_part(const f32x16 &dz, const f32x16 &z, int
     return acc;
 }
 
-// Masked score tile into S (bf16, [32][SSB]): D[mr][nr] = sum_k Am[mr][k] Bn[nr][k]
-// over 128 columns (lane: nr = lane % 32; registers: mr), times Gamma and stored at
-// S[nr][mr .. mr+3].  kLaneLater: the lane's token nr is the later one (Gamma_{nr,mr},
-// mr <= nr); otherwise mr is (Gamma_{mr,nr}, mr >= nr).
+// One 16 x 16 block of a masked 32 x 32 score tile into S (bf16, [32][SSB]):
+// D[mr][nr] = sum_k Am[mr][k] Bn[nr][k] over 128 columns for mr in m0 .. m0+15 and nr in
+// n0 .. n0+15 (v_mfma_f32_16x16x32: lane nr = n0 + lane % 16, registers mr = m0 +
+// 4 (lane / 16) + q), times Gamma and stored at S[nr][mr .. mr+3].  kLaneLater: nr is
+// the later token (Gamma_{nr,mr}, mr <= nr); otherwise mr is (Gamma_{mr,nr}, mr >= nr).
+// A block on the zero side of the diagonal is written as zeros without products.
+// Gamma is ea eb when the chunk factors (every |G_r| <= 60), else exp of the difference.
 template <bool kLaneLater>
-__device__ __forceinline__ void score_tile(const __bf16 *Am, const __bf16 *Bn, __bf16 *S, const Sc &sc,
-                                           int l32, int hl) {
-    f32x16 acc = zero_acc();
+__device__ __forceinline__ void score_block(const __bf16 *Am, int m0, const __bf16 *Bn, int n0, __bf16 *S,
+                                            const Sc &sc, int lane) {
+    const int l16 = lane & 15, g = lane >> 4;
+    const int nr = n0 + l16, mb = m0 + 4 * g;
+    bf16x4 o = bf16x4{};
+    if (kLaneLater ? m0 <= n0 : m0 >= n0) {
+        f32x4 acc = zero_acc4();
+        const __bf16 *ap = Am + (m0 + l16) * PS + 8 * g;
+        const __bf16 *bp = Bn + nr * PS + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) acc = mma(rd_row(Am, QS, l32, 16 * ks, hl), rd_row(Bn, QS, l32, 16 * ks, hl), acc);
-    const float Gn = sc.G[l32];
-    __bf16 *row = S + l32 * SSB + 4 * hl;
+        for (int ks = 0; ks < 4; ++ks) acc = mma16(lds8(ap + 32 * ks), lds8(bp + 32 * ks), acc);
+        const bool fac = uniform(sc.ctl[3]) != 0.f;
 #pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-        bf16x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int mr = 8 * g4 + 4 * hl + e;
-            const float Gm = sc.G[mr];
-            float val = 0.f;
-            if (kLaneLater ? mr <= l32 : mr >= l32)
-                val = acc[4 * g4 + e] * __expf(kLaneLater ? Gn - Gm : Gm - Gn);
-            o[e] = (__bf16)val;
+        for (int q = 0; q < 4; ++q) {
+            const int mr = mb + q;
+            float gm;
+            if (fac) gm = kLaneLater ? sc.ea[nr] * sc.eb[mr] : sc.ea[mr] * sc.eb[nr];
+            else gm = __expf(kLaneLater ? sc.G[nr] - sc.G[mr] : sc.G[mr] - sc.G[nr]);
+            o[q] = (__bf16)((kLaneLater ? mr <= nr : mr >= nr) ? acc[q] * gm : 0.f);
         }
-        *reinterpret_cast<bf16x4 *>(row + 8 * g4) = o;
+    }
+    *reinterpret_cast<bf16x4 *>(S + nr * SSB + mb) = o;
+}
+
+// Rows 0 .. nrows-1 of a [32][PS] tile to global memory (row r at dst + r row_stride):
+// each group of sixteen lanes writes one whole 256-byte row.
+__device__ __forceinline__ void copy_rows_out(const __bf16 *T, __bf16 *dst, size_t row_stride, int nrows, int tid,
+                                              const Sw &z) {
+    const int r0 = tid >> 4, c8 = (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int r = r0 + 16 * it;
+        if (r < nrows)
+            *reinterpret_cast<uint4 *>(dst + (size_t)r * row_stride + c8) =
+                *reinterpret_cast<const uint4 *>(cbyte(T) + 16 * PSB * it + z.cp);
     }
 }
 
@@ -478,12 +549,12 @@ __device__ __forceinline__ void store_out(__bf16 *dst, const f32x16 &acc, bool l
         *reinterpret_cast<bf16x4 *>(dst + 8 * g4) = o;
     }
 }
-// <row of a bf16 tile, accumulator> over the lane's 16 columns
-__device__ __forceinline__ float dot_row(const __bf16 *row, const f32x16 &acc) {
+// <the lane's part of a bf16 tile block (as store_block), accumulator>
+__device__ __forceinline__ float dot_block(const __bf16 *T, int col0, const f32x16 &acc, const Sw &z) {
     float s = 0.f;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-        const bf16x4 x = *reinterpret_cast<const bf16x4 *>(row + 8 * g4);
+        const bf16x4 x = *reinterpret_cast<const bf16x4 *>(cbyte(T) + z.st + 2 * (col0 + 8 * g4));
 #pragma unroll
         for (int e = 0; e < 4; ++e) s = fmaf((float)x[e], acc[4 * g4 + e], s);
     }
@@ -524,7 +595,7 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
         __syncthreads();
     }
     if (tid == 0) a.gclk[(size_t)bh * p.groups + g] = carry;
-    const int trl = tr_off(QS, lane);
+    const Sw z = make_sw(tid);
     f32x16 kacc[4], vacc[4];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
@@ -546,12 +617,12 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
     double gsum = 0.0;
     float Ls = 0.f;                                   // states: exp(Ls) x registers
     for (int c = c_begin; c < c_end; ++c) {
-        store_rows(Kt, tid, rk);
-        store_rows(Vt, tid, rv);
+        store_rows(Kt, rk, z);
+        store_rows(Vt, rv, z);
         if (w == 0) chunk_scalars<kLazy>(sc, lane, m, tk, carry, true, Ls);
         if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
-        build_A(sc, At, tid, m);
+        build_A(sc, At, tid, m, z);
         gsum += (double)sc.G[kC - 1];
         {
             const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
@@ -564,11 +635,11 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
         lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = rd_tr(At, trl, 16 * ks, 32 * w);
+            const bf16x8 ad = stro(At, 16 * ks, 32 * w, z);
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
-                kacc[x] = mma(rd_tr(Kt, trl, 16 * ks, 32 * x), ad, kacc[x]);
-                vacc[x] = mma(rd_tr(Vt, trl, 16 * ks, 32 * x), ad, vacc[x]);
+                kacc[x] = mma(stro(Kt, 16 * ks, 32 * x, z), ad, kacc[x]);
+                vacc[x] = mma(stro(Vt, 16 * ks, 32 * x, z), ad, vacc[x]);
             }
         }
         lds_barrier();
@@ -583,8 +654,8 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
 
 // ---------------------------------------------------------------------------
 // (3) readout recomputation and its adjoint, per (sequence, chunk group).
-// LDS: padded [32][QS] tiles Q, K, V, dO, A, X, W (later dp), dY (later scale dZ);
-// [128][QS] tiles of the entering key state (bf16) and the readout matrix; three
+// LDS: padded [32][PS] tiles Q, K, V, dO, A, X, W (later dp), dY (later scale dZ);
+// [128][PS] tiles of the entering key state (bf16) and the readout matrix; three
 // score tiles; chunk scalars; per-token reduction slots.
 struct RLay {
     static constexpr int Q = 0, K = kT32, V = 2 * kT32, O = 3 * kT32, A = 4 * kT32;
@@ -614,7 +685,7 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
     float2 *red1 = lds_at<float2>(smem, L::R1);
     float *red2 = lds_at<float>(smem, L::R2);
     float2 *red3 = lds_at<float2>(smem, L::R3);
-    const int trl = tr_off(QS, lane);
+    const Sw z = make_sw(tid);
     const float scale = p.scale;
     const float zs = scale * 1.4426950408889634f;   // the LDS readout matrix is zs M
     const float inv_zs = 1.f / zs;
@@ -624,7 +695,8 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 #pragma unroll
         for (int it = 0; it < 8; ++it) {
             const int e = it * kNT + tid, row = e >> 4, c0 = (e & 15) * 8;
-            *reinterpret_cast<uint4 *>(MZ + row * QS + c0) = *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
+            *reinterpret_cast<uint4 *>(cbyte(MZ) + 16 * PSB * it + z.cp) =
+                *reinterpret_cast<const uint4 *>(Mh + row * 128 + c0);
         }
     }
     f32x16 kacc[4], vacc[4], macc[4];
@@ -672,10 +744,10 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         // -- A: stage the chunk and its scalars; entering key state in bf16; writes
-        store_rows(Qt, tid, pq);
-        store_rows(Kt, tid, pk);
-        store_rows(Vt, tid, pv);
-        store_rows(Ot, tid, po);
+        store_rows(Qt, pq, z);
+        store_rows(Kt, pk, z);
+        store_rows(Vt, pv, z);
+        store_rows(Ot, po, z);
         if (w == 0) {
             if (lane == 0) a.cclk[(size_t)bh * p.nc + c] = carry;
             chunk_scalars<kLazy>(sc, lane, m, tk, carry, false, Ls);
@@ -688,20 +760,21 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
                 scale_acc(vacc, pre);
             }
         }
-        dump_tile(KB, w, l32, h4, kacc);
-        build_A(sc, At, tid, m);
+        dump_tile(KB, w, kacc, z);
+        build_A(sc, At, tid, m, z);
         lds_barrier();
         // -- B: scores, inter-chunk terms of p and du, state update; prefetch the next chunk
         const float gr = sc.gam[l32];
-        if (w == 0) score_tile<true>(Kt, Qt, S1, sc, l32, hl);   // S1[r][s] = Gamma (q_r . k_s)
-        if (w == 1) score_tile<true>(Vt, Ot, S2, sc, l32, hl);   // S2[r][s] = Gamma (do_r . v_s)
+        // S1[r][s] = Gamma (q_r . k_s), S2[r][s] = Gamma (do_r . v_s): wave w forms the 16 x 16
+        // block (r block w / 2, s block w % 2) of each
+        score_block<true>(Kt, 16 * (w & 1), Qt, 16 * (w >> 1), S1, sc, lane);
+        score_block<true>(Vt, 16 * (w & 1), Ot, 16 * (w >> 1), S2, sc, lane);
         f32x16 pacc = zero_acc(), dacc = zero_acc();
         {
-            const __bf16 *orow = Ot + l32 * QS;
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                pacc = mma(rd_row(KB, QS, 32 * w + l32, 16 * ks, hl), rd_row(Qt, QS, l32, 16 * ks, hl), pacc);
-                dacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), lds8_perm(orow, 16 * ks, hl), dacc);
+                pacc = mma(srow(KB, 32 * w, ks, z), srow(Qt, 0, ks, z), pacc);
+                dacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), sperm(Ot, ks, z), dacc);
             }
         }
 #pragma unroll
@@ -717,21 +790,20 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
             }
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 ad = scale_k(rd_tr(At, trl, 16 * ks, 32 * w), sc.rho + 16 * ks + 8 * hl);
+                const bf16x8 ad = scale_k(stro(At, 16 * ks, 32 * w, z), sc.rho + 16 * ks + 8 * hl);
 #pragma unroll
                 for (int x = 0; x < 4; ++x) {
-                    kacc[x] = mma(rd_tr(Kt, trl, 16 * ks, 32 * x), ad, kacc[x]);
-                    vacc[x] = mma(rd_tr(Vt, trl, 16 * ks, 32 * x), ad, vacc[x]);
+                    kacc[x] = mma(stro(Kt, 16 * ks, 32 * x, z), ad, kacc[x]);
+                    vacc[x] = mma(stro(Vt, 16 * ks, 32 * x, z), ad, vacc[x]);
                 }
             }
         }
         Ls = next_scale(sc, Ls);
-        if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
         // -- C: intra-chunk terms; X = U(lambda) p (scale folded into M); slot logits
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 at = rd_tr(At, trl, 16 * ks, 32 * w);
+            const bf16x8 at = stro(At, 16 * ks, 32 * w, z);
             pacc = mma(at, rd_row(S1, SSB, l32, 16 * ks, hl), pacc);
             dacc = mma(at, rd_row(S2, SSB, l32, 16 * ks, hl), dacc);
         }
@@ -741,12 +813,12 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
         {
             f32x16 xs = pacc;
             if (w == 3 && hl == 1) xs[15] = 1.f;      // column 127 = 1: inactive slots get the mask logit
-            store_block(Xt, l32, 32 * w, h4, xs);
+            store_block(Xt, 32 * w, xs, z);
         }
         lds_barrier();
         f32x16 wr = zero_acc();                       // slot logits (log2 units), then W
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) wr = mma(rd_row(MZ, QS, 32 * w + l32, 16 * ks, hl), rd_row(Xt, QS, l32, 16 * ks, hl), wr);
+        for (int ks = 0; ks < 8; ++ks) wr = mma(srow(MZ, 32 * w, ks, z), srow(Xt, 0, ks, z), wr);
         {
             float mx = wr[0];
 #pragma unroll
@@ -771,12 +843,12 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) wr[v] *= f;
         }
-        store_block(Wt, l32, 32 * w, h4, wr);
+        store_block(Wt, 32 * w, wr, z);
         {
             f32x16 dy = dacc;                          // dY = U(lambda) du
             rotate<1>(dy, pc, ps, 1.f);
             if (w == 3 && hl == 1) dy[15] = 0.f;
-            store_block(Yt, l32, 32 * w, h4, dy);
+            store_block(Yt, 32 * w, dy, z);
         }
         lds_barrier();
         // -- D: u = U(-lambda) M^T W; dW = M dY; dM += W dY^T
@@ -786,9 +858,9 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
         {
             f32x16 ya = zero_acc();
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) ya = mma(rd_tr(MZ, trl, 16 * ks, 32 * w), rd_row(Wt, QS, l32, 16 * ks, hl), ya);
+            for (int ks = 0; ks < 8; ++ks) ya = mma(stro(MZ, 16 * ks, 32 * w, z), srow(Wt, 0, ks, z), ya);
             rotate<-1>(ya, qc, qs, inv_zs);
-            store_out(a.U + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, ya, true);
+            store_block(Ot, 32 * w, ya, z);            // u, staged in dO's place
             float ud = 0.f;
 #pragma unroll
             for (int v = 0; v < 16; ++v) ud = fmaf(ya[v], dacc[v], ud);
@@ -797,12 +869,12 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
         }
         f32x16 dw = zero_acc();
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) dw = mma(rd_row(MZ, QS, 32 * w + l32, 16 * ks, hl), rd_row(Yt, QS, l32, 16 * ks, hl), dw);
+        for (int ks = 0; ks < 8; ++ks) dw = mma(srow(MZ, 32 * w, ks, z), srow(Yt, 0, ks, z), dw);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 wa = rd_tr(Wt, trl, 16 * ks, 32 * w);
+            const bf16x8 wa = stro(Wt, 16 * ks, 32 * w, z);
 #pragma unroll
-            for (int x = 0; x < 4; ++x) macc[x] = mma(wa, rd_tr(Yt, trl, 16 * ks, 32 * x), macc[x]);
+            for (int x = 0; x < 4; ++x) macc[x] = mma(wa, stro(Yt, 16 * ks, 32 * x, z), macc[x]);
         }
         {
             float sw = 0.f;
@@ -815,51 +887,56 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
             if (hl == 0) red2[w * kC + l32] = sw;
         }
         lds_barrier();
+        copy_rows_out(Ot, a.U + ((size_t)bh * p.Tpad + t0) * 128, 128, kC, tid, z);
         {
             const float sW = (red2[l32] + red2[kC + l32]) + (red2[2 * kC + l32] + red2[3 * kC + l32]);
             // dZ = W (.) (dW - <W, dW>), stored times scale in the dY tile's place
 #pragma unroll
             for (int v = 0; v < 16; ++v) dw[v] = wr[v] * (dw[v] - sW) * scale;
-            store_block(Yt, l32, 32 * w, h4, dw);
+            store_block(Yt, 32 * w, dw, z);
         }
         lds_barrier();
-        // -- E: dX = M^T dZ; dM += dZ X^T; dp = scale U(-lambda) dX
+        // -- E: dX = M^T dZ; dM += dZ X^T; dp = scale U(-lambda) dX; prefetch the next chunk
+        if (c + 1 < c_end) prefetch(c + 1);
         {
             f32x16 xa = zero_acc();
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) xa = mma(rd_tr(MZ, trl, 16 * ks, 32 * w), rd_row(Yt, QS, l32, 16 * ks, hl), xa);
+            for (int ks = 0; ks < 8; ++ks) xa = mma(stro(MZ, 16 * ks, 32 * w, z), srow(Yt, 0, ks, z), xa);
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 za = rd_tr(Yt, trl, 16 * ks, 32 * w);
+                const bf16x8 za = stro(Yt, 16 * ks, 32 * w, z);
 #pragma unroll
-                for (int x = 0; x < 4; ++x) macc[x] = mma(za, rd_tr(Xt, trl, 16 * ks, 32 * x), macc[x]);
+                for (int x = 0; x < 4; ++x) macc[x] = mma(za, stro(Xt, 16 * ks, 32 * x, z), macc[x]);
             }
             const float fx = inv_zs / scale;
 #pragma unroll
             for (int v = 0; v < 16; ++v) xa[v] *= fx;
-            tclk += scale * rot_part(xa, pacc, w, hl, m);
+            f32x16 xt;                                 // X' from its tile
+            load_block(Xt, 32 * w, xt, z);
+            tclk += scale * rot_part(xa, xt, w, hl, m);
             rotate<-1>(xa, qc, qs, scale);
-            store_block(Wt, l32, 32 * w, h4, xa);
-            store_out(a.dP + ((size_t)bh * p.Tpad + t0 + l32) * 128 + 32 * w + h4, xa, true);
+            store_block(Wt, 32 * w, xa, z);
         }
         lds_barrier();
+        copy_rows_out(Wt, a.dP + ((size_t)bh * p.Tpad + t0) * 128, 128, kC, tid, z);
         // -- F: dq = gamma (.) dP Kbar + (dP A^T (.) Gamma) K
-        if (w == 0) score_tile<true>(At, Wt, S3, sc, l32, hl);   // S3[r][s] = Gamma (dp_r . a_s)
+        score_block<true>(At, 16 * (w & 1), Wt, 16 * (w >> 1), S3, sc, lane);   // S3[r][s] = Gamma (dp_r . a_s)
         f32x16 qa = zero_acc();
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) qa = mma(rd_tr(KB, trl, 16 * ks, 32 * w), rd_row(Wt, QS, l32, 16 * ks, hl), qa);
+        for (int ks = 0; ks < 8; ++ks) qa = mma(stro(KB, 16 * ks, 32 * w, z), srow(Wt, 0, ks, z), qa);
 #pragma unroll
         for (int v = 0; v < 16; ++v) qa[v] *= gr;
         lds_barrier();
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) qa = mma(rd_tr(Kt, trl, 16 * ks, 32 * w), rd_row(S3, SSB, l32, 16 * ks, hl), qa);
-        const bool live = l32 < n;
-        if (t0 + l32 < p.T) store_out(gq + (((size_t)b * p.T + t0 + l32) * p.H + h) * 128 + 32 * w + h4, qa, live);
-        tsum += dot_row(Qt + l32 * QS + 32 * w + h4, qa);
+        for (int ks = 0; ks < 2; ++ks) qa = mma(stro(Kt, 16 * ks, 32 * w, z), rd_row(S3, SSB, l32, 16 * ks, hl), qa);
+        tsum += dot_block(Qt, 32 * w, qa, z);
+        if (l32 >= n) qa = zero_acc();                 // rows past the sequence: dq = 0
+        store_block(Xt, 32 * w, qa, z);                // dq, staged in X's place
         tsum += __shfl_xor(tsum, 32);
         tclk += __shfl_xor(tclk, 32);
         if (hl == 0) red3[w * kC + l32] = make_float2(tsum, tclk);
         lds_barrier();
+        copy_rows_out(Xt, gq + (((size_t)b * p.T + t0) * p.H + h) * 128, (size_t)p.H * 128, min(kC, p.T - t0), tid, z);
         if (w == 0 && lane < kC) {
             float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -918,7 +995,7 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     Sc &sc = *lds_at<Sc>(smem, L::SC);
     __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Ot = lds_at<__bf16>(smem, L::O);
     __bf16 *Ut = lds_at<__bf16>(smem, L::U), *Pt = lds_at<__bf16>(smem, L::P);
-    const int trl = tr_off(QS, lane);
+    const Sw z = make_sw(tid);
     f32x16 kacc[4], vacc[4];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
@@ -946,10 +1023,10 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     float Ls = 0.f;                                   // adjoint states: exp(Ls) x registers
     double clk = 0.0;                                 // (the clock is not used here)
     for (int c = c_end - 1; c >= c_begin; --c) {
-        store_rows(Qt, tid, rq);
-        store_rows(Ot, tid, ro);
-        store_rows(Ut, tid, ru);
-        store_rows(Pt, tid, rp);
+        store_rows(Qt, rq, z);
+        store_rows(Ot, ro, z);
+        store_rows(Ut, ru, z);
+        store_rows(Pt, rp, z);
         if (w == 0) chunk_scalars<kLazyAdj>(sc, lane, 3, tk, clk, false, Ls);
         if (c > c_begin) prefetch(c - 1);
         lds_barrier();
@@ -963,12 +1040,12 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const float *gk = sc.gam + 16 * ks + 8 * hl;
-            const bf16x8 bp = scale_k(rd_tr(Pt, trl, 16 * ks, 32 * w), gk);
-            const bf16x8 bu = scale_k(rd_tr(Ut, trl, 16 * ks, 32 * w), gk);
+            const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * w, z), gk);
+            const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * w, z), gk);
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
-                kacc[x] = mma(rd_tr(Qt, trl, 16 * ks, 32 * x), bp, kacc[x]);
-                vacc[x] = mma(rd_tr(Ot, trl, 16 * ks, 32 * x), bu, vacc[x]);
+                kacc[x] = mma(stro(Qt, 16 * ks, 32 * x, z), bp, kacc[x]);
+                vacc[x] = mma(stro(Ot, 16 * ks, 32 * x, z), bu, vacc[x]);
             }
         }
         Ls = next_scale(sc, Ls);
@@ -983,7 +1060,7 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
 
 // ---------------------------------------------------------------------------
 // (6) token gradients, per (sequence, chunk group), chunks in reverse.
-// LDS: padded [32][QS] tiles Q, K, V, dO, U, dP, A; [128][QS] tiles of the adjoint
+// LDS: padded [32][PS] tiles Q, K, V, dO, U, dP, A; [128][PS] tiles of the adjoint
 // states at the chunk's end (bf16); four score tiles stored [s][r]; scalars;
 // per-token reduction slots.
 struct GLay {
@@ -1010,7 +1087,7 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     __bf16 *T1 = lds_at<__bf16>(smem, L::T1), *T2 = lds_at<__bf16>(smem, L::T2);
     __bf16 *T3 = lds_at<__bf16>(smem, L::T3), *T4 = lds_at<__bf16>(smem, L::T4);
     float4 *red = lds_at<float4>(smem, L::RED);
-    const int trl = tr_off(QS, lane);
+    const Sw z = make_sw(tid);
     f32x16 kacc[4], vacc[4];
     {
         // adjoint at the group's end: (dK_T, dV_T) decayed through the later groups, plus
@@ -1060,12 +1137,12 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         // -- A: stage, scalars (clock entering the chunk from the forward walk), adjoint
         //    states at the chunk's end in bf16, writes
-        store_rows(Qt, tid, pq);
-        store_rows(Kt, tid, pk);
-        store_rows(Vt, tid, pv);
-        store_rows(Ot, tid, po);
-        store_rows(Ut, tid, pu);
-        store_rows(Pt, tid, pp);
+        store_rows(Qt, pq, z);
+        store_rows(Kt, pk, z);
+        store_rows(Vt, pv, z);
+        store_rows(Ot, po, z);
+        store_rows(Ut, pu, z);
+        store_rows(Pt, pp, z);
         if (w == 0) {
             double carry = a.cclk[(size_t)bh * p.nc + c];
             chunk_scalars<kLazyAdj>(sc, lane, m, tk, carry, false, Ls);
@@ -1078,29 +1155,34 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
                 scale_acc(vacc, pre);
             }
         }
-        dump_tile(DKt, w, l32, h4, kacc);
-        dump_tile(DVt, w, l32, h4, vacc);
-        build_A(sc, At, tid, m);
+        dump_tile(DKt, w, kacc, z);
+        dump_tile(DVt, w, vacc, z);
+        build_A(sc, At, tid, m, z);
         lds_barrier();
         // -- B: score tiles (one per wave, stored [s][r]); inter-chunk terms of da, dk,
         //    dv; adjoint update; prefetch the previous chunk
-        if (w == 0) score_tile<false>(Qt, Kt, T1, sc, l32, hl);   // T1[s][r] = Gamma (q_r . k_s)
-        if (w == 1) score_tile<false>(Ot, Vt, T2, sc, l32, hl);   // T2[s][r] = Gamma (do_r . v_s)
-        if (w == 2) score_tile<false>(Pt, At, T3, sc, l32, hl);   // T3[s][r] = Gamma (dp_r . a_s)
-        if (w == 3) score_tile<false>(Ut, At, T4, sc, l32, hl);   // T4[s][r] = Gamma (u_r . a_s)
+        // T1[s][r] = Gamma (q_r . k_s), T2 (do_r . v_s), T3 (dp_r . a_s), T4 (u_r . a_s): wave w
+        // forms the 16 x 16 block (s block w / 2, r block w % 2) of each
+        {
+            const int m0 = 16 * (w & 1), n0 = 16 * (w >> 1);
+            score_block<false>(Qt, m0, Kt, n0, T1, sc, lane);
+            score_block<false>(Ot, m0, Vt, n0, T2, sc, lane);
+            score_block<false>(Pt, m0, At, n0, T3, sc, lane);
+            score_block<false>(Ut, m0, At, n0, T4, sc, lane);
+        }
         const float rs_ = sc.rho[l32];
         f32x16 da = zero_acc(), dka = zero_acc(), dva = zero_acc();
         {
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                da = mma(rd_row(DKt, QS, 32 * w + l32, 16 * ks, hl), rd_row(Kt, QS, l32, 16 * ks, hl), da);
-                da = mma(rd_row(DVt, QS, 32 * w + l32, 16 * ks, hl), rd_row(Vt, QS, l32, 16 * ks, hl), da);
+                da = mma(srow(DKt, 32 * w, ks, z), srow(Kt, 0, ks, z), da);
+                da = mma(srow(DVt, 32 * w, ks, z), srow(Vt, 0, ks, z), da);
             }
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 ar = rd_row(At, QS, l32, 16 * ks, hl);
-                dka = mma(rd_tr(DKt, trl, 16 * ks, 32 * w), ar, dka);
-                dva = mma(rd_tr(DVt, trl, 16 * ks, 32 * w), ar, dva);
+                const bf16x8 ar = srow(At, 0, ks, z);
+                dka = mma(stro(DKt, 16 * ks, 32 * w, z), ar, dka);
+                dva = mma(stro(DVt, 16 * ks, 32 * w, z), ar, dva);
             }
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
@@ -1118,12 +1200,12 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const float *gk8 = sc.gam + 16 * ks + 8 * hl;
-                const bf16x8 bp = scale_k(rd_tr(Pt, trl, 16 * ks, 32 * w), gk8);
-                const bf16x8 bu = scale_k(rd_tr(Ut, trl, 16 * ks, 32 * w), gk8);
+                const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * w, z), gk8);
+                const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * w, z), gk8);
 #pragma unroll
                 for (int x = 0; x < 4; ++x) {
-                    kacc[x] = mma(rd_tr(Qt, trl, 16 * ks, 32 * x), bp, kacc[x]);
-                    vacc[x] = mma(rd_tr(Ot, trl, 16 * ks, 32 * x), bu, vacc[x]);
+                    kacc[x] = mma(stro(Qt, 16 * ks, 32 * x, z), bp, kacc[x]);
+                    vacc[x] = mma(stro(Ot, 16 * ks, 32 * x, z), bu, vacc[x]);
                 }
             }
         }
@@ -1133,18 +1215,18 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         // -- C: intra-chunk terms
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            da = mma(rd_tr(Pt, trl, 16 * ks, 32 * w), rd_row(T1, SSB, l32, 16 * ks, hl), da);
-            da = mma(rd_tr(Ut, trl, 16 * ks, 32 * w), rd_row(T2, SSB, l32, 16 * ks, hl), da);
-            dka = mma(rd_tr(Qt, trl, 16 * ks, 32 * w), rd_row(T3, SSB, l32, 16 * ks, hl), dka);
-            dva = mma(rd_tr(Ot, trl, 16 * ks, 32 * w), rd_row(T4, SSB, l32, 16 * ks, hl), dva);
+            da = mma(stro(Pt, 16 * ks, 32 * w, z), rd_row(T1, SSB, l32, 16 * ks, hl), da);
+            da = mma(stro(Ut, 16 * ks, 32 * w, z), rd_row(T2, SSB, l32, 16 * ks, hl), da);
+            dka = mma(stro(Qt, 16 * ks, 32 * w, z), rd_row(T3, SSB, l32, 16 * ks, hl), dka);
+            dva = mma(stro(Ot, 16 * ks, 32 * w, z), rd_row(T4, SSB, l32, 16 * ks, hl), dva);
         }
-        const bool live = l32 < n;
-        if (t0 + l32 < p.T) {
-            const size_t go = (((size_t)b * p.T + t0 + l32) * p.H + h) * 128 + 32 * w + h4;
-            store_out(gk + go, dka, live);
-            store_out(gv + go, dva, live);
+        float r1 = dot_block(Kt, 32 * w, dka, z) + dot_block(Vt, 32 * w, dva, z);
+        if (l32 >= n) {                                // rows past the sequence: dk = dv = 0
+            dka = zero_acc();
+            dva = zero_acc();
         }
-        float r1 = dot_row(Kt + l32 * QS + 32 * w + h4, dka) + dot_row(Vt + l32 * QS + 32 * w + h4, dva);
+        store_block(DKt, 32 * w, dka, z);              // dk, dv staged in the first rows of the
+        store_block(DVt, 32 * w, dva, z);              // adjoint-state tiles (read only in B)
         // dbeta = <da, U(-lambda) b>; clock gradient of a = beta U(-lambda) b
         float r2 = 0.f, r3 = 0.f;
         {
@@ -1167,6 +1249,12 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         r3 += __shfl_xor(r3, 32);
         if (hl == 0) red[w * kC + l32] = make_float4(r1, r2, r3, 0.f);
         lds_barrier();
+        {
+            const size_t go = (((size_t)b * p.T + t0) * p.H + h) * 128;
+            const int nr = min(kC, p.T - t0);
+            copy_rows_out(DKt, gk + go, (size_t)p.H * 128, nr, tid, z);
+            copy_rows_out(DVt, gv + go, (size_t)p.H * 128, nr, tid, z);
+        }
         if (w == 0 && lane < kC) {
             float s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll

@@ -1116,6 +1116,8 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     __bf16 *gk = static_cast<__bf16 *>(p.gk), *gv = static_cast<__bf16 *>(p.gv);
     Rows2 pq, pk, pv, po, pu, pp;
     Tok tk;
+    double pclk = 0.0;
+    float pudu = 0.f, pdl = 0.f;
     auto prefetch = [&](int c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
@@ -1127,6 +1129,14 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         load_rows(a.U + wb, 128, kC, tid, pu);
         load_rows(a.dP + wb, 128, kC, tid, pp);
         load_tok(p, b, h, t0, Tb, tid, tk);
+        // the readout walk's per-token terms and the chunk's entering clock
+        pclk = a.cclk[(size_t)bh * p.nc + c];
+        pudu = 0.f;
+        pdl = 0.f;
+        if (tid < kC) {
+            pudu = p.udu[(size_t)bh * p.Tpad + t0 + tid];
+            pdl = p.dlam[(size_t)bh * p.Tpad + t0 + tid];
+        }
     };
     if (c_begin < c_end) prefetch(c_end - 1);
     const float sq2m = sqrtf(2.f / (float)m), dcw = 1.f / sqrtf((float)m);
@@ -1143,8 +1153,9 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         store_rows(Ot, po, z);
         store_rows(Ut, pu, z);
         store_rows(Pt, pp, z);
+        const float cur_udu = pudu, cur_dl = pdl;    // this chunk's (the prefetch moves on)
         if (w == 0) {
-            double carry = a.cclk[(size_t)bh * p.nc + c];
+            double carry = pclk;
             chunk_scalars<kLazyAdj>(sc, lane, m, tk, carry, false, Ls);
         }
         lds_barrier();
@@ -1266,8 +1277,8 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
             }
             const size_t ti = (size_t)bh * p.Tpad + t0 + lane;
             const bool lv = lane < n;
-            p.dG[ti] = lv ? p.udu[ti] - s1 : 0.f;
-            p.dlam[ti] = lv ? p.dlam[ti] - s3 * (kTwoPi / (float)m) : 0.f;
+            p.dG[ti] = lv ? cur_udu - s1 : 0.f;
+            p.dlam[ti] = lv ? cur_dl - s3 * (kTwoPi / (float)m) : 0.f;
             if (p.gbeta && t0 + lane < p.T) p.gbeta[((size_t)b * p.T + t0 + lane) * p.H + h] = lv ? s2 : 0.f;
         }
     }

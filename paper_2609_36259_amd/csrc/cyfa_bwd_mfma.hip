@@ -131,11 +131,21 @@ __device__ __forceinline__ void store_acc(float *E, int w, int lane, const f32x1
             *reinterpret_cast<float4 *>(E + dump_off(w, x, lane, 4 * q)) =
                 make_float4(acc[x][4 * q], acc[x][4 * q + 1], acc[x][4 * q + 2], acc[x][4 * q + 3]);
 }
-__device__ __forceinline__ void scale_acc(f32x16 (&acc)[4], float f) {
+template <int N>
+__device__ __forceinline__ void scale_acc(f32x16 (&acc)[N], float f) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int x = 0; x < N; ++x)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[x][v] *= f;
+}
+// two accumulators of wave block w: column blocks x0, x0 + 1
+__device__ __forceinline__ void store_acc2(float *E, int w, int x0, int lane, const f32x16 (&acc)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<float4 *>(E + dump_off(w, x0 + j, lane, 4 * q)) =
+                make_float4(acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]);
 }
 // acc += f * (a state in the ABI layout [128 paper rows][128], active rows only)
 __device__ __forceinline__ void add_abi_state(f32x16 (&acc)[4], const float *S, float f, int w, int lane, int m) {
@@ -319,6 +329,16 @@ __device__ __forceinline__ void store_rows(__bf16 *T, const Rows2 &o, const Sw &
     for (int it = 0; it < 2; ++it) *reinterpret_cast<uint4 *>(cbyte(T) + 16 * PSB * it + z.cp) = o.r[it];
 }
 
+// 512-thread variant: one 16-byte piece per thread (row tid/16, columns 8 (tid % 16)).
+__device__ __forceinline__ void load_row1(const __bf16 *base, size_t row_stride, int n, int tid, uint4 &o) {
+    const int r = tid >> 4, c8 = (tid & 15) * 8;
+    const uint4 v = *reinterpret_cast<const uint4 *>(base + (size_t)min(r, max(n - 1, 0)) * row_stride + c8);
+    o = r < n ? v : make_uint4(0, 0, 0, 0);
+}
+__device__ __forceinline__ void store_row1(__bf16 *T, const uint4 &o, const Sw &z) {
+    *reinterpret_cast<uint4 *>(cbyte(T) + z.cp) = o;
+}
+
 // Per-token scalars of a chunk (lanes 0..31 of wave 0; zero elsewhere and past the
 // sequence: no shift, no decay, no write).
 struct Tok {
@@ -419,11 +439,12 @@ __device__ __forceinline__ float next_scale(const Sc &s, float Ls) {
 // sqrt 2 = beta_r / sqrt m on DC (126), 0 on 127.  Thread (row tid/16 + 16 it,
 // q = tid % 16) fills columns 8q .. 8q+7 (pairs 4q+1 .. 4q+4); the phases advance
 // by angle addition from a start reduced in revolutions.
+template <int NTH = kNT>
 __device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m, const Sw &z) {
     const int q = tid & 15, r0 = tid >> 4;
     const int J = (m - 1) >> 1;
 #pragma unroll 1
-    for (int it = 0; it < 2; ++it) {
+    for (int it = 0; it < kC * 16 / NTH; ++it) {
         const int r = r0 + 16 * it;
         const float4 rec = s.bw[r];
         const float amp = rec.x, u = rec.y, c1 = rec.z, s1 = rec.w;
@@ -563,16 +584,20 @@ __device__ __forceinline__ float dot_block(const __bf16 *T, int col0, const f32x
 
 // ---------------------------------------------------------------------------
 // (1) group contributions to the forward states and the group's clock entry.
+// Eight waves: wave w8 holds basis rows 32 (w8 % 4) .. and column blocks 2 (w8 / 4),
+// 2 (w8 / 4) + 1 of both states (two waves per SIMD: the chunk loop waits on LDS and
+// global loads, which the second wave covers).
+constexpr int kNT8 = 512;
 struct CLay {
     static constexpr int K = 0, V = kT32, A = 2 * kT32, SC = 3 * kT32, RED = SC + kScBytes;
-    static constexpr int BYTES = RED + kNT * 8;
+    static constexpr int BYTES = RED + kNT8 * 8;
 };
-__global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
+__global__ __launch_bounds__(kNT8, 1) void fwd_contrib_kernel(Args a) {
     using L = CLay;
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
     const BwdParams &p = a.p;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w8 = tid >> 6, wi = w8 & 3, xh = w8 >> 2;
     const int m = p.m;
     const int Tb = tokens_of(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
@@ -584,10 +609,10 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
         double *red = lds_at<double>(smem, L::RED);
         const int t_start = min(c_begin * kC, Tb);
         double ds = 0.0;
-        for (int t = tid; t < t_start; t += kNT) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
+        for (int t = tid; t < t_start; t += kNT8) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
         red[tid] = ds;
         __syncthreads();
-        for (int s = kNT / 2; s > 0; s >>= 1) {
+        for (int s = kNT8 / 2; s > 0; s >>= 1) {
             if (tid < s) red[tid] += red[tid + s];
             __syncthreads();
         }
@@ -596,33 +621,33 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
     }
     if (tid == 0) a.gclk[(size_t)bh * p.groups + g] = carry;
     const Sw z = make_sw(tid);
-    f32x16 kacc[4], vacc[4];
+    f32x16 kacc[2], vacc[2];
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        kacc[x] = zero_acc();
-        vacc[x] = zero_acc();
+    for (int j = 0; j < 2; ++j) {
+        kacc[j] = zero_acc();
+        vacc[j] = zero_acc();
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
-    Rows2 rk, rv;
+    uint4 rk, rv;
     Tok tk;
     auto prefetch = [&](int c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
-        load_rows(kin + base, rs, n, tid, rk);
-        load_rows(vin + base, rs, n, tid, rv);
+        load_row1(kin + base, rs, n, tid, rk);
+        load_row1(vin + base, rs, n, tid, rv);
         load_tok(p, b, h, t0, Tb, tid, tk);
     };
     if (c_begin < c_end) prefetch(c_begin);
     double gsum = 0.0;
     float Ls = 0.f;                                   // states: exp(Ls) x registers
     for (int c = c_begin; c < c_end; ++c) {
-        store_rows(Kt, rk, z);
-        store_rows(Vt, rv, z);
-        if (w == 0) chunk_scalars<kLazy>(sc, lane, m, tk, carry, true, Ls);
+        store_row1(Kt, rk, z);
+        store_row1(Vt, rv, z);
+        if (w8 == 0) chunk_scalars<kLazy>(sc, lane, m, tk, carry, true, Ls);
         if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
-        build_A(sc, At, tid, m, z);
+        build_A<kNT8>(sc, At, tid, m, z);
         gsum += (double)sc.G[kC - 1];
         {
             const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
@@ -635,11 +660,11 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
         lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = stro(At, 16 * ks, 32 * w, z);
+            const bf16x8 ad = stro(At, 16 * ks, 32 * wi, z);
 #pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                kacc[x] = mma(stro(Kt, 16 * ks, 32 * x, z), ad, kacc[x]);
-                vacc[x] = mma(stro(Vt, 16 * ks, 32 * x, z), ad, vacc[x]);
+            for (int j = 0; j < 2; ++j) {
+                kacc[j] = mma(stro(Kt, 16 * ks, 32 * (2 * xh + j), z), ad, kacc[j]);
+                vacc[j] = mma(stro(Vt, 16 * ks, 32 * (2 * xh + j), z), ad, vacc[j]);
             }
         }
         lds_barrier();
@@ -647,13 +672,13 @@ __global__ __launch_bounds__(kNT, 2) void fwd_contrib_kernel(Args a) {
     scale_acc(kacc, __expf(Ls));
     scale_acc(vacc, __expf(Ls));
     float *E = a.Ef + ((size_t)bh * p.groups + g) * 2 * kSE;
-    store_acc(E, w, lane, kacc);
-    store_acc(E + kSE, w, lane, vacc);
+    store_acc2(E, wi, 2 * xh, lane, kacc);
+    store_acc2(E + kSE, wi, 2 * xh, lane, vacc);
     if (tid == 0) a.Gg[(size_t)bh * p.groups + g] = (float)gsum;
 }
 
 // ---------------------------------------------------------------------------
-// (3) readout recomputation and its adjoint, per (sequence, chunk group).
+// (2) readout recomputation and its adjoint, per (sequence, chunk group).
 // LDS: padded [32][PS] tiles Q, K, V, dO, A, X, W (later dp), dY (later scale dZ);
 // [128][PS] tiles of the entering key state (bf16) and the readout matrix; three
 // score tiles; chunk scalars; per-token reduction slots.
@@ -977,43 +1002,43 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
 }
 
 // ---------------------------------------------------------------------------
-// (4) group contributions to the adjoint states (reverse over the group's chunks,
+// (3) group contributions to the adjoint states (reverse over the group's chunks,
 // zero adjoint at its end): DK <- exp(G_C) DK + (gamma (.) dP)^T Q, DV likewise
-// with (gamma (.) U)^T dO.
+// with (gamma (.) U)^T dO.  Eight waves, split as in (1).
 struct ALay {
     static constexpr int Q = 0, O = kT32, U = 2 * kT32, P = 3 * kT32, SC = 4 * kT32;
     static constexpr int BYTES = SC + kScBytes;
 };
-__global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
+__global__ __launch_bounds__(kNT8, 1) void adj_contrib_kernel(Args a) {
     using L = ALay;
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
     const BwdParams &p = a.p;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, w8 = tid >> 6, wi = w8 & 3, xh = w8 >> 2, hl = lane >> 5;
     const int Tb = tokens_of(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
     Sc &sc = *lds_at<Sc>(smem, L::SC);
     __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Ot = lds_at<__bf16>(smem, L::O);
     __bf16 *Ut = lds_at<__bf16>(smem, L::U), *Pt = lds_at<__bf16>(smem, L::P);
     const Sw z = make_sw(tid);
-    f32x16 kacc[4], vacc[4];
+    f32x16 kacc[2], vacc[2];
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        kacc[x] = zero_acc();
-        vacc[x] = zero_acc();
+    for (int j = 0; j < 2; ++j) {
+        kacc[j] = zero_acc();
+        vacc[j] = zero_acc();
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *qin = static_cast<const __bf16 *>(p.q), *oin = static_cast<const __bf16 *>(p.dout);
-    Rows2 rq, ro, ru, rp;
+    uint4 rq, ro, ru, rp;
     Tok tk;
     auto prefetch = [&](int c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
         const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
-        load_rows(qin + base, rs, n, tid, rq);
-        load_rows(oin + base, rs, n, tid, ro);
-        load_rows(a.U + wb, 128, kC, tid, ru);
-        load_rows(a.dP + wb, 128, kC, tid, rp);
+        load_row1(qin + base, rs, n, tid, rq);
+        load_row1(oin + base, rs, n, tid, ro);
+        load_row1(a.U + wb, 128, kC, tid, ru);
+        load_row1(a.dP + wb, 128, kC, tid, rp);
         tk.g = 0.f;
         tk.dl = 0.f;
         tk.be = 0.f;
@@ -1023,11 +1048,11 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     float Ls = 0.f;                                   // adjoint states: exp(Ls) x registers
     double clk = 0.0;                                 // (the clock is not used here)
     for (int c = c_end - 1; c >= c_begin; --c) {
-        store_rows(Qt, rq, z);
-        store_rows(Ot, ro, z);
-        store_rows(Ut, ru, z);
-        store_rows(Pt, rp, z);
-        if (w == 0) chunk_scalars<kLazyAdj>(sc, lane, 3, tk, clk, false, Ls);
+        store_row1(Qt, rq, z);
+        store_row1(Ot, ro, z);
+        store_row1(Ut, ru, z);
+        store_row1(Pt, rp, z);
+        if (w8 == 0) chunk_scalars<kLazyAdj>(sc, lane, 3, tk, clk, false, Ls);
         if (c > c_begin) prefetch(c - 1);
         lds_barrier();
         {
@@ -1040,12 +1065,12 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const float *gk = sc.gam + 16 * ks + 8 * hl;
-            const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * w, z), gk);
-            const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * w, z), gk);
+            const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * wi, z), gk);
+            const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * wi, z), gk);
 #pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                kacc[x] = mma(stro(Qt, 16 * ks, 32 * x, z), bp, kacc[x]);
-                vacc[x] = mma(stro(Ot, 16 * ks, 32 * x, z), bu, vacc[x]);
+            for (int j = 0; j < 2; ++j) {
+                kacc[j] = mma(stro(Qt, 16 * ks, 32 * (2 * xh + j), z), bp, kacc[j]);
+                vacc[j] = mma(stro(Ot, 16 * ks, 32 * (2 * xh + j), z), bu, vacc[j]);
             }
         }
         Ls = next_scale(sc, Ls);
@@ -1054,12 +1079,12 @@ __global__ __launch_bounds__(kNT, 2) void adj_contrib_kernel(Args a) {
     scale_acc(kacc, __expf(Ls));
     scale_acc(vacc, __expf(Ls));
     float *E = a.Ea + ((size_t)bh * p.groups + g) * 2 * kSE;
-    store_acc(E, w, lane, kacc);
-    store_acc(E + kSE, w, lane, vacc);
+    store_acc2(E, wi, 2 * xh, lane, kacc);
+    store_acc2(E + kSE, wi, 2 * xh, lane, vacc);
 }
 
 // ---------------------------------------------------------------------------
-// (6) token gradients, per (sequence, chunk group), chunks in reverse.
+// (4) token gradients, per (sequence, chunk group), chunks in reverse.
 // LDS: padded [32][PS] tiles Q, K, V, dO, U, dP, A; [128][PS] tiles of the adjoint
 // states at the chunk's end (bf16); four score tiles stored [s][r]; scalars;
 // per-token reduction slots.
@@ -1340,9 +1365,9 @@ hipError_t launch_bwd_mfma(BwdParams p, void *ws, hipStream_t s) {
     hipError_t e = launch_readout_prep(p.H, p.m, p.R, nullptr, Mz, p.scale * 1.4426950408889634f, s);
     if (e != hipSuccess) return e;
     const dim3 block(kNT), grp(BH, G);
-    hipLaunchKernelGGL(fwd_contrib_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(fwd_contrib_kernel, grp, dim3(kNT8), 0, s, a);
     hipLaunchKernelGGL(readout_kernel, grp, block, 0, s, a);
-    hipLaunchKernelGGL(adj_contrib_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(adj_contrib_kernel, grp, dim3(kNT8), 0, s, a);
     hipLaunchKernelGGL(grad_kernel, grp, block, 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

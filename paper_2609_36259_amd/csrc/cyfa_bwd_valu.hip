@@ -42,6 +42,7 @@
 #include <type_traits>
 
 #include "cyfa_bwd.h"
+#include "cyfa_mfma_common.h"   // wave-level prefix sums (DPP)
 
 namespace cyfa {
 
@@ -960,10 +961,13 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
 // ---------------------------------------------------------------------------
 // (5) reverse cumulative sums per sequence: dlog_alpha_t = sum_{tau >= t} dG_tau
 // (with the final-state term at the last token), ddelta_t = sum_{tau >= t}
-// dlambda_tau, dclock0 = sum_t dlambda_t.
+// dlambda_tau, dclock0 = sum_t dlambda_t.  Thread i sums its own run of tokens; the
+// sum of all later runs is the total minus an inclusive prefix over the threads
+// (wave prefix sums, then one offset per wave), all in double.
 __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
-    __shared__ double sG[kNT], sL[kNT];
-    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
+    constexpr int kW = kNT / 64;
+    __shared__ double sG[kW], sL[kW];
+    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int Tb = bwd_tokens(p, b);
     const float *dG = p.dG + (size_t)bh * p.Tpad;
     const float *dl = p.dlam + (size_t)bh * p.Tpad;
@@ -976,23 +980,24 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
         aG += dG[t] + (t == Tb - 1 ? fin : 0.f);
         aL += dl[t];
     }
-    sG[tid] = aG;
-    sL[tid] = aL;
-    __syncthreads();
-    if (tid == 0) {
-        // exclusive suffix sums over the thread ranges
-        double rg = 0.0, rl = 0.0;
-        for (int u = kNT - 1; u >= 0; --u) {
-            const double g = sG[u], l = sL[u];
-            sG[u] = rg;
-            sL[u] = rl;
-            rg += g;
-            rl += l;
-        }
-        if (p.gclock0) p.gclock0[bh] = rl;
+    const double iG = mfma::wave_incl_scan(aG), iL = mfma::wave_incl_scan(aL);
+    if (lane == 63) {
+        sG[wv] = iG;
+        sL[wv] = iL;
     }
     __syncthreads();
-    double rg = sG[tid], rl = sL[tid];
+    double oG = 0.0, oL = 0.0, TG = 0.0, TL = 0.0;
+#pragma unroll
+    for (int u = 0; u < kW; ++u) {
+        if (u < wv) {
+            oG += sG[u];
+            oL += sL[u];
+        }
+        TG += sG[u];
+        TL += sL[u];
+    }
+    if (tid == 0 && p.gclock0) p.gclock0[bh] = TL;
+    double rg = TG - (oG + iG), rl = TL - (oL + iL);   // sums over the later runs
     for (int t = t_hi - 1; t >= t_lo; --t) {
         rg += dG[t] + (t == Tb - 1 ? fin : 0.f);
         rl += dl[t];
@@ -1038,8 +1043,10 @@ __global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
         const int ii = e / m, s = e % m;
         if (i0 + ii >= m) continue;
         float acc = dM[ii][0] * dc;
+        int n = 0;                                  // l s mod m, advanced by s per step
         for (int l = 1; 2 * l < m; ++l) {
-            const int n = (l * s) % m;
+            n += s;
+            if (n >= m) n -= m;
             acc = fmaf(dM[ii][2 * l - 1], ac * tab[0][n], acc);
             acc = fmaf(dM[ii][2 * l], ac * tab[1][n], acc);
         }

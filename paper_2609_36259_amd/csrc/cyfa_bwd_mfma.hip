@@ -147,65 +147,74 @@ __device__ __forceinline__ void store_acc2(float *E, int w, int x0, int lane, co
             *reinterpret_cast<float4 *>(E + dump_off(w, x0 + j, lane, 4 * q)) =
                 make_float4(acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]);
 }
+// The helpers below take N accumulators of one wave, column blocks x0 .. x0+N-1 of
+// the basis rows 32 w + lane % 32 (the four-wave kernels hold N = 4 from x0 = 0).
 // acc += f * (a state in the ABI layout [128 paper rows][128], active rows only)
-__device__ __forceinline__ void add_abi_state(f32x16 (&acc)[4], const float *S, float f, int w, int lane, int m) {
+template <int N>
+__device__ __forceinline__ void add_abi_state(f32x16 (&acc)[N], const float *S, float f, int w, int x0, int lane,
+                                              int m) {
     const int i = 32 * w + (lane & 31);
     if (!row_active(i, m)) return;
     const float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int j = 0; j < N; ++j)
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
-            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
-            acc[x][4 * v4] = fmaf(f, q.x, acc[x][4 * v4]);
-            acc[x][4 * v4 + 1] = fmaf(f, q.y, acc[x][4 * v4 + 1]);
-            acc[x][4 * v4 + 2] = fmaf(f, q.z, acc[x][4 * v4 + 2]);
-            acc[x][4 * v4 + 3] = fmaf(f, q.w, acc[x][4 * v4 + 3]);
+            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * (x0 + j) + 8 * v4);
+            acc[j][4 * v4] = fmaf(f, q.x, acc[j][4 * v4]);
+            acc[j][4 * v4 + 1] = fmaf(f, q.y, acc[j][4 * v4 + 1]);
+            acc[j][4 * v4 + 2] = fmaf(f, q.z, acc[j][4 * v4 + 2]);
+            acc[j][4 * v4 + 3] = fmaf(f, q.w, acc[j][4 * v4 + 3]);
         }
 }
 // acc += f * (a state in the dump layout)
-__device__ __forceinline__ void add_dump_state(f32x16 (&acc)[4], const float *E, float f, int w, int lane) {
+template <int N>
+__device__ __forceinline__ void add_dump_state(f32x16 (&acc)[N], const float *E, float f, int w, int x0, int lane) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int j = 0; j < N; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float4 e = *reinterpret_cast<const float4 *>(E + dump_off(w, x, lane, 4 * q));
-            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
-            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
-            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
-            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+            const float4 e = *reinterpret_cast<const float4 *>(E + dump_off(w, x0 + j, lane, 4 * q));
+            acc[j][4 * q] = fmaf(f, e.x, acc[j][4 * q]);
+            acc[j][4 * q + 1] = fmaf(f, e.y, acc[j][4 * q + 1]);
+            acc[j][4 * q + 2] = fmaf(f, e.z, acc[j][4 * q + 2]);
+            acc[j][4 * q + 3] = fmaf(f, e.w, acc[j][4 * q + 3]);
         }
 }
 // sum over the lane's elements of S (ABI layout, active rows) times acc
-__device__ __forceinline__ float dot_abi_state(const f32x16 (&acc)[4], const float *S, int w, int lane, int m) {
+template <int N>
+__device__ __forceinline__ float dot_abi_state(const f32x16 (&acc)[N], const float *S, int w, int x0, int lane,
+                                               int m) {
     const int i = 32 * w + (lane & 31);
     if (!S || !row_active(i, m)) return 0.f;
     const float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
     float t = 0.f;
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int j = 0; j < N; ++j)
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
-            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
-            t = fmaf(q.x, acc[x][4 * v4], t);
-            t = fmaf(q.y, acc[x][4 * v4 + 1], t);
-            t = fmaf(q.z, acc[x][4 * v4 + 2], t);
-            t = fmaf(q.w, acc[x][4 * v4 + 3], t);
+            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * (x0 + j) + 8 * v4);
+            t = fmaf(q.x, acc[j][4 * v4], t);
+            t = fmaf(q.y, acc[j][4 * v4 + 1], t);
+            t = fmaf(q.z, acc[j][4 * v4 + 2], t);
+            t = fmaf(q.w, acc[j][4 * v4 + 3], t);
         }
     return t;
 }
 // f * acc into a state in the ABI layout (rows that are not active written as 0)
-__device__ __forceinline__ void store_abi_state(float *S, const f32x16 (&acc)[4], float f, int w, int lane, int m) {
+template <int N>
+__device__ __forceinline__ void store_abi_state(float *S, const f32x16 (&acc)[N], float f, int w, int x0, int lane,
+                                                int m) {
     const int i = 32 * w + (lane & 31);
     const bool act = row_active(i, m);
     float *row = S + (size_t)paper_row(i) * 128 + 4 * (lane >> 5);
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int j = 0; j < N; ++j)
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4)
-            *reinterpret_cast<float4 *>(row + 32 * x + 8 * v4) =
-                act ? make_float4(f * acc[x][4 * v4], f * acc[x][4 * v4 + 1], f * acc[x][4 * v4 + 2],
-                                  f * acc[x][4 * v4 + 3])
+            *reinterpret_cast<float4 *>(row + 32 * (x0 + j) + 8 * v4) =
+                act ? make_float4(f * acc[j][4 * v4], f * acc[j][4 * v4 + 1], f * acc[j][4 * v4 + 2],
+                                  f * acc[j][4 * v4 + 3])
                     : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
@@ -257,17 +266,18 @@ __device__ __forceinline__ bf16x8 stro(const __bf16 *T, int k0, int n0, const Sw
     return lds8_tr(reinterpret_cast<const __bf16 *>(cbyte(T) + z.tr) + k0 * PS + n0, PS);
 }
 // Accumulators as bf16 rows of a [128][PS] tile: row 32 w + lane%32, columns
-// 32 x + 8 g4 + 4 (lane/32) .. +3 per store.
-__device__ __forceinline__ void dump_tile(__bf16 *T, int w, const f32x16 (&acc)[4], const Sw &z) {
+// 32 (x0 + j) + 8 g4 + 4 (lane/32) .. +3 per store.
+template <int N>
+__device__ __forceinline__ void dump_tile(__bf16 *T, int w, int x0, const f32x16 (&acc)[N], const Sw &z) {
     char *b = cbyte(T) + z.st + 32 * w * PSB;
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int j = 0; j < N; ++j)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             bf16x4 o;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[x][4 * g4 + e];
-            *reinterpret_cast<bf16x4 *>(b + 2 * (32 * x + 8 * g4)) = o;
+            for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[j][4 * g4 + e];
+            *reinterpret_cast<bf16x4 *>(b + 2 * (32 * (x0 + j) + 8 * g4)) = o;
         }
 }
 // A 32 x 32 output block D[m][n] in registers (lane: n = lane % 32; register v:
@@ -739,13 +749,13 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
         for (int q = g - 1; q >= 0; --q) {
             const float f = __expf(tail);
             const float *E = a.Ef + ((size_t)bh * p.groups + q) * 2 * kSE;
-            add_dump_state(kacc, E, f, w, lane);
-            add_dump_state(vacc, E + kSE, f, w, lane);
+            add_dump_state(kacc, E, f, w, 0, lane);
+            add_dump_state(vacc, E + kSE, f, w, 0, lane);
             tail += Gg[q];
         }
         const size_t sb = (size_t)bh * kStoreRows * 128;
-        if (p.K0) add_abi_state(kacc, p.K0 + sb, __expf(tail), w, lane, m);
-        if (p.V0) add_abi_state(vacc, p.V0 + sb, __expf(tail), w, lane, m);
+        if (p.K0) add_abi_state(kacc, p.K0 + sb, __expf(tail), w, 0, lane, m);
+        if (p.V0) add_abi_state(vacc, p.V0 + sb, __expf(tail), w, 0, lane, m);
     }
     double carry = a.gclk[(size_t)bh * p.groups + g];
     const size_t rs = (size_t)p.H * 128;
@@ -785,7 +795,7 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
                 scale_acc(vacc, pre);
             }
         }
-        dump_tile(KB, w, kacc, z);
+        dump_tile(KB, w, 0, kacc, z);
         build_A(sc, At, tid, m, z);
         lds_barrier();
         // -- B: scores, inter-chunk terms of p and du, state update; prefetch the next chunk
@@ -979,8 +989,8 @@ __global__ __launch_bounds__(kNT, 1) void readout_kernel(Args a) {
     // the last group holds the final states: the loss <dK_T, Kbar_T> + <dV_T, Vbar_T>
     if (g == p.groups - 1) {
         const size_t sb = (size_t)bh * kStoreRows * 128;
-        float t = __expf(Ls) * (dot_abi_state(kacc, p.dK_T ? p.dK_T + sb : nullptr, w, lane, m) +
-                                dot_abi_state(vacc, p.dV_T ? p.dV_T + sb : nullptr, w, lane, m));
+        float t = __expf(Ls) * (dot_abi_state(kacc, p.dK_T ? p.dK_T + sb : nullptr, w, 0, lane, m) +
+                                dot_abi_state(vacc, p.dV_T ? p.dV_T + sb : nullptr, w, 0, lane, m));
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
         if (lane == 0) {
@@ -1085,23 +1095,28 @@ __global__ __launch_bounds__(kNT8, 1) void adj_contrib_kernel(Args a) {
 
 // ---------------------------------------------------------------------------
 // (4) token gradients, per (sequence, chunk group), chunks in reverse.
+// Eight waves, two per SIMD: wave w8 holds column blocks 2 (w8 / 4), 2 (w8 / 4) + 1 of
+// both adjoint states for the basis rows 32 (w8 % 4) ..; waves 0-3 form da for basis
+// rows 32 (w8 % 4) .. and its per-token terms (dbeta, the write's clock term), waves
+// 4-7 dk and dv for columns 32 (w8 % 4) .. and <k, dk> + <v, dv>.
 // LDS: padded [32][PS] tiles Q, K, V, dO, U, dP, A; [128][PS] tiles of the adjoint
-// states at the chunk's end (bf16); four score tiles stored [s][r]; scalars;
-// per-token reduction slots.
+// states at the chunk's end (bf16; their first 32 rows then stage dk and dv); four
+// score tiles stored [s][r]; scalars; per-token reduction slots.
 struct GLay {
     static constexpr int Q = 0, K = kT32, V = 2 * kT32, O = 3 * kT32, U = 4 * kT32, P = 5 * kT32, A = 6 * kT32;
     static constexpr int DK = 7 * kT32, DV = DK + kT128;
     static constexpr int T1 = DV + kT128, T2 = T1 + kTS, T3 = T2 + kTS, T4 = T3 + kTS;
     static constexpr int SC = T4 + kTS, RED = SC + kScBytes;
-    static constexpr int BYTES = RED + 4 * kC * 16;
+    static constexpr int BYTES = RED + 8 * kC * 16;
     static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
 };
-__global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
+__global__ __launch_bounds__(kNT8, 1) void grad_kernel(Args a) {
     using L = GLay;
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
     const BwdParams &p = a.p;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5, h4 = 4 * hl;
+    const int tid = threadIdx.x, lane = tid & 63, w8 = tid >> 6, wi = w8 & 3, xh = w8 >> 2;
+    const int l32 = lane & 31, hl = lane >> 5;
     const int m = p.m;
     const int Tb = tokens_of(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);
@@ -1113,33 +1128,34 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     __bf16 *T3 = lds_at<__bf16>(smem, L::T3), *T4 = lds_at<__bf16>(smem, L::T4);
     float4 *red = lds_at<float4>(smem, L::RED);
     const Sw z = make_sw(tid);
-    f32x16 kacc[4], vacc[4];
+    const int x0 = 2 * xh;                          // this wave's column blocks x0, x0 + 1
+    f32x16 kacc[2], vacc[2];
     {
         // adjoint at the group's end: (dK_T, dV_T) decayed through the later groups, plus
         // each later group's own contribution decayed through the groups before it
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            kacc[x] = zero_acc();
-            vacc[x] = zero_acc();
+        for (int j = 0; j < 2; ++j) {
+            kacc[j] = zero_acc();
+            vacc[j] = zero_acc();
         }
         const float *Gg = a.Gg + (size_t)bh * p.groups;
         float head = 0.f;                         // log decay of groups g+1 .. q-1
         for (int q = g + 1; q < p.groups; ++q) {
             const float f = __expf(head);
             const float *E = a.Ea + ((size_t)bh * p.groups + q) * 2 * kSE;
-            add_dump_state(kacc, E, f, w, lane);
-            add_dump_state(vacc, E + kSE, f, w, lane);
+            add_dump_state(kacc, E, f, wi, x0, lane);
+            add_dump_state(vacc, E + kSE, f, wi, x0, lane);
             head += Gg[q];
         }
         const size_t sb = (size_t)bh * kStoreRows * 128;
-        if (p.dK_T) add_abi_state(kacc, p.dK_T + sb, __expf(head), w, lane, m);
-        if (p.dV_T) add_abi_state(vacc, p.dV_T + sb, __expf(head), w, lane, m);
+        if (p.dK_T) add_abi_state(kacc, p.dK_T + sb, __expf(head), wi, x0, lane, m);
+        if (p.dV_T) add_abi_state(vacc, p.dV_T + sb, __expf(head), wi, x0, lane, m);
     }
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
     const __bf16 *vin = static_cast<const __bf16 *>(p.v), *oin = static_cast<const __bf16 *>(p.dout);
     __bf16 *gk = static_cast<__bf16 *>(p.gk), *gv = static_cast<__bf16 *>(p.gv);
-    Rows2 pq, pk, pv, po, pu, pp;
+    uint4 pq, pk, pv, po, pu, pp;
     Tok tk;
     double pclk = 0.0;
     float pudu = 0.f, pdl = 0.f;
@@ -1147,12 +1163,12 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
         const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
-        load_rows(qin + base, rs, n, tid, pq);
-        load_rows(kin + base, rs, n, tid, pk);
-        load_rows(vin + base, rs, n, tid, pv);
-        load_rows(oin + base, rs, n, tid, po);
-        load_rows(a.U + wb, 128, kC, tid, pu);
-        load_rows(a.dP + wb, 128, kC, tid, pp);
+        load_row1(qin + base, rs, n, tid, pq);
+        load_row1(kin + base, rs, n, tid, pk);
+        load_row1(vin + base, rs, n, tid, pv);
+        load_row1(oin + base, rs, n, tid, po);
+        load_row1(a.U + wb, 128, kC, tid, pu);
+        load_row1(a.dP + wb, 128, kC, tid, pp);
         load_tok(p, b, h, t0, Tb, tid, tk);
         // the readout walk's per-token terms and the chunk's entering clock
         pclk = a.cclk[(size_t)bh * p.nc + c];
@@ -1172,14 +1188,14 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         // -- A: stage, scalars (clock entering the chunk from the forward walk), adjoint
         //    states at the chunk's end in bf16, writes
-        store_rows(Qt, pq, z);
-        store_rows(Kt, pk, z);
-        store_rows(Vt, pv, z);
-        store_rows(Ot, po, z);
-        store_rows(Ut, pu, z);
-        store_rows(Pt, pp, z);
+        store_row1(Qt, pq, z);
+        store_row1(Kt, pk, z);
+        store_row1(Vt, pv, z);
+        store_row1(Ot, po, z);
+        store_row1(Ut, pu, z);
+        store_row1(Pt, pp, z);
         const float cur_udu = pudu, cur_dl = pdl;    // this chunk's (the prefetch moves on)
-        if (w == 0) {
+        if (w8 == 0) {
             double carry = pclk;
             chunk_scalars<kLazyAdj>(sc, lane, m, tk, carry, false, Ls);
         }
@@ -1191,40 +1207,44 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
                 scale_acc(vacc, pre);
             }
         }
-        dump_tile(DKt, w, kacc, z);
-        dump_tile(DVt, w, vacc, z);
-        build_A(sc, At, tid, m, z);
+        dump_tile(DKt, wi, x0, kacc, z);
+        dump_tile(DVt, wi, x0, vacc, z);
+        build_A<kNT8>(sc, At, tid, m, z);
         lds_barrier();
-        // -- B: score tiles (one per wave, stored [s][r]); inter-chunk terms of da, dk,
-        //    dv; adjoint update; prefetch the previous chunk
-        // T1[s][r] = Gamma (q_r . k_s), T2 (do_r . v_s), T3 (dp_r . a_s), T4 (u_r . a_s): wave w
-        // forms the 16 x 16 block (s block w / 2, r block w % 2) of each
-        {
-            const int m0 = 16 * (w & 1), n0 = 16 * (w >> 1);
-            score_block<false>(Qt, m0, Kt, n0, T1, sc, lane);
-            score_block<false>(Ot, m0, Vt, n0, T2, sc, lane);
-            score_block<false>(Pt, m0, At, n0, T3, sc, lane);
-            score_block<false>(Ut, m0, At, n0, T4, sc, lane);
-        }
+        // -- B: score tiles (stored [s][r]; the 16 x 16 block (s block wi / 2, r block wi % 2)
+        //    of T1, T2 on waves 0-3 and of T3, T4 on waves 4-7); inter-chunk terms of da
+        //    (waves 0-3) or of dk, dv (waves 4-7); adjoint update; prefetch
         const float rs_ = sc.rho[l32];
-        f32x16 da = zero_acc(), dka = zero_acc(), dva = zero_acc();
+        f32x16 r0 = zero_acc(), r1 = zero_acc();     // da, or dk and dv
         {
+            const int m0 = 16 * (wi & 1), n0 = 16 * (wi >> 1);
+            if (xh == 0) {
+                score_block<false>(Qt, m0, Kt, n0, T1, sc, lane);   // T1[s][r] = Gamma (q_r . k_s)
+                score_block<false>(Ot, m0, Vt, n0, T2, sc, lane);   // T2[s][r] = Gamma (do_r . v_s)
+            } else {
+                score_block<false>(Pt, m0, At, n0, T3, sc, lane);   // T3[s][r] = Gamma (dp_r . a_s)
+                score_block<false>(Ut, m0, At, n0, T4, sc, lane);   // T4[s][r] = Gamma (u_r . a_s)
+            }
+        }
+        if (xh == 0) {
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                da = mma(srow(DKt, 32 * w, ks, z), srow(Kt, 0, ks, z), da);
-                da = mma(srow(DVt, 32 * w, ks, z), srow(Vt, 0, ks, z), da);
+                r0 = mma(srow(DKt, 32 * wi, ks, z), srow(Kt, 0, ks, z), r0);
+                r0 = mma(srow(DVt, 32 * wi, ks, z), srow(Vt, 0, ks, z), r0);
             }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) r0[v] *= rs_;
+        } else {
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
                 const bf16x8 ar = srow(At, 0, ks, z);
-                dka = mma(stro(DKt, 16 * ks, 32 * w, z), ar, dka);
-                dva = mma(stro(DVt, 16 * ks, 32 * w, z), ar, dva);
+                r0 = mma(stro(DKt, 16 * ks, 32 * wi, z), ar, r0);
+                r1 = mma(stro(DVt, 16 * ks, 32 * wi, z), ar, r1);
             }
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                da[v] *= rs_;
-                dka[v] *= rs_;
-                dva[v] *= rs_;
+                r0[v] *= rs_;
+                r1[v] *= rs_;
             }
         }
         {
@@ -1236,65 +1256,69 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const float *gk8 = sc.gam + 16 * ks + 8 * hl;
-                const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * w, z), gk8);
-                const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * w, z), gk8);
+                const bf16x8 bp = scale_k(stro(Pt, 16 * ks, 32 * wi, z), gk8);
+                const bf16x8 bu = scale_k(stro(Ut, 16 * ks, 32 * wi, z), gk8);
 #pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    kacc[x] = mma(stro(Qt, 16 * ks, 32 * x, z), bp, kacc[x]);
-                    vacc[x] = mma(stro(Ot, 16 * ks, 32 * x, z), bu, vacc[x]);
+                for (int j = 0; j < 2; ++j) {
+                    kacc[j] = mma(stro(Qt, 16 * ks, 32 * (x0 + j), z), bp, kacc[j]);
+                    vacc[j] = mma(stro(Ot, 16 * ks, 32 * (x0 + j), z), bu, vacc[j]);
                 }
             }
         }
         Ls = next_scale(sc, Ls);
         if (c > c_begin) prefetch(c - 1);
         lds_barrier();
-        // -- C: intra-chunk terms
+        // -- C: intra-chunk terms and the per-token terms
+        float t1 = 0.f, t2 = 0.f, t3 = 0.f;
+        if (xh == 0) {
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            da = mma(stro(Pt, 16 * ks, 32 * w, z), rd_row(T1, SSB, l32, 16 * ks, hl), da);
-            da = mma(stro(Ut, 16 * ks, 32 * w, z), rd_row(T2, SSB, l32, 16 * ks, hl), da);
-            dka = mma(stro(Qt, 16 * ks, 32 * w, z), rd_row(T3, SSB, l32, 16 * ks, hl), dka);
-            dva = mma(stro(Ot, 16 * ks, 32 * w, z), rd_row(T4, SSB, l32, 16 * ks, hl), dva);
-        }
-        float r1 = dot_block(Kt, 32 * w, dka, z) + dot_block(Vt, 32 * w, dva, z);
-        if (l32 >= n) {                                // rows past the sequence: dk = dv = 0
-            dka = zero_acc();
-            dva = zero_acc();
-        }
-        store_block(DKt, 32 * w, dka, z);              // dk, dv staged in the first rows of the
-        store_block(DVt, 32 * w, dva, z);              // adjoint-state tiles (read only in B)
-        // dbeta = <da, U(-lambda) b>; clock gradient of a = beta U(-lambda) b
-        float r2 = 0.f, r3 = 0.f;
-        {
+            for (int ks = 0; ks < 2; ++ks) {
+                r0 = mma(stro(Pt, 16 * ks, 32 * wi, z), rd_row(T1, SSB, l32, 16 * ks, hl), r0);
+                r0 = mma(stro(Ut, 16 * ks, 32 * wi, z), rd_row(T2, SSB, l32, 16 * ks, hl), r0);
+            }
+            // dbeta = <da, U(-lambda) b>; clock term of a = beta U(-lambda) b
             float pc[8], ps[8];
-            lane_phases(sc.urev[l32], w, hl, m, pc, ps);
+            lane_phases(sc.urev[l32], wi, hl, m, pc, ps);
             const float amp = sc.bw[l32].x;            // beta sqrt(2/m)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int j = pair_freq(w, hl, e);
+                const int j = pair_freq(wi, hl, e);
                 if (j <= J) {
-                    r2 = fmaf(sq2m, pc[e] * da[2 * e] - ps[e] * da[2 * e + 1], r2);
+                    t2 = fmaf(sq2m, pc[e] * r0[2 * e] - ps[e] * r0[2 * e + 1], t2);
                     // j (da_sin a_cos - da_cos a_sin) with a_cos = amp c, a_sin = -amp s
-                    r3 = fmaf((float)j * amp, da[2 * e + 1] * pc[e] + da[2 * e] * ps[e], r3);
+                    t3 = fmaf((float)j * amp, r0[2 * e + 1] * pc[e] + r0[2 * e] * ps[e], t3);
                 }
             }
-            if (w == 3 && hl == 1) r2 = fmaf(dcw, da[14], r2);   // DC (internal row 126)
+            if (wi == 3 && hl == 1) t2 = fmaf(dcw, r0[14], t2);   // DC (internal row 126)
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                r0 = mma(stro(Qt, 16 * ks, 32 * wi, z), rd_row(T3, SSB, l32, 16 * ks, hl), r0);
+                r1 = mma(stro(Ot, 16 * ks, 32 * wi, z), rd_row(T4, SSB, l32, 16 * ks, hl), r1);
+            }
+            t1 = dot_block(Kt, 32 * wi, r0, z) + dot_block(Vt, 32 * wi, r1, z);
+            if (l32 >= n) {                            // rows past the sequence: dk = dv = 0
+                r0 = zero_acc();
+                r1 = zero_acc();
+            }
+            store_block(DKt, 32 * wi, r0, z);          // dk, dv staged in the first rows of the
+            store_block(DVt, 32 * wi, r1, z);          // adjoint-state tiles (read only in B)
         }
-        r1 += __shfl_xor(r1, 32);
-        r2 += __shfl_xor(r2, 32);
-        r3 += __shfl_xor(r3, 32);
-        if (hl == 0) red[w * kC + l32] = make_float4(r1, r2, r3, 0.f);
+        t1 += __shfl_xor(t1, 32);
+        t2 += __shfl_xor(t2, 32);
+        t3 += __shfl_xor(t3, 32);
+        if (hl == 0) red[w8 * kC + l32] = make_float4(t1, t2, t3, 0.f);
         lds_barrier();
         {
             const size_t go = (((size_t)b * p.T + t0) * p.H + h) * 128;
             const int nr = min(kC, p.T - t0);
-            copy_rows_out(DKt, gk + go, (size_t)p.H * 128, nr, tid, z);
-            copy_rows_out(DVt, gv + go, (size_t)p.H * 128, nr, tid, z);
+            if (tid < 256) copy_rows_out(DKt, gk + go, (size_t)p.H * 128, nr, tid, z);
+            else copy_rows_out(DVt, gv + go, (size_t)p.H * 128, nr, tid - 256, make_sw(tid - 256));
         }
-        if (w == 0 && lane < kC) {
+        if (w8 == 0 && lane < kC) {
             float s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
-            for (int x = 0; x < 4; ++x) {
+            for (int x = 0; x < 8; ++x) {
                 const float4 v = red[x * kC + lane];
                 s1 += v.x;
                 s2 += v.y;
@@ -1311,8 +1335,8 @@ __global__ __launch_bounds__(kNT, 1) void grad_kernel(Args a) {
     if (g == 0) {
         const size_t sb = (size_t)bh * kStoreRows * 128;
         const float f = __expf(Ls);
-        if (p.gK0) store_abi_state(p.gK0 + sb, kacc, f, w, lane, m);
-        if (p.gV0) store_abi_state(p.gV0 + sb, vacc, f, w, lane, m);
+        if (p.gK0) store_abi_state(p.gK0 + sb, kacc, f, wi, x0, lane, m);
+        if (p.gV0) store_abi_state(p.gV0 + sb, vacc, f, wi, x0, lane, m);
     }
 }
 
@@ -1368,7 +1392,7 @@ hipError_t launch_bwd_mfma(BwdParams p, void *ws, hipStream_t s) {
     hipLaunchKernelGGL(fwd_contrib_kernel, grp, dim3(kNT8), 0, s, a);
     hipLaunchKernelGGL(readout_kernel, grp, block, 0, s, a);
     hipLaunchKernelGGL(adj_contrib_kernel, grp, dim3(kNT8), 0, s, a);
-    hipLaunchKernelGGL(grad_kernel, grp, block, 0, s, a);
+    hipLaunchKernelGGL(grad_kernel, grp, dim3(kNT8), 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_bwd_tail(p, s);

@@ -10,8 +10,9 @@
 // matrix-core tiles with fp32 accumulation, and the states stay in MFMA
 // accumulators while a workgroup walks its chunk group:
 //   (1) fwd_contrib_kernel (b, h, group): the group's own contribution to the
-//       states at its end (zero entering state), the clock entering the group
-//       and the group's total log decay.
+//       states at its end (zero entering state; not for the last group, whose
+//       contribution no walk reads), the clock entering the group and the group's
+//       total log decay.
 //   (2) readout_kernel (b, h, group): forms the state entering its group from
 //       (K0, V0) and the earlier groups' contributions, then walks the group's
 //       chunks forward with both states in accumulators, recomputes the key
@@ -20,8 +21,8 @@
 //       the clock gradients of X and u; u and dp go to the workspace in bf16 for
 //       (3) and (4).  The last group ends with the final states and forms the
 //       final-state loss <dK_T, Kbar_T> + <dV_T, Vbar_T>.
-//   (3) adj_contrib_kernel (b, h, group): the group's own contribution to the
-//       adjoint states entering it from its tokens (zero adjoint at its end).
+//   (3) adj_contrib_kernel (b, h, group > 0): the group's own contribution to
+//       the adjoint states entering it from its tokens (zero adjoint at its end).
 //   (4) grad_kernel (b, h, group): forms the adjoint at its group's end from
 //       (dK_T, dV_T) and the later groups' contributions, then walks the group's
 //       chunks in reverse with both adjoint states in accumulators: dk, dv, da and
@@ -592,15 +593,43 @@ __device__ __forceinline__ float dot_block(const __bf16 *T, int col0, const f32x
     return s;
 }
 
+constexpr int kNT8 = 512;                           // eight-wave kernels
+
+// Sum of a per-token scalar x[t * stride] over tokens [t_lo, t_hi) in double, over the
+// whole workgroup (kNT8 threads, eight loads in flight per thread); every thread gets
+// the sum.  red: kNT8 / 64 doubles of LDS.
+__device__ __forceinline__ double block_token_sum(const float *x, int stride, int t_lo, int t_hi, double *red,
+                                                  int tid) {
+    double ds = 0.0;
+    for (int t0 = t_lo; t0 < t_hi; t0 += 8 * kNT8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = t0 + u * kNT8 + tid;
+            v[u] = t < t_hi ? x[(size_t)t * stride] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ds += (double)v[u];
+    }
+    for (int o = 32; o > 0; o >>= 1) ds += __shfl_xor(ds, o);
+    if ((tid & 63) == 0) red[tid >> 6] = ds;
+    __syncthreads();
+    double tot = 0.0;
+#pragma unroll
+    for (int i = 0; i < kNT8 / 64; ++i) tot += red[i];
+    __syncthreads();
+    return tot;
+}
 // ---------------------------------------------------------------------------
 // (1) group contributions to the forward states and the group's clock entry.
 // Eight waves: wave w8 holds basis rows 32 (w8 % 4) .. and column blocks 2 (w8 / 4),
 // 2 (w8 / 4) + 1 of both states (two waves per SIMD: the chunk loop waits on LDS and
-// global loads, which the second wave covers).
-constexpr int kNT8 = 512;
+// global loads, which the second wave covers).  The last group's contribution is
+// never read (no walk starts after it), so its workgroups form only its clock entry
+// and total log decay.
 struct CLay {
     static constexpr int K = 0, V = kT32, A = 2 * kT32, SC = 3 * kT32, RED = SC + kScBytes;
-    static constexpr int BYTES = RED + kNT8 * 8;
+    static constexpr int BYTES = RED + kNT8 / 64 * 8;
 };
 __global__ __launch_bounds__(kNT8, 1) void fwd_contrib_kernel(Args a) {
     using L = CLay;
@@ -614,22 +643,20 @@ __global__ __launch_bounds__(kNT8, 1) void fwd_contrib_kernel(Args a) {
     Sc &sc = *lds_at<Sc>(smem, L::SC);
     __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V), *At = lds_at<__bf16>(smem, L::A);
     // clock entering the group: clock0 plus every increment before it (double)
-    double carry;
-    {
-        double *red = lds_at<double>(smem, L::RED);
-        const int t_start = min(c_begin * kC, Tb);
-        double ds = 0.0;
-        for (int t = tid; t < t_start; t += kNT8) ds += (double)p.delta[((size_t)b * p.T + t) * p.H + h];
-        red[tid] = ds;
-        __syncthreads();
-        for (int s = kNT8 / 2; s > 0; s >>= 1) {
-            if (tid < s) red[tid] += red[tid + s];
-            __syncthreads();
-        }
-        carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) + red[0], (double)m, 1.0 / (double)m);
-        __syncthreads();
-    }
+    double *red = lds_at<double>(smem, L::RED);
+    const size_t tok0 = (size_t)b * p.T * p.H + h;
+    double carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
+                                          block_token_sum(p.delta + tok0, p.H, 0, min(c_begin * kC, Tb), red, tid),
+                                      (double)m, 1.0 / (double)m);
     if (tid == 0) a.gclk[(size_t)bh * p.groups + g] = carry;
+    if (g == p.groups - 1) {
+        // the last group's contribution is not read: only its total log decay
+        const double gs = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, min(c_begin * kC, Tb),
+                                                        min(c_end * kC, Tb), red, tid)
+                                      : 0.0;
+        if (tid == 0) a.Gg[(size_t)bh * p.groups + g] = (float)gs;
+        return;
+    }
     const Sw z = make_sw(tid);
     f32x16 kacc[2], vacc[2];
 #pragma unroll
@@ -1024,6 +1051,7 @@ __global__ __launch_bounds__(kNT8, 1) void adj_contrib_kernel(Args a) {
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
     const BwdParams &p = a.p;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    if (g == 0) return;                               // the first group's contribution is not read
     const int tid = threadIdx.x, lane = tid & 63, w8 = tid >> 6, wi = w8 & 3, xh = w8 >> 2, hl = lane >> 5;
     const int Tb = tokens_of(p, b);
     const int c_begin = g * p.cpg, c_end = min(c_begin + p.cpg, p.nc);

@@ -961,20 +961,60 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
 // ---------------------------------------------------------------------------
 // (5) reverse cumulative sums per sequence: dlog_alpha_t = sum_{tau >= t} dG_tau
 // (with the final-state term at the last token), ddelta_t = sum_{tau >= t}
-// dlambda_tau, dclock0 = sum_t dlambda_t.  Thread i sums its own run of tokens; the
-// sum of all later runs is the total minus an inclusive prefix over the threads
-// (wave prefix sums, then one offset per wave), all in double.
+// dlambda_tau, dclock0 = sum_t dlambda_t, all in double.  Workgroup (b h, piece)
+// handles one of kScanPieces consecutive pieces of the sequence: it sums the tokens
+// after its piece itself (loads batched eight per thread), and within the piece each
+// thread sums its own run of tokens; the sum of the later runs is the piece total
+// minus an inclusive prefix over the threads (wave prefix sums, then one offset per
+// wave).  The thread that ends at token 0 holds the whole sum, dclock0.
+constexpr int kScanPieces = 8;
 __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
     constexpr int kW = kNT / 64;
     __shared__ double sG[kW], sL[kW];
-    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int bh = blockIdx.x, pc = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x, lane = tid & 63,
+              wv = tid >> 6;
     const int Tb = bwd_tokens(p, b);
     const float *dG = p.dG + (size_t)bh * p.Tpad;
     const float *dl = p.dlam + (size_t)bh * p.Tpad;
     float fin = 0.f;
     for (int u = 0; u < kCombBlocks; ++u) fin += p.fin[(size_t)bh * kCombBlocks + u];
-    const int per = (Tb + kNT - 1) / kNT;
-    const int t_lo = min(tid * per, Tb), t_hi = min(t_lo + per, Tb);
+    const int pp = (Tb + kScanPieces - 1) / kScanPieces;
+    const int P0 = min(pc * pp, Tb), P1 = min(P0 + pp, Tb);
+    // tokens after the piece
+    double lG = 0.0, lL = 0.0;
+    for (int t0 = P1; t0 < Tb; t0 += 8 * kNT) {
+        float vg[8], vl[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = t0 + u * kNT + tid;
+            vg[u] = t < Tb ? dG[t] : 0.f;
+            vl[u] = t < Tb ? dl[t] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            lG += vg[u];
+            lL += vl[u];
+        }
+    }
+    if (P1 < Tb && tid == 0) lG += fin;
+    for (int o = 32; o > 0; o >>= 1) {
+        lG += __shfl_xor(lG, o);
+        lL += __shfl_xor(lL, o);
+    }
+    if (lane == 0) {
+        sG[wv] = lG;
+        sL[wv] = lL;
+    }
+    __syncthreads();
+    double LG = 0.0, LL = 0.0;
+#pragma unroll
+    for (int u = 0; u < kW; ++u) {
+        LG += sG[u];
+        LL += sL[u];
+    }
+    __syncthreads();
+    const int per = (P1 - P0 + kNT - 1) / kNT;
+    const int t_lo = min(P0 + tid * per, P1), t_hi = min(t_lo + per, P1);
     double aG = 0.0, aL = 0.0;
     for (int t = t_lo; t < t_hi; ++t) {
         aG += dG[t] + (t == Tb - 1 ? fin : 0.f);
@@ -996,8 +1036,7 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
         TG += sG[u];
         TL += sL[u];
     }
-    if (tid == 0 && p.gclock0) p.gclock0[bh] = TL;
-    double rg = TG - (oG + iG), rl = TL - (oL + iL);   // sums over the later runs
+    double rg = LG + (TG - (oG + iG)), rl = LL + (TL - (oL + iL));   // sums over the later tokens
     for (int t = t_hi - 1; t >= t_lo; --t) {
         rg += dG[t] + (t == Tb - 1 ? fin : 0.f);
         rl += dl[t];
@@ -1005,7 +1044,8 @@ __global__ __launch_bounds__(kNT) void bwd_scan_kernel(BwdParams p) {
         if (p.glog_alpha) p.glog_alpha[si] = (float)rg;
         p.gdelta[si] = (float)rl;
     }
-    for (int t = Tb + tid; t < p.T; t += kNT) {
+    if (pc == 0 && tid == 0 && p.gclock0) p.gclock0[bh] = rl;       // t_lo = 0: every token
+    for (int t = Tb + pc * kNT + tid; t < p.T; t += kScanPieces * kNT) {
         const size_t si = (brow0(p, b) + t) * p.H + h;
         if (p.glog_alpha) p.glog_alpha[si] = 0.f;
         p.gdelta[si] = 0.f;
@@ -1025,9 +1065,17 @@ __global__ __launch_bounds__(kNT) void bwd_dR_kernel(BwdParams p) {
     for (int e = tid; e < kDRRows * kStoreRows; e += kNT) {
         const int ii = e >> 7, j = e & 127;
         float s = 0.f;
-        for (int u = 0; u < nb; ++u) {
-            const int b = u / p.groups, g = u % p.groups;
-            s += p.dMp[(((size_t)(b * p.H + h) * p.groups + g) * kStoreRows + i0 + ii) * kStoreRows + j];
+        for (int u0 = 0; u0 < nb; u0 += 8) {
+            float v[8];                             // eight loads in flight, summed in order
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int u = u0 + k, b = u / p.groups, g = u % p.groups;
+                v[k] = u < nb ? p.dMp[(((size_t)(b * p.H + h) * p.groups + g) * kStoreRows + i0 + ii) * kStoreRows + j]
+                              : 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                if (u0 + k < nb) s += v[k];
         }
         dM[ii][j] = s;
     }
@@ -1077,7 +1125,7 @@ size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
 }  // namespace
 
 hipError_t launch_bwd_tail(const BwdParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(bwd_scan_kernel, dim3(p.B * p.H), dim3(kNT), 0, s, p);
+    hipLaunchKernelGGL(bwd_scan_kernel, dim3(p.B * p.H, kScanPieces), dim3(kNT), 0, s, p);
     if (p.gR) hipLaunchKernelGGL(bwd_dR_kernel, dim3(p.H, kStoreRows / kDRRows), dim3(kNT), 0, s, p);
     return hipGetLastError();
 }

@@ -92,13 +92,13 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     probe.B = d->B; probe.T = d->T; probe.H = d->H; probe.dk = d->d_k; probe.dv = d->d_v;
     probe.m = d->m; probe.dtype = d->dtype;
     probe.chunk = d->chunk ? d->chunk : cyfa::mfma_default_chunk();
-    const bool mfma_ok = !wide && cyfa::mfma_supported(probe);
+    const bool mfma_ok = wide ? cyfa::mfma_wide_supported(probe) : cyfa::mfma_supported(probe);
     bool use_mfma;
     if (d->kernel == CYFA_KERNEL_MFMA) {
         if (!mfma_ok)
             return fail(CYFA_ERR_UNSUPPORTED,
-                        "matrix-core kernel needs dtype=BF16, d_k=d_v=128 or d_k=d_v=256, m <= 127 and "
-                        "chunk 32 or 64");
+                        "matrix-core kernel needs dtype=BF16, chunk 32 or 64, and d_k=d_v=128 (m up to 255) "
+                        "or d_k=d_v=256 (m <= 127)");
         use_mfma = true;
     } else if (d->kernel == CYFA_KERNEL_VALU) {
         use_mfma = false;
@@ -107,7 +107,14 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     }
     plan->mfma = use_mfma;
     size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
-    if (use_mfma) {
+    if (use_mfma && wide) {
+        // one workgroup walks each sequence (no segment pre-pass for 256 storage rows)
+        if (d->segments > 1)
+            return fail(CYFA_ERR_UNSUPPORTED, "m > 127 on the matrix cores runs one segment per sequence");
+        plan->chunk = cyfa::mfma_default_chunk();
+        plan->segments = 1;
+        ws += round_up(cyfa::mfma_wide_workspace_bytes(probe));
+    } else if (use_mfma) {
         probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
         plan->segments = d->segments ? d->segments : cyfa::mfma_auto_segments(probe);
@@ -309,7 +316,13 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
     char *ws = static_cast<char *>(workspace);
     float *M = reinterpret_cast<float *>(ws);
     hipError_t e;
-    if (plan.mfma) {
+    if (plan.mfma && p.m > cyfa::kMaxActive) {
+        // fp32 readout matrix first, then its bf16 copies in the kernel's basis order
+        e = cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s);
+        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
+        e = cyfa::launch_fwd_mfma_wide(p, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s, g_ev_start,
+                                       g_ev_stop);
+    } else if (plan.mfma) {
         // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop, mix);
     } else {

@@ -67,25 +67,32 @@ def test_status_codes():
     d = cyfa.forward_desc(1, 16, 1, 64, 64, m=257)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     assert b"255" in lib.cyfa_last_error()
-    # 127 < m <= 255: 256 storage rows on the vector-ALU kernel only
+    # 127 < m <= 255: 256 storage rows; fp32 or d = 64 on the vector-ALU kernel
     d = cyfa.forward_desc(1, 16, 1, 64, 64, m=255)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
     assert n.value == 256 * 256 * 4
-    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
-    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     d = cyfa.forward_desc(1, 16, 1, 256, 64, m=255)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
-    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16)
-    assert cyfa.selected_kernel(d) == "valu"
+    # bf16 with d = 128: the matrix-core kernel (fp32 M, then its bf16 copy and transpose)
+    d = cyfa.forward_desc(1, 16, 3, 128, 128, m=255, dtype=cyfa.BF16)
+    assert cyfa.selected_kernel(d) == "mfma"
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert n.value == 3 * 256 * 256 * 4 + 2 * 3 * 256 * 256 * 2
+    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=129, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA, segments=2)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA, chunk=16)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     d = cyfa.forward_desc(1, 16, 1, 96, 64)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     assert lib.cyfa_forward_workspace_size(None, ctypes.byref(n)) == 1
 
 
 def test_matrix_core_head_dims():
-    """bf16 with d_k = d_v = 128 or 256 (m <= 127) selects the matrix-core kernel;
-    mixed head dims, m > 127 or fp32 inputs do not, and asking for it there fails
-    with CYFA_ERR_UNSUPPORTED.  At 256 the workspace holds two 128 x 128 state
+    """bf16 with d_k = d_v = 128 (m up to 255) or 256 (m <= 127) selects the
+    matrix-core kernel; mixed head dims, d = 256 with m > 127 or fp32 inputs do not,
+    and asking for it there fails with CYFA_ERR_UNSUPPORTED.  At 256 the workspace holds two 128 x 128 state
     pairs per head and segment."""
     lib = cyfa.load()
     n = ctypes.c_size_t(0)

@@ -1,0 +1,217 @@
+"""GPU parity of the matrix-core forward for slot counts above 127 (256 storage
+rows: m = 129, the smallest, and m = 255, the largest of the paper's ablation;
+bf16, d_k = d_v = 128, 32-token chunks) against the oracle.
+
+Every output element, the slot logits, the final states and the clock are
+compared with the oracle on the same seeded inputs (several chunks and a ragged
+tail, with and without initial states); bar: max relative error 2e-2 (bf16
+inputs, fp32 accumulation), clock 1e-9.  Packed sequences (cyfa_forward_varlen)
+must reproduce the padded entry point with lengths bit for bit; a forward split
+in two and resumed in place must equal one pass; one full-size 1.4B-layer shape
+at m = 255 is compared on sampled sequences.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_36259_amd.inputs import make_forward_inputs
+from tests.harness import TOL_BF16, clock_err, oracle_states_abs, pairs_view, rel_err, state_view, upload
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+ROWS = 256
+
+
+def _cyfa():
+    from paper_2609_36259_amd import cyfa
+    return cyfa
+
+
+def _fwd(x, t, **kw):
+    cyfa = _cyfa()
+    kw.setdefault("kernel", cyfa.KERNEL_MFMA)
+    print("wide forward", x["q"].shape, "m", x["m"], {k: v for k, v in kw.items() if not hasattr(v, "shape")},
+          flush=True)
+    return cyfa.forward(t["q"], t["k"], t["v"], t["delta"], t["log_alpha"], t["beta"], t["R"],
+                        scale=x["scale"], m=x["m"], **kw)
+
+
+def _init_states(B, H, m, seed):
+    """Absolute-clock initial states in the ABI layout (paper row order, rows >= m zero)."""
+    g = torch.Generator().manual_seed(seed)
+    K0 = torch.randn(B, H, ROWS, 128, generator=g) * 0.2
+    V0 = torch.randn(B, H, ROWS, 128, generator=g) * 0.2
+    K0[:, :, m:] = 0
+    V0[:, :, m:] = 0
+    c0 = torch.rand(B, H, generator=g, dtype=torch.float64) * 2 * m
+    return K0.cuda(), V0.cuda(), c0.cuda()
+
+
+def _oracle_init(init, b, H, m):
+    K0, V0, c0 = init
+    Kr = np.stack([oracle.relative_from_storage(m, c0[b, h].item(), K0[b, h].cpu().numpy()) for h in range(H)])
+    Vr = np.stack([oracle.relative_from_storage(m, c0[b, h].item(), V0[b, h].cpu().numpy()) for h in range(H)])
+    return dict(K0=Kr, V0=Vr, lam0=c0[b].cpu().numpy())
+
+
+def _check(x, res, init=None, lens=None):
+    """Each sequence against the oracle on its own tokens."""
+    B, T, H = x["delta"].shape
+    m = x["m"]
+    worst = {}
+    for b in range(B):
+        n = T if lens is None else lens[b]
+        xs = {k: (a[b:b + 1, :max(n, 1)] if k not in ("R", "scale", "m", "dtype") and a is not None else a)
+              for k, a in x.items()}
+        kw = _oracle_init(init, b, H, m) if init is not None else {}
+        ref = oracle.forward(xs["q"], xs["k"], xs["v"], xs["delta"], xs["log_alpha"], xs["beta"], x["R"],
+                             m=m, scale=x["scale"], T_run=n, **kw)
+        pairs = [b * H + h for h in range(H)]
+        if n > 0:
+            worst["o"] = max(worst.get("o", 0), rel_err(pairs_view(res["o"], pairs, H)[:, :n], ref["o"]))
+            if "logits" in res:
+                worst["z"] = max(worst.get("z", 0), rel_err(pairs_view(res["logits"], pairs, H)[:, :n], ref["z"]))
+        Kref, Vref = oracle_states_abs(ref, m)
+        if np.abs(Kref).max() > 0:
+            worst["K"] = max(worst.get("K", 0), rel_err(state_view(res["K"], pairs, H), Kref))
+            worst["V"] = max(worst.get("V", 0), rel_err(state_view(res["V"], pairs, H), Vref))
+        else:
+            assert torch.count_nonzero(res["K"][b]) == 0 and torch.count_nonzero(res["V"][b]) == 0
+        worst["clock"] = max(worst.get("clock", 0),
+                             clock_err(res["clock"][b].cpu().numpy(), ref["lam"], m))
+    print("errors", {k: f"{v:.2e}" for k, v in worst.items()}, flush=True)
+    for k, v in worst.items():
+        assert v <= (1e-9 if k == "clock" else TOL_BF16), (k, v)
+    return worst
+
+
+@pytest.mark.parametrize("m", [129, 255])
+@pytest.mark.parametrize("with_init", [False, True])
+def test_full_parity(m, with_init):
+    x = make_forward_inputs(2, 32 * 3 + 7, 2, 128, 128, seed=71, dtype="bf16", m=m)
+    t = upload(x)
+    init = _init_states(2, 2, m, 72) if with_init else None
+    kw = dict(K0=init[0], V0=init[1], clock0=init[2]) if init else {}
+    res = _fwd(x, t, return_state=True, return_logits=True, **kw)
+    torch.cuda.synchronize()
+    assert res["K"].shape == (2, 2, ROWS, 128)
+    _check(x, res, init=init)
+
+
+def test_automatic_choice_and_vector_alu_agreement():
+    cyfa = _cyfa()
+    desc = cyfa.forward_desc(2, 70, 2, 128, 128, m=255, dtype=cyfa.BF16)
+    assert cyfa.selected_kernel(desc) == "mfma"
+    x = make_forward_inputs(2, 70, 2, 128, 128, seed=73, dtype="bf16", m=255)
+    t = upload(x)
+    a = _fwd(x, t, kernel=cyfa.KERNEL_AUTO, return_state=True)
+    b = _fwd(x, t, kernel=cyfa.KERNEL_VALU, return_state=True)
+    torch.cuda.synchronize()
+    for k in ("o", "K", "V"):
+        err = rel_err(a[k].float().cpu().numpy(), b[k].float().cpu().numpy())
+        print(k, f"{err:.2e}", flush=True)
+        assert err <= TOL_BF16, k
+
+
+def test_lengths_and_packed_sequences():
+    """cyfa_forward_lens (rows past a sequence not written) and cyfa_forward_varlen
+    on the same sequences: bit-identical, and each sequence against the oracle."""
+    cyfa = _cyfa()
+    lens = [97, 0, 1, 40]
+    B, T, H, m = len(lens), max(lens), 2, 255
+    x = make_forward_inputs(B, T, H, 128, 128, seed=74, dtype="bf16", m=m)
+    t = upload(x)
+    init = _init_states(B, H, m, 75)
+    lt = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    sentinel = torch.full((B, T, H, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+    pad = _fwd(x, t, lens=lt, K0=init[0], V0=init[1], clock0=init[2], return_state=True, return_logits=True,
+               out=sentinel)
+    tp = {k: (torch.cat([a[b, :n] for b, n in enumerate(lens)], dim=0).contiguous()
+              if a is not None and k != "R" else a) for k, a in t.items()}
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device="cuda")
+    res = cyfa.forward_varlen(tp["q"], tp["k"], tp["v"], tp["delta"], cu, tp["log_alpha"], tp["beta"], t["R"],
+                              max_len=T, scale=x["scale"], m=m, kernel=cyfa.KERNEL_MFMA, K0=init[0], V0=init[1],
+                              clock0=init[2], return_state=True, return_logits=True)
+    torch.cuda.synchronize()
+    for b, n in enumerate(lens):
+        assert torch.all(pad["o"][b, n:] == 7.0), b               # rows past the sequence untouched
+    packed_o = torch.cat([pad["o"][b, :n] for b, n in enumerate(lens)], dim=0)
+    packed_z = torch.cat([pad["logits"][b, :n] for b, n in enumerate(lens)], dim=0)
+    assert torch.equal(res["o"], packed_o) and torch.equal(res["logits"], packed_z)
+    assert torch.equal(res["K"], pad["K"]) and torch.equal(res["V"], pad["V"])
+    assert torch.equal(res["clock"], pad["clock"])
+    _check(x, pad, init=init, lens=lens)
+
+
+def test_split_and_resume_in_place():
+    """Two calls, the second resuming from the first's states, equal one pass (the
+    chunk boundaries differ, so the bf16 products round differently: bar 1e-2); the
+    resume in place (K_out = K0, V_out = V0, clock_out = clock0) is bit-identical to
+    the resume into fresh outputs."""
+    cyfa = _cyfa()
+    x = make_forward_inputs(1, 150, 2, 128, 128, seed=76, dtype="bf16", m=255)
+    t = upload(x)
+    full = _fwd(x, t, return_state=True)
+    t1 = 70                                                     # not a multiple of the chunk
+    a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
+    first = _fwd(x, a, return_state=True)
+    K, V, c = first["K"], first["V"], first["clock"]
+    ref = _fwd(x, b, K0=K.clone(), V0=V.clone(), clock0=c.clone(), return_state=True)
+    got = _fwd(x, b, K0=K, V0=V, clock0=c, K_out=K, V_out=V, clock_out=c)
+    torch.cuda.synchronize()
+    assert torch.equal(got["o"], ref["o"])
+    assert torch.equal(K, ref["K"]) and torch.equal(V, ref["V"]) and torch.equal(c, ref["clock"])
+    o_split = torch.cat([first["o"], got["o"]], dim=1).float().cpu().numpy()
+    errs = {"o": rel_err(o_split, full["o"].float().cpu().numpy()),
+            "K": rel_err(K.cpu().numpy(), full["K"].cpu().numpy()),
+            "V": rel_err(V.cpu().numpy(), full["V"].cpu().numpy())}
+    print("split vs one pass", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= 1e-2, k
+    assert clock_err(c.cpu().numpy(), full["clock"].cpu().numpy(), 255) <= 1e-9
+
+
+def test_empty_sequence_passes_states_through():
+    x = make_forward_inputs(1, 0, 2, 128, 128, seed=77, dtype="bf16", m=255)
+    t = upload(x)
+    init = _init_states(1, 2, 255, 78)
+    res = _fwd(x, t, K0=init[0], V0=init[1], clock0=init[2], return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(res["K"], init[0]) and torch.equal(res["V"], init[1])
+    assert clock_err(res["clock"].cpu().numpy(), np.mod(init[2].cpu().numpy(), 255), 255) <= 1e-9
+
+
+@pytest.mark.timeout(400)
+def test_full_size_sampled_sequences():
+    """The 1.4B-layer shape (B = 4, T = 4096, H = 16, d = 128, bf16) at m = 255, in
+    the configuration the benchmark's wide leg times (one workgroup per sequence):
+    four sampled (b, h) sequences, all tokens, against the oracle run on them."""
+    B, T, H, m = 4, 4096, 16, 255
+    x = make_forward_inputs(B, T, H, 128, 128, seed=79, dtype="bf16", m=m)
+    t = upload(x)
+    res = _fwd(x, t, return_state=True)
+    torch.cuda.synchronize()
+    pairs = np.array([0 * H + 3, 1 * H + 10, 2 * H + 0, 3 * H + 15], np.int32)
+    print("oracle on", pairs.tolist(), flush=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["delta"], x["log_alpha"], x["beta"], x["R"], m=m,
+                         scale=x["scale"], pairs=pairs, want_z=False)
+    err = {"o": rel_err(pairs_view(res["o"], pairs, H), ref["o"])}
+    Kref, Vref = oracle_states_abs(ref, m)
+    err["K"] = rel_err(state_view(res["K"], pairs, H), Kref)
+    err["V"] = rel_err(state_view(res["V"], pairs, H), Vref)
+    err["clock"] = clock_err(res["clock"].cpu().numpy().reshape(-1)[pairs], ref["lam"], m)
+    print("errors", {k: f"{v:.2e}" for k, v in err.items()}, flush=True)
+    for k, v in err.items():
+        assert v <= (1e-9 if k == "clock" else TOL_BF16), (k, v)
+
+
+def test_rejects_segments():
+    cyfa = _cyfa()
+    x = make_forward_inputs(1, 64, 1, 128, 128, seed=80, dtype="bf16", m=255)
+    t = upload(x)
+    with pytest.raises(cyfa.CyfaError) as ei:
+        _fwd(x, t, segments=2)
+    assert ei.value.status == 2

@@ -63,6 +63,9 @@ DECODE = Workload("decode N256 H16 d128 prefix512 steps64", 256, 512 + 64, 16, 1
 # The paper's own operator benchmark shape (its 400M model's layer at 2K tokens:
 # 4 heads of 256 channels, 32 sequences), with the value distributions above.
 FWD_PAPER_OP = Workload("paper-op B32 T2048 H4 d256", 32, 2048, 4, 256, 256, seed=5)
+# The largest slot count of the paper's ablation (m = 255, 256 storage rows) at the
+# 1.4B-scale layer shape.
+FWD_1P4B_M255 = Workload("1.4B-layer m255 B4 T4096 H16 d128", 4, 4096, 16, 128, 128, seed=6, m=255)
 
 FORWARD_WORKLOADS = (FWD_TINY, FWD_400M, FWD_1P4B, FWD_LONG)
 

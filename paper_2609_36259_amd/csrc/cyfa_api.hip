@@ -108,12 +108,14 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
     plan->mfma = use_mfma;
     size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
     if (use_mfma && wide) {
-        // one workgroup walks each sequence (no segment pre-pass for 256 storage rows)
-        if (d->segments > 1)
-            return fail(CYFA_ERR_UNSUPPORTED, "m > 127 on the matrix cores runs one segment per sequence");
-        plan->chunk = cyfa::mfma_default_chunk();
-        plan->segments = 1;
-        ws += round_up(cyfa::mfma_wide_workspace_bytes(probe));
+        // chunk groups of a sequence, one workgroup each
+        probe.chunk = cyfa::mfma_default_chunk();
+        plan->chunk = probe.chunk;
+        plan->segments = d->segments ? d->segments : cyfa::mfma_wide_auto_groups(probe);
+        const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
+        if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
+        if (plan->segments < 1) plan->segments = 1;
+        ws += round_up(cyfa::mfma_wide_workspace_bytes(probe, plan->segments));
     } else if (use_mfma) {
         probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
@@ -320,8 +322,8 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
         // fp32 readout matrix first, then its bf16 copies in the kernel's basis order
         e = cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s);
         if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
-        e = cyfa::launch_fwd_mfma_wide(p, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s, g_ev_start,
-                                       g_ev_stop);
+        e = cyfa::launch_fwd_mfma_wide(p, plan.segments, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s,
+                                       g_ev_start, g_ev_stop);
     } else if (plan.mfma) {
         // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop, mix);

@@ -15,7 +15,8 @@
 //   Kbar <- exp(G_C) Kbar + (rho (.) A)^T K,  Vbar likewise with V.
 //
 // One eight-wave workgroup (two waves per SIMD, one workgroup per compute unit)
-// walks a whole sequence with both 256 x 128 fp32 states in MFMA accumulators:
+// walks a chunk group of a sequence with both 256 x 128 fp32 states in MFMA
+// accumulators (groups > 1 fill the chip when B H is small):
 //   Kbar: wave w holds slots i = 32 w + lane % 32 and all 128 channels (four
 //     accumulators, the transposed product D[c][i]), so the key pass and its slot
 //     logits are formed per wave without reductions;
@@ -27,6 +28,15 @@
 // from global memory (L2) as MFMA operands: at 128 KiB each they do not fit in LDS
 // beside the chunk tiles.  Tiles are padded rows: [32][128] at 288 bytes, [32][256]
 // at 544 bytes (each row 8 banks after the previous one).
+//
+// Chunk groups: wide_contrib_kernel (b, h, group) forms each group's own contribution
+// to the absolute-clock states at its end (zero entering state, App. B's recurrence
+// unrolled), its total log decay and the clock entering it (a double-precision sum of
+// every earlier increment); the forward's workgroup for group g then starts from
+// (K0, V0) decayed through groups 0 .. g-1 plus each earlier contribution decayed
+// through the groups after it.  Absolute-clock states need no rotation between
+// groups.  The contributions stay fp32 in the workspace, in the accumulators' own
+// lane-major layout.
 //
 // Internal basis order: pair j = 1 .. 127 at (2j-2, 2j-1), DC at 254, padding 255;
 // the ABI's state arrays [B][H][256][128] use the paper order (0 = DC, 2j-1, 2j).
@@ -387,6 +397,66 @@ __device__ __forceinline__ void store_value_state(float *S, const f32x16 (&acc)[
         }
 }
 
+// ---- chunk-group contributions (fp32, lane-major: wave w, accumulator x, lane, register)
+constexpr int kStateW = kR * 128;                   // floats of one 256 x 128 state
+__device__ __forceinline__ int dump_w(int w, int x, int lane) { return ((w * 4 + x) * 64 + lane) * 16; }
+__device__ __forceinline__ void store_dump(float *E, const f32x16 (&acc)[4], float f, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<float4 *>(E + dump_w(w, x, lane) + 4 * q) =
+                make_float4(f * acc[x][4 * q], f * acc[x][4 * q + 1], f * acc[x][4 * q + 2], f * acc[x][4 * q + 3]);
+}
+__device__ __forceinline__ void add_dump(f32x16 (&acc)[4], const float *E, float f, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 e = *reinterpret_cast<const float4 *>(E + dump_w(w, x, lane) + 4 * q);
+            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
+            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
+            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
+            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+        }
+}
+
+struct WideArgs {
+    FwdParams p;
+    const __bf16 *Mz, *MzT;  // [H][256][256] readout matrix times scale log2 e, and its transpose
+    int groups, cpg;         // chunk groups per sequence, chunks per group
+    float *Ef;               // [BH][groups][2][kStateW] each group's own contribution (K, V)
+    float *Gg;               // [BH][groups] total log decay of each group
+    double *gclk;            // [BH][groups] clock entering each group (reduced mod m)
+    float *S0;               // [BH][2][kStateW] copy of (K0, V0) (groups > 1: the states may be
+                             // overwritten in place by the last group)
+};
+
+// Sum over tokens [t_lo, t_hi) of x[t * stride] in double over the workgroup (eight
+// loads in flight per thread); every thread gets the sum.  red: 8 doubles of LDS.
+__device__ __forceinline__ double block_token_sum(const float *x, int stride, int t_lo, int t_hi, double *red,
+                                                  int tid) {
+    double ds = 0.0;
+    for (int t0 = t_lo; t0 < t_hi; t0 += 8 * kNT) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = t0 + u * kNT + tid;
+            v[u] = t < t_hi ? x[(size_t)t * stride] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ds += (double)v[u];
+    }
+    for (int o = 32; o > 0; o >>= 1) ds += __shfl_xor(ds, o);
+    if ((tid & 63) == 0) red[tid >> 6] = ds;
+    __syncthreads();
+    double tot = 0.0;
+#pragma unroll
+    for (int i = 0; i < kNT / 64; ++i) tot += red[i];
+    __syncthreads();
+    return tot;
+}
+
 // ---- LDS map (bytes) ------------------------------------------------------------
 struct Lay {
     static constexpr int T1 = kC * PSB;            // [32][128] tile
@@ -407,16 +477,19 @@ struct Lay {
     static_assert(BYTES <= 160 * 1024, "one workgroup per compute unit");
 };
 
-__global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(FwdParams p, const __bf16 *Mz, const __bf16 *MzT) {
+__global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(WideArgs a) {
     using L = Lay;
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
-    const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H;
+    const FwdParams &p = a.p;
+    const __bf16 *Mz = a.Mz, *MzT = a.MzT;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
     const int hh = w >> 2, cb = w & 3;             // value-state slot half and channel block
     const int m = p.m;
     const int Tb = seq_tokens(p, b);
     const size_t row0 = seq_row0(p, b);
-    const int nch = (Tb + kC - 1) / kC;
+    // this group's chunks, up to the sequence's last one
+    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
     Sc &sc = *lds_at<Sc>(smem, L::SC);
     __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
     __bf16 *At = lds_at<__bf16>(smem, L::A), *Xt = lds_at<__bf16>(smem, L::X), *Wt = lds_at<__bf16>(smem, L::W);
@@ -436,10 +509,45 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(FwdParams p, const
         kacc[x] = zero_acc();
         vacc[x] = zero_acc();
     }
-    const size_t sb = (size_t)bh * kR * 128;
-    if (p.K0) add_key_state(kacc, p.K0 + sb, w, lane, m);
-    if (p.V0) add_value_state(vacc, p.V0 + sb, hh, cb, lane, m);
-    double carry = reduce_clock(p.clock0 ? p.clock0[bh] : 0.0, (double)m, 1.0 / (double)m);
+    const size_t sb = (size_t)bh * kStateW;
+    double carry;
+    if (a.groups == 1) {
+        if (p.K0) add_key_state(kacc, p.K0 + sb, w, lane, m);
+        if (p.V0) add_value_state(vacc, p.V0 + sb, hh, cb, lane, m);
+        carry = reduce_clock(p.clock0 ? p.clock0[bh] : 0.0, (double)m, 1.0 / (double)m);
+    } else {
+        // state entering the group: each earlier group's contribution decayed through
+        // the groups after it, plus (K0, V0) decayed through all earlier groups
+        const float *Gg = a.Gg + (size_t)bh * a.groups;
+        float tail = 0.f;                         // log decay of groups q+1 .. g-1
+        for (int q = g - 1; q >= 0; --q) {
+            const float f = __expf(tail);
+            const float *E = a.Ef + ((size_t)bh * a.groups + q) * 2 * kStateW;
+            add_dump(kacc, E, f, w, lane);
+            add_dump(vacc, E + kStateW, f, w, lane);
+            tail += Gg[q];
+        }
+        if (p.K0 || p.V0) {
+            f32x16 k0[4], v0[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                k0[x] = zero_acc();
+                v0[x] = zero_acc();
+            }
+            const float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
+            if (p.K0) add_key_state(k0, S0, w, lane, m);
+            if (p.V0) add_value_state(v0, S0 + kStateW, hh, cb, lane, m);
+            const float f = __expf(tail);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    kacc[x][v] = fmaf(f, k0[x][v], kacc[x][v]);
+                    vacc[x][v] = fmaf(f, v0[x][v], vacc[x][v]);
+                }
+        }
+        carry = a.gclk[(size_t)bh * a.groups + g];
+    }
 
     const size_t rs = (size_t)p.H * 128;
     const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
@@ -455,16 +563,16 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(FwdParams p, const
         load_row1(vin + base, rs, n, tid, rv);
         load_tok(p, row0, h, t0, Tb, tid, tk);
     };
-    if (nch > 0) prefetch(0);
+    if (c_begin < c_end) prefetch(c_begin);
     float Ls = 0.f;                                   // carried states: exp(Ls) x registers
-    for (int c = 0; c < nch; ++c) {
+    for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         // -- stage the chunk and its scalars
         store_row1(Qt, rq, z);
         store_row1(Kt, rk, z);
         store_row1(Vt, rv, z);
         if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
-        if (c + 1 < nch) prefetch(c + 1);
+        if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
         {
             const float pre = uniform(sc.ctl[0]);
@@ -598,10 +706,109 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(FwdParams p, const
         copy_row1_out(Qt, o + ((row0 + t0) * p.H + h) * 128, rs, n, tid, z);
         lds_barrier();
     }
+    // the last group ends with the final states (chunks past a sequence change nothing)
+    if (g == a.groups - 1) {
+        const float f = __expf(Ls);
+        if (p.K_out) store_key_state(p.K_out + sb, kacc, f, w, lane, m);
+        if (p.V_out) store_value_state(p.V_out + sb, vacc, f, hh, cb, lane, m);
+        if (p.clock_out && tid == 0) p.clock_out[bh] = carry;
+    }
+}
+
+// Each chunk group's own contribution (groups > 1; launched before the forward).
+// The last group's contribution is never read, so its workgroup copies (K0, V0)
+// for the forward's prologues instead and forms only its total log decay.
+__global__ __launch_bounds__(kNT, 1) void wide_contrib_kernel(WideArgs a) {
+    using L = Lay;
+    __shared__ __attribute__((aligned(256))) char smem[L::V + L::T1];   // K and V tiles
+    __shared__ __attribute__((aligned(256))) __bf16 Asm[kC * PW];
+    __shared__ Sc sc;
+    __shared__ double red[kNT / 64];
+    const FwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int hh = w >> 2, cb = w & 3;
+    const int m = p.m;
+    const int Tb = seq_tokens(p, b);
+    const size_t row0 = seq_row0(p, b);
+    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
+    const size_t tok0 = row0 * p.H + h;
+    const size_t pi = (size_t)bh * a.groups + g;
+    // clock entering the group: clock0 plus every increment before it (double)
+    double carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
+                                    block_token_sum(p.delta + tok0, p.H, 0, min(c_begin * kC, Tb), red, tid),
+                                (double)m, 1.0 / (double)m);
+    if (tid == 0) a.gclk[pi] = carry;
+    if (g == a.groups - 1) {
+        const double gs = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, min(c_begin * kC, Tb),
+                                                        min(c_end * kC, Tb), red, tid)
+                                      : 0.0;
+        if (tid == 0) a.Gg[pi] = (float)gs;
+        float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
+        const size_t sb = (size_t)bh * kStateW;
+        for (int e = 4 * tid; e < kStateW; e += 4 * kNT) {
+            if (p.K0) *reinterpret_cast<float4 *>(S0 + e) = *reinterpret_cast<const float4 *>(p.K0 + sb + e);
+            if (p.V0) *reinterpret_cast<float4 *>(S0 + kStateW + e) = *reinterpret_cast<const float4 *>(p.V0 + sb + e);
+        }
+        return;
+    }
+    __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
+    const Sw z = make_sw(tid);
+    f32x16 kacc[4], vacc[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
+    }
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
+    uint4 rk, rv;
+    Tok tk;
+    auto prefetch = [&](int c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = ((row0 + t0) * p.H + h) * 128;
+        load_row1(kin + base, rs, n, tid, rk);
+        load_row1(vin + base, rs, n, tid, rv);
+        load_tok(p, row0, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_begin);
+    double gsum = 0.0;
+    float Ls = 0.f;
+    for (int c = c_begin; c < c_end; ++c) {
+        store_row1(Kt, rk, z);
+        store_row1(Vt, rv, z);
+        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
+        if (c + 1 < c_end) prefetch(c + 1);
+        lds_barrier();
+        build_A(sc, Asm, tid, m);
+        gsum += (double)sc.G[kC - 1];
+        {
+            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
+            if (f != 1.f) {
+                scale_acc(kacc, f);
+                scale_acc(vacc, f);
+            }
+        }
+        Ls = next_scale(sc, Ls);
+        lds_barrier();
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 ad = scale_k(stro_w(Asm, 16 * ks, 32 * w, z), sc.rho + 16 * ks + 8 * hl);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 32 * x, z), ad, kacc[x]);
+            const bf16x8 vb = stro(Vt, 16 * ks, 32 * cb, z);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                vacc[j] = mma(scale_k(stro_w(Asm, 16 * ks, 128 * hh + 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb,
+                              vacc[j]);
+        }
+        lds_barrier();
+    }
     const float f = __expf(Ls);
-    if (p.K_out) store_key_state(p.K_out + sb, kacc, f, w, lane, m);
-    if (p.V_out) store_value_state(p.V_out + sb, vacc, f, hh, cb, lane, m);
-    if (p.clock_out && tid == 0) p.clock_out[bh] = carry;
+    float *E = a.Ef + pi * 2 * kStateW;
+    store_dump(E, kacc, f, w, lane);
+    store_dump(E + kStateW, vacc, f, w, lane);
+    if (tid == 0) a.Gg[pi] = (float)gsum;
 }
 
 // bf16 readout matrix for the kernel above from the fp32 one (paper basis order,
@@ -625,20 +832,73 @@ bool mfma_wide_supported(const FwdParams &p) {
            (p.chunk == 32 || p.chunk == 64);
 }
 
-size_t mfma_wide_workspace_bytes(const FwdParams &p) {
-    return 2 * (((size_t)p.H * kR * kR * 2 + 255) / 256 * 256);
+int mfma_wide_auto_groups(const FwdParams &p) {
+    // one eight-wave workgroup per compute unit: split sequences into chunk groups
+    // until B H G covers the 256 compute units
+    const int nc = (p.T + kC - 1) / kC;
+    const int BH = p.B * p.H;
+    int g = (256 + BH - 1) / BH;
+    if (g > nc) g = nc;
+    return g < 1 ? 1 : g;
 }
 
-hipError_t launch_fwd_mfma_wide(const FwdParams &p, const float *M, void *ws, hipStream_t st, hipEvent_t ev_start,
-                                hipEvent_t ev_stop) {
-    const size_t half = ((size_t)p.H * kR * kR * 2 + 255) / 256 * 256;
-    __bf16 *Mz = static_cast<__bf16 *>(ws);
-    __bf16 *MzT = reinterpret_cast<__bf16 *>(static_cast<char *>(ws) + half);
-    hipLaunchKernelGGL(wide_mz_kernel, dim3(p.H, kR), dim3(kR), 0, st, p.m, M, Mz, MzT,
-                       p.scale * 1.4426950408889634f);
+namespace {
+struct WideWs {
+    size_t mz, mzt, ef, gg, gclk, s0, total;
+};
+WideWs wide_ws(const FwdParams &p, int groups) {
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t BH = (size_t)p.B * p.H, G = groups;
+    WideWs L{};
+    size_t off = 0;
+    L.mz = off;
+    off += up((size_t)p.H * kR * kR * 2);
+    L.mzt = off;
+    off += up((size_t)p.H * kR * kR * 2);
+    if (groups > 1) {
+        L.ef = off;
+        off += up(BH * G * 2 * kStateW * 4);
+        L.gg = off;
+        off += up(BH * G * 4);
+        L.gclk = off;
+        off += up(BH * G * 8);
+        L.s0 = off;
+        off += up(BH * 2 * kStateW * 4);
+    }
+    L.total = off;
+    return L;
+}
+}  // namespace
+
+size_t mfma_wide_workspace_bytes(const FwdParams &p, int groups) { return wide_ws(p, groups).total; }
+
+hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
+                                hipEvent_t ev_start, hipEvent_t ev_stop) {
+    char *base = static_cast<char *>(ws);
+    const WideWs L = wide_ws(p, groups);
+    WideArgs a{};
+    a.p = p;
+    a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
+    a.MzT = reinterpret_cast<const __bf16 *>(base + L.mzt);
+    const int nc = (p.T + kC - 1) / kC;
+    a.cpg = nc > 0 ? (nc + groups - 1) / groups : 1;
+    a.groups = nc > 0 ? (nc + a.cpg - 1) / a.cpg : 1;      // no empty trailing group
+    if (a.groups > 1) {
+        a.Ef = reinterpret_cast<float *>(base + L.ef);
+        a.Gg = reinterpret_cast<float *>(base + L.gg);
+        a.gclk = reinterpret_cast<double *>(base + L.gclk);
+        a.S0 = reinterpret_cast<float *>(base + L.s0);
+    }
+    hipLaunchKernelGGL(wide_mz_kernel, dim3(p.H, kR), dim3(kR), 0, st, p.m, M, const_cast<__bf16 *>(a.Mz),
+                       const_cast<__bf16 *>(a.MzT), p.scale * 1.4426950408889634f);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipExtLaunchKernelGGL(wide_forward_kernel, dim3(p.B * p.H), dim3(kNT), 0, st, ev_start, ev_stop, 0, p, Mz, MzT);
+    const dim3 grid(p.B * p.H, a.groups);
+    if (a.groups > 1) {
+        hipLaunchKernelGGL(wide_contrib_kernel, grid, dim3(kNT), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipExtLaunchKernelGGL(wide_forward_kernel, grid, dim3(kNT), 0, st, ev_start, ev_stop, 0, a);
     return hipGetLastError();
 }
 

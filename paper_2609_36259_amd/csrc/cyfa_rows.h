@@ -23,13 +23,15 @@ inline size_t readout_bytes(int H, int m) {
 hipError_t launch_readout_prep_wide(int H, int m, const float *R, float *M, hipStream_t s);
 
 // Matrix-core forward for 127 < m <= 255 (bf16, d_k = d_v = 128, chunk 32 or 64 run
-// as 32-token chunks, one workgroup per sequence).  ws (mfma_wide_workspace_bytes)
-// receives the bf16 readout matrix and its transpose, formed from the fp32 M of
-// launch_readout_prep_wide; the events, when given, bracket the fused kernel.
+// as 32-token chunks, one workgroup per chunk group of a sequence).  ws
+// (mfma_wide_workspace_bytes) receives the bf16 readout matrix and its transpose,
+// formed from the fp32 M of launch_readout_prep_wide, and with groups > 1 the groups'
+// contributions; the events, when given, bracket the fused kernel.
 bool mfma_wide_supported(const FwdParams &p);
-size_t mfma_wide_workspace_bytes(const FwdParams &p);
-hipError_t launch_fwd_mfma_wide(const FwdParams &p, const float *M, void *ws, hipStream_t st, hipEvent_t ev_start,
-                                hipEvent_t ev_stop);
+int mfma_wide_auto_groups(const FwdParams &p);
+size_t mfma_wide_workspace_bytes(const FwdParams &p, int groups);
+hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
+                                hipEvent_t ev_start, hipEvent_t ev_stop);
 
 // Vector-ALU forward over chunk groups (d_k, d_v <= 128 and m <= 127; other
 // shapes run one group per sequence): groups > 1 forms the state entering each

@@ -80,8 +80,13 @@ def test_status_codes():
     assert n.value == 3 * 256 * 256 * 4 + 2 * 3 * 256 * 256 * 2
     d = cyfa.forward_desc(1, 16, 1, 128, 128, m=129, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
-    d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA, segments=2)
-    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
+    # chunk groups (one workgroup each): their contributions, decays, clocks and a copy
+    # of the initial states join the workspace
+    d = cyfa.forward_desc(2, 4096, 4, 128, 128, m=255, dtype=cyfa.BF16)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    G, BH = 32, 8
+    assert n.value == (4 * 256 * 256 * 4 + 2 * 4 * 256 * 256 * 2 + BH * G * 2 * 256 * 128 * 4 + BH * G * 4
+                       + BH * G * 8 + BH * 2 * 256 * 128 * 4)
     d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA, chunk=16)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     d = cyfa.forward_desc(1, 16, 1, 96, 64)

@@ -5,10 +5,11 @@ bf16, d_k = d_v = 128, 32-token chunks) against the oracle.
 Every output element, the slot logits, the final states and the clock are
 compared with the oracle on the same seeded inputs (several chunks and a ragged
 tail, with and without initial states); bar: max relative error 2e-2 (bf16
-inputs, fp32 accumulation), clock 1e-9.  Packed sequences (cyfa_forward_varlen)
-must reproduce the padded entry point with lengths bit for bit; a forward split
-in two and resumed in place must equal one pass; one full-size 1.4B-layer shape
-at m = 255 is compared on sampled sequences.
+inputs, fp32 accumulation), clock 1e-9.  One workgroup per sequence and
+the automatic chunk groups are both covered, and 1, 2 and 5 groups agree.
+Packed sequences (cyfa_forward_varlen) must reproduce the padded entry point with
+lengths bit for bit; a forward split in two and resumed in place must equal one
+pass; one full-size 1.4B-layer shape at m = 255 is compared on sampled sequences.
 """
 import numpy as np
 import pytest
@@ -89,12 +90,15 @@ def _check(x, res, init=None, lens=None):
 
 @pytest.mark.parametrize("m", [129, 255])
 @pytest.mark.parametrize("with_init", [False, True])
-def test_full_parity(m, with_init):
+@pytest.mark.parametrize("segments", [1, 0])
+def test_full_parity(m, with_init, segments):
+    """segments 1: one workgroup per sequence; 0: the automatic chunk groups (four
+    here, each starting from the earlier groups' contributions)."""
     x = make_forward_inputs(2, 32 * 3 + 7, 2, 128, 128, seed=71, dtype="bf16", m=m)
     t = upload(x)
     init = _init_states(2, 2, m, 72) if with_init else None
     kw = dict(K0=init[0], V0=init[1], clock0=init[2]) if init else {}
-    res = _fwd(x, t, return_state=True, return_logits=True, **kw)
+    res = _fwd(x, t, return_state=True, return_logits=True, segments=segments, **kw)
     torch.cuda.synchronize()
     assert res["K"].shape == (2, 2, ROWS, 128)
     _check(x, res, init=init)
@@ -208,10 +212,19 @@ def test_full_size_sampled_sequences():
         assert v <= (1e-9 if k == "clock" else TOL_BF16), (k, v)
 
 
-def test_rejects_segments():
-    cyfa = _cyfa()
-    x = make_forward_inputs(1, 64, 1, 128, 128, seed=80, dtype="bf16", m=255)
+def test_chunk_group_invariance():
+    """One, two and five chunk groups per sequence give the same result up to
+    rounding: each group scales its decayed write operands from its own start before
+    they are rounded to bf16, so the state updates round differently (bar 1e-2 for
+    outputs and states; measured ~3e-3)."""
+    x = make_forward_inputs(1, 32 * 9 + 5, 3, 128, 128, seed=80, dtype="bf16", m=255)
     t = upload(x)
-    with pytest.raises(cyfa.CyfaError) as ei:
-        _fwd(x, t, segments=2)
-    assert ei.value.status == 2
+    init = _init_states(1, 3, 255, 81)
+    runs = [_fwd(x, t, segments=s, K0=init[0], V0=init[1], clock0=init[2], return_state=True) for s in (1, 2, 5)]
+    torch.cuda.synchronize()
+    for r in runs[1:]:
+        errs = {k: rel_err(r[k].float().cpu().numpy(), runs[0][k].float().cpu().numpy()) for k in ("o", "K", "V")}
+        print("against one group", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+        assert max(errs.values()) <= 1e-2, errs
+        assert torch.equal(r["clock"], runs[0]["clock"]) or \
+            clock_err(r["clock"].cpu().numpy(), runs[0]["clock"].cpu().numpy(), 255) <= 1e-9

@@ -92,21 +92,22 @@ def test_bf16_valu_kernel_d256():
 
 
 def test_bf16_m255_and_resume():
-    """m = 255 (256 storage rows) with bf16 inputs; split-and-resume through the
-    256-row states equals one pass."""
+    """m = 255 (256 storage rows) with bf16 inputs on the vector-ALU kernel (the
+    matrix-core one has its own tests); split-and-resume through the 256-row states
+    equals one pass."""
     cyfa = _cyfa()
     x = make_forward_inputs(2, 60, 2, 128, 128, seed=25, dtype="bf16", m=255)
     t = upload(x)
-    full = _fwd(x, t, return_state=True, return_logits=True)
+    full = _fwd(x, t, return_state=True, return_logits=True, kernel=cyfa.KERNEL_VALU)
     assert full["K"].shape == (2, 2, 256, 128)
     _check_full(x, full, TOL_BF16)
     t1 = 29
     a = {k: (v[:, :t1].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
     b = {k: (v[:, t1:].contiguous() if v is not None and k != "R" else v) for k, v in t.items()}
-    first = _fwd(x, a, return_state=True)
+    first = _fwd(x, a, return_state=True, kernel=cyfa.KERNEL_VALU)
     second = cyfa.forward(b["q"], b["k"], b["v"], b["delta"], b["log_alpha"], b["beta"], b["R"],
                           scale=x["scale"], m=255, K0=first["K"], V0=first["V"], clock0=first["clock"],
-                          return_state=True)
+                          return_state=True, kernel=cyfa.KERNEL_VALU)
     torch.cuda.synchronize()
     o_split = torch.cat([first["o"], second["o"]], dim=1).float().cpu().numpy()
     assert rel_err(o_split, full["o"].float().cpu().numpy()) <= 1e-2

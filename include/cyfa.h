@@ -36,8 +36,9 @@
  *     basis order of App. A.1 (row 0 = DC component, row 2j-1 = cosine of
  *     frequency j, row 2j = its sine) and rows m..S-1 are padding: ignored on
  *     input, written as zero on output.  Below, "128" in a state shape reads
- *     S.  m > 127 runs the vector-ALU forward and the decode step with head
- *     dims 64 or 128; the matrix-core kernel and the backward take m <= 127.
+ *     S.  m > 127 runs the forward (matrix-core kernel for BF16 with d_k = d_v
+ *     = 128, else the vector-ALU kernel) and the decode step with head dims 64 or
+ *     128; the backward takes m <= 127.
  *   - Clocks are double precision and are reported reduced modulo m, which is
  *     exact because U(tau + m) = U(tau) (App. A.1, Prop. 1) and the output
  *     depends only on clock differences (App. A.4, Prop. 6).
@@ -67,14 +68,14 @@ typedef enum {
 } cyfa_dtype;
 
 typedef enum {
-    CYFA_KERNEL_AUTO = 0,  /* BF16 with d_k = d_v = 128 or d_k = d_v = 256 and
-                              m <= 127: matrix-core kernel; anything else: the
-                              vector-ALU kernel                               */
+    CYFA_KERNEL_AUTO = 0,  /* BF16 with d_k = d_v = 128 (m up to 255) or d_k =
+                              d_v = 256 (m <= 127): matrix-core kernel; anything
+                              else: the vector-ALU kernel                     */
     CYFA_KERNEL_VALU = 1,  /* vector-ALU chunk kernel, fp32 arithmetic, any
                               supported shape and dtype                        */
     CYFA_KERNEL_MFMA = 2   /* matrix-core (bf16 MFMA) chunk kernel: BF16,
-                              d_k = d_v = 128 or d_k = d_v = 256, m <= 127,
-                              chunk 32 or 64                                   */
+                              d_k = d_v = 128 (m up to 255) or d_k = d_v = 256
+                              (m <= 127), chunk 32 or 64                       */
 } cyfa_kernel;
 
 /*
@@ -90,9 +91,10 @@ typedef enum {
  *                it beyond rounding (App. B: the chunk form is exact).
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
  *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
- *                than one only for d_k, d_v <= 128 and m <= 127).  The state
- *                entering a segment is obtained from a pre-pass over the earlier
- *                segments.  Results do not depend on it beyond rounding.
+ *                than one only for d_k, d_v <= 128 and m <= 127; the MFMA kernel
+ *                at m > 127: groups of 32-token chunks).  The state entering a
+ *                segment is obtained from a pre-pass over the earlier segments.
+ *                Results do not depend on it beyond rounding.
  *   scale        logit scale (the paper leaves the dot-product scaling out of
  *                its notation, Sec. 3.1 footnote); multiplies R K_t q_t
  *   dtype        storage type of q, k, v and o

@@ -341,7 +341,12 @@ __device__ __forceinline__ void store_rows(__bf16 *T, const Rows2 &o, const Sw &
 }
 
 // 512-thread variant: one 16-byte piece per thread (row tid/16, columns 8 (tid % 16)).
+// kOpq: the lane's offsets are recomputed at every call, opaque to the compiler (in the
+// reverse walk, kept live across the chunk loop as 64-bit addresses they are spilled,
+// and every reload waits for all of the wave's outstanding loads).
+template <bool kOpq = false>
 __device__ __forceinline__ void load_row1(const __bf16 *base, size_t row_stride, int n, int tid, uint4 &o) {
+    if (kOpq) tid = opq(tid);
     const int r = tid >> 4, c8 = (tid & 15) * 8;
     const uint4 v = *reinterpret_cast<const uint4 *>(base + (size_t)min(r, max(n - 1, 0)) * row_stride + c8);
     o = r < n ? v : make_uint4(0, 0, 0, 0);
@@ -399,9 +404,12 @@ static_assert(kScBytes % 16 == 0, "scalar block");
 // plain values and the registers are multiplied by exp(G_C) (ctl[1]) before the
 // update.  Every thread tracks Ls itself from the same LDS values.
 enum { kPlain = 0, kLazy = 1, kLazyAdj = 2 };
-template <int kMode>
+// kOpq: the lane's LDS offsets are recomputed at every call rather than kept (and
+// spilled) across the reverse walk's chunk loop.
+template <int kMode, bool kOpq = false>
 __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, bool dec_amp,
                                               float Ls = 0.f) {
+    if (kOpq) lane = opq(lane);
     const double inv_m = 1.0 / (double)m;
     const float G = wave_incl_scan(k.g);
     const double lam = carry + wave_incl_scan((double)k.dl);
@@ -1191,12 +1199,12 @@ __global__ __launch_bounds__(kNT8, 1) void grad_kernel(Args a) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
         const size_t base = (((size_t)b * p.T + t0) * p.H + h) * 128;
         const size_t wb = ((size_t)bh * p.Tpad + t0) * 128;
-        load_row1(qin + base, rs, n, tid, pq);
-        load_row1(kin + base, rs, n, tid, pk);
-        load_row1(vin + base, rs, n, tid, pv);
-        load_row1(oin + base, rs, n, tid, po);
-        load_row1(a.U + wb, 128, kC, tid, pu);
-        load_row1(a.dP + wb, 128, kC, tid, pp);
+        load_row1<true>(qin + base, rs, n, tid, pq);
+        load_row1<true>(kin + base, rs, n, tid, pk);
+        load_row1<true>(vin + base, rs, n, tid, pv);
+        load_row1<true>(oin + base, rs, n, tid, po);
+        load_row1<true>(a.U + wb, 128, kC, tid, pu);
+        load_row1<true>(a.dP + wb, 128, kC, tid, pp);
         load_tok(p, b, h, t0, Tb, tid, tk);
         // the readout walk's per-token terms and the chunk's entering clock
         pclk = a.cclk[(size_t)bh * p.nc + c];
@@ -1225,7 +1233,7 @@ __global__ __launch_bounds__(kNT8, 1) void grad_kernel(Args a) {
         const float cur_udu = pudu, cur_dl = pdl;    // this chunk's (the prefetch moves on)
         if (w8 == 0) {
             double carry = pclk;
-            chunk_scalars<kLazyAdj>(sc, lane, m, tk, carry, false, Ls);
+            chunk_scalars<kLazyAdj, true>(sc, lane, m, tk, carry, false, Ls);
         }
         lds_barrier();
         {

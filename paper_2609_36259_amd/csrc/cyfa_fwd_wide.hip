@@ -164,7 +164,11 @@ __device__ __forceinline__ void scale_acc(f32x16 (&acc)[N], float f) {
 }
 
 // ---- chunk staging (one 16-byte piece of each [32][128] tile per thread) ------
+// (The lane's offsets are recomputed at every call, opaque to the compiler: kept live
+// across the chunk loop as 64-bit addresses they would be spilled, and every reload
+// would wait for all of the wave's outstanding loads.)
 __device__ __forceinline__ void load_row1(const __bf16 *base, size_t row_stride, int n, int tid, uint4 &o) {
+    tid = opq(tid);
     const int r = tid >> 4, c8 = (tid & 15) * 8;
     const uint4 v = *reinterpret_cast<const uint4 *>(base + (size_t)min(r, max(n - 1, 0)) * row_stride + c8);
     o = r < n ? v : make_uint4(0, 0, 0, 0);
@@ -219,6 +223,7 @@ struct Sc {
 // chunk is eager (registers times exp(Ls) first, Ls restarts at 0, plain gam and rho,
 // registers times exp(G_C) before the update).
 __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, float Ls) {
+    lane = opq(lane);                               // per-lane LDS offsets recomputed, not spilled
     const double inv_m = 1.0 / (double)m;
     const float G = wave_incl_scan(k.g);
     const double lam = carry + wave_incl_scan((double)k.dl);
@@ -342,7 +347,7 @@ __device__ __forceinline__ void score_block(const __bf16 *Am, int m0, const __bf
 
 // ---- state in / out (ABI layout [B][H][256][128], paper row order) ------------
 // Key state (kacc[x]: slot i = 32 w + lane % 32, channel c = 32 x + 8 (v/4) + 4 (lane/32) + v%4).
-__device__ __forceinline__ void add_key_state(f32x16 (&acc)[4], const float *S, int w, int lane, int m) {
+__device__ __forceinline__ void add_key_state(f32x16 (&acc)[4], const float *S, float f, int w, int lane, int m) {
     const int i = 32 * w + (lane & 31);
     if (!row_active_w(i, m)) return;
     const float *row = S + (size_t)paper_row_w(i) * 128 + 4 * (lane >> 5);
@@ -351,10 +356,10 @@ __device__ __forceinline__ void add_key_state(f32x16 (&acc)[4], const float *S, 
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
             const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
-            acc[x][4 * v4] += q.x;
-            acc[x][4 * v4 + 1] += q.y;
-            acc[x][4 * v4 + 2] += q.z;
-            acc[x][4 * v4 + 3] += q.w;
+            acc[x][4 * v4] = fmaf(f, q.x, acc[x][4 * v4]);
+            acc[x][4 * v4 + 1] = fmaf(f, q.y, acc[x][4 * v4 + 1]);
+            acc[x][4 * v4 + 2] = fmaf(f, q.z, acc[x][4 * v4 + 2]);
+            acc[x][4 * v4 + 3] = fmaf(f, q.w, acc[x][4 * v4 + 3]);
         }
 }
 __device__ __forceinline__ void store_key_state(float *S, const f32x16 (&acc)[4], float f, int w, int lane, int m) {
@@ -375,14 +380,15 @@ __device__ __forceinline__ void store_key_state(float *S, const f32x16 (&acc)[4]
 __device__ __forceinline__ int value_slot(int hh, int j, int v, int hl) {
     return 128 * hh + 32 * j + 8 * (v >> 2) + 4 * hl + (v & 3);
 }
-__device__ __forceinline__ void add_value_state(f32x16 (&acc)[4], const float *S, int hh, int cb, int lane, int m) {
+__device__ __forceinline__ void add_value_state(f32x16 (&acc)[4], const float *S, float f, int hh, int cb, int lane,
+                                                int m) {
     const int c = 32 * cb + (lane & 31), hl = lane >> 5;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int i = value_slot(hh, j, v, hl);
-            if (row_active_w(i, m)) acc[j][v] += S[(size_t)paper_row_w(i) * 128 + c];
+            if (row_active_w(i, m)) acc[j][v] = fmaf(f, S[(size_t)paper_row_w(i) * 128 + c], acc[j][v]);
         }
 }
 __device__ __forceinline__ void store_value_state(float *S, const f32x16 (&acc)[4], float f, int hh, int cb, int lane,
@@ -512,8 +518,8 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(WideArgs a) {
     const size_t sb = (size_t)bh * kStateW;
     double carry;
     if (a.groups == 1) {
-        if (p.K0) add_key_state(kacc, p.K0 + sb, w, lane, m);
-        if (p.V0) add_value_state(vacc, p.V0 + sb, hh, cb, lane, m);
+        if (p.K0) add_key_state(kacc, p.K0 + sb, 1.f, w, lane, m);
+        if (p.V0) add_value_state(vacc, p.V0 + sb, 1.f, hh, cb, lane, m);
         carry = reduce_clock(p.clock0 ? p.clock0[bh] : 0.0, (double)m, 1.0 / (double)m);
     } else {
         // state entering the group: each earlier group's contribution decayed through
@@ -527,25 +533,9 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(WideArgs a) {
             add_dump(vacc, E + kStateW, f, w, lane);
             tail += Gg[q];
         }
-        if (p.K0 || p.V0) {
-            f32x16 k0[4], v0[4];
-#pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                k0[x] = zero_acc();
-                v0[x] = zero_acc();
-            }
-            const float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
-            if (p.K0) add_key_state(k0, S0, w, lane, m);
-            if (p.V0) add_value_state(v0, S0 + kStateW, hh, cb, lane, m);
-            const float f = __expf(tail);
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    kacc[x][v] = fmaf(f, k0[x][v], kacc[x][v]);
-                    vacc[x][v] = fmaf(f, v0[x][v], vacc[x][v]);
-                }
-        }
+        const float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
+        if (p.K0) add_key_state(kacc, S0, __expf(tail), w, lane, m);
+        if (p.V0) add_value_state(vacc, S0 + kStateW, __expf(tail), hh, cb, lane, m);
         carry = a.gclk[(size_t)bh * a.groups + g];
     }
 

@@ -156,9 +156,11 @@ cyfa_status plan_backward(const cyfa_fwd_desc *d, BwdPlan *plan) {
         return fail(CYFA_ERR_INVALID_ARGUMENT, "problem too large");
     if (d->d_k <= 0 || d->d_v <= 0)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "head dims must be positive");
-    if ((d->d_k != 64 && d->d_k != 128) || (d->d_v != 64 && d->d_v != 128))
-        return fail(CYFA_ERR_UNSUPPORTED, "backward head dims must be 64 or 128 (got d_k=%d d_v=%d)",
-                    d->d_k, d->d_v);
+    const bool dims = ((d->d_k == 64 || d->d_k == 128) && (d->d_v == 64 || d->d_v == 128)) ||
+                      (d->d_k == 256 && d->d_v == 256);
+    if (!dims)
+        return fail(CYFA_ERR_UNSUPPORTED,
+                    "backward head dims must be 64 or 128 each, or both 256 (got d_k=%d d_v=%d)", d->d_k, d->d_v);
     if (d->m < 3 || d->m > cyfa::kMaxActive || (d->m % 2) == 0)
         return fail(d->m > cyfa::kMaxActive && (d->m % 2) == 1 ? CYFA_ERR_UNSUPPORTED
                                                                : CYFA_ERR_INVALID_ARGUMENT,

@@ -675,13 +675,17 @@ template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
     constexpr int KH = DK / kRP, VH = DV / kRP;
     constexpr int IHK = kNT / DK, IHV = kNT / DV;          // row blocks of the column products
-    __shared__ float Qs[kC][DK + 1], Ks[kC][DK + 1], gQ[kC][DK + 1], gK[kC][DK + 1];
+    // token rows per pass of the column products: all of them up to d = 128; two passes
+    // at d = 256, which halves their partial-sum buffer so that the tiles fit LDS
+    constexpr int kCP = (DK > 128 || DV > 128) ? kC / 2 : kC;
+    __shared__ float Qs[kC][DK + 1], Ks[kC][DK + 1];
     __shared__ float Vs[kC][DV + 1], dOs[kC][DV + 1];
     __shared__ float dPs[kC][kLD], Us[kC][kLD], As[kC][kLD], dAK[kC][kLD], dAV[kC][kLD];
     __shared__ __attribute__((aligned(16))) float dPT[kStoreRows][kC];   // dp and A transposed:
     __shared__ __attribute__((aligned(16))) float AT[kStoreRows][kC];    // all tokens of a row in 64 bytes
     __shared__ float Sqk[kC][kC + 1], Sdpa[kC][kC + 1], Suoa[kC][kC + 1], Sdov[kC][kC + 1];
-    __shared__ float red[kNT * kC];
+    __shared__ float red[kNT * kCP];
+    __shared__ float qkp[2][kC][kNT / 64];    // <q, dq> and <k, dk> per token, per 64 columns
     __shared__ ChunkTab tab;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -756,102 +760,112 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 Suoa[r][s] = a1;
             }
         }
-        // dq: gamma_r (dP Kbar_c)[r] + (Sdpa K)[r]
-        {
-            const int cc = tid % DK, ih = tid / DK;
-            constexpr int RB = kStoreRows / IHK;
-            float acc[kC];
+        // dq = gamma_r (dP Kbar_c)[r] + (Sdpa K)[r], dk = (Sdpa^T Q)[s] + rho_s (A DK')[s] and
+        // dv = (Suoa^T dO)[s] + rho_s (A DV')[s], written out as formed, kCP token rows per
+        // pass; the per-token <q, dq> and <k, dk> are reduced on the way (per wave: 64
+        // columns of one row)
+        for (int r0 = 0; r0 < kC; r0 += kCP) {
+            {
+                const int cc = tid % DK, ih = tid / DK;
+                constexpr int RB = kStoreRows / IHK;
+                float acc[kCP];
 #pragma unroll
-            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+                for (int r = 0; r < kCP; ++r) acc[r] = 0.f;
 #pragma unroll 2
-            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float kb = fmaf(dec_in, p.EcK[(sg + ii) * DK + cc], p.Kst[(st + ii) * DK + cc]);
+                for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                    const float kb = fmaf(dec_in, p.EcK[(sg + ii) * DK + cc], p.Kst[(st + ii) * DK + cc]);
 #pragma unroll
-                for (int q4 = 0; q4 < kC / 4; ++q4) {
-                    const float4 x = *reinterpret_cast<const float4 *>(&dPT[ii][4 * q4]);
-                    acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
-                    acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
-                    acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
-                    acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                    for (int q4 = 0; q4 < kCP / 4; ++q4) {
+                        const float4 x = *reinterpret_cast<const float4 *>(&dPT[ii][r0 + 4 * q4]);
+                        acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
+                        acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
+                        acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
+                        acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                    }
                 }
+#pragma unroll
+                for (int r = 0; r < kCP; ++r) red[(ih * kCP + r) * DK + cc] = acc[r];
             }
+            __syncthreads();
+            for (int e = tid; e < kCP * DK; e += kNT) {
+                const int r = r0 + e / DK, cc = e % DK;
+                float sum = 0.f;
+                for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kCP + r - r0) * DK + cc];
+                float acc = __expf(tab.G[r]) * sum;
+                for (int s = 0; s <= r; ++s) acc = fmaf(Sdpa[r][s], Ks[s][cc], acc);
+                const float part = wsum(Qs[r][cc] * acc);
+                if (lane == 0) qkp[0][r][cc >> 6] = part;
+                const int t = t0 + r;
+                if (t < p.T) store_from_float(gq, ((brow0(p, b) + t) * p.H + h) * DK + cc, t < Tb ? acc : 0.f);
+            }
+            __syncthreads();
+            {
+                const int cc = tid % DK, ih = tid / DK;
+                constexpr int RB = kStoreRows / IHK;
+                float acc[kCP];
 #pragma unroll
-            for (int r = 0; r < kC; ++r) red[(ih * kC + r) * DK + cc] = acc[r];
-        }
-        __syncthreads();
-        for (int e = tid; e < kC * DK; e += kNT) {
-            const int r = e / DK, cc = e % DK;
-            float sum = 0.f;
-            for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kC + r) * DK + cc];
-            float acc = __expf(tab.G[r]) * sum;
-            for (int s = 0; s <= r; ++s) acc = fmaf(Sdpa[r][s], Ks[s][cc], acc);
-            gQ[r][cc] = acc;
-        }
-        __syncthreads();
-        // dk: (Sdpa^T Q)[s] + rho_s (A DK')[s]
-        {
-            const int cc = tid % DK, ih = tid / DK;
-            constexpr int RB = kStoreRows / IHK;
-            float acc[kC];
-#pragma unroll
-            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+                for (int r = 0; r < kCP; ++r) acc[r] = 0.f;
 #pragma unroll 2
-            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float kb = fmaf(dec_out, p.AcK[(sg + ii) * DK + cc], p.DKe[(st + ii) * DK + cc]);
+                for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                    const float kb = fmaf(dec_out, p.AcK[(sg + ii) * DK + cc], p.DKe[(st + ii) * DK + cc]);
 #pragma unroll
-                for (int q4 = 0; q4 < kC / 4; ++q4) {
-                    const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][4 * q4]);
-                    acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
-                    acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
-                    acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
-                    acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                    for (int q4 = 0; q4 < kCP / 4; ++q4) {
+                        const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][r0 + 4 * q4]);
+                        acc[4 * q4] = fmaf(x.x, kb, acc[4 * q4]);
+                        acc[4 * q4 + 1] = fmaf(x.y, kb, acc[4 * q4 + 1]);
+                        acc[4 * q4 + 2] = fmaf(x.z, kb, acc[4 * q4 + 2]);
+                        acc[4 * q4 + 3] = fmaf(x.w, kb, acc[4 * q4 + 3]);
+                    }
                 }
+#pragma unroll
+                for (int s2 = 0; s2 < kCP; ++s2) red[(ih * kCP + s2) * DK + cc] = acc[s2];
             }
+            __syncthreads();
+            for (int e = tid; e < kCP * DK; e += kNT) {
+                const int s2 = r0 + e / DK, cc = e % DK;
+                float sum = 0.f;
+                for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kCP + s2 - r0) * DK + cc];
+                float acc = __expf(GC - tab.G[s2]) * sum;
+                for (int r = s2; r < kC; ++r) acc = fmaf(Sdpa[r][s2], Qs[r][cc], acc);
+                const float part = wsum(Ks[s2][cc] * acc);
+                if (lane == 0) qkp[1][s2][cc >> 6] = part;
+                const int t = t0 + s2;
+                if (t < p.T) store_from_float(gk, ((brow0(p, b) + t) * p.H + h) * DK + cc, t < Tb ? acc : 0.f);
+            }
+            __syncthreads();
+            {
+                const int cc = tid % DV, ih = tid / DV;
+                constexpr int RB = kStoreRows / IHV;
+                float acc[kCP];
 #pragma unroll
-            for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DK + cc] = acc[s];
-        }
-        __syncthreads();
-        for (int e = tid; e < kC * DK; e += kNT) {
-            const int s = e / DK, cc = e % DK;
-            float sum = 0.f;
-            for (int ih = 0; ih < IHK; ++ih) sum += red[(ih * kC + s) * DK + cc];
-            float acc = __expf(GC - tab.G[s]) * sum;
-            for (int r = s; r < kC; ++r) acc = fmaf(Sdpa[r][s], Qs[r][cc], acc);
-            gK[s][cc] = acc;
-        }
-        __syncthreads();
-        // dv: (Suoa^T dO)[s] + rho_s (A DV')[s], written out directly
-        {
-            const int cc = tid % DV, ih = tid / DV;
-            constexpr int RB = kStoreRows / IHV;
-            float acc[kC];
-#pragma unroll
-            for (int r = 0; r < kC; ++r) acc[r] = 0.f;
+                for (int r = 0; r < kCP; ++r) acc[r] = 0.f;
 #pragma unroll 2
-            for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
-                const float vb = fmaf(dec_out, p.AcV[(sg + ii) * DV + cc], p.DVe[(st + ii) * DV + cc]);
+                for (int ii = ih * RB; ii < (ih + 1) * RB; ++ii) {
+                    const float vb = fmaf(dec_out, p.AcV[(sg + ii) * DV + cc], p.DVe[(st + ii) * DV + cc]);
 #pragma unroll
-                for (int q4 = 0; q4 < kC / 4; ++q4) {
-                    const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][4 * q4]);
-                    acc[4 * q4] = fmaf(x.x, vb, acc[4 * q4]);
-                    acc[4 * q4 + 1] = fmaf(x.y, vb, acc[4 * q4 + 1]);
-                    acc[4 * q4 + 2] = fmaf(x.z, vb, acc[4 * q4 + 2]);
-                    acc[4 * q4 + 3] = fmaf(x.w, vb, acc[4 * q4 + 3]);
+                    for (int q4 = 0; q4 < kCP / 4; ++q4) {
+                        const float4 x = *reinterpret_cast<const float4 *>(&AT[ii][r0 + 4 * q4]);
+                        acc[4 * q4] = fmaf(x.x, vb, acc[4 * q4]);
+                        acc[4 * q4 + 1] = fmaf(x.y, vb, acc[4 * q4 + 1]);
+                        acc[4 * q4 + 2] = fmaf(x.z, vb, acc[4 * q4 + 2]);
+                        acc[4 * q4 + 3] = fmaf(x.w, vb, acc[4 * q4 + 3]);
+                    }
                 }
-            }
 #pragma unroll
-            for (int s = 0; s < kC; ++s) red[(ih * kC + s) * DV + cc] = acc[s];
-        }
-        __syncthreads();
-        for (int e = tid; e < kC * DV; e += kNT) {
-            const int s = e / DV, cc = e % DV;
-            const int t = t0 + s;
-            if (t >= p.T) continue;
-            float sum = 0.f;
-            for (int ih = 0; ih < IHV; ++ih) sum += red[(ih * kC + s) * DV + cc];
-            float acc = __expf(GC - tab.G[s]) * sum;
-            for (int r = s; r < kC; ++r) acc = fmaf(Suoa[r][s], dOs[r][cc], acc);
-            store_from_float(gv, ((brow0(p, b) + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
+                for (int s2 = 0; s2 < kCP; ++s2) red[(ih * kCP + s2) * DV + cc] = acc[s2];
+            }
+            __syncthreads();
+            for (int e = tid; e < kCP * DV; e += kNT) {
+                const int s2 = r0 + e / DV, cc = e % DV;
+                const int t = t0 + s2;
+                if (t >= p.T) continue;
+                float sum = 0.f;
+                for (int ih = 0; ih < IHV; ++ih) sum += red[(ih * kCP + s2 - r0) * DV + cc];
+                float acc = __expf(GC - tab.G[s2]) * sum;
+                for (int r = s2; r < kC; ++r) acc = fmaf(Suoa[r][s2], dOs[r][cc], acc);
+                store_from_float(gv, ((brow0(p, b) + t) * p.H + h) * DV + cc, t < Tb ? acc : 0.f);
+            }
+            __syncthreads();
         }
         // da, carried-state parts: rho_s (K DK'^T)[s][i] and rho_s (V DV'^T)[s][i];
         // thread (row i, part) sums its share of the columns for every token s
@@ -919,10 +933,10 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
         // per token: dbeta, clock gradient of a, dL/dG; dq and dk rows out
         for (int s = wave; s < kC; s += kNT / 64) {
             const int t = t0 + s;
-            float qdq = 0.f, kdk = 0.f;
-            for (int cc = lane; cc < DK; cc += 64) {
-                qdq = fmaf(Qs[s][cc], gQ[s][cc], qdq);
-                kdk = fmaf(Ks[s][cc], gK[s][cc], kdk);
+            float qdq = 0.f, kdk = 0.f;                // whole-token sums (every lane alike)
+            for (int j = 0; j < DK / 64; ++j) {
+                qdq += qkp[0][s][j];
+                kdk += qkp[1][s][j];
             }
             const float adav = As[s][lane] * dAV[s][lane] + As[s][lane + 64] * dAV[s][lane + 64];
             // <da, U(-lambda) b>: DC entry and the (cos, -sin) pairs
@@ -936,7 +950,7 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 if (lane == 0) db += dAK[s][0] / sqrtf((float)m);
             }
             const float gl = rot_grad(dAK[s], As[s], m, -1.f, lane);
-            const float sums = wsum(qdq - kdk - adav);
+            const float sums = (qdq - kdk) - wsum(adav);
             db = wsum(db);
             if (lane == 0 && t < p.T) {
                 const size_t ti = row0 + s;
@@ -945,14 +959,6 @@ __global__ __launch_bounds__(kNT) void bwd_grad_kernel(BwdParams p) {
                 p.dlam[ti] = live ? p.dlam[ti] + gl : 0.f;
                 if (p.gbeta) p.gbeta[(brow0(p, b) + t) * p.H + h] = live ? db : 0.f;
             }
-        }
-        for (int e = tid; e < kC * DK; e += kNT) {
-            const int r = e / DK, cc = e % DK;
-            const int t = t0 + r;
-            if (t >= p.T) continue;
-            const size_t gi = ((brow0(p, b) + t) * p.H + h) * DK + cc;
-            store_from_float(gq, gi, t < Tb ? gQ[r][cc] : 0.f);
-            store_from_float(gk, gi, t < Tb ? gK[r][cc] : 0.f);
         }
         __syncthreads();
     }
@@ -1240,6 +1246,7 @@ hipError_t launch_bwd_valu(BwdParams p, void *ws, hipStream_t s) {
     if (p.dk == 64 && p.dv == 64) return launch_dtype<64, 64>(p, s);
     if (p.dk == 64 && p.dv == 128) return launch_dtype<64, 128>(p, s);
     if (p.dk == 128 && p.dv == 64) return launch_dtype<128, 64>(p, s);
+    if (p.dk == 256 && p.dv == 256) return launch_dtype<256, 256>(p, s);
     return launch_dtype<128, 128>(p, s);
 }
 

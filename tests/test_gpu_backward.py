@@ -1,5 +1,5 @@
 """GPU parity of the vector-ALU backward (cyfa_backward, kernel VALU) against the
-backward oracle.
+backward oracle (head dims 64 and 128 in any combination, and both 256).
 
 Every gradient tensor is compared element by element with the oracle's float64
 reverse-mode gradients on the same seeded inputs, the same upstream gradient
@@ -103,6 +103,26 @@ def test_f32_head_dims(dk, dv):
     x = make_forward_inputs(1, 37, 2, dk, dv, seed=72, dtype="f32")
     e = _extras(x, 2)
     _compare(_run(x, e), _oracle(x, e), TOL_F32)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_head_dim_256(dtype):
+    """The paper's head size (d_k = d_v = 256; its 400M model's layer), initial
+    states, final-state adjoints, two chunk groups and a ragged tail."""
+    x = make_forward_inputs(2, 16 * 3 + 5, 2, 256, 256, seed=79, dtype=dtype)
+    e = _extras(x, 9)
+    _compare(_run(x, e, groups=2), _oracle(x, e), TOL_F32 if dtype == "f32" else TOL_BF16)
+
+
+def test_head_dim_256_ragged():
+    T = 16 * 3 + 7
+    x = make_forward_inputs(3, T, 1, 256, 256, seed=80, dtype="f32")
+    e = _extras(x, 10)
+    lens = [T, 20, 0]
+    g = _run(x, e, lens=lens, groups=2)
+    _compare(g, _oracle(x, e, lens=lens), TOL_F32)
+    for name in ("dq", "dk", "dv", "d_delta"):
+        assert np.all(g[name][1, 20:] == 0) and np.all(g[name][2] == 0), name
 
 
 def test_bf16_d128():

@@ -18,7 +18,7 @@ fp64 CPU oracle timed on a bounded sample of the same workload on this host),
 prologue and epilogue kernels at the same shape), ``layer`` (prologue, forward
 and epilogue as three calls against the layer forward cyfa_forward_mixer) and
 ``paper_op`` (the forward at the paper's operator-benchmark shape, B 32, T 2048,
-H 4, d 256) and ``wide`` (the forward with m = 255 slots, 256 storage rows, at the
+H 4, d 256, and the vector-ALU backward there) and ``wide`` (the forward with m = 255 slots, 256 storage rows, at the
 1.4B-scale layer shape, against the vector-ALU forward there).
 """
 from __future__ import annotations
@@ -452,22 +452,28 @@ def paper_op_bench(args, torch, cyfa):
     import argparse as _ap
     from paper_2609_36259_amd.inputs import FWD_PAPER_OP as w
     sub = _ap.Namespace(kernel="auto", chunk=0, segments=0, steps=200, warmup=100, cold_steps=0)
-    fb = forward_bench(sub, torch, cyfa, w, forward_inputs(sub, torch, w))
+    prepared = forward_inputs(sub, torch, w)
+    fb = forward_bench(sub, torch, cyfa, w, prepared)
     ks = fb["kernel_ms"] * 1e-3
+    res = dict(workload=w.name, kernel=fb["kernel"], chunk=fb["chunk"], steps=sub.steps,
+               ms_per_step=fb["ms_per_step"], tokens_per_s=w.B * w.T / (fb["ms_per_step"] * 1e-3),
+               fused_kernel_ms=fb["kernel_ms"],
+               mfma={"achieved": fb["flops"] / ks / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": fb["flops"] / ks / 1e12 / PEAK_BF16_TFLOPS},
+               hbm={"achieved": fb["bytes"] / ks / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": fb["bytes"] / ks / 1e9 / PEAK_HBM_GBS})
+    if not args.no_backward:
+        # the backward at the paper's head size runs on the vector ALU
+        res["backward"] = backward_bench(args, torch, cyfa, w, prepared)
+    del prepared
     torch.cuda.empty_cache()
-    return dict(workload=w.name, kernel=fb["kernel"], chunk=fb["chunk"], steps=sub.steps,
-                ms_per_step=fb["ms_per_step"], tokens_per_s=w.B * w.T / (fb["ms_per_step"] * 1e-3),
-                fused_kernel_ms=fb["kernel_ms"],
-                mfma={"achieved": fb["flops"] / ks / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                      "frac": fb["flops"] / ks / 1e12 / PEAK_BF16_TFLOPS},
-                hbm={"achieved": fb["bytes"] / ks / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": fb["bytes"] / ks / 1e9 / PEAK_HBM_GBS})
+    return res
 
 
 def wide_bench(args, torch, cyfa):
     """The forward with the largest slot count of the paper's ablation (m = 255,
     256 storage rows) at the 1.4B-scale layer shape: the matrix-core kernel (the
-    automatic choice, one workgroup per sequence; fused kernel timed with HIP events)
+    automatic choice, automatic chunk groups; fused kernel timed with HIP events)
     and the vector-ALU forward on the same inputs."""
     import argparse as _ap
     from paper_2609_36259_amd.inputs import FWD_1P4B_M255 as w

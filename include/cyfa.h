@@ -204,10 +204,12 @@ cyfa_status cyfa_forward_varlen(const cyfa_fwd_desc *desc,
 
 /*
  * Bytes of device workspace cyfa_backward needs for `desc` (host-only).  The
- * backward keeps the states entering every 16-token chunk and the adjoint
- * states at every chunk's end (2 x B H ceil(T/16) 128 (d_k + d_v) floats) and
- * two 128-float rows per token and head; at B=4, T=4096, H=16, d=128 that is
- * about 4.6 GB.
+ * vector-ALU backward keeps the states entering every 16-token chunk and the
+ * adjoint states at every chunk's end (2 x B H ceil(T/16) 128 (d_k + d_v)
+ * floats) and two 128-float rows per token and head: about 4.6 GB at B=4,
+ * T=4096, H=16, d=128.  The matrix-core backward keeps each chunk group's state
+ * contributions and two bf16 128-element rows per token and head: about 0.23 GB
+ * there.
  */
 cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes);
 
@@ -221,9 +223,12 @@ cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *byte
  * gradients (Eq. app-clock-gradient-accumulation).  The forward is recomputed
  * inside the call (only the inputs are needed).
  *
- * desc       as for cyfa_forward: d_k, d_v in {64, 128}; dtype F32 or BF16;
- *            chunk 0 or 16; segments = chunk groups per sequence for the
- *            parallel kernels (0 = automatic); kernel AUTO or VALU
+ * desc       as for cyfa_forward: d_k, d_v in {64, 128}, or both 256; m <= 127;
+ *            dtype F32 or BF16; segments = chunk groups per sequence for the
+ *            parallel kernels (0 = automatic).  kernel MFMA: the matrix-core
+ *            backward (BF16 with d_k = d_v = 128; chunk 0 or 32), the automatic
+ *            choice there unless chunk is 16; VALU: the vector-ALU backward (chunk
+ *            0 or 16; fp32 arithmetic)
  * q .. lens, K0, V0, clock0   the forward's inputs, same layouts and NULL rules
  * d_o        [B, T, H, d_v] dtype: dL/do (required)
  * dK_T, dV_T [B, H, 128, d_k] / [B, H, 128, d_v] float: dL/dK_out, dL/dV_out,
@@ -239,7 +244,9 @@ cyfa_status cyfa_backward_workspace_size(const cyfa_fwd_desc *desc, size_t *byte
  * Rows t >= lens[b] of every per-token gradient are written as 0.  Gradients
  * are written, not accumulated.  Outputs must not alias inputs or each other.
  * workspace  at least cyfa_backward_workspace_size bytes, 256-byte aligned.
- * Arithmetic is fp32; bf16 gradients are rounded to nearest even.
+ * The vector-ALU backward computes in fp32; the matrix-core one multiplies bf16
+ * operands with fp32 accumulation (states, adjoints and reductions in fp32).  bf16
+ * gradients are rounded to nearest even.
  */
 cyfa_status cyfa_backward(const cyfa_fwd_desc *desc,
                           const void *q, const void *k, const void *v,

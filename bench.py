@@ -18,8 +18,10 @@ fp64 CPU oracle timed on a bounded sample of the same workload on this host),
 prologue and epilogue kernels at the same shape), ``layer`` (prologue, forward
 and epilogue as three calls against the layer forward cyfa_forward_mixer) and
 ``paper_op`` (the forward at the paper's operator-benchmark shape, B 32, T 2048,
-H 4, d 256, and the vector-ALU backward there) and ``wide`` (the forward with m = 255 slots, 256 storage rows, at the
-1.4B-scale layer shape, against the vector-ALU forward there).
+H 4, d 256, and the vector-ALU backward there), ``wide`` (the forward with
+m = 255 slots, 256 storage rows, at the 1.4B-scale layer shape, against the
+vector-ALU forward there) and ``narrow`` (the forward with m = 63 slots on 64
+storage rows at the same shape).
 """
 from __future__ import annotations
 
@@ -496,6 +498,29 @@ def wide_bench(args, torch, cyfa):
                       "steps": valu.steps})
 
 
+def narrow_bench(args, torch, cyfa):
+    """The forward with the smallest slot count of the paper's ablation (m = 63, 64
+    storage rows) at the 1.4B-scale layer shape: the matrix-core kernel on 64 rows
+    (the automatic choice, automatic chunk groups; fused kernel timed with HIP
+    events).  The 128-row kernel's cost does not depend on m <= 127, so the
+    headline forward at m = 127 is its figure at m = 63 too."""
+    import argparse as _ap
+    from paper_2609_36259_amd.inputs import FWD_1P4B_M63 as w
+    prepared = forward_inputs(None, torch, w)
+    sub = _ap.Namespace(kernel="auto", chunk=0, segments=0, steps=200, warmup=100, cold_steps=0)
+    fb = forward_bench(sub, torch, cyfa, w, prepared)
+    del prepared
+    torch.cuda.empty_cache()
+    ks = fb["kernel_ms"] * 1e-3
+    return dict(workload=w.name, m=w.m, kernel=fb["kernel"], chunk=fb["chunk"], steps=sub.steps,
+                ms_per_step=fb["ms_per_step"], tokens_per_s=w.B * w.T / (fb["ms_per_step"] * 1e-3),
+                fused_kernel_ms=fb["kernel_ms"],
+                mfma={"achieved": fb["flops"] / ks / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                      "frac": fb["flops"] / ks / 1e12 / PEAK_BF16_TFLOPS, "alg_flops_per_launch": fb["flops"]},
+                hbm={"achieved": fb["bytes"] / ks / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": fb["bytes"] / ks / 1e9 / PEAK_HBM_GBS})
+
+
 def cpu_baseline(w, budget_s: float):
     """Time the CPU oracle on a bounded sample of the workload (leading (b, h)
     sequences, leading tokens), sized to about `budget_s` seconds."""
@@ -542,6 +567,7 @@ def main():
     ap.add_argument("--no-paper-op", action="store_true")
     ap.add_argument("--no-layer", action="store_true")
     ap.add_argument("--no-wide", action="store_true")
+    ap.add_argument("--no-narrow", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -585,6 +611,8 @@ def main():
         extra["paper_op"] = paper_op_bench(args, torch, cyfa)
     if not args.no_wide:
         extra["wide"] = wide_bench(args, torch, cyfa)
+    if not args.no_narrow:
+        extra["narrow"] = narrow_bench(args, torch, cyfa)
     prepared = forward_inputs(args, torch, w)
     if not args.no_decode:
         extra["decode"] = decode_bench(args, torch, cyfa)

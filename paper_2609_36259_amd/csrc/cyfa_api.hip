@@ -55,12 +55,14 @@ bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
 
 struct FwdPlan {
     bool mfma;
+    bool narrow;    // the 64-row matrix-core kernel (m <= 63)
     int chunk;
     int segments;
     size_t ws_bytes;
 };
 
-cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
+// layer: the layer forward (cyfa_forward_mixer), which runs the 128-row kernel
+cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan, bool layer = false) {
     if (!d) return fail(CYFA_ERR_INVALID_ARGUMENT, "desc is NULL");
     if (d->B < 1 || d->H < 1 || d->T < 0)
         return fail(CYFA_ERR_INVALID_ARGUMENT, "need B >= 1, H >= 1, T >= 0 (got B=%d T=%d H=%d)",
@@ -106,8 +108,18 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan) {
         use_mfma = mfma_ok;          // chunk 0, 32 or 64 with bf16 and d = 128 or 256
     }
     plan->mfma = use_mfma;
+    plan->narrow = use_mfma && !wide && !layer && cyfa::mfma_narrow_supported(probe);
     size_t ws = round_up(cyfa::readout_bytes(d->H, d->m));
-    if (use_mfma && wide) {
+    if (plan->narrow) {
+        // m <= 63 on 64 storage rows: chunk groups of a sequence, one workgroup each
+        probe.chunk = cyfa::mfma_default_chunk();
+        plan->chunk = probe.chunk;
+        plan->segments = d->segments ? d->segments : cyfa::mfma_narrow_auto_groups(probe);
+        const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
+        if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
+        if (plan->segments < 1) plan->segments = 1;
+        ws += round_up(cyfa::mfma_narrow_workspace_bytes(probe, plan->segments));
+    } else if (use_mfma && wide) {
         // chunk groups of a sequence, one workgroup each
         probe.chunk = cyfa::mfma_default_chunk();
         plan->chunk = probe.chunk;
@@ -283,7 +295,7 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
                          float *logits_out, void *workspace, size_t workspace_bytes, void *stream,
                          const cyfa::MixIn *mix = nullptr) {
     FwdPlan plan;
-    cyfa_status st = plan_forward(desc, &plan);
+    cyfa_status st = plan_forward(desc, &plan, mix != nullptr);
     if (st != CYFA_OK) return st;
     const bool has_tokens = desc->T > 0;
     if (has_tokens && (!q || !k || !v || (!delta && !mix) || !o))
@@ -320,7 +332,13 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
     char *ws = static_cast<char *>(workspace);
     float *M = reinterpret_cast<float *>(ws);
     hipError_t e;
-    if (plan.mfma && p.m > cyfa::kMaxActive) {
+    if (plan.narrow) {
+        // fp32 readout matrix first, then its 64 x 64 bf16 copies in the kernel's basis order
+        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
+        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
+        e = cyfa::launch_fwd_mfma_narrow(p, plan.segments, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s,
+                                         g_ev_start, g_ev_stop);
+    } else if (plan.mfma && p.m > cyfa::kMaxActive) {
         // fp32 readout matrix first, then its bf16 copies in the kernel's basis order
         e = cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s);
         if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
@@ -361,7 +379,7 @@ cyfa_status cyfa_forward_mixer_workspace_size(const cyfa_fwd_desc *desc, const c
     cyfa_fwd_desc d2 = *desc;
     d2.kernel = CYFA_KERNEL_MFMA;
     FwdPlan plan;
-    cyfa_status st = plan_forward(&d2, &plan);
+    cyfa_status st = plan_forward(&d2, &plan, true);
     if (st != CYFA_OK) return st;
     *bytes = plan.ws_bytes + mixer_qkv_bytes(desc, mw);
     return ok();
@@ -397,7 +415,7 @@ cyfa_status cyfa_forward_mixer(const cyfa_fwd_desc *desc, const cyfa_mixer_weigh
     cyfa_fwd_desc d2 = *desc;
     d2.kernel = CYFA_KERNEL_MFMA;
     FwdPlan plan;
-    cyfa_status st = plan_forward(&d2, &plan);
+    cyfa_status st = plan_forward(&d2, &plan, true);
     if (st != CYFA_OK) return st;
     const size_t need = plan.ws_bytes + mixer_qkv_bytes(desc, mw);
     if (!workspace || workspace_bytes < need)

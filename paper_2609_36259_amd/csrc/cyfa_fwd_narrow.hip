@@ -1,0 +1,918 @@
+// Matrix-core (bf16 MFMA) forward for slot counts m <= 63 on m* = 64 storage rows
+// (the smallest slot count of the paper's ablation), d_k = d_v = 128, 32-token
+// chunks, bf16 inputs with fp32 accumulation.
+//
+// The same chunk-wise forward as the 128-row fused kernel (App. B: clock and
+// log-decay prefix sums, temporal writes A (Eq. app-temporal-writes), key pass (Eq.
+// app-cyfa-key-chunk), token-wise softmax readout (Eq. cyfa-two-pass, middle line),
+// value pass (Eq. app-cyfa-value-chunk)) with the slot / basis space cut to 64
+// rows: the states are 64 x 128, the temporal writes, X, W and u are [32][64], the
+// readout matrix is 64 x 64, so the state products and the readout cost half (the
+// readout a quarter) of the 128-row kernel's.  Per chunk (token rows t, s; gamma_t
+// = exp(G_t), rho_s = exp(G_C - G_s), Gamma_ts = exp(G_t - G_s) for s <= t):
+//   p = gamma (.) Q Kbar^T + (Q K^T (.) Gamma) A            [32 x 64]
+//   X = U(lambda) p (scale folded into M);  W = softmax over the slots of M X
+//   u = U(-lambda) M^T W                                      [32 x 64]
+//   o = gamma (.) u Vbar + (u A^T (.) Gamma) V                [32 x 128]
+//   Kbar <- exp(G_C) Kbar + (rho (.) A)^T K,  Vbar likewise with V.
+//
+// Four waves, two workgroups per compute unit, each walking a chunk group of a
+// sequence with both 64 x 128 fp32 states in MFMA accumulators (32 registers of
+// each per lane):
+//   Kbar: wave w = (sb, ch) = (w % 2, w / 2) holds basis rows i = 32 sb + lane % 32
+//     and channels 64 ch .. 64 ch + 63 (two accumulators of the transposed product
+//     D[c][i]); the key pass's state term is formed per channel half and the
+//     ch = 1 waves hand theirs to the ch = 0 waves through LDS, which then run the
+//     rotation, the slot logits and the softmax for their 32 slots;
+//   Vbar: wave w holds channel block 32 w + lane % 32 over all 64 basis rows (two
+//     accumulators D[i][c]), so each wave forms the value output of its channel
+//     block with no reduction.
+// The bf16 readout matrix Mz = zs M (zs = scale log2 e) and its transpose sit in LDS
+// for the whole group.  Tiles are padded rows: [32][128] at 288 bytes, [32][64] and
+// [64][64] at 160 bytes (each row 8 banks after the previous one).
+//
+// Chunk groups, as the 256-row kernel: narrow_contrib_kernel forms each group's own
+// contribution to the absolute-clock states (zero entering state), its total log
+// decay and the clock entering it (a double-precision sum of every earlier
+// increment); the forward's workgroup for group g starts from (K0, V0) decayed
+// through groups 0 .. g-1 plus each earlier contribution decayed through the groups
+// after it (absolute-clock states need no rotation between groups).
+//
+// Internal basis order: pair j = 1 .. 31 at (2j-2, 2j-1), DC at 62, padding 63.  The
+// ABI's state arrays keep their [B][H][128][128] layout in the paper order (0 = DC,
+// 2j-1, 2j); this kernel reads rows 0 .. 63 of them and writes rows 64 .. 127 of the
+// final states as zeros (every row >= m of a state is zero).
+#include "cyfa_internal.h"
+#include "cyfa_mfma_common.h"
+#include "cyfa_rows.h"
+#include "cyfa_prep.h"
+
+#include <hip/hip_ext.h>
+
+namespace cyfa {
+
+using namespace mfma;
+
+namespace {
+
+constexpr int kC = 32;              // tokens per chunk
+constexpr int kNT = 256;            // four waves
+constexpr int kR = kNarrowRows;     // 64 storage rows
+constexpr int kDCn = kR - 2;        // internal index of DC
+constexpr int PS = 144, PSB = 288;  // [32][128] tiles
+constexpr int PN = 80, PNB = 160;   // [32][64] and [64][64] tiles
+constexpr int SSB = 40;             // [32][32] score tiles
+
+__device__ __forceinline__ int paper_row_n(int i) { return i < kDCn ? i + 1 : (i == kDCn ? 0 : kR - 1); }
+__device__ __forceinline__ bool row_active_n(int i, int m) { return i < m - 1 || i == kDCn; }
+__device__ __forceinline__ float uniform(float x) {
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+__device__ __forceinline__ float opqf(float x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+__device__ __forceinline__ const char *cbyte(const __bf16 *T) { return reinterpret_cast<const char *>(T); }
+__device__ __forceinline__ char *cbyte(__bf16 *T) { return reinterpret_cast<char *>(T); }
+
+// Lane offsets (bytes) into the padded tiles.
+struct Sw {
+    int st, tr;             // [32][128]: 8-byte pieces, transposed operand
+    int rown, stn, trn;     // [32][64]: row operand, 8-byte pieces, transposed operand
+    int cp;                 // 16-byte pieces of whole [32][128] rows: row tid/16 (+16), columns 8 (tid%16)
+};
+__device__ __forceinline__ Sw make_sw(int tid) {
+    const int lane = tid & 63, l32 = lane & 31, hl = lane >> 5;
+    Sw z;
+    z.st = l32 * PSB + 8 * hl;
+    z.tr = 2 * tr_off(PS, lane);
+    z.rown = l32 * PNB + 16 * hl;
+    z.stn = l32 * PNB + 8 * hl;
+    z.trn = 2 * tr_off(PN, lane);
+    z.cp = (tid >> 4) * PSB + (tid & 15) * 16;
+    return z;
+}
+// Row operand of a [32][64] tile: element [lane%32][16 ks + 8 (lane/32) + p].
+__device__ __forceinline__ bf16x8 srow_n(const __bf16 *T, int ks, const Sw &z) {
+    return *reinterpret_cast<const bf16x8 *>(cbyte(T) + z.rown + 32 * ks);
+}
+// Row operand in the permuted k order of a fed-back accumulator (columns 16 ks +
+// 4 (lane/32) .. +3 and 16 ks + 8 + 4 (lane/32) .. +3 of row lane%32).
+__device__ __forceinline__ bf16x8 perm8(const char *p) {
+    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(p);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(p + 16);
+    bf16x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+}
+__device__ __forceinline__ bf16x8 sperm(const __bf16 *T, int ks, const Sw &z) { return perm8(cbyte(T) + z.st + 32 * ks); }
+__device__ __forceinline__ bf16x8 sperm_n(const __bf16 *T, int ks, const Sw &z) {
+    return perm8(cbyte(T) + z.stn + 32 * ks);
+}
+// Transposed operands: element [k0 + 8 (lane/32) + p][n0 + lane % 32].
+__device__ __forceinline__ bf16x8 stro(const __bf16 *T, int k0, int n0, const Sw &z) {
+    return lds8_tr(reinterpret_cast<const __bf16 *>(cbyte(T) + z.tr) + k0 * PS + n0, PS);
+}
+__device__ __forceinline__ bf16x8 stro_n(const __bf16 *T, int k0, int n0, const Sw &z) {
+    return lds8_tr(reinterpret_cast<const __bf16 *>(cbyte(T) + z.trn) + k0 * PN + n0, PN);
+}
+// Row operand of a [64][64] LDS matrix: element [r0 + lane%32][16 ks + 8 (lane/32) + p].
+__device__ __forceinline__ bf16x8 mrow(const __bf16 *M, int r0, int ks, int lane) {
+    return lds8(M + (r0 + (lane & 31)) * PN + 16 * ks + 8 * (lane >> 5));
+}
+// A 32 x 32 output block D[mr][n] (lane: n = lane % 32; register v: mr = 8 (v / 4) +
+// 4 (lane / 32) + v % 4) stored as bf16 at row n, columns col0 + mr.
+__device__ __forceinline__ void store_block(__bf16 *T, int col0, const f32x16 &acc, const Sw &z) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[4 * g4 + e];
+        *reinterpret_cast<bf16x4 *>(cbyte(T) + z.st + 2 * (col0 + 8 * g4)) = o;
+    }
+}
+__device__ __forceinline__ void store_block_n(__bf16 *T, int col0, const f32x16 &acc, const Sw &z) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[4 * g4 + e];
+        *reinterpret_cast<bf16x4 *>(cbyte(T) + z.stn + 2 * (col0 + 8 * g4)) = o;
+    }
+}
+// Row operand of a score tile: element [row][k0 + 8 (lane/32) + p].
+__device__ __forceinline__ bf16x8 rd_row(const __bf16 *S, int row, int k0, int hl) {
+    return lds8(S + row * SSB + k0 + 8 * hl);
+}
+// The operand's k indices k0 + 8 (lane/32) + p scaled by f[p].
+__device__ __forceinline__ bf16x8 scale_k(bf16x8 v, const float *f) {
+    const float4 a = *reinterpret_cast<const float4 *>(f);
+    const float4 b = *reinterpret_cast<const float4 *>(f + 4);
+    const float d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    bf16x8 r;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = (__bf16)((float)v[q] * d[q]);
+    return r;
+}
+template <int N>
+__device__ __forceinline__ void scale_acc(f32x16 (&acc)[N], float f) {
+#pragma unroll
+    for (int x = 0; x < N; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[x][v] *= f;
+}
+
+// ---- chunk staging (two 16-byte pieces of each [32][128] tile per thread) ------
+// (The lane's offsets are recomputed at every call, opaque to the compiler, so that
+// no 64-bit address is kept, and spilled, across the chunk loop.)
+__device__ __forceinline__ void load_rows2(const __bf16 *base, size_t row_stride, int n, int tid, uint4 (&o)[2]) {
+    tid = opq(tid);
+    const int r = tid >> 4, c8 = (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int rr = r + 16 * it;
+        const uint4 v = *reinterpret_cast<const uint4 *>(base + (size_t)min(rr, max(n - 1, 0)) * row_stride + c8);
+        o[it] = rr < n ? v : make_uint4(0, 0, 0, 0);
+    }
+}
+__device__ __forceinline__ void store_rows2(__bf16 *T, const uint4 (&o)[2], const Sw &z) {
+    *reinterpret_cast<uint4 *>(cbyte(T) + z.cp) = o[0];
+    *reinterpret_cast<uint4 *>(cbyte(T) + z.cp + 16 * PSB) = o[1];
+}
+__device__ __forceinline__ void copy_rows2_out(const __bf16 *T, __bf16 *dst, size_t row_stride, int nrows, int tid,
+                                               const Sw &z) {
+    const int r = tid >> 4, c8 = (tid & 15) * 8;
+#pragma unroll
+    for (int it = 0; it < 2; ++it)
+        if (r + 16 * it < nrows)
+            *reinterpret_cast<uint4 *>(dst + (size_t)(r + 16 * it) * row_stride + c8) =
+                *reinterpret_cast<const uint4 *>(cbyte(T) + z.cp + 16 * PSB * it);
+}
+
+// Per-token scalars of a chunk (lanes 0..31 of wave 0; zero past the sequence: no
+// shift, no decay, no write).
+struct Tok {
+    float g, dl, be;
+};
+__device__ __forceinline__ void load_tok(const FwdParams &p, size_t row0, int h, int t0, int Tb, int tid, Tok &k) {
+    k.g = 0.f;
+    k.dl = 0.f;
+    k.be = 0.f;
+    const int t = t0 + tid;
+    if (tid < kC && t < Tb) {
+        const size_t si = (row0 + t) * p.H + h;
+        k.g = p.log_alpha ? p.log_alpha[si] : 0.f;
+        k.dl = p.delta[si];
+        k.be = p.beta ? p.beta[si] : 1.f;
+    }
+}
+
+// Chunk scalars in LDS.
+struct Sc {
+    float G[kC];      // chunk-local inclusive sums of log alpha
+    float gam[kC];    // exp(G_t) (times the carried states' scale)
+    float rho[kC];    // exp(G_C - G_s) (likewise)
+    float urev[kC];   // clock after token t over m, mod 1 (revolutions)
+    float4 bw[kC];    // write-builder record: amplitude, urev, cos and sin of 2 pi urev
+    float ea[kC];     // exp(G_t) and exp(-G_t): Gamma_ts = ea_t eb_s when every |G_t| <= 60
+    float eb[kC];
+    float ctl[4];     // [0] factor on the carried states before the chunk, [1] before their
+                      // update, [2] 1 while lazily scaled, [3] 1 when Gamma factors into ea, eb
+};
+
+// Wave 0: prefix sums of the chunk and the builder records; carry is the clock
+// entering the chunk (reduced), advanced past it.  The carried states are held as
+// exp(Ls) times the registers: a chunk's decay moves Ls (gam_t = exp(G_t + Ls) scales
+// the inter-chunk terms, rho_s = exp(-Ls - G_s) the update operand, then Ls += G_C)
+// instead of rescaling every accumulator; when an exponent could leave [-60, 60] the
+// chunk is eager (registers times exp(Ls) first, Ls restarts at 0, plain gam and rho,
+// registers times exp(G_C) before the update).
+__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, float Ls) {
+    lane = opq(lane);
+    const double inv_m = 1.0 / (double)m;
+    const float G = wave_incl_scan(k.g);
+    const double lam = carry + wave_incl_scan((double)k.dl);
+    const float GC = lane63(G);
+    const float gabs = wave_max_nonneg(fabsf(G));
+    const bool lazy = fabsf(Ls) + gabs <= 60.f;
+    if (lane < kC) {
+        s.G[lane] = G;
+        s.ea[lane] = __expf(G);
+        s.eb[lane] = __expf(-G);
+        s.gam[lane] = lazy ? __expf(G + Ls) : __expf(G);
+        s.rho[lane] = lazy ? __expf(-Ls - G) : __expf(GC - G);
+        const double q = lam * inv_m;
+        const float u = (float)(q - floor(q));
+        s.urev[lane] = u;
+        float s1, c1;
+        sincos_rev(u, &s1, &c1);
+        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m), u, c1, s1);
+    }
+    if (lane == 0) {
+        s.ctl[0] = lazy ? 1.f : __expf(Ls);
+        s.ctl[1] = lazy ? 1.f : __expf(GC);
+        s.ctl[2] = lazy ? 1.f : 0.f;
+        s.ctl[3] = gabs <= 60.f ? 1.f : 0.f;
+    }
+    carry = reduce_clock(lane63(lam), (double)m, inv_m);
+}
+__device__ __forceinline__ float next_scale(const Sc &s, float Ls) {
+    return s.ctl[2] != 0.f ? Ls + s.G[kC - 1] : 0.f;
+}
+
+// Temporal write rows (Eq. app-temporal-writes) into a [32][64] tile: amp_t [cos
+// th_j, -sin th_j] on pair j (internal columns 2j-2, 2j-1), amp_t / sqrt 2 = beta_t /
+// sqrt m on DC (62), 0 on 63.  Thread (row tid/8, q = tid % 8) fills columns 8q ..
+// 8q+7 (pairs 4q+1 .. 4q+4); the phases advance by angle addition from a start
+// reduced in revolutions.
+__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) {
+    const int q = tid & 7, r = tid >> 3;
+    const int J = (m - 1) >> 1;
+    const float4 rec = s.bw[r];
+    const float amp = rec.x, u = rec.y, c1 = rec.z, s1 = rec.w;
+    float sn, cs;
+    sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
+    bf16x8 a8;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        const int j = 4 * q + 1 + jj;
+        const bool live = j <= J;
+        float a0 = live ? amp * cs : 0.f, a1 = live ? -amp * sn : 0.f;
+        if (jj == 3 && q == 7) {
+            a0 = amp * 0.70710678118654752f;
+            a1 = 0.f;
+        }
+        a8[2 * jj] = (__bf16)a0;
+        a8[2 * jj + 1] = (__bf16)a1;
+        if (jj < 3) {
+            const float nc = cs * c1 - sn * s1;
+            const float ns = sn * c1 + cs * s1;
+            cs = nc;
+            sn = ns;
+        }
+    }
+    *reinterpret_cast<bf16x8 *>(cbyte(T) + r * PNB + 16 * q) = a8;
+}
+
+// (cos, sin) of 2 pi j urev for the eight pairs of a lane's 16 rows in basis block sb:
+// pair e (registers 2e, 2e+1) has frequency j = 16 sb + 4(e/2) + 2hl + e%2 + 1.  DC,
+// padding and inactive pairs get (1, 0).
+__device__ __forceinline__ void lane_phases(float u, int sb, int hl, int m, float (&c)[8], float (&s)[8]) {
+    const int J = (m - 1) >> 1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int j = 16 * sb + 4 * (e >> 1) + 2 * hl + (e & 1) + 1;
+        c[e] = 1.f;
+        s[e] = 0.f;
+        if (j <= J) sincos_rev(__builtin_amdgcn_fractf((float)j * u), &s[e], &c[e]);
+    }
+}
+// acc <- mul U(SIGN lambda) acc on a lane's pairs; DC and padding are multiplied by mul.
+template <int SIGN>
+__device__ __forceinline__ void rotate(f32x16 &a, const float (&c)[8], const float (&s)[8], float mul) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float x0 = a[2 * e], x1 = a[2 * e + 1];
+        const float sn = SIGN > 0 ? s[e] : -s[e];
+        a[2 * e] = mul * (c[e] * x0 - sn * x1);
+        a[2 * e + 1] = mul * (sn * x0 + c[e] * x1);
+    }
+}
+
+// One 16 x 16 block of a causal 32 x 32 score tile into S (bf16, [32][SSB]):
+// S[nr][mr] = Gamma_{nr, mr} sum_k Am[mr][k] Bn[nr][k] for mr in m0 .., nr in n0 ..
+// (mr <= nr), over KS k-steps of 32 columns of tiles with row stride STR
+// (v_mfma_f32_16x16x32: lane nr = n0 + lane % 16, registers mr = m0 + 4 (lane / 16) + q).
+template <int KS, int STR>
+__device__ __forceinline__ void score_block(const __bf16 *Am, int m0, const __bf16 *Bn, int n0, __bf16 *S,
+                                            const Sc &sc, int lane) {
+    const int l16 = lane & 15, g = lane >> 4;
+    const int nr = n0 + l16, mb = m0 + 4 * g;
+    bf16x4 o = bf16x4{};
+    if (m0 <= n0) {
+        f32x4 acc = zero_acc4();
+        const __bf16 *ap = Am + (m0 + l16) * STR + 8 * g;
+        const __bf16 *bp = Bn + nr * STR + 8 * g;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc = mma16(lds8(ap + 32 * ks), lds8(bp + 32 * ks), acc);
+        const bool fac = uniform(sc.ctl[3]) != 0.f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int mr = mb + q;
+            const float gm = fac ? sc.ea[nr] * sc.eb[mr] : __expf(sc.G[nr] - sc.G[mr]);
+            o[q] = (__bf16)(mr <= nr ? acc[q] * gm : 0.f);
+        }
+    }
+    *reinterpret_cast<bf16x4 *>(S + nr * SSB + mb) = o;
+}
+
+// ---- state in / out (ABI layout [B][H][128][128], paper row order) ------------
+// Key state (kacc[x]: basis row i = 32 sb + lane % 32, channel c = 64 ch + 32 x + 8 (v/4)
+// + 4 (lane/32) + v%4).
+__device__ __forceinline__ void add_key_state(f32x16 (&acc)[2], const float *S, float f, int sb, int ch, int lane,
+                                              int m) {
+    const int i = 32 * sb + (lane & 31);
+    if (!row_active_n(i, m)) return;
+    const float *row = S + (size_t)paper_row_n(i) * 128 + 64 * ch + 4 * (lane >> 5);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+            const float4 q = *reinterpret_cast<const float4 *>(row + 32 * x + 8 * v4);
+            acc[x][4 * v4] = fmaf(f, q.x, acc[x][4 * v4]);
+            acc[x][4 * v4 + 1] = fmaf(f, q.y, acc[x][4 * v4 + 1]);
+            acc[x][4 * v4 + 2] = fmaf(f, q.z, acc[x][4 * v4 + 2]);
+            acc[x][4 * v4 + 3] = fmaf(f, q.w, acc[x][4 * v4 + 3]);
+        }
+}
+__device__ __forceinline__ void store_key_state(float *S, const f32x16 (&acc)[2], float f, int sb, int ch, int lane,
+                                                int m) {
+    const int i = 32 * sb + (lane & 31);
+    const bool live = row_active_n(i, m);
+    float *row = S + (size_t)paper_row_n(i) * 128 + 64 * ch + 4 * (lane >> 5);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4)
+            *reinterpret_cast<float4 *>(row + 32 * x + 8 * v4) =
+                live ? make_float4(f * acc[x][4 * v4], f * acc[x][4 * v4 + 1], f * acc[x][4 * v4 + 2],
+                                   f * acc[x][4 * v4 + 3])
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+// Value state (vacc[j]: basis row i = 32 j + 8 (v/4) + 4 (lane/32) + v%4, channel c =
+// 32 w + lane % 32).
+__device__ __forceinline__ int value_row(int j, int v, int hl) { return 32 * j + 8 * (v >> 2) + 4 * hl + (v & 3); }
+__device__ __forceinline__ void add_value_state(f32x16 (&acc)[2], const float *S, float f, int w, int lane, int m) {
+    const int c = 32 * w + (lane & 31), hl = lane >> 5;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int i = value_row(j, v, hl);
+            if (row_active_n(i, m)) acc[j][v] = fmaf(f, S[(size_t)paper_row_n(i) * 128 + c], acc[j][v]);
+        }
+}
+__device__ __forceinline__ void store_value_state(float *S, const f32x16 (&acc)[2], float f, int w, int lane, int m) {
+    const int c = 32 * w + (lane & 31), hl = lane >> 5;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int i = value_row(j, v, hl);
+            S[(size_t)paper_row_n(i) * 128 + c] = row_active_n(i, m) ? f * acc[j][v] : 0.f;
+        }
+}
+// Rows 64 .. 127 of a final state (never active at m <= 63) are zero.
+__device__ __forceinline__ void zero_upper_rows(float *S, int tid) {
+#pragma unroll
+    for (int it = 0; it < 8; ++it)
+        *reinterpret_cast<float4 *>(S + kR * 128 + 4 * (it * kNT + tid)) = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// ---- chunk-group contributions (fp32, lane-major: wave w, accumulator x, lane, register)
+constexpr int kStateN = kR * 128;                   // floats of one 64 x 128 state
+__device__ __forceinline__ int dump_n(int w, int x, int lane) { return ((w * 2 + x) * 64 + lane) * 16; }
+__device__ __forceinline__ void store_dump(float *E, const f32x16 (&acc)[2], float f, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<float4 *>(E + dump_n(w, x, lane) + 4 * q) =
+                make_float4(f * acc[x][4 * q], f * acc[x][4 * q + 1], f * acc[x][4 * q + 2], f * acc[x][4 * q + 3]);
+}
+__device__ __forceinline__ void add_dump(f32x16 (&acc)[2], const float *E, float f, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 e = *reinterpret_cast<const float4 *>(E + dump_n(w, x, lane) + 4 * q);
+            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
+            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
+            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
+            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+        }
+}
+
+struct NarrowArgs {
+    FwdParams p;
+    const __bf16 *Mz, *MzT;  // [H][64][64] readout matrix times scale log2 e, and its transpose
+    int groups, cpg;         // chunk groups per sequence, chunks per group
+    float *Ef;               // [BH][groups][2][kStateN] each group's own contribution (K, V)
+    float *Gg;               // [BH][groups] total log decay of each group
+    double *gclk;            // [BH][groups] clock entering each group (reduced mod m)
+    float *S0;               // [BH][2][64 x 128] rows 0 .. 63 of (K0, V0) (groups > 1: the states
+                             // may be overwritten in place by the last group)
+};
+
+// Sum over tokens [t_lo, t_hi) of x[t * stride] in double over the workgroup (eight
+// loads in flight per thread); every thread gets the sum.  red: 4 doubles of LDS.
+__device__ __forceinline__ double block_token_sum(const float *x, int stride, int t_lo, int t_hi, double *red,
+                                                  int tid) {
+    double ds = 0.0;
+    for (int t0 = t_lo; t0 < t_hi; t0 += 8 * kNT) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = t0 + u * kNT + tid;
+            v[u] = t < t_hi ? x[(size_t)t * stride] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ds += (double)v[u];
+    }
+    for (int o = 32; o > 0; o >>= 1) ds += __shfl_xor(ds, o);
+    if ((tid & 63) == 0) red[tid >> 6] = ds;
+    __syncthreads();
+    double tot = 0.0;
+#pragma unroll
+    for (int i = 0; i < kNT / 64; ++i) tot += red[i];
+    __syncthreads();
+    return tot;
+}
+
+// ---- LDS map (bytes) ------------------------------------------------------------
+struct Lay {
+    static constexpr int T1 = kC * PSB;            // [32][128] tile
+    static constexpr int TN = kC * PNB;            // [32][64] tile
+    static constexpr int TM = kR * PNB;            // [64][64] matrix
+    static constexpr int TS = kC * SSB * 2;        // score tile
+    static constexpr int PART = 2 * 64 * 16 * 4;   // the ch = 1 waves' key-pass partials
+    static constexpr int Q = 0;                    // Q, then the output tile
+    static constexpr int K = Q + T1;
+    static constexpr int V = K + T1;
+    static constexpr int A = V + T1;               // temporal writes
+    static constexpr int X = A + TN;               // X, then u
+    static constexpr int W = X + TN;               // key-pass partials, then W
+    static constexpr int S1 = W + PART;            // Gamma (.) Q K^T
+    static constexpr int S2 = S1 + TS;             // Gamma (.) u A^T
+    static constexpr int MT = S2 + TS;             // Mz [slot][basis]
+    static constexpr int MTT = MT + TM;            // MzT [basis][slot]
+    static constexpr int RED = MTT + TM;           // softmax partials [2 slot blocks][32 tokens] float2
+    static constexpr int SC = RED + 2 * kC * 8;
+    static constexpr int BYTES = SC + (int)sizeof(Sc);
+    static_assert(TN <= PART, "W fits the partials' place");
+    static_assert(BYTES <= 80 * 1024, "two workgroups per compute unit");
+};
+
+__global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
+    using L = Lay;
+    __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
+    const FwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
+    const int sb = w & 1, ch = w >> 1;             // key-state basis block and channel half
+    const int m = p.m;
+    const int Tb = seq_tokens(p, b);
+    const size_t row0 = seq_row0(p, b);
+    // this group's chunks, up to the sequence's last one
+    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
+    Sc &sc = *lds_at<Sc>(smem, L::SC);
+    __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
+    __bf16 *At = lds_at<__bf16>(smem, L::A), *Xt = lds_at<__bf16>(smem, L::X), *Wt = lds_at<__bf16>(smem, L::W);
+    __bf16 *S1 = lds_at<__bf16>(smem, L::S1), *S2 = lds_at<__bf16>(smem, L::S2);
+    __bf16 *Mt = lds_at<__bf16>(smem, L::MT), *MTt = lds_at<__bf16>(smem, L::MTT);
+    float2 *red = lds_at<float2>(smem, L::RED);
+    float *part = lds_at<float>(smem, L::W);
+    const Sw z = make_sw(tid);
+    const float zs = p.scale * 1.4426950408889634f;     // Mz = zs M: logits in log2 units
+    const float inv_zs = 1.f / zs;
+
+    // the readout matrix and its transpose, resident for the group (two 16-byte
+    // pieces of each per thread)
+    {
+        const __bf16 *Mg = a.Mz + (size_t)h * kR * kR, *MTg = a.MzT + (size_t)h * kR * kR;
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int e = it * kNT + tid, r = e >> 3, c8 = (e & 7) * 8;
+            *reinterpret_cast<uint4 *>(Mt + r * PN + c8) = *reinterpret_cast<const uint4 *>(Mg + r * kR + c8);
+            *reinterpret_cast<uint4 *>(MTt + r * PN + c8) = *reinterpret_cast<const uint4 *>(MTg + r * kR + c8);
+        }
+    }
+
+    f32x16 kacc[2], vacc[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
+    }
+    const size_t sbase = (size_t)bh * kStoreRows * 128;   // (b, h) in the ABI state arrays
+    double carry;
+    if (a.groups == 1) {
+        if (p.K0) add_key_state(kacc, p.K0 + sbase, 1.f, sb, ch, lane, m);
+        if (p.V0) add_value_state(vacc, p.V0 + sbase, 1.f, w, lane, m);
+        carry = reduce_clock(p.clock0 ? p.clock0[bh] : 0.0, (double)m, 1.0 / (double)m);
+    } else {
+        // state entering the group: each earlier group's contribution decayed through
+        // the groups after it, plus (K0, V0) decayed through all earlier groups
+        const float *Gg = a.Gg + (size_t)bh * a.groups;
+        float tail = 0.f;                         // log decay of groups q+1 .. g-1
+        for (int q = g - 1; q >= 0; --q) {
+            const float f = __expf(tail);
+            const float *E = a.Ef + ((size_t)bh * a.groups + q) * 2 * kStateN;
+            add_dump(kacc, E, f, w, lane);
+            add_dump(vacc, E + kStateN, f, w, lane);
+            tail += Gg[q];
+        }
+        const float *S0 = a.S0 + (size_t)bh * 2 * kStateN;
+        if (p.K0) add_key_state(kacc, S0, __expf(tail), sb, ch, lane, m);
+        if (p.V0) add_value_state(vacc, S0 + kStateN, __expf(tail), w, lane, m);
+        carry = a.gclk[(size_t)bh * a.groups + g];
+    }
+
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *qin = static_cast<const __bf16 *>(p.q), *kin = static_cast<const __bf16 *>(p.k);
+    const __bf16 *vin = static_cast<const __bf16 *>(p.v);
+    __bf16 *o = static_cast<__bf16 *>(p.o);
+    uint4 rq[2], rk[2], rv[2];
+    Tok tk;
+    auto prefetch = [&](int c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = ((row0 + t0) * p.H + h) * 128;
+        load_rows2(qin + base, rs, n, tid, rq);
+        load_rows2(kin + base, rs, n, tid, rk);
+        load_rows2(vin + base, rs, n, tid, rv);
+        load_tok(p, row0, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_begin);
+    float Ls = 0.f;                                   // carried states: exp(Ls) x registers
+    for (int c = c_begin; c < c_end; ++c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        // -- stage the chunk and its scalars
+        store_rows2(Qt, rq, z);
+        store_rows2(Kt, rk, z);
+        store_rows2(Vt, rv, z);
+        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
+        if (c + 1 < c_end) prefetch(c + 1);
+        lds_barrier();
+        {
+            const float pre = uniform(sc.ctl[0]);
+            if (pre != 1.f) {
+                scale_acc(kacc, pre);
+                scale_acc(vacc, pre);
+            }
+        }
+        build_A(sc, At, tid, m);
+        score_block<4, PS>(Kt, 16 * (w & 1), Qt, 16 * (w >> 1), S1, sc, lane);   // S1[t][s]
+        // -- key pass: p = gamma (.) Q Kbar^T + S1 A (D[basis][t]) over this wave's channel
+        //    half; then its part of the key state update
+        const float gr = sc.gam[l32];
+        f32x16 pacc = zero_acc();
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            pacc = mma(acc_to_operand(kacc[ks >> 1], ks & 1), sperm(Qt, 4 * ch + ks, z), pacc);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) pacc[v] *= gr;
+        lds_barrier();
+        const float post = uniform(sc.ctl[1]);
+        if (post != 1.f) scale_acc(kacc, post);
+        // the intra-chunk term's two k-steps split over the channel halves
+        pacc = mma(stro_n(At, 16 * ch, 32 * sb, z), rd_row(S1, l32, 16 * ch, hl), pacc);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 ad = scale_k(stro_n(At, 16 * ks, 32 * sb, z), sc.rho + 16 * ks + 8 * hl);
+#pragma unroll
+            for (int x = 0; x < 2; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 64 * ch + 32 * x, z), ad, kacc[x]);
+        }
+        if (ch == 1) {
+            float *dst = part + (sb * 64 + lane) * 16;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<float4 *>(dst + 4 * q) =
+                    make_float4(pacc[4 * q], pacc[4 * q + 1], pacc[4 * q + 2], pacc[4 * q + 3]);
+        }
+        lds_barrier();
+        // -- X = U(lambda) p (the scale is folded into Mz); the padding column carries 1
+        if (ch == 0) {
+            const float *src = part + (sb * 64 + lane) * 16;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 e = *reinterpret_cast<const float4 *>(src + 4 * q);
+                pacc[4 * q] += e.x;
+                pacc[4 * q + 1] += e.y;
+                pacc[4 * q + 2] += e.z;
+                pacc[4 * q + 3] += e.w;
+            }
+            float pc[8], ps[8];
+            lane_phases(opqf(sc.urev[l32]), sb, hl, m, pc, ps);
+            rotate<1>(pacc, pc, ps, 1.f);
+            if (sb == 1 && hl == 1) pacc[15] = 1.f;
+            store_block_n(Xt, 32 * sb, pacc, z);
+        }
+        lds_barrier();
+        // -- slot logits of the 32 slots of block sb (log2 units; inactive slots about -1e30)
+        f32x16 wr = zero_acc();
+        float mx = 0.f;
+        if (ch == 0) {
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) wr = mma(mrow(Mt, 32 * sb, ks, lane), srow_n(Xt, ks, z), wr);
+            if (p.logits && l32 < n) {
+                float *lg = p.logits + ((row0 + t0 + l32) * p.H + h) * m;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int slot = 32 * sb + 8 * (v >> 2) + 4 * hl + (v & 3);
+                    if (slot < m) lg[slot] = wr[v] * 0.69314718055994531f;
+                }
+            }
+            mx = wr[0];
+#pragma unroll
+            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, wr[v]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+#pragma unroll
+            for (int v = 0; v < 16; ++v) wr[v] = __builtin_amdgcn_exp2f(wr[v] - mx);
+            float sm = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sm += wr[v];
+            sm += __shfl_xor(sm, 32);
+            if (hl == 0) red[sb * kC + l32] = make_float2(mx, sm);
+        }
+        lds_barrier();
+        if (ch == 0) {
+            const float2 r0 = red[l32], r1 = red[kC + l32];
+            const float M = fmaxf(r0.x, r1.x);
+            const float Lsum = r0.y * __builtin_amdgcn_exp2f(r0.x - M) + r1.y * __builtin_amdgcn_exp2f(r1.x - M);
+            const float f = __builtin_amdgcn_exp2f(mx - M) / Lsum;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) wr[v] *= f;
+            store_block_n(Wt, 32 * sb, wr, z);
+        }
+        lds_barrier();
+        // -- u = U(-lambda) M^T W of basis block sb, in X's place
+        if (ch == 0) {
+            f32x16 ya = zero_acc();
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) ya = mma(mrow(MTt, 32 * sb, ks, lane), srow_n(Wt, ks, z), ya);
+            float pc[8], ps[8];
+            lane_phases(opqf(sc.urev[l32]), sb, hl, m, pc, ps);
+            rotate<-1>(ya, pc, ps, inv_zs);
+            store_block_n(Xt, 32 * sb, ya, z);
+        }
+        lds_barrier();
+        // -- value pass: o = gamma (.) u Vbar + S2 V, this wave's channel block (D[c][t]);
+        //    then the value state update
+        score_block<2, PN>(At, 16 * (w & 1), Xt, 16 * (w >> 1), S2, sc, lane);   // S2[t][s]
+        f32x16 oacc = zero_acc();
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) oacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), sperm_n(Xt, ks, z), oacc);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[v] *= gr;
+        if (post != 1.f) scale_acc(vacc, post);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 vb = stro(Vt, 16 * ks, 32 * w, z);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                vacc[j] = mma(scale_k(stro_n(At, 16 * ks, 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb, vacc[j]);
+        }
+        lds_barrier();
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) oacc = mma(stro(Vt, 16 * ks, 32 * w, z), rd_row(S2, l32, 16 * ks, hl), oacc);
+        store_block(Qt, 32 * w, oacc, z);              // o[t][c], in Q's place
+        Ls = next_scale(sc, Ls);
+        lds_barrier();
+        copy_rows2_out(Qt, o + ((row0 + t0) * p.H + h) * 128, rs, n, tid, z);
+        lds_barrier();
+    }
+    // the last group ends with the final states (chunks past a sequence change nothing)
+    if (g == a.groups - 1) {
+        const float f = __expf(Ls);
+        if (p.K_out) {
+            store_key_state(p.K_out + sbase, kacc, f, sb, ch, lane, m);
+            zero_upper_rows(p.K_out + sbase, tid);
+        }
+        if (p.V_out) {
+            store_value_state(p.V_out + sbase, vacc, f, w, lane, m);
+            zero_upper_rows(p.V_out + sbase, tid);
+        }
+        if (p.clock_out && tid == 0) p.clock_out[bh] = carry;
+    }
+}
+
+// Each chunk group's own contribution (groups > 1; launched before the forward).
+// The last group's contribution is never read, so its workgroup copies rows 0 .. 63
+// of (K0, V0) for the forward's prologues instead and forms only its total log decay.
+__global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
+    using L = Lay;
+    __shared__ __attribute__((aligned(256))) char smem[L::V + L::T1];   // K and V tiles
+    __shared__ __attribute__((aligned(256))) __bf16 Asm[kC * PN];
+    __shared__ Sc sc;
+    __shared__ double red[kNT / 64];
+    const FwdParams &p = a.p;
+    const int bh = blockIdx.x, g = blockIdx.y, h = bh % p.H, b = bh / p.H;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int sb = w & 1, ch = w >> 1;
+    const int m = p.m;
+    const int Tb = seq_tokens(p, b);
+    const size_t row0 = seq_row0(p, b);
+    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
+    const size_t tok0 = row0 * p.H + h;
+    const size_t pi = (size_t)bh * a.groups + g;
+    // clock entering the group: clock0 plus every increment before it (double)
+    double carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
+                                    block_token_sum(p.delta + tok0, p.H, 0, min(c_begin * kC, Tb), red, tid),
+                                (double)m, 1.0 / (double)m);
+    if (tid == 0) a.gclk[pi] = carry;
+    if (g == a.groups - 1) {
+        const double gs = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, min(c_begin * kC, Tb),
+                                                        min(c_end * kC, Tb), red, tid)
+                                      : 0.0;
+        if (tid == 0) a.Gg[pi] = (float)gs;
+        float *S0 = a.S0 + (size_t)bh * 2 * kStateN;
+        const size_t sbase = (size_t)bh * kStoreRows * 128;
+        for (int e = 4 * tid; e < kStateN; e += 4 * kNT) {
+            if (p.K0) *reinterpret_cast<float4 *>(S0 + e) = *reinterpret_cast<const float4 *>(p.K0 + sbase + e);
+            if (p.V0)
+                *reinterpret_cast<float4 *>(S0 + kStateN + e) = *reinterpret_cast<const float4 *>(p.V0 + sbase + e);
+        }
+        return;
+    }
+    __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
+    const Sw z = make_sw(tid);
+    f32x16 kacc[2], vacc[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        kacc[x] = zero_acc();
+        vacc[x] = zero_acc();
+    }
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
+    uint4 rk[2], rv[2];
+    Tok tk;
+    auto prefetch = [&](int c) {
+        const int t0 = c * kC, n = min(kC, Tb - t0);
+        const size_t base = ((row0 + t0) * p.H + h) * 128;
+        load_rows2(kin + base, rs, n, tid, rk);
+        load_rows2(vin + base, rs, n, tid, rv);
+        load_tok(p, row0, h, t0, Tb, tid, tk);
+    };
+    if (c_begin < c_end) prefetch(c_begin);
+    double gsum = 0.0;
+    float Ls = 0.f;
+    for (int c = c_begin; c < c_end; ++c) {
+        store_rows2(Kt, rk, z);
+        store_rows2(Vt, rv, z);
+        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
+        if (c + 1 < c_end) prefetch(c + 1);
+        lds_barrier();
+        build_A(sc, Asm, tid, m);
+        gsum += (double)sc.G[kC - 1];
+        {
+            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
+            if (f != 1.f) {
+                scale_acc(kacc, f);
+                scale_acc(vacc, f);
+            }
+        }
+        Ls = next_scale(sc, Ls);
+        lds_barrier();
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 ad = scale_k(stro_n(Asm, 16 * ks, 32 * sb, z), sc.rho + 16 * ks + 8 * hl);
+#pragma unroll
+            for (int x = 0; x < 2; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 64 * ch + 32 * x, z), ad, kacc[x]);
+            const bf16x8 vb = stro(Vt, 16 * ks, 32 * w, z);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                vacc[j] = mma(scale_k(stro_n(Asm, 16 * ks, 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb, vacc[j]);
+        }
+        lds_barrier();
+    }
+    const float f = __expf(Ls);
+    float *E = a.Ef + pi * 2 * kStateN;
+    store_dump(E, kacc, f, w, lane);
+    store_dump(E + kStateN, vacc, f, w, lane);
+    if (tid == 0) a.Gg[pi] = (float)gsum;
+}
+
+// bf16 readout matrix for the kernels above from the fp32 one (paper basis order,
+// [H][128][128], zero outside the active m x m block): Mz[i][j_int] = zs M[i][paper(j_int)]
+// for slots i < 64, with kMaskLogit in the padding column of inactive slots (i >= m), and
+// its transpose MzT[j_int][i].
+__global__ __launch_bounds__(kR) void narrow_mz_kernel(int m, const float *__restrict__ M, __bf16 *__restrict__ Mz,
+                                                       __bf16 *__restrict__ MzT, float zs) {
+    const int h = blockIdx.x, i = blockIdx.y, jint = threadIdx.x;
+    const int jp = jint < kDCn ? jint + 1 : (jint == kDCn ? 0 : -1);
+    float val = jp >= 0 ? zs * M[((size_t)h * kStoreRows + i) * kStoreRows + jp] : 0.f;
+    if (jint == kR - 1 && i >= m) val = kMaskLogit;
+    const __bf16 bv = (__bf16)val;
+    Mz[((size_t)h * kR + i) * kR + jint] = bv;
+    MzT[((size_t)h * kR + jint) * kR + i] = bv;
+}
+
+}  // namespace
+
+bool mfma_narrow_supported(const FwdParams &p) {
+    return p.dtype == 1 && p.dk == 128 && p.dv == 128 && p.m <= kMaxActiveNarrow &&
+           (p.chunk == 32 || p.chunk == 64);
+}
+
+int mfma_narrow_auto_groups(const FwdParams &p) {
+    // two four-wave workgroups per compute unit: split sequences into chunk groups
+    // until B H G covers the 256 compute units twice
+    const int nc = (p.T + kC - 1) / kC;
+    const int BH = p.B * p.H;
+    int g = (512 + BH - 1) / BH;
+    if (g > nc) g = nc;
+    return g < 1 ? 1 : g;
+}
+
+namespace {
+struct NarrowWs {
+    size_t mz, mzt, ef, gg, gclk, s0, total;
+};
+NarrowWs narrow_ws(const FwdParams &p, int groups) {
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t BH = (size_t)p.B * p.H, G = groups;
+    NarrowWs L{};
+    size_t off = 0;
+    L.mz = off;
+    off += up((size_t)p.H * kR * kR * 2);
+    L.mzt = off;
+    off += up((size_t)p.H * kR * kR * 2);
+    if (groups > 1) {
+        L.ef = off;
+        off += up(BH * G * 2 * kStateN * 4);
+        L.gg = off;
+        off += up(BH * G * 4);
+        L.gclk = off;
+        off += up(BH * G * 8);
+        L.s0 = off;
+        off += up(BH * 2 * kStateN * 4);
+    }
+    L.total = off;
+    return L;
+}
+}  // namespace
+
+size_t mfma_narrow_workspace_bytes(const FwdParams &p, int groups) { return narrow_ws(p, groups).total; }
+
+hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
+                                  hipEvent_t ev_start, hipEvent_t ev_stop) {
+    char *base = static_cast<char *>(ws);
+    const NarrowWs L = narrow_ws(p, groups);
+    NarrowArgs a{};
+    a.p = p;
+    a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
+    a.MzT = reinterpret_cast<const __bf16 *>(base + L.mzt);
+    const int nc = (p.T + kC - 1) / kC;
+    a.cpg = nc > 0 ? (nc + groups - 1) / groups : 1;
+    a.groups = nc > 0 ? (nc + a.cpg - 1) / a.cpg : 1;      // no empty trailing group
+    if (a.groups > 1) {
+        a.Ef = reinterpret_cast<float *>(base + L.ef);
+        a.Gg = reinterpret_cast<float *>(base + L.gg);
+        a.gclk = reinterpret_cast<double *>(base + L.gclk);
+        a.S0 = reinterpret_cast<float *>(base + L.s0);
+    }
+    hipLaunchKernelGGL(narrow_mz_kernel, dim3(p.H, kR), dim3(kR), 0, st, p.m, M, const_cast<__bf16 *>(a.Mz),
+                       const_cast<__bf16 *>(a.MzT), p.scale * 1.4426950408889634f);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid(p.B * p.H, a.groups);
+    if (a.groups > 1) {
+        hipLaunchKernelGGL(narrow_contrib_kernel, grid, dim3(kNT), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipExtLaunchKernelGGL(narrow_forward_kernel, grid, dim3(kNT), 0, st, ev_start, ev_stop, 0, a);
+    return hipGetLastError();
+}
+
+}  // namespace cyfa

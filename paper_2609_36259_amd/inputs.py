@@ -66,6 +66,8 @@ FWD_PAPER_OP = Workload("paper-op B32 T2048 H4 d256", 32, 2048, 4, 256, 256, see
 # The largest slot count of the paper's ablation (m = 255, 256 storage rows) at the
 # 1.4B-scale layer shape.
 FWD_1P4B_M255 = Workload("1.4B-layer m255 B4 T4096 H16 d128", 4, 4096, 16, 128, 128, seed=6, m=255)
+# the smallest slot count of the same ablation (m = 63) at the same layer shape
+FWD_1P4B_M63 = Workload("1.4B-layer m63 B4 T4096 H16 d128", 4, 4096, 16, 128, 128, seed=7, m=63)
 
 FORWARD_WORKLOADS = (FWD_TINY, FWD_400M, FWD_1P4B, FWD_LONG)
 

@@ -118,7 +118,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan, bool layer = fal
         const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
         if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
         if (plan->segments < 1) plan->segments = 1;
-        ws += round_up(cyfa::mfma_narrow_workspace_bytes(probe, plan->segments));
+        ws = round_up(cyfa::mfma_narrow_workspace_bytes(probe, plan->segments));   // no fp32 readout matrix
     } else if (use_mfma && wide) {
         // chunk groups of a sequence, one workgroup each
         probe.chunk = cyfa::mfma_default_chunk();
@@ -333,11 +333,8 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
     float *M = reinterpret_cast<float *>(ws);
     hipError_t e;
     if (plan.narrow) {
-        // fp32 readout matrix first, then its 64 x 64 bf16 copies in the kernel's basis order
-        e = cyfa::launch_readout_prep(p.H, p.m, R, M, nullptr, 1.f, s);
-        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
-        e = cyfa::launch_fwd_mfma_narrow(p, plan.segments, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s,
-                                         g_ev_start, g_ev_stop);
+        // forms its own 64 x 64 bf16 readout matrix
+        e = cyfa::launch_fwd_mfma_narrow(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else if (plan.mfma && p.m > cyfa::kMaxActive) {
         // fp32 readout matrix first, then its bf16 copies in the kernel's basis order
         e = cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s);

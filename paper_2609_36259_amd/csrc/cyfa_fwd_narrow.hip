@@ -16,7 +16,7 @@
 //   o = gamma (.) u Vbar + (u A^T (.) Gamma) V                [32 x 128]
 //   Kbar <- exp(G_C) Kbar + (rho (.) A)^T K,  Vbar likewise with V.
 //
-// Four waves, two workgroups per compute unit, each walking a chunk group of a
+// Four waves, three workgroups per compute unit, each walking a chunk group of a
 // sequence with both 64 x 128 fp32 states in MFMA accumulators (32 registers of
 // each per lane):
 //   Kbar: wave w = (sb, ch) = (w % 2, w / 2) holds basis rows i = 32 sb + lane % 32
@@ -27,9 +27,10 @@
 //   Vbar: wave w holds channel block 32 w + lane % 32 over all 64 basis rows (two
 //     accumulators D[i][c]), so each wave forms the value output of its channel
 //     block with no reduction.
-// The bf16 readout matrix Mz = zs M (zs = scale log2 e) and its transpose sit in LDS
-// for the whole group.  Tiles are padded rows: [32][128] at 288 bytes, [32][64] and
-// [64][64] at 160 bytes (each row 8 banks after the previous one).
+// The bf16 readout matrix Mz = zs M (zs = scale log2 e) sits in LDS for the whole
+// group; the readout's second product reads it transposed.  Tiles are padded rows:
+// [32][128] at 288 bytes, [32][64] and [64][64] at 160 bytes (each row 8 banks after
+// the previous one).  168 registers and 49.9 KB of LDS per workgroup.
 //
 // Chunk groups, as the 256-row kernel: narrow_contrib_kernel forms each group's own
 // contribution to the absolute-clock states (zero entering state), its total log
@@ -67,6 +68,12 @@ __device__ __forceinline__ int paper_row_n(int i) { return i < kDCn ? i + 1 : (i
 __device__ __forceinline__ bool row_active_n(int i, int m) { return i < m - 1 || i == kDCn; }
 __device__ __forceinline__ float uniform(float x) {
     return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+__device__ __forceinline__ double uniform_d(double x) {
+    const unsigned long long v = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)v);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(v >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 __device__ __forceinline__ float opqf(float x) {
     asm volatile("" : "+v"(x));
@@ -145,16 +152,6 @@ __device__ __forceinline__ void store_block_n(__bf16 *T, int col0, const f32x16 
 __device__ __forceinline__ bf16x8 rd_row(const __bf16 *S, int row, int k0, int hl) {
     return lds8(S + row * SSB + k0 + 8 * hl);
 }
-// The operand's k indices k0 + 8 (lane/32) + p scaled by f[p].
-__device__ __forceinline__ bf16x8 scale_k(bf16x8 v, const float *f) {
-    const float4 a = *reinterpret_cast<const float4 *>(f);
-    const float4 b = *reinterpret_cast<const float4 *>(f + 4);
-    const float d[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    bf16x8 r;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) r[q] = (__bf16)((float)v[q] * d[q]);
-    return r;
-}
 template <int N>
 __device__ __forceinline__ void scale_acc(f32x16 (&acc)[N], float f) {
 #pragma unroll
@@ -228,9 +225,10 @@ struct Sc {
 // instead of rescaling every accumulator; when an exponent could leave [-60, 60] the
 // chunk is eager (registers times exp(Ls) first, Ls restarts at 0, plain gam and rho,
 // registers times exp(G_C) before the update).
-__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok &k, double &carry, float Ls) {
+// dm = m, inv_m = 1/m and amp0 = sqrt(2/m) come in as wave-uniform (scalar) values.
+__device__ __forceinline__ void chunk_scalars(Sc &s, int lane, double dm, double inv_m, float amp0, const Tok &k,
+                                              double &carry, float Ls) {
     lane = opq(lane);
-    const double inv_m = 1.0 / (double)m;
     const float G = wave_incl_scan(k.g);
     const double lam = carry + wave_incl_scan((double)k.dl);
     const float GC = lane63(G);
@@ -247,7 +245,7 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
         s.urev[lane] = u;
         float s1, c1;
         sincos_rev(u, &s1, &c1);
-        s.bw[lane] = make_float4(k.be * sqrtf(2.f / (float)m), u, c1, s1);
+        s.bw[lane] = make_float4(k.be * amp0, u, c1, s1);
     }
     if (lane == 0) {
         s.ctl[0] = lazy ? 1.f : __expf(Ls);
@@ -255,25 +253,28 @@ __device__ __forceinline__ void chunk_scalars(Sc &s, int lane, int m, const Tok 
         s.ctl[2] = lazy ? 1.f : 0.f;
         s.ctl[3] = gabs <= 60.f ? 1.f : 0.f;
     }
-    carry = reduce_clock(lane63(lam), (double)m, inv_m);
+    carry = reduce_clock(lane63(lam), dm, inv_m);
 }
 __device__ __forceinline__ float next_scale(const Sc &s, float Ls) {
     return s.ctl[2] != 0.f ? Ls + s.G[kC - 1] : 0.f;
 }
 
-// Temporal write rows (Eq. app-temporal-writes) into a [32][64] tile: amp_t [cos
-// th_j, -sin th_j] on pair j (internal columns 2j-2, 2j-1), amp_t / sqrt 2 = beta_t /
-// sqrt m on DC (62), 0 on 63.  Thread (row tid/8, q = tid % 8) fills columns 8q ..
-// 8q+7 (pairs 4q+1 .. 4q+4); the phases advance by angle addition from a start
-// reduced in revolutions.
-__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) {
+// Temporal write rows (Eq. app-temporal-writes) into [32][64] tiles: amp_t [cos th_j,
+// -sin th_j] on pair j (internal columns 2j-2, 2j-1), amp_t / sqrt 2 = beta_t / sqrt m on
+// DC (62), 0 on 63; into T the rows themselves (kPlain: the intra-chunk products), into
+// Td the rows times rho_t (the operand of both state updates, Eq. app-chunk-rescale).
+// Thread (row tid/8, q = tid % 8) fills columns 8q .. 8q+7 (pairs 4q+1 .. 4q+4); the
+// phases advance by angle addition from a start reduced in revolutions.
+template <bool kPlain>
+__device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, __bf16 *Td, int tid, int m) {
     const int q = tid & 7, r = tid >> 3;
     const int J = (m - 1) >> 1;
     const float4 rec = s.bw[r];
     const float amp = rec.x, u = rec.y, c1 = rec.z, s1 = rec.w;
+    const float rho = s.rho[r];
     float sn, cs;
     sincos_rev(__builtin_amdgcn_fractf((float)(4 * q + 1) * u), &sn, &cs);
-    bf16x8 a8;
+    bf16x8 a8, d8;
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
         const int j = 4 * q + 1 + jj;
@@ -285,6 +286,8 @@ __device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) 
         }
         a8[2 * jj] = (__bf16)a0;
         a8[2 * jj + 1] = (__bf16)a1;
+        d8[2 * jj] = (__bf16)(a0 * rho);
+        d8[2 * jj + 1] = (__bf16)(a1 * rho);
         if (jj < 3) {
             const float nc = cs * c1 - sn * s1;
             const float ns = sn * c1 + cs * s1;
@@ -292,7 +295,8 @@ __device__ __forceinline__ void build_A(const Sc &s, __bf16 *T, int tid, int m) 
             sn = ns;
         }
     }
-    *reinterpret_cast<bf16x8 *>(cbyte(T) + r * PNB + 16 * q) = a8;
+    if constexpr (kPlain) *reinterpret_cast<bf16x8 *>(cbyte(T) + r * PNB + 16 * q) = a8;
+    *reinterpret_cast<bf16x8 *>(cbyte(Td) + r * PNB + 16 * q) = d8;
 }
 
 // (cos, sin) of 2 pi j urev for the eight pairs of a lane's 16 rows in basis block sb:
@@ -436,7 +440,8 @@ __device__ __forceinline__ void add_dump(f32x16 (&acc)[2], const float *E, float
 
 struct NarrowArgs {
     FwdParams p;
-    const __bf16 *Mz, *MzT;  // [H][64][64] readout matrix times scale log2 e, and its transpose
+    const __bf16 *Mz;        // [H][64][64] readout matrix times scale log2 e (internal basis order)
+    float zs;                // scale log2 e
     int groups, cpg;         // chunk groups per sequence, chunks per group
     float *Ef;               // [BH][groups][2][kStateN] each group's own contribution (K, V)
     float *Gg;               // [BH][groups] total log decay of each group
@@ -471,30 +476,34 @@ __device__ __forceinline__ double block_token_sum(const float *x, int stride, in
 }
 
 // ---- LDS map (bytes) ------------------------------------------------------------
+// Tiles share space by lifetime: X (then u) lives in K's place (K is last read by the
+// key-state update), the ch = 1 waves' key-pass partials and then W in Q's place (Q is
+// last read by the key pass and the score tile; the output tile comes after W), and
+// the value pass's score tile in the key pass's.
 struct Lay {
     static constexpr int T1 = kC * PSB;            // [32][128] tile
     static constexpr int TN = kC * PNB;            // [32][64] tile
     static constexpr int TM = kR * PNB;            // [64][64] matrix
     static constexpr int TS = kC * SSB * 2;        // score tile
     static constexpr int PART = 2 * 64 * 16 * 4;   // the ch = 1 waves' key-pass partials
-    static constexpr int Q = 0;                    // Q, then the output tile
-    static constexpr int K = Q + T1;
+    static constexpr int Q = 0;                    // Q, the key-pass partials, W, the output tile
+    static constexpr int K = Q + T1;               // K, then X, then u
     static constexpr int V = K + T1;
     static constexpr int A = V + T1;               // temporal writes
-    static constexpr int X = A + TN;               // X, then u
-    static constexpr int W = X + TN;               // key-pass partials, then W
-    static constexpr int S1 = W + PART;            // Gamma (.) Q K^T
-    static constexpr int S2 = S1 + TS;             // Gamma (.) u A^T
-    static constexpr int MT = S2 + TS;             // Mz [slot][basis]
-    static constexpr int MTT = MT + TM;            // MzT [basis][slot]
-    static constexpr int RED = MTT + TM;           // softmax partials [2 slot blocks][32 tokens] float2
+    static constexpr int AD = A + TN;              // temporal writes times rho (state updates)
+    static constexpr int X = K;
+    static constexpr int W = Q;
+    static constexpr int S1 = AD + TN;             // Gamma (.) Q K^T
+    static constexpr int S2 = S1;                  // Gamma (.) u A^T (S1 is dead by then)
+    static constexpr int MT = S1 + TS;             // Mz [slot][basis] (M^T by transposed reads)
+    static constexpr int RED = MT + TM;            // softmax partials [2 slot blocks][32 tokens] float2
     static constexpr int SC = RED + 2 * kC * 8;
     static constexpr int BYTES = SC + (int)sizeof(Sc);
-    static_assert(TN <= PART, "W fits the partials' place");
-    static_assert(BYTES <= 80 * 1024, "two workgroups per compute unit");
+    static_assert(TN <= T1 && PART <= T1, "X, W and the partials fit a [32][128] tile's place");
+    static_assert(3 * BYTES <= 160 * 1024, "three workgroups per compute unit");
 };
 
-__global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
+__global__ __launch_bounds__(kNT, 3) void narrow_forward_kernel(NarrowArgs a) {
     using L = Lay;
     __shared__ __attribute__((aligned(256))) char smem[L::BYTES];
     const FwdParams &p = a.p;
@@ -508,24 +517,25 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
     const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
     Sc &sc = *lds_at<Sc>(smem, L::SC);
     __bf16 *Qt = lds_at<__bf16>(smem, L::Q), *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
-    __bf16 *At = lds_at<__bf16>(smem, L::A), *Xt = lds_at<__bf16>(smem, L::X), *Wt = lds_at<__bf16>(smem, L::W);
+    __bf16 *At = lds_at<__bf16>(smem, L::A), *Ad = lds_at<__bf16>(smem, L::AD);
+    __bf16 *Xt = lds_at<__bf16>(smem, L::X), *Wt = lds_at<__bf16>(smem, L::W);
     __bf16 *S1 = lds_at<__bf16>(smem, L::S1), *S2 = lds_at<__bf16>(smem, L::S2);
-    __bf16 *Mt = lds_at<__bf16>(smem, L::MT), *MTt = lds_at<__bf16>(smem, L::MTT);
+    __bf16 *Mt = lds_at<__bf16>(smem, L::MT);
     float2 *red = lds_at<float2>(smem, L::RED);
     float *part = lds_at<float>(smem, L::W);
-    const Sw z = make_sw(tid);
-    const float zs = p.scale * 1.4426950408889634f;     // Mz = zs M: logits in log2 units
-    const float inv_zs = 1.f / zs;
+    // wave-uniform constants in scalar registers (computed on the vector ALU they would
+    // hold vector registers across the chunk loop)
+    const float inv_zs = uniform(1.f / (p.scale * 1.4426950408889634f));   // Mz = zs M, zs = scale log2 e
+    const double dm = uniform_d((double)m), inv_m = uniform_d(1.0 / (double)m);
+    const float amp0 = uniform(sqrtf(2.f / (float)m));
 
-    // the readout matrix and its transpose, resident for the group (two 16-byte
-    // pieces of each per thread)
+    // the readout matrix, resident for the group (two 16-byte pieces per thread)
     {
-        const __bf16 *Mg = a.Mz + (size_t)h * kR * kR, *MTg = a.MzT + (size_t)h * kR * kR;
+        const __bf16 *Mg = a.Mz + (size_t)h * kR * kR;
 #pragma unroll
         for (int it = 0; it < 2; ++it) {
             const int e = it * kNT + tid, r = e >> 3, c8 = (e & 7) * 8;
             *reinterpret_cast<uint4 *>(Mt + r * PN + c8) = *reinterpret_cast<const uint4 *>(Mg + r * kR + c8);
-            *reinterpret_cast<uint4 *>(MTt + r * PN + c8) = *reinterpret_cast<const uint4 *>(MTg + r * kR + c8);
         }
     }
 
@@ -577,12 +587,15 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
     float Ls = 0.f;                                   // carried states: exp(Ls) x registers
     for (int c = c_begin; c < c_end; ++c) {
         const int t0 = c * kC, n = min(kC, Tb - t0);
+        // lane offsets recomputed each chunk from an opaque thread index: kept across the
+        // loop they would be spilled
+        const int tq = opq(tid), lq = tq & 63;
+        const Sw z = make_sw(tq);
         // -- stage the chunk and its scalars
         store_rows2(Qt, rq, z);
         store_rows2(Kt, rk, z);
         store_rows2(Vt, rv, z);
-        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
-        if (c + 1 < c_end) prefetch(c + 1);
+        if (w == 0) chunk_scalars(sc, lane, dm, inv_m, amp0, tk, carry, Ls);
         lds_barrier();
         {
             const float pre = uniform(sc.ctl[0]);
@@ -591,8 +604,8 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
                 scale_acc(vacc, pre);
             }
         }
-        build_A(sc, At, tid, m);
-        score_block<4, PS>(Kt, 16 * (w & 1), Qt, 16 * (w >> 1), S1, sc, lane);   // S1[t][s]
+        build_A<true>(sc, At, Ad, tq, m);
+        score_block<4, PS>(Kt, 16 * (w & 1), Qt, 16 * (w >> 1), S1, sc, lq);   // S1[t][s]
         // -- key pass: p = gamma (.) Q Kbar^T + S1 A (D[basis][t]) over this wave's channel
         //    half; then its part of the key state update
         const float gr = sc.gam[l32];
@@ -609,7 +622,7 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
         pacc = mma(stro_n(At, 16 * ch, 32 * sb, z), rd_row(S1, l32, 16 * ch, hl), pacc);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = scale_k(stro_n(At, 16 * ks, 32 * sb, z), sc.rho + 16 * ks + 8 * hl);
+            const bf16x8 ad = stro_n(Ad, 16 * ks, 32 * sb, z);
 #pragma unroll
             for (int x = 0; x < 2; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 64 * ch + 32 * x, z), ad, kacc[x]);
         }
@@ -633,7 +646,7 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
                 pacc[4 * q + 3] += e.w;
             }
             float pc[8], ps[8];
-            lane_phases(opqf(sc.urev[l32]), sb, hl, m, pc, ps);
+            lane_phases(opqf(sc.urev[l32]), sb, opq(lane) >> 5, m, pc, ps);
             rotate<1>(pacc, pc, ps, 1.f);
             if (sb == 1 && hl == 1) pacc[15] = 1.f;
             store_block_n(Xt, 32 * sb, pacc, z);
@@ -644,12 +657,13 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
         float mx = 0.f;
         if (ch == 0) {
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) wr = mma(mrow(Mt, 32 * sb, ks, lane), srow_n(Xt, ks, z), wr);
-            if (p.logits && l32 < n) {
-                float *lg = p.logits + ((row0 + t0 + l32) * p.H + h) * m;
+            for (int ks = 0; ks < 4; ++ks) wr = mma(mrow(Mt, 32 * sb, ks, lq), srow_n(Xt, ks, z), wr);
+            if (p.logits && (lq & 31) < n) {
+                float *lg = p.logits + ((row0 + t0 + (lq & 31)) * p.H + h) * m;
+                const int slot0 = 32 * sb + 4 * (lq >> 5);
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int slot = 32 * sb + 8 * (v >> 2) + 4 * hl + (v & 3);
+                    const int slot = slot0 + 8 * (v >> 2) + (v & 3);
                     if (slot < m) lg[slot] = wr[v] * 0.69314718055994531f;
                 }
             }
@@ -680,16 +694,19 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
         if (ch == 0) {
             f32x16 ya = zero_acc();
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) ya = mma(mrow(MTt, 32 * sb, ks, lane), srow_n(Wt, ks, z), ya);
+            for (int ks = 0; ks < 4; ++ks) ya = mma(stro_n(Mt, 16 * ks, 32 * sb, z), srow_n(Wt, ks, z), ya);
             float pc[8], ps[8];
-            lane_phases(opqf(sc.urev[l32]), sb, hl, m, pc, ps);
+            lane_phases(opqf(sc.urev[l32]), sb, opq(lane) >> 5, m, pc, ps);
             rotate<-1>(ya, pc, ps, inv_zs);
             store_block_n(Xt, 32 * sb, ya, z);
         }
+        // the next chunk's rows, issued once the readout's registers are free (with three
+        // workgroups per compute unit the rest of the chunk covers their latency)
+        if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
         // -- value pass: o = gamma (.) u Vbar + S2 V, this wave's channel block (D[c][t]);
         //    then the value state update
-        score_block<2, PN>(At, 16 * (w & 1), Xt, 16 * (w >> 1), S2, sc, lane);   // S2[t][s]
+        score_block<2, PN>(At, 16 * (w & 1), Xt, 16 * (w >> 1), S2, sc, lq);   // S2[t][s]
         f32x16 oacc = zero_acc();
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) oacc = mma(acc_to_operand(vacc[ks >> 1], ks & 1), sperm_n(Xt, ks, z), oacc);
@@ -700,8 +717,7 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
         for (int ks = 0; ks < 2; ++ks) {
             const bf16x8 vb = stro(Vt, 16 * ks, 32 * w, z);
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                vacc[j] = mma(scale_k(stro_n(At, 16 * ks, 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb, vacc[j]);
+            for (int j = 0; j < 2; ++j) vacc[j] = mma(stro_n(Ad, 16 * ks, 32 * j, z), vb, vacc[j]);
         }
         lds_barrier();
 #pragma unroll
@@ -709,7 +725,7 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
         store_block(Qt, 32 * w, oacc, z);              // o[t][c], in Q's place
         Ls = next_scale(sc, Ls);
         lds_barrier();
-        copy_rows2_out(Qt, o + ((row0 + t0) * p.H + h) * 128, rs, n, tid, z);
+        copy_rows2_out(Qt, o + ((row0 + t0) * p.H + h) * 128, rs, n, tq, z);
         lds_barrier();
     }
     // the last group ends with the final states (chunks past a sequence change nothing)
@@ -727,9 +743,78 @@ __global__ __launch_bounds__(kNT, 2) void narrow_forward_kernel(NarrowArgs a) {
     }
 }
 
+// Rows [32 rb, 32 rb + 32) of the bf16 readout matrix Mz = zs R Phi (zs = scale log2 e)
+// on 64 storage rows: slot i on rows, the kernels' internal basis order on columns
+// (Mz[i][j_int] = zs M[i][paper(j_int)]), zero outside the active m x m block, and
+// kMaskLogit in the padding column of inactive slots (i >= m).  Phi is the real
+// Fourier basis of App. A.1 (Eq. app-real-fourier): column 0 = 1/sqrt(m), column
+// 2l-1 = sqrt(2/m) cos(2 pi l s / m), column 2l = sqrt(2/m) sin(2 pi l s / m).  256
+// threads: thread (j = tid % 64, g = tid / 64) forms paper column j of rows 32 rb + 8 g
+// .. + 7 from R's rows staged in LDS (zero-padded to 64 columns) and a table of the m
+// angles 2 pi r / m (the index l s mod m advances by l per step).  lds: 8704 bytes.
+__device__ __forceinline__ void narrow_mz_rows(int m, const float *__restrict__ R, __bf16 *__restrict__ Mz,
+                                               float zs, int h, int rb, int tid, char *lds) {
+    float *tab = reinterpret_cast<float *>(lds);             // [2][64] cos, sin of 2 pi r / m
+    float *Rr = tab + 2 * kR;                                // [32][64]
+    const int row0 = 32 * rb;
+    if (tid < m) {
+        double sn, cs;
+        sincospi(2.0 * (double)tid / (double)m, &sn, &cs);
+        tab[tid] = (float)cs;
+        tab[kR + tid] = (float)sn;
+    }
+    const float *Rh = R ? R + (size_t)h * m * m : nullptr;
+    for (int e = tid; e < 32 * kR; e += kNT) {
+        const int r = e >> 6, sc = e & (kR - 1), i = row0 + r;
+        Rr[e] = (i < m && sc < m) ? (Rh ? Rh[(size_t)i * m + sc] : (sc == i ? 1.f : 0.f)) : 0.f;
+    }
+    __syncthreads();
+    const int j = tid & (kR - 1), g = tid >> 6;
+    const float *t = (j == 0 || (j & 1)) ? tab : tab + kR;
+    const int l = (j + 1) >> 1;
+    float acc[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) acc[r] = 0.f;
+    if (j < m) {
+        int idx = 0;
+        for (int s0 = 0; s0 < kR; s0 += 4) {
+            float ph[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                ph[q] = t[idx];
+                idx += l;
+                if (idx >= m) idx -= m;
+            }
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const float4 rv = *reinterpret_cast<const float4 *>(Rr + (8 * g + r) * kR + s0);
+                acc[r] = fmaf(rv.x, ph[0], fmaf(rv.y, ph[1], fmaf(rv.z, ph[2], fmaf(rv.w, ph[3], acc[r]))));
+            }
+        }
+    }
+    const float cscale = j == 0 ? (float)(1.0 / sqrt((double)m)) : (float)sqrt(2.0 / (double)m);
+    const int jint = j == 0 ? kDCn : (j == kR - 1 ? kR - 1 : j - 1);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        const int i = row0 + 8 * g + r;
+        const float val = (j < m && i < m) ? acc[r] * cscale : 0.f;
+        const float zv = (j == kR - 1 && i >= m) ? kMaskLogit : zs * val;
+        Mz[((size_t)h * kR + i) * kR + jint] = (__bf16)zv;
+    }
+}
+
+// The readout matrix alone (one chunk group per sequence: no contribution launch)
+__global__ __launch_bounds__(kNT) void narrow_mz_kernel(int m, const float *__restrict__ R, __bf16 *__restrict__ Mz,
+                                                        float zs) {
+    __shared__ __attribute__((aligned(16))) char lds[(2 * kR + 32 * kR) * 4];
+    narrow_mz_rows(m, R, Mz, zs, blockIdx.x >> 1, blockIdx.x & 1, threadIdx.x, lds);
+}
+
 // Each chunk group's own contribution (groups > 1; launched before the forward).
 // The last group's contribution is never read, so its workgroup copies rows 0 .. 63
 // of (K0, V0) for the forward's prologues instead and forms only its total log decay.
+// Blocks (b h) G + g; 2 H extra blocks of the same launch form the readout matrix, 32
+// rows each.
 __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
     using L = Lay;
     __shared__ __attribute__((aligned(256))) char smem[L::V + L::T1];   // K and V tiles
@@ -737,7 +822,13 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
     __shared__ Sc sc;
     __shared__ double red[kNT / 64];
     const FwdParams &p = a.p;
-    const int bh = blockIdx.x, g = blockIdx.y, h = bh % p.H, b = bh / p.H;
+    const int nseg = p.B * p.H * a.groups;
+    if ((int)blockIdx.x >= nseg) {
+        const int q = (int)blockIdx.x - nseg;
+        narrow_mz_rows(p.m, p.R, const_cast<__bf16 *>(a.Mz), a.zs, q >> 1, q & 1, threadIdx.x, smem);
+        return;
+    }
+    const int bh = (int)blockIdx.x / a.groups, g = (int)blockIdx.x % a.groups, h = bh % p.H, b = bh / p.H;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
     const int sb = w & 1, ch = w >> 1;
     const int m = p.m;
@@ -767,6 +858,8 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
     }
     __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
     const Sw z = make_sw(tid);
+    const double dm = uniform_d((double)m), inv_m = uniform_d(1.0 / (double)m);
+    const float amp0 = uniform(sqrtf(2.f / (float)m));
     f32x16 kacc[2], vacc[2];
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
@@ -790,10 +883,10 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
     for (int c = c_begin; c < c_end; ++c) {
         store_rows2(Kt, rk, z);
         store_rows2(Vt, rv, z);
-        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
+        if (w == 0) chunk_scalars(sc, lane, dm, inv_m, amp0, tk, carry, Ls);
         if (c + 1 < c_end) prefetch(c + 1);
         lds_barrier();
-        build_A(sc, Asm, tid, m);
+        build_A<false>(sc, nullptr, Asm, tid, m);
         gsum += (double)sc.G[kC - 1];
         {
             const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
@@ -806,13 +899,12 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
         lds_barrier();
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = scale_k(stro_n(Asm, 16 * ks, 32 * sb, z), sc.rho + 16 * ks + 8 * hl);
+            const bf16x8 ad = stro_n(Asm, 16 * ks, 32 * sb, z);
 #pragma unroll
             for (int x = 0; x < 2; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 64 * ch + 32 * x, z), ad, kacc[x]);
             const bf16x8 vb = stro(Vt, 16 * ks, 32 * w, z);
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                vacc[j] = mma(scale_k(stro_n(Asm, 16 * ks, 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb, vacc[j]);
+            for (int j = 0; j < 2; ++j) vacc[j] = mma(stro_n(Asm, 16 * ks, 32 * j, z), vb, vacc[j]);
         }
         lds_barrier();
     }
@@ -823,21 +915,6 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
     if (tid == 0) a.Gg[pi] = (float)gsum;
 }
 
-// bf16 readout matrix for the kernels above from the fp32 one (paper basis order,
-// [H][128][128], zero outside the active m x m block): Mz[i][j_int] = zs M[i][paper(j_int)]
-// for slots i < 64, with kMaskLogit in the padding column of inactive slots (i >= m), and
-// its transpose MzT[j_int][i].
-__global__ __launch_bounds__(kR) void narrow_mz_kernel(int m, const float *__restrict__ M, __bf16 *__restrict__ Mz,
-                                                       __bf16 *__restrict__ MzT, float zs) {
-    const int h = blockIdx.x, i = blockIdx.y, jint = threadIdx.x;
-    const int jp = jint < kDCn ? jint + 1 : (jint == kDCn ? 0 : -1);
-    float val = jp >= 0 ? zs * M[((size_t)h * kStoreRows + i) * kStoreRows + jp] : 0.f;
-    if (jint == kR - 1 && i >= m) val = kMaskLogit;
-    const __bf16 bv = (__bf16)val;
-    Mz[((size_t)h * kR + i) * kR + jint] = bv;
-    MzT[((size_t)h * kR + jint) * kR + i] = bv;
-}
-
 }  // namespace
 
 bool mfma_narrow_supported(const FwdParams &p) {
@@ -846,18 +923,18 @@ bool mfma_narrow_supported(const FwdParams &p) {
 }
 
 int mfma_narrow_auto_groups(const FwdParams &p) {
-    // two four-wave workgroups per compute unit: split sequences into chunk groups
-    // until B H G covers the 256 compute units twice
+    // three four-wave workgroups per compute unit: split sequences into chunk groups
+    // until B H G covers the 256 compute units three times
     const int nc = (p.T + kC - 1) / kC;
     const int BH = p.B * p.H;
-    int g = (512 + BH - 1) / BH;
+    int g = (768 + BH - 1) / BH;
     if (g > nc) g = nc;
     return g < 1 ? 1 : g;
 }
 
 namespace {
 struct NarrowWs {
-    size_t mz, mzt, ef, gg, gclk, s0, total;
+    size_t mz, ef, gg, gclk, s0, total;
 };
 NarrowWs narrow_ws(const FwdParams &p, int groups) {
     auto up = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -865,8 +942,6 @@ NarrowWs narrow_ws(const FwdParams &p, int groups) {
     NarrowWs L{};
     size_t off = 0;
     L.mz = off;
-    off += up((size_t)p.H * kR * kR * 2);
-    L.mzt = off;
     off += up((size_t)p.H * kR * kR * 2);
     if (groups > 1) {
         L.ef = off;
@@ -885,33 +960,32 @@ NarrowWs narrow_ws(const FwdParams &p, int groups) {
 
 size_t mfma_narrow_workspace_bytes(const FwdParams &p, int groups) { return narrow_ws(p, groups).total; }
 
-hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
-                                  hipEvent_t ev_start, hipEvent_t ev_stop) {
+hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, void *ws, hipStream_t st, hipEvent_t ev_start,
+                                  hipEvent_t ev_stop) {
     char *base = static_cast<char *>(ws);
     const NarrowWs L = narrow_ws(p, groups);
     NarrowArgs a{};
     a.p = p;
     a.Mz = reinterpret_cast<const __bf16 *>(base + L.mz);
-    a.MzT = reinterpret_cast<const __bf16 *>(base + L.mzt);
+    a.zs = p.scale * 1.4426950408889634f;
     const int nc = (p.T + kC - 1) / kC;
     a.cpg = nc > 0 ? (nc + groups - 1) / groups : 1;
     a.groups = nc > 0 ? (nc + a.cpg - 1) / a.cpg : 1;      // no empty trailing group
+    hipError_t e;
     if (a.groups > 1) {
         a.Ef = reinterpret_cast<float *>(base + L.ef);
         a.Gg = reinterpret_cast<float *>(base + L.gg);
         a.gclk = reinterpret_cast<double *>(base + L.gclk);
         a.S0 = reinterpret_cast<float *>(base + L.s0);
+        // the groups' contributions and, in extra blocks, the readout matrix
+        hipLaunchKernelGGL(narrow_contrib_kernel, dim3(p.B * p.H * a.groups + 2 * p.H), dim3(kNT), 0, st, a);
+    } else {
+        hipLaunchKernelGGL(narrow_mz_kernel, dim3(2 * p.H), dim3(kNT), 0, st, p.m, p.R, const_cast<__bf16 *>(a.Mz),
+                           a.zs);
     }
-    hipLaunchKernelGGL(narrow_mz_kernel, dim3(p.H, kR), dim3(kR), 0, st, p.m, M, const_cast<__bf16 *>(a.Mz),
-                       const_cast<__bf16 *>(a.MzT), p.scale * 1.4426950408889634f);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const dim3 grid(p.B * p.H, a.groups);
-    if (a.groups > 1) {
-        hipLaunchKernelGGL(narrow_contrib_kernel, grid, dim3(kNT), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    hipExtLaunchKernelGGL(narrow_forward_kernel, grid, dim3(kNT), 0, st, ev_start, ev_stop, 0, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipExtLaunchKernelGGL(narrow_forward_kernel, dim3(p.B * p.H, a.groups), dim3(kNT), 0, st, ev_start, ev_stop, 0,
+                          a);
     return hipGetLastError();
 }
 

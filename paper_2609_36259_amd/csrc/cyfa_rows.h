@@ -39,14 +39,14 @@ hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, 
 // 32 or 64 run as 32-token chunks, one workgroup per chunk group of a sequence, two per
 // compute unit).  The state arrays keep the [B][H][128][d] layout of m <= 127; the kernel
 // reads their rows 0 .. 63 and writes rows 64 .. 127 of the final states as zeros.  ws
-// (mfma_narrow_workspace_bytes) receives the bf16 64 x 64 readout matrix and its
-// transpose, formed from the fp32 M of launch_readout_prep, and with groups > 1 the
-// groups' contributions; the events, when given, bracket the fused kernel.
+// (mfma_narrow_workspace_bytes) receives the bf16 64 x 64 readout matrix, formed from
+// p.R, and with groups > 1 the groups' contributions; the events, when given, bracket
+// the fused kernel.
 bool mfma_narrow_supported(const FwdParams &p);
 int mfma_narrow_auto_groups(const FwdParams &p);
 size_t mfma_narrow_workspace_bytes(const FwdParams &p, int groups);
-hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
-                                  hipEvent_t ev_start, hipEvent_t ev_stop);
+hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, void *ws, hipStream_t st, hipEvent_t ev_start,
+                                  hipEvent_t ev_stop);
 
 // Vector-ALU forward over chunk groups (d_k, d_v <= 128 and m <= 127; other
 // shapes run one group per sequence): groups > 1 forms the state entering each

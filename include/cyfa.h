@@ -38,7 +38,10 @@
  *     input, written as zero on output.  Below, "128" in a state shape reads
  *     S.  m > 127 runs the forward (matrix-core kernel for BF16 with d_k = d_v
  *     = 128, else the vector-ALU kernel) and the decode step with head dims 64 or
- *     128; the backward takes m <= 127.
+ *     128; the backward takes m <= 127.  For m <= 63 the matrix-core forward with
+ *     d_k = d_v = 128 computes on m* = 64 storage rows (the smallest slot count
+ *     of the paper's ablation); its state arrays keep S = 128 rows, of which it
+ *     reads rows 0..63 and writes rows 64..127 as zero.
  *   - Clocks are double precision and are reported reduced modulo m, which is
  *     exact because U(tau + m) = U(tau) (App. A.1, Prop. 1) and the output
  *     depends only on clock differences (App. A.4, Prop. 6).
@@ -92,7 +95,8 @@ typedef enum {
  *   segments     sequence segments per (b, h) run in parallel: 0 = automatic,
  *                else 1..1024 (the VALU kernel: groups of 16-token chunks, more
  *                than one only for d_k, d_v <= 128 and m <= 127; the MFMA kernel
- *                at m > 127: groups of 32-token chunks).  The state entering a
+ *                at m > 127 and, with d = 128, at m <= 63: groups of 32-token
+ *                chunks).  The state entering a
  *                segment is obtained from a pre-pass over the earlier segments.
  *                Results do not depend on it beyond rounding.
  *   scale        logit scale (the paper leaves the dot-product scaling out of

@@ -414,28 +414,34 @@ __device__ __forceinline__ void zero_upper_rows(float *S, int tid) {
         *reinterpret_cast<float4 *>(S + kR * 128 + 4 * (it * kNT + tid)) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// ---- chunk-group contributions (fp32, lane-major: wave w, accumulator x, lane, register)
-constexpr int kStateN = kR * 128;                   // floats of one 64 x 128 state
+// ---- chunk-group contributions (bf16, lane-major: wave w, accumulator x, lane, register;
+// the precision in which the chunk products consume the state, as the 128-row kernel's
+// segment states)
+constexpr int kStateN = kR * 128;                   // elements of one 64 x 128 state
 __device__ __forceinline__ int dump_n(int w, int x, int lane) { return ((w * 2 + x) * 64 + lane) * 16; }
-__device__ __forceinline__ void store_dump(float *E, const f32x16 (&acc)[2], float f, int w, int lane) {
+__device__ __forceinline__ void store_dump(__bf16 *E, const f32x16 (&acc)[2], int w, int lane) {
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<float4 *>(E + dump_n(w, x, lane) + 4 * q) =
-                make_float4(f * acc[x][4 * q], f * acc[x][4 * q + 1], f * acc[x][4 * q + 2], f * acc[x][4 * q + 3]);
-}
-__device__ __forceinline__ void add_dump(f32x16 (&acc)[2], const float *E, float f, int w, int lane) {
+        for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 o;
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float4 e = *reinterpret_cast<const float4 *>(E + dump_n(w, x, lane) + 4 * q);
-            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
-            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
-            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
-            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+            for (int v = 0; v < 8; ++v) o[v] = (__bf16)acc[x][8 * hf + v];
+            *reinterpret_cast<bf16x8 *>(E + dump_n(w, x, lane) + 8 * hf) = o;
         }
+}
+// a lane's part of one contribution: [x][half] pieces of 8 registers
+__device__ __forceinline__ void load_dump(bf16x8 (&e)[4], const __bf16 *E, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) e[2 * x + hf] = *reinterpret_cast<const bf16x8 *>(E + dump_n(w, x, lane) + 8 * hf);
+}
+__device__ __forceinline__ void add_dump(f32x16 (&acc)[2], const bf16x8 (&e)[4], float f) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[x][v] = fmaf(f, (float)e[2 * x + (v >> 3)][v & 7], acc[x][v]);
 }
 
 struct NarrowArgs {
@@ -443,7 +449,7 @@ struct NarrowArgs {
     const __bf16 *Mz;        // [H][64][64] readout matrix times scale log2 e (internal basis order)
     float zs;                // scale log2 e
     int groups, cpg;         // chunk groups per sequence, chunks per group
-    float *Ef;               // [BH][groups][2][kStateN] each group's own contribution (K, V)
+    __bf16 *Ef;              // [BH][groups][2][kStateN] each group's own contribution (K, V), bf16
     float *Gg;               // [BH][groups] total log decay of each group
     double *gclk;            // [BH][groups] clock entering each group (reduced mod m)
     float *S0;               // [BH][2][64 x 128] rows 0 .. 63 of (K0, V0) (groups > 1: the states
@@ -554,14 +560,28 @@ __global__ __launch_bounds__(kNT, 3) void narrow_forward_kernel(NarrowArgs a) {
     } else {
         // state entering the group: each earlier group's contribution decayed through
         // the groups after it, plus (K0, V0) decayed through all earlier groups
+        // (two contributions per round trip: their loads are issued before either sum)
         const float *Gg = a.Gg + (size_t)bh * a.groups;
         float tail = 0.f;                         // log decay of groups q+1 .. g-1
-        for (int q = g - 1; q >= 0; --q) {
-            const float f = __expf(tail);
-            const float *E = a.Ef + ((size_t)bh * a.groups + q) * 2 * kStateN;
-            add_dump(kacc, E, f, w, lane);
-            add_dump(vacc, E + kStateN, f, w, lane);
+        for (int q = g - 1; q >= 0; q -= 2) {
+            bf16x8 ek0[4], ev0[4], ek1[4], ev1[4];
+            const __bf16 *E0 = a.Ef + ((size_t)bh * a.groups + q) * 2 * kStateN;
+            load_dump(ek0, E0, w, lane);
+            load_dump(ev0, E0 + kStateN, w, lane);
+            if (q >= 1) {
+                load_dump(ek1, E0 - 2 * kStateN, w, lane);
+                load_dump(ev1, E0 - kStateN, w, lane);
+            }
+            const float f0 = __expf(tail);
             tail += Gg[q];
+            add_dump(kacc, ek0, f0);
+            add_dump(vacc, ev0, f0);
+            if (q >= 1) {
+                const float f1 = __expf(tail);
+                tail += Gg[q - 1];
+                add_dump(kacc, ek1, f1);
+                add_dump(vacc, ev1, f1);
+            }
         }
         const float *S0 = a.S0 + (size_t)bh * 2 * kStateN;
         if (p.K0) add_key_state(kacc, S0, __expf(tail), sb, ch, lane, m);
@@ -810,16 +830,22 @@ __global__ __launch_bounds__(kNT) void narrow_mz_kernel(int m, const float *__re
     narrow_mz_rows(m, R, Mz, zs, blockIdx.x >> 1, blockIdx.x & 1, threadIdx.x, lds);
 }
 
-// Each chunk group's own contribution (groups > 1; launched before the forward).
-// The last group's contribution is never read, so its workgroup copies rows 0 .. 63
-// of (K0, V0) for the forward's prologues instead and forms only its total log decay.
-// Blocks (b h) G + g; 2 H extra blocks of the same launch form the readout matrix, 32
-// rows each.
-__global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
-    using L = Lay;
-    __shared__ __attribute__((aligned(256))) char smem[L::V + L::T1];   // K and V tiles
-    __shared__ __attribute__((aligned(256))) __bf16 Asm[kC * PN];
-    __shared__ Sc sc;
+// Each chunk group's own contribution (groups > 1; launched before the forward):
+// sum_t exp(G_end - G_t) a_t [k_t | v_t]^T over the group's tokens, a plain weighted
+// sum, so every token's decay to the group end is one factor in [0, 1] folded into its
+// write row (no running rescale; G_end, the group's total log decay, is reduced
+// first).  64-token steps: every wave runs the step's clock and decay scans itself
+// (lane = token), builds 16 of the decayed write rows (taking its token's phase and
+// amplitude from the scanning lane), and after one barrier updates its state blocks
+// from the shared tiles.  The last group's contribution is never read, so its
+// workgroup copies rows 0 .. 63 of (K0, V0) for the forward's prologues instead and
+// forms only its total log decay.  Blocks (b h) G + g; 2 H extra blocks of the same
+// launch form the readout matrix, 32 rows each.
+constexpr int kCS = 64;                              // tokens per step
+__global__ __launch_bounds__(kNT, 3) void narrow_contrib_kernel(NarrowArgs a) {
+    constexpr int TK = kCS * PSB;                    // [64][128] tile
+    constexpr int TA = kCS * PNB;                    // [64][64] tile
+    __shared__ __attribute__((aligned(256))) char smem[2 * TK + TA];
     __shared__ double red[kNT / 64];
     const FwdParams &p = a.p;
     const int nseg = p.B * p.H * a.groups;
@@ -829,24 +855,48 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
         return;
     }
     const int bh = (int)blockIdx.x / a.groups, g = (int)blockIdx.x % a.groups, h = bh % p.H, b = bh / p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int sb = w & 1, ch = w >> 1;
     const int m = p.m;
     const int Tb = seq_tokens(p, b);
     const size_t row0 = seq_row0(p, b);
-    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
+    const int t_begin = min(g * a.cpg * kC, Tb), t_end = min((g + 1) * a.cpg * kC, Tb);
     const size_t tok0 = row0 * p.H + h;
     const size_t pi = (size_t)bh * a.groups + g;
+    const bool last = g == a.groups - 1;
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
+    // K, V pieces: rows tid/16 + 16 it, 16-byte column block tid%16; token `lane`'s scalars
+    uint4 rk[4], rv[4];
+    float dl, gg, be;
+    auto prefetch = [&](int t0) {
+        const int tq = opq(tid);
+        const int r = tq >> 4, c8 = (tq & 15) * 8;
+        const size_t base = ((row0 + t0) * p.H + h) * 128 + c8;
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int rr = r + 16 * it;
+            const bool in = t0 + rr < t_end;
+            rk[it] = in ? *reinterpret_cast<const uint4 *>(kin + base + (size_t)rr * rs) : make_uint4(0, 0, 0, 0);
+            rv[it] = in ? *reinterpret_cast<const uint4 *>(vin + base + (size_t)rr * rs) : make_uint4(0, 0, 0, 0);
+        }
+        const int t = t0 + lane;
+        const size_t si = (row0 + t) * p.H + h;
+        const bool tin = t < t_end;
+        dl = tin ? p.delta[si] : 0.f;
+        gg = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
+        be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+    };
+    // the first step's rows are in flight while the two sums below are formed
+    if (!last && t_begin < t_end) prefetch(t_begin);
     // clock entering the group: clock0 plus every increment before it (double)
-    double carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
-                                    block_token_sum(p.delta + tok0, p.H, 0, min(c_begin * kC, Tb), red, tid),
-                                (double)m, 1.0 / (double)m);
-    if (tid == 0) a.gclk[pi] = carry;
-    if (g == a.groups - 1) {
-        const double gs = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, min(c_begin * kC, Tb),
-                                                        min(c_end * kC, Tb), red, tid)
-                                      : 0.0;
-        if (tid == 0) a.Gg[pi] = (float)gs;
+    const double c_in = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
+                                         block_token_sum(p.delta + tok0, p.H, 0, t_begin, red, tid),
+                                     (double)m, 1.0 / (double)m);
+    if (tid == 0) a.gclk[pi] = c_in;
+    const double G_end = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, t_begin, t_end, red, tid) : 0.0;
+    if (tid == 0) a.Gg[pi] = (float)G_end;
+    if (last) {
         float *S0 = a.S0 + (size_t)bh * 2 * kStateN;
         const size_t sbase = (size_t)bh * kStoreRows * 128;
         for (int e = 4 * tid; e < kStateN; e += 4 * kNT) {
@@ -856,63 +906,92 @@ __global__ __launch_bounds__(kNT, 2) void narrow_contrib_kernel(NarrowArgs a) {
         }
         return;
     }
-    __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
-    const Sw z = make_sw(tid);
+    __bf16 *Kt = lds_at<__bf16>(smem, 0), *Vt = lds_at<__bf16>(smem, TK), *Adt = lds_at<__bf16>(smem, 2 * TK);
     const double dm = uniform_d((double)m), inv_m = uniform_d(1.0 / (double)m);
     const float amp0 = uniform(sqrtf(2.f / (float)m));
+    const int J = (m - 1) >> 1;
     f32x16 kacc[2], vacc[2];
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
         kacc[x] = zero_acc();
         vacc[x] = zero_acc();
     }
-    const size_t rs = (size_t)p.H * 128;
-    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
-    uint4 rk[2], rv[2];
-    Tok tk;
-    auto prefetch = [&](int c) {
-        const int t0 = c * kC, n = min(kC, Tb - t0);
-        const size_t base = ((row0 + t0) * p.H + h) * 128;
-        load_rows2(kin + base, rs, n, tid, rk);
-        load_rows2(vin + base, rs, n, tid, rv);
-        load_tok(p, row0, h, t0, Tb, tid, tk);
-    };
-    if (c_begin < c_end) prefetch(c_begin);
-    double gsum = 0.0;
-    float Ls = 0.f;
-    for (int c = c_begin; c < c_end; ++c) {
-        store_rows2(Kt, rk, z);
-        store_rows2(Vt, rv, z);
-        if (w == 0) chunk_scalars(sc, lane, dm, inv_m, amp0, tk, carry, Ls);
-        if (c + 1 < c_end) prefetch(c + 1);
-        lds_barrier();
-        build_A<false>(sc, nullptr, Asm, tid, m);
-        gsum += (double)sc.G[kC - 1];
+    double carry = c_in, gsum = 0.0;
+    for (int t0 = t_begin; t0 < t_end; t0 += kCS) {
+        const int tq = opq(tid);
+        const Sw z = make_sw(tq);
         {
-            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
-            if (f != 1.f) {
-                scale_acc(kacc, f);
-                scale_acc(vacc, f);
+            const int r = tq >> 4, c16 = (tq & 15) * 16;
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+                *reinterpret_cast<uint4 *>(cbyte(Kt) + (r + 16 * it) * PSB + c16) = rk[it];
+                *reinterpret_cast<uint4 *>(cbyte(Vt) + (r + 16 * it) * PSB + c16) = rv[it];
             }
         }
-        Ls = next_scale(sc, Ls);
+        // the step's scans on every wave (lane = token): clock (double, absolute from the
+        // group's entering clock) and the decay from the token to the group end
+        float u, amp;
+        {
+            const double lam = carry + wave_incl_scan((double)dl);
+            const float Gl = wave_incl_scan(gg);
+            const float rem = (float)(G_end - gsum);
+            const double q = lam * inv_m;
+            u = (float)(q - floor(q));
+            amp = be * amp0 * __expf(rem - Gl);
+            carry = reduce_clock(lane63(lam), dm, inv_m);
+            gsum += (double)lane63(Gl);
+        }
+        if (t0 + kCS < t_end) prefetch(t0 + kCS);
+        {
+            // decayed write rows: thread (row 16 w + lane / 4, quarter e = lane % 4) fills
+            // columns 16 e .. 16 e + 15 (pairs 8 e + 1 .. 8 e + 8; DC and padding at 62, 63)
+            const int lq = opq(lane);
+            const int r = 16 * w + (lq >> 2), e = lq & 3;
+            const float ur = __shfl(u, r), ar = __shfl(amp, r);
+            float s1, c1;
+            sincos_rev(ur, &s1, &c1);
+            bf16x8 d8[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                float sn, cs;
+                sincos_rev(__builtin_amdgcn_fractf((float)(8 * e + 4 * hh + 1) * ur), &sn, &cs);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int j = 8 * e + 4 * hh + 1 + jj;
+                    const bool live = j <= J;
+                    float a0 = live ? ar * cs : 0.f, a1 = live ? -ar * sn : 0.f;
+                    if (j == kR / 2) {                           // internal columns 62, 63
+                        a0 = ar * 0.70710678118654752f;
+                        a1 = 0.f;
+                    }
+                    d8[hh][2 * jj] = (__bf16)a0;
+                    d8[hh][2 * jj + 1] = (__bf16)a1;
+                    if (jj < 3) {
+                        const float nc = cs * c1 - sn * s1;
+                        const float ns = sn * c1 + cs * s1;
+                        cs = nc;
+                        sn = ns;
+                    }
+                }
+            }
+            *reinterpret_cast<bf16x8 *>(cbyte(Adt) + r * PNB + 32 * e) = d8[0];
+            *reinterpret_cast<bf16x8 *>(cbyte(Adt) + r * PNB + 32 * e + 16) = d8[1];
+        }
         lds_barrier();
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = stro_n(Asm, 16 * ks, 32 * sb, z);
+        for (int ks = 0; ks < kCS / 16; ++ks) {
+            const bf16x8 ad = stro_n(Adt, 16 * ks, 32 * sb, z);
 #pragma unroll
             for (int x = 0; x < 2; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 64 * ch + 32 * x, z), ad, kacc[x]);
             const bf16x8 vb = stro(Vt, 16 * ks, 32 * w, z);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) vacc[j] = mma(stro_n(Asm, 16 * ks, 32 * j, z), vb, vacc[j]);
+            for (int j = 0; j < 2; ++j) vacc[j] = mma(stro_n(Adt, 16 * ks, 32 * j, z), vb, vacc[j]);
         }
         lds_barrier();
     }
-    const float f = __expf(Ls);
-    float *E = a.Ef + pi * 2 * kStateN;
-    store_dump(E, kacc, f, w, lane);
-    store_dump(E + kStateN, vacc, f, w, lane);
-    if (tid == 0) a.Gg[pi] = (float)gsum;
+    __bf16 *E = a.Ef + pi * 2 * kStateN;
+    store_dump(E, kacc, w, lane);
+    store_dump(E + kStateN, vacc, w, lane);
 }
 
 }  // namespace
@@ -945,7 +1024,7 @@ NarrowWs narrow_ws(const FwdParams &p, int groups) {
     off += up((size_t)p.H * kR * kR * 2);
     if (groups > 1) {
         L.ef = off;
-        off += up(BH * G * 2 * kStateN * 4);
+        off += up(BH * G * 2 * kStateN * 2);
         L.gg = off;
         off += up(BH * G * 4);
         L.gclk = off;
@@ -973,7 +1052,7 @@ hipError_t launch_fwd_mfma_narrow(const FwdParams &p, int groups, void *ws, hipS
     a.groups = nc > 0 ? (nc + a.cpg - 1) / a.cpg : 1;      // no empty trailing group
     hipError_t e;
     if (a.groups > 1) {
-        a.Ef = reinterpret_cast<float *>(base + L.ef);
+        a.Ef = reinterpret_cast<__bf16 *>(base + L.ef);
         a.Gg = reinterpret_cast<float *>(base + L.gg);
         a.gclk = reinterpret_cast<double *>(base + L.gclk);
         a.S0 = reinterpret_cast<float *>(base + L.s0);

@@ -127,7 +127,7 @@ cyfa_status plan_forward(const cyfa_fwd_desc *d, FwdPlan *plan, bool layer = fal
         const int nchunks = (d->T + probe.chunk - 1) / probe.chunk;
         if (plan->segments > nchunks && nchunks > 0) plan->segments = nchunks;
         if (plan->segments < 1) plan->segments = 1;
-        ws += round_up(cyfa::mfma_wide_workspace_bytes(probe, plan->segments));
+        ws = round_up(cyfa::mfma_wide_workspace_bytes(probe, plan->segments));   // no fp32 readout matrix
     } else if (use_mfma) {
         probe.chunk = cyfa::mfma_default_chunk();    // a requested 64 runs as two 32-token chunks
         plan->chunk = probe.chunk;
@@ -336,11 +336,8 @@ cyfa_status forward_impl(const cyfa_fwd_desc *desc, const void *q, const void *k
         // forms its own 64 x 64 bf16 readout matrix
         e = cyfa::launch_fwd_mfma_narrow(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else if (plan.mfma && p.m > cyfa::kMaxActive) {
-        // fp32 readout matrix first, then its bf16 copies in the kernel's basis order
-        e = cyfa::launch_readout_prep_wide(p.H, p.m, R, M, s);
-        if (e != hipSuccess) return fail(CYFA_ERR_LAUNCH, "readout prep launch: %s", hipGetErrorString(e));
-        e = cyfa::launch_fwd_mfma_wide(p, plan.segments, M, ws + round_up(cyfa::readout_bytes(p.H, p.m)), s,
-                                       g_ev_start, g_ev_stop);
+        // forms its own bf16 readout matrix and its transpose
+        e = cyfa::launch_fwd_mfma_wide(p, plan.segments, ws, s, g_ev_start, g_ev_stop);
     } else if (plan.mfma) {
         // forms its own bf16 readout matrix
         e = cyfa::launch_fwd_mfma(p, plan.segments, ws, s, g_ev_start, g_ev_stop, mix);

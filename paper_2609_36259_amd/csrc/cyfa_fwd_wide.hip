@@ -403,35 +403,40 @@ __device__ __forceinline__ void store_value_state(float *S, const f32x16 (&acc)[
         }
 }
 
-// ---- chunk-group contributions (fp32, lane-major: wave w, accumulator x, lane, register)
-constexpr int kStateW = kR * 128;                   // floats of one 256 x 128 state
+// ---- chunk-group contributions (bf16, lane-major: wave w, accumulator x, lane, register;
+// the precision in which the chunk products consume the state)
+constexpr int kStateW = kR * 128;                   // elements of one 256 x 128 state
 __device__ __forceinline__ int dump_w(int w, int x, int lane) { return ((w * 4 + x) * 64 + lane) * 16; }
-__device__ __forceinline__ void store_dump(float *E, const f32x16 (&acc)[4], float f, int w, int lane) {
+__device__ __forceinline__ void store_dump(__bf16 *E, const f32x16 (&acc)[4], int w, int lane) {
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<float4 *>(E + dump_w(w, x, lane) + 4 * q) =
-                make_float4(f * acc[x][4 * q], f * acc[x][4 * q + 1], f * acc[x][4 * q + 2], f * acc[x][4 * q + 3]);
-}
-__device__ __forceinline__ void add_dump(f32x16 (&acc)[4], const float *E, float f, int w, int lane) {
+        for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 o;
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float4 e = *reinterpret_cast<const float4 *>(E + dump_w(w, x, lane) + 4 * q);
-            acc[x][4 * q] = fmaf(f, e.x, acc[x][4 * q]);
-            acc[x][4 * q + 1] = fmaf(f, e.y, acc[x][4 * q + 1]);
-            acc[x][4 * q + 2] = fmaf(f, e.z, acc[x][4 * q + 2]);
-            acc[x][4 * q + 3] = fmaf(f, e.w, acc[x][4 * q + 3]);
+            for (int v = 0; v < 8; ++v) o[v] = (__bf16)acc[x][8 * hf + v];
+            *reinterpret_cast<bf16x8 *>(E + dump_w(w, x, lane) + 8 * hf) = o;
         }
+}
+// a lane's part of one state of one contribution: [x][half] pieces of 8 registers
+__device__ __forceinline__ void load_dump(bf16x8 (&e)[8], const __bf16 *E, int w, int lane) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) e[2 * x + hf] = *reinterpret_cast<const bf16x8 *>(E + dump_w(w, x, lane) + 8 * hf);
+}
+__device__ __forceinline__ void add_dump(f32x16 (&acc)[4], const bf16x8 (&e)[8], float f) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[x][v] = fmaf(f, (float)e[2 * x + (v >> 3)][v & 7], acc[x][v]);
 }
 
 struct WideArgs {
     FwdParams p;
     const __bf16 *Mz, *MzT;  // [H][256][256] readout matrix times scale log2 e, and its transpose
     int groups, cpg;         // chunk groups per sequence, chunks per group
-    float *Ef;               // [BH][groups][2][kStateW] each group's own contribution (K, V)
+    __bf16 *Ef;              // [BH][groups][2][kStateW] each group's own contribution (K, V), bf16
     float *Gg;               // [BH][groups] total log decay of each group
     double *gclk;            // [BH][groups] clock entering each group (reduced mod m)
     float *S0;               // [BH][2][kStateW] copy of (K0, V0) (groups > 1: the states may be
@@ -524,15 +529,27 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(WideArgs a) {
     } else {
         // state entering the group: each earlier group's contribution decayed through
         // the groups after it, plus (K0, V0) decayed through all earlier groups
+        // (key states first, then value states, two contributions per memory round trip)
         const float *Gg = a.Gg + (size_t)bh * a.groups;
-        float tail = 0.f;                         // log decay of groups q+1 .. g-1
-        for (int q = g - 1; q >= 0; --q) {
-            const float f = __expf(tail);
-            const float *E = a.Ef + ((size_t)bh * a.groups + q) * 2 * kStateW;
-            add_dump(kacc, E, f, w, lane);
-            add_dump(vacc, E + kStateW, f, w, lane);
-            tail += Gg[q];
-        }
+        const __bf16 *Eb = a.Ef + (size_t)bh * a.groups * 2 * kStateW;
+        auto sum_groups = [&](f32x16 (&acc)[4], int sv) {
+            float tl = 0.f;                       // log decay of groups q+1 .. g-1
+            for (int q = g - 1; q >= 0; q -= 2) {
+                bf16x8 e0[8], e1[8];
+                load_dump(e0, Eb + ((size_t)q * 2 + sv) * kStateW, w, lane);
+                if (q >= 1) load_dump(e1, Eb + ((size_t)(q - 1) * 2 + sv) * kStateW, w, lane);
+                add_dump(acc, e0, __expf(tl));
+                tl += Gg[q];
+                if (q >= 1) {
+                    add_dump(acc, e1, __expf(tl));
+                    tl += Gg[q - 1];
+                }
+            }
+        };
+        sum_groups(kacc, 0);
+        sum_groups(vacc, 1);
+        float tail = 0.f;                         // log decay of groups 0 .. g-1
+        for (int q = 0; q < g; ++q) tail += Gg[q];
         const float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
         if (p.K0) add_key_state(kacc, S0, __expf(tail), w, lane, m);
         if (p.V0) add_value_state(vacc, S0 + kStateW, __expf(tail), hh, cb, lane, m);
@@ -705,35 +722,66 @@ __global__ __launch_bounds__(kNT, 1) void wide_forward_kernel(WideArgs a) {
     }
 }
 
-// Each chunk group's own contribution (groups > 1; launched before the forward).
-// The last group's contribution is never read, so its workgroup copies (K0, V0)
-// for the forward's prologues instead and forms only its total log decay.
+// Each chunk group's own contribution (groups > 1; launched before the forward):
+// sum_t exp(G_end - G_t) a_t [k_t | v_t]^T over the group's tokens, a plain weighted
+// sum, so every token's decay to the group end is one factor in [0, 1] folded into its
+// write row (no running rescale; G_end, the group's total log decay, is reduced
+// first).  64-token steps: every wave runs the step's clock and decay scans itself
+// (lane = token), builds 8 of the decayed write rows (taking its token's phase and
+// amplitude from the scanning lane), and after one barrier updates its state blocks
+// from the shared tiles.  The last group's contribution is never read, so its
+// workgroup copies (K0, V0) for the forward's prologues instead and forms only its
+// total log decay.
+constexpr int kCS = 64;                             // tokens per step
 __global__ __launch_bounds__(kNT, 1) void wide_contrib_kernel(WideArgs a) {
-    using L = Lay;
-    __shared__ __attribute__((aligned(256))) char smem[L::V + L::T1];   // K and V tiles
-    __shared__ __attribute__((aligned(256))) __bf16 Asm[kC * PW];
-    __shared__ Sc sc;
+    constexpr int TK = kCS * PSB;                   // [64][128] tile
+    constexpr int TA = kCS * PWB;                   // [64][256] tile
+    __shared__ __attribute__((aligned(256))) char smem[2 * TK + TA];
     __shared__ double red[kNT / 64];
     const FwdParams &p = a.p;
     const int bh = blockIdx.x, g = blockIdx.y, b = bh / p.H, h = bh % p.H;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hl = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int hh = w >> 2, cb = w & 3;
     const int m = p.m;
     const int Tb = seq_tokens(p, b);
     const size_t row0 = seq_row0(p, b);
-    const int c_begin = g * a.cpg, c_end = min(c_begin + a.cpg, (Tb + kC - 1) / kC);
+    const int t_begin = min(g * a.cpg * kC, Tb), t_end = min((g + 1) * a.cpg * kC, Tb);
     const size_t tok0 = row0 * p.H + h;
     const size_t pi = (size_t)bh * a.groups + g;
+    const bool last = g == a.groups - 1;
+    const size_t rs = (size_t)p.H * 128;
+    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
+    // K, V pieces: rows tid/16 + 32 it, 16-byte column block tid%16; token `lane`'s scalars
+    uint4 rk[2], rv[2];
+    float dl, gg, be;
+    auto prefetch = [&](int t0) {
+        const int tq = opq(tid);
+        const int r = tq >> 4, c8 = (tq & 15) * 8;
+        const size_t base = ((row0 + t0) * p.H + h) * 128 + c8;
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int rr = r + 32 * it;
+            const bool in = t0 + rr < t_end;
+            rk[it] = in ? *reinterpret_cast<const uint4 *>(kin + base + (size_t)rr * rs) : make_uint4(0, 0, 0, 0);
+            rv[it] = in ? *reinterpret_cast<const uint4 *>(vin + base + (size_t)rr * rs) : make_uint4(0, 0, 0, 0);
+        }
+        const int t = t0 + lane;
+        const size_t si = (row0 + t) * p.H + h;
+        const bool tin = t < t_end;
+        dl = tin ? p.delta[si] : 0.f;
+        gg = (tin && p.log_alpha) ? p.log_alpha[si] : 0.f;
+        be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
+    };
+    // the first step's rows are in flight while the two sums below are formed
+    if (!last && t_begin < t_end) prefetch(t_begin);
     // clock entering the group: clock0 plus every increment before it (double)
-    double carry = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
-                                    block_token_sum(p.delta + tok0, p.H, 0, min(c_begin * kC, Tb), red, tid),
-                                (double)m, 1.0 / (double)m);
-    if (tid == 0) a.gclk[pi] = carry;
-    if (g == a.groups - 1) {
-        const double gs = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, min(c_begin * kC, Tb),
-                                                        min(c_end * kC, Tb), red, tid)
-                                      : 0.0;
-        if (tid == 0) a.Gg[pi] = (float)gs;
+    const double c_in = reduce_clock((p.clock0 ? p.clock0[bh] : 0.0) +
+                                         block_token_sum(p.delta + tok0, p.H, 0, t_begin, red, tid),
+                                     (double)m, 1.0 / (double)m);
+    if (tid == 0) a.gclk[pi] = c_in;
+    const double G_end = p.log_alpha ? block_token_sum(p.log_alpha + tok0, p.H, t_begin, t_end, red, tid) : 0.0;
+    if (tid == 0) a.Gg[pi] = (float)G_end;
+    if (last) {
         float *S0 = a.S0 + (size_t)bh * 2 * kStateW;
         const size_t sb = (size_t)bh * kStateW;
         for (int e = 4 * tid; e < kStateW; e += 4 * kNT) {
@@ -742,77 +790,92 @@ __global__ __launch_bounds__(kNT, 1) void wide_contrib_kernel(WideArgs a) {
         }
         return;
     }
-    __bf16 *Kt = lds_at<__bf16>(smem, L::K), *Vt = lds_at<__bf16>(smem, L::V);
-    const Sw z = make_sw(tid);
+    __bf16 *Kt = lds_at<__bf16>(smem, 0), *Vt = lds_at<__bf16>(smem, TK), *Adt = lds_at<__bf16>(smem, 2 * TK);
+    const double dm = (double)m, inv_m = 1.0 / (double)m;
+    const float amp0 = sqrtf(2.f / (float)m);
+    const int J = (m - 1) >> 1;
     f32x16 kacc[4], vacc[4];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
         kacc[x] = zero_acc();
         vacc[x] = zero_acc();
     }
-    const size_t rs = (size_t)p.H * 128;
-    const __bf16 *kin = static_cast<const __bf16 *>(p.k), *vin = static_cast<const __bf16 *>(p.v);
-    uint4 rk, rv;
-    Tok tk;
-    auto prefetch = [&](int c) {
-        const int t0 = c * kC, n = min(kC, Tb - t0);
-        const size_t base = ((row0 + t0) * p.H + h) * 128;
-        load_row1(kin + base, rs, n, tid, rk);
-        load_row1(vin + base, rs, n, tid, rv);
-        load_tok(p, row0, h, t0, Tb, tid, tk);
-    };
-    if (c_begin < c_end) prefetch(c_begin);
-    double gsum = 0.0;
-    float Ls = 0.f;
-    for (int c = c_begin; c < c_end; ++c) {
-        store_row1(Kt, rk, z);
-        store_row1(Vt, rv, z);
-        if (w == 0) chunk_scalars(sc, lane, m, tk, carry, Ls);
-        if (c + 1 < c_end) prefetch(c + 1);
-        lds_barrier();
-        build_A(sc, Asm, tid, m);
-        gsum += (double)sc.G[kC - 1];
+    double carry = c_in, gsum = 0.0;
+    for (int t0 = t_begin; t0 < t_end; t0 += kCS) {
+        const int tq = opq(tid);
+        const Sw z = make_sw(tq);
         {
-            const float f = uniform(sc.ctl[0]) * uniform(sc.ctl[1]);
-            if (f != 1.f) {
-                scale_acc(kacc, f);
-                scale_acc(vacc, f);
+            const int r = tq >> 4, c16 = (tq & 15) * 16;
+#pragma unroll
+            for (int it = 0; it < 2; ++it) {
+                *reinterpret_cast<uint4 *>(cbyte(Kt) + (r + 32 * it) * PSB + c16) = rk[it];
+                *reinterpret_cast<uint4 *>(cbyte(Vt) + (r + 32 * it) * PSB + c16) = rv[it];
             }
         }
-        Ls = next_scale(sc, Ls);
+        // the step's scans on every wave (lane = token): clock (double, absolute from the
+        // group's entering clock) and the decay from the token to the group end
+        float u, amp;
+        {
+            const double lam = carry + wave_incl_scan((double)dl);
+            const float Gl = wave_incl_scan(gg);
+            const float rem = (float)(G_end - gsum);
+            const double q = lam * inv_m;
+            u = (float)(q - floor(q));
+            amp = be * amp0 * __expf(rem - Gl);
+            carry = reduce_clock(lane63(lam), dm, inv_m);
+            gsum += (double)lane63(Gl);
+        }
+        if (t0 + kCS < t_end) prefetch(t0 + kCS);
+        {
+            // decayed write rows: thread (row 8 w + lane / 8, eighth e = lane % 8) fills
+            // columns 32 e .. 32 e + 31 (pairs 16 e + 1 .. 16 e + 16; DC and padding at
+            // 254, 255), from four starts advanced by angle addition
+            const int lq = opq(lane);
+            const int r = 8 * w + (lq >> 3), e = lq & 7;
+            const float ur = __shfl(u, r), ar = __shfl(amp, r);
+            float s1, c1;
+            sincos_rev(ur, &s1, &c1);
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                float sn, cs;
+                sincos_rev(__builtin_amdgcn_fractf((float)(16 * e + 4 * qq + 1) * ur), &sn, &cs);
+                bf16x8 d8;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int j = 16 * e + 4 * qq + 1 + jj;
+                    const bool live = j <= J;
+                    float a0 = live ? ar * cs : 0.f, a1 = live ? -ar * sn : 0.f;
+                    if (j == kR / 2) {                          // internal columns 254, 255
+                        a0 = ar * 0.70710678118654752f;
+                        a1 = 0.f;
+                    }
+                    d8[2 * jj] = (__bf16)a0;
+                    d8[2 * jj + 1] = (__bf16)a1;
+                    if (jj < 3) {
+                        const float nc = cs * c1 - sn * s1;
+                        const float ns = sn * c1 + cs * s1;
+                        cs = nc;
+                        sn = ns;
+                    }
+                }
+                *reinterpret_cast<bf16x8 *>(cbyte(Adt) + r * PWB + 64 * e + 16 * qq) = d8;
+            }
+        }
         lds_barrier();
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 ad = scale_k(stro_w(Asm, 16 * ks, 32 * w, z), sc.rho + 16 * ks + 8 * hl);
+        for (int ks = 0; ks < kCS / 16; ++ks) {
+            const bf16x8 ad = stro_w(Adt, 16 * ks, 32 * w, z);
 #pragma unroll
             for (int x = 0; x < 4; ++x) kacc[x] = mma(stro(Kt, 16 * ks, 32 * x, z), ad, kacc[x]);
             const bf16x8 vb = stro(Vt, 16 * ks, 32 * cb, z);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                vacc[j] = mma(scale_k(stro_w(Asm, 16 * ks, 128 * hh + 32 * j, z), sc.rho + 16 * ks + 8 * hl), vb,
-                              vacc[j]);
+            for (int j = 0; j < 4; ++j) vacc[j] = mma(stro_w(Adt, 16 * ks, 128 * hh + 32 * j, z), vb, vacc[j]);
         }
         lds_barrier();
     }
-    const float f = __expf(Ls);
-    float *E = a.Ef + pi * 2 * kStateW;
-    store_dump(E, kacc, f, w, lane);
-    store_dump(E + kStateW, vacc, f, w, lane);
-    if (tid == 0) a.Gg[pi] = (float)gsum;
-}
-
-// bf16 readout matrix for the kernel above from the fp32 one (paper basis order,
-// [H][256][256]): Mz[i][j_int] = zs M[i][paper(j_int)], with kMaskLogit in the padding
-// column of inactive slots (i >= m), and its transpose MzT[j_int][i].
-__global__ __launch_bounds__(256) void wide_mz_kernel(int m, const float *__restrict__ M, __bf16 *__restrict__ Mz,
-                                                      __bf16 *__restrict__ MzT, float zs) {
-    const int h = blockIdx.x, i = blockIdx.y, jint = threadIdx.x;
-    const int jp = jint < kDCw ? jint + 1 : (jint == kDCw ? 0 : -1);
-    float val = jp >= 0 ? zs * M[((size_t)h * kR + i) * kR + jp] : 0.f;
-    if (jint == kR - 1 && i >= m) val = kMaskLogit;
-    const __bf16 b = (__bf16)val;
-    Mz[((size_t)h * kR + i) * kR + jint] = b;
-    MzT[((size_t)h * kR + jint) * kR + i] = b;
+    __bf16 *E = a.Ef + pi * 2 * kStateW;
+    store_dump(E, kacc, w, lane);
+    store_dump(E + kStateW, vacc, w, lane);
 }
 
 }  // namespace
@@ -847,7 +910,7 @@ WideWs wide_ws(const FwdParams &p, int groups) {
     off += up((size_t)p.H * kR * kR * 2);
     if (groups > 1) {
         L.ef = off;
-        off += up(BH * G * 2 * kStateW * 4);
+        off += up(BH * G * 2 * kStateW * 2);
         L.gg = off;
         off += up(BH * G * 4);
         L.gclk = off;
@@ -862,8 +925,8 @@ WideWs wide_ws(const FwdParams &p, int groups) {
 
 size_t mfma_wide_workspace_bytes(const FwdParams &p, int groups) { return wide_ws(p, groups).total; }
 
-hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
-                                hipEvent_t ev_start, hipEvent_t ev_stop) {
+hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, void *ws, hipStream_t st, hipEvent_t ev_start,
+                                hipEvent_t ev_stop) {
     char *base = static_cast<char *>(ws);
     const WideWs L = wide_ws(p, groups);
     WideArgs a{};
@@ -874,14 +937,13 @@ hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, 
     a.cpg = nc > 0 ? (nc + groups - 1) / groups : 1;
     a.groups = nc > 0 ? (nc + a.cpg - 1) / a.cpg : 1;      // no empty trailing group
     if (a.groups > 1) {
-        a.Ef = reinterpret_cast<float *>(base + L.ef);
+        a.Ef = reinterpret_cast<__bf16 *>(base + L.ef);
         a.Gg = reinterpret_cast<float *>(base + L.gg);
         a.gclk = reinterpret_cast<double *>(base + L.gclk);
         a.S0 = reinterpret_cast<float *>(base + L.s0);
     }
-    hipLaunchKernelGGL(wide_mz_kernel, dim3(p.H, kR), dim3(kR), 0, st, p.m, M, const_cast<__bf16 *>(a.Mz),
-                       const_cast<__bf16 *>(a.MzT), p.scale * 1.4426950408889634f);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_readout_prep_wide_bf16(p.H, p.m, p.R, const_cast<__bf16 *>(a.Mz),
+                                                 const_cast<__bf16 *>(a.MzT), p.scale * 1.4426950408889634f, st);
     if (e != hipSuccess) return e;
     const dim3 grid(p.B * p.H, a.groups);
     if (a.groups > 1) {

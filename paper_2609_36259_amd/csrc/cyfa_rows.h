@@ -23,17 +23,22 @@ inline size_t readout_bytes(int H, int m) {
 // M_h = R_h Phi as float [H][256][256] for 127 < m <= 255 (slot row, basis
 // column in the order of App. A.1, zero outside the active m x m block).
 hipError_t launch_readout_prep_wide(int H, int m, const float *R, float *M, hipStream_t s);
+// The same matrix for the matrix-core kernel: bf16 Mz = zs M in its internal basis
+// order (DC at 254, padding 255, kMaskLogit in the padding column of inactive slots)
+// and its transpose MzT, [H][256][256] each.
+hipError_t launch_readout_prep_wide_bf16(int H, int m, const float *R, __bf16 *Mz, __bf16 *MzT, float zs,
+                                         hipStream_t s);
 
 // Matrix-core forward for 127 < m <= 255 (bf16, d_k = d_v = 128, chunk 32 or 64 run
 // as 32-token chunks, one workgroup per chunk group of a sequence).  ws
 // (mfma_wide_workspace_bytes) receives the bf16 readout matrix and its transpose,
-// formed from the fp32 M of launch_readout_prep_wide, and with groups > 1 the groups'
-// contributions; the events, when given, bracket the fused kernel.
+// formed from p.R, and with groups > 1 the groups' contributions; the events, when
+// given, bracket the fused kernel.
 bool mfma_wide_supported(const FwdParams &p);
 int mfma_wide_auto_groups(const FwdParams &p);
 size_t mfma_wide_workspace_bytes(const FwdParams &p, int groups);
-hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, const float *M, void *ws, hipStream_t st,
-                                hipEvent_t ev_start, hipEvent_t ev_stop);
+hipError_t launch_fwd_mfma_wide(const FwdParams &p, int groups, void *ws, hipStream_t st, hipEvent_t ev_start,
+                                hipEvent_t ev_stop);
 
 // Matrix-core forward for m <= 63 on m* = 64 storage rows (bf16, d_k = d_v = 128, chunk
 // 32 or 64 run as 32-token chunks, one workgroup per chunk group of a sequence, two per

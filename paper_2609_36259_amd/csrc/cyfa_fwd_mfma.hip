@@ -434,20 +434,6 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
     const float mult = cidx < 2 * J ? 1.f : (cidx == kDC ? 0.70710678118654752f : 0.f);
     const float amp0 = sqrtf(2.f / (float)m);
 
-    // segment total of log alpha (the decay reference G_end)
-    double gpart = 0.0;
-    if constexpr (kMix) {
-        const MixIn &mx = a.mix;
-        if (mx.z_alpha)
-            for (int t = t_begin + tid; t < t_end; t += NT)
-                gpart += (double)(-mx.A[h] * mix_softplus(mx.z_alpha[(seq_row0(p, b) + t) * p.H + h] +
-                                                          (mx.b_alpha ? mx.b_alpha[h] : 0.f)));
-    } else if (p.log_alpha) {
-        for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[(seq_row0(p, b) + t) * p.H + h];
-    }
-    gpart = lane63(wave_incl_scan(gpart));
-    if (lane == 0) red[w] = gpart;
-
     // K, V pieces: rows tid/16 + RPP it, 16-byte column block tid%16; scalars of
     // token `lane` of the chunk on every wave
     const size_t row_el = (size_t)Hv * D;
@@ -482,8 +468,23 @@ __global__ __launch_bounds__(NT, 2) void segment_state_kernel(MfmaArgs a, float 
             be = tin ? (p.beta ? p.beta[si] : 1.f) : 0.f;
         }
     };
+    // the first chunk's rows are in flight while the segment total below is formed
     if (c_begin < c_end) load(c_begin);
-    __syncthreads();
+    // segment total of log alpha (the decay reference G_end)
+    double gpart = 0.0;
+    if constexpr (kMix) {
+        const MixIn &mx = a.mix;
+        if (mx.z_alpha)
+            for (int t = t_begin + tid; t < t_end; t += NT)
+                gpart += (double)(-mx.A[h] * mix_softplus(mx.z_alpha[(seq_row0(p, b) + t) * p.H + h] +
+                                                          (mx.b_alpha ? mx.b_alpha[h] : 0.f)));
+    } else if (p.log_alpha) {
+        for (int t = t_begin + tid; t < t_end; t += NT) gpart += (double)p.log_alpha[(seq_row0(p, b) + t) * p.H + h];
+    }
+    gpart = lane63(wave_incl_scan(gpart));
+    if (lane == 0) red[w] = gpart;
+
+    lds_barrier();                                     // (the chunk's loads stay in flight)
     const double G_end = (red[0] + red[1]) + (red[2] + red[3]);
 
     f32x16 kacc[4], vacc[4];

@@ -73,20 +73,33 @@ def test_status_codes():
     assert n.value == 256 * 256 * 4
     d = cyfa.forward_desc(1, 16, 1, 256, 64, m=255)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
-    # bf16 with d = 128: the matrix-core kernel (fp32 M, then its bf16 copy and transpose)
+    # bf16 with d = 128: the matrix-core kernel (the bf16 readout matrix and its
+    # transpose, formed from R directly)
     d = cyfa.forward_desc(1, 16, 3, 128, 128, m=255, dtype=cyfa.BF16)
     assert cyfa.selected_kernel(d) == "mfma"
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
-    assert n.value == 3 * 256 * 256 * 4 + 2 * 3 * 256 * 256 * 2
+    assert n.value == 2 * 3 * 256 * 256 * 2
     d = cyfa.forward_desc(1, 16, 1, 128, 128, m=129, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
-    # chunk groups (one workgroup each): their contributions, decays, clocks and a copy
-    # of the initial states join the workspace
+    # chunk groups (one workgroup each): their bf16 contributions, decays, clocks and a
+    # copy of the initial states join the workspace
     d = cyfa.forward_desc(2, 4096, 4, 128, 128, m=255, dtype=cyfa.BF16)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
     G, BH = 32, 8
-    assert n.value == (4 * 256 * 256 * 4 + 2 * 4 * 256 * 256 * 2 + BH * G * 2 * 256 * 128 * 4 + BH * G * 4
+    assert n.value == (2 * 4 * 256 * 256 * 2 + BH * G * 2 * 256 * 128 * 2 + BH * G * 4
                        + BH * G * 8 + BH * 2 * 256 * 128 * 4)
+    # m <= 63, bf16 with d = 128: the 64-row matrix-core kernel (its 64 x 64 bf16 readout
+    # matrix; with chunk groups their bf16 contributions, decays, clocks and rows 0 .. 63
+    # of the initial states)
+    d = cyfa.forward_desc(1, 16, 3, 128, 128, m=63, dtype=cyfa.BF16)
+    assert cyfa.selected_kernel(d) == "mfma"
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert n.value == 3 * 64 * 64 * 2
+    d = cyfa.forward_desc(2, 4096, 4, 128, 128, m=63, dtype=cyfa.BF16)
+    assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    G, BH = 96, 8                                 # ceil(768 / 8) groups of 32-token chunks
+    assert n.value == (4 * 64 * 64 * 2 + BH * G * 2 * 64 * 128 * 2 + BH * G * 4 + BH * G * 8
+                       + BH * 2 * 64 * 128 * 4)
     d = cyfa.forward_desc(1, 16, 1, 128, 128, m=255, dtype=cyfa.BF16, kernel=cyfa.KERNEL_MFMA, chunk=16)
     assert lib.cyfa_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 2
     d = cyfa.forward_desc(1, 16, 1, 96, 64)

@@ -282,3 +282,19 @@ def test_full_size_every_sequence():
     print("errors", {k: f"{v:.2e}" for k, v in err.items()}, flush=True)
     for k, v in err.items():
         assert v <= (1e-9 if k == "clock" else TOL_BF16), (k, v)
+
+
+@pytest.mark.parametrize("segments", [1, 3])
+def test_extreme_and_mixed_gates(segments):
+    """Stretches of heavy forgetting (the carried states' eager rescaling, and group
+    contributions whose early tokens decay to nothing), of no forgetting and of
+    ordinary gates, with one chunk group and with three."""
+    x = make_forward_inputs(1, 517, 2, 128, 128, seed=185, dtype="bf16", m=63)
+    g = x["log_alpha"]
+    g[:, 40:140] = -6.0          # exp(-6 * 32) per chunk: forces the rescaling branch
+    g[:, 200:330] = 0.0          # alpha = 1
+    g[:, 400:410] = -40.0        # near-total erasure
+    t = upload(x)
+    res = _fwd(x, t, segments=segments, return_state=True, return_logits=True)
+    torch.cuda.synchronize()
+    _check(x, res)

@@ -127,7 +127,11 @@ cyfa_status cyfa_forward_workspace_size(const cyfa_fwd_desc *desc, size_t *bytes
  *               clock); any finite value is accepted (the paper draws them from
  *               (0, 1); negative values run the clock backwards)
  *   log_alpha   [B, T, H] float g_t = log alpha_t (forget gate, normally <= 0);
- *               NULL means alpha = 1
+ *               NULL means alpha = 1.  The matrix-core kernels' segment and
+ *               group contributions fold each token's decay to the end of its
+ *               segment or group into one fp32 factor exp(sum of the later g),
+ *               which overflows if positive g sum beyond about 88 there; the
+ *               carried states themselves are rescaled and take any sign.
  *   beta        [B, T, H] float write strength beta_t; NULL means beta = 1
  *   R           [H, m, m] float readout matrices R_h (Sec. 3.1); NULL = identity
  *   K0, V0      [B, H, 128, d_k] / [B, H, 128, d_v] float initial absolute-clock

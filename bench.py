@@ -50,9 +50,9 @@ M_ACTIVE = 127
 # factors come from the same counters on a 1 GiB device copy), taken on the kernel
 # sources whose digest is recorded here.  Reported only while those sources are
 # unchanged (profiles/cyfa_fused_mfma32_1p4b_hbm_traffic.md).
-TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 116364 * 2 * 1024 + 65536 * 1024,
-           "fetch_kib": 116364, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
-           "sources_sha256": "b8bb06f03e4326011af8ff2c107c6bd283c701fced3fd10ed5004a21852e0e45"}
+TRAFFIC = {"chunk": 32, "workload": "1.4B", "bytes": 116363 * 2 * 1024 + 65536 * 1024,
+           "fetch_kib": 116363, "write_kib": 65536, "fetch_factor": 2.0, "write_factor": 1.0,
+           "sources_sha256": "1d4c4e945befd5aafce5aeb48a76093b239c85133b298281ae5fca6e3ee57532"}
 TRAFFIC_SOURCES = ("cyfa_fwd_mfma.hip", "cyfa_mfma_chunk.h", "cyfa_mfma_common.h", "cyfa_internal.h",
                    "cyfa_prep.h")
 

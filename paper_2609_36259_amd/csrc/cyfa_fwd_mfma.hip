@@ -698,22 +698,30 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
     }
     const double inv_m = 1.0 / (double)m;
     double origin = reduce_clock(c0, (double)m, inv_m);
-    // Segment contributions are fetched kBatch segments at a time, ahead of the
-    // dependent chain through them.  Every thread owns the same offsets in every
+    // Segment contributions, log-alpha sums and clock spans are fetched kBatch
+    // segments at a time, ahead of the dependent chain through them (loaded inside
+    // the chain, each segment's scalars would wait for a memory round trip behind
+    // the previous segment's stores).  Every thread owns the same offsets in every
     // segment, so the loads of a batch never see this batch's stores.  The chain
     // itself runs in fp32; contributions and entering states are stored as bf16.
     constexpr int kBatch = 8;
     for (int q0 = 0; q0 < a.P; q0 += kBatch) {
         bf16x4 da[kBatch], db[kBatch];
+        double gs[kBatch], sp[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int q = q0 + u;
             da[u] = bf16x4{};
             db[u] = da[u];
+            gs[u] = 0.0;
+            sp[u] = 0.0;
             if (q < a.P - 1) {
-                const __bf16 *st = a.seg_state + ((size_t)bh * a.P + q) * kStateFloats;
+                const size_t slot = (size_t)bh * a.P + q;
+                const __bf16 *st = a.seg_state + slot * kStateFloats;
                 da[u] = *reinterpret_cast<const bf16x4 *>(st + off0);
                 db[u] = *reinterpret_cast<const bf16x4 *>(st + off1);
+                gs[u] = a.seg_gsum[slot];
+                sp[u] = a.seg_span[slot];
             }
         }
 #pragma unroll
@@ -744,8 +752,8 @@ __device__ __forceinline__ void segment_scan(const MfmaArgs &a, int bh, int y, i
                 *reinterpret_cast<bf16x4 *>(st + off1) = s1;
             }
             if (q < a.P - 1) {
-                const float gdec = __expf((float)a.seg_gsum[slot]);
-                const double span = a.seg_span[slot];    // already reduced to [0, m)
+                const float gdec = __expf((float)gs[u]);
+                const double span = sp[u];               // already reduced to [0, m)
                 const double u1 = span * inv_m;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
